@@ -1,0 +1,281 @@
+#!/usr/bin/env python3
+"""Owner-local Muon step on one MI355X: latency, NS TFLOP/s and roofline fractions.
+
+One "step" is the whole owner update for one synthetic owner share: mfsdp_muon_step over every
+owned matrix (momentum + Nesterov, Frobenius normalisation, K quintic Newton-Schulz steps on bf16
+MFMA, shape-scaled lr with decoupled weight decay) followed by mfsdp_adamw_step over the tail
+tensors. Inputs are resident in HBM before the timed region starts.
+
+Default workload: 4 of 32 Llama-3-8B layers (28 matrices: Wq, Wo 4096x4096; Wk, Wv 1024x4096;
+gate, up 14336x4096; down 4096x14336 per layer) plus 8 RMSNorm vectors of 4096 on AdamW.
+
+Prints ONE JSON line. `value` is nominal NS TFLOP/s over the whole step (NS flops / step time);
+`roofline` describes the NS GEMM kernel; `cpu_baseline` is the fp64 oracle timed on a bounded
+sample of the same share on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
+PEAK_HBM_GBS = 8000.0       # HBM3E
+METRIC = "owner Muon-step latency (ms) and NS TFLOP/s (% MFMA bf16 peak) at 1 MI355X"
+GEMM_KERNEL = "gemm_bf16_kernel"
+GEMM_SOURCE = os.path.join(ROOT, "paper_2607_05895_amd", "csrc", "kernels_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_bf16_traffic_llama3_8b_share.json")
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t helpers from the HIP runtime torch already loaded (same runtime instance)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self) -> int:
+        ev = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(ev))
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreate failed: {rc}")
+        return ev.value
+
+    def record(self, ev: int, stream: int) -> None:
+        rc = self.hip.hipEventRecord(ev, stream)
+        if rc != 0:
+            raise RuntimeError(f"hipEventRecord failed: {rc}")
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        out = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed: {rc}")
+        return float(out.value)
+
+
+def _to_dev(arr, dtype, torch, dev):
+    import numpy as np
+    import synth
+    if dtype == synth.BF16:
+        return torch.from_numpy(arr.view(np.int16)).view(torch.bfloat16).to(dev)
+    return torch.from_numpy(arr).to(dev)
+
+
+def cpu_baseline(wl, sample_idx, pool) -> dict:
+    """Time the fp64 oracle on a bounded sample of the share (host cores)."""
+    import numpy as np
+    import oracle
+    import synth
+    try:
+        import threadpoolctl
+        threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    hp = wl.hp
+    flops = 0.0
+    elapsed = 0.0
+    for i in sample_idx:
+        t = synth.muon_entry(wl, i, pool)
+        e = wl.muon[i]
+        r, s = min(e.m, e.n), max(e.m, e.n)
+        flops += hp.ns_steps * (4.0 * r * r * s + 2.0 * r ** 3)
+        t0 = time.perf_counter()
+        oracle.muon_step(t.param, t.grad, t.momentum, lr=hp.lr, weight_decay=hp.weight_decay,
+                         momentum=hp.momentum, nesterov=hp.nesterov, a=hp.a, b=hp.b, c=hp.c,
+                         ns_steps=hp.ns_steps, eps=hp.eps, lr_adjust=hp.lr_adjust)
+        elapsed += time.perf_counter() - t0
+    names = [wl.muon[i].name + f" {wl.muon[i].m}x{wl.muon[i].n}" for i in sample_idx]
+    return {"value": flops / elapsed / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"full fp64 oracle Muon step of {len(sample_idx)} of the share's "
+                      f"{len(wl.muon)} matrices ({', '.join(names)}): {elapsed:.1f} s for "
+                      f"{flops:.3e} nominal NS flop; estimated whole-share step "
+                      f"{elapsed * wl.ns_flops_nominal() / flops:.0f} s"}
+
+
+def traffic_entry(launches: int):
+    """HBM traffic of the NS GEMM kernel from committed rocprofv3 counter runs, if they were taken
+    on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+        sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+        if rec.get("kernel_source_sha256") != sha:
+            return None
+        return rec.get("bytes_per_launch")
+    except Exception:
+        return None
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, help="owner share 1..5 (default 3: Llama-3-8B)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the owner-local Muon "
+                                   "step has no cross-GPU work; run with --gpus 1"}), flush=True)
+        return 2
+    if int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print(json.dumps({"error": "launched with WORLD_SIZE > 1; this benchmark is single-GPU"}))
+        return 2
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_05895_amd import native
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.workload(args.workload)
+    hp = wl.hp
+    pool = synth.thread_pool()
+    log(f"workload {wl.name}: {len(wl.muon)} matrices, {wl.muon_elements() / 1e6:.1f} M Muon "
+        f"elements, {wl.adamw_elements() / 1e6:.2f} M AdamW elements; generating inputs")
+    t0 = time.time()
+    keep, ents = [], []
+    for i, e in enumerate(wl.muon):
+        t = synth.muon_entry(wl, i, pool)
+        p = _to_dev(t.param, e.param_dtype, torch, dev)
+        g = _to_dev(t.grad, e.grad_dtype, torch, dev)
+        mo = _to_dev(t.momentum, synth.F32, torch, dev)
+        keep.append((p, g, mo))
+        ents.append(native.muon_entry_t(p, g, mo))
+    aents = []
+    for j, e in enumerate(wl.adamw):
+        t = synth.adamw_entry(wl, j, pool)
+        tens = (_to_dev(t.param, e.param_dtype, torch, dev), _to_dev(t.grad, e.grad_dtype, torch, dev),
+                _to_dev(t.exp_avg, synth.F32, torch, dev), _to_dev(t.exp_avg_sq, synth.F32, torch, dev))
+        keep.append(tens)
+        aents.append(native.adamw_entry_t(*tens))
+    h = native.muon_hparams(lr=hp.lr, weight_decay=hp.weight_decay, momentum=hp.momentum,
+                            nesterov=hp.nesterov, a=hp.a, b=hp.b, c=hp.c, ns_steps=hp.ns_steps,
+                            eps=hp.eps, lr_adjust=hp.lr_adjust, ns_dtype=hp.ns_dtype)
+    ws = native.muon_workspace_t(ents, h, device=dev)
+    torch.cuda.synchronize()
+    log(f"inputs resident ({time.time() - t0:.1f} s); workspace {ws.numel() / 2**30:.2f} GiB")
+
+    ah = wl.adamw_hp
+    stream = torch.cuda.current_stream().cuda_stream
+    hev = HipEvents()
+    n_ev = args.steps
+    ev = [[hev.create() for _ in range(6)] for _ in range(n_ev)]
+    ev_start, ev_stop = hev.create(), hev.create()
+
+    def step(events=None, aev=None):
+        native.mfsdp_muon_step_timed(ents, h, ws.data_ptr(), ws.numel(), stream,
+                                     events if events else [None] * 4)
+        if aents:
+            if aev:
+                hev.record(aev[0], stream)
+            native.mfsdp_adamw_step(aents, ah.lr, ah.beta1, ah.beta2, ah.eps, ah.weight_decay,
+                                    ah.step, stream)
+            if aev:
+                hev.record(aev[1], stream)
+
+    for w in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
+    hev.record(ev_start, stream)
+    for k in range(args.steps):
+        step(ev[k][:4], ev[k][4:6])
+    hev.record(ev_stop, stream)
+    torch.cuda.synchronize()
+    total_ms = hev.elapsed_ms(ev_start, ev_stop)
+    ms_per_step = total_ms / args.steps
+    prep_ms = sum(hev.elapsed_ms(e[0], e[1]) for e in ev) / n_ev
+    ns_ms = sum(hev.elapsed_ms(e[1], e[2]) for e in ev) / n_ev
+    apply_ms = sum(hev.elapsed_ms(e[2], e[3]) for e in ev) / n_ev
+    adamw_ms = (sum(hev.elapsed_ms(e[4], e[5]) for e in ev) / n_ev) if aents else 0.0
+    log(f"step {ms_per_step:.3f} ms: prep+norm {prep_ms:.3f}, NS {ns_ms:.3f}, apply {apply_ms:.3f}, "
+        f"AdamW {adamw_ms:.3f}")
+
+    flops = wl.ns_flops_nominal()
+    launches = 3 * hp.ns_steps
+    ns_tflops = flops / (ns_ms * 1e-3) / 1e12 if ns_ms > 0 else 0.0
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    elts = wl.muon_elements()
+    es_g = 2 if all(e.grad_dtype == synth.BF16 for e in wl.muon) else 4
+    es_p = 2 if all(e.param_dtype == synth.BF16 for e in wl.muon) else 4
+    es_ns = 2 if hp.ns_dtype == synth.BF16 else 4
+    prep_bytes = elts * (es_g + 4 + 4 + 2 * es_ns)       # g, m in/out, u and u^T
+    apply_bytes = elts * (es_ns + 2 * es_p)               # O, p in/out
+    alg_bytes = elts * (es_g + 8 + 2 * es_p)              # g, m in/out, p in/out
+    adamw_bytes = sum(e.numel * ({"bf16": 2, "f32": 4}[e.param_dtype] * 2 +
+                                 {"bf16": 2, "f32": 4}[e.grad_dtype] + 16) for e in wl.adamw)
+    traffic = traffic_entry(launches)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if hp.ns_dtype == synth.BF16 else "f32",
+        "data": "synthetic (seeded Gaussian gradients/params/momentum of the share's shapes)",
+        "config": {"workload": wl.name, "description": wl.description,
+                   "muon_matrices": len(wl.muon), "muon_elements": elts,
+                   "adamw_tensors": len(wl.adamw), "adamw_elements": wl.adamw_elements(),
+                   "ns_steps": hp.ns_steps, "ns_coefficients": [hp.a, hp.b, hp.c],
+                   "momentum": hp.momentum, "nesterov": hp.nesterov, "lr": hp.lr,
+                   "weight_decay": hp.weight_decay, "lr_adjust": hp.lr_adjust,
+                   "nominal_ns_flop_per_step": flops},
+        "roofline": {
+            "kernel": GEMM_KERNEL,
+            "bound": "mfma",
+            "achieved": round(ns_tflops, 2),
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(ns_tflops / PEAK_BF16_TFLOPS, 4),
+            "traffic": traffic,
+            "launches_per_step": launches,
+            "avg_launch_ms": round(ns_ms / launches, 4) if launches else 0.0,
+            "nominal_flop_per_launch": flops / launches if launches else 0.0,
+        },
+        "phases_ms": {"prep_norm": round(prep_ms, 4), "ns": round(ns_ms, 4),
+                      "apply": round(apply_ms, 4), "adamw": round(adamw_ms, 4)},
+        "elementwise": {
+            "prep_GBps": round(prep_bytes / (prep_ms * 1e-3) / 1e9, 1) if prep_ms else None,
+            "apply_GBps": round(apply_bytes / (apply_ms * 1e-3) / 1e9, 1) if apply_ms else None,
+            "muon_elementwise_frac_hbm": round((prep_bytes + apply_bytes) / ((prep_ms + apply_ms) * 1e-3) / 1e9
+                                               / PEAK_HBM_GBS, 4) if (prep_ms + apply_ms) else None,
+            "muon_algorithmic_bytes": alg_bytes,
+            "adamw_GBps": round(adamw_bytes / (adamw_ms * 1e-3) / 1e9, 1) if adamw_ms else None,
+        },
+    }
+    if not args.no_cpu_baseline:
+        sample = {3: [0, 1], 2: [0, 4], 1: [0], 4: [0], 5: [1]}.get(args.workload, [0])
+        log("timing the fp64 oracle on a bounded sample (cpu_baseline)")
+        out["cpu_baseline"] = cpu_baseline(wl, sample, pool)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

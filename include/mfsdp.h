@@ -1,0 +1,168 @@
+/*
+ * mfsdp.h -- C ABI of the owner-local Muon / AdamW step for MI355X (gfx950).
+ *
+ * MatrixFSDP (arxiv 2607.05895) places every data-parallel-sharded 2D weight whole on one owner
+ * rank. After backward the owner holds the complete gradient of each matrix it owns and runs the
+ * Muon update on it locally, with no collective (Section 3; Section 4.4 routes each owned full
+ * matrix to Muon and the packed non-matrix "tail" tensors to AdamW). This library is that
+ * owner-side computation on one GPU:
+ *
+ *   mfsdp_muon_step      -- Muon over a heterogeneous list of whole matrices the rank owns
+ *   mfsdp_newton_schulz  -- the Newton-Schulz orthogonalisation of one matrix
+ *   mfsdp_adamw_step     -- AdamW over the rank's tail tensors
+ *
+ * Muon, per owned matrix with stored shape m x n (Section 5.1 uses torch.optim.Muon's update):
+ *   buf <- buf + (1 - beta) (g - buf)                    momentum EMA
+ *   u   <- g + beta (buf - g)   (Nesterov) or  u <- buf
+ *   X   <- u, or u^T when m > n  (r = min(m,n) rows, s = max(m,n) columns)
+ *   X   <- X / max(||X||_F, eps)
+ *   K times:  A = X X^T;  B = b A + c A A;  X <- a X + B X      (quintic NS)
+ *   O   <- X, transposed back when m > n
+ *   p   <- p (1 - lr wd) - lr f(m, n) O
+ *   f = 1 | sqrt(max(1, m/n)) | 0.2 sqrt(max(m, n))   (lr_adjust NONE | ORIGINAL | MATCH_RMS_ADAMW)
+ *
+ * Conventions shared by every entry point
+ *   - Pointers are device pointers (hipMalloc'd memory, e.g. torch CUDA tensors), contiguous
+ *     row-major, 16-byte aligned. The caller owns every buffer: parameters, gradients, optimizer
+ *     state, workspace and optional outputs. The library never frees or keeps them.
+ *   - Calls are asynchronous: they validate, enqueue kernels on `stream` (a hipStream_t, NULL =
+ *     the null stream) and return. Buffers must stay alive until the stream work completes.
+ *     A workspace may be reused by the next call on the same stream; calls on different streams
+ *     need different workspaces.
+ *   - Every argument check runs before anything is enqueued: on error nothing is modified.
+ *   - Results are deterministic: identical inputs give bitwise-identical outputs (fixed reduction
+ *     orders, no floating-point atomics).
+ *   - Non-finite inputs propagate; they are not checked.
+ *   - Entries must not overlap each other; grad must not alias param or state. Not checked.
+ *   - Return 0 on success, a negative mfsdp_status on failure; mfsdp_last_error() then describes
+ *     the failure (thread-local text).
+ */
+#ifndef MFSDP_H
+#define MFSDP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MFSDP_ABI_VERSION 1
+
+typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
+
+typedef enum {
+  MFSDP_LR_NONE = 0,            /* f = 1 */
+  MFSDP_LR_ORIGINAL = 1,        /* f = sqrt(max(1, m/n))  (torch.optim.Muon default) */
+  MFSDP_LR_MATCH_RMS_ADAMW = 2  /* f = 0.2 sqrt(max(m, n))  (the paper's setting, Section 5.1) */
+} mfsdp_lr_adjust;
+
+typedef enum {
+  MFSDP_OK = 0,
+  MFSDP_E_INVALID = -1,    /* bad argument: NULL, size <= 0, dtype, alignment, hyperparameter */
+  MFSDP_E_WORKSPACE = -2,  /* workspace NULL, misaligned or smaller than the size query */
+  MFSDP_E_HIP = -3         /* a HIP runtime call or kernel launch failed */
+} mfsdp_status;
+
+/* One whole matrix the rank owns (Section 3: the owner's full 2D shard).
+ *   param      m x n, param_dtype (F32 or BF16), updated in place (fp32 math, bf16 stored with
+ *              round-to-nearest-even)
+ *   grad       m x n, grad_dtype (F32 or BF16), read only
+ *   momentum   m x n fp32 Muon buffer, updated in place
+ *   m, n       stored rows and columns (the parameter's shape), both >= 1
+ *   update_out optional m x n fp32: receives O (the NS output, before lr scaling). NULL = off. */
+typedef struct {
+  void* param;
+  const void* grad;
+  float* momentum;
+  int64_t m;
+  int64_t n;
+  int32_t param_dtype;
+  int32_t grad_dtype;
+  float* update_out;
+} mfsdp_muon_entry;
+
+/* Muon hyperparameters, shared by every entry of one call.
+ *   lr >= 0, weight_decay >= 0, 0 <= momentum < 1, nesterov 0/1,
+ *   (a, b, c) NS coefficients, 0 <= ns_steps < 100, eps > 0 (norm clamp),
+ *   lr_adjust an mfsdp_lr_adjust, ns_dtype: BF16 = NS products on bf16 MFMA with fp32
+ *   accumulation and bf16 storage between products; F32 = fp32 throughout. */
+typedef struct {
+  float lr;
+  float weight_decay;
+  float momentum;
+  int32_t nesterov;
+  float a, b, c;
+  int32_t ns_steps;
+  float eps;
+  int32_t lr_adjust;
+  int32_t ns_dtype;
+} mfsdp_muon_hparams;
+
+/* One tail tensor (Section 4.4: non-matrix tensors stay on AdamW), flattened.
+ *   param, grad  numel elements of param_dtype / grad_dtype (F32 or BF16)
+ *   exp_avg, exp_avg_sq  numel fp32 moments, updated in place. */
+typedef struct {
+  void* param;
+  const void* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  int64_t numel;
+  int32_t param_dtype;
+  int32_t grad_dtype;
+} mfsdp_adamw_entry;
+
+/* Bytes of device workspace mfsdp_muon_step needs for these entries and hyperparameters
+ * (Newton-Schulz iterates in both layouts, the r x r Gram and polynomial matrices, norm
+ * partials and launch descriptors). Returns 0 if the arguments are invalid (see
+ * mfsdp_last_error). count == 0 returns 0 with no error. */
+size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,
+                                 const mfsdp_muon_hparams* hp);
+
+/* The owner's Muon step (Section 3; hyperparameters as in Section 5.1) for every entry.
+ * workspace: device memory of at least mfsdp_muon_workspace_size bytes, 256-byte aligned; its
+ * contents on entry are ignored and on return are unspecified. count == 0 is a no-op. */
+int mfsdp_muon_step(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* mfsdp_muon_step that also records caller-created HIP events (hipEvent_t, any may be NULL) on
+ * `stream` at the phase boundaries of the step, for timing each phase on the stream it runs on:
+ *   events[0] before the momentum pass, events[1] before the first Newton-Schulz product,
+ *   events[2] after the last Newton-Schulz product, events[3] after the parameter update.
+ * `events` itself may be NULL (then identical to mfsdp_muon_step). */
+int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
+                          const mfsdp_muon_hparams* hp, void* workspace, size_t workspace_bytes,
+                          void* stream, void* const* events);
+
+/* Bytes of workspace mfsdp_newton_schulz needs for one m x n matrix. 0 on invalid input. */
+size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype);
+
+/* out = NS_steps(x / max(||x||_F, eps)) for one m x n matrix (Section 2: iterations of
+ * whole-matrix products X X^T), transposing internally when m > n.
+ *   x    m x n, x_dtype (F32 or BF16), read only
+ *   out  m x n, out_dtype (F32 or BF16); must not alias x
+ *   ns_dtype as in mfsdp_muon_hparams; workspace sized by mfsdp_ns_workspace_size. */
+int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
+                        int64_t n, float a, float b, float c, int32_t steps, float eps,
+                        int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* AdamW on the tail tensors (Section 4.4; PyTorch AdamW per Section 5.1):
+ *   p <- p (1 - lr wd);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2
+ *   p <- p - lr / (1 - beta1^t) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps)
+ * step = t >= 1 is the step number after increment. lr, wd >= 0; betas in [0, 1); eps > 0.
+ * Needs no workspace. count == 0 is a no-op. */
+int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, float lr, float beta1,
+                     float beta2, float eps, float weight_decay, int64_t step, void* stream);
+
+/* Text for the last failure on the calling thread ("" if none). */
+const char* mfsdp_last_error(void);
+/* Name of a status code. */
+const char* mfsdp_status_string(int status);
+/* MFSDP_ABI_VERSION of the built library. */
+int mfsdp_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MFSDP_H */

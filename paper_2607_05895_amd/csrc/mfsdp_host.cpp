@@ -1,0 +1,591 @@
+// Host side of the C ABI declared in include/mfsdp.h: argument validation (all before any
+// launch), workspace planning, descriptor upload and the launch sequence of the owner step.
+//
+// Launch sequence of mfsdp_muon_step (all on the caller's stream):
+//   1. descriptor upload (pinned staging slot -> workspace)
+//   2. prep     : momentum EMA + Nesterov, Sum u^2 partials, u in both layouts   (one launch)
+//   3. norm     : per-matrix scale 1 / max(||u||_F, eps)                          (one launch)
+//   4. K times  : Gram A = X X^T, square B = bA + cAA, update X' = aX + BX        (3 launches
+//                 per step, each grouped over every matrix, heaviest tiles first)
+//   5. apply    : p <- p (1 - lr wd) - lr f O                                     (one launch)
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/mfsdp.h"
+#include "mfsdp_internal.h"
+
+using namespace mfsdp;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return status;
+}
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+bool valid_dtype(int32_t dt) { return dt == MFSDP_F32 || dt == MFSDP_BF16; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------------------------------------
+// Workspace plan for one NS problem (shared by the Muon step and standalone NS).
+struct NsPlan {
+  int64_t m, n, r, s, r_pad, s_pad;
+  bool tall;
+  int es;                   // element size of the NS dtype
+  size_t off_x[2], off_xt[2], off_g, off_h, off_partials, off_scale;
+  int prep_tiles_m, prep_tiles_n;
+  size_t bytes;             // total for this problem
+};
+
+NsPlan plan_ns(int64_t m, int64_t n, int ns_dtype, size_t base) {
+  NsPlan p{};
+  p.m = m;
+  p.n = n;
+  p.tall = m > n;
+  p.r = std::min(m, n);
+  p.s = std::max(m, n);
+  const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
+  p.r_pad = round_up(p.r, tile);
+  p.s_pad = round_up(p.s, tile);
+  p.es = ns_dtype == MFSDP_BF16 ? 2 : 4;
+  const size_t xb = align_up(size_t(p.r_pad) * size_t(p.s_pad) * p.es);
+  const size_t gb = align_up(size_t(p.r_pad) * size_t(p.r_pad) * p.es);
+  const int64_t rows = p.tall ? p.s_pad : p.r_pad, cols = p.tall ? p.r_pad : p.s_pad;
+  p.prep_tiles_m = int(rows / kPrepTile);
+  p.prep_tiles_n = int(cols / kPrepTile);
+  size_t o = base;
+  p.off_x[0] = o; o += xb;
+  p.off_x[1] = o; o += xb;
+  p.off_xt[0] = o; o += xb;
+  p.off_xt[1] = o; o += xb;
+  p.off_g = o; o += gb;
+  p.off_h = o; o += gb;
+  p.off_partials = o; o += align_up(size_t(p.prep_tiles_m) * p.prep_tiles_n * sizeof(float));
+  p.off_scale = o; o += kAlign;
+  p.bytes = o - base;
+  return p;
+}
+
+// Descriptor region at the start of the workspace.
+struct DescLayout {
+  size_t off_prep, off_norm, off_gemm[3], off_apply, bytes;
+};
+
+DescLayout plan_descs(int64_t count) {
+  DescLayout d{};
+  size_t o = 0;
+  d.off_prep = o; o += align_up(sizeof(PrepDesc) * count);
+  d.off_norm = o; o += align_up(sizeof(NormDesc) * count);
+  for (int k = 0; k < 3; ++k) { d.off_gemm[k] = o; o += align_up(sizeof(GemmDesc) * count); }
+  d.off_apply = o; o += align_up(sizeof(ApplyDesc) * count);
+  d.bytes = o;
+  return d;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Pinned staging ring for descriptor uploads. A slot is reused only after the copy that read it
+// has completed (event per slot).
+class StagingRing {
+ public:
+  static constexpr int kSlots = 16;
+  int acquire(size_t bytes, void** host, hipStream_t st) {
+    (void)st;
+    std::lock_guard<std::mutex> lk(mu_);
+    const int s = next_;
+    next_ = (next_ + 1) % kSlots;
+    Slot& sl = slots_[s];
+    if (sl.event) {
+      hipError_t e = hipEventSynchronize(sl.event);
+      if (e != hipSuccess) return fail(MFSDP_E_HIP, "staging event: %s", hipGetErrorString(e));
+    }
+    if (sl.cap < bytes) {
+      if (sl.ptr) (void)hipHostFree(sl.ptr);
+      sl.ptr = nullptr;
+      sl.cap = 0;
+      size_t cap = std::max<size_t>(bytes, 64 * 1024);
+      hipError_t e = hipHostMalloc(&sl.ptr, cap, hipHostMallocDefault);
+      if (e != hipSuccess) return fail(MFSDP_E_HIP, "hipHostMalloc: %s", hipGetErrorString(e));
+      sl.cap = cap;
+    }
+    if (!sl.event) {
+      hipError_t e = hipEventCreateWithFlags(&sl.event, hipEventDisableTiming);
+      if (e != hipSuccess) return fail(MFSDP_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+    }
+    *host = sl.ptr;
+    return s;
+  }
+  int upload(int slot, void* dst, size_t bytes, hipStream_t st) {
+    Slot& sl = slots_[slot];
+    hipError_t e = hipMemcpyAsync(dst, sl.ptr, bytes, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(MFSDP_E_HIP, "descriptor upload: %s", hipGetErrorString(e));
+    e = hipEventRecord(sl.event, st);
+    if (e != hipSuccess) return fail(MFSDP_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+    return MFSDP_OK;
+  }
+
+ private:
+  struct Slot {
+    void* ptr = nullptr;
+    size_t cap = 0;
+    hipEvent_t event = nullptr;
+  };
+  std::mutex mu_;
+  int next_ = 0;
+  Slot slots_[kSlots];
+};
+
+StagingRing& ring() {
+  static StagingRing* r = new StagingRing();  // lives until process exit
+  return *r;
+}
+
+int check_hp(const mfsdp_muon_hparams* hp) {
+  if (!hp) return fail(MFSDP_E_INVALID, "hparams is NULL");
+  if (!(hp->lr >= 0.0f) || !std::isfinite(hp->lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
+  if (!(hp->weight_decay >= 0.0f) || !std::isfinite(hp->weight_decay))
+    return fail(MFSDP_E_INVALID, "weight_decay must be >= 0");
+  if (!(hp->momentum >= 0.0f && hp->momentum < 1.0f))
+    return fail(MFSDP_E_INVALID, "momentum must be in [0, 1)");
+  if (hp->nesterov != 0 && hp->nesterov != 1) return fail(MFSDP_E_INVALID, "nesterov must be 0 or 1");
+  if (!std::isfinite(hp->a) || !std::isfinite(hp->b) || !std::isfinite(hp->c))
+    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
+  if (hp->ns_steps < 0 || hp->ns_steps >= 100) return fail(MFSDP_E_INVALID, "ns_steps must be in [0, 100)");
+  if (!(hp->eps > 0.0f) || !std::isfinite(hp->eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (hp->lr_adjust < MFSDP_LR_NONE || hp->lr_adjust > MFSDP_LR_MATCH_RMS_ADAMW)
+    return fail(MFSDP_E_INVALID, "unknown lr_adjust %d", hp->lr_adjust);
+  if (!valid_dtype(hp->ns_dtype)) return fail(MFSDP_E_INVALID, "unknown ns_dtype %d", hp->ns_dtype);
+  return MFSDP_OK;
+}
+
+constexpr int64_t kMaxDim = int64_t(1) << 20;   // per-side limit (index math stays in int32 tiles)
+
+int check_shape(int64_t m, int64_t n, const char* what, int64_t i) {
+  if (m <= 0 || n <= 0) return fail(MFSDP_E_INVALID, "%s %lld: shape %lldx%lld must be positive", what,
+                                    (long long)i, (long long)m, (long long)n);
+  if (m > kMaxDim || n > kMaxDim)
+    return fail(MFSDP_E_INVALID, "%s %lld: side larger than %lld", what, (long long)i, (long long)kMaxDim);
+  return MFSDP_OK;
+}
+
+int check_entries(const mfsdp_muon_entry* entries, int64_t count) {
+  if (count < 0) return fail(MFSDP_E_INVALID, "count must be >= 0");
+  if (count > 0 && !entries) return fail(MFSDP_E_INVALID, "entries is NULL");
+  if (count > (1 << 20)) return fail(MFSDP_E_INVALID, "too many entries");
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_muon_entry& e = entries[i];
+    if (!e.param || !e.grad || !e.momentum) return fail(MFSDP_E_INVALID, "entry %lld: NULL pointer", (long long)i);
+    int st = check_shape(e.m, e.n, "entry", i);
+    if (st) return st;
+    if (!valid_dtype(e.param_dtype) || !valid_dtype(e.grad_dtype))
+      return fail(MFSDP_E_INVALID, "entry %lld: unsupported dtype", (long long)i);
+    if (!aligned16(e.param) || !aligned16(e.grad) || !aligned16(e.momentum) ||
+        (e.update_out && !aligned16(e.update_out)))
+      return fail(MFSDP_E_INVALID, "entry %lld: pointers must be 16-byte aligned", (long long)i);
+  }
+  return MFSDP_OK;
+}
+
+float lr_factor(int64_t m, int64_t n, int mode) {
+  if (mode == MFSDP_LR_ORIGINAL) return float(std::sqrt(std::max(1.0, double(m) / double(n))));
+  if (mode == MFSDP_LR_MATCH_RMS_ADAMW) return float(0.2 * std::sqrt(double(std::max(m, n))));
+  return 1.0f;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MFSDP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Builds and enqueues the NS pipeline for a set of problems that already have their prep
+// descriptors filled. Shared by the Muon step and standalone NS.
+struct Problem {
+  NsPlan plan;
+  size_t base;  // not used after planning, kept for clarity
+};
+
+void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_muon_hparams& hp,
+                     GemmDesc* syrk, GemmDesc* sqr, GemmDesc* upd, int tile,
+                     int* tiles_syrk, int* tiles_sqr, int* tiles_upd) {
+  const int n = int(plans.size());
+  std::vector<int> order(n);
+  for (int i = 0; i < n; ++i) order[i] = i;
+  auto fill = [&](GemmDesc* out, int phase, int* total) {
+    // heaviest K first: with tiles of equal size the per-tile work is proportional to K
+    std::vector<int> ord = order;
+    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) {
+      const NsPlan& a = plans[x];
+      const NsPlan& b = plans[y];
+      const int64_t ka = phase == 0 ? a.s_pad : a.r_pad, kb = phase == 0 ? b.s_pad : b.r_pad;
+      return ka > kb;
+    });
+    int begin = 0;
+    for (int k = 0; k < n; ++k) {
+      const NsPlan& p = plans[ord[k]];
+      GemmDesc d{};
+      const int tr = int(p.r_pad / tile), ts = int(p.s_pad / tile);
+      for (int par = 0; par < 2; ++par) {
+        uint8_t* xin = ws + p.off_x[par];
+        uint8_t* xtin = ws + p.off_xt[par];
+        uint8_t* xout = ws + p.off_x[par ^ 1];
+        uint8_t* xtout = ws + p.off_xt[par ^ 1];
+        if (phase == 0) {         // A = X X^T
+          d.P[par] = xin; d.Q[par] = xin; d.E[par] = nullptr;
+          d.C[par] = ws + p.off_g; d.CT[par] = nullptr;
+        } else if (phase == 1) {  // B = c A A + b A
+          d.P[par] = ws + p.off_g; d.Q[par] = ws + p.off_g; d.E[par] = ws + p.off_g;
+          d.C[par] = ws + p.off_h; d.CT[par] = nullptr;
+        } else {                  // X' = B X + a X, stored as X' and X'^T
+          d.P[par] = ws + p.off_h; d.Q[par] = xtin; d.E[par] = xin;
+          d.C[par] = xout; d.CT[par] = xtout;
+        }
+      }
+      d.scale = reinterpret_cast<const float*>(ws + p.off_scale);
+      if (phase == 0) {
+        d.ldp = d.ldq = p.s_pad; d.lde = 0; d.ldc = p.r_pad; d.ldct = 0;
+        d.M = d.N = int(p.r_pad); d.K = int(p.s_pad);
+        d.alpha = 1.0f; d.beta = 0.0f; d.alpha_scale_pow = 2; d.beta_scale_pow = 0;
+        d.sym = 1; d.tiles_m = d.tiles_n = tr;
+        d.tile_count = tr * (tr + 1) / 2;
+        d.last_c = 1; d.last_ct = 0;
+      } else if (phase == 1) {
+        d.ldp = d.ldq = d.lde = d.ldc = p.r_pad; d.ldct = 0;
+        d.M = d.N = d.K = int(p.r_pad);
+        d.alpha = hp.c; d.beta = hp.b; d.alpha_scale_pow = 0; d.beta_scale_pow = 0;
+        d.sym = 1; d.tiles_m = d.tiles_n = tr;
+        d.tile_count = tr * (tr + 1) / 2;
+        d.last_c = 1; d.last_ct = 0;
+      } else {
+        d.ldp = p.r_pad; d.ldq = p.r_pad; d.lde = p.s_pad; d.ldc = p.s_pad; d.ldct = p.r_pad;
+        d.M = int(p.r_pad); d.N = int(p.s_pad); d.K = int(p.r_pad);
+        d.alpha = 1.0f; d.beta = hp.a; d.alpha_scale_pow = 1; d.beta_scale_pow = 1;
+        d.sym = 0; d.tiles_m = tr; d.tiles_n = ts;
+        d.tile_count = tr * ts;
+        // the final iterate is read in the parameter's orientation only
+        d.last_c = p.tall ? 0 : 1;
+        d.last_ct = p.tall ? 1 : 0;
+      }
+      d.tile_begin = begin;
+      begin += d.tile_count;
+      out[k] = d;
+    }
+    *total = begin;
+  };
+  fill(syrk, 0, tiles_syrk);
+  fill(sqr, 1, tiles_sqr);
+  fill(upd, 2, tiles_upd);
+}
+
+PrepDesc make_prep(const NsPlan& p, uint8_t* ws, const void* grad, int grad_dtype, float* momentum,
+                   int tile_begin) {
+  PrepDesc d{};
+  d.grad = grad;
+  d.momentum = momentum;
+  // u in its stored orientation is X (wide) or X^T (tall); its transpose goes to the other one
+  if (p.tall) {
+    d.d_out = ws + p.off_xt[0]; d.ld_d = p.r_pad;
+    d.t_out = ws + p.off_x[0];  d.ld_t = p.s_pad;
+  } else {
+    d.d_out = ws + p.off_x[0];  d.ld_d = p.s_pad;
+    d.t_out = ws + p.off_xt[0]; d.ld_t = p.r_pad;
+  }
+  d.partials = reinterpret_cast<float*>(ws + p.off_partials);
+  d.m = p.m;
+  d.n = p.n;
+  d.tiles_m = p.prep_tiles_m;
+  d.tiles_n = p.prep_tiles_n;
+  d.grad_dtype = grad_dtype;
+  d.tile_begin = tile_begin;
+  return d;
+}
+
+ApplyDesc make_apply(const NsPlan& p, uint8_t* ws, int steps, void* param, int param_dtype,
+                     float* update_out, int mode, float decay, float step, int tile_begin) {
+  ApplyDesc d{};
+  const int par = steps & 1;  // parity of the buffer holding the final iterate
+  if (p.tall) { d.o = ws + p.off_xt[par]; d.ld_o = p.r_pad; }
+  else        { d.o = ws + p.off_x[par];  d.ld_o = p.s_pad; }
+  d.param = param;
+  d.update_out = update_out;
+  d.scale = reinterpret_cast<const float*>(ws + p.off_scale);
+  d.use_scale = steps == 0 ? 1 : 0;
+  d.m = p.m;
+  d.n = p.n;
+  d.param_dtype = param_dtype;
+  d.mode = mode;
+  d.decay = decay;
+  d.step = step;
+  d.tiles_m = int((p.m + 63) / 64);
+  d.tiles_n = int((p.n + 63) / 64);
+  d.tile_begin = tile_begin;
+  return d;
+}
+
+size_t muon_ws_bytes(const mfsdp_muon_entry* entries, int64_t count, int ns_dtype,
+                     std::vector<NsPlan>* plans) {
+  const DescLayout dl = plan_descs(count);
+  size_t o = dl.bytes;
+  for (int64_t i = 0; i < count; ++i) {
+    NsPlan p = plan_ns(entries[i].m, entries[i].n, ns_dtype, o);
+    o += p.bytes;
+    if (plans) plans->push_back(p);
+  }
+  return o;
+}
+
+// Enqueue everything after the descriptors are in host staging memory `h`.
+int record(void* const* events, int k, hipStream_t st) {
+  if (!events || !events[k]) return MFSDP_OK;
+  hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[k]), st);
+  return e == hipSuccess ? MFSDP_OK : hip_fail(e, "hipEventRecord");
+}
+
+int enqueue_pipeline(const std::vector<NsPlan>& plans, uint8_t* ws, const DescLayout& dl,
+                     int slot, int steps, int ns_dtype, float beta, int nesterov, float eps,
+                     int prep_tiles, int apply_tiles, int t0, int t1, int t2, hipStream_t st,
+                     void* const* events) {
+  const int count = int(plans.size());
+  int rc = ring().upload(slot, ws, dl.bytes, st);
+  if (rc) return rc;
+  if ((rc = record(events, 0, st))) return rc;
+  hipError_t e;
+  e = launch_prep(reinterpret_cast<const PrepDesc*>(ws + dl.off_prep), count, prep_tiles, ns_dtype,
+                  beta, nesterov, st);
+  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  e = launch_norm(reinterpret_cast<const NormDesc*>(ws + dl.off_norm), count, eps, st);
+  if (e != hipSuccess) return hip_fail(e, "norm launch");
+  if ((rc = record(events, 1, st))) return rc;
+  const int tiles[3] = {t0, t1, t2};
+  for (int k = 0; k < steps; ++k) {
+    for (int ph = 0; ph < 3; ++ph) {
+      e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, tiles[ph],
+                      ns_dtype, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0, st);
+      if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+    }
+  }
+  if ((rc = record(events, 2, st))) return rc;
+  e = launch_apply(reinterpret_cast<const ApplyDesc*>(ws + dl.off_apply), count, apply_tiles,
+                   ns_dtype, st);
+  if (e != hipSuccess) return hip_fail(e, "apply launch");
+  return record(events, 3, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+int mfsdp_abi_version(void) { return MFSDP_ABI_VERSION; }
+
+const char* mfsdp_last_error(void) { return g_last_error.c_str(); }
+
+const char* mfsdp_status_string(int status) {
+  switch (status) {
+    case MFSDP_OK: return "MFSDP_OK";
+    case MFSDP_E_INVALID: return "MFSDP_E_INVALID";
+    case MFSDP_E_WORKSPACE: return "MFSDP_E_WORKSPACE";
+    case MFSDP_E_HIP: return "MFSDP_E_HIP";
+    default: return "MFSDP_E_UNKNOWN";
+  }
+}
+
+size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,
+                                 const mfsdp_muon_hparams* hp) {
+  g_last_error.clear();
+  if (check_hp(hp) || check_entries(entries, count)) return 0;
+  if (count == 0) return 0;
+  return muon_ws_bytes(entries, count, hp->ns_dtype, nullptr);
+}
+
+int mfsdp_muon_step(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  return mfsdp_muon_step_timed(entries, count, hp, workspace, workspace_bytes, stream, nullptr);
+}
+
+int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
+                          const mfsdp_muon_hparams* hp, void* workspace, size_t workspace_bytes,
+                          void* stream, void* const* events) {
+  g_last_error.clear();
+  int rc = check_hp(hp);
+  if (rc) return rc;
+  rc = check_entries(entries, count);
+  if (rc) return rc;
+  if (count == 0) return MFSDP_OK;
+  std::vector<NsPlan> plans;
+  const size_t need = muon_ws_bytes(entries, count, hp->ns_dtype, &plans);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return fail(MFSDP_E_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(MFSDP_E_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  const DescLayout dl = plan_descs(count);
+  void* hptr = nullptr;
+  const int slot = ring().acquire(dl.bytes, &hptr, st);
+  if (slot < 0) return slot;
+  uint8_t* h = static_cast<uint8_t*>(hptr);
+  std::memset(h, 0, dl.bytes);
+
+  auto* prep = reinterpret_cast<PrepDesc*>(h + dl.off_prep);
+  auto* norm = reinterpret_cast<NormDesc*>(h + dl.off_norm);
+  auto* apply = reinterpret_cast<ApplyDesc*>(h + dl.off_apply);
+  int prep_tiles = 0, apply_tiles = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_muon_entry& en = entries[i];
+    const NsPlan& p = plans[i];
+    prep[i] = make_prep(p, ws, en.grad, en.grad_dtype, en.momentum, prep_tiles);
+    prep_tiles += p.prep_tiles_m * p.prep_tiles_n;
+    norm[i].partials = reinterpret_cast<const float*>(ws + p.off_partials);
+    norm[i].count = p.prep_tiles_m * p.prep_tiles_n;
+    norm[i].scale = reinterpret_cast<float*>(ws + p.off_scale);
+    const float f = lr_factor(en.m, en.n, hp->lr_adjust);
+    apply[i] = make_apply(p, ws, hp->ns_steps, en.param, en.param_dtype, en.update_out, 0,
+                          1.0f - hp->lr * hp->weight_decay, hp->lr * f, apply_tiles);
+    apply_tiles += apply[i].tiles_m * apply[i].tiles_n;
+  }
+  const int tile = hp->ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
+  int t0 = 0, t1 = 0, t2 = 0;
+  fill_gemm_descs(plans, ws, *hp, reinterpret_cast<GemmDesc*>(h + dl.off_gemm[0]),
+                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[1]),
+                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[2]), tile, &t0, &t1, &t2);
+  return enqueue_pipeline(plans, ws, dl, slot, hp->ns_steps, hp->ns_dtype, hp->momentum,
+                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, t0, t1, t2, st, events);
+}
+
+size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype) {
+  g_last_error.clear();
+  if (!valid_dtype(ns_dtype)) { fail(MFSDP_E_INVALID, "unknown ns_dtype %d", ns_dtype); return 0; }
+  if (check_shape(m, n, "matrix", 0)) return 0;
+  const DescLayout dl = plan_descs(1);
+  return dl.bytes + plan_ns(m, n, ns_dtype, dl.bytes).bytes;
+}
+
+int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
+                        int64_t n, float a, float b, float c, int32_t steps, float eps,
+                        int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (!x || !out) return fail(MFSDP_E_INVALID, "x and out must be non-NULL");
+  if (x == out) return fail(MFSDP_E_INVALID, "out must not alias x");
+  if (!valid_dtype(x_dtype) || !valid_dtype(out_dtype) || !valid_dtype(ns_dtype))
+    return fail(MFSDP_E_INVALID, "unsupported dtype");
+  int rc = check_shape(m, n, "matrix", 0);
+  if (rc) return rc;
+  if (!aligned16(x) || !aligned16(out)) return fail(MFSDP_E_INVALID, "pointers must be 16-byte aligned");
+  if (steps < 0 || steps >= 100) return fail(MFSDP_E_INVALID, "steps must be in [0, 100)");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
+    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
+  const DescLayout dl = plan_descs(1);
+  std::vector<NsPlan> plans{plan_ns(m, n, ns_dtype, dl.bytes)};
+  const size_t need = dl.bytes + plans[0].bytes;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return fail(MFSDP_E_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
+  if (workspace_bytes < need)
+    return fail(MFSDP_E_WORKSPACE, "workspace too small: %zu < %zu bytes", workspace_bytes, need);
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  void* hptr = nullptr;
+  const int slot = ring().acquire(dl.bytes, &hptr, st);
+  if (slot < 0) return slot;
+  uint8_t* h = static_cast<uint8_t*>(hptr);
+  std::memset(h, 0, dl.bytes);
+  const NsPlan& p = plans[0];
+  auto* prep = reinterpret_cast<PrepDesc*>(h + dl.off_prep);
+  auto* norm = reinterpret_cast<NormDesc*>(h + dl.off_norm);
+  auto* apply = reinterpret_cast<ApplyDesc*>(h + dl.off_apply);
+  prep[0] = make_prep(p, ws, x, x_dtype, nullptr, 0);
+  norm[0].partials = reinterpret_cast<const float*>(ws + p.off_partials);
+  norm[0].count = p.prep_tiles_m * p.prep_tiles_n;
+  norm[0].scale = reinterpret_cast<float*>(ws + p.off_scale);
+  apply[0] = make_apply(p, ws, steps, out, out_dtype, nullptr, 1, 1.0f, 0.0f, 0);
+  mfsdp_muon_hparams hp{};
+  hp.a = a; hp.b = b; hp.c = c;
+  const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
+  int t0 = 0, t1 = 0, t2 = 0;
+  fill_gemm_descs(plans, ws, hp, reinterpret_cast<GemmDesc*>(h + dl.off_gemm[0]),
+                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[1]),
+                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[2]), tile, &t0, &t1, &t2);
+  return enqueue_pipeline(plans, ws, dl, slot, steps, ns_dtype, 0.0f, 0, eps,
+                          p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n,
+                          t0, t1, t2, st, nullptr);
+}
+
+int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, float lr, float beta1,
+                     float beta2, float eps, float weight_decay, int64_t step, void* stream) {
+  g_last_error.clear();
+  if (count < 0) return fail(MFSDP_E_INVALID, "count must be >= 0");
+  if (count > 0 && !entries) return fail(MFSDP_E_INVALID, "entries is NULL");
+  if (!(lr >= 0.0f) || !std::isfinite(lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
+  if (!(weight_decay >= 0.0f) || !std::isfinite(weight_decay))
+    return fail(MFSDP_E_INVALID, "weight_decay must be >= 0");
+  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+    return fail(MFSDP_E_INVALID, "betas must be in [0, 1)");
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (step < 1) return fail(MFSDP_E_INVALID, "step must be >= 1");
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_adamw_entry& e = entries[i];
+    if (!e.param || !e.grad || !e.exp_avg || !e.exp_avg_sq)
+      return fail(MFSDP_E_INVALID, "entry %lld: NULL pointer", (long long)i);
+    if (e.numel <= 0) return fail(MFSDP_E_INVALID, "entry %lld: numel must be positive", (long long)i);
+    if (e.numel > (int64_t(1) << 40)) return fail(MFSDP_E_INVALID, "entry %lld: numel too large", (long long)i);
+    if (!valid_dtype(e.param_dtype) || !valid_dtype(e.grad_dtype))
+      return fail(MFSDP_E_INVALID, "entry %lld: unsupported dtype", (long long)i);
+    if (!aligned16(e.param) || !aligned16(e.grad) || !aligned16(e.exp_avg) || !aligned16(e.exp_avg_sq))
+      return fail(MFSDP_E_INVALID, "entry %lld: pointers must be 16-byte aligned", (long long)i);
+  }
+  if (count == 0) return MFSDP_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const double bc1 = 1.0 - std::pow(double(beta1), double(step));
+  const double bc2 = 1.0 - std::pow(double(beta2), double(step));
+  AdamWBatch batch{};
+  batch.decay = 1.0f - lr * weight_decay;
+  batch.beta1 = beta1;
+  batch.beta2 = beta2;
+  batch.step_size = float(double(lr) / bc1);
+  batch.inv_sqrt_bc2 = float(1.0 / std::sqrt(bc2));
+  batch.eps = eps;
+  int64_t i = 0;
+  while (i < count) {
+    batch.count = 0;
+    int64_t blocks = 0;
+    // one launch per group of up to kAdamWMaxPerLaunch tensors; grid kept below 2^31 blocks
+    while (i < count && batch.count < kAdamWMaxPerLaunch) {
+      const int64_t nb = (entries[i].numel + kAdamWBlockElems - 1) / kAdamWBlockElems;
+      if (batch.count > 0 && blocks + nb > (int64_t(1) << 30)) break;
+      AdamWDesc& d = batch.d[batch.count++];
+      d.param = entries[i].param;
+      d.grad = entries[i].grad;
+      d.exp_avg = entries[i].exp_avg;
+      d.exp_avg_sq = entries[i].exp_avg_sq;
+      d.numel = entries[i].numel;
+      d.param_dtype = entries[i].param_dtype;
+      d.grad_dtype = entries[i].grad_dtype;
+      d.block_begin = int32_t(blocks);
+      blocks += nb;
+      ++i;
+    }
+    hipError_t e = launch_adamw(batch, int(blocks), st);
+    if (e != hipSuccess) return hip_fail(e, "AdamW launch");
+  }
+  return MFSDP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// Internal descriptors and kernel launchers shared by the host library and the HIP kernels.
+//
+// Data layout in HBM for one Muon entry with stored shape m x n (r = min, s = max):
+//   the NS iterate is kept in both layouts, zero padded to the NS tile size:
+//     X[0], X[1]   r_pad x s_pad row-major   (ld = s_pad)   -- ping-pong over NS steps
+//     XT[0], XT[1] s_pad x r_pad row-major   (ld = r_pad)   -- X^T of the same iterate
+//     G            r_pad x r_pad             A = X X^T (symmetric)
+//     H            r_pad x r_pad             B = b A + c A A (symmetric)
+//   Zero padding is exact for the iteration: padded rows/columns of X give zero rows/columns of
+//   A and B, and stay zero in a X + B X.
+//   Every NS product is then an "NT" product C = P Q^T with both operands K-contiguous:
+//     Gram      A = X X^T             P = Q = X,  K = s_pad
+//     square    A A = A A^T           P = Q = A,  K = r_pad   (A symmetric)
+//     update    B X = B (X^T)^T       P = B, Q = X^T, K = r_pad
+//   The update writes X' in both layouts so the next step again reads K-contiguous operands.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mfsdp {
+
+constexpr int kDtF32 = 0;
+constexpr int kDtBF16 = 1;
+
+// ---------------------------------------------------------------------------------------------
+// prep: momentum EMA + Nesterov (or a plain copy for standalone NS), Sum u^2 partials, and the
+// NS input written in both layouts. One 64 x 64 tile of the stored m x n matrix per workgroup.
+struct PrepDesc {
+  const void* grad;      // m x n, grad_dtype (the NS input for standalone NS)
+  float* momentum;       // m x n fp32, or null for standalone NS
+  void* d_out;           // u in stored orientation, padded rows x cols, ld_d (ns dtype)
+  void* t_out;           // u^T, ld_t (ns dtype)
+  float* partials;       // one Sum u^2 per tile
+  int64_t m, n;          // stored shape
+  int64_t ld_d, ld_t;
+  int32_t tiles_m, tiles_n;  // over the padded domain, 64 x 64
+  int32_t grad_dtype;
+  int32_t tile_begin;    // first global tile index of this entry
+};
+
+// norm finalize: scale = 1 / max(sqrt(Sum partials), eps), deterministic order.
+struct NormDesc {
+  const float* partials;
+  int32_t count;
+  float* scale;
+};
+
+// Grouped NT GEMM problem: C = alpha * P Q^T + beta * E, stored row-major in C and/or
+// transposed in CT. Both ping-pong alternatives are kept, indexed by step parity.
+struct GemmDesc {
+  const void* P[2];
+  const void* Q[2];
+  const void* E[2];
+  void* C[2];
+  void* CT[2];
+  const float* scale;    // per-matrix norm scale (used on the first NS step), may be null
+  int64_t ldp, ldq, lde, ldc, ldct;
+  int32_t M, N, K;       // padded sizes, multiples of the tile
+  float alpha, beta;
+  int32_t alpha_scale_pow;  // on the first step alpha *= scale^pow
+  int32_t beta_scale_pow;
+  int32_t sym;           // 1: only tiles bi <= bj, stored to (bi,bj) and mirrored to (bj,bi)
+  int32_t tiles_m, tiles_n;
+  int32_t tile_begin;    // prefix over the problems of one launch
+  int32_t tile_count;
+  int32_t last_c, last_ct;  // on the last step: write C / CT (1) or skip (0)
+};
+
+// apply: p <- p (1 - lr wd) - lr f (oscale O), or out <- oscale O for standalone NS.
+struct ApplyDesc {
+  const void* o;         // O in stored orientation (ns dtype), ld_o
+  void* param;           // m x n, param dtype (or NS output)
+  float* update_out;     // optional fp32 m x n
+  const float* scale;    // norm scale, applied when no NS step ran (K = 0)
+  int64_t m, n, ld_o;
+  int32_t param_dtype;
+  int32_t use_scale;
+  int32_t mode;          // 0 = Muon parameter update, 1 = write O to param (standalone NS)
+  float decay;           // 1 - lr wd
+  float step;            // lr f
+  int32_t tiles_m, tiles_n;
+  int32_t tile_begin;
+};
+
+constexpr int kAdamWMaxPerLaunch = 32;
+struct AdamWDesc {
+  void* param;
+  const void* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  int64_t numel;
+  int32_t param_dtype, grad_dtype;
+  int32_t block_begin;
+};
+struct AdamWBatch {
+  AdamWDesc d[kAdamWMaxPerLaunch];
+  int32_t count;
+  float decay;           // 1 - lr wd
+  float beta1, beta2;
+  float step_size;       // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
+  float eps;
+};
+constexpr int kAdamWBlockElems = 4096;
+
+// Launchers (return hipError_t of the launch).
+hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
+                       float beta, int nesterov, hipStream_t st);
+hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
+hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, int ns_dtype,
+                       int parity, int first_step, int last_step, hipStream_t st);
+hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
+                        hipStream_t st);
+hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);
+
+// NS tile sizes (padding granularity of the workspace buffers).
+constexpr int kTileBF16 = 256;
+constexpr int kTileF32 = 64;
+constexpr int kPrepTile = 64;
+
+}  // namespace mfsdp

@@ -1,0 +1,217 @@
+"""ctypes binding of libmfsdp.so (the C ABI in include/mfsdp.h).
+
+Argument marshalling only: every step of the owner update runs in the library's HIP kernels.
+The functions keep the C names; the ``*_t`` helpers accept torch tensors and pass their device
+pointers and the current HIP stream. Loading fails loudly if the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmfsdp.so")
+
+F32, BF16 = 0, 1
+LR_NONE, LR_ORIGINAL, LR_MATCH_RMS_ADAMW = 0, 1, 2
+OK, E_INVALID, E_WORKSPACE, E_HIP = 0, -1, -2, -3
+_NS_DT = {"bf16": BF16, "f32": F32}
+_LR_MODES = {"none": LR_NONE, "original": LR_ORIGINAL, "match_rms_adamw": LR_MATCH_RMS_ADAMW}
+EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_timed", "mfsdp_ns_workspace_size",
+           "mfsdp_newton_schulz", "mfsdp_adamw_step", "mfsdp_last_error", "mfsdp_status_string",
+           "mfsdp_abi_version")
+
+
+class MuonEntry(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("momentum", ctypes.c_void_p), ("m", ctypes.c_int64), ("n", ctypes.c_int64),
+                ("param_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
+                ("update_out", ctypes.c_void_p)]
+
+
+class MuonHParams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("momentum", ctypes.c_float), ("nesterov", ctypes.c_int32),
+                ("a", ctypes.c_float), ("b", ctypes.c_float), ("c", ctypes.c_float),
+                ("ns_steps", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("lr_adjust", ctypes.c_int32), ("ns_dtype", ctypes.c_int32)]
+
+
+class AdamWEntry(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p),
+                ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
+                ("numel", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
+                ("grad_dtype", ctypes.c_int32)]
+
+
+class MfsdpError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmfsdp.so once. Raises if it is missing: there is no fallback path."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2607_05895_amd.build_lib`")
+        # torch (the memory/stream plumbing) must be loaded first so the library binds to the same
+        # HIP runtime instance (its libamdhip64 carries the soname the library links against)
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+        L.mfsdp_muon_workspace_size.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams)]
+        L.mfsdp_muon_workspace_size.restype = sz
+        L.mfsdp_muon_step.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams), vp, sz, vp]
+        L.mfsdp_muon_step.restype = ctypes.c_int
+        L.mfsdp_muon_step_timed.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams),
+                                            vp, sz, vp, ctypes.POINTER(ctypes.c_void_p)]
+        L.mfsdp_muon_step_timed.restype = ctypes.c_int
+        L.mfsdp_ns_workspace_size.argtypes = [i64, i64, i32]
+        L.mfsdp_ns_workspace_size.restype = sz
+        L.mfsdp_newton_schulz.argtypes = [vp, i32, vp, i32, i64, i64, f32, f32, f32, i32, f32, i32, vp, sz, vp]
+        L.mfsdp_newton_schulz.restype = ctypes.c_int
+        L.mfsdp_adamw_step.argtypes = [ctypes.POINTER(AdamWEntry), i64, f32, f32, f32, f32, f32, i64, vp]
+        L.mfsdp_adamw_step.restype = ctypes.c_int
+        L.mfsdp_last_error.argtypes = []
+        L.mfsdp_last_error.restype = ctypes.c_char_p
+        L.mfsdp_status_string.argtypes = [ctypes.c_int]
+        L.mfsdp_status_string.restype = ctypes.c_char_p
+        L.mfsdp_abi_version.argtypes = []
+        L.mfsdp_abi_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int) -> None:
+    if status != OK:
+        raise MfsdpError(status, lib().mfsdp_last_error().decode())
+
+
+def _entries(arr, cls):
+    arr = list(arr)
+    return (cls * max(1, len(arr)))(*arr), len(arr)
+
+
+# ------------------------------------------------------------------- C names, raw arguments
+
+def mfsdp_abi_version() -> int:
+    return lib().mfsdp_abi_version()
+
+
+def mfsdp_last_error() -> str:
+    return lib().mfsdp_last_error().decode()
+
+
+def mfsdp_status_string(status: int) -> str:
+    return lib().mfsdp_status_string(status).decode()
+
+
+def mfsdp_muon_workspace_size(entries: Sequence[MuonEntry], hp: MuonHParams) -> int:
+    arr, n = _entries(entries, MuonEntry)
+    size = lib().mfsdp_muon_workspace_size(arr, n, ctypes.byref(hp))
+    if size == 0 and n > 0:
+        raise MfsdpError(E_INVALID, mfsdp_last_error())
+    return size
+
+
+def mfsdp_muon_step(entries: Sequence[MuonEntry], hp: MuonHParams, workspace: int,
+                    workspace_bytes: int, stream: int = 0) -> None:
+    arr, n = _entries(entries, MuonEntry)
+    _check(lib().mfsdp_muon_step(arr, n, ctypes.byref(hp), workspace, workspace_bytes, stream))
+
+
+def mfsdp_muon_step_timed(entries: Sequence[MuonEntry], hp: MuonHParams, workspace: int,
+                          workspace_bytes: int, stream: int, events: Sequence[int]) -> None:
+    arr, n = _entries(entries, MuonEntry)
+    ev = (ctypes.c_void_p * 4)(*list(events))
+    _check(lib().mfsdp_muon_step_timed(arr, n, ctypes.byref(hp), workspace, workspace_bytes,
+                                       stream, ev))
+
+
+def mfsdp_ns_workspace_size(m: int, n: int, ns_dtype: int) -> int:
+    size = lib().mfsdp_ns_workspace_size(m, n, ns_dtype)
+    if size == 0:
+        raise MfsdpError(E_INVALID, mfsdp_last_error())
+    return size
+
+
+def mfsdp_newton_schulz(x: int, x_dtype: int, out: int, out_dtype: int, m: int, n: int, a: float,
+                        b: float, c: float, steps: int, eps: float, ns_dtype: int, workspace: int,
+                        workspace_bytes: int, stream: int = 0) -> None:
+    _check(lib().mfsdp_newton_schulz(x, x_dtype, out, out_dtype, m, n, a, b, c, steps, eps,
+                                     ns_dtype, workspace, workspace_bytes, stream))
+
+
+def mfsdp_adamw_step(entries: Sequence[AdamWEntry], lr: float, beta1: float, beta2: float,
+                     eps: float, weight_decay: float, step: int, stream: int = 0) -> None:
+    arr, n = _entries(entries, AdamWEntry)
+    _check(lib().mfsdp_adamw_step(arr, n, lr, beta1, beta2, eps, weight_decay, step, stream))
+
+
+# ------------------------------------------------------------------- torch tensor helpers
+
+def _dt(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream() -> int:
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def muon_hparams(lr=0.02, weight_decay=0.0, momentum=0.95, nesterov=True, a=3.4445, b=-4.7750,
+                 c=2.0315, ns_steps=5, eps=1e-7, lr_adjust="original", ns_dtype="bf16") -> MuonHParams:
+    return MuonHParams(lr, weight_decay, momentum, int(bool(nesterov)), a, b, c, ns_steps, eps,
+                       _LR_MODES[lr_adjust] if isinstance(lr_adjust, str) else int(lr_adjust),
+                       _NS_DT[ns_dtype] if isinstance(ns_dtype, str) else int(ns_dtype))
+
+
+def muon_entry_t(param, grad, momentum, update_out=None) -> MuonEntry:
+    m, n = param.shape
+    return MuonEntry(param.data_ptr(), grad.data_ptr(), momentum.data_ptr(), m, n, _dt(param),
+                     _dt(grad), update_out.data_ptr() if update_out is not None else None)
+
+
+def muon_workspace_t(entries: Sequence[MuonEntry], hp: MuonHParams, device="cuda"):
+    import torch
+    size = mfsdp_muon_workspace_size(entries, hp)
+    return torch.empty(max(size, 256), dtype=torch.uint8, device=device)
+
+
+def muon_step_t(entries: Sequence[MuonEntry], hp: MuonHParams, workspace) -> None:
+    mfsdp_muon_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def newton_schulz_t(x, out, a=3.4445, b=-4.7750, c=2.0315, steps=5, eps=1e-7, ns_dtype="bf16",
+                    workspace=None) -> None:
+    import torch
+    m, n = x.shape
+    nsd = BF16 if ns_dtype in ("bf16", BF16) else F32
+    if workspace is None:
+        workspace = torch.empty(mfsdp_ns_workspace_size(m, n, nsd), dtype=torch.uint8, device=x.device)
+    mfsdp_newton_schulz(x.data_ptr(), _dt(x), out.data_ptr(), _dt(out), m, n, a, b, c, steps, eps,
+                        nsd, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def adamw_entry_t(param, grad, exp_avg, exp_avg_sq) -> AdamWEntry:
+    return AdamWEntry(param.data_ptr(), grad.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(),
+                      param.numel(), _dt(param), _dt(grad))
+
+
+def adamw_step_t(entries: Sequence[AdamWEntry], lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                 weight_decay=1e-2, step=1) -> None:
+    mfsdp_adamw_step(entries, lr, beta1, beta2, eps, weight_decay, step, _stream())

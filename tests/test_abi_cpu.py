@@ -1,0 +1,138 @@
+"""Host-side tests of the C ABI that need no GPU: the library loads, exports every symbol the header
+declares, and rejects invalid arguments before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_05895_amd import native
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_symbols():
+    text = open(os.path.join(ROOT, "include", "mfsdp.h")).read()
+    return sorted(set(re.findall(r"\b(mfsdp_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = native.lib()
+    decl = _declared_symbols()
+    assert set(decl) == set(native.EXPORTS)
+    for name in decl:
+        assert hasattr(L, name), name
+
+
+def test_abi_version_and_status_strings():
+    assert native.mfsdp_abi_version() == 1
+    assert native.mfsdp_status_string(0) == "MFSDP_OK"
+    assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
+    assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
+    assert native.mfsdp_status_string(-3) == "MFSDP_E_HIP"
+
+
+FAKE = 1 << 20  # a 16-byte aligned non-NULL address; never dereferenced (validation fails first)
+
+
+def _entry(**kw):
+    d = dict(param=FAKE, grad=FAKE * 2, momentum=FAKE * 3, m=64, n=128, param_dtype=1,
+             grad_dtype=1, update_out=None)
+    d.update(kw)
+    return native.MuonEntry(**d)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(m=0), dict(n=-1), dict(param=None), dict(grad=None), dict(momentum=None),
+    dict(param_dtype=7), dict(grad_dtype=-1), dict(param=FAKE + 8), dict(update_out=FAKE + 4),
+])
+def test_muon_rejects_bad_entries(bad):
+    hp = native.muon_hparams()
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry(), _entry(**bad)], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+@pytest.mark.parametrize("bad", [
+    dict(ns_steps=100), dict(ns_steps=-1), dict(lr=-1.0), dict(weight_decay=-0.1),
+    dict(momentum=1.0), dict(momentum=-0.5), dict(eps=0.0), dict(lr_adjust=3), dict(ns_dtype=5),
+    dict(a=float("inf")),
+])
+def test_muon_rejects_bad_hparams(bad):
+    hp = native.muon_hparams(**bad)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry()], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+def test_muon_workspace_checks():
+    hp = native.muon_hparams()
+    need = native.mfsdp_muon_workspace_size([_entry()], hp)
+    assert need > 0
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry()], hp, FAKE * 16, need - 1, 0)
+    assert ei.value.status == native.E_WORKSPACE
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry()], hp, FAKE * 16 + 16, need, 0)  # not 256-aligned
+    assert ei.value.status == native.E_WORKSPACE
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry()], hp, None, need, 0)
+    assert ei.value.status == native.E_WORKSPACE
+
+
+def test_workspace_size_scales_with_padding():
+    hp = native.muon_hparams()
+    small = native.mfsdp_muon_workspace_size([_entry(m=100, n=300)], hp)
+    exact = native.mfsdp_muon_workspace_size([_entry(m=256, n=512)], hp)
+    assert small == exact  # both pad to 256 x 512 tiles
+    f32 = native.muon_hparams(ns_dtype="f32")
+    assert native.mfsdp_muon_workspace_size([_entry(m=100, n=300)], f32) < 2 * small
+    # the sum over entries: two entries need more than one
+    assert native.mfsdp_muon_workspace_size([_entry(), _entry()], hp) > \
+        native.mfsdp_muon_workspace_size([_entry()], hp)
+
+
+def test_zero_count_is_noop():
+    hp = native.muon_hparams()
+    native.mfsdp_muon_step([], hp, None, 0, 0)
+    assert native.lib().mfsdp_muon_workspace_size(None, 0, ctypes.byref(hp)) == 0
+    native.mfsdp_adamw_step([], 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 0)
+
+
+def test_newton_schulz_argument_checks():
+    ws = native.mfsdp_ns_workspace_size(64, 64, native.BF16)
+    for kw in [dict(steps=100), dict(m=0), dict(x_dtype=3), dict(eps=-1.0), dict(out=FAKE)]:
+        args = dict(x=FAKE, x_dtype=1, out=FAKE * 2, out_dtype=1, m=64, n=64, a=3.4445, b=-4.775,
+                    c=2.0315, steps=5, eps=1e-7, ns_dtype=1, workspace=FAKE * 16,
+                    workspace_bytes=ws, stream=0)
+        args.update(kw)
+        with pytest.raises(native.MfsdpError) as ei:
+            native.mfsdp_newton_schulz(**args)
+        assert ei.value.status == native.E_INVALID
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_newton_schulz(FAKE, 1, FAKE * 2, 1, 64, 64, 3.4, -4.7, 2.0, 5, 1e-7, 1,
+                                   FAKE * 16, ws - 256, 0)
+    assert ei.value.status == native.E_WORKSPACE
+
+
+@pytest.mark.parametrize("kw", [dict(step=0), dict(lr=-1.0), dict(beta1=1.0), dict(beta2=-0.1),
+                                dict(eps=0.0), dict(weight_decay=-1.0)])
+def test_adamw_rejects_bad_hparams(kw):
+    args = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.0, step=1)
+    args.update(kw)
+    e = native.AdamWEntry(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 100, 1, 1)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_adamw_step([e], **args)
+    assert ei.value.status == native.E_INVALID
+
+
+@pytest.mark.parametrize("bad", [dict(numel=0), dict(param=None), dict(exp_avg=FAKE + 4),
+                                 dict(grad_dtype=2)])
+def test_adamw_rejects_bad_entries(bad):
+    d = dict(param=FAKE, grad=FAKE * 2, exp_avg=FAKE * 3, exp_avg_sq=FAKE * 4, numel=100,
+             param_dtype=1, grad_dtype=1)
+    d.update(bad)
+    good = native.AdamWEntry(FAKE, FAKE * 2, FAKE * 3, FAKE * 4, 100, 1, 1)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_adamw_step([good, native.AdamWEntry(**d)], 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 0)
+    assert ei.value.status == native.E_INVALID
