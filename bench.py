@@ -130,6 +130,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="owner share 1..5 (default 3: Llama-3-8B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="before timing, run one plain 1 GiB -> 1 GiB elementwise copy kernel (the "
+                         "reference dispatch for scaling HBM counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -175,6 +178,14 @@ def main() -> int:
     ws = native.muon_workspace_t(ents, h, device=dev)
     torch.cuda.synchronize()
     log(f"inputs resident ({time.time() - t0:.1f} s); workspace {ws.numel() / 2**30:.2f} GiB")
+
+    if args.copy_calibration:
+        x = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        y = torch.empty_like(x)
+        torch.mul(x, 2.0, out=y)
+        torch.cuda.synchronize()
+        log("copy calibration: one elementwise kernel reading 1 GiB and writing 1 GiB")
+        del x, y
 
     ah = wl.adamw_hp
     stream = torch.cuda.current_stream().cuda_stream

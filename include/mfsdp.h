@@ -82,19 +82,20 @@ typedef struct {
   float* update_out;
 } mfsdp_muon_entry;
 
-/* Muon hyperparameters, shared by every entry of one call.
+/* Muon hyperparameters, shared by every entry of one call. Given in double precision; derived
+ * constants (1 - momentum, 1 - lr wd, lr f) are formed in double and rounded once to fp32.
  *   lr >= 0, weight_decay >= 0, 0 <= momentum < 1, nesterov 0/1,
  *   (a, b, c) NS coefficients, 0 <= ns_steps < 100, eps > 0 (norm clamp),
  *   lr_adjust an mfsdp_lr_adjust, ns_dtype: BF16 = NS products on bf16 MFMA with fp32
  *   accumulation and bf16 storage between products; F32 = fp32 throughout. */
 typedef struct {
-  float lr;
-  float weight_decay;
-  float momentum;
+  double lr;
+  double weight_decay;
+  double momentum;
   int32_t nesterov;
-  float a, b, c;
+  double a, b, c;
   int32_t ns_steps;
-  float eps;
+  double eps;
   int32_t lr_adjust;
   int32_t ns_dtype;
 } mfsdp_muon_hparams;
@@ -143,16 +144,18 @@ size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype);
  *   out  m x n, out_dtype (F32 or BF16); must not alias x
  *   ns_dtype as in mfsdp_muon_hparams; workspace sized by mfsdp_ns_workspace_size. */
 int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
-                        int64_t n, float a, float b, float c, int32_t steps, float eps,
+                        int64_t n, double a, double b, double c, int32_t steps, double eps,
                         int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream);
 
 /* AdamW on the tail tensors (Section 4.4; PyTorch AdamW per Section 5.1):
  *   p <- p (1 - lr wd);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2
  *   p <- p - lr / (1 - beta1^t) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps)
  * step = t >= 1 is the step number after increment. lr, wd >= 0; betas in [0, 1); eps > 0.
+ * Hyperparameters are doubles; 1 - beta, the bias corrections and lr / (1 - beta1^t) are formed in
+ * double and rounded once to fp32 (the elementwise math is fp32).
  * Needs no workspace. count == 0 is a no-op. */
-int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, float lr, float beta1,
-                     float beta2, float eps, float weight_decay, int64_t step, void* stream);
+int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,
+                     double beta2, double eps, double weight_decay, int64_t step, void* stream);
 
 /* Text for the last failure on the calling thread ("" if none). */
 const char* mfsdp_last_error(void);

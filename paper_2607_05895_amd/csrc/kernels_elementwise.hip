@@ -79,7 +79,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 // Thread t owns columns 4*(t%16) .. +3 of rows t/16 + 16 q, q = 0..3.
 template <int NSDT>
 __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ descs, int count,
-                                                   float beta, int nesterov) {
+                                                   float beta, float omb, int nesterov) {
   __shared__ float tile[64][65];
   __shared__ float red[4];
   const int e = find_entry(descs, count, blockIdx.x);
@@ -88,7 +88,6 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
   const int64_t row0 = int64_t(lt / d.tiles_n) * 64, col0 = int64_t(lt % d.tiles_n) * 64;
   const int t = threadIdx.x;
   const int c4 = (t & 15) * 4, rr = t >> 4;
-  const float omb = 1.0f - beta;
   float ss = 0.0f;
   const bool vec = (d.n % 4 == 0);
 #pragma unroll
@@ -228,8 +227,8 @@ __global__ __launch_bounds__(256) void apply_kernel(const ApplyDesc* __restrict_
 // kAdamWBlockElems consecutive elements of one tensor, 16 per thread (4 groups of 4).
 __device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v, const AdamWBatch& b) {
   p = p * b.decay;
-  m = m + (1.0f - b.beta1) * (g - m);
-  v = b.beta2 * v + (1.0f - b.beta2) * g * g;
+  m = m + b.omb1 * (g - m);
+  v = b.beta2 * v + b.omb2 * g * g;
   const float denom = sqrtf(v) * b.inv_sqrt_bc2 + b.eps;
   p = p - b.step_size * (m / denom);
 }
@@ -273,12 +272,14 @@ __global__ __launch_bounds__(256) void adamw_kernel(const AdamWBatch batch) {
 }  // namespace
 
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       float beta, int nesterov, hipStream_t st) {
+                       float beta, float one_minus_beta, int nesterov, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16)
-    hipLaunchKernelGGL(prep_kernel<kDtBF16>, dim3(total_tiles), dim3(256), 0, st, d_descs, count, beta, nesterov);
+    hipLaunchKernelGGL(prep_kernel<kDtBF16>, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
+                       beta, one_minus_beta, nesterov);
   else
-    hipLaunchKernelGGL(prep_kernel<kDtF32>, dim3(total_tiles), dim3(256), 0, st, d_descs, count, beta, nesterov);
+    hipLaunchKernelGGL(prep_kernel<kDtF32>, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
+                       beta, one_minus_beta, nesterov);
   return hipGetLastError();
 }
 

@@ -72,15 +72,38 @@ __device__ __forceinline__ float scale_pow(const float* s, int pw) {
 
 // ---------------------------------------------------------------------------------------------
 // bf16 MFMA kernel
-constexpr int BT = 256;             // output tile (both sides)
-constexpr int BKE = 64;             // K elements per stage
-constexpr int ROWB = BKE * 2;       // bytes per staged row (128)
-constexpr int STAGE_BYTES = 2 * BT * ROWB;  // P rows then Q rows: 64 KiB
+//
+// Main loop: K in steps of 32 elements. A stage holds the P rows (256 x 32 bf16 = 16 KiB) followed
+// by the Q rows (16 KiB) of one K step. Stages are filled by direct global->LDS loads
+// (global_load_lds_dwordx4: each wave instruction writes 64 x 16 B = 1 KiB of LDS contiguously),
+// so no registers or ds_write instructions carry the tiles. One workgroup barrier per K step kt,
+// placed between its two 16-wide K slices: before it every wave waits (explicit vmcnt) for its own
+// loads of step kt + 1; after it the loads of step kt + NSTAGE - 1 are issued into the stage of step
+// kt - 1 (whose last fragments were consumed by MFMAs issued before the barrier), and the first
+// fragments of step kt + 1 are read while the second slice of step kt is multiplied. Steps
+// kt + 2 .. kt + NSTAGE - 1 are in flight meanwhile.
+//
+// LDS row layout: 64 B per row = four 16-B chunks; chunk c of row r is stored in slot c ^ g(r)
+// with g(r) = (r1 ^ r3) | r2 << 1 (bits of r). Groups of 8 (or 16) consecutive rows read by one
+// ds_read_b128 cycle then hit distinct banks for 32 (or 64) banks of 4 B.
+constexpr int BT = 256;                      // output tile (both sides)
+constexpr int BKE = 32;                      // K elements per stage
+constexpr int ROWB = BKE * 2;                // bytes per staged row (64)
+constexpr int STAGE_BYTES = 2 * BT * ROWB;   // 32 KiB
+constexpr int NSTAGE = 5;                    // 160 KiB of LDS
+constexpr int LOADS_PER_STAGE = STAGE_BYTES / (256 * 16);  // DMA instructions per thread per stage (8)
+
+typedef __attribute__((address_space(3))) uint8_t lds_byte;
+
+__device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((r >> 2) & 1) << 1); }
+
+// s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt left at their maxima).
+#define MFSDP_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (7 << 4) | (0xF << 8))
 
 __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
                                                            int count, int parity, int first,
                                                            int last) {
-  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * STAGE_BYTES];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[NSTAGE * STAGE_BYTES];
 
   const int e = find_entry(descs, count, blockIdx.x);
   const GemmDesc& dd = descs[e];
@@ -90,21 +113,32 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
   const uint16_t* __restrict__ P = static_cast<const uint16_t*>(dd.P[parity]);
   const uint16_t* __restrict__ Q = static_cast<const uint16_t*>(dd.Q[parity]);
   const int64_t ldp = dd.ldp, ldq = dd.ldq;
-  const int K = dd.K;
+  const int nk = dd.K / BKE;
 
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int wm = w >> 1, wn = w & 1;
 
-  // Loader: thread t covers staged rows c * 32 + t / 8 (c = 0..15; rows 0..255 are P, 256..511
-  // are Q) and 16-byte slot t % 8 of each row; the slot holds global chunk slot ^ (row % 8).
-  const int lrow = t >> 3, lslot = t & 7;
-  const int lchunk = lslot ^ (lrow & 7);
-  // rows c*32 + lrow: c < 8 from P, c >= 8 from Q; consecutive c are 32 rows apart
-  const uint16_t* psrc = P + (int64_t(bi) * BT + lrow) * ldp + lchunk * 8;
-  const uint16_t* qsrc = Q + (int64_t(bj) * BT + lrow) * ldq + lchunk * 8;
-  const int64_t pstep = 32 * ldp, qstep = 32 * ldq;
-  const int lds_w_off = lrow * ROWB + lslot * 16;  // + c * 32 * ROWB
+  // DMA mapping: instruction c (0..7) of wave w covers staged rows (4c + w) * 16 + lane / 4;
+  // c < 4 are P rows c*64 + w*16 + lane/4, c >= 4 the same rows of Q. Lane slot = lane % 4 holds
+  // global chunk slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
+  const int drow = w * 16 + (lane >> 2);
+  const int dchunk = (lane & 3) ^ swz(lane >> 2);
+  const uint16_t* psrc = P + (int64_t(bi) * BT + drow) * ldp + dchunk * 8;
+  const uint16_t* qsrc = Q + (int64_t(bj) * BT + drow) * ldq + dchunk * 8;
+  const int64_t pstep = 64 * ldp, qstep = 64 * ldq;
+  const int dma_wave_off = w * 1024;  // + c * 4096 within a stage
+
+  auto issue = [&](int kt, int stage) {
+    const int64_t koff = int64_t(kt) * BKE;
+    lds_byte* sb = (lds_byte*)(smem + stage * STAGE_BYTES + dma_wave_off);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      __builtin_amdgcn_global_load_lds(psrc + c * pstep + koff, sb + c * 4096, 16, 0, 0);
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      __builtin_amdgcn_global_load_lds(qsrc + c * qstep + koff, sb + (4 + c) * 4096, 16, 0, 0);
+  };
 
   f32x16_t acc[4][4];
 #pragma unroll
@@ -114,93 +148,75 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
 
-  const int nk = K / BKE;
-  // fragment read offsets: row (base + l%32), chunk q = 2*kk + l/32, slot q ^ (l % 8)
+  // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
   const int frow = lane & 31, fhalf = lane >> 5;
   const int pbase = (wm * 128 + frow) * ROWB;
   const int qbase = (BT + wn * 128 + frow) * ROWB;
+  const int slot0 = ((0 + fhalf) ^ swz(frow)) * 16;
+  const int slot1 = ((2 + fhalf) ^ swz(frow)) * 16;
 
-  uint4 s0, s1, s2, s3, s4, s5, s6, s7, s8, s9, s10, s11, s12, s13, s14, s15;
-#define MFSDP_GLOAD(koff)                                                                \
-  do {                                                                                   \
-    const uint16_t* pp = psrc + (koff);                                                  \
-    const uint16_t* qq = qsrc + (koff);                                                  \
-    s0 = *reinterpret_cast<const uint4*>(pp);                                            \
-    s1 = *reinterpret_cast<const uint4*>(pp + pstep);                                    \
-    s2 = *reinterpret_cast<const uint4*>(pp + 2 * pstep);                                \
-    s3 = *reinterpret_cast<const uint4*>(pp + 3 * pstep);                                \
-    s4 = *reinterpret_cast<const uint4*>(pp + 4 * pstep);                                \
-    s5 = *reinterpret_cast<const uint4*>(pp + 5 * pstep);                                \
-    s6 = *reinterpret_cast<const uint4*>(pp + 6 * pstep);                                \
-    s7 = *reinterpret_cast<const uint4*>(pp + 7 * pstep);                                \
-    s8 = *reinterpret_cast<const uint4*>(qq);                                            \
-    s9 = *reinterpret_cast<const uint4*>(qq + qstep);                                    \
-    s10 = *reinterpret_cast<const uint4*>(qq + 2 * qstep);                               \
-    s11 = *reinterpret_cast<const uint4*>(qq + 3 * qstep);                               \
-    s12 = *reinterpret_cast<const uint4*>(qq + 4 * qstep);                               \
-    s13 = *reinterpret_cast<const uint4*>(qq + 5 * qstep);                               \
-    s14 = *reinterpret_cast<const uint4*>(qq + 6 * qstep);                               \
-    s15 = *reinterpret_cast<const uint4*>(qq + 7 * qstep);                               \
-  } while (0)
-#define MFSDP_LSTORE(buf)                                                                \
-  do {                                                                                   \
-    uint8_t* b_ = (buf) + lds_w_off;                                                     \
-    *reinterpret_cast<uint4*>(b_ + 0 * 32 * ROWB) = s0;                                  \
-    *reinterpret_cast<uint4*>(b_ + 1 * 32 * ROWB) = s1;                                  \
-    *reinterpret_cast<uint4*>(b_ + 2 * 32 * ROWB) = s2;                                  \
-    *reinterpret_cast<uint4*>(b_ + 3 * 32 * ROWB) = s3;                                  \
-    *reinterpret_cast<uint4*>(b_ + 4 * 32 * ROWB) = s4;                                  \
-    *reinterpret_cast<uint4*>(b_ + 5 * 32 * ROWB) = s5;                                  \
-    *reinterpret_cast<uint4*>(b_ + 6 * 32 * ROWB) = s6;                                  \
-    *reinterpret_cast<uint4*>(b_ + 7 * 32 * ROWB) = s7;                                  \
-    *reinterpret_cast<uint4*>(b_ + 8 * 32 * ROWB) = s8;                                  \
-    *reinterpret_cast<uint4*>(b_ + 9 * 32 * ROWB) = s9;                                  \
-    *reinterpret_cast<uint4*>(b_ + 10 * 32 * ROWB) = s10;                                \
-    *reinterpret_cast<uint4*>(b_ + 11 * 32 * ROWB) = s11;                                \
-    *reinterpret_cast<uint4*>(b_ + 12 * 32 * ROWB) = s12;                                \
-    *reinterpret_cast<uint4*>(b_ + 13 * 32 * ROWB) = s13;                                \
-    *reinterpret_cast<uint4*>(b_ + 14 * 32 * ROWB) = s14;                                \
-    *reinterpret_cast<uint4*>(b_ + 15 * 32 * ROWB) = s15;                                \
-  } while (0)
-
-  // Fragments of K-slice kk + 1 are read while the 16 MFMAs of slice kk run.
-  auto compute = [&](const uint8_t* sb) {
-    bf16x8_t pf[2][4], qf[2][4];
-    auto read_frags = [&](int kk, int b) {
-      const int slot = ((2 * kk + fhalf) ^ (lane & 7)) * 16;
+  bf16x8_t pf0[4], qf0[4], pf1[4], qf1[4];
+  auto read_frags = [&](const uint8_t* sb, int slot, bf16x8_t* pf, bf16x8_t* qf) {
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-        pf[b][mi] = *reinterpret_cast<const bf16x8_t*>(sb + pbase + mi * 32 * ROWB + slot);
+    for (int mi = 0; mi < 4; ++mi)
+      pf[mi] = *reinterpret_cast<const bf16x8_t*>(sb + pbase + mi * 32 * ROWB + slot);
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni)
+      qf[ni] = *reinterpret_cast<const bf16x8_t*>(sb + qbase + ni * 32 * ROWB + slot);
+  };
+  auto mfma16 = [&](const bf16x8_t* pf, const bf16x8_t* qf) {
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
       for (int ni = 0; ni < 4; ++ni)
-        qf[b][ni] = *reinterpret_cast<const bf16x8_t*>(sb + qbase + ni * 32 * ROWB + slot);
-    };
-    read_frags(0, 0);
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      if (kk < 3) read_frags(kk + 1, (kk + 1) & 1);
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[kk & 1][ni], pf[kk & 1][mi],
-                                                                acc[mi][ni], 0, 0, 0);
-    }
+        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ni], pf[mi], acc[mi][ni], 0, 0, 0);
   };
 
-  MFSDP_GLOAD(0);
-  MFSDP_LSTORE(smem);
-  __syncthreads();
-  for (int kt = 0; kt + 1 < nk; ++kt) {
-    const int cur = kt & 1;
-    MFSDP_GLOAD(int64_t(kt + 1) * BKE);
-    compute(smem + cur * STAGE_BYTES);
-    MFSDP_LSTORE(smem + (cur ^ 1) * STAGE_BYTES);
-    __syncthreads();
+  // prologue: steps 0 .. NSTAGE-2 in flight, then step 0 visible. Steps past the end are clamped to
+  // the last one (in-bounds reloads into stages nobody reads).
+  const int last_kt = nk - 1;
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s) issue(s < nk ? s : last_kt, s);
+  MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS_PER_STAGE);
+  __builtin_amdgcn_s_barrier();
+  read_frags(smem, slot0, pf0, qf0);
+
+  int cur = 0;                  // stage of step kt
+  int nxt = 1;                  // stage of step kt + 1
+  int fill = NSTAGE - 1;        // stage that receives step kt + NSTAGE - 1 (the stage of kt - 1)
+  for (int kt = 0; kt < nk; ++kt) {
+    const uint8_t* sb = smem + cur * STAGE_BYTES;
+    read_frags(sb, slot1, pf1, qf1);
+    mfma16(pf0, qf0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
+    MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS_PER_STAGE);
+    __builtin_amdgcn_s_barrier();
+    {
+      const int kload = kt + NSTAGE - 1;
+      issue(kload < nk ? kload : last_kt, fill);
+    }
+    read_frags(smem + nxt * STAGE_BYTES, slot0, pf0, qf0);
+    mfma16(pf1, qf1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    cur = nxt;
+    nxt = (nxt + 1 == NSTAGE) ? 0 : nxt + 1;
+    fill = (fill + 1 == NSTAGE) ? 0 : fill + 1;
   }
-  compute(smem + ((nk - 1) & 1) * STAGE_BYTES);
-#undef MFSDP_GLOAD
-#undef MFSDP_LSTORE
+  // drain the DMA of the clamped tail steps before the workgroup can exit
+  MFSDP_WAIT_VMCNT(0);
+#undef MFSDP_WAIT_VMCNT
 
   // Epilogue. acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
   // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t.

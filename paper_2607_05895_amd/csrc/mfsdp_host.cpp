@@ -160,16 +160,16 @@ StagingRing& ring() {
 
 int check_hp(const mfsdp_muon_hparams* hp) {
   if (!hp) return fail(MFSDP_E_INVALID, "hparams is NULL");
-  if (!(hp->lr >= 0.0f) || !std::isfinite(hp->lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
-  if (!(hp->weight_decay >= 0.0f) || !std::isfinite(hp->weight_decay))
+  if (!(hp->lr >= 0.0) || !std::isfinite(hp->lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
+  if (!(hp->weight_decay >= 0.0) || !std::isfinite(hp->weight_decay))
     return fail(MFSDP_E_INVALID, "weight_decay must be >= 0");
-  if (!(hp->momentum >= 0.0f && hp->momentum < 1.0f))
+  if (!(hp->momentum >= 0.0 && hp->momentum < 1.0))
     return fail(MFSDP_E_INVALID, "momentum must be in [0, 1)");
   if (hp->nesterov != 0 && hp->nesterov != 1) return fail(MFSDP_E_INVALID, "nesterov must be 0 or 1");
   if (!std::isfinite(hp->a) || !std::isfinite(hp->b) || !std::isfinite(hp->c))
     return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
   if (hp->ns_steps < 0 || hp->ns_steps >= 100) return fail(MFSDP_E_INVALID, "ns_steps must be in [0, 100)");
-  if (!(hp->eps > 0.0f) || !std::isfinite(hp->eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (!(hp->eps > 0.0) || !std::isfinite(hp->eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
   if (hp->lr_adjust < MFSDP_LR_NONE || hp->lr_adjust > MFSDP_LR_MATCH_RMS_ADAMW)
     return fail(MFSDP_E_INVALID, "unknown lr_adjust %d", hp->lr_adjust);
   if (!valid_dtype(hp->ns_dtype)) return fail(MFSDP_E_INVALID, "unknown ns_dtype %d", hp->ns_dtype);
@@ -204,10 +204,10 @@ int check_entries(const mfsdp_muon_entry* entries, int64_t count) {
   return MFSDP_OK;
 }
 
-float lr_factor(int64_t m, int64_t n, int mode) {
-  if (mode == MFSDP_LR_ORIGINAL) return float(std::sqrt(std::max(1.0, double(m) / double(n))));
-  if (mode == MFSDP_LR_MATCH_RMS_ADAMW) return float(0.2 * std::sqrt(double(std::max(m, n))));
-  return 1.0f;
+double lr_factor(int64_t m, int64_t n, int mode) {
+  if (mode == MFSDP_LR_ORIGINAL) return std::sqrt(std::max(1.0, double(m) / double(n)));
+  if (mode == MFSDP_LR_MATCH_RMS_ADAMW) return 0.2 * std::sqrt(double(std::max(m, n)));
+  return 1.0;
 }
 
 int hip_fail(hipError_t e, const char* what) {
@@ -275,7 +275,7 @@ void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_
       } else {
         d.ldp = p.r_pad; d.ldq = p.r_pad; d.lde = p.s_pad; d.ldc = p.s_pad; d.ldct = p.r_pad;
         d.M = int(p.r_pad); d.N = int(p.s_pad); d.K = int(p.r_pad);
-        d.alpha = 1.0f; d.beta = hp.a; d.alpha_scale_pow = 1; d.beta_scale_pow = 1;
+        d.alpha = 1.0f; d.beta = float(hp.a); d.alpha_scale_pow = 1; d.beta_scale_pow = 1;
         d.sym = 0; d.tiles_m = tr; d.tiles_n = ts;
         d.tile_count = tr * ts;
         // the final iterate is read in the parameter's orientation only
@@ -358,7 +358,7 @@ int record(void* const* events, int k, hipStream_t st) {
 }
 
 int enqueue_pipeline(const std::vector<NsPlan>& plans, uint8_t* ws, const DescLayout& dl,
-                     int slot, int steps, int ns_dtype, float beta, int nesterov, float eps,
+                     int slot, int steps, int ns_dtype, double beta, int nesterov, double eps,
                      int prep_tiles, int apply_tiles, int t0, int t1, int t2, hipStream_t st,
                      void* const* events) {
   const int count = int(plans.size());
@@ -367,9 +367,9 @@ int enqueue_pipeline(const std::vector<NsPlan>& plans, uint8_t* ws, const DescLa
   if ((rc = record(events, 0, st))) return rc;
   hipError_t e;
   e = launch_prep(reinterpret_cast<const PrepDesc*>(ws + dl.off_prep), count, prep_tiles, ns_dtype,
-                  beta, nesterov, st);
+                  float(beta), float(1.0 - beta), nesterov, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
-  e = launch_norm(reinterpret_cast<const NormDesc*>(ws + dl.off_norm), count, eps, st);
+  e = launch_norm(reinterpret_cast<const NormDesc*>(ws + dl.off_norm), count, float(eps), st);
   if (e != hipSuccess) return hip_fail(e, "norm launch");
   if ((rc = record(events, 1, st))) return rc;
   const int tiles[3] = {t0, t1, t2};
@@ -455,9 +455,9 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
     norm[i].partials = reinterpret_cast<const float*>(ws + p.off_partials);
     norm[i].count = p.prep_tiles_m * p.prep_tiles_n;
     norm[i].scale = reinterpret_cast<float*>(ws + p.off_scale);
-    const float f = lr_factor(en.m, en.n, hp->lr_adjust);
+    const double f = lr_factor(en.m, en.n, hp->lr_adjust);
     apply[i] = make_apply(p, ws, hp->ns_steps, en.param, en.param_dtype, en.update_out, 0,
-                          1.0f - hp->lr * hp->weight_decay, hp->lr * f, apply_tiles);
+                          float(1.0 - hp->lr * hp->weight_decay), float(hp->lr * f), apply_tiles);
     apply_tiles += apply[i].tiles_m * apply[i].tiles_n;
   }
   const int tile = hp->ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
@@ -478,7 +478,7 @@ size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype) {
 }
 
 int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
-                        int64_t n, float a, float b, float c, int32_t steps, float eps,
+                        int64_t n, double a, double b, double c, int32_t steps, double eps,
                         int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
   if (!x || !out) return fail(MFSDP_E_INVALID, "x and out must be non-NULL");
@@ -489,7 +489,7 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   if (rc) return rc;
   if (!aligned16(x) || !aligned16(out)) return fail(MFSDP_E_INVALID, "pointers must be 16-byte aligned");
   if (steps < 0 || steps >= 100) return fail(MFSDP_E_INVALID, "steps must be in [0, 100)");
-  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (!(eps > 0.0) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
   if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
     return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
   const DescLayout dl = plan_descs(1);
@@ -523,22 +523,22 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   fill_gemm_descs(plans, ws, hp, reinterpret_cast<GemmDesc*>(h + dl.off_gemm[0]),
                   reinterpret_cast<GemmDesc*>(h + dl.off_gemm[1]),
                   reinterpret_cast<GemmDesc*>(h + dl.off_gemm[2]), tile, &t0, &t1, &t2);
-  return enqueue_pipeline(plans, ws, dl, slot, steps, ns_dtype, 0.0f, 0, eps,
+  return enqueue_pipeline(plans, ws, dl, slot, steps, ns_dtype, 0.0, 0, eps,
                           p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n,
                           t0, t1, t2, st, nullptr);
 }
 
-int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, float lr, float beta1,
-                     float beta2, float eps, float weight_decay, int64_t step, void* stream) {
+int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,
+                     double beta2, double eps, double weight_decay, int64_t step, void* stream) {
   g_last_error.clear();
   if (count < 0) return fail(MFSDP_E_INVALID, "count must be >= 0");
   if (count > 0 && !entries) return fail(MFSDP_E_INVALID, "entries is NULL");
-  if (!(lr >= 0.0f) || !std::isfinite(lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
-  if (!(weight_decay >= 0.0f) || !std::isfinite(weight_decay))
+  if (!(lr >= 0.0) || !std::isfinite(lr)) return fail(MFSDP_E_INVALID, "lr must be >= 0");
+  if (!(weight_decay >= 0.0) || !std::isfinite(weight_decay))
     return fail(MFSDP_E_INVALID, "weight_decay must be >= 0");
-  if (!(beta1 >= 0.0f && beta1 < 1.0f) || !(beta2 >= 0.0f && beta2 < 1.0f))
+  if (!(beta1 >= 0.0 && beta1 < 1.0) || !(beta2 >= 0.0 && beta2 < 1.0))
     return fail(MFSDP_E_INVALID, "betas must be in [0, 1)");
-  if (!(eps > 0.0f) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
+  if (!(eps > 0.0) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
   if (step < 1) return fail(MFSDP_E_INVALID, "step must be >= 1");
   for (int64_t i = 0; i < count; ++i) {
     const mfsdp_adamw_entry& e = entries[i];
@@ -553,15 +553,17 @@ int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, float lr, 
   }
   if (count == 0) return MFSDP_OK;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const double bc1 = 1.0 - std::pow(double(beta1), double(step));
-  const double bc2 = 1.0 - std::pow(double(beta2), double(step));
+  const double bc1 = 1.0 - std::pow(beta1, double(step));
+  const double bc2 = 1.0 - std::pow(beta2, double(step));
   AdamWBatch batch{};
-  batch.decay = 1.0f - lr * weight_decay;
-  batch.beta1 = beta1;
-  batch.beta2 = beta2;
-  batch.step_size = float(double(lr) / bc1);
+  batch.decay = float(1.0 - lr * weight_decay);
+  batch.beta1 = float(beta1);
+  batch.beta2 = float(beta2);
+  batch.omb1 = float(1.0 - beta1);
+  batch.omb2 = float(1.0 - beta2);
+  batch.step_size = float(lr / bc1);
   batch.inv_sqrt_bc2 = float(1.0 / std::sqrt(bc2));
-  batch.eps = eps;
+  batch.eps = float(eps);
   int64_t i = 0;
   while (i < count) {
     batch.count = 0;

@@ -98,6 +98,7 @@ struct AdamWBatch {
   int32_t count;
   float decay;           // 1 - lr wd
   float beta1, beta2;
+  float omb1, omb2;      // 1 - beta1, 1 - beta2 (formed in double)
   float step_size;       // lr / (1 - beta1^t)
   float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
   float eps;
@@ -106,7 +107,7 @@ constexpr int kAdamWBlockElems = 4096;
 
 // Launchers (return hipError_t of the launch).
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       float beta, int nesterov, hipStream_t st);
+                       float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, int ns_dtype,
                        int parity, int first_step, int last_step, hipStream_t st);

@@ -31,10 +31,10 @@ class MuonEntry(ctypes.Structure):
 
 
 class MuonHParams(ctypes.Structure):
-    _fields_ = [("lr", ctypes.c_float), ("weight_decay", ctypes.c_float),
-                ("momentum", ctypes.c_float), ("nesterov", ctypes.c_int32),
-                ("a", ctypes.c_float), ("b", ctypes.c_float), ("c", ctypes.c_float),
-                ("ns_steps", ctypes.c_int32), ("eps", ctypes.c_float),
+    _fields_ = [("lr", ctypes.c_double), ("weight_decay", ctypes.c_double),
+                ("momentum", ctypes.c_double), ("nesterov", ctypes.c_int32),
+                ("a", ctypes.c_double), ("b", ctypes.c_double), ("c", ctypes.c_double),
+                ("ns_steps", ctypes.c_int32), ("eps", ctypes.c_double),
                 ("lr_adjust", ctypes.c_int32), ("ns_dtype", ctypes.c_int32)]
 
 
@@ -67,7 +67,7 @@ def lib() -> ctypes.CDLL:
         except ImportError:
             pass
         L = ctypes.CDLL(LIB_PATH)
-        vp, i64, i32, f32, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_float, ctypes.c_size_t
+        vp, i64, i32, f64, sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
         L.mfsdp_muon_workspace_size.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams)]
         L.mfsdp_muon_workspace_size.restype = sz
         L.mfsdp_muon_step.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams), vp, sz, vp]
@@ -77,9 +77,9 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_muon_step_timed.restype = ctypes.c_int
         L.mfsdp_ns_workspace_size.argtypes = [i64, i64, i32]
         L.mfsdp_ns_workspace_size.restype = sz
-        L.mfsdp_newton_schulz.argtypes = [vp, i32, vp, i32, i64, i64, f32, f32, f32, i32, f32, i32, vp, sz, vp]
+        L.mfsdp_newton_schulz.argtypes = [vp, i32, vp, i32, i64, i64, f64, f64, f64, i32, f64, i32, vp, sz, vp]
         L.mfsdp_newton_schulz.restype = ctypes.c_int
-        L.mfsdp_adamw_step.argtypes = [ctypes.POINTER(AdamWEntry), i64, f32, f32, f32, f32, f32, i64, vp]
+        L.mfsdp_adamw_step.argtypes = [ctypes.POINTER(AdamWEntry), i64, f64, f64, f64, f64, f64, i64, vp]
         L.mfsdp_adamw_step.restype = ctypes.c_int
         L.mfsdp_last_error.argtypes = []
         L.mfsdp_last_error.restype = ctypes.c_char_p
