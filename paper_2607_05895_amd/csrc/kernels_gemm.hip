@@ -32,11 +32,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return cvt(lo) | (cvt(hi) << 16);
 }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
+// DPP quad permutations: lane i of each group of 4 reads lane i ^ 1 (quad_perm [1,0,3,2]) or
+// lane i ^ 2 (quad_perm [2,3,0,1]).
+__device__ __forceinline__ float dpp_quad_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_quad_xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false));
 }
 
 template <typename D>
@@ -91,7 +93,6 @@ constexpr int BKE = 32;                      // K elements per stage
 constexpr int ROWB = BKE * 2;                // bytes per staged row (64)
 constexpr int STAGE_BYTES = 2 * BT * ROWB;   // 32 KiB
 constexpr int NSTAGE = 5;                    // 160 KiB of LDS
-constexpr int LOADS_PER_STAGE = STAGE_BYTES / (256 * 16);  // DMA instructions per thread per stage (8)
 
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
 
@@ -100,9 +101,27 @@ __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((
 // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt left at their maxima).
 #define MFSDP_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (7 << 4) | (0xF << 8))
 
-__global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
-                                                           int count, int parity, int first,
-                                                           int last) {
+#ifndef MFSDP_GEMM_WAVES
+#define MFSDP_GEMM_WAVES 8
+#endif
+// NW waves per workgroup arranged WM x WN over the 256 x 256 tile; each wave owns
+// (256 / WM) x (256 / WN) outputs as MI x NI blocks of 32 x 32. With 8 waves two share each SIMD,
+// so one can issue while the other waits.
+template <int NW>
+struct WaveGrid {
+  static constexpr int WM = 2;
+  static constexpr int WN = NW / 2;
+  static constexpr int MI = BT / (WM * 32);
+  static constexpr int NI = BT / (WN * 32);
+  static constexpr int LOADS = 32 / NW;  // DMA instructions per thread per stage
+};
+
+template <int NW>
+__global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
+                                                               int count, int parity, int first,
+                                                               int last) {
+  using WG = WaveGrid<NW>;
+  constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS;
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NSTAGE * STAGE_BYTES];
 
   const int e = find_entry(descs, count, blockIdx.x);
@@ -117,67 +136,70 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
 
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
-  const int wm = w >> 1, wn = w & 1;
+  const int wm = w / WG::WN, wn = w % WG::WN;
 
-  // DMA mapping: instruction c (0..7) of wave w covers staged rows (4c + w) * 16 + lane / 4;
-  // c < 4 are P rows c*64 + w*16 + lane/4, c >= 4 the same rows of Q. Lane slot = lane % 4 holds
-  // global chunk slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
+  // DMA mapping: instruction c of wave w covers staged rows j * 16 + lane / 4 with j = c * NW + w;
+  // j < 16 are P rows, j >= 16 the rows j - 16 of Q. Lane slot = lane % 4 holds global chunk
+  // slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
   const int drow = w * 16 + (lane >> 2);
   const int dchunk = (lane & 3) ^ swz(lane >> 2);
   const uint16_t* psrc = P + (int64_t(bi) * BT + drow) * ldp + dchunk * 8;
   const uint16_t* qsrc = Q + (int64_t(bj) * BT + drow) * ldq + dchunk * 8;
-  const int64_t pstep = 64 * ldp, qstep = 64 * ldq;
-  const int dma_wave_off = w * 1024;  // + c * 4096 within a stage
+  const int64_t pstep = int64_t(NW * 16) * ldp, qstep = int64_t(NW * 16) * ldq;
+  const int dma_wave_off = w * 1024;  // + c * NW * 1024 within a stage
+  constexpr int PL = LOADS / 2;        // instructions for P (and for Q) per thread
 
   auto issue = [&](int kt, int stage) {
     const int64_t koff = int64_t(kt) * BKE;
     lds_byte* sb = (lds_byte*)(smem + stage * STAGE_BYTES + dma_wave_off);
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
-      __builtin_amdgcn_global_load_lds(psrc + c * pstep + koff, sb + c * 4096, 16, 0, 0);
+    for (int c = 0; c < PL; ++c)
+      __builtin_amdgcn_global_load_lds(psrc + c * pstep + koff, sb + c * NW * 1024, 16, 0, 0);
 #pragma unroll
-    for (int c = 0; c < 4; ++c)
-      __builtin_amdgcn_global_load_lds(qsrc + c * qstep + koff, sb + (4 + c) * 4096, 16, 0, 0);
+    for (int c = 0; c < PL; ++c)
+      __builtin_amdgcn_global_load_lds(qsrc + c * qstep + koff, sb + 16384 + c * NW * 1024, 16, 0, 0);
   };
 
-  f32x16_t acc[4][4];
+  f32x16_t acc[MI][NI];
 #pragma unroll
-  for (int a = 0; a < 4; ++a)
+  for (int a = 0; a < MI; ++a)
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+    for (int b = 0; b < NI; ++b)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
 
   // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
   const int frow = lane & 31, fhalf = lane >> 5;
-  const int pbase = (wm * 128 + frow) * ROWB;
-  const int qbase = (BT + wn * 128 + frow) * ROWB;
+  const int pbase = (wm * (MI * 32) + frow) * ROWB;
+  const int qbase = (BT + wn * (NI * 32) + frow) * ROWB;
   const int slot0 = ((0 + fhalf) ^ swz(frow)) * 16;
   const int slot1 = ((2 + fhalf) ^ swz(frow)) * 16;
 
-  bf16x8_t pf0[4], qf0[4], pf1[4], qf1[4];
+  bf16x8_t pf0[MI], qf0[NI], pf1[MI], qf1[NI];
   auto read_frags = [&](const uint8_t* sb, int slot, bf16x8_t* pf, bf16x8_t* qf) {
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
       pf[mi] = *reinterpret_cast<const bf16x8_t*>(sb + pbase + mi * 32 * ROWB + slot);
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
+    for (int ni = 0; ni < NI; ++ni)
       qf[ni] = *reinterpret_cast<const bf16x8_t*>(sb + qbase + ni * 32 * ROWB + slot);
   };
-  auto mfma16 = [&](const bf16x8_t* pf, const bf16x8_t* qf) {
+  auto mfma_slice = [&](const bf16x8_t* pf, const bf16x8_t* qf) {
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
+      for (int ni = 0; ni < NI; ++ni)
         acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ni], pf[mi], acc[mi][ni], 0, 0, 0);
   };
+  constexpr int NMF = MI * NI;      // MFMAs per 16-wide K slice
+  constexpr int NRD = MI + NI;      // fragment reads per slice
 
   // prologue: steps 0 .. NSTAGE-2 in flight, then step 0 visible. Steps past the end are clamped to
   // the last one (in-bounds reloads into stages nobody reads).
   const int last_kt = nk - 1;
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s) issue(s < nk ? s : last_kt, s);
-  MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS_PER_STAGE);
+  MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS);
   __builtin_amdgcn_s_barrier();
   read_frags(smem, slot0, pf0, qf0);
 
@@ -187,41 +209,49 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
   for (int kt = 0; kt < nk; ++kt) {
     const uint8_t* sb = smem + cur * STAGE_BYTES;
     read_frags(sb, slot1, pf1, qf1);
-    mfma16(pf0, qf0);
+    mfma_slice(pf0, qf0);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < NRD; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
     // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
-    MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS_PER_STAGE);
+    MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS);
     __builtin_amdgcn_s_barrier();
     {
       const int kload = kt + NSTAGE - 1;
       issue(kload < nk ? kload : last_kt, fill);
     }
     read_frags(smem + nxt * STAGE_BYTES, slot0, pf0, qf0);
-    mfma16(pf1, qf1);
+    mfma_slice(pf1, qf1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+    for (int i = 0; i < LOADS; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
+    }
+#pragma unroll
+    for (int i = 0; i < NRD; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD - LOADS, 0);
     cur = nxt;
     nxt = (nxt + 1 == NSTAGE) ? 0 : nxt + 1;
     fill = (fill + 1 == NSTAGE) ? 0 : fill + 1;
   }
   // drain the DMA of the clamped tail steps before the workgroup can exit
   MFSDP_WAIT_VMCNT(0);
-#undef MFSDP_WAIT_VMCNT
 
   // Epilogue. acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
-  // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t.
+  // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t: each lane has 4 consecutive columns
+  // of one row per group g (one 8-byte row-major store). For the transposed stores (X'^T, and the
+  // mirrored tile of a symmetric product) the 4 x 4 blocks held by lane quads are transposed with
+  // two DPP exchanges, so each lane then holds 4 consecutive rows of one column (again one 8-byte
+  // store).
   const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
   const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
+  const float diag = (dd.sym && bi == bj) ? dd.diag : 0.0f;
   const uint16_t* E = static_cast<const uint16_t*>(dd.E[parity]);
   uint16_t* C = static_cast<uint16_t*>(dd.C[parity]);
   uint16_t* CT = static_cast<uint16_t*>(dd.CT[parity]);
@@ -229,16 +259,21 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
     if (!dd.last_c) C = nullptr;
     if (!dd.last_ct) CT = nullptr;
   }
-  const bool mirror = dd.sym && bi != bj && C;
-  const int64_t lde = dd.lde, ldc = dd.ldc, ldct = dd.ldct;
+  // transposed destination: the mirror tile of a symmetric product, or X'^T
+  uint16_t* TD = (dd.sym && bi != bj && C) ? C : CT;
+  const int64_t ldtd = (TD == C) ? dd.ldc : dd.ldct;
+  const int64_t lde = dd.lde, ldc = dd.ldc;
+  const int q = lane & 3;
+  const bool q_odd = q & 1, q_hi = q & 2;
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi) {
-    const int64_t i = int64_t(bi) * BT + wm * 128 + mi * 32 + frow;
+  for (int mi = 0; mi < MI; ++mi) {
+    const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
+    const int64_t iq = i - q;  // first row of this lane quad
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
+    for (int ni = 0; ni < NI; ++ni) {
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int64_t j = int64_t(bj) * BT + wn * 128 + ni * 32 + g * 8 + fhalf * 4;
+        const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + g * 8 + fhalf * 4;
         float v0 = alpha * acc[mi][ni][4 * g + 0];
         float v1 = alpha * acc[mi][ni][4 * g + 1];
         float v2 = alpha * acc[mi][ni][4 * g + 2];
@@ -250,26 +285,35 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_kernel(const GemmDesc* __res
           v2 += beta * __uint_as_float(ev.y << 16);
           v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
         }
-        const uint32_t w01 = pack_bf16x2(v0, v1), w23 = pack_bf16x2(v2, v3);
-        if (C) {
-          *reinterpret_cast<uint2*>(C + i * ldc + j) = make_uint2(w01, w23);
-          if (mirror) {
-            C[(j + 0) * ldc + i] = uint16_t(w01);
-            C[(j + 1) * ldc + i] = uint16_t(w01 >> 16);
-            C[(j + 2) * ldc + i] = uint16_t(w23);
-            C[(j + 3) * ldc + i] = uint16_t(w23 >> 16);
-          }
+        if (diag != 0.0f) {
+          if (i == j + 0) v0 += diag;
+          if (i == j + 1) v1 += diag;
+          if (i == j + 2) v2 += diag;
+          if (i == j + 3) v3 += diag;
         }
-        if (CT) {
-          CT[(j + 0) * ldct + i] = uint16_t(w01);
-          CT[(j + 1) * ldct + i] = uint16_t(w01 >> 16);
-          CT[(j + 2) * ldct + i] = uint16_t(w23);
-          CT[(j + 3) * ldct + i] = uint16_t(w23 >> 16);
+        if (C) *reinterpret_cast<uint2*>(C + i * ldc + j) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+        if (TD) {
+          // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
+          {
+            const float x0 = q_odd ? v0 : v1, x1 = q_odd ? v2 : v3;
+            const float y0 = dpp_quad_xor1(x0), y1 = dpp_quad_xor1(x1);
+            if (q_odd) { v0 = y0; v2 = y1; } else { v1 = y0; v3 = y1; }
+          }
+          // exchange across lane ^ 2: low lanes take the partner's elements 0, 1 as their 2, 3
+          {
+            const float x0 = q_hi ? v0 : v2, x1 = q_hi ? v1 : v3;
+            const float y0 = dpp_quad_xor2(x0), y1 = dpp_quad_xor2(x1);
+            if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
+          }
+          // lane q now holds column j + q at rows iq .. iq + 3
+          *reinterpret_cast<uint2*>(TD + (j + q) * ldtd + iq) =
+              make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
         }
       }
     }
   }
 }
+#undef MFSDP_WAIT_VMCNT
 
 // ---------------------------------------------------------------------------------------------
 // fp32 kernel: 64 x 64 tile, 256 threads of 4 x 4 outputs, K step 16 through LDS.
@@ -329,6 +373,10 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
       const float4 ev = *reinterpret_cast<const float4*>(E + i * dd.lde + j);
       v[0] += beta * ev.x; v[1] += beta * ev.y; v[2] += beta * ev.z; v[3] += beta * ev.w;
     }
+    if (dd.sym && bi == bj)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (i == j + c) v[c] += dd.diag;
     if (C) {
       *reinterpret_cast<float4*>(C + i * dd.ldc + j) = make_float4(v[0], v[1], v[2], v[3]);
       if (mirror)
@@ -347,8 +395,9 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, int 
                        int parity, int first_step, int last_step, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16)
-    hipLaunchKernelGGL(gemm_bf16_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
-                       parity, first_step, last_step);
+    hipLaunchKernelGGL(gemm_bf16_kernel<MFSDP_GEMM_WAVES>, dim3(total_tiles),
+                       dim3(MFSDP_GEMM_WAVES * 64), 0, st, d_descs, count, parity, first_step,
+                       last_step);
   else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
                        parity, first_step, last_step);

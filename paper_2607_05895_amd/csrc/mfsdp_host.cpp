@@ -249,11 +249,11 @@ void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_
         if (phase == 0) {         // A = X X^T
           d.P[par] = xin; d.Q[par] = xin; d.E[par] = nullptr;
           d.C[par] = ws + p.off_g; d.CT[par] = nullptr;
-        } else if (phase == 1) {  // B = c A A + b A
+        } else if (phase == 1) {  // B' = c A A + b A + a I
           d.P[par] = ws + p.off_g; d.Q[par] = ws + p.off_g; d.E[par] = ws + p.off_g;
           d.C[par] = ws + p.off_h; d.CT[par] = nullptr;
-        } else {                  // X' = B X + a X, stored as X' and X'^T
-          d.P[par] = ws + p.off_h; d.Q[par] = xtin; d.E[par] = xin;
+        } else {                  // X' = B' X (= a X + B X), stored as X' and X'^T
+          d.P[par] = ws + p.off_h; d.Q[par] = xtin; d.E[par] = nullptr;
           d.C[par] = xout; d.CT[par] = xtout;
         }
       }
@@ -261,21 +261,22 @@ void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_
       if (phase == 0) {
         d.ldp = d.ldq = p.s_pad; d.lde = 0; d.ldc = p.r_pad; d.ldct = 0;
         d.M = d.N = int(p.r_pad); d.K = int(p.s_pad);
-        d.alpha = 1.0f; d.beta = 0.0f; d.alpha_scale_pow = 2; d.beta_scale_pow = 0;
+        d.alpha = 1.0f; d.beta = 0.0f; d.diag = 0.0f; d.alpha_scale_pow = 2; d.beta_scale_pow = 0;
         d.sym = 1; d.tiles_m = d.tiles_n = tr;
         d.tile_count = tr * (tr + 1) / 2;
         d.last_c = 1; d.last_ct = 0;
       } else if (phase == 1) {
         d.ldp = d.ldq = d.lde = d.ldc = p.r_pad; d.ldct = 0;
         d.M = d.N = d.K = int(p.r_pad);
-        d.alpha = hp.c; d.beta = hp.b; d.alpha_scale_pow = 0; d.beta_scale_pow = 0;
+        d.alpha = float(hp.c); d.beta = float(hp.b); d.diag = float(hp.a);
+        d.alpha_scale_pow = 0; d.beta_scale_pow = 0;
         d.sym = 1; d.tiles_m = d.tiles_n = tr;
         d.tile_count = tr * (tr + 1) / 2;
         d.last_c = 1; d.last_ct = 0;
       } else {
-        d.ldp = p.r_pad; d.ldq = p.r_pad; d.lde = p.s_pad; d.ldc = p.s_pad; d.ldct = p.r_pad;
+        d.ldp = p.r_pad; d.ldq = p.r_pad; d.lde = 0; d.ldc = p.s_pad; d.ldct = p.r_pad;
         d.M = int(p.r_pad); d.N = int(p.s_pad); d.K = int(p.r_pad);
-        d.alpha = 1.0f; d.beta = float(hp.a); d.alpha_scale_pow = 1; d.beta_scale_pow = 1;
+        d.alpha = 1.0f; d.beta = 0.0f; d.diag = 0.0f; d.alpha_scale_pow = 1; d.beta_scale_pow = 0;
         d.sym = 0; d.tiles_m = tr; d.tiles_n = ts;
         d.tile_count = tr * ts;
         // the final iterate is read in the parameter's orientation only

@@ -12,7 +12,9 @@
 //     Gram      A = X X^T             P = Q = X,  K = s_pad
 //     square    A A = A A^T           P = Q = A,  K = r_pad   (A symmetric)
 //     update    B X = B (X^T)^T       P = B, Q = X^T, K = r_pad
-//   The update writes X' in both layouts so the next step again reads K-contiguous operands.
+//   The square product stores B' = c A A + b A + a I, so the update X' = a X + B X = B' X is a plain
+//   product with no addend. It writes X' in both layouts so the next step again reads
+//   K-contiguous operands.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -58,6 +60,7 @@ struct GemmDesc {
   int64_t ldp, ldq, lde, ldc, ldct;
   int32_t M, N, K;       // padded sizes, multiples of the tile
   float alpha, beta;
+  float diag;            // added to the diagonal elements (i == j) after the axpby
   int32_t alpha_scale_pow;  // on the first step alpha *= scale^pow
   int32_t beta_scale_pow;
   int32_t sym;           // 1: only tiles bi <= bj, stored to (bi,bj) and mirrored to (bj,bi)
