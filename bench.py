@@ -108,17 +108,18 @@ def cpu_baseline(wl, sample_idx, pool) -> dict:
                       f"{elapsed * wl.ns_flops_nominal() / flops:.0f} s"}
 
 
-def traffic_entry(launches: int):
-    """HBM traffic of the NS GEMM kernel from committed rocprofv3 counter runs, if they were taken
-    on the current kernel source; else None."""
+def traffic_record(workload_name: str):
+    """HBM traffic of the NS GEMM kernel per launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE runs (scaled by the plain-copy calibration), if they were taken on the current
+    kernel source and on this workload; else None."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     try:
         rec = json.load(open(TRAFFIC_FILE))
         sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
-        if rec.get("kernel_source_sha256") != sha:
+        if rec.get("kernel_source_sha256") != sha or rec.get("workload") != workload_name:
             return None
-        return rec.get("bytes_per_launch")
+        return rec
     except Exception:
         return None
 
@@ -236,7 +237,8 @@ def main() -> int:
     alg_bytes = elts * (es_g + 8 + 2 * es_p)              # g, m in/out, p in/out
     adamw_bytes = sum(e.numel * ({"bf16": 2, "f32": 4}[e.param_dtype] * 2 +
                                  {"bf16": 2, "f32": 4}[e.grad_dtype] + 16) for e in wl.adamw)
-    traffic = traffic_entry(launches)
+    trec = traffic_record(wl.name)
+    traffic = trec["bytes_per_launch"] if trec else None
     out = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -265,6 +267,8 @@ def main() -> int:
             "unit": "TFLOP/s",
             "frac": round(ns_tflops / PEAK_BF16_TFLOPS, 4),
             "traffic": traffic,
+            "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
+            "algorithmic_bytes_per_launch": trec["algorithmic_bytes_per_launch"] if trec else None,
             "launches_per_step": launches,
             "avg_launch_ms": round(ns_ms / launches, 4) if launches else 0.0,
             "nominal_flop_per_launch": flops / launches if launches else 0.0,
@@ -281,7 +285,8 @@ def main() -> int:
         },
     }
     if not args.no_cpu_baseline:
-        sample = {3: [0, 1], 2: [0, 4], 1: [0], 4: [0], 5: [1]}.get(args.workload, [0])
+        # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
+        sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])
         log("timing the fp64 oracle on a bounded sample (cpu_baseline)")
         out["cpu_baseline"] = cpu_baseline(wl, sample, pool)
     print(json.dumps(out), flush=True)

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "mfsdp_internal.h"
 
 namespace mfsdp {
@@ -75,78 +77,178 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// prep: one 64 x 64 tile of the stored (padded) matrix per workgroup of 256 threads.
-// Thread t owns columns 4*(t%16) .. +3 of rows t/16 + 16 q, q = 0..3.
+// 8-element vector helpers (16 B of bf16, 32 B of fp32). NT = non-temporal access (measured to
+// help the parameter-update pass and to hurt the momentum pass).
+struct V8 { float v[8]; };
+
+template <bool NT, typename V>
+__device__ __forceinline__ V ld_stream(const V* p) {
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <bool NT, typename V>
+__device__ __forceinline__ void st_stream(V* p, V v) {
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
+
+template <int DT, bool NT = false>
+__device__ __forceinline__ void load8(const void* base, int64_t idx, V8& x) {
+  if constexpr (DT == kDtBF16) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 w = ld_stream<NT>(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(base) + idx));
+    const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      x.v[2 * k] = __uint_as_float(u[k] << 16);
+      x.v[2 * k + 1] = __uint_as_float(u[k] & 0xffff0000u);
+    }
+  } else {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    const f32x4 a = ld_stream<NT>(reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + idx));
+    const f32x4 b = ld_stream<NT>(reinterpret_cast<const f32x4*>(static_cast<const float*>(base) + idx + 4));
+    x.v[0] = a.x; x.v[1] = a.y; x.v[2] = a.z; x.v[3] = a.w;
+    x.v[4] = b.x; x.v[5] = b.y; x.v[6] = b.z; x.v[7] = b.w;
+  }
+}
+
+template <int DT, bool NT = false>
+__device__ __forceinline__ void store8(void* base, int64_t idx, const V8& x) {
+  if constexpr (DT == kDtBF16) {
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    u32x4 w;
+    w.x = uint32_t(f2bf(x.v[0])) | (uint32_t(f2bf(x.v[1])) << 16);
+    w.y = uint32_t(f2bf(x.v[2])) | (uint32_t(f2bf(x.v[3])) << 16);
+    w.z = uint32_t(f2bf(x.v[4])) | (uint32_t(f2bf(x.v[5])) << 16);
+    w.w = uint32_t(f2bf(x.v[6])) | (uint32_t(f2bf(x.v[7])) << 16);
+    st_stream<NT>(reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + idx), w);
+  } else {
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    float* p = static_cast<float*>(base) + idx;
+    st_stream<NT>(reinterpret_cast<f32x4*>(p), f32x4{x.v[0], x.v[1], x.v[2], x.v[3]});
+    st_stream<NT>(reinterpret_cast<f32x4*>(p + 4), f32x4{x.v[4], x.v[5], x.v[6], x.v[7]});
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// prep: one tile of 64 rows x TW columns of the stored (padded) matrix per workgroup of 256
+// threads (TW = 128 on the bf16 path, 64 on the fp32 path). Phase 1: thread t owns columns
+// 8 (t % (TW/8)) .. +7 of rows t / (TW/8) + (2048/TW) q: gradient and momentum in 16-B vectors,
+// u to the stored-orientation buffer and to an LDS tile. Phase 2: the transposed copy; thread t
+// gathers 8 consecutive tile rows 8 (t % 8) .. +7 of tile column t / 8 + 32 q and writes them as one
+// 16-B (bf16) vector, so 8 lanes cover 128 contiguous bytes of a transposed row. In LDS, element
+// (i, j) sits at column j ^ 8 ((i >> 3) & 7): the 16-B row writes stay contiguous and the 8-row
+// column gathers of a wave hit distinct banks.
+template <int NSDT>
+struct PrepTraits {
+  using elem = typename std::conditional<NSDT == kDtBF16, uint16_t, float>::type;
+  static constexpr int TW = NSDT == kDtBF16 ? kPrepColsBF16 : kPrepColsF32;
+};
+
 template <int NSDT>
 __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ descs, int count,
                                                    float beta, float omb, int nesterov) {
-  __shared__ float tile[64][65];
+  using T = typename PrepTraits<NSDT>::elem;
+  constexpr int TW = PrepTraits<NSDT>::TW;
+  constexpr int CPR = TW / 8;          // 8-column chunks per tile row
+  constexpr int RPP = 256 / CPR;       // tile rows covered per pass
+  __shared__ __attribute__((aligned(16))) T tile[64 * TW];
   __shared__ float red[4];
   const int e = find_entry(descs, count, blockIdx.x);
-  const PrepDesc d = descs[e];
+  const PrepDesc& d = descs[e];
   const int lt = blockIdx.x - d.tile_begin;
-  const int64_t row0 = int64_t(lt / d.tiles_n) * 64, col0 = int64_t(lt % d.tiles_n) * 64;
+  const int64_t row0 = int64_t(lt / d.tiles_n) * 64, col0 = int64_t(lt % d.tiles_n) * TW;
+  const int64_t m = d.m, n = d.n;
   const int t = threadIdx.x;
-  const int c4 = (t & 15) * 4, rr = t >> 4;
+  const int c8 = (t % CPR) * 8, rr = t / CPR;
   float ss = 0.0f;
-  const bool vec = (d.n % 4 == 0);
+  const bool vec = (n % 8 == 0);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t i = row0 + rr + 16 * q;
-    const int64_t j0 = col0 + c4;
-    float u[4];
-    if (i < d.m && vec && j0 + 3 < d.n) {
-      const int64_t idx = i * d.n + j0;
-      float g[4];
-      if (d.grad_dtype == kDtBF16) load4<kDtBF16>(d.grad, idx, g); else load4<kDtF32>(d.grad, idx, g);
+  for (int q = 0; q < 64 / RPP; ++q) {
+    const int ti = rr + RPP * q;
+    const int64_t i = row0 + ti;
+    const int64_t j0 = col0 + c8;
+    V8 u;
+    if (i < m && vec && j0 + 7 < n) {
+      const int64_t idx = i * n + j0;
+      V8 g;
+      if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, idx, g); else load8<kDtF32>(d.grad, idx, g);
       if (d.momentum) {
-        float4 mo = *reinterpret_cast<const float4*>(d.momentum + idx);
-        float mv[4] = {mo.x, mo.y, mo.z, mo.w};
+        V8 mv;
+        load8<kDtF32>(d.momentum, idx, mv);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          mv[k] = mv[k] + omb * (g[k] - mv[k]);
-          u[k] = nesterov ? g[k] + beta * (mv[k] - g[k]) : mv[k];
+        for (int k = 0; k < 8; ++k) {
+          mv.v[k] = mv.v[k] + omb * (g.v[k] - mv.v[k]);
+          u.v[k] = nesterov ? g.v[k] + beta * (mv.v[k] - g.v[k]) : mv.v[k];
         }
-        *reinterpret_cast<float4*>(d.momentum + idx) = make_float4(mv[0], mv[1], mv[2], mv[3]);
+        store8<kDtF32>(d.momentum, idx, mv);
       } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) u[k] = g[k];
+        u = g;
       }
     } else {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
+      for (int k = 0; k < 8; ++k) {
         const int64_t j = j0 + k;
-        u[k] = 0.0f;
-        if (i < d.m && j < d.n) {
-          const int64_t idx = i * d.n + j;
+        u.v[k] = 0.0f;
+        if (i < m && j < n) {
+          const int64_t idx = i * n + j;
           const float g = load_as_f32(d.grad, idx, d.grad_dtype);
           if (d.momentum) {
             float mv = d.momentum[idx];
             mv = mv + omb * (g - mv);
             d.momentum[idx] = mv;
-            u[k] = nesterov ? g + beta * (mv - g) : mv;
+            u.v[k] = nesterov ? g + beta * (mv - g) : mv;
           } else {
-            u[k] = g;
+            u.v[k] = g;
           }
         }
       }
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      ss += u[k] * u[k];
-      tile[rr + 16 * q][c4 + k] = u[k];
+    for (int k = 0; k < 8; ++k) ss += u.v[k] * u.v[k];
+    store8<NSDT>(d.d_out, i * d.ld_d + j0, u);
+    // LDS copy (rounded to the NS dtype exactly as the global one)
+    T* trow = tile + ti * TW + (c8 ^ (8 * ((ti >> 3) & 7)));
+    if constexpr (NSDT == kDtBF16) {
+      uint4 w;
+      w.x = uint32_t(f2bf(u.v[0])) | (uint32_t(f2bf(u.v[1])) << 16);
+      w.y = uint32_t(f2bf(u.v[2])) | (uint32_t(f2bf(u.v[3])) << 16);
+      w.z = uint32_t(f2bf(u.v[4])) | (uint32_t(f2bf(u.v[5])) << 16);
+      w.w = uint32_t(f2bf(u.v[6])) | (uint32_t(f2bf(u.v[7])) << 16);
+      *reinterpret_cast<uint4*>(trow) = w;
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) trow[k] = u.v[k];
     }
-    store4<NSDT>(d.d_out, i * d.ld_d + j0, u);
   }
   __syncthreads();
-  // transposed copy: rows col0 + jj of the T buffer, columns row0 + c4 .. +3
+  // transposed copy: buffer row col0 + jj, columns row0 + 8 mm .. +7
+  {
+    const int mm = t & 7;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int jj = rr + 16 * q;
-    float v[4];
+    for (int q = 0; q < TW / 32; ++q) {
+      const int jj = (t >> 3) + 32 * q;
+      T* dst = static_cast<T*>(d.t_out) + (col0 + jj) * d.ld_t + row0 + 8 * mm;
+      if constexpr (NSDT == kDtBF16) {
+        uint32_t h[8];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) v[k] = tile[c4 + k][jj];
-    store4<NSDT>(d.t_out, (col0 + jj) * d.ld_t + row0 + c4, v);
+        for (int k = 0; k < 8; ++k) {
+          const int ti = 8 * mm + k;
+          h[k] = tile[ti * TW + (jj ^ (8 * ((ti >> 3) & 7)))];
+        }
+        *reinterpret_cast<uint4*>(dst) =
+            make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+      } else {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int ti = 8 * mm + k;
+          v[k] = tile[ti * TW + (jj ^ (8 * ((ti >> 3) & 7)))];
+        }
+        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      }
+    }
   }
   ss = wave_sum(ss);
   if ((t & 63) == 0) red[t >> 6] = ss;
@@ -174,48 +276,52 @@ __global__ __launch_bounds__(256) void norm_kernel(const NormDesc* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------------------------
-// apply: one 64 x 64 tile of the stored m x n matrix per workgroup (no padding here).
+// apply: one kApplyRows x kApplyCols tile of the stored m x n matrix per workgroup (no padding
+// here); thread t owns columns 8 (t % (kApplyCols / 8)) .. +7 of rows t / (kApplyCols / 8) + ...,
+// in 16-B vectors.
 template <int NSDT>
 __global__ __launch_bounds__(256) void apply_kernel(const ApplyDesc* __restrict__ descs, int count) {
   const int e = find_entry(descs, count, blockIdx.x);
-  const ApplyDesc d = descs[e];
+  const ApplyDesc& d = descs[e];
   const int lt = blockIdx.x - d.tile_begin;
-  const int64_t row0 = int64_t(lt / d.tiles_n) * 64, col0 = int64_t(lt % d.tiles_n) * 64;
+  constexpr int CPR = kApplyCols / 8, RPP = 256 / CPR;
+  const int64_t row0 = int64_t(lt / d.tiles_n) * kApplyRows, col0 = int64_t(lt % d.tiles_n) * kApplyCols;
   const int t = threadIdx.x;
-  const int c4 = (t & 15) * 4, rr = t >> 4;
+  const int c8 = (t % CPR) * 8, rr = t / CPR;
   const float osc = d.use_scale ? d.scale[0] : 1.0f;
-  const bool vec = (d.n % 4 == 0);
+  const int64_t m = d.m, n = d.n;
+  const bool vec = (n % 8 == 0);
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t i = row0 + rr + 16 * q;
-    if (i >= d.m) continue;
-    const int64_t j0 = col0 + c4;
-    float o[4];
-    load4<NSDT>(d.o, i * d.ld_o + j0, o);  // the padded O buffer always has the 4 columns
+  for (int q = 0; q < kApplyRows / RPP; ++q) {
+    const int64_t i = row0 + rr + RPP * q;
+    const int64_t j0 = col0 + c8;
+    if (i >= m || j0 >= n) continue;
+    V8 o;
+    load8<NSDT, true>(d.o, i * d.ld_o + j0, o);  // j0 < n: the padded O row holds these 8 columns
 #pragma unroll
-    for (int k = 0; k < 4; ++k) o[k] *= osc;
-    const int64_t idx = i * d.n + j0;
-    if (vec && j0 + 3 < d.n) {
+    for (int k = 0; k < 8; ++k) o.v[k] *= osc;
+    const int64_t idx = i * n + j0;
+    if (vec && j0 + 7 < n) {
       if (d.mode == 0) {
-        float p[4];
-        if (d.param_dtype == kDtBF16) load4<kDtBF16>(d.param, idx, p); else load4<kDtF32>(d.param, idx, p);
+        V8 p;
+        if (d.param_dtype == kDtBF16) load8<kDtBF16, true>(d.param, idx, p); else load8<kDtF32, true>(d.param, idx, p);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) p[k] = p[k] * d.decay - d.step * o[k];
-        if (d.param_dtype == kDtBF16) store4<kDtBF16>(d.param, idx, p); else store4<kDtF32>(d.param, idx, p);
-        if (d.update_out) store4<kDtF32>(d.update_out, idx, o);
+        for (int k = 0; k < 8; ++k) p.v[k] = p.v[k] * d.decay - d.step * o.v[k];
+        if (d.param_dtype == kDtBF16) store8<kDtBF16, true>(d.param, idx, p); else store8<kDtF32, true>(d.param, idx, p);
+        if (d.update_out) store8<kDtF32, true>(d.update_out, idx, o);
       } else {
-        if (d.param_dtype == kDtBF16) store4<kDtBF16>(d.param, idx, o); else store4<kDtF32>(d.param, idx, o);
+        if (d.param_dtype == kDtBF16) store8<kDtBF16, true>(d.param, idx, o); else store8<kDtF32, true>(d.param, idx, o);
       }
     } else {
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (j0 + k >= d.n) break;
+      for (int k = 0; k < 8; ++k) {
+        if (j0 + k >= n) break;
         if (d.mode == 0) {
           const float p = load_as_f32(d.param, idx + k, d.param_dtype);
-          store_from_f32(d.param, idx + k, p * d.decay - d.step * o[k], d.param_dtype);
-          if (d.update_out) d.update_out[idx + k] = o[k];
+          store_from_f32(d.param, idx + k, p * d.decay - d.step * o.v[k], d.param_dtype);
+          if (d.update_out) d.update_out[idx + k] = o.v[k];
         } else {
-          store_from_f32(d.param, idx + k, o[k], d.param_dtype);
+          store_from_f32(d.param, idx + k, o.v[k], d.param_dtype);
         }
       }
     }
@@ -224,7 +330,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const ApplyDesc* __restrict_
 
 // ---------------------------------------------------------------------------------------------
 // AdamW: grouped over up to kAdamWMaxPerLaunch tensors passed by value; each workgroup owns
-// kAdamWBlockElems consecutive elements of one tensor, 16 per thread (4 groups of 4).
+// kAdamWBlockElems consecutive elements of one tensor, in 8-element (16-B bf16) vectors.
 __device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v, const AdamWBatch& b) {
   p = p * b.decay;
   m = m + b.omb1 * (g - m);
@@ -239,22 +345,22 @@ __global__ __launch_bounds__(256) void adamw_kernel(const AdamWBatch batch) {
     if (batch.d[k].block_begin <= int(blockIdx.x)) e = k;
   const AdamWDesc& d = batch.d[e];
   const int64_t base = int64_t(blockIdx.x - d.block_begin) * kAdamWBlockElems;
+  // thread t owns elements base + (q * 256 + t) * 8 .. +7, q = 0 .. kAdamWBlockElems / 2048 - 1
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int64_t i0 = base + (int64_t(q) * 256 + threadIdx.x) * 4;
+  for (int q = 0; q < kAdamWBlockElems / 2048; ++q) {
+    const int64_t i0 = base + (int64_t(q) * 256 + threadIdx.x) * 8;
     if (i0 >= d.numel) break;
-    if (i0 + 3 < d.numel) {
-      float p[4], g[4];
-      if (d.param_dtype == kDtBF16) load4<kDtBF16>(d.param, i0, p); else load4<kDtF32>(d.param, i0, p);
-      if (d.grad_dtype == kDtBF16) load4<kDtBF16>(d.grad, i0, g); else load4<kDtF32>(d.grad, i0, g);
-      float4 m4 = *reinterpret_cast<const float4*>(d.exp_avg + i0);
-      float4 v4 = *reinterpret_cast<const float4*>(d.exp_avg_sq + i0);
-      float m[4] = {m4.x, m4.y, m4.z, m4.w}, v[4] = {v4.x, v4.y, v4.z, v4.w};
+    if (i0 + 7 < d.numel) {
+      V8 p, g, m, v;
+      if (d.param_dtype == kDtBF16) load8<kDtBF16>(d.param, i0, p); else load8<kDtF32>(d.param, i0, p);
+      if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, i0, g); else load8<kDtF32>(d.grad, i0, g);
+      load8<kDtF32>(d.exp_avg, i0, m);
+      load8<kDtF32>(d.exp_avg_sq, i0, v);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) adamw_elem(p[k], g[k], m[k], v[k], batch);
-      if (d.param_dtype == kDtBF16) store4<kDtBF16>(d.param, i0, p); else store4<kDtF32>(d.param, i0, p);
-      *reinterpret_cast<float4*>(d.exp_avg + i0) = make_float4(m[0], m[1], m[2], m[3]);
-      *reinterpret_cast<float4*>(d.exp_avg_sq + i0) = make_float4(v[0], v[1], v[2], v[3]);
+      for (int k = 0; k < 8; ++k) adamw_elem(p.v[k], g.v[k], m.v[k], v.v[k], batch);
+      if (d.param_dtype == kDtBF16) store8<kDtBF16>(d.param, i0, p); else store8<kDtF32>(d.param, i0, p);
+      store8<kDtF32>(d.exp_avg, i0, m);
+      store8<kDtF32>(d.exp_avg_sq, i0, v);
     } else {
       for (int64_t i = i0; i < d.numel; ++i) {
         float p = load_as_f32(d.param, i, d.param_dtype);

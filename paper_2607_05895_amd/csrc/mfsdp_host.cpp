@@ -70,8 +70,8 @@ NsPlan plan_ns(int64_t m, int64_t n, int ns_dtype, size_t base) {
   const size_t xb = align_up(size_t(p.r_pad) * size_t(p.s_pad) * p.es);
   const size_t gb = align_up(size_t(p.r_pad) * size_t(p.r_pad) * p.es);
   const int64_t rows = p.tall ? p.s_pad : p.r_pad, cols = p.tall ? p.r_pad : p.s_pad;
-  p.prep_tiles_m = int(rows / kPrepTile);
-  p.prep_tiles_n = int(cols / kPrepTile);
+  p.prep_tiles_m = int(rows / kPrepRows);
+  p.prep_tiles_n = int(cols / (ns_dtype == MFSDP_BF16 ? kPrepColsBF16 : kPrepColsF32));
   size_t o = base;
   p.off_x[0] = o; o += xb;
   p.off_x[1] = o; o += xb;
@@ -333,8 +333,8 @@ ApplyDesc make_apply(const NsPlan& p, uint8_t* ws, int steps, void* param, int p
   d.mode = mode;
   d.decay = decay;
   d.step = step;
-  d.tiles_m = int((p.m + 63) / 64);
-  d.tiles_n = int((p.n + 63) / 64);
+  d.tiles_m = int((p.m + kApplyRows - 1) / kApplyRows);
+  d.tiles_n = int((p.n + kApplyCols - 1) / kApplyCols);
   d.tile_begin = tile_begin;
   return d;
 }
