@@ -116,57 +116,72 @@ struct WaveGrid {
   static constexpr int LOADS = 32 / NW;  // DMA instructions per thread per stage
 };
 
+// Per-tile state of the persistent kernel: operand sources of the DMA and the tile coordinates.
+struct TileCtx {
+  const GemmDesc* d;
+  int bi, bj, nk;
+  const uint16_t* psrc;
+  const uint16_t* qsrc;
+  int64_t pstep, qstep;
+};
+
 template <int NW>
 __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
-                                                               int count, int parity, int first,
+                                                               const TileRef* __restrict__ sched,
+                                                               int ngroups, int parity, int first,
                                                                int last) {
   using WG = WaveGrid<NW>;
   constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS;
+  constexpr int PL = LOADS / 2;        // DMA instructions for P (and for Q) per thread per stage
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NSTAGE * STAGE_BYTES];
 
-  const int e = find_entry(descs, count, blockIdx.x);
-  const GemmDesc& dd = descs[e];
-  const int lt = blockIdx.x - dd.tile_begin;
-  int bi, bj;
-  tile_coords(dd, lt, bi, bj);
-  const uint16_t* __restrict__ P = static_cast<const uint16_t*>(dd.P[parity]);
-  const uint16_t* __restrict__ Q = static_cast<const uint16_t*>(dd.Q[parity]);
-  const int64_t ldp = dd.ldp, ldq = dd.ldq;
-  const int nk = dd.K / BKE;
-
+  const int xcd = blockIdx.x % kGemmXcds, slot = blockIdx.x / kGemmXcds;
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int wm = w / WG::WN, wn = w % WG::WN;
-
   // DMA mapping: instruction c of wave w covers staged rows j * 16 + lane / 4 with j = c * NW + w;
   // j < 16 are P rows, j >= 16 the rows j - 16 of Q. Lane slot = lane % 4 holds global chunk
   // slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
   const int drow = w * 16 + (lane >> 2);
   const int dchunk = (lane & 3) ^ swz(lane >> 2);
-  const uint16_t* psrc = P + (int64_t(bi) * BT + drow) * ldp + dchunk * 8;
-  const uint16_t* qsrc = Q + (int64_t(bj) * BT + drow) * ldq + dchunk * 8;
-  const int64_t pstep = int64_t(NW * 16) * ldp, qstep = int64_t(NW * 16) * ldq;
   const int dma_wave_off = w * 1024;  // + c * NW * 1024 within a stage
-  constexpr int PL = LOADS / 2;        // instructions for P (and for Q) per thread
 
-  auto issue = [&](int kt, int stage) {
+  // next non-idle tile of this workgroup at or after group g (g advances by kGemmXcds)
+  auto next_tile = [&](int& g, TileCtx& c) -> bool {
+    for (; g < ngroups; g += kGemmXcds) {
+      const TileRef r = sched[g * kGemmSlots + slot];
+      if (r.e < 0) continue;
+      const GemmDesc& dd = descs[r.e];
+      c.d = &dd;
+      c.bi = r.bi;
+      c.bj = r.bj;
+      c.nk = dd.K / BKE;
+      const uint16_t* P = static_cast<const uint16_t*>(dd.P[parity]);
+      const uint16_t* Q = static_cast<const uint16_t*>(dd.Q[parity]);
+      c.psrc = P + (int64_t(c.bi) * BT + drow) * dd.ldp + dchunk * 8;
+      c.qsrc = Q + (int64_t(c.bj) * BT + drow) * dd.ldq + dchunk * 8;
+      c.pstep = int64_t(NW * 16) * dd.ldp;
+      c.qstep = int64_t(NW * 16) * dd.ldq;
+      return true;
+    }
+    return false;
+  };
+  auto issue = [&](const TileCtx& c, int kt, int stage) {
     const int64_t koff = int64_t(kt) * BKE;
     lds_byte* sb = (lds_byte*)(smem + stage * STAGE_BYTES + dma_wave_off);
 #pragma unroll
-    for (int c = 0; c < PL; ++c)
-      __builtin_amdgcn_global_load_lds(psrc + c * pstep + koff, sb + c * NW * 1024, 16, 0, 0);
+    for (int i = 0; i < PL; ++i)
+      __builtin_amdgcn_global_load_lds(c.psrc + i * c.pstep + koff, sb + i * NW * 1024, 16, 0, 0);
 #pragma unroll
-    for (int c = 0; c < PL; ++c)
-      __builtin_amdgcn_global_load_lds(qsrc + c * qstep + koff, sb + 16384 + c * NW * 1024, 16, 0, 0);
+    for (int i = 0; i < PL; ++i)
+      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + 16384 + i * NW * 1024, 16, 0, 0);
   };
-
-  f32x16_t acc[MI][NI];
+  // steps 0 .. NSTAGE-2 of a tile into stages 0 .. NSTAGE-2 (steps past the end are clamped to the
+  // last one: in-bounds reloads into stages nobody reads)
+  auto prologue = [&](const TileCtx& c) {
 #pragma unroll
-  for (int a = 0; a < MI; ++a)
-#pragma unroll
-    for (int b = 0; b < NI; ++b)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+    for (int s = 0; s < NSTAGE - 1; ++s) issue(c, s < c.nk ? s : c.nk - 1, s);
+  };
 
   // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
   const int frow = lane & 31, fhalf = lane >> 5;
@@ -174,144 +189,168 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   const int qbase = (BT + wn * (NI * 32) + frow) * ROWB;
   const int slot0 = ((0 + fhalf) ^ swz(frow)) * 16;
   const int slot1 = ((2 + fhalf) ^ swz(frow)) * 16;
-
-  bf16x8_t pf0[MI], qf0[NI], pf1[MI], qf1[NI];
-  auto read_frags = [&](const uint8_t* sb, int slot, bf16x8_t* pf, bf16x8_t* qf) {
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-      pf[mi] = *reinterpret_cast<const bf16x8_t*>(sb + pbase + mi * 32 * ROWB + slot);
-#pragma unroll
-    for (int ni = 0; ni < NI; ++ni)
-      qf[ni] = *reinterpret_cast<const bf16x8_t*>(sb + qbase + ni * 32 * ROWB + slot);
-  };
-  auto mfma_slice = [&](const bf16x8_t* pf, const bf16x8_t* qf) {
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < NI; ++ni)
-        acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ni], pf[mi], acc[mi][ni], 0, 0, 0);
-  };
   constexpr int NMF = MI * NI;      // MFMAs per 16-wide K slice
   constexpr int NRD = MI + NI;      // fragment reads per slice
 
-  // prologue: steps 0 .. NSTAGE-2 in flight, then step 0 visible. Steps past the end are clamped to
-  // the last one (in-bounds reloads into stages nobody reads).
-  const int last_kt = nk - 1;
-#pragma unroll
-  for (int s = 0; s < NSTAGE - 1; ++s) issue(s < nk ? s : last_kt, s);
-  MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS);
-  __builtin_amdgcn_s_barrier();
-  read_frags(smem, slot0, pf0, qf0);
+  int g = xcd;
+  TileCtx cur;
+  if (!next_tile(g, cur)) return;
+  prologue(cur);
+  while (true) {
+    g += kGemmXcds;
+    TileCtx nxt;
+    const bool has_next = next_tile(g, nxt);
 
-  int cur = 0;                  // stage of step kt
-  int nxt = 1;                  // stage of step kt + 1
-  int fill = NSTAGE - 1;        // stage that receives step kt + NSTAGE - 1 (the stage of kt - 1)
-  for (int kt = 0; kt < nk; ++kt) {
-    const uint8_t* sb = smem + cur * STAGE_BYTES;
-    read_frags(sb, slot1, pf1, qf1);
-    mfma_slice(pf0, qf0);
+    f32x16_t acc[MI][NI];
 #pragma unroll
-    for (int i = 0; i < NRD; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-    }
-    __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
-    // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
-    MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS);
+    for (int a = 0; a < MI; ++a)
+#pragma unroll
+      for (int b = 0; b < NI; ++b)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[a][b][v] = 0.0f;
+
+    bf16x8_t pf0[MI], qf0[NI], pf1[MI], qf1[NI];
+    auto read_frags = [&](const uint8_t* sb, int sl, bf16x8_t* pf, bf16x8_t* qf) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+        pf[mi] = *reinterpret_cast<const bf16x8_t*>(sb + pbase + mi * 32 * ROWB + sl);
+#pragma unroll
+      for (int ni = 0; ni < NI; ++ni)
+        qf[ni] = *reinterpret_cast<const bf16x8_t*>(sb + qbase + ni * 32 * ROWB + sl);
+    };
+    auto mfma_slice = [&](const bf16x8_t* pf, const bf16x8_t* qf) {
+#pragma unroll
+      for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < NI; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ni], pf[mi], acc[mi][ni], 0, 0, 0);
+    };
+
+    // Main loop. Outstanding vector-memory operations of this wave at this point: this tile's
+    // prologue loads, then the previous tile's epilogue stores. Loads complete in order among
+    // themselves, so "at most (NSTAGE - 2) * LOADS outstanding" implies step 0 has landed whether
+    // or not stores retire in order with loads (if they do, this waits a little longer than needed).
+    const int nk = cur.nk, last_kt = nk - 1;
+    MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS);
     __builtin_amdgcn_s_barrier();
-    {
-      const int kload = kt + NSTAGE - 1;
-      issue(kload < nk ? kload : last_kt, fill);
-    }
-    read_frags(smem + nxt * STAGE_BYTES, slot0, pf0, qf0);
-    mfma_slice(pf1, qf1);
+    read_frags(smem, slot0, pf0, qf0);
+    int cs = 0, ns = 1, fs = NSTAGE - 1;  // stages of steps kt, kt + 1 and of step kt + NSTAGE - 1
+    for (int kt = 0; kt < nk; ++kt) {
+      const uint8_t* sb = smem + cs * STAGE_BYTES;
+      read_frags(sb, slot1, pf1, qf1);
+      mfma_slice(pf0, qf0);
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
-    }
+      for (int i = 0; i < NRD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
+      // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
+      MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS);
+      __builtin_amdgcn_s_barrier();
+      {
+        const int kload = kt + NSTAGE - 1;
+        issue(cur, kload < nk ? kload : last_kt, fs);
+      }
+      read_frags(smem + ns * STAGE_BYTES, slot0, pf0, qf0);
+      mfma_slice(pf1, qf1);
 #pragma unroll
-    for (int i = 0; i < NRD; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int i = 0; i < LOADS; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
+      }
+#pragma unroll
+      for (int i = 0; i < NRD; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD - LOADS, 0);
+      cs = ns;
+      ns = (ns + 1 == NSTAGE) ? 0 : ns + 1;
+      fs = (fs + 1 == NSTAGE) ? 0 : fs + 1;
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD - LOADS, 0);
-    cur = nxt;
-    nxt = (nxt + 1 == NSTAGE) ? 0 : nxt + 1;
-    fill = (fill + 1 == NSTAGE) ? 0 : fill + 1;
-  }
-  // drain the DMA of the clamped tail steps before the workgroup can exit
-  MFSDP_WAIT_VMCNT(0);
+    // The clamped tail loads of this tile must land before the next tile's prologue reuses the
+    // stages, and every wave must be done reading LDS (its last fragments were consumed by MFMAs).
+    MFSDP_WAIT_VMCNT(0);
+    __builtin_amdgcn_s_barrier();
+    if (has_next) prologue(nxt);  // overlaps the epilogue below
 
-  // Epilogue. acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
-  // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t: each lane has 4 consecutive columns
-  // of one row per group g (one 8-byte row-major store). For the transposed stores (X'^T, and the
-  // mirrored tile of a symmetric product) the 4 x 4 blocks held by lane quads are transposed with
-  // two DPP exchanges, so each lane then holds 4 consecutive rows of one column (again one 8-byte
-  // store).
-  const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
-  const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
-  const float diag = (dd.sym && bi == bj) ? dd.diag : 0.0f;
-  const uint16_t* E = static_cast<const uint16_t*>(dd.E[parity]);
-  uint16_t* C = static_cast<uint16_t*>(dd.C[parity]);
-  uint16_t* CT = static_cast<uint16_t*>(dd.CT[parity]);
-  if (last) {
-    if (!dd.last_c) C = nullptr;
-    if (!dd.last_ct) CT = nullptr;
-  }
-  // transposed destination: the mirror tile of a symmetric product, or X'^T
-  uint16_t* TD = (dd.sym && bi != bj && C) ? C : CT;
-  const int64_t ldtd = (TD == C) ? dd.ldc : dd.ldct;
-  const int64_t lde = dd.lde, ldc = dd.ldc;
-  const int q = lane & 3;
-  const bool q_odd = q & 1, q_hi = q & 2;
+    // Epilogue. acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
+    // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t: each lane has 4 consecutive columns
+    // of one row per group g (one 8-byte row-major store). For the transposed stores (X'^T, and the
+    // mirrored tile of a symmetric product) the 4 x 4 blocks held by lane quads are transposed with
+    // two DPP exchanges, so each lane then holds 4 consecutive rows of one column (again one 8-byte
+    // store).
+    const GemmDesc& dd = *cur.d;
+    const int bi = cur.bi, bj = cur.bj;
+    const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
+    const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
+    const float diag = (dd.sym && bi == bj) ? dd.diag : 0.0f;
+    const uint16_t* E = static_cast<const uint16_t*>(dd.E[parity]);
+    uint16_t* C = static_cast<uint16_t*>(dd.C[parity]);
+    uint16_t* CT = static_cast<uint16_t*>(dd.CT[parity]);
+    if (last) {
+      if (!dd.last_c) C = nullptr;
+      if (!dd.last_ct) CT = nullptr;
+    }
+    // transposed destination: the mirror tile of a symmetric product, or X'^T
+    uint16_t* TD = (dd.sym && bi != bj && C) ? C : CT;
+    const int64_t ldtd = (TD == C) ? dd.ldc : dd.ldct;
+    const int64_t lde = dd.lde, ldc = dd.ldc;
+    const int q = lane & 3;
+    const bool q_odd = q & 1, q_hi = q & 2;
 #pragma unroll
-  for (int mi = 0; mi < MI; ++mi) {
-    const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
-    const int64_t iq = i - q;  // first row of this lane quad
+    for (int mi = 0; mi < MI; ++mi) {
+      const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
+      const int64_t iq = i - q;  // first row of this lane quad
 #pragma unroll
-    for (int ni = 0; ni < NI; ++ni) {
+      for (int ni = 0; ni < NI; ++ni) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + g * 8 + fhalf * 4;
-        float v0 = alpha * acc[mi][ni][4 * g + 0];
-        float v1 = alpha * acc[mi][ni][4 * g + 1];
-        float v2 = alpha * acc[mi][ni][4 * g + 2];
-        float v3 = alpha * acc[mi][ni][4 * g + 3];
-        if (E) {
-          const uint2 ev = *reinterpret_cast<const uint2*>(E + i * lde + j);
-          v0 += beta * __uint_as_float(ev.x << 16);
-          v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
-          v2 += beta * __uint_as_float(ev.y << 16);
-          v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
-        }
-        if (diag != 0.0f) {
-          if (i == j + 0) v0 += diag;
-          if (i == j + 1) v1 += diag;
-          if (i == j + 2) v2 += diag;
-          if (i == j + 3) v3 += diag;
-        }
-        if (C) *reinterpret_cast<uint2*>(C + i * ldc + j) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
-        if (TD) {
-          // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
-          {
-            const float x0 = q_odd ? v0 : v1, x1 = q_odd ? v2 : v3;
-            const float y0 = dpp_quad_xor1(x0), y1 = dpp_quad_xor1(x1);
-            if (q_odd) { v0 = y0; v2 = y1; } else { v1 = y0; v3 = y1; }
+        for (int gg = 0; gg < 4; ++gg) {
+          const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+          float v0 = alpha * acc[mi][ni][4 * gg + 0];
+          float v1 = alpha * acc[mi][ni][4 * gg + 1];
+          float v2 = alpha * acc[mi][ni][4 * gg + 2];
+          float v3 = alpha * acc[mi][ni][4 * gg + 3];
+          if (E) {
+            const uint2 ev = *reinterpret_cast<const uint2*>(E + i * lde + j);
+            v0 += beta * __uint_as_float(ev.x << 16);
+            v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
+            v2 += beta * __uint_as_float(ev.y << 16);
+            v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
           }
-          // exchange across lane ^ 2: low lanes take the partner's elements 0, 1 as their 2, 3
-          {
-            const float x0 = q_hi ? v0 : v2, x1 = q_hi ? v1 : v3;
-            const float y0 = dpp_quad_xor2(x0), y1 = dpp_quad_xor2(x1);
-            if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
+          if (diag != 0.0f) {
+            if (i == j + 0) v0 += diag;
+            if (i == j + 1) v1 += diag;
+            if (i == j + 2) v2 += diag;
+            if (i == j + 3) v3 += diag;
           }
-          // lane q now holds column j + q at rows iq .. iq + 3
-          *reinterpret_cast<uint2*>(TD + (j + q) * ldtd + iq) =
-              make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          if (C) *reinterpret_cast<uint2*>(C + i * ldc + j) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          if (TD) {
+            // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
+            {
+              const float x0 = q_odd ? v0 : v1, x1 = q_odd ? v2 : v3;
+              const float y0 = dpp_quad_xor1(x0), y1 = dpp_quad_xor1(x1);
+              if (q_odd) { v0 = y0; v2 = y1; } else { v1 = y0; v3 = y1; }
+            }
+            // exchange across lane ^ 2: low lanes take the partner's elements 0, 1 as their 2, 3
+            {
+              const float x0 = q_hi ? v0 : v2, x1 = q_hi ? v1 : v3;
+              const float y0 = dpp_quad_xor2(x0), y1 = dpp_quad_xor2(x1);
+              if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
+            }
+            // lane q now holds column j + q at rows iq .. iq + 3
+            *reinterpret_cast<uint2*>(TD + (j + q) * ldtd + iq) =
+                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          }
         }
       }
     }
+    if (!has_next) break;
+    cur = nxt;
   }
+  // nothing of this workgroup may still be in flight when it exits
+  MFSDP_WAIT_VMCNT(0);
 }
 #undef MFSDP_WAIT_VMCNT
 
@@ -391,13 +430,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
 
 }  // namespace
 
-hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       int parity, int first_step, int last_step, hipStream_t st) {
+hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
+                       int ngroups, int ns_dtype, int parity, int first_step, int last_step,
+                       hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16)
-    hipLaunchKernelGGL(gemm_bf16_kernel<MFSDP_GEMM_WAVES>, dim3(total_tiles),
-                       dim3(MFSDP_GEMM_WAVES * 64), 0, st, d_descs, count, parity, first_step,
-                       last_step);
+    hipLaunchKernelGGL(gemm_bf16_kernel<MFSDP_GEMM_WAVES>, dim3(kGemmXcds * kGemmSlots),
+                       dim3(MFSDP_GEMM_WAVES * 64), 0, st, d_descs, d_sched, ngroups, parity,
+                       first_step, last_step);
   else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
                        parity, first_step, last_step);

@@ -87,16 +87,73 @@ NsPlan plan_ns(int64_t m, int64_t n, int ns_dtype, size_t base) {
 
 // Descriptor region at the start of the workspace.
 struct DescLayout {
-  size_t off_prep, off_norm, off_gemm[3], off_apply, bytes;
+  size_t off_prep, off_norm, off_gemm[3], off_apply, off_sched[3], bytes;
+  int ngroups[3];
 };
 
-DescLayout plan_descs(int64_t count) {
+// Per-problem tile shape of the three NS products (tiles of kTileBF16 / kTileF32).
+struct TileGrid {
+  int tm, tn;
+  bool sym;
+};
+
+// Tile schedule of one product for the persistent bf16 kernel. Tiles are put in locality order
+// (bands of kGroupRows block rows, within a band column by column, upper triangle only for
+// symmetric products) and cut into groups of kGemmSlots tiles, so that the workgroups of one XCD
+// run the tiles of a group together and share its operand blocks in L2. Groups are then dealt to
+// the XCDs longest first, each to the XCD with the least work so far (a group's cost is the
+// largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
+// g % kGemmXcds; XCDs with fewer groups get empty ones (every slot e = -1).
+std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
+                                    const std::vector<int64_t>& cost) {
+  std::vector<TileRef> flat;
+  for (int e : order) {
+    const TileGrid& g = grids[e];
+    for (int r0 = 0; r0 < g.tm; r0 += kGroupRows) {
+      const int r1 = std::min(g.tm, r0 + kGroupRows);
+      for (int c = g.sym ? r0 : 0; c < g.tn; ++c)
+        for (int r = r0; r < r1; ++r)
+          if (!g.sym || r <= c) flat.push_back(TileRef{e, int16_t(r), int16_t(c)});
+    }
+  }
+  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0});
+  const size_t ng = flat.size() / kGemmSlots;
+  std::vector<int64_t> gcost(ng, 0);
+  for (size_t g = 0; g < ng; ++g)
+    for (int s = 0; s < kGemmSlots; ++s) {
+      const TileRef& t = flat[g * kGemmSlots + s];
+      if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e]);
+    }
+  std::vector<size_t> by(ng);
+  for (size_t g = 0; g < ng; ++g) by[g] = g;
+  std::stable_sort(by.begin(), by.end(), [&](size_t x, size_t y) { return gcost[x] > gcost[y]; });
+  std::vector<std::vector<size_t>> lists(kGemmXcds);
+  int64_t load[kGemmXcds] = {};
+  for (size_t g : by) {
+    int best = 0;
+    for (int x = 1; x < kGemmXcds; ++x)
+      if (load[x] < load[best]) best = x;
+    lists[best].push_back(g);
+    load[best] += gcost[g];
+  }
+  size_t rounds = 0;
+  for (const auto& l : lists) rounds = std::max(rounds, l.size());
+  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0});
+  for (int x = 0; x < kGemmXcds; ++x)
+    for (size_t i = 0; i < lists[x].size(); ++i)
+      std::memcpy(&s[(i * kGemmXcds + x) * kGemmSlots], &flat[lists[x][i] * kGemmSlots],
+                  kGemmSlots * sizeof(TileRef));
+  return s;
+}
+
+DescLayout plan_descs(int64_t count, const size_t sched_bytes[3]) {
   DescLayout d{};
   size_t o = 0;
   d.off_prep = o; o += align_up(sizeof(PrepDesc) * count);
   d.off_norm = o; o += align_up(sizeof(NormDesc) * count);
   for (int k = 0; k < 3; ++k) { d.off_gemm[k] = o; o += align_up(sizeof(GemmDesc) * count); }
   d.off_apply = o; o += align_up(sizeof(ApplyDesc) * count);
+  for (int k = 0; k < 3; ++k) { d.off_sched[k] = o; o += align_up(sched_bytes[k]); }
   d.bytes = o;
   return d;
 }
@@ -216,29 +273,79 @@ int hip_fail(hipError_t e, const char* what) {
 
 // Builds and enqueues the NS pipeline for a set of problems that already have their prep
 // descriptors filled. Shared by the Muon step and standalone NS.
-struct Problem {
-  NsPlan plan;
-  size_t base;  // not used after planning, kept for clarity
+// Problem order of one NS product: heaviest K first (all tiles have the same size, so the work
+// of a tile is proportional to K).
+std::vector<int> phase_order(const std::vector<NsPlan>& plans, int phase) {
+  std::vector<int> ord(plans.size());
+  for (size_t i = 0; i < ord.size(); ++i) ord[i] = int(i);
+  std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) {
+    const int64_t kx = phase == 0 ? plans[x].s_pad : plans[x].r_pad;
+    const int64_t ky = phase == 0 ? plans[y].s_pad : plans[y].r_pad;
+    return kx > ky;
+  });
+  return ord;
+}
+
+// Everything about a call that follows from the shapes and the NS dtype: per-matrix buffers,
+// the problem order and tile schedule of each NS product, and the descriptor region layout.
+struct Plan {
+  std::vector<NsPlan> ns;
+  std::vector<int> order[3];
+  std::vector<TileRef> sched[3];
+  int tiles[3] = {0, 0, 0};
+  DescLayout dl{};
+  size_t bytes = 0;
 };
 
-void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_muon_hparams& hp,
-                     GemmDesc* syrk, GemmDesc* sqr, GemmDesc* upd, int tile,
-                     int* tiles_syrk, int* tiles_sqr, int* tiles_upd) {
-  const int n = int(plans.size());
-  std::vector<int> order(n);
-  for (int i = 0; i < n; ++i) order[i] = i;
-  auto fill = [&](GemmDesc* out, int phase, int* total) {
-    // heaviest K first: with tiles of equal size the per-tile work is proportional to K
-    std::vector<int> ord = order;
-    std::stable_sort(ord.begin(), ord.end(), [&](int x, int y) {
-      const NsPlan& a = plans[x];
-      const NsPlan& b = plans[y];
-      const int64_t ka = phase == 0 ? a.s_pad : a.r_pad, kb = phase == 0 ? b.s_pad : b.r_pad;
-      return ka > kb;
-    });
+template <typename ShapeAt>
+Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
+  Plan P;
+  std::vector<NsPlan> shapes;
+  for (int64_t i = 0; i < count; ++i) {
+    int64_t m, n;
+    shape_at(i, m, n);
+    shapes.push_back(plan_ns(m, n, ns_dtype, 0));
+  }
+  const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
+  size_t sched_bytes[3] = {0, 0, 0};
+  for (int ph = 0; ph < 3; ++ph) {
+    P.order[ph] = phase_order(shapes, ph);
+    std::vector<TileGrid> grids;
+    std::vector<int> pos;
+    std::vector<int64_t> cost;
+    for (int k = 0; k < int(count); ++k) {
+      const NsPlan& p = shapes[P.order[ph][k]];
+      const int tr = int(p.r_pad / tile), ts = int(p.s_pad / tile);
+      const TileGrid g = ph == 2 ? TileGrid{tr, ts, false} : TileGrid{tr, tr, true};
+      grids.push_back(g);
+      pos.push_back(k);
+      cost.push_back(ph == 0 ? p.s_pad : p.r_pad);
+      P.tiles[ph] += g.sym ? g.tm * (g.tm + 1) / 2 : g.tm * g.tn;
+    }
+    if (ns_dtype == MFSDP_BF16) P.sched[ph] = build_schedule(pos, grids, cost);
+    sched_bytes[ph] = P.sched[ph].size() * sizeof(TileRef);
+  }
+  P.dl = plan_descs(count, sched_bytes);
+  for (int ph = 0; ph < 3; ++ph) P.dl.ngroups[ph] = int(P.sched[ph].size() / kGemmSlots);
+  size_t o = P.dl.bytes;
+  for (int64_t i = 0; i < count; ++i) {
+    P.ns.push_back(plan_ns(shapes[i].m, shapes[i].n, ns_dtype, o));
+    o += P.ns.back().bytes;
+  }
+  P.bytes = o;
+  return P;
+}
+
+// Descriptors of the three products, stored in the phase's problem order; the schedules refer
+// to problems by that position.
+void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, uint8_t* h, int tile) {
+  const int n = int(P.ns.size());
+  for (int phase = 0; phase < 3; ++phase) {
+    GemmDesc* out = reinterpret_cast<GemmDesc*>(h + P.dl.off_gemm[phase]);
+    const std::vector<int>& ord = P.order[phase];
     int begin = 0;
     for (int k = 0; k < n; ++k) {
-      const NsPlan& p = plans[ord[k]];
+      const NsPlan& p = P.ns[ord[k]];
       GemmDesc d{};
       const int tr = int(p.r_pad / tile), ts = int(p.s_pad / tile);
       for (int par = 0; par < 2; ++par) {
@@ -287,11 +394,10 @@ void fill_gemm_descs(const std::vector<NsPlan>& plans, uint8_t* ws, const mfsdp_
       begin += d.tile_count;
       out[k] = d;
     }
-    *total = begin;
-  };
-  fill(syrk, 0, tiles_syrk);
-  fill(sqr, 1, tiles_sqr);
-  fill(upd, 2, tiles_upd);
+    if (!P.sched[phase].empty())
+      std::memcpy(h + P.dl.off_sched[phase], P.sched[phase].data(),
+                  P.sched[phase].size() * sizeof(TileRef));
+  }
 }
 
 PrepDesc make_prep(const NsPlan& p, uint8_t* ws, const void* grad, int grad_dtype, float* momentum,
@@ -339,18 +445,6 @@ ApplyDesc make_apply(const NsPlan& p, uint8_t* ws, int steps, void* param, int p
   return d;
 }
 
-size_t muon_ws_bytes(const mfsdp_muon_entry* entries, int64_t count, int ns_dtype,
-                     std::vector<NsPlan>* plans) {
-  const DescLayout dl = plan_descs(count);
-  size_t o = dl.bytes;
-  for (int64_t i = 0; i < count; ++i) {
-    NsPlan p = plan_ns(entries[i].m, entries[i].n, ns_dtype, o);
-    o += p.bytes;
-    if (plans) plans->push_back(p);
-  }
-  return o;
-}
-
 // Enqueue everything after the descriptors are in host staging memory `h`.
 int record(void* const* events, int k, hipStream_t st) {
   if (!events || !events[k]) return MFSDP_OK;
@@ -358,11 +452,11 @@ int record(void* const* events, int k, hipStream_t st) {
   return e == hipSuccess ? MFSDP_OK : hip_fail(e, "hipEventRecord");
 }
 
-int enqueue_pipeline(const std::vector<NsPlan>& plans, uint8_t* ws, const DescLayout& dl,
-                     int slot, int steps, int ns_dtype, double beta, int nesterov, double eps,
-                     int prep_tiles, int apply_tiles, int t0, int t1, int t2, hipStream_t st,
+int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dtype, double beta,
+                     int nesterov, double eps, int prep_tiles, int apply_tiles, hipStream_t st,
                      void* const* events) {
-  const int count = int(plans.size());
+  const int count = int(P.ns.size());
+  const DescLayout& dl = P.dl;
   int rc = ring().upload(slot, ws, dl.bytes, st);
   if (rc) return rc;
   if ((rc = record(events, 0, st))) return rc;
@@ -373,10 +467,10 @@ int enqueue_pipeline(const std::vector<NsPlan>& plans, uint8_t* ws, const DescLa
   e = launch_norm(reinterpret_cast<const NormDesc*>(ws + dl.off_norm), count, float(eps), st);
   if (e != hipSuccess) return hip_fail(e, "norm launch");
   if ((rc = record(events, 1, st))) return rc;
-  const int tiles[3] = {t0, t1, t2};
   for (int k = 0; k < steps; ++k) {
     for (int ph = 0; ph < 3; ++ph) {
-      e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, tiles[ph],
+      e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, P.tiles[ph],
+                      reinterpret_cast<const TileRef*>(ws + dl.off_sched[ph]), dl.ngroups[ph],
                       ns_dtype, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0, st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
@@ -411,7 +505,10 @@ size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,
   g_last_error.clear();
   if (check_hp(hp) || check_entries(entries, count)) return 0;
   if (count == 0) return 0;
-  return muon_ws_bytes(entries, count, hp->ns_dtype, nullptr);
+  return make_plan(count, hp->ns_dtype, [&](int64_t i, int64_t& m, int64_t& n) {
+           m = entries[i].m;
+           n = entries[i].n;
+         }).bytes;
 }
 
 int mfsdp_muon_step(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
@@ -428,8 +525,12 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
   rc = check_entries(entries, count);
   if (rc) return rc;
   if (count == 0) return MFSDP_OK;
-  std::vector<NsPlan> plans;
-  const size_t need = muon_ws_bytes(entries, count, hp->ns_dtype, &plans);
+  const Plan P = make_plan(count, hp->ns_dtype, [&](int64_t i, int64_t& m, int64_t& n) {
+    m = entries[i].m;
+    n = entries[i].n;
+  });
+  const std::vector<NsPlan>& plans = P.ns;
+  const size_t need = P.bytes;
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return fail(MFSDP_E_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
   if (workspace_bytes < need)
@@ -437,7 +538,7 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  const DescLayout dl = plan_descs(count);
+  const DescLayout& dl = P.dl;
   void* hptr = nullptr;
   const int slot = ring().acquire(dl.bytes, &hptr, st);
   if (slot < 0) return slot;
@@ -462,20 +563,16 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
     apply_tiles += apply[i].tiles_m * apply[i].tiles_n;
   }
   const int tile = hp->ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
-  int t0 = 0, t1 = 0, t2 = 0;
-  fill_gemm_descs(plans, ws, *hp, reinterpret_cast<GemmDesc*>(h + dl.off_gemm[0]),
-                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[1]),
-                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[2]), tile, &t0, &t1, &t2);
-  return enqueue_pipeline(plans, ws, dl, slot, hp->ns_steps, hp->ns_dtype, hp->momentum,
-                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, t0, t1, t2, st, events);
+  fill_gemm_descs(P, ws, *hp, h, tile);
+  return enqueue_pipeline(P, ws, slot, hp->ns_steps, hp->ns_dtype, hp->momentum, hp->nesterov,
+                          hp->eps, prep_tiles, apply_tiles, st, events);
 }
 
 size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype) {
   g_last_error.clear();
   if (!valid_dtype(ns_dtype)) { fail(MFSDP_E_INVALID, "unknown ns_dtype %d", ns_dtype); return 0; }
   if (check_shape(m, n, "matrix", 0)) return 0;
-  const DescLayout dl = plan_descs(1);
-  return dl.bytes + plan_ns(m, n, ns_dtype, dl.bytes).bytes;
+  return make_plan(1, ns_dtype, [&](int64_t, int64_t& mm, int64_t& nn) { mm = m; nn = n; }).bytes;
 }
 
 int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
@@ -493,9 +590,10 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   if (!(eps > 0.0) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
   if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
     return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
-  const DescLayout dl = plan_descs(1);
-  std::vector<NsPlan> plans{plan_ns(m, n, ns_dtype, dl.bytes)};
-  const size_t need = dl.bytes + plans[0].bytes;
+  const Plan P = make_plan(1, ns_dtype, [&](int64_t, int64_t& mm, int64_t& nn) { mm = m; nn = n; });
+  const DescLayout& dl = P.dl;
+  const std::vector<NsPlan>& plans = P.ns;
+  const size_t need = P.bytes;
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return fail(MFSDP_E_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
   if (workspace_bytes < need)
@@ -520,13 +618,10 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   mfsdp_muon_hparams hp{};
   hp.a = a; hp.b = b; hp.c = c;
   const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
-  int t0 = 0, t1 = 0, t2 = 0;
-  fill_gemm_descs(plans, ws, hp, reinterpret_cast<GemmDesc*>(h + dl.off_gemm[0]),
-                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[1]),
-                  reinterpret_cast<GemmDesc*>(h + dl.off_gemm[2]), tile, &t0, &t1, &t2);
-  return enqueue_pipeline(plans, ws, dl, slot, steps, ns_dtype, 0.0, 0, eps,
-                          p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n,
-                          t0, t1, t2, st, nullptr);
+  fill_gemm_descs(P, ws, hp, h, tile);
+  return enqueue_pipeline(P, ws, slot, steps, ns_dtype, 0.0, 0, eps,
+                          p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n, st,
+                          nullptr);
 }
 
 int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,

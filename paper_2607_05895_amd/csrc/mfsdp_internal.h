@@ -70,6 +70,18 @@ struct GemmDesc {
   int32_t last_c, last_ct;  // on the last step: write C / CT (1) or skip (0)
 };
 
+// One output tile of a grouped NS product: problem (matrix) index and 256 x 256 block coordinates;
+// e < 0 marks an idle slot. The bf16 NS kernels run a persistent grid of kGemmXcds x
+// kGemmSlots workgroups; workgroup b serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes
+// tile sched[g * kGemmSlots + slot] of every group g = xcd, xcd + kGemmXcds, ...
+struct TileRef {
+  int32_t e;
+  int16_t bi, bj;
+};
+constexpr int kGemmXcds = 8;    // MI355X: 8 XCDs (workgroups are dealt to them round robin)
+constexpr int kGemmSlots = 32;  // CUs per XCD = tiles per group
+constexpr int kGroupRows = 4;   // a group covers 4 block rows x 8 block columns of one matrix
+
 // apply: p <- p (1 - lr wd) - lr f (oscale O), or out <- oscale O for standalone NS.
 struct ApplyDesc {
   const void* o;         // O in stored orientation (ns dtype), ld_o
@@ -112,8 +124,9 @@ constexpr int kAdamWBlockElems = 4096;
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
                        float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
-hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       int parity, int first_step, int last_step, hipStream_t st);
+hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
+                       int ngroups, int ns_dtype, int parity, int first_step, int last_step,
+                       hipStream_t st);
 hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
                         hipStream_t st);
 hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);
