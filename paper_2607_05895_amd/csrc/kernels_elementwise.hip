@@ -206,7 +206,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
     }
 #pragma unroll
     for (int k = 0; k < 8; ++k) ss += u.v[k] * u.v[k];
-    store8<NSDT>(d.d_out, i * d.ld_d + j0, u);
+    store8<NSDT>(d.d_out, blk_index(i, j0, d.ld_d), u);
     // LDS copy (rounded to the NS dtype exactly as the global one)
     T* trow = tile + ti * TW + (c8 ^ (8 * ((ti >> 3) & 7)));
     if constexpr (NSDT == kDtBF16) {
@@ -228,7 +228,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
 #pragma unroll
     for (int q = 0; q < TW / 32; ++q) {
       const int jj = (t >> 3) + 32 * q;
-      T* dst = static_cast<T*>(d.t_out) + (col0 + jj) * d.ld_t + row0 + 8 * mm;
+      T* dst = static_cast<T*>(d.t_out) + blk_index(col0 + jj, row0 + 8 * mm, d.ld_t);
       if constexpr (NSDT == kDtBF16) {
         uint32_t h[8];
 #pragma unroll
@@ -297,7 +297,7 @@ __global__ __launch_bounds__(256) void apply_kernel(const ApplyDesc* __restrict_
     const int64_t j0 = col0 + c8;
     if (i >= m || j0 >= n) continue;
     V8 o;
-    load8<NSDT, true>(d.o, i * d.ld_o + j0, o);  // j0 < n: the padded O row holds these 8 columns
+    load8<NSDT, true>(d.o, blk_index(i, j0, d.ld_o), o);  // j0 < n: the padded O row holds these 8 columns
 #pragma unroll
     for (int k = 0; k < 8; ++k) o.v[k] *= osc;
     const int64_t idx = i * n + j0;

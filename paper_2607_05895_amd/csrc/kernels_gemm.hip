@@ -1,15 +1,16 @@
 // Newton-Schulz products on gfx950.
 //
 // Every product of the quintic step is computed as one grouped "NT" GEMM
-//     C = alpha * P Q^T + beta * E        (P: M x K, Q: N x K, both row-major, K-contiguous)
-// over all matrices of the owner in one launch (one problem per matrix, tiles of all problems
-// enumerated heaviest-K first). Symmetric products (A = X X^T and A A) compute only the tiles on
-// and above the diagonal and store each off-diagonal tile twice (as is and transposed).
+//     C = alpha * P Q^T + beta * E        (P: M x K, Q: N x K, both K-contiguous, panel blocked)
+// over all matrices of the owner in one launch (one problem per matrix). Symmetric products
+// (A = X X^T and B' = c A A + b A + a I) compute only the tiles on and above the diagonal and
+// store each off-diagonal tile twice (as is and transposed).
 //
-// bf16 path: 256 x 256 output tile per workgroup of 4 waves (2 x 2), 128 x 128 per wave as 4 x 4
-// v_mfma_f32_32x32x16_bf16 blocks with fp32 accumulation; K step 64 staged through LDS (two
-// stages of 64 KiB) with an XOR swizzle of 16-byte chunks so that fragment reads are free of bank
-// conflicts. The next K step's global loads are in flight while the current one is multiplied.
+// bf16 path: a persistent grid of one workgroup per CU (8 waves) walks a host-built tile schedule
+// (TileRef); each 256 x 256 output tile is 2 x 4 waves of 128 x 64, as 4 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulation. K advances 32 elements per step through a
+// five-stage LDS ring filled by direct global->LDS loads; the next tile's first loads overlap the
+// current tile's epilogue.
 // fp32 path: 64 x 64 tiles on the vector ALUs (a correctness path for fp32 NS).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -158,16 +159,16 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       c.nk = dd.K / BKE;
       const uint16_t* P = static_cast<const uint16_t*>(dd.P[parity]);
       const uint16_t* Q = static_cast<const uint16_t*>(dd.Q[parity]);
-      c.psrc = P + (int64_t(c.bi) * BT + drow) * dd.ldp + dchunk * 8;
-      c.qsrc = Q + (int64_t(c.bj) * BT + drow) * dd.ldq + dchunk * 8;
-      c.pstep = int64_t(NW * 16) * dd.ldp;
-      c.qstep = int64_t(NW * 16) * dd.ldq;
+      c.psrc = P + blk_index(int64_t(c.bi) * BT + drow, dchunk * 8, dd.ldp);
+      c.qsrc = Q + blk_index(int64_t(c.bj) * BT + drow, dchunk * 8, dd.ldq);
+      c.pstep = int64_t(NW * kBlkRows) * dd.ldp;  // NW row panels further down
+      c.qstep = int64_t(NW * kBlkRows) * dd.ldq;
       return true;
     }
     return false;
   };
   auto issue = [&](const TileCtx& c, int kt, int stage) {
-    const int64_t koff = int64_t(kt) * BKE;
+    const int64_t koff = int64_t(kt) * (kBlkRows * BKE);  // next 16 x 32 block of the panel
     lds_byte* sb = (lds_byte*)(smem + stage * STAGE_BYTES + dma_wave_off);
 #pragma unroll
     for (int i = 0; i < PL; ++i)
@@ -313,7 +314,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
           float v2 = alpha * acc[mi][ni][4 * gg + 2];
           float v3 = alpha * acc[mi][ni][4 * gg + 3];
           if (E) {
-            const uint2 ev = *reinterpret_cast<const uint2*>(E + i * lde + j);
+            const uint2 ev = *reinterpret_cast<const uint2*>(E + blk_index(i, j, lde));
             v0 += beta * __uint_as_float(ev.x << 16);
             v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
             v2 += beta * __uint_as_float(ev.y << 16);
@@ -325,7 +326,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
             if (i == j + 2) v2 += diag;
             if (i == j + 3) v3 += diag;
           }
-          if (C) *reinterpret_cast<uint2*>(C + i * ldc + j) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          if (C) *reinterpret_cast<uint2*>(C + blk_index(i, j, ldc)) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
           if (TD) {
             // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
             {
@@ -340,7 +341,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
               if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
             }
             // lane q now holds column j + q at rows iq .. iq + 3
-            *reinterpret_cast<uint2*>(TD + (j + q) * ldtd + iq) =
+            *reinterpret_cast<uint2*>(TD + blk_index(j + q, iq, ldtd)) =
                 make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
           }
         }
@@ -370,12 +371,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
   const int t = threadIdx.x;
   const int tx = t & 15, ty = t >> 4;
   const int lr = t >> 2, lk = (t & 3) * 4;
-  const float* psrc = P + (int64_t(bi) * 64 + lr) * dd.ldp + lk;
-  const float* qsrc = Q + (int64_t(bj) * 64 + lr) * dd.ldq + lk;
+  const int64_t prow = int64_t(bi) * 64 + lr, qrow = int64_t(bj) * 64 + lr;
   float acc[4][4] = {};
   for (int k0 = 0; k0 < dd.K; k0 += 16) {
-    const float4 pv = *reinterpret_cast<const float4*>(psrc + k0);
-    const float4 qv = *reinterpret_cast<const float4*>(qsrc + k0);
+    const float4 pv = *reinterpret_cast<const float4*>(P + blk_index(prow, k0 + lk, dd.ldp));
+    const float4 qv = *reinterpret_cast<const float4*>(Q + blk_index(qrow, k0 + lk, dd.ldq));
     Ps[lk + 0][lr] = pv.x; Ps[lk + 1][lr] = pv.y; Ps[lk + 2][lr] = pv.z; Ps[lk + 3][lr] = pv.w;
     Qs[lk + 0][lr] = qv.x; Qs[lk + 1][lr] = qv.y; Qs[lk + 2][lr] = qv.z; Qs[lk + 3][lr] = qv.w;
     __syncthreads();
@@ -409,7 +409,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
 #pragma unroll
     for (int c = 0; c < 4; ++c) v[c] = alpha * acc[r][c];
     if (E) {
-      const float4 ev = *reinterpret_cast<const float4*>(E + i * dd.lde + j);
+      const float4 ev = *reinterpret_cast<const float4*>(E + blk_index(i, j, dd.lde));
       v[0] += beta * ev.x; v[1] += beta * ev.y; v[2] += beta * ev.z; v[3] += beta * ev.w;
     }
     if (dd.sym && bi == bj)
@@ -417,14 +417,14 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
       for (int c = 0; c < 4; ++c)
         if (i == j + c) v[c] += dd.diag;
     if (C) {
-      *reinterpret_cast<float4*>(C + i * dd.ldc + j) = make_float4(v[0], v[1], v[2], v[3]);
+      *reinterpret_cast<float4*>(C + blk_index(i, j, dd.ldc)) = make_float4(v[0], v[1], v[2], v[3]);
       if (mirror)
 #pragma unroll
-        for (int c = 0; c < 4; ++c) C[(j + c) * dd.ldc + i] = v[c];
+        for (int c = 0; c < 4; ++c) C[blk_index(j + c, i, dd.ldc)] = v[c];
     }
     if (CT)
 #pragma unroll
-      for (int c = 0; c < 4; ++c) CT[(j + c) * dd.ldct + i] = v[c];
+      for (int c = 0; c < 4; ++c) CT[blk_index(j + c, i, dd.ldct)] = v[c];
   }
 }
 

@@ -2,25 +2,38 @@
 //
 // Data layout in HBM for one Muon entry with stored shape m x n (r = min, s = max):
 //   the NS iterate is kept in both layouts, zero padded to the NS tile size:
-//     X[0], X[1]   r_pad x s_pad row-major   (ld = s_pad)   -- ping-pong over NS steps
-//     XT[0], XT[1] s_pad x r_pad row-major   (ld = r_pad)   -- X^T of the same iterate
-//     G            r_pad x r_pad             A = X X^T (symmetric)
-//     H            r_pad x r_pad             B = b A + c A A (symmetric)
+//     X[0], X[1]   r_pad x s_pad   (K = s_pad columns)   -- ping-pong over NS steps
+//     XT[0], XT[1] s_pad x r_pad   (K = r_pad)           -- X^T of the same iterate
+//     G            r_pad x r_pad   A = X X^T (symmetric)
+//     H            r_pad x r_pad   B' = b A + c A A + a I (symmetric)
 //   Zero padding is exact for the iteration: padded rows/columns of X give zero rows/columns of
-//   A and B, and stay zero in a X + B X.
+//   A and B', and stay zero in B' X.
 //   Every NS product is then an "NT" product C = P Q^T with both operands K-contiguous:
 //     Gram      A = X X^T             P = Q = X,  K = s_pad
 //     square    A A = A A^T           P = Q = A,  K = r_pad   (A symmetric)
-//     update    B X = B (X^T)^T       P = B, Q = X^T, K = r_pad
+//     update    B' X = B' (X^T)^T     P = B', Q = X^T, K = r_pad
 //   The square product stores B' = c A A + b A + a I, so the update X' = a X + B X = B' X is a plain
 //   product with no addend. It writes X' in both layouts so the next step again reads
 //   K-contiguous operands.
+//
+//   All of these buffers are panel blocked (blk_index below): rows in blocks of 16, columns in
+//   blocks of 32, each 16 x 32 block contiguous (1 KiB in bf16), the blocks of one 16-row panel
+//   following each other along K. One K step of a 16-row slice of an operand is then one
+//   contiguous KiB, which the GEMM's direct-to-LDS loads fetch as eight whole 128-B lines.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace mfsdp {
+
+// Element (r, k) of a panel-blocked buffer with K columns (K a multiple of 32, rows a multiple of
+// 16). Eight consecutive k starting at a multiple of 8 are contiguous.
+constexpr int kBlkRows = 16;
+constexpr int kBlkCols = 32;
+__host__ __device__ constexpr int64_t blk_index(int64_t r, int64_t k, int64_t K) {
+  return (r >> 4) * (K << 4) + ((k >> 5) << 9) + ((r & 15) << 5) + (k & 31);
+}
 
 constexpr int kDtF32 = 0;
 constexpr int kDtBF16 = 1;
@@ -31,8 +44,8 @@ constexpr int kDtBF16 = 1;
 struct PrepDesc {
   const void* grad;      // m x n, grad_dtype (the NS input for standalone NS)
   float* momentum;       // m x n fp32, or null for standalone NS
-  void* d_out;           // u in stored orientation, padded rows x cols, ld_d (ns dtype)
-  void* t_out;           // u^T, ld_t (ns dtype)
+  void* d_out;           // u in stored orientation, padded, panel blocked with ld_d columns
+  void* t_out;           // u^T, panel blocked with ld_t columns (ns dtype)
   float* partials;       // one Sum u^2 per tile
   int64_t m, n;          // stored shape
   int64_t ld_d, ld_t;
@@ -48,8 +61,8 @@ struct NormDesc {
   float* scale;
 };
 
-// Grouped NT GEMM problem: C = alpha * P Q^T + beta * E, stored row-major in C and/or
-// transposed in CT. Both ping-pong alternatives are kept, indexed by step parity.
+// Grouped NT GEMM problem: C = alpha * P Q^T + beta * E, stored in C and/or transposed in CT.
+// Every operand is panel blocked; the ld* fields are the column counts. Both ping-pong alternatives are kept, indexed by step parity.
 struct GemmDesc {
   const void* P[2];
   const void* Q[2];
@@ -84,7 +97,7 @@ constexpr int kGroupRows = 4;   // a group covers 4 block rows x 8 block columns
 
 // apply: p <- p (1 - lr wd) - lr f (oscale O), or out <- oscale O for standalone NS.
 struct ApplyDesc {
-  const void* o;         // O in stored orientation (ns dtype), ld_o
+  const void* o;         // O in stored orientation (ns dtype), panel blocked with ld_o columns
   void* param;           // m x n, param dtype (or NS output)
   float* update_out;     // optional fp32 m x n
   const float* scale;    // norm scale, applied when no NS step ran (K = 0)
