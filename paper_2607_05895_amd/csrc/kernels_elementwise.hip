@@ -13,13 +13,7 @@ namespace {
 
 __device__ __forceinline__ float bf2f(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  // round to nearest even; NaN stays NaN (quiet bit set)
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
-}
+__device__ __forceinline__ uint16_t f2bf(float f) { return uint16_t(pack_bf16x2(f, 0.0f)); }
 
 __device__ __forceinline__ float load_as_f32(const void* p, int64_t i, int dt) {
   return dt == kDtBF16 ? bf2f(static_cast<const uint16_t*>(p)[i]) : static_cast<const float*>(p)[i];
@@ -30,33 +24,6 @@ __device__ __forceinline__ void store_from_f32(void* p, int64_t i, float v, int 
     static_cast<uint16_t*>(p)[i] = f2bf(v);
   else
     static_cast<float*>(p)[i] = v;
-}
-
-// Store 4 consecutive values (16-byte aligned fp32 or 8-byte aligned bf16 destination).
-template <int DT>
-__device__ __forceinline__ void store4(void* base, int64_t idx, const float v[4]) {
-  if constexpr (DT == kDtBF16) {
-    uint2 w;
-    w.x = uint32_t(f2bf(v[0])) | (uint32_t(f2bf(v[1])) << 16);
-    w.y = uint32_t(f2bf(v[2])) | (uint32_t(f2bf(v[3])) << 16);
-    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(base) + idx) = w;
-  } else {
-    *reinterpret_cast<float4*>(static_cast<float*>(base) + idx) = make_float4(v[0], v[1], v[2], v[3]);
-  }
-}
-
-template <int DT>
-__device__ __forceinline__ void load4(const void* base, int64_t idx, float v[4]) {
-  if constexpr (DT == kDtBF16) {
-    uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(base) + idx);
-    v[0] = __uint_as_float(w.x << 16);
-    v[1] = __uint_as_float(w.x & 0xffff0000u);
-    v[2] = __uint_as_float(w.y << 16);
-    v[3] = __uint_as_float(w.y & 0xffff0000u);
-  } else {
-    float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + idx);
-    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-  }
 }
 
 // Entry lookup: the largest i with begin(i) <= key (begins are increasing, begin(0) = 0).
@@ -81,15 +48,22 @@ __device__ __forceinline__ float wave_sum(float v) {
 // help the parameter-update pass and to hurt the momentum pass).
 struct V8 { float v[8]; };
 
+// Every buffer here is device memory; accessing it through global-address-space pointers gives
+// global_load/global_store instead of flat instructions (which also count against lgkmcnt).
+template <typename V>
+using gptr = __attribute__((address_space(1))) V*;
+
 template <bool NT, typename V>
 __device__ __forceinline__ V ld_stream(const V* p) {
-  if constexpr (NT) return __builtin_nontemporal_load(p);
-  else return *p;
+  const gptr<const V> g = (gptr<const V>)p;
+  if constexpr (NT) return __builtin_nontemporal_load(g);
+  else return *g;
 }
 template <bool NT, typename V>
 __device__ __forceinline__ void st_stream(V* p, V v) {
-  if constexpr (NT) __builtin_nontemporal_store(v, p);
-  else *p = v;
+  const gptr<V> g = (gptr<V>)p;
+  if constexpr (NT) __builtin_nontemporal_store(v, g);
+  else *g = v;
 }
 
 template <int DT, bool NT = false>
@@ -117,10 +91,10 @@ __device__ __forceinline__ void store8(void* base, int64_t idx, const V8& x) {
   if constexpr (DT == kDtBF16) {
     typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
     u32x4 w;
-    w.x = uint32_t(f2bf(x.v[0])) | (uint32_t(f2bf(x.v[1])) << 16);
-    w.y = uint32_t(f2bf(x.v[2])) | (uint32_t(f2bf(x.v[3])) << 16);
-    w.z = uint32_t(f2bf(x.v[4])) | (uint32_t(f2bf(x.v[5])) << 16);
-    w.w = uint32_t(f2bf(x.v[6])) | (uint32_t(f2bf(x.v[7])) << 16);
+    w.x = pack_bf16x2(x.v[0], x.v[1]);
+    w.y = pack_bf16x2(x.v[2], x.v[3]);
+    w.z = pack_bf16x2(x.v[4], x.v[5]);
+    w.w = pack_bf16x2(x.v[6], x.v[7]);
     st_stream<NT>(reinterpret_cast<u32x4*>(static_cast<uint16_t*>(base) + idx), w);
   } else {
     typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -163,47 +137,12 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
   const int c8 = (t % CPR) * 8, rr = t / CPR;
   float ss = 0.0f;
   const bool vec = (n % 8 == 0);
-#pragma unroll
-  for (int q = 0; q < 64 / RPP; ++q) {
+  constexpr int NP = 64 / RPP;         // passes over the tile rows
+  // u of pass q: to the stored-orientation buffer and to the LDS tile
+  auto emit = [&](int q, const V8& u) {
     const int ti = rr + RPP * q;
     const int64_t i = row0 + ti;
     const int64_t j0 = col0 + c8;
-    V8 u;
-    if (i < m && vec && j0 + 7 < n) {
-      const int64_t idx = i * n + j0;
-      V8 g;
-      if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, idx, g); else load8<kDtF32>(d.grad, idx, g);
-      if (d.momentum) {
-        V8 mv;
-        load8<kDtF32>(d.momentum, idx, mv);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          mv.v[k] = mv.v[k] + omb * (g.v[k] - mv.v[k]);
-          u.v[k] = nesterov ? g.v[k] + beta * (mv.v[k] - g.v[k]) : mv.v[k];
-        }
-        store8<kDtF32>(d.momentum, idx, mv);
-      } else {
-        u = g;
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int64_t j = j0 + k;
-        u.v[k] = 0.0f;
-        if (i < m && j < n) {
-          const int64_t idx = i * n + j;
-          const float g = load_as_f32(d.grad, idx, d.grad_dtype);
-          if (d.momentum) {
-            float mv = d.momentum[idx];
-            mv = mv + omb * (g - mv);
-            d.momentum[idx] = mv;
-            u.v[k] = nesterov ? g + beta * (mv - g) : mv;
-          } else {
-            u.v[k] = g;
-          }
-        }
-      }
-    }
 #pragma unroll
     for (int k = 0; k < 8; ++k) ss += u.v[k] * u.v[k];
     store8<NSDT>(d.d_out, blk_index(i, j0, d.ld_d), u);
@@ -211,14 +150,86 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
     T* trow = tile + ti * TW + (c8 ^ (8 * ((ti >> 3) & 7)));
     if constexpr (NSDT == kDtBF16) {
       uint4 w;
-      w.x = uint32_t(f2bf(u.v[0])) | (uint32_t(f2bf(u.v[1])) << 16);
-      w.y = uint32_t(f2bf(u.v[2])) | (uint32_t(f2bf(u.v[3])) << 16);
-      w.z = uint32_t(f2bf(u.v[4])) | (uint32_t(f2bf(u.v[5])) << 16);
-      w.w = uint32_t(f2bf(u.v[6])) | (uint32_t(f2bf(u.v[7])) << 16);
+      w.x = pack_bf16x2(u.v[0], u.v[1]);
+      w.y = pack_bf16x2(u.v[2], u.v[3]);
+      w.z = pack_bf16x2(u.v[4], u.v[5]);
+      w.w = pack_bf16x2(u.v[6], u.v[7]);
       *reinterpret_cast<uint4*>(trow) = w;
     } else {
 #pragma unroll
       for (int k = 0; k < 8; ++k) trow[k] = u.v[k];
+    }
+  };
+  if (vec && row0 + 64 <= m && col0 + TW <= n) {
+    // interior tile: every load of the tile is issued before the first result is formed
+    auto interior = [&](auto gdt) {
+      constexpr int GDT = decltype(gdt)::value;
+      V8 g[NP], mv[NP];
+#pragma unroll
+      for (int q = 0; q < NP; ++q) load8<GDT>(d.grad, (row0 + rr + RPP * q) * n + col0 + c8, g[q]);
+      if (d.momentum) {
+#pragma unroll
+        for (int q = 0; q < NP; ++q) load8<kDtF32>(d.momentum, (row0 + rr + RPP * q) * n + col0 + c8, mv[q]);
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          V8 u;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            mv[q].v[k] = mv[q].v[k] + omb * (g[q].v[k] - mv[q].v[k]);
+            u.v[k] = nesterov ? g[q].v[k] + beta * (mv[q].v[k] - g[q].v[k]) : mv[q].v[k];
+          }
+          store8<kDtF32>(d.momentum, (row0 + rr + RPP * q) * n + col0 + c8, mv[q]);
+          emit(q, u);
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < NP; ++q) emit(q, g[q]);
+      }
+    };
+    if (d.grad_dtype == kDtBF16) interior(std::integral_constant<int, kDtBF16>{});
+    else interior(std::integral_constant<int, kDtF32>{});
+  } else {
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      const int64_t i = row0 + rr + RPP * q;
+      const int64_t j0 = col0 + c8;
+      V8 u;
+      if (i < m && vec && j0 + 7 < n) {
+        const int64_t idx = i * n + j0;
+        V8 g;
+        if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, idx, g); else load8<kDtF32>(d.grad, idx, g);
+        if (d.momentum) {
+          V8 mv;
+          load8<kDtF32>(d.momentum, idx, mv);
+#pragma unroll
+          for (int k = 0; k < 8; ++k) {
+            mv.v[k] = mv.v[k] + omb * (g.v[k] - mv.v[k]);
+            u.v[k] = nesterov ? g.v[k] + beta * (mv.v[k] - g.v[k]) : mv.v[k];
+          }
+          store8<kDtF32>(d.momentum, idx, mv);
+        } else {
+          u = g;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int64_t j = j0 + k;
+          u.v[k] = 0.0f;
+          if (i < m && j < n) {
+            const int64_t idx = i * n + j;
+            const float g = load_as_f32(d.grad, idx, d.grad_dtype);
+            if (d.momentum) {
+              float mv = d.momentum[idx];
+              mv = mv + omb * (g - mv);
+              d.momentum[idx] = mv;
+              u.v[k] = nesterov ? g + beta * (mv - g) : mv;
+            } else {
+              u.v[k] = g;
+            }
+          }
+        }
+      }
+      emit(q, u);
     }
   }
   __syncthreads();

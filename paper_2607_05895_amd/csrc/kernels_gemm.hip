@@ -23,16 +23,6 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  auto cvt = [](float f) -> uint32_t {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return u >> 16;
-  };
-  return cvt(lo) | (cvt(hi) << 16);
-}
-
 // DPP quad permutations: lane i of each group of 4 reads lane i ^ 1 (quad_perm [1,0,3,2]) or
 // lane i ^ 2 (quad_perm [2,3,0,1]).
 __device__ __forceinline__ float dpp_quad_xor1(float v) {
@@ -96,6 +86,10 @@ constexpr int STAGE_BYTES = 2 * BT * ROWB;   // 32 KiB
 constexpr int NSTAGE = 5;                    // 160 KiB of LDS
 
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
+// global-address-space element types (pointers derived from these give global_* instructions)
+typedef __attribute__((address_space(1))) uint16_t gu16;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) u32x2 gu2;
 
 __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((r >> 2) & 1) << 1); }
 
@@ -276,7 +270,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     __builtin_amdgcn_s_barrier();
     if (has_next) prologue(nxt);  // overlaps the epilogue below
 
-    // Epilogue. acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
+    // Epilogue (global-address-space accesses: flat ones would also hold lgkmcnt, which the next
+    // tile's LDS reads wait on). acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
     // j = j0 + 8 g + 4 (lane / 32) + t for element v = 4 g + t: each lane has 4 consecutive columns
     // of one row per group g (one 8-byte row-major store). For the transposed stores (X'^T, and the
     // mirrored tile of a symmetric product) the 4 x 4 blocks held by lane quads are transposed with
@@ -287,15 +282,15 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
     const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
     const float diag = (dd.sym && bi == bj) ? dd.diag : 0.0f;
-    const uint16_t* E = static_cast<const uint16_t*>(dd.E[parity]);
-    uint16_t* C = static_cast<uint16_t*>(dd.C[parity]);
-    uint16_t* CT = static_cast<uint16_t*>(dd.CT[parity]);
+    const gu16* E = (const gu16*)dd.E[parity];
+    gu16* C = (gu16*)dd.C[parity];
+    gu16* CT = (gu16*)dd.CT[parity];
     if (last) {
       if (!dd.last_c) C = nullptr;
       if (!dd.last_ct) CT = nullptr;
     }
     // transposed destination: the mirror tile of a symmetric product, or X'^T
-    uint16_t* TD = (dd.sym && bi != bj && C) ? C : CT;
+    gu16* TD = (dd.sym && bi != bj && C) ? C : CT;
     const int64_t ldtd = (TD == C) ? dd.ldc : dd.ldct;
     const int64_t lde = dd.lde, ldc = dd.ldc;
     const int q = lane & 3;
@@ -314,7 +309,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
           float v2 = alpha * acc[mi][ni][4 * gg + 2];
           float v3 = alpha * acc[mi][ni][4 * gg + 3];
           if (E) {
-            const uint2 ev = *reinterpret_cast<const uint2*>(E + blk_index(i, j, lde));
+            const u32x2 ev = *(const gu2*)(E + blk_index(i, j, lde));
             v0 += beta * __uint_as_float(ev.x << 16);
             v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
             v2 += beta * __uint_as_float(ev.y << 16);
@@ -326,7 +321,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
             if (i == j + 2) v2 += diag;
             if (i == j + 3) v3 += diag;
           }
-          if (C) *reinterpret_cast<uint2*>(C + blk_index(i, j, ldc)) = make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+          if (C)
+            *(gu2*)(C + blk_index(i, j, ldc)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
           if (TD) {
             // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
             {
@@ -341,8 +337,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
               if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
             }
             // lane q now holds column j + q at rows iq .. iq + 3
-            *reinterpret_cast<uint2*>(TD + blk_index(j + q, iq, ldtd)) =
-                make_uint2(pack_bf16x2(v0, v1), pack_bf16x2(v2, v3));
+            *(gu2*)(TD + blk_index(j + q, iq, ldtd)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
           }
         }
       }

@@ -35,6 +35,13 @@ __host__ __device__ constexpr int64_t blk_index(int64_t r, int64_t k, int64_t K)
   return (r >> 4) * (K << 4) + ((k >> 5) << 9) + ((r & 15) << 5) + (k & 31);
 }
 
+// Two floats to packed bf16 (lo in bits 0..15), round to nearest even, one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
+}
+
 constexpr int kDtF32 = 0;
 constexpr int kDtBF16 = 1;
 
