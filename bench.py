@@ -223,6 +223,8 @@ def main() -> int:
     adamw_ms = (sum(hev.elapsed_ms(e[4], e[5]) for e in ev) / n_ev) if aents else 0.0
     log(f"step {ms_per_step:.3f} ms: prep+norm {prep_ms:.3f}, NS {ns_ms:.3f}, apply {apply_ms:.3f}, "
         f"AdamW {adamw_ms:.3f}")
+    if hp.ns_dtype == synth.BF16 and hp.ns_steps >= 1:
+        apply_ms = 0.0  # the events around the (absent) apply pass bracket no kernel
 
     flops = wl.ns_flops_nominal()
     launches = 3 * hp.ns_steps
@@ -233,7 +235,9 @@ def main() -> int:
     es_p = 2 if all(e.param_dtype == synth.BF16 for e in wl.muon) else 4
     es_ns = 2 if hp.ns_dtype == synth.BF16 else 4
     prep_bytes = elts * (es_g + 4 + 4 + 2 * es_ns)       # g, m in/out, u and u^T
-    apply_bytes = elts * (es_ns + 2 * es_p)               # O, p in/out
+    # on the bf16 path the parameter update runs in the last NS update's epilogue (no apply pass)
+    apply_fused = hp.ns_dtype == synth.BF16 and hp.ns_steps >= 1
+    apply_bytes = 0 if apply_fused else elts * (es_ns + 2 * es_p)   # O, p in/out
     alg_bytes = elts * (es_g + 8 + 2 * es_p)              # g, m in/out, p in/out
     adamw_bytes = sum(e.numel * ({"bf16": 2, "f32": 4}[e.param_dtype] * 2 +
                                  {"bf16": 2, "f32": 4}[e.grad_dtype] + 16) for e in wl.adamw)
@@ -277,9 +281,11 @@ def main() -> int:
                       "apply": round(apply_ms, 4), "adamw": round(adamw_ms, 4)},
         "elementwise": {
             "prep_GBps": round(prep_bytes / (prep_ms * 1e-3) / 1e9, 1) if prep_ms else None,
-            "apply_GBps": round(apply_bytes / (apply_ms * 1e-3) / 1e9, 1) if apply_ms else None,
-            "muon_elementwise_frac_hbm": round((prep_bytes + apply_bytes) / ((prep_ms + apply_ms) * 1e-3) / 1e9
-                                               / PEAK_HBM_GBS, 4) if (prep_ms + apply_ms) else None,
+            "apply_fused_into_ns": apply_fused,
+            "apply_GBps": (round(apply_bytes / (apply_ms * 1e-3) / 1e9, 1)
+                           if apply_ms and not apply_fused else None),
+            "muon_elementwise_frac_hbm": (round((prep_bytes + apply_bytes) / ((prep_ms + apply_ms) * 1e-3) / 1e9
+                                                / PEAK_HBM_GBS, 4) if (prep_ms + apply_ms) else None),
             "muon_algorithmic_bytes": alg_bytes,
             "adamw_GBps": round(adamw_bytes / (adamw_ms * 1e-3) / 1e9, 1) if adamw_ms else None,
         },

@@ -15,6 +15,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+#include <utility>
+
 #include "mfsdp_internal.h"
 
 namespace mfsdp {
@@ -22,6 +25,20 @@ namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+// global-address-space element types (pointers derived from these give global_* instructions)
+typedef __attribute__((address_space(1))) uint16_t gu16;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) u32x2 gu2;
+
+// f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), unrolled by construction.
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
 
 // DPP quad permutations: lane i of each group of 4 reads lane i ^ 1 (quad_perm [1,0,3,2]) or
 // lane i ^ 2 (quad_perm [2,3,0,1]).
@@ -63,6 +80,54 @@ __device__ __forceinline__ float scale_pow(const float* s, int pw) {
   return pw == 1 ? v : v * v;
 }
 
+// Fused parameter update for 4 consecutive elements (pr, pc .. pc + 3) of the stored m x n
+// parameter, pc a multiple of 4: p <- p (1 - lr wd) - lr f O (mode 0, optionally also writing O to
+// update_out), or p <- O (mode 1, standalone NS output). Elements outside m x n are skipped.
+__device__ __forceinline__ void apply4(const ApplyDesc& a, int64_t pr, int64_t pc, float o0,
+                                       float o1, float o2, float o3) {
+  typedef __attribute__((address_space(1))) float gf32;
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) f32x4 gf4;
+  const int64_t m = a.m, n = a.n;
+  if (pr >= m || pc >= n) return;
+  const int64_t idx = pr * n + pc;
+  const float o[4] = {o0, o1, o2, o3};
+  const bool bf = a.param_dtype == kDtBF16;
+  if ((n & 3) == 0) {  // then pc + 3 < n, and the 4 elements are 8 / 16-byte aligned
+    float r[4] = {o0, o1, o2, o3};
+    if (a.mode == 0) {
+      float p[4];
+      if (bf) {
+        const u32x2 w = *(const gu2*)((const gu16*)a.param + idx);
+        p[0] = __uint_as_float(w.x << 16); p[1] = __uint_as_float(w.x & 0xffff0000u);
+        p[2] = __uint_as_float(w.y << 16); p[3] = __uint_as_float(w.y & 0xffff0000u);
+      } else {
+        const f32x4 w = *(const gf4*)((const gf32*)a.param + idx);
+        p[0] = w.x; p[1] = w.y; p[2] = w.z; p[3] = w.w;
+      }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) r[k] = p[k] * a.decay - a.step * o[k];
+      if (a.update_out) *(gf4*)((gf32*)a.update_out + idx) = f32x4{o0, o1, o2, o3};
+    }
+    if (bf) *(gu2*)((gu16*)a.param + idx) = u32x2{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3])};
+    else *(gf4*)((gf32*)a.param + idx) = f32x4{r[0], r[1], r[2], r[3]};
+  } else {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (pc + k >= n) break;
+      float r = o[k];
+      if (a.mode == 0) {
+        const float p = bf ? __uint_as_float(uint32_t(((const gu16*)a.param)[idx + k]) << 16)
+                           : ((const gf32*)a.param)[idx + k];
+        r = p * a.decay - a.step * o[k];
+        if (a.update_out) ((gf32*)a.update_out)[idx + k] = o[k];
+      }
+      if (bf) ((gu16*)a.param)[idx + k] = uint16_t(pack_bf16x2(r, 0.0f));
+      else ((gf32*)a.param)[idx + k] = r;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------------------------
 // bf16 MFMA kernel
 //
@@ -86,10 +151,6 @@ constexpr int STAGE_BYTES = 2 * BT * ROWB;   // 32 KiB
 constexpr int NSTAGE = 5;                    // 160 KiB of LDS
 
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
-// global-address-space element types (pointers derived from these give global_* instructions)
-typedef __attribute__((address_space(1))) uint16_t gu16;
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(1))) u32x2 gu2;
 
 __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((r >> 2) & 1) << 1); }
 
@@ -285,24 +346,101 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     const gu16* E = (const gu16*)dd.E[parity];
     gu16* C = (gu16*)dd.C[parity];
     gu16* CT = (gu16*)dd.CT[parity];
+    const ApplyDesc* fa = last ? dd.fused : nullptr;
     if (last) {
-      if (!dd.last_c) C = nullptr;
-      if (!dd.last_ct) CT = nullptr;
+      if (!dd.last_c || fa) C = nullptr;
+      if (!dd.last_ct || fa) CT = nullptr;
     }
+    // fused update of a tall parameter: it is X'^T, so it takes the transposed values
+    const bool fa_t = fa && fa->m > fa->n;
     // transposed destination: the mirror tile of a symmetric product, or X'^T
     gu16* TD = (dd.sym && bi != bj && C) ? C : CT;
     const int64_t ldtd = (TD == C) ? dd.ldc : dd.ldct;
     const int64_t lde = dd.lde, ldc = dd.ldc;
     const int q = lane & 3;
     const bool q_odd = q & 1, q_hi = q & 2;
-#pragma unroll
-    for (int mi = 0; mi < MI; ++mi) {
+    // 4 x 4 transpose within each lane quad: afterwards lane q holds column j + q at rows iq .. iq + 3
+    auto quad_transpose = [&](float& v0, float& v1, float& v2, float& v3) {
+      // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
+      {
+        const float x0 = q_odd ? v0 : v1, x1 = q_odd ? v2 : v3;
+        const float y0 = dpp_quad_xor1(x0), y1 = dpp_quad_xor1(x1);
+        if (q_odd) { v0 = y0; v2 = y1; } else { v1 = y0; v3 = y1; }
+      }
+      // exchange across lane ^ 2: low lanes take the partner's elements 0, 1 as their 2, 3
+      {
+        const float x0 = q_hi ? v0 : v2, x1 = q_hi ? v1 : v3;
+        const float y0 = dpp_quad_xor2(x0), y1 = dpp_quad_xor2(x1);
+        if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
+      }
+    };
+    if (fa && fa->param_dtype == kDtBF16 && (fa->n & 3) == 0) {
+      // Fused update of a bf16 parameter with n % 4 == 0: per 32 x 32 block, the parameter values
+      // of its four groups are loaded first (one round trip), then updated and stored.
+      typedef __attribute__((address_space(1))) float gf32;
+      typedef float f32x4 __attribute__((ext_vector_type(4)));
+      typedef __attribute__((address_space(1))) f32x4 gf4;
+      const int64_t fm = fa->m, fn = fa->n;
+      const float decay = fa->decay, stp = fa->step;
+      const int mode = fa->mode;
+      gu16* prm = (gu16*)fa->param;
+      gf32* uo = (gf32*)fa->update_out;
+      static_for<MI>([&](auto mi_c) {
+        constexpr int mi = decltype(mi_c)::value;
+        const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
+        const int64_t iq = i - q;
+        // parameter elements (pr, pc .. pc + 3) this lane owns in group (ni, gg)
+        auto coords = [&](int ni, int gg, int64_t& pr, int64_t& pc) {
+          const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+          if (fa_t) { pr = j + q; pc = iq; } else { pr = i; pc = j; }
+        };
+        static_for<NI>([&](auto ni_c) {
+          constexpr int ni = decltype(ni_c)::value;
+          u32x2 pw[4];
+          static_for<4>([&](auto gg_c) {
+            constexpr int gg = decltype(gg_c)::value;
+            int64_t pr, pc;
+            coords(ni, gg, pr, pc);
+            pw[gg] = u32x2{0u, 0u};
+            if (mode == 0 && pr < fm && pc < fn) pw[gg] = *(const gu2*)(prm + pr * fn + pc);
+          });
+          static_for<4>([&](auto gg_c) {
+            constexpr int gg = decltype(gg_c)::value;
+            float v0 = alpha * acc[mi][ni][4 * gg + 0];
+            float v1 = alpha * acc[mi][ni][4 * gg + 1];
+            float v2 = alpha * acc[mi][ni][4 * gg + 2];
+            float v3 = alpha * acc[mi][ni][4 * gg + 3];
+            if (fa_t) quad_transpose(v0, v1, v2, v3);
+            int64_t pr, pc;
+            coords(ni, gg, pr, pc);
+            if (pr < fm && pc < fn) {
+              float r0 = v0, r1 = v1, r2 = v2, r3 = v3;
+              if (mode == 0) {
+                const u32x2 w = pw[gg];
+                r0 = __uint_as_float(w.x << 16) * decay - stp * v0;
+                r1 = __uint_as_float(w.x & 0xffff0000u) * decay - stp * v1;
+                r2 = __uint_as_float(w.y << 16) * decay - stp * v2;
+                r3 = __uint_as_float(w.y & 0xffff0000u) * decay - stp * v3;
+                if (uo) *(gf4*)(uo + pr * fn + pc) = f32x4{v0, v1, v2, v3};
+              }
+              *(gu2*)(prm + pr * fn + pc) = u32x2{pack_bf16x2(r0, r1), pack_bf16x2(r2, r3)};
+            }
+          });
+        });
+      });
+      if (!has_next) break;
+      cur = nxt;
+      continue;
+    }
+    // (compile-time loops: every acc index must be a constant for acc to stay in registers)
+    static_for<MI>([&](auto mi_c) {
+      constexpr int mi = decltype(mi_c)::value;
       const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
       const int64_t iq = i - q;  // first row of this lane quad
-#pragma unroll
-      for (int ni = 0; ni < NI; ++ni) {
-#pragma unroll
-        for (int gg = 0; gg < 4; ++gg) {
+      static_for<NI>([&](auto ni_c) {
+        constexpr int ni = decltype(ni_c)::value;
+        static_for<4>([&](auto gg_c) {
+          constexpr int gg = decltype(gg_c)::value;
           const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
           float v0 = alpha * acc[mi][ni][4 * gg + 0];
           float v1 = alpha * acc[mi][ni][4 * gg + 1];
@@ -323,25 +461,17 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
           }
           if (C)
             *(gu2*)(C + blk_index(i, j, ldc)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-          if (TD) {
-            // exchange across lane ^ 1: even lanes take the partner's elements 0, 2 as their 1, 3
-            {
-              const float x0 = q_odd ? v0 : v1, x1 = q_odd ? v2 : v3;
-              const float y0 = dpp_quad_xor1(x0), y1 = dpp_quad_xor1(x1);
-              if (q_odd) { v0 = y0; v2 = y1; } else { v1 = y0; v3 = y1; }
-            }
-            // exchange across lane ^ 2: low lanes take the partner's elements 0, 1 as their 2, 3
-            {
-              const float x0 = q_hi ? v0 : v2, x1 = q_hi ? v1 : v3;
-              const float y0 = dpp_quad_xor2(x0), y1 = dpp_quad_xor2(x1);
-              if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
-            }
+          if (TD || fa_t) {
+            quad_transpose(v0, v1, v2, v3);
             // lane q now holds column j + q at rows iq .. iq + 3
-            *(gu2*)(TD + blk_index(j + q, iq, ldtd)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+            if (TD) *(gu2*)(TD + blk_index(j + q, iq, ldtd)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+            else apply4(*fa, j + q, iq, v0, v1, v2, v3);
+          } else if (fa) {
+            apply4(*fa, i, j, v0, v1, v2, v3);
           }
-        }
-      }
-    }
+        });
+      });
+    });
     if (!has_next) break;
     cur = nxt;
   }

@@ -336,6 +336,10 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   return P;
 }
 
+// On the bf16 path with at least one NS step the last update product applies the parameter update
+// in its epilogue (from the fp32 accumulators); otherwise a separate apply pass reads the iterate.
+bool apply_fused(int ns_dtype, int steps) { return ns_dtype == MFSDP_BF16 && steps >= 1; }
+
 // Descriptors of the three products, stored in the phase's problem order; the schedules refer
 // to problems by that position.
 void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, uint8_t* h, int tile) {
@@ -389,6 +393,8 @@ void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, u
         // the final iterate is read in the parameter's orientation only
         d.last_c = p.tall ? 0 : 1;
         d.last_ct = p.tall ? 1 : 0;
+        if (apply_fused(hp.ns_dtype, hp.ns_steps))
+          d.fused = reinterpret_cast<const ApplyDesc*>(ws + P.dl.off_apply) + ord[k];
       }
       d.tile_begin = begin;
       begin += d.tile_count;
@@ -476,9 +482,11 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dty
     }
   }
   if ((rc = record(events, 2, st))) return rc;
-  e = launch_apply(reinterpret_cast<const ApplyDesc*>(ws + dl.off_apply), count, apply_tiles,
-                   ns_dtype, st);
-  if (e != hipSuccess) return hip_fail(e, "apply launch");
+  if (!apply_fused(ns_dtype, steps)) {
+    e = launch_apply(reinterpret_cast<const ApplyDesc*>(ws + dl.off_apply), count, apply_tiles,
+                     ns_dtype, st);
+    if (e != hipSuccess) return hip_fail(e, "apply launch");
+  }
   return record(events, 3, st);
 }
 
@@ -617,6 +625,8 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   apply[0] = make_apply(p, ws, steps, out, out_dtype, nullptr, 1, 1.0f, 0.0f, 0);
   mfsdp_muon_hparams hp{};
   hp.a = a; hp.b = b; hp.c = c;
+  hp.ns_steps = steps;
+  hp.ns_dtype = ns_dtype;
   const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
   fill_gemm_descs(P, ws, hp, h, tile);
   return enqueue_pipeline(P, ws, slot, steps, ns_dtype, 0.0, 0, eps,

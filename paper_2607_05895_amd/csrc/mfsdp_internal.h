@@ -68,6 +68,22 @@ struct NormDesc {
   float* scale;
 };
 
+// apply: p <- p (1 - lr wd) - lr f (oscale O), or out <- oscale O for standalone NS.
+struct ApplyDesc {
+  const void* o;         // O in stored orientation (ns dtype), panel blocked with ld_o columns
+  void* param;           // m x n, param dtype (or NS output)
+  float* update_out;     // optional fp32 m x n
+  const float* scale;    // norm scale, applied when no NS step ran (K = 0)
+  int64_t m, n, ld_o;
+  int32_t param_dtype;
+  int32_t use_scale;
+  int32_t mode;          // 0 = Muon parameter update, 1 = write O to param (standalone NS)
+  float decay;           // 1 - lr wd
+  float step;            // lr f
+  int32_t tiles_m, tiles_n;
+  int32_t tile_begin;
+};
+
 // Grouped NT GEMM problem: C = alpha * P Q^T + beta * E, stored in C and/or transposed in CT.
 // Every operand is panel blocked; the ld* fields are the column counts. Both ping-pong alternatives are kept, indexed by step parity.
 struct GemmDesc {
@@ -88,6 +104,9 @@ struct GemmDesc {
   int32_t tile_begin;    // prefix over the problems of one launch
   int32_t tile_count;
   int32_t last_c, last_ct;  // on the last step: write C / CT (1) or skip (0)
+  // bf16 update product only: on the last step, apply the parameter update (or write the
+  // standalone NS output) from the fp32 accumulators instead of storing the final iterate
+  const ApplyDesc* fused;
 };
 
 // One output tile of a grouped NS product: problem (matrix) index and 256 x 256 block coordinates;
@@ -101,22 +120,6 @@ struct TileRef {
 constexpr int kGemmXcds = 8;    // MI355X: 8 XCDs (workgroups are dealt to them round robin)
 constexpr int kGemmSlots = 32;  // CUs per XCD = tiles per group
 constexpr int kGroupRows = 4;   // a group covers 4 block rows x 8 block columns of one matrix
-
-// apply: p <- p (1 - lr wd) - lr f (oscale O), or out <- oscale O for standalone NS.
-struct ApplyDesc {
-  const void* o;         // O in stored orientation (ns dtype), panel blocked with ld_o columns
-  void* param;           // m x n, param dtype (or NS output)
-  float* update_out;     // optional fp32 m x n
-  const float* scale;    // norm scale, applied when no NS step ran (K = 0)
-  int64_t m, n, ld_o;
-  int32_t param_dtype;
-  int32_t use_scale;
-  int32_t mode;          // 0 = Muon parameter update, 1 = write O to param (standalone NS)
-  float decay;           // 1 - lr wd
-  float step;            // lr f
-  int32_t tiles_m, tiles_n;
-  int32_t tile_begin;
-};
 
 constexpr int kAdamWMaxPerLaunch = 32;
 struct AdamWDesc {

@@ -44,7 +44,7 @@ def _sync():
 # ------------------------------------------------------------------ standalone Newton-Schulz
 
 NS_SHAPES_BF16 = [(256, 512), (512, 256), (100, 300), (300, 100), (257, 513), (768, 768),
-                  (1, 300), (640, 1152), (1024, 4096)]
+                  (1, 300), (640, 1152), (1024, 4096), (513, 257)]
 
 
 @pytest.mark.parametrize("shape", NS_SHAPES_BF16)
