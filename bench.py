@@ -28,6 +28,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 PEAK_HBM_GBS = 8000.0       # HBM3E
+PEAK_F32_TFLOPS = 157.3     # fp32 vector (the fp32 NS path runs on the vector ALUs)
 METRIC = "owner Muon-step latency (ms) and NS TFLOP/s (% MFMA bf16 peak) at 1 MI355X"
 GEMM_KERNEL = "gemm_bf16_kernel"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2607_05895_amd", "csrc", "kernels_gemm.hip")
@@ -217,6 +218,9 @@ def main() -> int:
     torch.cuda.synchronize()
     total_ms = hev.elapsed_ms(ev_start, ev_stop)
     ms_per_step = total_ms / args.steps
+    # per-step times: from one step's first event to the next step's (the last one to the stop)
+    step_ms = sorted(hev.elapsed_ms(ev[k][0], ev[k + 1][0] if k + 1 < n_ev else ev_stop)
+                     for k in range(n_ev))
     prep_ms = sum(hev.elapsed_ms(e[0], e[1]) for e in ev) / n_ev
     ns_ms = sum(hev.elapsed_ms(e[1], e[2]) for e in ev) / n_ev
     apply_ms = sum(hev.elapsed_ms(e[2], e[3]) for e in ev) / n_ev
@@ -227,6 +231,8 @@ def main() -> int:
         apply_ms = 0.0  # the events around the (absent) apply pass bracket no kernel
 
     flops = wl.ns_flops_nominal()
+    bf16_ns = hp.ns_dtype == synth.BF16
+    peak = PEAK_BF16_TFLOPS if bf16_ns else PEAK_F32_TFLOPS
     launches = 3 * hp.ns_steps
     ns_tflops = flops / (ns_ms * 1e-3) / 1e12 if ns_ms > 0 else 0.0
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -264,12 +270,12 @@ def main() -> int:
                    "weight_decay": hp.weight_decay, "lr_adjust": hp.lr_adjust,
                    "nominal_ns_flop_per_step": flops},
         "roofline": {
-            "kernel": GEMM_KERNEL,
-            "bound": "mfma",
+            "kernel": GEMM_KERNEL if bf16_ns else "gemm_f32_kernel",
+            "bound": "mfma" if bf16_ns else "alu",
             "achieved": round(ns_tflops, 2),
-            "peak": PEAK_BF16_TFLOPS,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(ns_tflops / PEAK_BF16_TFLOPS, 4),
+            "frac": round(ns_tflops / peak, 4),
             "traffic": traffic,
             "traffic_unit": "bytes per launch (HBM, calibrated rocprofv3 FETCH_SIZE + WRITE_SIZE)",
             "algorithmic_bytes_per_launch": trec["algorithmic_bytes_per_launch"] if trec else None,
@@ -277,6 +283,11 @@ def main() -> int:
             "avg_launch_ms": round(ns_ms / launches, 4) if launches else 0.0,
             "nominal_flop_per_launch": flops / launches if launches else 0.0,
         },
+        "step_ms_stats": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
+                          "max": round(step_ms[-1], 4)},
+        # (nominal NS flop / MFMA peak + algorithmic elementwise bytes / HBM peak) / step time
+        "step_roofline_frac": round((flops / (peak * 1e12) + (alg_bytes + adamw_bytes) / (PEAK_HBM_GBS * 1e9))
+                                    / (ms_per_step * 1e-3), 4),
         "phases_ms": {"prep_norm": round(prep_ms, 4), "ns": round(ns_ms, 4),
                       "apply": round(apply_ms, 4), "adamw": round(adamw_ms, 4)},
         "elementwise": {

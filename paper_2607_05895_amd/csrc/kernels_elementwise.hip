@@ -113,6 +113,10 @@ __device__ __forceinline__ void store8(void* base, int64_t idx, const V8& x) {
 // 16-B (bf16) vector, so 8 lanes cover 128 contiguous bytes of a transposed row. In LDS, element
 // (i, j) sits at column j ^ 8 ((i >> 3) & 7): the 16-B row writes stay contiguous and the 8-row
 // column gathers of a wave hit distinct banks.
+// Non-temporal stores of the NS input u and u^T (they are read back from HBM by the first NS
+// products anyway: the iterate does not fit the caches at the sizes that matter).
+constexpr bool kPrepNtU = true;
+
 template <int NSDT>
 struct PrepTraits {
   using elem = typename std::conditional<NSDT == kDtBF16, uint16_t, float>::type;
@@ -145,7 +149,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
     const int64_t j0 = col0 + c8;
 #pragma unroll
     for (int k = 0; k < 8; ++k) ss += u.v[k] * u.v[k];
-    store8<NSDT>(d.d_out, blk_index(i, j0, d.ld_d), u);
+    store8<NSDT, kPrepNtU>(d.d_out, blk_index(i, j0, d.ld_d), u);
     // LDS copy (rounded to the NS dtype exactly as the global one)
     T* trow = tile + ti * TW + (c8 ^ (8 * ((ti >> 3) & 7)));
     if constexpr (NSDT == kDtBF16) {
@@ -247,8 +251,9 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
           const int ti = 8 * mm + k;
           h[k] = tile[ti * TW + (jj ^ (8 * ((ti >> 3) & 7)))];
         }
-        *reinterpret_cast<uint4*>(dst) =
-            make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+        typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+        st_stream<kPrepNtU>(reinterpret_cast<u32x4*>(dst),
+                            u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)});
       } else {
         float v[8];
 #pragma unroll
@@ -256,8 +261,9 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
           const int ti = 8 * mm + k;
           v[k] = tile[ti * TW + (jj ^ (8 * ((ti >> 3) & 7)))];
         }
-        *reinterpret_cast<float4*>(dst) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(dst + 4) = make_float4(v[4], v[5], v[6], v[7]);
+        typedef float f32x4 __attribute__((ext_vector_type(4)));
+        st_stream<kPrepNtU>(reinterpret_cast<f32x4*>(dst), f32x4{v[0], v[1], v[2], v[3]});
+        st_stream<kPrepNtU>(reinterpret_cast<f32x4*>(dst + 4), f32x4{v[4], v[5], v[6], v[7]});
       }
     }
   }
@@ -350,15 +356,50 @@ __device__ __forceinline__ void adamw_elem(float& p, float g, float& m, float& v
   p = p - b.step_size * (m / denom);
 }
 
+constexpr bool kAdamWNtLoad = false;   // non-temporal loads / stores of the AdamW streams
+constexpr bool kAdamWNtStore = false;
+
 __global__ __launch_bounds__(256) void adamw_kernel(const AdamWBatch batch) {
   int e = 0;
   for (int k = 1; k < batch.count; ++k)
     if (batch.d[k].block_begin <= int(blockIdx.x)) e = k;
   const AdamWDesc& d = batch.d[e];
   const int64_t base = int64_t(blockIdx.x - d.block_begin) * kAdamWBlockElems;
-  // thread t owns elements base + (q * 256 + t) * 8 .. +7, q = 0 .. kAdamWBlockElems / 2048 - 1
+  constexpr int NQ = kAdamWBlockElems / 2048;
+  // thread t owns elements base + (q * 256 + t) * 8 .. +7, q = 0 .. NQ - 1
+  if (base + kAdamWBlockElems <= d.numel) {
+    // whole block inside the tensor: every load of the block is issued before the first store
+    auto run = [&](auto pdt, auto gdt) {
+      constexpr int PDT = decltype(pdt)::value, GDT = decltype(gdt)::value;
+      V8 p[NQ], g[NQ], m[NQ], v[NQ];
 #pragma unroll
-  for (int q = 0; q < kAdamWBlockElems / 2048; ++q) {
+      for (int q = 0; q < NQ; ++q) {
+        const int64_t i0 = base + (int64_t(q) * 256 + threadIdx.x) * 8;
+        load8<PDT, kAdamWNtLoad>(d.param, i0, p[q]);
+        load8<GDT, kAdamWNtLoad>(d.grad, i0, g[q]);
+        load8<kDtF32, kAdamWNtLoad>(d.exp_avg, i0, m[q]);
+        load8<kDtF32, kAdamWNtLoad>(d.exp_avg_sq, i0, v[q]);
+      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int64_t i0 = base + (int64_t(q) * 256 + threadIdx.x) * 8;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) adamw_elem(p[q].v[k], g[q].v[k], m[q].v[k], v[q].v[k], batch);
+        store8<PDT, kAdamWNtStore>(d.param, i0, p[q]);
+        store8<kDtF32, kAdamWNtStore>(d.exp_avg, i0, m[q]);
+        store8<kDtF32, kAdamWNtStore>(d.exp_avg_sq, i0, v[q]);
+      }
+    };
+    using BF = std::integral_constant<int, kDtBF16>;
+    using F32 = std::integral_constant<int, kDtF32>;
+    if (d.param_dtype == kDtBF16) {
+      if (d.grad_dtype == kDtBF16) run(BF{}, BF{}); else run(BF{}, F32{});
+    } else {
+      if (d.grad_dtype == kDtBF16) run(F32{}, BF{}); else run(F32{}, F32{});
+    }
+    return;
+  }
+  for (int q = 0; q < NQ; ++q) {
     const int64_t i0 = base + (int64_t(q) * 256 + threadIdx.x) * 8;
     if (i0 >= d.numel) break;
     if (i0 + 7 < d.numel) {
