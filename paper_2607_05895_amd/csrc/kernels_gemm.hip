@@ -29,6 +29,8 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(1))) uint16_t gu16;
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(1))) u32x2 gu2;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) u32x4 gu4;
 
 // f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), unrolled by construction.
 template <typename F, int... I>
@@ -156,6 +158,9 @@ __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((
 
 // s_waitcnt with only vmcnt constrained (expcnt and lgkmcnt left at their maxima).
 #define MFSDP_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (7 << 4) | (0xF << 8))
+// s_waitcnt lgkmcnt(0) only (LDS writes done before a barrier; outstanding global loads and stores
+// are not waited for)
+#define MFSDP_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (0 << 8) | (3 << 14))
 
 #ifndef MFSDP_GEMM_WAVES
 #define MFSDP_GEMM_WAVES 8
@@ -239,6 +244,17 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     for (int s = 0; s < NSTAGE - 1; ++s) issue(c, s < c.nk ? s : c.nk - 1, s);
   };
 
+  // the same in two parts: steps 0 .. NSTAGE-3 overlap a staged epilogue, which needs stages
+  // NSTAGE-2 and NSTAGE-1; step NSTAGE-2 follows once that epilogue is done with its stage
+  auto prologue_head = [&](const TileCtx& c) {
+#pragma unroll
+    for (int s = 0; s < NSTAGE - 2; ++s) issue(c, s < c.nk ? s : c.nk - 1, s);
+  };
+  auto prologue_tail = [&](const TileCtx& c) {
+    constexpr int s = NSTAGE - 2;
+    issue(c, s < c.nk ? s : c.nk - 1, s);
+  };
+
   // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
   const int frow = lane & 31, fhalf = lane >> 5;
   const int pbase = (wm * (MI * 32) + frow) * ROWB;
@@ -295,6 +311,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       const uint8_t* sb = smem + cs * STAGE_BYTES;
       read_frags(sb, slot1, pf1, qf1);
       mfma_slice(pf0, qf0);
+      // scheduling: pairs of 1 MFMA + 1 fragment read, then the remaining MFMAs
+      static_assert(NMF >= NRD && NMF >= LOADS, "slice schedule assumes more MFMAs than reads");
 #pragma unroll
       for (int i = 0; i < NRD; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
@@ -310,17 +328,21 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       }
       read_frags(smem + ns * STAGE_BYTES, slot0, pf0, qf0);
       mfma_slice(pf1, qf1);
+      // scheduling: pairs of 1 MFMA + 1 DMA issue, then pairs of 1 MFMA + 1 fragment read while
+      // MFMAs last, then the remaining reads
+      constexpr int PAIRED = (NMF - LOADS < NRD) ? NMF - LOADS : NRD;
 #pragma unroll
       for (int i = 0; i < LOADS; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
       }
 #pragma unroll
-      for (int i = 0; i < NRD; ++i) {
+      for (int i = 0; i < PAIRED; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD - LOADS, 0);
+      if constexpr (NRD > PAIRED) __builtin_amdgcn_sched_group_barrier(0x100, NRD - PAIRED, 0);
+      if constexpr (NMF - LOADS > PAIRED) __builtin_amdgcn_sched_group_barrier(0x008, NMF - LOADS - PAIRED, 0);
       cs = ns;
       ns = (ns + 1 == NSTAGE) ? 0 : ns + 1;
       fs = (fs + 1 == NSTAGE) ? 0 : fs + 1;
@@ -329,7 +351,11 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     // stages, and every wave must be done reading LDS (its last fragments were consumed by MFMAs).
     MFSDP_WAIT_VMCNT(0);
     __builtin_amdgcn_s_barrier();
-    if (has_next) prologue(nxt);  // overlaps the epilogue below
+    // the epilogue stages its output through LDS unless it applies the fused parameter update
+    const bool staged = !(last && cur.d->fused);
+    if (has_next) {  // overlaps the epilogue below
+      if (staged) prologue_head(nxt); else prologue(nxt);
+    }
 
     // Epilogue (global-address-space accesses: flat ones would also hold lgkmcnt, which the next
     // tile's LDS reads wait on). acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
@@ -432,6 +458,105 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       cur = nxt;
       continue;
     }
+    if (staged) {
+      // Staged epilogue. The output tile leaves through the two LDS stages the next tile's first
+      // prologue steps do not use, one 64-row slab (32 rows of each wave row) per round: the waves
+      // write their values into one stage in the global panel-blocked layout and the transposed
+      // values (X'^T, or the mirror tile of a symmetric product) into the other, then each wave
+      // stores whole 1 KiB blocks with 16-byte lanes. (Scattered 8-byte stores straight from the
+      // accumulators measured much slower.)
+      lds_byte* slab = (lds_byte*)(smem + (NSTAGE - 2) * STAGE_BYTES);
+      lds_byte* tslab = (lds_byte*)(smem + (NSTAGE - 1) * STAGE_BYTES);
+      // byte offset of element (row sr, column c) of the 64 x 256 slab: 16 x 32 blocks, 16-byte
+      // chunks of a 64-byte block row swizzled by swz(row)
+      auto slab_off = [](int sr, int c) -> int {
+        return ((((sr >> 4) << 3) + (c >> 5)) << 10) + ((sr & 15) << 6) +
+               ((((c & 31) >> 3) ^ swz(sr & 15)) << 4) + ((c & 7) << 1);
+      };
+      // transposed slab: 256 rows (tile columns) x 2 groups of 32 columns (the slab rows of wave
+      // row g), as 32 blocks of 16 x 32
+      auto tslab_off = [](int jj, int g, int x) -> int {
+        return ((((jj >> 4) << 1) + g) << 10) + ((jj & 15) << 6) + (((x >> 3) ^ swz(jj & 15)) << 4) +
+               ((x & 7) << 1);
+      };
+      typedef __attribute__((address_space(3))) u32x2 l2x;
+      typedef __attribute__((address_space(3))) u32x4 l4x;
+      // The lane index passes through an empty asm so that the lane-dependent offsets below are
+      // formed here, per tile: hoisted out of the tile loop they would stay live through the main
+      // loop and push it into spilling.
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      const int frow = ln & 31, fhalf = ln >> 5, q = ln & 3;
+      const int row_in = ln >> 2, ch = ln & 3;  // block row / 16-byte chunk of the block stores
+      const int rd_off = (row_in << 6) + ((ch ^ swz(row_in)) << 4);
+      constexpr int BPW = 32 / NW;                   // blocks of a slab stored per wave
+      // tile origins (the blocked layout is linear in whole 16 x 32 blocks, so in-tile offsets are
+      // 32-bit blk_index values of the in-tile coordinates)
+      const int ldc32 = int(ldc), ldtd32 = int(ldtd), lde32 = int(dd.lde);
+      const gu16* Et = E ? E + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, dd.lde) : nullptr;
+      gu16* Ct = C ? C + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, ldc) : nullptr;
+      gu16* Tt = TD ? TD + blk_index(int64_t(bj) * BT, int64_t(bi) * BT, ldtd) : nullptr;
+      const bool on_diag = diag != 0.0f;
+      static_for<MI>([&](auto mi_c) {
+        constexpr int mi = decltype(mi_c)::value;
+        const int il = wm * (MI * 32) + mi * 32 + frow;  // row within the tile
+        const int sr = wm * 32 + frow;
+        static_for<NI>([&](auto ni_c) {
+          constexpr int ni = decltype(ni_c)::value;
+          static_for<4>([&](auto gg_c) {
+            constexpr int gg = decltype(gg_c)::value;
+            const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;  // column within the tile
+            float v0 = alpha * acc[mi][ni][4 * gg + 0];
+            float v1 = alpha * acc[mi][ni][4 * gg + 1];
+            float v2 = alpha * acc[mi][ni][4 * gg + 2];
+            float v3 = alpha * acc[mi][ni][4 * gg + 3];
+            if (Et) {
+              const u32x2 ev = *(const gu2*)(Et + int(blk_index(il, lc, lde32)));
+              v0 += beta * __uint_as_float(ev.x << 16);
+              v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
+              v2 += beta * __uint_as_float(ev.y << 16);
+              v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
+            }
+            if (on_diag) {  // diagonal tile of a symmetric product
+              if (il == lc + 0) v0 += diag;
+              if (il == lc + 1) v1 += diag;
+              if (il == lc + 2) v2 += diag;
+              if (il == lc + 3) v3 += diag;
+            }
+            if (Ct) *(l2x*)(slab + slab_off(sr, lc)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+            if (Tt) {
+              quad_transpose(v0, v1, v2, v3);  // lane q: column lc + q, rows frow - q .. + 3
+              *(l2x*)(tslab + tslab_off(lc + q, wm, frow - q)) =
+                  u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
+            }
+          });
+        });
+        MFSDP_WAIT_LGKM0();
+        __builtin_amdgcn_s_barrier();
+        if (Ct) {
+#pragma unroll
+          for (int bb = 0; bb < BPW; ++bb) {
+            const int blk = w * BPW + bb, sp = blk >> 3, cb = blk & 7;
+            const u32x4 val = *(l4x*)(slab + (blk << 10) + rd_off);
+            const int dr = (sp >> 1) * (MI * 32) + mi * 32 + (sp & 1) * 16 + row_in;
+            *(gu4*)(Ct + int(blk_index(dr, cb * 32 + ch * 8, ldc32))) = val;
+          }
+        }
+        if (Tt) {
+#pragma unroll
+          for (int bb = 0; bb < BPW; ++bb) {
+            const int tb = w * BPW + bb, jp = tb >> 1, g = tb & 1;
+            const u32x4 val = *(l4x*)(tslab + (tb << 10) + rd_off);
+            *(gu4*)(Tt + int(blk_index(jp * 16 + row_in, g * (MI * 32) + mi * 32 + ch * 8, ldtd32))) = val;
+          }
+        }
+        __builtin_amdgcn_s_barrier();  // slab reads done before the next round overwrites it
+      });
+      if (!has_next) break;
+      prologue_tail(nxt);
+      cur = nxt;
+      continue;
+    }
     // (compile-time loops: every acc index must be a constant for acc to stay in registers)
     static_for<MI>([&](auto mi_c) {
       constexpr int mi = decltype(mi_c)::value;
@@ -479,6 +604,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   MFSDP_WAIT_VMCNT(0);
 }
 #undef MFSDP_WAIT_VMCNT
+#undef MFSDP_WAIT_LGKM0
 
 // ---------------------------------------------------------------------------------------------
 // fp32 kernel: 64 x 64 tile, 256 threads of 4 x 4 outputs, K step 16 through LDS.
