@@ -106,7 +106,7 @@ __device__ __forceinline__ void store8(void* base, int64_t idx, const V8& x) {
 
 // ---------------------------------------------------------------------------------------------
 // prep: one tile of 64 rows x TW columns of the stored (padded) matrix per workgroup of 256
-// threads (TW = 128 on the bf16 path, 64 on the fp32 path). Phase 1: thread t owns columns
+// threads (TW = kPrepColsBF16 on the bf16 path, 64 on the fp32 path). Phase 1: thread t owns columns
 // 8 (t % (TW/8)) .. +7 of rows t / (TW/8) + (2048/TW) q: gradient and momentum in 16-B vectors,
 // u to the stored-orientation buffer and to an LDS tile. Phase 2: the transposed copy; thread t
 // gathers 8 consecutive tile rows 8 (t % 8) .. +7 of tile column t / 8 + 32 q and writes them as one

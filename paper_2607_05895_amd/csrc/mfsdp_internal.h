@@ -141,7 +141,7 @@ struct AdamWBatch {
   float inv_sqrt_bc2;    // 1 / sqrt(1 - beta2^t)
   float eps;
 };
-constexpr int kAdamWBlockElems = 4096;
+constexpr int kAdamWBlockElems = 2048;
 
 // Launchers (return hipError_t of the launch).
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
@@ -158,7 +158,7 @@ hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t s
 constexpr int kTileBF16 = 256;
 constexpr int kTileF32 = 64;
 #ifndef MFSDP_PREP_COLS
-#define MFSDP_PREP_COLS 128
+#define MFSDP_PREP_COLS 256
 #endif
 #ifndef MFSDP_APPLY_COLS
 #define MFSDP_APPLY_COLS 128
