@@ -24,6 +24,7 @@ namespace mfsdp {
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 // global-address-space element types (pointers derived from these give global_* instructions)
 typedef __attribute__((address_space(1))) uint16_t gu16;
@@ -186,7 +187,12 @@ struct TileCtx {
   int64_t pstep, qstep;
 };
 
-template <int NW>
+// Product kinds of one NS step (one launch each); the epilogue is specialised per kind.
+constexpr int kProdGram = 0;    // A = X X^T: symmetric, mirror stores
+constexpr int kProdSquare = 1;  // B' = c A A + b A + a I: symmetric, addend E = A, diagonal term
+constexpr int kProdUpdate = 2;  // X' = B' X: stores X' and X'^T, or the fused parameter update
+
+template <int NW, int PK>
 __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
                                                                const TileRef* __restrict__ sched,
                                                                int ngroups, int parity, int first,
@@ -242,17 +248,6 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   auto prologue = [&](const TileCtx& c) {
 #pragma unroll
     for (int s = 0; s < NSTAGE - 1; ++s) issue(c, s < c.nk ? s : c.nk - 1, s);
-  };
-
-  // the same in two parts: steps 0 .. NSTAGE-3 overlap a staged epilogue, which needs stages
-  // NSTAGE-2 and NSTAGE-1; step NSTAGE-2 follows once that epilogue is done with its stage
-  auto prologue_head = [&](const TileCtx& c) {
-#pragma unroll
-    for (int s = 0; s < NSTAGE - 2; ++s) issue(c, s < c.nk ? s : c.nk - 1, s);
-  };
-  auto prologue_tail = [&](const TileCtx& c) {
-    constexpr int s = NSTAGE - 2;
-    issue(c, s < c.nk ? s : c.nk - 1, s);
   };
 
   // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
@@ -352,10 +347,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     MFSDP_WAIT_VMCNT(0);
     __builtin_amdgcn_s_barrier();
     // the epilogue stages its output through LDS unless it applies the fused parameter update
-    const bool staged = !(last && cur.d->fused);
-    if (has_next) {  // overlaps the epilogue below
-      if (staged) prologue_head(nxt); else prologue(nxt);
-    }
+    const bool staged = !(PK == kProdUpdate && last && cur.d->fused);
+    if (has_next) prologue(nxt);  // overlaps the epilogue below (it leaves stage NSTAGE-1 free)
 
     // Epilogue (global-address-space accesses: flat ones would also hold lgkmcnt, which the next
     // tile's LDS reads wait on). acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
@@ -372,7 +365,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     const gu16* E = (const gu16*)dd.E[parity];
     gu16* C = (gu16*)dd.C[parity];
     gu16* CT = (gu16*)dd.CT[parity];
-    const ApplyDesc* fa = last ? dd.fused : nullptr;
+    const ApplyDesc* fa = (PK == kProdUpdate && last) ? dd.fused : nullptr;
     if (last) {
       if (!dd.last_c || fa) C = nullptr;
       if (!dd.last_ct || fa) CT = nullptr;
@@ -459,78 +452,102 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       continue;
     }
     if (staged) {
-      // Staged epilogue. The output tile leaves through the two LDS stages the next tile's first
-      // prologue steps do not use, one 64-row slab (32 rows of each wave row) per round: the waves
-      // write their values into one stage in the global panel-blocked layout and the transposed
-      // values (X'^T, or the mirror tile of a symmetric product) into the other, then each wave
-      // stores whole 1 KiB blocks with 16-byte lanes. (Scattered 8-byte stores straight from the
-      // accumulators measured much slower.)
-      lds_byte* slab = (lds_byte*)(smem + (NSTAGE - 2) * STAGE_BYTES);
-      lds_byte* tslab = (lds_byte*)(smem + (NSTAGE - 1) * STAGE_BYTES);
-      // byte offset of element (row sr, column c) of the 64 x 256 slab: 16 x 32 blocks, 16-byte
-      // chunks of a 64-byte block row swizzled by swz(row)
-      auto slab_off = [](int sr, int c) -> int {
-        return ((((sr >> 4) << 3) + (c >> 5)) << 10) + ((sr & 15) << 6) +
-               ((((c & 31) >> 3) ^ swz(sr & 15)) << 4) + ((c & 7) << 1);
-      };
-      // transposed slab: 256 rows (tile columns) x 2 groups of 32 columns (the slab rows of wave
-      // row g), as 32 blocks of 16 x 32
-      auto tslab_off = [](int jj, int g, int x) -> int {
-        return ((((jj >> 4) << 1) + g) << 10) + ((jj & 15) << 6) + (((x >> 3) ^ swz(jj & 15)) << 4) +
-               ((x & 7) << 1);
-      };
+      // Staged epilogue. The output tile leaves through the LDS stage the next tile's prologue does
+      // not use, one 64-row slab (32 rows of each wave row) per round: the waves write their
+      // values into the slab in the global panel-blocked layout, then each wave stores whole 1 KiB
+      // blocks with 16-byte lanes, read back as they are (C) or with transposing LDS reads (the
+      // transposed output: X'^T, or the mirror tile of a symmetric product). Per element this
+      // costs a scale, a conversion and a share of one LDS write; scattered 8-byte stores straight
+      // from the accumulators, and DPP transposes, measured much slower.
+      lds_byte* slab = (lds_byte*)(smem + (NSTAGE - 1) * STAGE_BYTES);
       typedef __attribute__((address_space(3))) u32x2 l2x;
       typedef __attribute__((address_space(3))) u32x4 l4x;
+      typedef __attribute__((address_space(3))) bf16x4_t lbf4;
       // The lane index passes through an empty asm so that the lane-dependent offsets below are
       // formed here, per tile: hoisted out of the tile loop they would stay live through the main
       // loop and push it into spilling.
       int ln = lane;
       asm volatile("" : "+v"(ln));
-      const int frow = ln & 31, fhalf = ln >> 5, q = ln & 3;
-      const int row_in = ln >> 2, ch = ln & 3;  // block row / 16-byte chunk of the block stores
+      const int frow = ln & 31, fhalf = ln >> 5;
+      // slab byte offset of (row sr, column c): 16 x 32 blocks (block (sr / 16, c / 32) at
+      // 1 KiB * (8 (sr / 16) + c / 32)), 64-byte block rows whose 16-byte chunks are swizzled by
+      // swz(row % 16)
+      auto slab_off = [](int sr, int c) -> int {
+        return ((((sr >> 4) << 3) + (c >> 5)) << 10) + ((sr & 15) << 6) +
+               ((((c & 31) >> 3) ^ swz(sr & 15)) << 4) + ((c & 7) << 1);
+      };
+      // this lane's slab writes: row wm * 32 + frow, columns wn * 64 + ni * 32 + gg * 8 + fhalf * 4
+      const int sr_w = wm * 32 + frow;
+      const int wr_base = slab_off(sr_w, wn * (NI * 32) + fhalf * 4);  // ni = gg = 0
+      const int wr_sw = swz(sr_w & 15);
+      // C block stores: lane = 4 row_in + ch holds row row_in, 16-byte chunk ch of a block
+      const int row_in = ln >> 2, ch = ln & 3;
       const int rd_off = (row_in << 6) + ((ch ^ swz(row_in)) << 4);
-      constexpr int BPW = 32 / NW;                   // blocks of a slab stored per wave
-      // tile origins (the blocked layout is linear in whole 16 x 32 blocks, so in-tile offsets are
-      // 32-bit blk_index values of the in-tile coordinates)
-      const int ldc32 = int(ldc), ldtd32 = int(ldtd), lde32 = int(dd.lde);
-      const gu16* Et = E ? E + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, dd.lde) : nullptr;
+      // transposed block stores: lane = 16 g + il holds row il (a tile column) and columns
+      // 8 g .. 8 g + 7 (tile rows) of a 16 x 32 block of the transposed tile, from two
+      // ds_read_b64_tr_b16 of slab rows 8 g + r (+ 4), r = 0..3, columns 4 c .. 4 c + 3 (lane of
+      // the 16-lane group = 4 r + c)
+      const int tg = ln >> 4, til = ln & 15, tr_r = (ln >> 2) & 3, tr_c = ln & 3;
+      constexpr int BPW = 32 / NW;  // blocks of a slab stored per wave
+      const float* dscale = dd.scale;
+      (void)dscale;
+      const int ldc32 = int(ldc), ldtd32 = int(ldtd);
       gu16* Ct = C ? C + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, ldc) : nullptr;
       gu16* Tt = TD ? TD + blk_index(int64_t(bj) * BT, int64_t(bi) * BT, ldtd) : nullptr;
-      const bool on_diag = diag != 0.0f;
-      static_for<MI>([&](auto mi_c) {
+      const gu16* Et = nullptr;
+      int lde32 = 0;
+      if constexpr (PK == kProdSquare) {
+        Et = E + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, dd.lde);
+        lde32 = int(dd.lde);
+      }
+      // values of round mi into the slab; DIAG: this is a diagonal tile of the square product
+      auto write_round = [&](auto mi_c, auto diag_c) {
         constexpr int mi = decltype(mi_c)::value;
-        const int il = wm * (MI * 32) + mi * 32 + frow;  // row within the tile
-        const int sr = wm * 32 + frow;
+        constexpr bool DIAG = decltype(diag_c)::value;
+        const int il = wm * (MI * 32) + mi * 32 + frow;  // tile row of this lane
+        u32x2 ev[NI][4];
+        if constexpr (PK == kProdSquare) {
+          static_for<NI>([&](auto ni) {
+            static_for<4>([&](auto gg) {
+              const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+              ev[ni][gg] = *(const gu2*)(Et + int(blk_index(il, lc, lde32)));
+            });
+          });
+        }
         static_for<NI>([&](auto ni_c) {
           constexpr int ni = decltype(ni_c)::value;
           static_for<4>([&](auto gg_c) {
             constexpr int gg = decltype(gg_c)::value;
-            const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;  // column within the tile
             float v0 = alpha * acc[mi][ni][4 * gg + 0];
             float v1 = alpha * acc[mi][ni][4 * gg + 1];
             float v2 = alpha * acc[mi][ni][4 * gg + 2];
             float v3 = alpha * acc[mi][ni][4 * gg + 3];
-            if (Et) {
-              const u32x2 ev = *(const gu2*)(Et + int(blk_index(il, lc, lde32)));
-              v0 += beta * __uint_as_float(ev.x << 16);
-              v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
-              v2 += beta * __uint_as_float(ev.y << 16);
-              v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
+            if constexpr (PK == kProdSquare) {
+              const u32x2 e = ev[ni][gg];
+              v0 += beta * __uint_as_float(e.x << 16);
+              v1 += beta * __uint_as_float(e.x & 0xffff0000u);
+              v2 += beta * __uint_as_float(e.y << 16);
+              v3 += beta * __uint_as_float(e.y & 0xffff0000u);
             }
-            if (on_diag) {  // diagonal tile of a symmetric product
+            if constexpr (DIAG) {
+              const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
               if (il == lc + 0) v0 += diag;
               if (il == lc + 1) v1 += diag;
               if (il == lc + 2) v2 += diag;
               if (il == lc + 3) v3 += diag;
             }
-            if (Ct) *(l2x*)(slab + slab_off(sr, lc)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-            if (Tt) {
-              quad_transpose(v0, v1, v2, v3);  // lane q: column lc + q, rows frow - q .. + 3
-              *(l2x*)(tslab + tslab_off(lc + q, wm, frow - q)) =
-                  u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-            }
+            // column block ni, chunk gg of this lane's slab row (chunk index swizzled)
+            const int off = wr_base + ni * 1024 + (((gg ^ wr_sw) - wr_sw) << 4);
+            *(l2x*)(slab + off) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
           });
         });
+      };
+      static_for<MI>([&](auto mi_c) {
+        constexpr int mi = decltype(mi_c)::value;
+        if (PK == kProdSquare && diag != 0.0f)
+          write_round(mi_c, std::true_type{});
+        else
+          write_round(mi_c, std::false_type{});
         MFSDP_WAIT_LGKM0();
         __builtin_amdgcn_s_barrier();
         if (Ct) {
@@ -545,15 +562,20 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         if (Tt) {
 #pragma unroll
           for (int bb = 0; bb < BPW; ++bb) {
-            const int tb = w * BPW + bb, jp = tb >> 1, g = tb & 1;
-            const u32x4 val = *(l4x*)(tslab + (tb << 10) + rd_off);
-            *(gu4*)(Tt + int(blk_index(jp * 16 + row_in, g * (MI * 32) + mi * 32 + ch * 8, ldtd32))) = val;
+            // transposed block tb: rows jp * 16 .. + 15 (tile columns), columns: the 32 tile rows
+            // of wave row g2 in this round
+            const int tb = w * BPW + bb, jp = tb >> 1, g2 = tb & 1;
+            const int sr0 = g2 * 32 + tg * 8 + tr_r;
+            const int cc = jp * 16 + tr_c * 4;
+            const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lbf4*)(slab + slab_off(sr0, cc)));
+            const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lbf4*)(slab + slab_off(sr0 + 4, cc)));
+            const u32x4 val = __builtin_bit_cast(u32x4, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+            *(gu4*)(Tt + int(blk_index(jp * 16 + til, g2 * (MI * 32) + mi * 32 + tg * 8, ldtd32))) = val;
           }
         }
         __builtin_amdgcn_s_barrier();  // slab reads done before the next round overwrites it
       });
       if (!has_next) break;
-      prologue_tail(nxt);
       cur = nxt;
       continue;
     }
@@ -682,14 +704,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
 }  // namespace
 
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
-                       int ngroups, int ns_dtype, int parity, int first_step, int last_step,
-                       hipStream_t st) {
+                       int ngroups, int ns_dtype, int product, int parity, int first_step,
+                       int last_step, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
-  if (ns_dtype == kDtBF16)
-    hipLaunchKernelGGL(gemm_bf16_kernel<MFSDP_GEMM_WAVES>, dim3(kGemmXcds * kGemmSlots),
-                       dim3(MFSDP_GEMM_WAVES * 64), 0, st, d_descs, d_sched, ngroups, parity,
-                       first_step, last_step);
-  else
+  if (ns_dtype == kDtBF16) {
+    const dim3 grid(kGemmXcds * kGemmSlots), block(MFSDP_GEMM_WAVES * 64);
+    if (product == kProdGram)
+      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdGram>), grid, block, 0, st,
+                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+    else if (product == kProdSquare)
+      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdSquare>), grid, block, 0, st,
+                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdUpdate>), grid, block, 0, st,
+                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+  } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
                        parity, first_step, last_step);
   return hipGetLastError();

@@ -477,7 +477,7 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dty
     for (int ph = 0; ph < 3; ++ph) {
       e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, P.tiles[ph],
                       reinterpret_cast<const TileRef*>(ws + dl.off_sched[ph]), dl.ngroups[ph],
-                      ns_dtype, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0, st);
+                      ns_dtype, ph, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0, st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
   }

@@ -147,9 +147,10 @@ constexpr int kAdamWBlockElems = 2048;
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
                        float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
+// product: 0 Gram, 1 square, 2 update (the order of the products in one NS step)
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
-                       int ngroups, int ns_dtype, int parity, int first_step, int last_step,
-                       hipStream_t st);
+                       int ngroups, int ns_dtype, int product, int parity, int first_step,
+                       int last_step, hipStream_t st);
 hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
                         hipStream_t st);
 hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);
