@@ -12,6 +12,10 @@ The quintic iteration is X <- a X + (b A + c A^2) X with A = X X^T, applied to t
 (the matrix is transposed when it has more rows than columns) after Frobenius normalisation with a
 clamped norm. The momentum buffer is an exponential moving average of the gradient with a Nesterov
 look-ahead. Everything is float64.
+
+Per-step coefficient schedules (one (a_k, b_k, c_k) per NS step) generalise the fixed triple; the
+paper does not use them (it runs one fixed triple), and with a constant schedule the iteration is
+exactly the paper's.
 """
 from __future__ import annotations
 
@@ -69,12 +73,22 @@ def ns_quintic_step(x: np.ndarray, a: float, b: float, c: float) -> np.ndarray:
     return a * x + B @ x
 
 
+def step_coefficients(a: float, b: float, c: float, steps: int, schedule=None):
+    """The (a_k, b_k, c_k) of each of the ``steps`` NS steps: the fixed triple, or ``schedule``."""
+    if schedule is None:
+        return [(a, b, c)] * steps
+    sched = [tuple(float(v) for v in t) for t in schedule]
+    if len(sched) != steps or any(len(t) != 3 for t in sched):
+        raise ValueError("schedule needs one (a, b, c) triple per NS step")
+    return sched
+
+
 def newton_schulz(u: np.ndarray, a: float, b: float, c: float, steps: int,
-                  eps: float = 1e-7) -> np.ndarray:
+                  eps: float = 1e-7, schedule=None) -> np.ndarray:
     """NS orthogonalisation of the whole matrix u (m x n), returned in u's orientation.
 
     Transpose when m > n (work on the short side), normalise by the clamped Frobenius norm, take
-    ``steps`` quintic steps, transpose back.
+    ``steps`` quintic steps (step k with schedule[k] if a schedule is given), transpose back.
     """
     x = _f64(u)
     if x.ndim != 2:
@@ -84,20 +98,23 @@ def newton_schulz(u: np.ndarray, a: float, b: float, c: float, steps: int,
     tall = x.shape[0] > x.shape[1]
     if tall:
         x = x.T
+    coeffs = step_coefficients(a, b, c, steps, schedule)
     x = frobenius_normalize(x, eps)
-    for _ in range(steps):
-        x = ns_quintic_step(x, a, b, c)
+    for ak, bk, ck in coeffs:
+        x = ns_quintic_step(x, ak, bk, ck)
     return np.ascontiguousarray(x.T if tall else x)
 
 
-def scalar_ns_map(sigma: float, a: float, b: float, c: float, steps: int) -> float:
-    """The scalar polynomial p(s) = a s + b s^3 + c s^5 iterated ``steps`` times.
+def scalar_ns_map(sigma: float, a: float, b: float, c: float, steps: int,
+                  schedule=None) -> float:
+    """The scalar polynomial p(s) = a s + b s^3 + c s^5 iterated ``steps`` times (p_k with the
+    step's coefficients under a schedule).
 
     NS acts on each singular value of the normalised input by this map; used by the pins.
     """
     s = float(sigma)
-    for _ in range(steps):
-        s = a * s + b * s ** 3 + c * s ** 5
+    for ak, bk, ck in step_coefficients(a, b, c, steps, schedule):
+        s = ak * s + bk * s ** 3 + ck * s ** 5
     return s
 
 
@@ -130,11 +147,11 @@ def apply_update(param: np.ndarray, update: np.ndarray, lr: float, weight_decay:
 
 def muon_step(param: np.ndarray, grad: np.ndarray, buf: np.ndarray, *, lr: float,
               weight_decay: float, momentum: float, nesterov: bool, a: float, b: float, c: float,
-              ns_steps: int, eps: float = 1e-7, lr_adjust: str = "original"
+              ns_steps: int, eps: float = 1e-7, lr_adjust: str = "original", ns_schedule=None
               ) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
     """One owner-local Muon step on one whole matrix (Section 3). Returns (param', buf', O)."""
     m, n = np.asarray(grad).shape
     buf_new, u = momentum_update(grad, buf, momentum, nesterov)
-    O = newton_schulz(u, a, b, c, ns_steps, eps)
+    O = newton_schulz(u, a, b, c, ns_steps, eps, ns_schedule)
     p_new = apply_update(param, O, lr, weight_decay, lr_factor(m, n, lr_adjust))
     return p_new, buf_new, O

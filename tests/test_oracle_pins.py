@@ -316,3 +316,92 @@ def test_paper_setup_matches_torch_optim_muon():
     np.testing.assert_allclose(buf, tbuf, rtol=1e-13)
     d_or, d_t = p - p0, tp - p0
     assert np.linalg.norm(d_or - d_t) / np.linalg.norm(d_or) < 3e-2
+
+
+# ---------------------------------------------------------------- per-step coefficient schedules
+
+def _p_coef(s, a, b, c):
+    s2 = s * s
+    return s * (a + s2 * (b + s2 * c))
+
+
+def _random_schedule(rng, k):
+    # perturbations of the fixed triple: every step different
+    base = np.array([A, B, C])
+    return [tuple(base * (1.0 + 0.05 * rng.standard_normal(3))) for _ in range(k)]
+
+
+def test_schedule_constant_equals_fixed_triple():
+    rng = np.random.default_rng(40)
+    x = _rand(rng, 24, 56)
+    o1 = oracle.newton_schulz(x, A, B, C, 5)
+    o2 = oracle.newton_schulz(x, 0.0, 0.0, 0.0, 5, schedule=[(A, B, C)] * 5)
+    assert np.array_equal(o1, o2)
+
+
+@pytest.mark.parametrize("shape", [(6, 6), (4, 9), (9, 4)])
+def test_schedule_diagonal_composes_step_polynomials(shape):
+    # NS of a diagonal matrix acts entrywise; step k applies its own polynomial p_k
+    m, n = shape
+    rng = np.random.default_rng(41)
+    sched = _random_schedule(rng, 4)
+    k = min(m, n)
+    d = rng.uniform(0.2, 2.0, size=k) * rng.choice([-1.0, 1.0], size=k)
+    x = np.zeros((m, n))
+    x[np.arange(k), np.arange(k)] = d
+    nrm = math.sqrt(float((d ** 2).sum()))
+    vals = []
+    for v in d:
+        s = v / nrm
+        for (a, b, c) in sched:
+            s = _p_coef(s, a, b, c)
+        vals.append(s)
+    exp = np.zeros((m, n))
+    exp[np.arange(k), np.arange(k)] = vals
+    np.testing.assert_allclose(oracle.newton_schulz(x, A, B, C, 4, schedule=sched), exp, rtol=0, atol=1e-12)
+
+
+def test_schedule_one_step_expanded():
+    # K = 1 with triple (a0, b0, c0): a0 X + b0 X X^T X + c0 (X X^T)^2 X, X = x / ||x||_F
+    rng = np.random.default_rng(42)
+    x = _rand(rng, 12, 20)
+    a0, b0, c0 = 2.0, -1.25, 0.375
+    X = x / np.linalg.norm(x)
+    G = X @ X.T
+    exp = a0 * X + b0 * G @ X + c0 * G @ G @ X
+    np.testing.assert_allclose(oracle.newton_schulz(x, A, B, C, 1, schedule=[(a0, b0, c0)]), exp,
+                               rtol=0, atol=1e-14)
+
+
+def test_schedule_cubic_newton_schulz_converges_to_polar_factor():
+    # the textbook cubic Newton-Schulz iteration X <- 1.5 X - 0.5 X X^T X (a schedule with c = 0)
+    # converges to the orthogonal polar factor U V^T for singular values in (0, sqrt(3))
+    # (full rank: zero singular values would only be amplified by rounding)
+    rng = np.random.default_rng(43)
+    U = _orth(rng, 8)
+    V = _orth(rng, 10)[:, :8]
+    s = np.linspace(0.3, 1.0, 8)
+    x = (U * s) @ V.T
+    o = oracle.newton_schulz(x, A, B, C, 20, schedule=[(1.5, -0.5, 0.0)] * 20)
+    np.testing.assert_allclose(o, U @ V.T, rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(5, 3), (8, 8), (16, 24)])
+def test_schedule_matches_svd_brute_force(shape):
+    rng = np.random.default_rng(44)
+    sched = _random_schedule(rng, 3)
+    x = _rand(rng, *shape)
+    Uu, s, Vt = np.linalg.svd(x, full_matrices=False)
+    s0 = s / math.sqrt(float((s ** 2).sum()))
+    mapped = []
+    for v in s0:
+        for (a, b, c) in sched:
+            v = _p_coef(v, a, b, c)
+        mapped.append(v)
+    exp = (Uu * np.array(mapped)) @ Vt
+    np.testing.assert_allclose(oracle.newton_schulz(x, A, B, C, 3, schedule=sched), exp, rtol=0, atol=1e-12)
+
+
+def test_schedule_length_must_match_steps():
+    with pytest.raises(ValueError):
+        oracle.newton_schulz(np.ones((3, 4)), A, B, C, 2, schedule=[(A, B, C)])
