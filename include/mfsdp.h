@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MFSDP_ABI_VERSION 1
+#define MFSDP_ABI_VERSION 2
 
 typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
 
@@ -87,7 +87,11 @@ typedef struct {
  *   lr >= 0, weight_decay >= 0, 0 <= momentum < 1, nesterov 0/1,
  *   (a, b, c) NS coefficients, 0 <= ns_steps < 100, eps > 0 (norm clamp),
  *   lr_adjust an mfsdp_lr_adjust, ns_dtype: BF16 = NS products on bf16 MFMA with fp32
- *   accumulation and bf16 storage between products; F32 = fp32 throughout. */
+ *   accumulation and bf16 storage between products; F32 = fp32 throughout.
+ *   ns_schedule: NULL = the triple (a, b, c) on every NS step; otherwise a host array of ns_steps
+ *   finite triples (a_k, b_k, c_k), k = 0 .. ns_steps - 1, step k computing
+ *   X <- a_k X + (b_k A + c_k A A) X. It is read during the call and not kept. (The paper runs one
+ *   fixed triple; a constant schedule is identical to it.) */
 typedef struct {
   double lr;
   double weight_decay;
@@ -98,6 +102,7 @@ typedef struct {
   double eps;
   int32_t lr_adjust;
   int32_t ns_dtype;
+  const double* ns_schedule;
 } mfsdp_muon_hparams;
 
 /* One tail tensor (Section 4.4: non-matrix tensors stay on AdamW), flattened.
@@ -146,6 +151,14 @@ size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype);
 int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m,
                         int64_t n, double a, double b, double c, int32_t steps, double eps,
                         int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream);
+
+/* mfsdp_newton_schulz with one coefficient triple per step: coeffs is a host array of `steps`
+ * finite triples (a_k, b_k, c_k) (read during the call, not kept); NULL is invalid unless
+ * steps == 0. Same workspace size. */
+int mfsdp_newton_schulz_schedule(const void* x, int32_t x_dtype, void* out, int32_t out_dtype,
+                                 int64_t m, int64_t n, const double* coeffs, int32_t steps,
+                                 double eps, int32_t ns_dtype, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* AdamW on the tail tensors (Section 4.4; PyTorch AdamW per Section 5.1):
  *   p <- p (1 - lr wd);  m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2

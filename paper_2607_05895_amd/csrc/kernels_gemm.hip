@@ -192,11 +192,14 @@ constexpr int kProdGram = 0;    // A = X X^T: symmetric, mirror stores
 constexpr int kProdSquare = 1;  // B' = c A A + b A + a I: symmetric, addend E = A, diagonal term
 constexpr int kProdUpdate = 2;  // X' = B' X: stores X' and X'^T, or the fused parameter update
 
+// (ca, cb, cc): this NS step's coefficients; the square product uses them as diagonal term, addend
+// factor and product factor (B' = cc A A + cb A + ca I).
 template <int NW, int PK>
 __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
                                                                const TileRef* __restrict__ sched,
                                                                int ngroups, int parity, int first,
-                                                               int last) {
+                                                               int last, float ca, float cb,
+                                                               float cc) {
   using WG = WaveGrid<NW>;
   constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS;
   constexpr int PL = LOADS / 2;        // DMA instructions for P (and for Q) per thread per stage
@@ -359,9 +362,9 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     // store).
     const GemmDesc& dd = *cur.d;
     const int bi = cur.bi, bj = cur.bj;
-    const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
-    const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
-    const float diag = (dd.sym && bi == bj) ? dd.diag : 0.0f;
+    const float alpha = PK == kProdSquare ? cc : dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
+    const float beta = PK == kProdSquare ? cb : dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
+    const float diag = (PK == kProdSquare && bi == bj) ? ca : 0.0f;
     const gu16* E = (const gu16*)dd.E[parity];
     gu16* C = (gu16*)dd.C[parity];
     gu16* CT = (gu16*)dd.CT[parity];
@@ -631,7 +634,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
 // ---------------------------------------------------------------------------------------------
 // fp32 kernel: 64 x 64 tile, 256 threads of 4 x 4 outputs, K step 16 through LDS.
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restrict__ descs, int count,
-                                                       int parity, int first, int last) {
+                                                       int parity, int first, int last, float ca,
+                                                       float cb, float cc) {
   __shared__ float Ps[16][68];
   __shared__ float Qs[16][68];
   const int e = find_entry(descs, count, blockIdx.x);
@@ -664,8 +668,11 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
     }
     __syncthreads();
   }
-  const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
-  const float beta = dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
+  // the square product (the only one with an addend) takes this step's coefficients
+  const bool square = dd.E[parity] != nullptr;
+  const float alpha = square ? cc : dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
+  const float beta = square ? cb : dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
+  const float diag = square ? ca : 0.0f;
   const float* E = static_cast<const float*>(dd.E[parity]);
   float* C = static_cast<float*>(dd.C[parity]);
   float* CT = static_cast<float*>(dd.CT[parity]);
@@ -688,7 +695,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
     if (dd.sym && bi == bj)
 #pragma unroll
       for (int c = 0; c < 4; ++c)
-        if (i == j + c) v[c] += dd.diag;
+        if (i == j + c) v[c] += diag;
     if (C) {
       *reinterpret_cast<float4*>(C + blk_index(i, j, dd.ldc)) = make_float4(v[0], v[1], v[2], v[3]);
       if (mirror)
@@ -705,22 +712,22 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
 
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
                        int ngroups, int ns_dtype, int product, int parity, int first_step,
-                       int last_step, hipStream_t st) {
+                       int last_step, float ca, float cb, float cc, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16) {
     const dim3 grid(kGemmXcds * kGemmSlots), block(MFSDP_GEMM_WAVES * 64);
     if (product == kProdGram)
       hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdGram>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
     else if (product == kProdSquare)
       hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdSquare>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
     else
       hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdUpdate>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step);
+                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
   } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
-                       parity, first_step, last_step);
+                       parity, first_step, last_step, ca, cb, cc);
   return hipGetLastError();
 }
 

@@ -223,9 +223,14 @@ int check_hp(const mfsdp_muon_hparams* hp) {
   if (!(hp->momentum >= 0.0 && hp->momentum < 1.0))
     return fail(MFSDP_E_INVALID, "momentum must be in [0, 1)");
   if (hp->nesterov != 0 && hp->nesterov != 1) return fail(MFSDP_E_INVALID, "nesterov must be 0 or 1");
-  if (!std::isfinite(hp->a) || !std::isfinite(hp->b) || !std::isfinite(hp->c))
-    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
   if (hp->ns_steps < 0 || hp->ns_steps >= 100) return fail(MFSDP_E_INVALID, "ns_steps must be in [0, 100)");
+  if (hp->ns_schedule) {
+    for (int i = 0; i < 3 * hp->ns_steps; ++i)
+      if (!std::isfinite(hp->ns_schedule[i]))
+        return fail(MFSDP_E_INVALID, "ns_schedule entry %d is not finite", i);
+  } else if (!std::isfinite(hp->a) || !std::isfinite(hp->b) || !std::isfinite(hp->c)) {
+    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
+  }
   if (!(hp->eps > 0.0) || !std::isfinite(hp->eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
   if (hp->lr_adjust < MFSDP_LR_NONE || hp->lr_adjust > MFSDP_LR_MATCH_RMS_ADAMW)
     return fail(MFSDP_E_INVALID, "unknown lr_adjust %d", hp->lr_adjust);
@@ -336,6 +341,17 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   return P;
 }
 
+// Coefficients of every NS step: the schedule if given, else the fixed triple.
+std::vector<double> step_coeffs(double a, double b, double c, int steps, const double* schedule) {
+  std::vector<double> v(3 * size_t(steps));
+  for (int k = 0; k < steps; ++k) {
+    v[3 * k] = schedule ? schedule[3 * k] : a;
+    v[3 * k + 1] = schedule ? schedule[3 * k + 1] : b;
+    v[3 * k + 2] = schedule ? schedule[3 * k + 2] : c;
+  }
+  return v;
+}
+
 // On the bf16 path with at least one NS step the last update product applies the parameter update
 // in its epilogue (from the fp32 accumulators); otherwise a separate apply pass reads the iterate.
 bool apply_fused(int ns_dtype, int steps) { return ns_dtype == MFSDP_BF16 && steps >= 1; }
@@ -372,14 +388,14 @@ void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, u
       if (phase == 0) {
         d.ldp = d.ldq = p.s_pad; d.lde = 0; d.ldc = p.r_pad; d.ldct = 0;
         d.M = d.N = int(p.r_pad); d.K = int(p.s_pad);
-        d.alpha = 1.0f; d.beta = 0.0f; d.diag = 0.0f; d.alpha_scale_pow = 2; d.beta_scale_pow = 0;
+        d.alpha = 1.0f; d.beta = 0.0f; d.alpha_scale_pow = 2; d.beta_scale_pow = 0;
         d.sym = 1; d.tiles_m = d.tiles_n = tr;
         d.tile_count = tr * (tr + 1) / 2;
         d.last_c = 1; d.last_ct = 0;
       } else if (phase == 1) {
         d.ldp = d.ldq = d.lde = d.ldc = p.r_pad; d.ldct = 0;
         d.M = d.N = d.K = int(p.r_pad);
-        d.alpha = float(hp.c); d.beta = float(hp.b); d.diag = float(hp.a);
+        d.alpha = 0.0f; d.beta = 0.0f;  // the step's (a, b, c) come with each launch
         d.alpha_scale_pow = 0; d.beta_scale_pow = 0;
         d.sym = 1; d.tiles_m = d.tiles_n = tr;
         d.tile_count = tr * (tr + 1) / 2;
@@ -387,7 +403,7 @@ void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, u
       } else {
         d.ldp = p.r_pad; d.ldq = p.r_pad; d.lde = 0; d.ldc = p.s_pad; d.ldct = p.r_pad;
         d.M = int(p.r_pad); d.N = int(p.s_pad); d.K = int(p.r_pad);
-        d.alpha = 1.0f; d.beta = 0.0f; d.diag = 0.0f; d.alpha_scale_pow = 1; d.beta_scale_pow = 0;
+        d.alpha = 1.0f; d.beta = 0.0f; d.alpha_scale_pow = 1; d.beta_scale_pow = 0;
         d.sym = 0; d.tiles_m = tr; d.tiles_n = ts;
         d.tile_count = tr * ts;
         // the final iterate is read in the parameter's orientation only
@@ -458,9 +474,10 @@ int record(void* const* events, int k, hipStream_t st) {
   return e == hipSuccess ? MFSDP_OK : hip_fail(e, "hipEventRecord");
 }
 
-int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dtype, double beta,
-                     int nesterov, double eps, int prep_tiles, int apply_tiles, hipStream_t st,
-                     void* const* events) {
+// coeffs: 3 * steps doubles, (a_k, b_k, c_k) of NS step k.
+int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const double* coeffs,
+                     int ns_dtype, double beta, int nesterov, double eps, int prep_tiles,
+                     int apply_tiles, hipStream_t st, void* const* events) {
   const int count = int(P.ns.size());
   const DescLayout& dl = P.dl;
   int rc = ring().upload(slot, ws, dl.bytes, st);
@@ -477,7 +494,8 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dty
     for (int ph = 0; ph < 3; ++ph) {
       e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, P.tiles[ph],
                       reinterpret_cast<const TileRef*>(ws + dl.off_sched[ph]), dl.ngroups[ph],
-                      ns_dtype, ph, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0, st);
+                      ns_dtype, ph, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0,
+                      float(coeffs[3 * k]), float(coeffs[3 * k + 1]), float(coeffs[3 * k + 2]), st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }
   }
@@ -489,6 +507,10 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, int ns_dty
   }
   return record(events, 3, st);
 }
+
+int ns_impl(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m, int64_t n,
+            const double* coeffs, int32_t steps, double eps, int32_t ns_dtype, void* workspace,
+            size_t workspace_bytes, void* stream);
 
 }  // namespace
 
@@ -572,8 +594,9 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
   }
   const int tile = hp->ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
   fill_gemm_descs(P, ws, *hp, h, tile);
-  return enqueue_pipeline(P, ws, slot, hp->ns_steps, hp->ns_dtype, hp->momentum, hp->nesterov,
-                          hp->eps, prep_tiles, apply_tiles, st, events);
+  const std::vector<double> coeffs = step_coeffs(hp->a, hp->b, hp->c, hp->ns_steps, hp->ns_schedule);
+  return enqueue_pipeline(P, ws, slot, hp->ns_steps, coeffs.data(), hp->ns_dtype, hp->momentum,
+                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events);
 }
 
 size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype) {
@@ -587,6 +610,36 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
                         int64_t n, double a, double b, double c, int32_t steps, double eps,
                         int32_t ns_dtype, void* workspace, size_t workspace_bytes, void* stream) {
   g_last_error.clear();
+  if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
+    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
+  if (steps < 0 || steps >= 100) return fail(MFSDP_E_INVALID, "steps must be in [0, 100)");
+  const std::vector<double> coeffs = step_coeffs(a, b, c, steps, nullptr);
+  return ns_impl(x, x_dtype, out, out_dtype, m, n, coeffs.data(), steps, eps, ns_dtype, workspace,
+                 workspace_bytes, stream);
+}
+
+int mfsdp_newton_schulz_schedule(const void* x, int32_t x_dtype, void* out, int32_t out_dtype,
+                                 int64_t m, int64_t n, const double* coeffs, int32_t steps,
+                                 double eps, int32_t ns_dtype, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (steps < 0 || steps >= 100) return fail(MFSDP_E_INVALID, "steps must be in [0, 100)");
+  if (steps > 0 && !coeffs) return fail(MFSDP_E_INVALID, "coeffs is NULL");
+  for (int i = 0; i < 3 * steps; ++i)
+    if (!std::isfinite(coeffs[i])) return fail(MFSDP_E_INVALID, "coeffs entry %d is not finite", i);
+  return ns_impl(x, x_dtype, out, out_dtype, m, n, coeffs, steps, eps, ns_dtype, workspace,
+                 workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Standalone NS: prep in copy mode (no momentum), the NS products, the output written by the last
+// update (bf16) or by the apply pass. coeffs: 3 * steps validated doubles.
+int ns_impl(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_t m, int64_t n,
+            const double* coeffs, int32_t steps, double eps, int32_t ns_dtype, void* workspace,
+            size_t workspace_bytes, void* stream) {
   if (!x || !out) return fail(MFSDP_E_INVALID, "x and out must be non-NULL");
   if (x == out) return fail(MFSDP_E_INVALID, "out must not alias x");
   if (!valid_dtype(x_dtype) || !valid_dtype(out_dtype) || !valid_dtype(ns_dtype))
@@ -594,10 +647,7 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   int rc = check_shape(m, n, "matrix", 0);
   if (rc) return rc;
   if (!aligned16(x) || !aligned16(out)) return fail(MFSDP_E_INVALID, "pointers must be 16-byte aligned");
-  if (steps < 0 || steps >= 100) return fail(MFSDP_E_INVALID, "steps must be in [0, 100)");
   if (!(eps > 0.0) || !std::isfinite(eps)) return fail(MFSDP_E_INVALID, "eps must be > 0");
-  if (!std::isfinite(a) || !std::isfinite(b) || !std::isfinite(c))
-    return fail(MFSDP_E_INVALID, "NS coefficients must be finite");
   const Plan P = make_plan(1, ns_dtype, [&](int64_t, int64_t& mm, int64_t& nn) { mm = m; nn = n; });
   const DescLayout& dl = P.dl;
   const std::vector<NsPlan>& plans = P.ns;
@@ -624,15 +674,18 @@ int mfsdp_newton_schulz(const void* x, int32_t x_dtype, void* out, int32_t out_d
   norm[0].scale = reinterpret_cast<float*>(ws + p.off_scale);
   apply[0] = make_apply(p, ws, steps, out, out_dtype, nullptr, 1, 1.0f, 0.0f, 0);
   mfsdp_muon_hparams hp{};
-  hp.a = a; hp.b = b; hp.c = c;
   hp.ns_steps = steps;
   hp.ns_dtype = ns_dtype;
   const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
   fill_gemm_descs(P, ws, hp, h, tile);
-  return enqueue_pipeline(P, ws, slot, steps, ns_dtype, 0.0, 0, eps,
+  return enqueue_pipeline(P, ws, slot, steps, coeffs, ns_dtype, 0.0, 0, eps,
                           p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n, st,
                           nullptr);
 }
+
+}  // namespace
+
+extern "C" {
 
 int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,
                      double beta2, double eps, double weight_decay, int64_t step, void* stream) {

@@ -95,8 +95,7 @@ struct GemmDesc {
   const float* scale;    // per-matrix norm scale (used on the first NS step), may be null
   int64_t ldp, ldq, lde, ldc, ldct;
   int32_t M, N, K;       // padded sizes, multiples of the tile
-  float alpha, beta;
-  float diag;            // added to the diagonal elements (i == j) after the axpby
+  float alpha, beta;     // (the square product takes its coefficients per launch instead)
   int32_t alpha_scale_pow;  // on the first step alpha *= scale^pow
   int32_t beta_scale_pow;
   int32_t sym;           // 1: only tiles bi <= bj, stored to (bi,bj) and mirrored to (bj,bi)
@@ -148,9 +147,10 @@ hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int 
                        float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
 // product: 0 Gram, 1 square, 2 update (the order of the products in one NS step)
+// (ca, cb, cc): the NS step's coefficients (a_k, b_k, c_k), used by the square product.
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
                        int ngroups, int ns_dtype, int product, int parity, int first_step,
-                       int last_step, hipStream_t st);
+                       int last_step, float ca, float cb, float cc, hipStream_t st);
 hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
                         hipStream_t st);
 hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);

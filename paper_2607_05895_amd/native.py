@@ -19,8 +19,9 @@ OK, E_INVALID, E_WORKSPACE, E_HIP = 0, -1, -2, -3
 _NS_DT = {"bf16": BF16, "f32": F32}
 _LR_MODES = {"none": LR_NONE, "original": LR_ORIGINAL, "match_rms_adamw": LR_MATCH_RMS_ADAMW}
 EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_timed", "mfsdp_ns_workspace_size",
-           "mfsdp_newton_schulz", "mfsdp_adamw_step", "mfsdp_last_error", "mfsdp_status_string",
-           "mfsdp_abi_version")
+           "mfsdp_newton_schulz", "mfsdp_newton_schulz_schedule", "mfsdp_adamw_step", "mfsdp_last_error",
+           "mfsdp_status_string", "mfsdp_abi_version")
+ABI_VERSION = 2
 
 
 class MuonEntry(ctypes.Structure):
@@ -35,7 +36,8 @@ class MuonHParams(ctypes.Structure):
                 ("momentum", ctypes.c_double), ("nesterov", ctypes.c_int32),
                 ("a", ctypes.c_double), ("b", ctypes.c_double), ("c", ctypes.c_double),
                 ("ns_steps", ctypes.c_int32), ("eps", ctypes.c_double),
-                ("lr_adjust", ctypes.c_int32), ("ns_dtype", ctypes.c_int32)]
+                ("lr_adjust", ctypes.c_int32), ("ns_dtype", ctypes.c_int32),
+                ("ns_schedule", ctypes.POINTER(ctypes.c_double))]
 
 
 class AdamWEntry(ctypes.Structure):
@@ -78,6 +80,9 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_ns_workspace_size.argtypes = [i64, i64, i32]
         L.mfsdp_ns_workspace_size.restype = sz
         L.mfsdp_newton_schulz.argtypes = [vp, i32, vp, i32, i64, i64, f64, f64, f64, i32, f64, i32, vp, sz, vp]
+        L.mfsdp_newton_schulz_schedule.restype = ctypes.c_int
+        L.mfsdp_newton_schulz_schedule.argtypes = [vp, i32, vp, i32, i64, i64, ctypes.POINTER(f64), i32, f64,
+                                                   i32, vp, sz, vp]
         L.mfsdp_newton_schulz.restype = ctypes.c_int
         L.mfsdp_adamw_step.argtypes = [ctypes.POINTER(AdamWEntry), i64, f64, f64, f64, f64, f64, i64, vp]
         L.mfsdp_adamw_step.restype = ctypes.c_int
@@ -151,6 +156,20 @@ def mfsdp_newton_schulz(x: int, x_dtype: int, out: int, out_dtype: int, m: int, 
                                      ns_dtype, workspace, workspace_bytes, stream))
 
 
+def _coeff_array(triples):
+    flat = [float(v) for t in triples for v in t]
+    return (ctypes.c_double * max(len(flat), 1))(*flat)
+
+
+def mfsdp_newton_schulz_schedule(x: int, x_dtype: int, out: int, out_dtype: int, m: int, n: int,
+                                 schedule, eps: float, ns_dtype: int, workspace: int,
+                                 workspace_bytes: int, stream: int = 0) -> None:
+    """schedule: a sequence of (a_k, b_k, c_k), one per NS step."""
+    arr = _coeff_array(schedule)
+    _check(lib().mfsdp_newton_schulz_schedule(x, x_dtype, out, out_dtype, m, n, arr, len(schedule),
+                                              eps, ns_dtype, workspace, workspace_bytes, stream))
+
+
 def mfsdp_adamw_step(entries: Sequence[AdamWEntry], lr: float, beta1: float, beta2: float,
                      eps: float, weight_decay: float, step: int, stream: int = 0) -> None:
     arr, n = _entries(entries, AdamWEntry)
@@ -174,10 +193,16 @@ def _stream() -> int:
 
 
 def muon_hparams(lr=0.02, weight_decay=0.0, momentum=0.95, nesterov=True, a=3.4445, b=-4.7750,
-                 c=2.0315, ns_steps=5, eps=1e-7, lr_adjust="original", ns_dtype="bf16") -> MuonHParams:
-    return MuonHParams(lr, weight_decay, momentum, int(bool(nesterov)), a, b, c, ns_steps, eps,
-                       _LR_MODES[lr_adjust] if isinstance(lr_adjust, str) else int(lr_adjust),
-                       _NS_DT[ns_dtype] if isinstance(ns_dtype, str) else int(ns_dtype))
+                 c=2.0315, ns_steps=5, eps=1e-7, lr_adjust="original", ns_dtype="bf16",
+                 ns_schedule=None) -> MuonHParams:
+    """ns_schedule: None, or one (a_k, b_k, c_k) per NS step (the array is kept on the struct)."""
+    hp = MuonHParams(lr, weight_decay, momentum, int(bool(nesterov)), a, b, c, ns_steps, eps,
+                     _LR_MODES[lr_adjust] if isinstance(lr_adjust, str) else int(lr_adjust),
+                     _NS_DT[ns_dtype] if isinstance(ns_dtype, str) else int(ns_dtype), None)
+    if ns_schedule is not None:
+        hp._schedule = _coeff_array(ns_schedule)  # keeps the memory alive as long as hp
+        hp.ns_schedule = hp._schedule
+    return hp
 
 
 def muon_entry_t(param, grad, momentum, update_out=None) -> MuonEntry:
@@ -205,6 +230,16 @@ def newton_schulz_t(x, out, a=3.4445, b=-4.7750, c=2.0315, steps=5, eps=1e-7, ns
         workspace = torch.empty(mfsdp_ns_workspace_size(m, n, nsd), dtype=torch.uint8, device=x.device)
     mfsdp_newton_schulz(x.data_ptr(), _dt(x), out.data_ptr(), _dt(out), m, n, a, b, c, steps, eps,
                         nsd, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def newton_schulz_schedule_t(x, out, schedule, eps=1e-7, ns_dtype="bf16", workspace=None) -> None:
+    import torch
+    m, n = x.shape
+    nsd = BF16 if ns_dtype in ("bf16", BF16) else F32
+    if workspace is None:
+        workspace = torch.empty(mfsdp_ns_workspace_size(m, n, nsd), dtype=torch.uint8, device=x.device)
+    mfsdp_newton_schulz_schedule(x.data_ptr(), _dt(x), out.data_ptr(), _dt(out), m, n, schedule, eps,
+                                 nsd, workspace.data_ptr(), workspace.numel(), _stream())
 
 
 def adamw_entry_t(param, grad, exp_avg, exp_avg_sq) -> AdamWEntry:

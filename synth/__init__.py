@@ -91,6 +91,7 @@ class MuonHParams:
     eps: float = 1e-7
     lr_adjust: str = "original"    # "none" | "original" | "match_rms_adamw"
     ns_dtype: str = BF16
+    ns_schedule: tuple = None      # None, or one (a, b, c) triple per NS step
 
 
 @dataclasses.dataclass

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert native.mfsdp_abi_version() == 1
+    assert native.mfsdp_abi_version() == native.ABI_VERSION == 2
     assert native.mfsdp_status_string(0) == "MFSDP_OK"
     assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
     assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
@@ -63,6 +63,37 @@ def test_muon_rejects_bad_hparams(bad):
     with pytest.raises(native.MfsdpError) as ei:
         native.mfsdp_muon_step([_entry()], hp, FAKE * 16, 1 << 40, 0)
     assert ei.value.status == native.E_INVALID
+
+
+@pytest.mark.parametrize("sched", [[(3.4, -4.7, float("nan"))] * 5, [(float("inf"), 0.0, 0.0)] * 5])
+def test_muon_rejects_non_finite_schedule(sched):
+    hp = native.muon_hparams(ns_schedule=sched)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry()], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+def test_schedule_replaces_the_fixed_triple_in_validation():
+    # with a schedule the (a, b, c) fields are not used, so they may be anything
+    hp = native.muon_hparams(a=float("nan"), ns_schedule=[(3.4445, -4.775, 2.0315)] * 5)
+    assert native.mfsdp_muon_workspace_size([_entry()], hp) > 0
+
+
+def test_newton_schulz_schedule_argument_checks():
+    ws = native.mfsdp_ns_workspace_size(64, 64, native.BF16)
+    good = [(3.4445, -4.775, 2.0315)] * 3
+    for sched, kw in [([(1.0, float("nan"), 0.0)] * 3, {}), (good, dict(m=0)), (good, dict(x_dtype=3)),
+                      ([(1.0, 0.0, 0.0)] * 100, {})]:
+        args = dict(x=FAKE, x_dtype=1, out=FAKE * 2, out_dtype=1, m=64, n=64, schedule=sched,
+                    eps=1e-7, ns_dtype=1, workspace=FAKE * 16, workspace_bytes=ws, stream=0)
+        args.update(kw)
+        with pytest.raises(native.MfsdpError) as ei:
+            native.mfsdp_newton_schulz_schedule(**args)
+        assert ei.value.status == native.E_INVALID
+    # NULL coefficients with steps > 0
+    L = native.lib()
+    assert L.mfsdp_newton_schulz_schedule(FAKE, 1, FAKE * 2, 1, 64, 64, None, 3, 1e-7, 1, FAKE * 16,
+                                          ws, None) == native.E_INVALID
 
 
 def test_muon_workspace_checks():

@@ -131,7 +131,8 @@ def _run_muon(native, tensors, specs, hp, with_update=True):
         ents.append(native.muon_entry_t(p, g, mo, uo))
     h = native.muon_hparams(lr=hp.lr, weight_decay=hp.weight_decay, momentum=hp.momentum,
                             nesterov=hp.nesterov, a=hp.a, b=hp.b, c=hp.c, ns_steps=hp.ns_steps,
-                            eps=hp.eps, lr_adjust=hp.lr_adjust, ns_dtype=hp.ns_dtype)
+                            eps=hp.eps, lr_adjust=hp.lr_adjust, ns_dtype=hp.ns_dtype,
+                            ns_schedule=hp.ns_schedule)
     ws = native.muon_workspace_t(ents, h)
     native.muon_step_t(ents, h, ws)
     _sync()
@@ -144,7 +145,7 @@ def _check_muon(tensors, specs, dev, hp, upd_tol):
         p_or, buf_or, O = oracle.muon_step(
             t.param, t.grad, t.momentum, lr=hp.lr, weight_decay=hp.weight_decay,
             momentum=hp.momentum, nesterov=hp.nesterov, a=hp.a, b=hp.b, c=hp.c,
-            ns_steps=hp.ns_steps, eps=hp.eps, lr_adjust=hp.lr_adjust)
+            ns_steps=hp.ns_steps, eps=hp.eps, lr_adjust=hp.lr_adjust, ns_schedule=hp.ns_schedule)
         assert rel_fro(from_dev(mo), buf_or) <= 1e-6, (e.name, "momentum")
         if uo is not None:
             err = rel_fro(from_dev(uo), O)
@@ -320,3 +321,59 @@ def test_adamw_matches_oracle(native, step):
                 else np.zeros_like(p_or))
         bound = half + 1e-6 * np.abs(p_or - p0) + 4 * 2.0 ** -24 * np.abs(p_or)
         assert np.all(np.abs(pg - p_or) <= bound), float(np.max(np.abs(pg - p_or) - bound))
+
+
+# ------------------------------------------------------------------ per-step NS coefficient schedules
+
+# Schedules that keep every singular value bounded (a schedule that lets them grow, e.g. random
+# perturbations of the triple, amplifies bf16 rounding beyond the tolerance on the bf16 path, in the
+# kernel and in a CPU emulation of its rounding alike):
+# two steps of the fixed triple, then three of the quintic p(s) = (15 s - 10 s^3 + 3 s^5) / 8
+# (p(1) = 1, p'(1) = p''(1) = 0)
+PADE_SCHEDULE = [(A, B, C)] * 2 + [(1.875, -1.25, 0.375)] * 3
+# three quintic steps then the textbook cubic iteration (a, b, c) = (1.5, -0.5, 0)
+MIXED_SCHEDULE = [(A, B, C)] * 3 + [(1.5, -0.5, 0.0)] * 3
+
+
+@pytest.mark.parametrize("ns_dtype,tol", [("bf16", 2e-2), ("f32", 1e-4)])
+@pytest.mark.parametrize("shape", [(256, 512), (513, 257), (100, 700)])
+@pytest.mark.parametrize("which", ["pade", "mixed"])
+def test_ns_schedule_matches_oracle(native, ns_dtype, tol, shape, which):
+    import torch
+    m, n = shape
+    sched = PADE_SCHEDULE if which == "pade" else MIXED_SCHEDULE
+    _say(f"ns schedule {which} {ns_dtype} {m}x{n}")
+    rng = np.random.default_rng(310 + m + n)
+    x = rng.standard_normal((m, n), dtype=np.float32)
+    xd = to_dev(x, synth.F32)
+    out = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    native.newton_schulz_schedule_t(xd, out, sched, 1e-7, ns_dtype)
+    _sync()
+    ref = oracle.newton_schulz(x, A, B, C, len(sched), schedule=sched)
+    err = rel_fro(from_dev(out), ref)
+    assert err <= tol, err
+
+
+@pytest.mark.parametrize("ns_dtype", ["bf16", "f32"])
+def test_ns_constant_schedule_is_bitwise_the_fixed_triple(native, ns_dtype):
+    import torch
+    m, n = 384, 640
+    rng = np.random.default_rng(320)
+    xd = to_dev(rng.standard_normal((m, n), dtype=np.float32), synth.F32)
+    o1 = torch.empty((m, n), dtype=torch.float32, device="cuda")
+    o2 = torch.empty_like(o1)
+    native.newton_schulz_t(xd, o1, A, B, C, 5, 1e-7, ns_dtype)
+    native.newton_schulz_schedule_t(xd, o2, [(A, B, C)] * 5, 1e-7, ns_dtype)
+    _sync()
+    assert torch.equal(o1, o2)
+
+
+def test_muon_with_schedule_matches_oracle(native):
+    _say("muon schedule")
+    rng = np.random.default_rng(330)
+    shapes = [(256, 512), (512, 256), (100, 700), (700, 100), (384, 384)]
+    specs = [synth.MuonSpec(m, n, f"s{m}x{n}") for (m, n) in shapes]
+    tensors = [synth.random_muon_tensors(rng, e.m, e.n) for e in specs]
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01, ns_steps=5, ns_schedule=tuple(PADE_SCHEDULE))
+    dev = _run_muon(native, tensors, specs, hp)
+    _check_muon(tensors, specs, dev, hp, 2e-2)
