@@ -29,5 +29,7 @@ from .muon import (  # noqa: F401
     apply_update,
     muon_step,
     scalar_ns_map,
+    reduce_gradients,
+    step_coefficients,
 )
 from .adamw import adamw_step  # noqa: F401

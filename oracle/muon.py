@@ -56,6 +56,22 @@ def momentum_update(grad: np.ndarray, buf: np.ndarray, beta: float,
     return b_new, u
 
 
+def reduce_gradients(parts, scale: float = 1.0) -> np.ndarray:
+    """Owner-side gradient reduction (Section 4.2, owner-segment collectives): every rank of the
+    shard span contributes its full-gradient buffer for the matrix and the owner keeps the
+    reduced result. Reading: the reduction is the sum of the W contributions times ``scale``
+    (1 / W for the data-parallel mean), formed here exactly in float64."""
+    parts = [_f64(p) for p in parts]
+    if not parts:
+        raise ValueError("at least one gradient part")
+    total = np.zeros_like(parts[0])
+    for p in parts:
+        if p.shape != total.shape:
+            raise ValueError("gradient parts must share one shape")
+        total = total + p
+    return total * float(scale)
+
+
 def frobenius_normalize(x: np.ndarray, eps: float) -> np.ndarray:
     """X0 = X / max(||X||_F, eps): bounds the spectral norm by 1 before NS (clamped-norm reading)."""
     x = _f64(x)

@@ -405,3 +405,43 @@ def test_schedule_matches_svd_brute_force(shape):
 def test_schedule_length_must_match_steps():
     with pytest.raises(ValueError):
         oracle.newton_schulz(np.ones((3, 4)), A, B, C, 2, schedule=[(A, B, C)])
+
+
+# ---------------------------------------------------------------- owner-side gradient reduction
+
+def test_reduce_single_part_is_identity():
+    rng = np.random.default_rng(50)
+    g = f32_to_bf16_bits(rng.standard_normal((7, 9)).astype(np.float32))
+    assert np.array_equal(oracle.reduce_gradients([g]), bf16_bits_to_f32(g).astype(np.float64))
+
+
+def test_reduce_identical_parts_and_mean():
+    rng = np.random.default_rng(51)
+    g = rng.standard_normal((5, 6)).astype(np.float32)
+    W = 8
+    s = oracle.reduce_gradients([g] * W)
+    np.testing.assert_array_equal(s, W * g.astype(np.float64))  # exact: W is a power of two
+    np.testing.assert_array_equal(oracle.reduce_gradients([g] * W, 1.0 / W), g.astype(np.float64))
+
+
+def test_reduce_is_the_plain_sum_on_integers():
+    # integer-valued parts: every partial sum is exact, so the result must equal the integer sum in
+    # any order
+    rng = np.random.default_rng(52)
+    parts = [rng.integers(-100, 100, size=(4, 5)).astype(np.float32) for _ in range(6)]
+    want = sum(p.astype(np.int64) for p in parts).astype(np.float64) * 0.5
+    np.testing.assert_array_equal(oracle.reduce_gradients(parts, 0.5), want)
+    np.testing.assert_array_equal(oracle.reduce_gradients(parts[::-1], 0.5), want)
+
+
+def test_reduce_then_muon_equals_muon_of_the_sum():
+    rng = np.random.default_rng(53)
+    parts = [rng.standard_normal((12, 20)) * 1e-3 for _ in range(3)]
+    p0 = rng.standard_normal((12, 20)) * 0.02
+    m0 = np.zeros((12, 20))
+    g = parts[0] + parts[1] + parts[2]
+    kw = dict(lr=0.02, weight_decay=0.01, momentum=0.95, nesterov=True, a=A, b=B, c=C, ns_steps=5)
+    r1 = oracle.muon_step(p0, oracle.reduce_gradients(parts), m0, **kw)
+    r2 = oracle.muon_step(p0, g, m0, **kw)
+    for x, y in zip(r1, r2):
+        np.testing.assert_allclose(x, y, rtol=0, atol=1e-15)
