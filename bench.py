@@ -125,6 +125,43 @@ def traffic_record(workload_name: str):
         return None
 
 
+def time_reduction(args, native, wl, keep, ents, h, ws, stream, hev, plain_step_ms, plain_prep_ms, es_g):
+    """Time mfsdp_muon_step_reduce with W gradient parts per matrix (parts derived on the device
+    from each matrix's gradient: the values do not change the cost). The reduction runs inside the
+    momentum pass, so its time is the step time minus the plain step's, plus the plain pass."""
+    import torch
+    import synth
+    W = args.grad_parts
+    parts = []
+    for (p, g, mo) in keep[:len(ents)]:
+        parts.append([(g.float() * (1.0 + 0.01 * w)).to(g.dtype) for w in range(W)])
+    torch.cuda.synchronize()
+
+    def rstep():
+        native.muon_step_reduce_t(ents, parts, 1.0 / W, h, ws)
+    for _ in range(args.warmup):
+        rstep()
+    torch.cuda.synchronize()
+    e0, e1 = hev.create(), hev.create()
+    hev.record(e0, stream)
+    for _ in range(args.steps):
+        rstep()
+    hev.record(e1, stream)
+    torch.cuda.synchronize()
+    step_ms = hev.elapsed_ms(e0, e1) / args.steps
+    prep_ms = plain_prep_ms + (step_ms - plain_step_ms)
+    elts = wl.muon_elements()
+    es_ns = 2 if wl.hp.ns_dtype == synth.BF16 else 4
+    nbytes = elts * (W * es_g + 8 + 2 * es_ns)      # W parts, momentum in/out, u and u^T
+    log(f"reduction W={W}: step {step_ms:.3f} ms, fused momentum+reduction pass ~{prep_ms:.3f} ms "
+        f"({nbytes / (prep_ms * 1e-3) / 1e9:.0f} GB/s)")
+    return {"grad_parts": W, "ms_per_step": round(step_ms, 4), "reduce_prep_ms": round(prep_ms, 4),
+            "reduce_prep_bytes": nbytes,
+            "reduce_prep_GBps": round(nbytes / (prep_ms * 1e-3) / 1e9, 1),
+            "reduce_prep_frac_hbm": round(nbytes / (prep_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "note": "pass time = reduce-step time - plain-step time + plain momentum-pass time"}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,6 +169,9 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="owner share 1..5 (default 3: Llama-3-8B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--grad-parts", type=int, default=0,
+                    help="also time the owner-side gradient reduction fused with the step: each "
+                         "matrix's gradient arrives as this many full-size parts (shard span W)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB -> 1 GiB elementwise copy kernel (the "
                          "reference dispatch for scaling HBM counters)")
@@ -301,6 +341,9 @@ def main() -> int:
             "adamw_GBps": round(adamw_bytes / (adamw_ms * 1e-3) / 1e9, 1) if adamw_ms else None,
         },
     }
+    if args.grad_parts > 0:
+        out["grad_reduction"] = time_reduction(args, native, wl, keep, ents, h, ws, stream, hev,
+                                               ms_per_step, prep_ms, es_g)
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])

@@ -118,10 +118,11 @@ typedef struct {
   int32_t grad_dtype;
 } mfsdp_adamw_entry;
 
-/* Bytes of device workspace mfsdp_muon_step needs for these entries and hyperparameters
- * (Newton-Schulz iterates in both layouts, the r x r Gram and polynomial matrices, norm
- * partials and launch descriptors). Returns 0 if the arguments are invalid (see
- * mfsdp_last_error). count == 0 returns 0 with no error. */
+/* Bytes of device workspace mfsdp_muon_step (and mfsdp_muon_step_reduce) needs for these entries
+ * and hyperparameters (Newton-Schulz iterates in both layouts, the r x r Gram and polynomial
+ * matrices, norm partials and launch descriptors); the entries' data pointers are not used.
+ * Returns 0 if the arguments are invalid (see mfsdp_last_error). count == 0 returns 0 with no
+ * error. */
 size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,
                                  const mfsdp_muon_hparams* hp);
 
@@ -139,6 +140,28 @@ int mfsdp_muon_step(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_
 int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
                           const mfsdp_muon_hparams* hp, void* workspace, size_t workspace_bytes,
                           void* stream, void* const* events);
+
+/* Most gradient parts one entry of mfsdp_muon_step_reduce may have (the paper's largest shard
+ * span is 64 ranks). */
+#define MFSDP_MAX_GRAD_PARTS 64
+
+/* Owner-side gradient reduction fused with the Muon step. In owner placement every rank of the
+ * shard span contributes its full-gradient buffer of a matrix and the reduced result is kept only
+ * in the owner's segment (Section 4.2, owner-segment collectives); here the owner has received the
+ * nparts contributions and the reduction runs inside the momentum pass. For entry i the Muon input
+ * gradient is
+ *     g_i = grad_scale * (P_i0 + P_i1 + ... + P_i,nparts-1)      (fp32, summed in that order)
+ * with P_iw = grad_parts[i * nparts + w]: m x n, entries[i].grad_dtype, device memory, read only,
+ * 16-byte aligned. grad_scale = 1 / nparts gives the data-parallel mean; it must be finite.
+ *   1 <= nparts <= MFSDP_MAX_GRAD_PARTS; entries[i].grad is not read (may be NULL).
+ *   reduced_out: NULL, or a host array of count device pointers, each NULL or an m x n buffer of
+ *                grad_dtype (16-byte aligned) that receives g_i (bf16: round to nearest even).
+ * Everything else as mfsdp_muon_step (same workspace size query); g_i enters the momentum pass
+ * unrounded. */
+int mfsdp_muon_step_reduce(const mfsdp_muon_entry* entries, int64_t count,
+                           const void* const* grad_parts, int32_t nparts, double grad_scale,
+                           void* const* reduced_out, const mfsdp_muon_hparams* hp, void* workspace,
+                           size_t workspace_bytes, void* stream);
 
 /* Bytes of workspace mfsdp_newton_schulz needs for one m x n matrix. 0 on invalid input. */
 size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype);

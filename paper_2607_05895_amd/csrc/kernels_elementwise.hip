@@ -123,7 +123,9 @@ struct PrepTraits {
   static constexpr int TW = NSDT == kDtBF16 ? kPrepColsBF16 : kPrepColsF32;
 };
 
-template <int NSDT>
+// RED: the entries' gradients are reductions of gradient parts (a separate instantiation keeps the
+// plain momentum pass at its register count).
+template <int NSDT, bool RED>
 __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ descs, int count,
                                                    float beta, float omb, int nesterov) {
   using T = typename PrepTraits<NSDT>::elem;
@@ -169,8 +171,30 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
     auto interior = [&](auto gdt) {
       constexpr int GDT = decltype(gdt)::value;
       V8 g[NP], mv[NP];
+      if constexpr (!RED) {
 #pragma unroll
-      for (int q = 0; q < NP; ++q) load8<GDT>(d.grad, (row0 + rr + RPP * q) * n + col0 + c8, g[q]);
+        for (int q = 0; q < NP; ++q) load8<GDT>(d.grad, (row0 + rr + RPP * q) * n + col0 + c8, g[q]);
+      } else {
+        // owner-side reduction of the shard span's contributions, in part order
+#pragma unroll
+        for (int q = 0; q < NP; ++q) load8<GDT>(d.parts[0], (row0 + rr + RPP * q) * n + col0 + c8, g[q]);
+        for (int w = 1; w < d.nparts; ++w) {
+          const void* pw = d.parts[w];
+          V8 t[NP];
+#pragma unroll
+          for (int q = 0; q < NP; ++q) load8<GDT>(pw, (row0 + rr + RPP * q) * n + col0 + c8, t[q]);
+#pragma unroll
+          for (int q = 0; q < NP; ++q)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) g[q].v[k] += t[q].v[k];
+        }
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) g[q].v[k] *= d.gscale;
+          if (d.gout) store8<GDT>(d.gout, (row0 + rr + RPP * q) * n + col0 + c8, g[q]);
+        }
+      }
       if (d.momentum) {
 #pragma unroll
         for (int q = 0; q < NP; ++q) load8<kDtF32>(d.momentum, (row0 + rr + RPP * q) * n + col0 + c8, mv[q]);
@@ -201,7 +225,23 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
       if (i < m && vec && j0 + 7 < n) {
         const int64_t idx = i * n + j0;
         V8 g;
-        if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, idx, g); else load8<kDtF32>(d.grad, idx, g);
+        if constexpr (!RED) {
+          if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.grad, idx, g); else load8<kDtF32>(d.grad, idx, g);
+        } else {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) g.v[k] = 0.0f;
+          for (int w = 0; w < d.nparts; ++w) {
+            V8 t;
+            if (d.grad_dtype == kDtBF16) load8<kDtBF16>(d.parts[w], idx, t); else load8<kDtF32>(d.parts[w], idx, t);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) g.v[k] = w == 0 ? t.v[k] : g.v[k] + t.v[k];
+          }
+#pragma unroll
+          for (int k = 0; k < 8; ++k) g.v[k] *= d.gscale;
+          if (d.gout) {
+            if (d.grad_dtype == kDtBF16) store8<kDtBF16>(d.gout, idx, g); else store8<kDtF32>(d.gout, idx, g);
+          }
+        }
         if (d.momentum) {
           V8 mv;
           load8<kDtF32>(d.momentum, idx, mv);
@@ -221,7 +261,15 @@ __global__ __launch_bounds__(256) void prep_kernel(const PrepDesc* __restrict__ 
           u.v[k] = 0.0f;
           if (i < m && j < n) {
             const int64_t idx = i * n + j;
-            const float g = load_as_f32(d.grad, idx, d.grad_dtype);
+            float g;
+            if constexpr (!RED) {
+              g = load_as_f32(d.grad, idx, d.grad_dtype);
+            } else {
+              g = load_as_f32(d.parts[0], idx, d.grad_dtype);
+              for (int w = 1; w < d.nparts; ++w) g += load_as_f32(d.parts[w], idx, d.grad_dtype);
+              g *= d.gscale;
+              if (d.gout) store_from_f32(d.gout, idx, g, d.grad_dtype);
+            }
             if (d.momentum) {
               float mv = d.momentum[idx];
               mv = mv + omb * (g - mv);
@@ -430,14 +478,23 @@ __global__ __launch_bounds__(256) void adamw_kernel(const AdamWBatch batch) {
 }  // namespace
 
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       float beta, float one_minus_beta, int nesterov, hipStream_t st) {
+                       int reduce, float beta, float one_minus_beta, int nesterov, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
+  if (reduce) {
+    if (ns_dtype == kDtBF16)
+      hipLaunchKernelGGL((prep_kernel<kDtBF16, true>), dim3(total_tiles), dim3(256), 0, st, d_descs,
+                         count, beta, one_minus_beta, nesterov);
+    else
+      hipLaunchKernelGGL((prep_kernel<kDtF32, true>), dim3(total_tiles), dim3(256), 0, st, d_descs,
+                         count, beta, one_minus_beta, nesterov);
+    return hipGetLastError();
+  }
   if (ns_dtype == kDtBF16)
-    hipLaunchKernelGGL(prep_kernel<kDtBF16>, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
-                       beta, one_minus_beta, nesterov);
+    hipLaunchKernelGGL((prep_kernel<kDtBF16, false>), dim3(total_tiles), dim3(256), 0, st, d_descs,
+                       count, beta, one_minus_beta, nesterov);
   else
-    hipLaunchKernelGGL(prep_kernel<kDtF32>, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
-                       beta, one_minus_beta, nesterov);
+    hipLaunchKernelGGL((prep_kernel<kDtF32, false>), dim3(total_tiles), dim3(256), 0, st, d_descs,
+                       count, beta, one_minus_beta, nesterov);
   return hipGetLastError();
 }
 

@@ -24,6 +24,8 @@
 
 using namespace mfsdp;
 
+static_assert(MFSDP_MAX_GRAD_PARTS == kMaxGradParts, "gradient part limit of the ABI and the descriptor");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -248,18 +250,21 @@ int check_shape(int64_t m, int64_t n, const char* what, int64_t i) {
   return MFSDP_OK;
 }
 
-int check_entries(const mfsdp_muon_entry* entries, int64_t count) {
+// need_grad: the entries' grad pointers are read (0 for the workspace query and the fused
+// reduction, which read no entry grad)
+int check_entries(const mfsdp_muon_entry* entries, int64_t count, bool need_grad = true) {
   if (count < 0) return fail(MFSDP_E_INVALID, "count must be >= 0");
   if (count > 0 && !entries) return fail(MFSDP_E_INVALID, "entries is NULL");
   if (count > (1 << 20)) return fail(MFSDP_E_INVALID, "too many entries");
   for (int64_t i = 0; i < count; ++i) {
     const mfsdp_muon_entry& e = entries[i];
-    if (!e.param || !e.grad || !e.momentum) return fail(MFSDP_E_INVALID, "entry %lld: NULL pointer", (long long)i);
+    if (!e.param || (need_grad && !e.grad) || !e.momentum)
+      return fail(MFSDP_E_INVALID, "entry %lld: NULL pointer", (long long)i);
     int st = check_shape(e.m, e.n, "entry", i);
     if (st) return st;
     if (!valid_dtype(e.param_dtype) || !valid_dtype(e.grad_dtype))
       return fail(MFSDP_E_INVALID, "entry %lld: unsupported dtype", (long long)i);
-    if (!aligned16(e.param) || !aligned16(e.grad) || !aligned16(e.momentum) ||
+    if (!aligned16(e.param) || (need_grad && !aligned16(e.grad)) || !aligned16(e.momentum) ||
         (e.update_out && !aligned16(e.update_out)))
       return fail(MFSDP_E_INVALID, "entry %lld: pointers must be 16-byte aligned", (long long)i);
   }
@@ -477,7 +482,7 @@ int record(void* const* events, int k, hipStream_t st) {
 // coeffs: 3 * steps doubles, (a_k, b_k, c_k) of NS step k.
 int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const double* coeffs,
                      int ns_dtype, double beta, int nesterov, double eps, int prep_tiles,
-                     int apply_tiles, hipStream_t st, void* const* events) {
+                     int apply_tiles, hipStream_t st, void* const* events, bool reduce = false) {
   const int count = int(P.ns.size());
   const DescLayout& dl = P.dl;
   int rc = ring().upload(slot, ws, dl.bytes, st);
@@ -485,7 +490,7 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const doub
   if ((rc = record(events, 0, st))) return rc;
   hipError_t e;
   e = launch_prep(reinterpret_cast<const PrepDesc*>(ws + dl.off_prep), count, prep_tiles, ns_dtype,
-                  float(beta), float(1.0 - beta), nesterov, st);
+                  reduce ? 1 : 0, float(beta), float(1.0 - beta), nesterov, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   e = launch_norm(reinterpret_cast<const NormDesc*>(ws + dl.off_norm), count, float(eps), st);
   if (e != hipSuccess) return hip_fail(e, "norm launch");
@@ -512,6 +517,17 @@ int ns_impl(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_
             const double* coeffs, int32_t steps, double eps, int32_t ns_dtype, void* workspace,
             size_t workspace_bytes, void* stream);
 
+// The fused owner-side gradient reduction of mfsdp_muon_step_reduce (validated).
+struct ReduceArgs {
+  const void* const* parts;  // count * nparts device pointers
+  int nparts;
+  double scale;
+  void* const* out;          // NULL or count pointers (each may be NULL)
+};
+int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
+              void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+              const ReduceArgs* ra);
+
 }  // namespace
 
 extern "C" {
@@ -533,7 +549,7 @@ const char* mfsdp_status_string(int status) {
 size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,
                                  const mfsdp_muon_hparams* hp) {
   g_last_error.clear();
-  if (check_hp(hp) || check_entries(entries, count)) return 0;
+  if (check_hp(hp) || check_entries(entries, count, false)) return 0;
   if (count == 0) return 0;
   return make_plan(count, hp->ns_dtype, [&](int64_t i, int64_t& m, int64_t& n) {
            m = entries[i].m;
@@ -550,9 +566,41 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
                           const mfsdp_muon_hparams* hp, void* workspace, size_t workspace_bytes,
                           void* stream, void* const* events) {
   g_last_error.clear();
+  return muon_impl(entries, count, hp, workspace, workspace_bytes, stream, events, nullptr);
+}
+
+int mfsdp_muon_step_reduce(const mfsdp_muon_entry* entries, int64_t count,
+                           const void* const* grad_parts, int32_t nparts, double grad_scale,
+                           void* const* reduced_out, const mfsdp_muon_hparams* hp, void* workspace,
+                           size_t workspace_bytes, void* stream) {
+  g_last_error.clear();
+  if (nparts < 1 || nparts > MFSDP_MAX_GRAD_PARTS)
+    return fail(MFSDP_E_INVALID, "nparts must be in [1, %d]", MFSDP_MAX_GRAD_PARTS);
+  if (!std::isfinite(grad_scale)) return fail(MFSDP_E_INVALID, "grad_scale must be finite");
+  if (count > 0 && !grad_parts) return fail(MFSDP_E_INVALID, "grad_parts is NULL");
+  for (int64_t i = 0; i < count; ++i) {
+    for (int w = 0; w < nparts; ++w) {
+      const void* pw = grad_parts[i * nparts + w];
+      if (!pw || !aligned16(pw))
+        return fail(MFSDP_E_INVALID, "entry %lld part %d: NULL or not 16-byte aligned", (long long)i, w);
+    }
+    if (reduced_out && reduced_out[i] && !aligned16(reduced_out[i]))
+      return fail(MFSDP_E_INVALID, "entry %lld: reduced_out not 16-byte aligned", (long long)i);
+  }
+  const ReduceArgs ra{grad_parts, nparts, grad_scale, reduced_out};
+  return muon_impl(entries, count, hp, workspace, workspace_bytes, stream, nullptr, &ra);
+}
+
+}  // extern "C"
+
+namespace {
+
+int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
+              void* workspace, size_t workspace_bytes, void* stream, void* const* events,
+              const ReduceArgs* ra) {
   int rc = check_hp(hp);
   if (rc) return rc;
-  rc = check_entries(entries, count);
+  rc = check_entries(entries, count, ra == nullptr);
   if (rc) return rc;
   if (count == 0) return MFSDP_OK;
   const Plan P = make_plan(count, hp->ns_dtype, [&](int64_t i, int64_t& m, int64_t& n) {
@@ -583,6 +631,12 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
     const mfsdp_muon_entry& en = entries[i];
     const NsPlan& p = plans[i];
     prep[i] = make_prep(p, ws, en.grad, en.grad_dtype, en.momentum, prep_tiles);
+    if (ra) {
+      prep[i].nparts = ra->nparts;
+      prep[i].gscale = float(ra->scale);
+      prep[i].gout = ra->out ? ra->out[i] : nullptr;
+      for (int w = 0; w < ra->nparts; ++w) prep[i].parts[w] = ra->parts[i * ra->nparts + w];
+    }
     prep_tiles += p.prep_tiles_m * p.prep_tiles_n;
     norm[i].partials = reinterpret_cast<const float*>(ws + p.off_partials);
     norm[i].count = p.prep_tiles_m * p.prep_tiles_n;
@@ -596,8 +650,12 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
   fill_gemm_descs(P, ws, *hp, h, tile);
   const std::vector<double> coeffs = step_coeffs(hp->a, hp->b, hp->c, hp->ns_steps, hp->ns_schedule);
   return enqueue_pipeline(P, ws, slot, hp->ns_steps, coeffs.data(), hp->ns_dtype, hp->momentum,
-                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events);
+                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events, ra != nullptr);
 }
+
+}  // namespace
+
+extern "C" {
 
 size_t mfsdp_ns_workspace_size(int64_t m, int64_t n, int32_t ns_dtype) {
   g_last_error.clear();

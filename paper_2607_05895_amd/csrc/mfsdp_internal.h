@@ -48,8 +48,10 @@ constexpr int kDtBF16 = 1;
 // ---------------------------------------------------------------------------------------------
 // prep: momentum EMA + Nesterov (or a plain copy for standalone NS), Sum u^2 partials, and the
 // NS input written in both layouts. One 64 x 64 tile of the stored m x n matrix per workgroup.
+constexpr int kMaxGradParts = 64;
+
 struct PrepDesc {
-  const void* grad;      // m x n, grad_dtype (the NS input for standalone NS)
+  const void* grad;      // m x n, grad_dtype (the NS input for standalone NS); unused if nparts > 0
   float* momentum;       // m x n fp32, or null for standalone NS
   void* d_out;           // u in stored orientation, padded, panel blocked with ld_d columns
   void* t_out;           // u^T, panel blocked with ld_t columns (ns dtype)
@@ -59,6 +61,12 @@ struct PrepDesc {
   int32_t tiles_m, tiles_n;  // over the padded domain, 64 x 64
   int32_t grad_dtype;
   int32_t tile_begin;    // first global tile index of this entry
+  // owner-side reduction: g = gscale * (parts[0] + ... + parts[nparts - 1]) in fp32, in that order,
+  // optionally stored to gout (grad_dtype); nparts == 0 reads grad instead
+  int32_t nparts;
+  float gscale;
+  void* gout;
+  const void* parts[kMaxGradParts];
 };
 
 // norm finalize: scale = 1 / max(sqrt(Sum partials), eps), deterministic order.
@@ -143,8 +151,9 @@ struct AdamWBatch {
 constexpr int kAdamWBlockElems = 2048;
 
 // Launchers (return hipError_t of the launch).
+// reduce: the descriptors' gradients are reductions of gradient parts (nparts >= 1 for all)
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
-                       float beta, float one_minus_beta, int nesterov, hipStream_t st);
+                       int reduce, float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
 // product: 0 Gram, 1 square, 2 update (the order of the products in one NS step)
 // (ca, cb, cc): the NS step's coefficients (a_k, b_k, c_k), used by the square product.

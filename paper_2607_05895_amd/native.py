@@ -20,7 +20,8 @@ _NS_DT = {"bf16": BF16, "f32": F32}
 _LR_MODES = {"none": LR_NONE, "original": LR_ORIGINAL, "match_rms_adamw": LR_MATCH_RMS_ADAMW}
 EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_timed", "mfsdp_ns_workspace_size",
            "mfsdp_newton_schulz", "mfsdp_newton_schulz_schedule", "mfsdp_adamw_step", "mfsdp_last_error",
-           "mfsdp_status_string", "mfsdp_abi_version")
+           "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce")
+MAX_GRAD_PARTS = 64
 ABI_VERSION = 2
 
 
@@ -77,6 +78,10 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_muon_step_timed.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams),
                                             vp, sz, vp, ctypes.POINTER(ctypes.c_void_p)]
         L.mfsdp_muon_step_timed.restype = ctypes.c_int
+        L.mfsdp_muon_step_reduce.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(ctypes.c_void_p),
+                                             i32, f64, ctypes.POINTER(ctypes.c_void_p),
+                                             ctypes.POINTER(MuonHParams), vp, sz, vp]
+        L.mfsdp_muon_step_reduce.restype = ctypes.c_int
         L.mfsdp_ns_workspace_size.argtypes = [i64, i64, i32]
         L.mfsdp_ns_workspace_size.restype = sz
         L.mfsdp_newton_schulz.argtypes = [vp, i32, vp, i32, i64, i64, f64, f64, f64, i32, f64, i32, vp, sz, vp]
@@ -140,6 +145,19 @@ def mfsdp_muon_step_timed(entries: Sequence[MuonEntry], hp: MuonHParams, workspa
     ev = (ctypes.c_void_p * 4)(*list(events))
     _check(lib().mfsdp_muon_step_timed(arr, n, ctypes.byref(hp), workspace, workspace_bytes,
                                        stream, ev))
+
+
+def mfsdp_muon_step_reduce(entries: Sequence[MuonEntry], grad_parts: Sequence[Sequence[int]],
+                           grad_scale: float, reduced_out: Optional[Sequence[Optional[int]]],
+                           hp: MuonHParams, workspace: int, workspace_bytes: int, stream: int = 0) -> None:
+    """grad_parts[i]: the nparts device pointers of entry i (same count for every entry)."""
+    arr, n = _entries(entries, MuonEntry)
+    nparts = len(grad_parts[0]) if grad_parts else 0
+    flat = [p for parts in grad_parts for p in parts]
+    pa = (ctypes.c_void_p * max(1, len(flat)))(*flat)
+    ro = (ctypes.c_void_p * max(1, n))(*list(reduced_out)) if reduced_out is not None else None
+    _check(lib().mfsdp_muon_step_reduce(arr, n, pa, nparts, grad_scale, ro, ctypes.byref(hp),
+                                        workspace, workspace_bytes, stream))
 
 
 def mfsdp_ns_workspace_size(m: int, n: int, ns_dtype: int) -> int:
@@ -219,6 +237,16 @@ def muon_workspace_t(entries: Sequence[MuonEntry], hp: MuonHParams, device="cuda
 
 def muon_step_t(entries: Sequence[MuonEntry], hp: MuonHParams, workspace) -> None:
     mfsdp_muon_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def muon_step_reduce_t(entries: Sequence[MuonEntry], parts, grad_scale: float, hp: MuonHParams,
+                       workspace, reduced_out=None) -> None:
+    """parts[i]: list of gradient-part tensors of entry i; reduced_out: None or a list of tensors
+    (or None) receiving the reduced gradients."""
+    mfsdp_muon_step_reduce(entries, [[t.data_ptr() for t in ps] for ps in parts], grad_scale,
+                           [t.data_ptr() if t is not None else None for t in reduced_out]
+                           if reduced_out is not None else None,
+                           hp, workspace.data_ptr(), workspace.numel(), _stream())
 
 
 def newton_schulz_t(x, out, a=3.4445, b=-4.7750, c=2.0315, steps=5, eps=1e-7, ns_dtype="bf16",

@@ -96,6 +96,32 @@ def test_newton_schulz_schedule_argument_checks():
                                           ws, None) == native.E_INVALID
 
 
+def test_muon_step_reduce_argument_checks():
+    hp = native.muon_hparams()
+    ents = [_entry(grad=None), _entry(grad=None)]
+    parts = [[FAKE * 4, FAKE * 5], [FAKE * 6, FAKE * 7]]
+    for kw in [dict(grad_parts=[[FAKE * 4, None], [FAKE * 6, FAKE * 7]]),
+               dict(grad_parts=[[FAKE * 4 + 8, FAKE * 5], [FAKE * 6, FAKE * 7]]),
+               dict(grad_parts=[[FAKE] * 65, [FAKE] * 65]),
+               dict(grad_scale=float("nan")),
+               dict(reduced_out=[None, FAKE + 4])]:
+        args = dict(entries=ents, grad_parts=parts, grad_scale=0.5, reduced_out=None, hp=hp,
+                    workspace=FAKE * 16, workspace_bytes=1 << 40, stream=0)
+        args.update(kw)
+        with pytest.raises(native.MfsdpError) as ei:
+            native.mfsdp_muon_step_reduce(**args)
+        assert ei.value.status == native.E_INVALID
+    # zero parts
+    L = native.lib()
+    arr = (native.MuonEntry * 1)(_entry(grad=None))
+    assert L.mfsdp_muon_step_reduce(arr, 1, None, 0, 1.0, None, ctypes.byref(hp), FAKE * 16,
+                                    1 << 40, None) == native.E_INVALID
+    # the plain step still needs the entry gradient
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step([_entry(grad=None)], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
 def test_muon_workspace_checks():
     hp = native.muon_hparams()
     need = native.mfsdp_muon_workspace_size([_entry()], hp)

@@ -377,3 +377,75 @@ def test_muon_with_schedule_matches_oracle(native):
     hp = synth.MuonHParams(lr=0.02, weight_decay=0.01, ns_steps=5, ns_schedule=tuple(PADE_SCHEDULE))
     dev = _run_muon(native, tensors, specs, hp)
     _check_muon(tensors, specs, dev, hp, 2e-2)
+
+
+# ------------------------------------------------------------------ owner-side gradient reduction
+
+def _parts(rng, W, m, n, dtype):
+    return [synth.f32_to_bf16_bits((rng.standard_normal((m, n)) * 1e-3).astype(np.float32))
+            if dtype == synth.BF16 else (rng.standard_normal((m, n)) * 1e-3).astype(np.float32)
+            for _ in range(W)]
+
+
+@pytest.mark.parametrize("W", [1, 3, 8])
+@pytest.mark.parametrize("gdt", [synth.BF16, synth.F32])
+def test_muon_reduce_matches_oracle(native, W, gdt):
+    import torch
+    _say(f"muon reduce W={W} grad={gdt}")
+    rng = np.random.default_rng(400 + W)
+    shapes = [(256, 512), (512, 256), (100, 700), (300, 101), (1, 50)]
+    specs = [synth.MuonSpec(m, n, f"r{m}x{n}", synth.BF16, gdt) for (m, n) in shapes]
+    tensors = [synth.random_muon_tensors(rng, e.m, e.n, e.param_dtype, gdt) for e in specs]
+    parts = [_parts(rng, W, e.m, e.n, gdt) for e in specs]
+    scale = 1.0 / W
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
+    dev, ents, dparts, outs = [], [], [], []
+    for i, (t, e) in enumerate(zip(tensors, specs)):
+        p = to_dev(t.param, e.param_dtype)
+        mo = to_dev(t.momentum, synth.F32)
+        uo = torch.empty((e.m, e.n), dtype=torch.float32, device="cuda")
+        dev.append((p, None, mo, uo))
+        dparts.append([to_dev(x, gdt) for x in parts[i]])
+        # the entry's grad is not read by the reduce step; its dtype names the parts' dtype
+        ents.append(native.muon_entry_t(p, dparts[-1][0], mo, uo))
+        outs.append(torch.empty((e.m, e.n), dtype=torch.bfloat16 if gdt == synth.BF16 else torch.float32,
+                                device="cuda") if i % 2 == 0 else None)
+    h = native.muon_hparams(lr=hp.lr, weight_decay=hp.weight_decay, momentum=hp.momentum,
+                            nesterov=hp.nesterov, ns_steps=hp.ns_steps, eps=hp.eps,
+                            lr_adjust=hp.lr_adjust, ns_dtype=hp.ns_dtype)
+    ws = native.muon_workspace_t(ents, h)
+    native.muon_step_reduce_t(ents, dparts, scale, h, ws, reduced_out=outs)
+    _sync()
+    for i, (t, e) in enumerate(zip(tensors, specs)):
+        g = oracle.reduce_gradients(parts[i], scale)
+        if outs[i] is not None:
+            got = from_dev(outs[i])
+            if gdt == synth.BF16:
+                half = 0.5 * 2.0 ** (np.floor(np.log2(np.maximum(np.abs(g), 1e-30))) - 7)
+                assert np.all(np.abs(got - g) <= half + 1e-6 * np.abs(g)), (e.name, "reduced bf16")
+            else:
+                assert rel_fro(got, g) <= 1e-6, (e.name, "reduced f32")
+        tt = synth.MuonTensors(t.param, g, t.momentum)
+        _check_muon([tt], [e], [dev[i]], hp, 2e-2)
+
+
+def test_muon_reduce_single_part_is_bitwise_the_plain_step(native):
+    import torch
+    rng = np.random.default_rng(410)
+    m, n = 384, 640
+    t = synth.random_muon_tensors(rng, m, n)
+    h = native.muon_hparams(lr=0.02, weight_decay=0.01)
+    res = []
+    for mode in ("plain", "reduce"):
+        p = to_dev(t.param, synth.BF16)
+        g = to_dev(t.grad, synth.BF16)
+        mo = to_dev(t.momentum, synth.F32)
+        e = native.muon_entry_t(p, g, mo)
+        ws = native.muon_workspace_t([e], h)
+        if mode == "plain":
+            native.muon_step_t([e], h, ws)
+        else:
+            native.muon_step_reduce_t([e], [[g]], 1.0, h, ws)
+        _sync()
+        res.append((p.clone(), mo.clone()))
+    assert torch.equal(res[0][0], res[1][0]) and torch.equal(res[0][1], res[1][1])
