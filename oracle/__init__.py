@@ -33,3 +33,4 @@ from .muon import (  # noqa: F401
     step_coefficients,
 )
 from .adamw import adamw_step  # noqa: F401
+from . import planner  # noqa: F401
