@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MFSDP_ABI_VERSION 2
+#define MFSDP_ABI_VERSION 3
 
 typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
 
@@ -192,6 +192,49 @@ int mfsdp_newton_schulz_schedule(const void* x, int32_t x_dtype, void* out, int3
  * Needs no workspace. count == 0 is a no-op. */
 int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,
                      double beta2, double eps, double weight_decay, int64_t step, void* stream);
+
+/* ---- Owner planning (host only; no GPU, no stream) ---------------------------------------- */
+
+/* Planner policies (Algorithm 1, "Balance-aware owner planning"). */
+typedef enum {
+  MFSDP_PLAN_ROLE_GREEDY = 0,   /* per block, in increasing block index, loads carried over */
+  MFSDP_PLAN_SCOPE_GREEDY = 1,  /* the roles of all blocks pooled */
+  MFSDP_PLAN_COST_AWARE = 2     /* scope plan if it balances strictly better within the cap */
+} mfsdp_plan_policy;
+
+/* One parameter of the sharded model, in the model's parameter order.
+ *   block      index of its communication block (>= 0; blocks need not be contiguous)
+ *   numel      element count (>= 0)
+ *   is_matrix  1: a 2D matrix, one role of its own; 0: a non-2D tensor, packed with the block's
+ *              other non-2D tensors into the block's one tail role (Section 4.1). */
+typedef struct {
+  int32_t block;
+  int32_t is_matrix;
+  int64_t numel;
+} mfsdp_plan_param;
+
+/* Owner rank of every parameter (Section 4.1, Algorithm 1): every role (a matrix, or a block's
+ * tail) goes whole to one rank. Greedy rule: roles largest first, each to the currently lightest
+ * rank (load = owned numel). ROLE_GREEDY runs it block by block in increasing block index, the
+ * loads carried from block to block; SCOPE_GREEDY runs it once over all roles; COST_AWARE keeps the
+ * SCOPE_GREEDY plan only if its largest rank load is strictly below ROLE_GREEDY's and, when
+ * gamma_cap > 0, every block's gamma_B under it is <= gamma_cap; otherwise ROLE_GREEDY.
+ * Ties (not fixed by the paper): roles of equal numel in the order (block, matrices before the
+ * tail, first parameter index); among equally loaded ranks the lowest index.
+ * gamma_B (Section 4.2 bandwidth model) = max_r O_{B,r} / (P_B / world), O_{B,r} the numel of
+ * block B owned by rank r, P_B the block's numel; 0 for a block with P_B = 0.
+ *   params, count     the parameters (host memory, read only); count == 0 is valid
+ *   world             shard span W, 1 .. 65536
+ *   policy            an mfsdp_plan_policy; gamma_cap is used by COST_AWARE only (<= 0: no cap)
+ *   owner             out, count int32 owner ranks (host)
+ *   rank_load         optional out (NULL = off), world int64 loads
+ *   block_gamma       optional out, (1 + max block index) doubles
+ *   policy_used       optional out, the policy whose plan was returned
+ * Returns MFSDP_OK or MFSDP_E_INVALID (NULL, world out of range, unknown policy, NaN cap, negative
+ * block or numel, is_matrix not 0/1); outputs are untouched on error. Thread safe; deterministic. */
+int mfsdp_plan_owners(const mfsdp_plan_param* params, int64_t count, int32_t world, int32_t policy,
+                      double gamma_cap, int32_t* owner, int64_t* rank_load, double* block_gamma,
+                      int32_t* policy_used);
 
 /* Text for the last failure on the calling thread ("" if none). */
 const char* mfsdp_last_error(void);

@@ -40,6 +40,17 @@ int fail(int status, const char* fmt, ...) {
   return status;
 }
 
+}  // namespace
+
+namespace mfsdp {
+int set_last_error(int status, const std::string& msg) {
+  g_last_error = msg;
+  return status;
+}
+}  // namespace mfsdp
+
+namespace {
+
 constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
 inline int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }

@@ -20,9 +20,9 @@ _NS_DT = {"bf16": BF16, "f32": F32}
 _LR_MODES = {"none": LR_NONE, "original": LR_ORIGINAL, "match_rms_adamw": LR_MATCH_RMS_ADAMW}
 EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_timed", "mfsdp_ns_workspace_size",
            "mfsdp_newton_schulz", "mfsdp_newton_schulz_schedule", "mfsdp_adamw_step", "mfsdp_last_error",
-           "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce")
+           "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners")
 MAX_GRAD_PARTS = 64
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 
 class MuonEntry(ctypes.Structure):
@@ -46,6 +46,13 @@ class AdamWEntry(ctypes.Structure):
                 ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
                 ("numel", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
                 ("grad_dtype", ctypes.c_int32)]
+
+
+class PlanParam(ctypes.Structure):
+    _fields_ = [("block", ctypes.c_int32), ("is_matrix", ctypes.c_int32), ("numel", ctypes.c_int64)]
+
+
+PLAN_ROLE_GREEDY, PLAN_SCOPE_GREEDY, PLAN_COST_AWARE = 0, 1, 2
 
 
 class MfsdpError(RuntimeError):
@@ -97,6 +104,9 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_status_string.restype = ctypes.c_char_p
         L.mfsdp_abi_version.argtypes = []
         L.mfsdp_abi_version.restype = ctypes.c_int
+        L.mfsdp_plan_owners.argtypes = [ctypes.POINTER(PlanParam), i64, i32, i32, f64, ctypes.POINTER(i32),
+                                        ctypes.POINTER(i64), ctypes.POINTER(f64), ctypes.POINTER(i32)]
+        L.mfsdp_plan_owners.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -123,6 +133,21 @@ def mfsdp_last_error() -> str:
 
 def mfsdp_status_string(status: int) -> str:
     return lib().mfsdp_status_string(status).decode()
+
+
+def mfsdp_plan_owners(params, world: int, policy: int, gamma_cap: float = 0.0):
+    """params: (block, numel, is_matrix) per parameter. Returns (owner list, rank loads, per-block
+    gamma_B list indexed by block, policy used). Host only: no GPU is touched."""
+    params = list(params)
+    arr = (PlanParam * max(1, len(params)))(*[PlanParam(int(b), int(bool(mx)), int(n)) for b, n, mx in params])
+    nblocks = 1 + max((int(b) for b, _, _ in params), default=-1)
+    owner = (ctypes.c_int32 * max(1, len(params)))()
+    loads = (ctypes.c_int64 * max(1, world))()
+    gam = (ctypes.c_double * max(1, nblocks))()
+    used = ctypes.c_int32(-1)
+    _check(lib().mfsdp_plan_owners(arr, len(params), world, policy, gamma_cap, owner, loads, gam,
+                                   ctypes.byref(used)))
+    return list(owner[:len(params)]), list(loads[:world]), list(gam[:nblocks]), used.value
 
 
 def mfsdp_muon_workspace_size(entries: Sequence[MuonEntry], hp: MuonHParams) -> int:

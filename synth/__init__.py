@@ -291,3 +291,81 @@ def random_muon_tensors(rng: np.random.Generator, m: int, n: int, param_dtype: s
     g = cast(rng.standard_normal((m, n), dtype=np.float32) * np.float32(g_std), grad_dtype)
     mo = (rng.standard_normal((m, n), dtype=np.float32) * np.float32(m_std)).astype(np.float32)
     return MuonTensors(p, g, mo)
+
+
+# ----------------------------------------------------------------------------------------------
+# Parameter lists for owner planning: (block, numel, is_matrix) per parameter, plus names and
+# 2D shapes. Only shapes; no planning arithmetic.
+# ----------------------------------------------------------------------------------------------
+
+@dataclasses.dataclass
+class PlanParam:
+    block: int
+    numel: int
+    is_matrix: bool
+    name: str
+    shape: Tuple[int, ...]
+
+    def tuple(self) -> Tuple[int, int, bool]:
+        return (self.block, self.numel, self.is_matrix)
+
+
+def decoder_plan_params(layers: int, hidden: int = 4096, intermediate: int = 16384,
+                        kv_hidden: Optional[int] = None, vocab: int = 0,
+                        norm: str = "rms") -> List[PlanParam]:
+    """A decoder-only transformer wrapped one block per layer (Section 5.1 shapes: hidden 4096,
+    intermediate 16384, 32 heads for the latency sweeps; hidden 768, intermediate 3072, vocab 50257
+    for the convergence model). Per layer: q, o (hidden x hidden), k, v (kv_hidden x hidden),
+    gate, up (intermediate x hidden), down (hidden x intermediate) as 2D matrices, and the two norm
+    weights (plus biases for norm="layer") as non-2D tensors. vocab > 0 adds an embedding block
+    before the layers and a final block with the final norm and an untied LM head, both 2D."""
+    kv = hidden if kv_hidden is None else kv_hidden
+    out: List[PlanParam] = []
+    blk = 0
+
+    def vec(b, name):
+        out.append(PlanParam(b, hidden, False, name, (hidden,)))
+        if norm == "layer":
+            out.append(PlanParam(b, hidden, False, name + ".bias", (hidden,)))
+
+    if vocab > 0:
+        out.append(PlanParam(blk, vocab * hidden, True, "embed", (vocab, hidden)))
+        blk += 1
+    for layer in range(layers):
+        vec(blk, f"l{layer}.attn_norm")
+        for nm, shp in (("q", (hidden, hidden)), ("k", (kv, hidden)), ("v", (kv, hidden)),
+                        ("o", (hidden, hidden))):
+            out.append(PlanParam(blk, shp[0] * shp[1], True, f"l{layer}.{nm}", shp))
+        vec(blk, f"l{layer}.ffn_norm")
+        for nm, shp in (("gate", (intermediate, hidden)), ("up", (intermediate, hidden)),
+                        ("down", (hidden, intermediate))):
+            out.append(PlanParam(blk, shp[0] * shp[1], True, f"l{layer}.{nm}", shp))
+        blk += 1
+    if vocab > 0:
+        vec(blk, "final_norm")
+        out.append(PlanParam(blk, vocab * hidden, True, "lm_head", (vocab, hidden)))
+    return out
+
+
+def random_plan_params(rng: np.random.Generator, blocks: int, max_matrices: int = 6,
+                       max_tail: int = 3, max_numel: int = 4096,
+                       tie_prob: float = 0.5) -> List[Tuple[int, int, bool]]:
+    """Random planner instances: `blocks` blocks (indices shuffled into the parameter order, some
+    left empty), each with 0..max_matrices matrices and 0..max_tail non-2D tensors. With
+    probability tie_prob the sizes come from a small set so that equal-size roles are common."""
+    sizes = rng.integers(0, max_numel + 1, size=4)
+    params = []
+    order = rng.permutation(blocks)
+    for b in order:
+        b = int(b)
+        if rng.random() < 0.1:
+            continue
+        items = [True] * int(rng.integers(0, max_matrices + 1)) + [False] * int(rng.integers(0, max_tail + 1))
+        rng.shuffle(items)
+        for is_m in items:
+            if rng.random() < tie_prob:
+                numel = int(sizes[int(rng.integers(0, 4))])
+            else:
+                numel = int(rng.integers(0, max_numel + 1))
+            params.append((b, numel, bool(is_m)))
+    return params

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert native.mfsdp_abi_version() == native.ABI_VERSION == 2
+    assert native.mfsdp_abi_version() == native.ABI_VERSION == 3
     assert native.mfsdp_status_string(0) == "MFSDP_OK"
     assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
     assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
