@@ -11,7 +11,9 @@ gate, up 14336x4096; down 4096x14336 per layer) plus 8 RMSNorm vectors of 4096 o
 
 Prints ONE JSON line. `value` is nominal NS TFLOP/s over the whole step (NS flops / step time);
 `roofline` describes the NS GEMM kernel; `cpu_baseline` is the fp64 oracle timed on a bounded
-sample of the same share on the host cores.
+sample of the same share on the host cores. `planner` reports the owner planner (Algorithm 1) on the
+paper's decoder sweep (planner time, rank-load imbalance, gamma_B per policy); with --plan-span W it
+also runs every rank's planned share on the GPU and reports the step-time imbalance over ranks.
 """
 from __future__ import annotations
 
@@ -162,6 +164,109 @@ def time_reduction(args, native, wl, keep, ents, h, ws, stream, hev, plain_step_
             "note": "pass time = reduce-step time - plain-step time + plain momentum-pass time"}
 
 
+# the paper's weak-scaling sweep: decoder layers (hidden 4096, intermediate 16384) per shard span
+PLAN_SWEEP = {8: 16, 16: 32, 32: 64, 64: 128}
+
+
+def _plan_share(params, owner, rank):
+    mats = sorted((p.shape for p, o in zip(params, owner) if o == rank and p.is_matrix), reverse=True)
+    tails = sorted((p.numel for p, o in zip(params, owner) if o == rank and not p.is_matrix), reverse=True)
+    return tuple(mats), tuple(tails)
+
+
+def _time_share(native, torch, dev, hev, stream, share, hp, ah, steps, warmup, gen):
+    """ms per owner step (Muon over the matrices + AdamW over the tail tensors) of one rank's share;
+    seeded device-drawn values (the step time does not depend on them)."""
+    mats, tails = share
+    keep, ents, aents = [], [], []
+    for (m, n) in mats:
+        p = (torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16)
+        g = (torch.randn(m, n, device=dev, generator=gen) * 1e-3).to(torch.bfloat16)
+        mo = torch.randn(m, n, device=dev, generator=gen) * 1e-3
+        keep.append((p, g, mo))
+        ents.append(native.muon_entry_t(p, g, mo))
+    for numel in tails:
+        t = (torch.ones(numel, device=dev, dtype=torch.bfloat16),
+             (torch.randn(numel, device=dev, generator=gen) * 1e-3).to(torch.bfloat16),
+             torch.zeros(numel, device=dev), torch.zeros(numel, device=dev))
+        keep.append(t)
+        aents.append(native.adamw_entry_t(*t))
+    ws = native.muon_workspace_t(ents, hp, device=dev) if ents else None
+    a, b = hev.create(), hev.create()
+
+    def step():
+        if ents:
+            native.mfsdp_muon_step(ents, hp, ws.data_ptr(), ws.numel(), stream)
+        if aents:
+            native.mfsdp_adamw_step(aents, ah.lr, ah.beta1, ah.beta2, ah.eps, ah.weight_decay, ah.step, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hev.record(a, stream)
+    for _ in range(steps):
+        step()
+    hev.record(b, stream)
+    torch.cuda.synchronize()
+    ms = hev.elapsed_ms(a, b) / steps
+    del keep, ws
+    return ms
+
+
+def planner_report(native, spans, gpu_span, ctx=None) -> dict:
+    """Owner planning (Algorithm 1) on the paper's sweep: planner time, rank-load (resident
+    parameter) imbalance max/avg and gamma_B per policy; for gpu_span, every rank's share under
+    RoleGreedy and ScopeGreedy (CostAware returns one of the two) run on the GPU, and the
+    optimizer-step imbalance max/avg over ranks."""
+    import synth
+    names = {0: "role_greedy", 1: "scope_greedy", 2: "cost_aware"}
+    out = {"model": "decoder, hidden 4096, intermediate 16384, 32 heads (q, k, v, o, gate, up, "
+                    "down per layer; 2 RMSNorm vectors per layer as the block tail)",
+           "spans": {}}
+    for span in spans:
+        layers = PLAN_SWEEP[span]
+        params = synth.decoder_plan_params(layers)
+        tuples = [p.tuple() for p in params]
+        rec = {"layers": layers, "parameters": len(params), "numel": sum(p.numel for p in params)}
+        owners = {}
+        for pol in (0, 1, 2):
+            reps, best = 5, float("inf")
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                owner, loads, gam, used = native.mfsdp_plan_owners(tuples, span, pol, 0.0)
+                best = min(best, time.perf_counter() - t0)
+            avg = sum(loads) / span
+            rec[names[pol]] = {"plan_ms": round(best * 1e3, 3),
+                               "load_max_over_avg": round(max(loads) / avg, 4),
+                               "gamma_max": round(max(gam), 4),
+                               "gamma_mean": round(sum(gam) / len(gam), 4),
+                               "policy_used": names[used]}
+            owners[pol] = owner
+        if span == gpu_span and ctx is not None:
+            torch, dev, hev, stream, hp, ah, steps, warmup = ctx
+            gen = torch.Generator(device=dev)
+            gen.manual_seed(span)
+            cache = {}
+            for pol in (0, 1):
+                shares = [_plan_share(params, owners[pol], r) for r in range(span)]
+                for r, sh in enumerate(shares):
+                    if sh not in cache:
+                        log(f"planner: span {span}, {names[pol]}: timing rank {r}'s share ({len(sh[0])} "
+                            f"matrices, {len(sh[1])} tail tensors)")
+                        cache[sh] = _time_share(native, torch, dev, hev, stream, sh, hp, ah, steps, warmup, gen)
+                ms = [cache[sh] for sh in shares]
+                heavy = max(range(span), key=lambda r: ms[r])
+                rec[names[pol]]["gpu_owner_step"] = {
+                    "distinct_shares": len(set(shares)),
+                    "ms_max": round(max(ms), 4), "ms_mean": round(sum(ms) / span, 4), "ms_min": round(min(ms), 4),
+                    "step_max_over_avg": round(max(ms) / (sum(ms) / span), 4),
+                    "heaviest_rank": heavy,
+                    "heaviest_share_matrices": [list(x) for x in shares[heavy][0]],
+                    "heaviest_share_tail_tensors": len(shares[heavy][1])}
+        out["spans"][str(span)] = rec
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -175,6 +280,9 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="before timing, run one plain 1 GiB -> 1 GiB elementwise copy kernel (the "
                          "reference dispatch for scaling HBM counters)")
+    ap.add_argument("--plan-span", type=int, default=0, choices=[0] + sorted(PLAN_SWEEP),
+                    help="also run every rank's owner share of the planned decoder sweep model at this "
+                         "shard span on the GPU and report the step-time imbalance over ranks")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -344,6 +452,10 @@ def main() -> int:
     if args.grad_parts > 0:
         out["grad_reduction"] = time_reduction(args, native, wl, keep, ents, h, ws, stream, hev,
                                                ms_per_step, prep_ms, es_g)
+    log("owner planner on the decoder sweep" + (f" (GPU shares at span {args.plan_span})"
+                                                  if args.plan_span else ""))
+    pctx = (torch, dev, hev, stream, h, ah, 5, 2) if args.plan_span else None
+    out["planner"] = planner_report(native, sorted(PLAN_SWEEP), args.plan_span, pctx)
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])
