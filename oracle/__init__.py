@@ -17,7 +17,11 @@ What it computes follows the paper (MatrixFSDP, arxiv 2607.05895):
 
 Where the paper is silent, the readings used are the ones stated in each function's docstring.
 
-Parity status: every function here is pinned by tests in ``tests/test_oracle_pins.py``.
+* Section 5.7 (Generality beyond Muon): the owner runs Shampoo (full left/right preconditioners,
+  inverse fourth root) on the same whole matrices (``shampoo.py``).
+
+Parity status: every function here is pinned by tests in ``tests/test_oracle_pins.py``,
+``tests/test_planner_pins.py`` and ``tests/test_shampoo_pins.py``.
 """
 from .muon import (  # noqa: F401
     bf16_widen,
@@ -34,3 +38,4 @@ from .muon import (  # noqa: F401
 )
 from .adamw import adamw_step  # noqa: F401
 from . import planner  # noqa: F401
+from . import shampoo  # noqa: F401
