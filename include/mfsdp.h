@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MFSDP_ABI_VERSION 3
+#define MFSDP_ABI_VERSION 4
 
 typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
 
@@ -192,6 +192,83 @@ int mfsdp_newton_schulz_schedule(const void* x, int32_t x_dtype, void* out, int3
  * Needs no workspace. count == 0 is a no-op. */
 int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr, double beta1,
                      double beta2, double eps, double weight_decay, int64_t step, void* stream);
+
+/* ---- Shampoo owner step (Section 5.7: a single-device matrix optimizer on the owner) --------- */
+
+/* One whole matrix the rank owns, for Shampoo (Gupta, Koren and Singer 2018, the matrix case:
+ * full left and right preconditioners with the inverse fourth root, as the paper runs it).
+ *   param      m x n, param_dtype (F32 or BF16), updated in place (fp32 math, bf16 rounded to
+ *              nearest even)
+ *   grad       m x n, grad_dtype (F32 or BF16), read only
+ *   L, R       m x m and n x n fp32 statistics (row-major), updated in place; start at zero
+ *   PL, PR     m x m and n x n fp32 preconditioners (row-major): written when hp->refresh is 1,
+ *              read (and left unchanged) when it is 0
+ *   m, n       1 .. 65536
+ *   update_out optional m x n fp32: receives U = PL G PR. NULL = off.
+ * All buffers are distinct device allocations (no aliasing), naturally aligned. */
+typedef struct {
+  void* param;
+  const void* grad;
+  float* L;
+  float* R;
+  float* PL;
+  float* PR;
+  int64_t m;
+  int64_t n;
+  int32_t param_dtype;
+  int32_t grad_dtype;
+  float* update_out;
+} mfsdp_shampoo_entry;
+
+/* Shampoo hyperparameters, shared by every entry of one call (doubles; fp32 math on the GPU).
+ *   lr >= 0, weight_decay >= 0: p <- p (1 - lr wd) - lr U (decoupled decay, both on the old p)
+ *   beta >= 0, weight >= 0: S <- beta S + weight G G^T (L) and G^T G (R); 1, 1 = accumulation
+ *   eps > 0, eps_rel >= 0: the root is taken of S + rho I, rho = eps + eps_rel ||S||_F
+ *   refresh 0/1: recompute PL, PR from the updated statistics (1) or use the stored ones (0)
+ *   root_iters 1 .. 100: iterations of the coupled Newton inverse-root iteration (20 reaches fp32
+ *   accuracy for rho >= 1e-6 ||S||_F on the tested spectra; see mfsdp_inverse_root). */
+typedef struct {
+  double lr;
+  double weight_decay;
+  double beta;
+  double weight;
+  double eps;
+  double eps_rel;
+  int32_t refresh;
+  int32_t root_iters;
+} mfsdp_shampoo_hparams;
+
+/* Bytes of device workspace mfsdp_shampoo_step needs for these entries and hyperparameters:
+ * per matrix, zero-padded fp32 copies of G and G^T and of P_L G (3 mp np floats) and five
+ * padded matrices per side for the root iteration (5 (mp^2 + np^2) floats), mp, np = m, n rounded
+ * up to 128; plus launch descriptors. Data pointers are not used. 0 on invalid arguments;
+ * count == 0 returns 0 with no error. */
+size_t mfsdp_shampoo_workspace_size(const mfsdp_shampoo_entry* entries, int64_t count,
+                                    const mfsdp_shampoo_hparams* hp);
+
+/* One Shampoo step on every entry (host array of count entries), enqueued on `stream`
+ * (hipStream_t, NULL = default stream); no host synchronisation. Statistics update, inverse
+ * fourth roots (on refresh), U = P_L G P_R on fp32 MFMA, then the parameter update. The
+ * workspace (device, 256-byte aligned, >= the size query) must not be in use by another call
+ * still running. Returns MFSDP_OK, MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an
+ * argument error nothing is enqueued. At most 4096 entries per call. */
+int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count,
+                       const mfsdp_shampoo_hparams* hp, void* workspace, size_t workspace_bytes,
+                       void* stream);
+
+/* Workspace bytes for mfsdp_inverse_root (0 on invalid arguments). */
+size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters);
+
+/* out = (a + rho I)^(-1/p), rho = eps + eps_rel ||a||_F, for a symmetric positive semidefinite
+ * d x d fp32 matrix `a` (row-major, device; read only; not checked for symmetry), by `iters`
+ * steps of the coupled Newton iteration (Guo and Higham 2006) on fp32 MFMA, the iteration the
+ * Shampoo step uses. p in {1, 2, 4}; 1 <= d <= 65536; eps > 0; eps_rel >= 0; 1 <= iters <= 100.
+ * `out` (d x d fp32, device) must not overlap `a`. In fp32 the iteration is stable while rho is
+ * at least about 1e-6 ||a||_F; a smaller ridge can diverge. Same stream, workspace and error
+ * rules as mfsdp_shampoo_step. */
+int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double eps,
+                       double eps_rel, int32_t iters, void* workspace, size_t workspace_bytes,
+                       void* stream);
 
 /* ---- Owner planning (host only; no GPU, no stream) ---------------------------------------- */
 

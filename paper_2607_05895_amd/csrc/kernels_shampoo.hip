@@ -1,0 +1,354 @@
+// HIP kernels of the Shampoo owner step (fp32): the NT GEMM on fp32 MFMA that every product of the
+// step reduces to (statistics G G^T and G^T G, the coupled Newton iteration for the inverse root,
+// P_L G P_R), and the small boundary, reduction and elementwise kernels around it.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mfsdp_internal.h"
+#include "shampoo_internal.h"
+
+namespace mfsdp {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+// global-address-space views (flat accesses would also count against the LDS wait counter)
+typedef __attribute__((address_space(1))) float g_f32;
+typedef __attribute__((address_space(1))) const float g_cf32;
+typedef __attribute__((address_space(1))) const f32x4 g_cf32x4;
+
+// The descriptor serving block b (descriptors sorted by tile_begin, the first one at 0).
+template <typename D>
+__device__ __forceinline__ int find_desc(const D* d, int count, int b) {
+  int lo = 0, hi = count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (d[mid].tile_begin <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ float ld_any(const void* p, int64_t i, int dt) {
+  if (dt == kDtBF16) return __uint_as_float(uint32_t(static_cast<const uint16_t*>(p)[i]) << 16);
+  return static_cast<const float*>(p)[i];
+}
+
+// LDS slot permutation of the GEMM operand tiles: row r's eight 16-byte chunks are XOR-permuted by
+// (r & 7) ^ ((r >> 3) & 1). The fragment reads (32 consecutive rows at one chunk per half wave) and
+// the tile stores (8 lanes per row) are then free of bank conflicts for 32 and for 64 banks.
+__device__ __forceinline__ int op_slot(int r, int chunk) {
+  return r * 8 + (chunk ^ ((r & 7) ^ ((r >> 3) & 1)));
+}
+
+// C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup.
+// 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of v_mfma_f32_32x32x2f32. K steps of
+// 32, double-buffered in LDS with the next step's global loads in registers during the current
+// step's MFMAs. The K index inside a step is permuted identically on both operands (lane half h of
+// instruction q within group g takes k = 8g + 4h + q), so each lane reads its operands as 16-byte
+// vectors. Symmetric problems compute the upper tiles only and store each tile transposed as well,
+// through LDS, with coalesced row stores.
+__global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs,
+                                                         int count) {
+  __shared__ f32x4 lds[2][2][kShTile * 8];  // [stage][P, Q][slot]: 64 KiB
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShGemmDesc& d = descs[e];
+  int lt = blockIdx.x - d.tile_begin;
+  int bi, bj;
+  if (d.sym) {
+    bi = 0;
+    int rowlen = d.tiles_n;
+    while (lt >= rowlen) {
+      lt -= rowlen;
+      ++bi;
+      --rowlen;
+    }
+    bj = bi + lt;
+  } else {
+    bi = lt / d.tiles_n;
+    bj = lt - bi * d.tiles_n;
+  }
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wr = w >> 1, wc = w & 1;
+  const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
+  const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
+  const int lrow = t >> 3, lch = t & 7;
+  f32x4 ra[4], rb[4];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = lrow + 32 * j;
+      ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
+      rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
+    }
+  };
+  auto lstore = [&](int s) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int slot = op_slot(lrow + 32 * j, lch);
+      lds[s][0][slot] = ra[j];
+      lds[s][1][slot] = rb[j];
+    }
+  };
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  const int nk = d.K / 32;
+  const int fr = lane & 31, fh = lane >> 5;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int s = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * 32);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      f32x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = lds[s][0][op_slot(wr * 64 + i * 32 + fr, 2 * g + fh)];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = lds[s][1][op_slot(wc * 64 + j * 32 + fr, 2 * g + fh)];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore(s ^ 1);
+    __syncthreads();
+  }
+
+  // Epilogue. Accumulator element v of block (i, j) is C row 8 (v / 4) + 4 h + v % 4, column
+  // lane % 32 of that 32 x 32 block (h = lane / 32). E may alias C: each element is read and then
+  // written by the same thread. Symmetric problems are stored exactly symmetric: an upper tile is
+  // also stored transposed, and a diagonal tile keeps its upper triangle and mirrors it into the
+  // lower one (in floating point the two triangles of a product of two different symmetric
+  // matrices differ; kept, that antisymmetric part is amplified by the NT form of the iteration).
+  g_f32* C = (g_f32*)(d.C);
+  const g_cf32* E = (const g_cf32*)(d.E);
+  const bool diag_tile = d.sym && bi == bj;
+  float* tl = reinterpret_cast<float*>(&lds[0][0][0]);  // 128 x 128 floats, element (r, c) at r*128 + (c ^ r)
+  const int64_t r0 = int64_t(bi) * kShTile, c0 = int64_t(bj) * kShTile;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = wr * 64 + i * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+        const int c = wc * 64 + j * 32 + fr;
+        if (diag_tile && r > c) continue;  // filled from the upper triangle below
+        const int64_t gr = r0 + r, gc = c0 + c;
+        float x = d.alpha * acc[i][j][v];
+        if (E) x += d.beta * E[gr * d.lde + gc];
+        if (gr == gc) x += d.diag;
+        C[gr * d.ldc + gc] = x;
+        if (d.sym) tl[r * kShTile + (c ^ r)] = x;
+      }
+  if (d.sym) {
+    __syncthreads();
+#pragma unroll 4
+    for (int it = 0; it < 32; ++it) {
+      const int c = (t >> 6) + 4 * it;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int r = lane + 64 * h;
+        // position (c, r) of the tile's transpose; on a diagonal tile only below the diagonal
+        if (!diag_tile || c > r) C[(c0 + c) * d.ldc + r0 + r] = tl[r * kShTile + (c ^ r)];
+      }
+    }
+  }
+}
+
+// Boundary copy into the padded workspace (optionally transposed as well), 64 x 64 tiles.
+__global__ __launch_bounds__(256) void sh_copy_in_kernel(const ShCopyDesc* __restrict__ descs, int count) {
+  __shared__ float tt[kShCopyTile][kShCopyTile + 1];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShCopyDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  g_f32* dst = (g_f32*)(d.dst);
+  const int64_t gc = int64_t(tj) * kShCopyTile + c;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;
+    const int64_t gr = int64_t(ti) * kShCopyTile + r;
+    const float v = (gr < d.rows && gc < d.cols) ? ld_any(d.src, gr * d.ld_src + gc, d.src_dtype) : 0.0f;
+    dst[gr * d.ld_dst + gc] = v;
+    tt[r][c] = v;
+  }
+  if (d.dstT) {
+    __syncthreads();
+#pragma unroll 4
+    for (int i = 0; i < 16; ++i) {
+      const int r = rr + 4 * i;  // row of the transposed tile = column of the source tile
+      ((g_f32*)d.dstT)[(int64_t(tj) * kShCopyTile + r) * d.ld_dstT + int64_t(ti) * kShCopyTile + c] = tt[c][r];
+    }
+  }
+}
+
+// Boundary copy out of the padded workspace into a caller fp32 rows x cols buffer.
+__global__ __launch_bounds__(256) void sh_copy_out_kernel(const ShCopyDesc* __restrict__ descs, int count) {
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShCopyDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const g_cf32* src = (const g_cf32*)(d.src);
+  g_f32* dst = (g_f32*)(d.dst);
+  const int64_t gc = int64_t(tj) * kShCopyTile + c;
+  if (gc >= d.cols) return;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int64_t gr = int64_t(ti) * kShCopyTile + rr + 4 * i;
+    if (gr < d.rows) dst[gr * d.ld_dst + gc] = src[gr * d.ld_src + gc];
+  }
+}
+
+// Sum of squares and trace of one row chunk of a padded statistic, fp64, fixed reduction order.
+__global__ __launch_bounds__(256) void sh_norm_kernel(const ShNormDesc* __restrict__ descs, int count) {
+  __shared__ double red[2][4];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShNormDesc& d = descs[e];
+  const int chunk = blockIdx.x - d.tile_begin;
+  const int t = threadIdx.x;
+  const int rb = chunk * d.chunk_rows;
+  const int re = min(d.rows_pad, rb + d.chunk_rows);
+  double ss = 0.0, tr = 0.0;
+  for (int r = rb; r < re; ++r) {
+    const float* row = d.S + int64_t(r) * d.ld;
+    for (int c = t; c < d.rows_pad; c += 256) {
+      const double v = row[c];
+      ss += v * v;
+      if (c == r) tr += v;
+    }
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    ss += __shfl_xor(ss, o);
+    tr += __shfl_xor(tr, o);
+  }
+  if ((t & 63) == 0) {
+    red[0][t >> 6] = ss;
+    red[1][t >> 6] = tr;
+  }
+  __syncthreads();
+  if (t == 0) {
+    d.partials[2 * chunk] = ((red[0][0] + red[0][1]) + red[0][2]) + red[0][3];
+    d.partials[2 * chunk + 1] = ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3];
+  }
+}
+
+__global__ void sh_scalars_kernel(const ShScalarDesc* __restrict__ descs, int count, double eps,
+                                  double eps_rel, int p) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= count) return;
+  const ShScalarDesc& d = descs[e];
+  double ss = 0.0, tr = 0.0;
+  for (int k = 0; k < d.nchunks; ++k) {
+    ss += d.partials[2 * k];
+    tr += d.partials[2 * k + 1];
+  }
+  const double rho = eps + eps_rel * sqrt(ss);
+  const double n2 = ss + 2.0 * rho * tr + double(d.d) * rho * rho;
+  const double z = double(1 + p) / (2.0 * sqrt(n2));
+  d.out[0] = float(rho);
+  d.out[1] = float(z);
+  d.out[2] = float(pow(z, 1.0 / double(p)));
+}
+
+// M = z (S + rho I), X = z^(1/p) I (M may alias S).
+__global__ __launch_bounds__(256) void sh_init_kernel(const ShInitDesc* __restrict__ descs, int count) {
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShInitDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const float rho = d.sc[0], z = d.sc[1], zp = d.sc[2];
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const int64_t gc = int64_t(tj) * kShCopyTile + c;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int64_t gr = int64_t(ti) * kShCopyTile + rr + 4 * i;
+    const int64_t o = gr * d.ld + gc;
+    const bool dg = gr == gc;
+    d.M[o] = z * (d.S[o] + (dg ? rho : 0.0f));
+    d.X[o] = dg ? zp : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(256) void sh_apply_kernel(const ShApplyDesc* __restrict__ descs, int count,
+                                                       float decay, float step) {
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShApplyDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const int64_t gc = int64_t(tj) * kShCopyTile + c;
+  if (gc >= d.n) return;
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int64_t gr = int64_t(ti) * kShCopyTile + rr + 4 * i;
+    if (gr >= d.m) continue;
+    const float u = d.U[gr * d.ldu + gc];
+    const int64_t o = gr * d.n + gc;
+    if (d.param_dtype == kDtBF16) {
+      uint16_t* pp = static_cast<uint16_t*>(d.param);
+      const float p = __uint_as_float(uint32_t(pp[o]) << 16);
+      pp[o] = uint16_t(pack_bf16x2(p * decay - step * u, 0.0f) & 0xffffu);
+    } else {
+      float* pp = static_cast<float*>(d.param);
+      pp[o] = pp[o] * decay - step * u;
+    }
+    if (d.update_out) d.update_out[o] = u;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sh_gemm(const ShGemmDesc* d, int count, int total_tiles, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sh_gemm_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_sh_copy(const ShCopyDesc* d, int count, int total_tiles, int dir, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  if (dir == 0)
+    hipLaunchKernelGGL(sh_copy_in_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  else
+    hipLaunchKernelGGL(sh_copy_out_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_sh_norm(const ShNormDesc* d, int count, int total_blocks, hipStream_t st) {
+  if (total_blocks <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sh_norm_kernel, dim3(total_blocks), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_sh_scalars(const ShScalarDesc* d, int count, double eps, double eps_rel, int p,
+                             hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sh_scalars_kernel, dim3((count + 63) / 64), dim3(64), 0, st, d, count, eps,
+                     eps_rel, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_sh_init(const ShInitDesc* d, int count, int total_tiles, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sh_init_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_sh_apply(const ShApplyDesc* d, int count, int total_tiles, float decay, float step,
+                           hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(sh_apply_kernel, dim3(total_tiles), dim3(256), 0, st, d, count, decay, step);
+  return hipGetLastError();
+}
+
+}  // namespace mfsdp

@@ -819,3 +819,11 @@ int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr,
 }
 
 }  // extern "C"
+
+namespace mfsdp {
+// Descriptor staging shared with the other host modules of the library.
+int staging_acquire(size_t bytes, void** host) { return ring().acquire(bytes, host, nullptr); }
+int staging_upload(int slot, void* dst, size_t bytes, hipStream_t st) {
+  return ring().upload(slot, dst, bytes, st);
+}
+}  // namespace mfsdp

@@ -1,0 +1,515 @@
+// Host side of the Shampoo owner step and of the standalone inverse p-th root: argument checks,
+// workspace plan, descriptor build and the launch sequence (all on the caller's stream).
+//
+// Shampoo (Section 5.7 of the paper; Gupta, Koren and Singer 2018, matrix case) per owned matrix:
+//   L <- beta L + weight G G^T,  R <- beta R + weight G^T G
+//   refresh: P_L = (L + rho_L I)^(-1/4), P_R = (R + rho_R I)^(-1/4), rho = eps + eps_rel ||S||_F
+//   U = P_L G P_R,  p <- p (1 - lr wd) - lr U
+//
+// Inverse p-th root by the coupled Newton iteration (Guo and Higham, SIAM J. Matrix Anal. Appl.
+// 2006; the form used for Shampoo by Anil et al. 2020): with z = (1 + p) / (2 ||A||_F),
+//   X_0 = z^(1/p) I,  M_0 = z A,  T_k = ((p + 1) I - M_k) / p,
+//   X_{k+1} = X_k T_k,  M_{k+1} = T_k^p M_k,
+// so that M_k -> I and X_k -> A^(-1/p). All iterates are polynomials in A, hence symmetric and
+// commuting: every product is an NT product of symmetric operands, computed on its upper tiles.
+// T_k is never stored; its affine form is folded into the products:
+//   X_{k+1}  = ((p+1)/p) X_k - (1/p) X_k M_k
+//   T_k^2    = (p+1)^2/p^2 I - 2(p+1)/p^2 M_k + 1/p^2 M_k M_k
+//   T_k^4    = T_k^2 T_k^2,   M_{k+1} = T_k^p M_k          (p = 1: M_{k+1} = 2 M_k - M_k M_k)
+// The last iteration forms X only.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/mfsdp.h"
+#include "mfsdp_internal.h"
+#include "shampoo_internal.h"
+
+namespace mfsdp {
+int set_last_error(int status, const std::string& msg);
+int staging_acquire(size_t bytes, void** host);
+int staging_upload(int slot, void* dst, size_t bytes, hipStream_t st);
+}  // namespace mfsdp
+
+using namespace mfsdp;
+
+namespace {
+
+constexpr size_t kAl = 256;
+constexpr int kNormChunkRows = 16;
+constexpr int64_t kMaxDim = 1 << 16;
+size_t al(size_t x) { return (x + kAl - 1) / kAl * kAl; }
+int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+int bad(const std::string& m) { return set_last_error(MFSDP_E_INVALID, m); }
+int hip_err(hipError_t e, const char* what) {
+  return set_last_error(MFSDP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// Workspace bump allocator (offsets only; the base is added when the workspace is known).
+struct Arena {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off = al(off + bytes);
+    return o;
+  }
+};
+
+// One inverse-root problem on a padded d_pad x d_pad statistic held in M.
+struct Side {
+  int64_t d = 0, dp = 0;
+  size_t M = 0, T2 = 0, T4 = 0, X[2] = {0, 0}, partials = 0, sc = 0;
+  float* out = nullptr;  // caller destination of the root (d x d, row stride d)
+  bool has_out = false;  // copy the root out (decided by the call, not by the pointer value,
+                         // so that the size query, which sees no pointers, builds the same ops)
+};
+
+void plan_side(Side& s, int64_t d, Arena& a) {
+  s.d = d;
+  s.dp = rup(d, kShTile);
+  const size_t mat = size_t(s.dp) * size_t(s.dp) * sizeof(float);
+  s.M = a.take(mat);
+  s.T2 = a.take(mat);
+  s.T4 = a.take(mat);
+  s.X[0] = a.take(mat);
+  s.X[1] = a.take(mat);
+  s.partials = a.take(size_t(s.dp / kNormChunkRows) * 2 * sizeof(double));
+  s.sc = a.take(4 * sizeof(float));
+}
+
+struct EntryPlan {
+  int64_t m, n, mp, np;
+  size_t Gp, GpT, Y;
+  Side L, R;
+};
+
+// The launch sequence: descriptor arrays packed in one host buffer (uploaded once into the
+// workspace) and the ops that consume them.
+enum OpKind { kOpCopyIn, kOpCopyOut, kOpGemm, kOpNorm, kOpScalars, kOpInit, kOpApply };
+struct Op {
+  OpKind kind;
+  size_t desc_off;
+  int count;
+  int total;  // grid blocks
+};
+
+struct Build {
+  char* base = nullptr;  // workspace base (nullptr while sizing)
+  std::vector<char> h;
+  std::vector<Op> ops;
+  template <class T>
+  T* ptr(size_t off) const {  // integer arithmetic: base is null while only sizing
+    return reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(base) + off);
+  }
+  template <class T>
+  size_t put(const std::vector<T>& v) {
+    const size_t o = al(h.size());
+    h.resize(o + v.size() * sizeof(T));
+    std::memcpy(h.data() + o, v.data(), v.size() * sizeof(T));
+    return o;
+  }
+  template <class T>
+  void op(OpKind k, const std::vector<T>& v, int total) {
+    if (v.empty() || total <= 0) return;
+    ops.push_back(Op{k, put(v), int(v.size()), total});
+  }
+};
+
+ShCopyDesc copy_desc(const void* src, int dt, void* dst, float* dstT, int64_t rows, int64_t cols,
+                     int64_t ld_src, int64_t ld_dst, int64_t ld_dstT, int64_t dom_rows,
+                     int64_t dom_cols, int& tiles) {
+  ShCopyDesc c{};
+  c.src = src;
+  c.dst = dst;
+  c.dstT = dstT;
+  c.rows = rows;
+  c.cols = cols;
+  c.ld_src = ld_src;
+  c.ld_dst = ld_dst;
+  c.ld_dstT = ld_dstT;
+  c.src_dtype = dt;
+  const int64_t tm = (dom_rows + kShCopyTile - 1) / kShCopyTile;
+  const int64_t tn = (dom_cols + kShCopyTile - 1) / kShCopyTile;
+  c.tiles_n = int32_t(tn);
+  c.tile_begin = tiles;
+  tiles += int(tm * tn);
+  return c;
+}
+
+ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, float* C, int64_t ldp,
+                     int64_t ldq, int64_t lde, int64_t ldc, int64_t M, int64_t N, int64_t K,
+                     int sym, float alpha, float beta, float diag, int& tiles) {
+  ShGemmDesc g{};
+  g.P = P;
+  g.Q = Q;
+  g.E = E;
+  g.C = C;
+  g.ldp = ldp;
+  g.ldq = ldq;
+  g.lde = lde;
+  g.ldc = ldc;
+  g.K = int32_t(K);
+  g.tiles_n = int32_t(N / kShTile);
+  g.sym = sym;
+  g.alpha = alpha;
+  g.beta = beta;
+  g.diag = diag;
+  g.tile_begin = tiles;
+  const int64_t tm = M / kShTile, tn = N / kShTile;
+  tiles += int(sym ? tn * (tn + 1) / 2 : tm * tn);
+  return g;
+}
+
+// Root ops for every side: norms, scalars, init, the iterations and the copy of X to side.out.
+void add_root_ops(Build& b, std::vector<Side*>& sides, int p, int iters) {
+  std::vector<ShNormDesc> nd;
+  std::vector<ShScalarDesc> sd;
+  std::vector<ShInitDesc> idesc;
+  int nblocks = 0, itiles = 0;
+  for (Side* s : sides) {
+    ShNormDesc n{};
+    n.S = b.ptr<float>(s->M);
+    n.ld = s->dp;
+    n.rows_pad = int32_t(s->dp);
+    n.chunk_rows = kNormChunkRows;
+    n.partials = b.ptr<double>(s->partials);
+    n.nchunks = int32_t(s->dp / kNormChunkRows);
+    n.tile_begin = nblocks;
+    nblocks += n.nchunks;
+    nd.push_back(n);
+    ShScalarDesc c{};
+    c.partials = n.partials;
+    c.nchunks = n.nchunks;
+    c.d = int32_t(s->d);
+    c.out = b.ptr<float>(s->sc);
+    sd.push_back(c);
+    ShInitDesc in{};
+    in.S = b.ptr<float>(s->M);
+    in.M = b.ptr<float>(s->M);
+    in.X = b.ptr<float>(s->X[0]);
+    in.ld = s->dp;
+    in.sc = c.out;
+    in.tiles_n = int32_t(s->dp / kShCopyTile);
+    in.tile_begin = itiles;
+    itiles += int((s->dp / kShCopyTile) * (s->dp / kShCopyTile));
+    idesc.push_back(in);
+  }
+  b.op(kOpNorm, nd, nblocks);
+  b.op(kOpScalars, sd, int(sd.size()));
+  b.op(kOpInit, idesc, itiles);
+
+  const float fp = float(p);
+  // per parity q: A holds M_k, B receives M_{k+1}; X[q] -> X[q ^ 1]
+  std::vector<ShGemmDesc> l1[2], l2[2], l3[2];
+  int t1[2] = {0, 0}, t1x[2] = {0, 0}, t2[2] = {0, 0}, t3[2] = {0, 0};
+  for (int q = 0; q < 2; ++q) {
+    for (Side* s : sides) {  // X products first, so the last iteration launches a prefix
+      const int64_t dp = s->dp;
+      float* A = b.ptr<float>(q == 0 ? s->M : s->T2);
+      l1[q].push_back(gemm_desc(b.ptr<float>(s->X[q]), A, b.ptr<float>(s->X[q]),
+                                b.ptr<float>(s->X[q ^ 1]), dp, dp, dp, dp, dp, dp, dp, 1,
+                                -1.0f / fp, (fp + 1.0f) / fp, 0.0f, t1[q]));
+    }
+    t1x[q] = t1[q];
+    for (Side* s : sides) {
+      const int64_t dp = s->dp;
+      float* A = b.ptr<float>(q == 0 ? s->M : s->T2);
+      float* B = b.ptr<float>(q == 0 ? s->T2 : s->M);
+      float* T4 = b.ptr<float>(s->T4);
+      if (p == 1) {
+        l1[q].push_back(gemm_desc(A, A, A, B, dp, dp, dp, dp, dp, dp, dp, 1, -1.0f, 2.0f, 0.0f, t1[q]));
+        continue;
+      }
+      const float ip2 = 1.0f / (fp * fp);
+      l1[q].push_back(gemm_desc(A, A, A, p == 4 ? B : T4, dp, dp, dp, dp, dp, dp, dp, 1, ip2,
+                                -2.0f * (fp + 1.0f) * ip2, (fp + 1.0f) * (fp + 1.0f) * ip2, t1[q]));
+      if (p == 4)
+        l2[q].push_back(gemm_desc(B, B, nullptr, T4, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f, t2[q]));
+      l3[q].push_back(gemm_desc(T4, A, nullptr, B, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f, t3[q]));
+    }
+  }
+  size_t o1[2], o2[2] = {0, 0}, o3[2] = {0, 0};
+  for (int q = 0; q < 2; ++q) {
+    o1[q] = b.put(l1[q]);
+    if (!l2[q].empty()) o2[q] = b.put(l2[q]);
+    if (!l3[q].empty()) o3[q] = b.put(l3[q]);
+  }
+  const int ns = int(sides.size());
+  for (int k = 0; k < iters; ++k) {
+    const int q = k & 1;
+    const bool last = k == iters - 1;
+    b.ops.push_back(Op{kOpGemm, o1[q], last ? ns : int(l1[q].size()), last ? t1x[q] : t1[q]});
+    if (last) break;
+    if (!l2[q].empty()) b.ops.push_back(Op{kOpGemm, o2[q], int(l2[q].size()), t2[q]});
+    if (!l3[q].empty()) b.ops.push_back(Op{kOpGemm, o3[q], int(l3[q].size()), t3[q]});
+  }
+  std::vector<ShCopyDesc> co;
+  int ct = 0;
+  for (Side* s : sides) {
+    if (!s->has_out) continue;
+    co.push_back(copy_desc(b.ptr<float>(s->X[iters & 1]), kDtF32, s->out, nullptr, s->d, s->d, s->dp,
+                           s->d, 0, s->d, s->d, ct));
+  }
+  b.op(kOpCopyOut, co, ct);
+}
+
+int run(Build& b, char* ws, size_t desc_at, hipStream_t st, double eps, double eps_rel, int p,
+        float decay, float step) {
+  if (!b.h.empty()) {
+    void* host = nullptr;
+    const int slot = staging_acquire(b.h.size(), &host);
+    if (slot < 0) return slot;
+    std::memcpy(host, b.h.data(), b.h.size());
+    const int rc = staging_upload(slot, ws + desc_at, b.h.size(), st);
+    if (rc != MFSDP_OK) return rc;
+  }
+  for (const Op& o : b.ops) {
+    char* dp = ws + desc_at + o.desc_off;
+    hipError_t e = hipSuccess;
+    switch (o.kind) {
+      case kOpCopyIn: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 0, st); break;
+      case kOpCopyOut: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 1, st); break;
+      case kOpGemm: e = launch_sh_gemm(reinterpret_cast<ShGemmDesc*>(dp), o.count, o.total, st); break;
+      case kOpNorm: e = launch_sh_norm(reinterpret_cast<ShNormDesc*>(dp), o.count, o.total, st); break;
+      case kOpScalars:
+        e = launch_sh_scalars(reinterpret_cast<ShScalarDesc*>(dp), o.count, eps, eps_rel, p, st);
+        break;
+      case kOpInit: e = launch_sh_init(reinterpret_cast<ShInitDesc*>(dp), o.count, o.total, st); break;
+      case kOpApply:
+        e = launch_sh_apply(reinterpret_cast<ShApplyDesc*>(dp), o.count, o.total, decay, step, st);
+        break;
+    }
+    if (e != hipSuccess) return hip_err(e, "Shampoo kernel launch");
+  }
+  return MFSDP_OK;
+}
+
+bool dtype_ok(int32_t dt) { return dt == MFSDP_F32 || dt == MFSDP_BF16; }
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int check_shampoo_hp(const mfsdp_shampoo_hparams* hp) {
+  if (!hp) return bad("hparams is NULL");
+  auto fin = [](double x) { return std::isfinite(x); };
+  if (!(hp->lr >= 0.0) || !fin(hp->lr)) return bad("lr must be finite and >= 0");
+  if (!(hp->weight_decay >= 0.0) || !fin(hp->weight_decay)) return bad("weight_decay must be finite and >= 0");
+  if (!(hp->beta >= 0.0) || !fin(hp->beta)) return bad("beta must be finite and >= 0");
+  if (!(hp->weight >= 0.0) || !fin(hp->weight)) return bad("weight must be finite and >= 0");
+  if (!(hp->eps > 0.0) || !fin(hp->eps)) return bad("eps must be finite and > 0");
+  if (!(hp->eps_rel >= 0.0) || !fin(hp->eps_rel)) return bad("eps_rel must be finite and >= 0");
+  if (hp->refresh != 0 && hp->refresh != 1) return bad("refresh must be 0 or 1");
+  if (hp->root_iters < 1 || hp->root_iters > 100) return bad("root_iters must be in [1, 100]");
+  return MFSDP_OK;
+}
+
+int check_shampoo_entries(const mfsdp_shampoo_entry* en, int64_t count, bool data) {
+  if (count < 0) return bad("count must be >= 0");
+  if (count > 0 && !en) return bad("entries is NULL");
+  if (count > 4096) return bad("at most 4096 entries per call");
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_shampoo_entry& e = en[i];
+    const std::string w = "entry " + std::to_string(i) + ": ";
+    if (e.m < 1 || e.n < 1 || e.m > kMaxDim || e.n > kMaxDim) return bad(w + "m and n must be in [1, 65536]");
+    if (!dtype_ok(e.param_dtype) || !dtype_ok(e.grad_dtype)) return bad(w + "dtype must be F32 or BF16");
+    if (!data) continue;
+    if (!e.param || !e.grad || !e.L || !e.R || !e.PL || !e.PR) return bad(w + "NULL pointer");
+    const size_t pa = e.param_dtype == MFSDP_BF16 ? 2 : 4, ga = e.grad_dtype == MFSDP_BF16 ? 2 : 4;
+    if (!aligned(e.param, pa) || !aligned(e.grad, ga) || !aligned(e.L, 4) || !aligned(e.R, 4) ||
+        !aligned(e.PL, 4) || !aligned(e.PR, 4) || !aligned(e.update_out, 4))
+      return bad(w + "misaligned pointer");
+  }
+  return MFSDP_OK;
+}
+
+// Builds the whole Shampoo step for `count` entries. Returns the workspace bytes (buffers, then
+// the descriptor region at desc_at).
+size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_shampoo_hparams* hp,
+                     char* ws, Build& b, size_t& desc_at) {
+  b.base = ws;
+  Arena a;
+  std::vector<EntryPlan> P(static_cast<size_t>(count));
+  for (int64_t i = 0; i < count; ++i) {
+    EntryPlan& e = P[size_t(i)];
+    e.m = en[i].m;
+    e.n = en[i].n;
+    e.mp = rup(e.m, kShTile);
+    e.np = rup(e.n, kShTile);
+    const size_t gbytes = size_t(e.mp) * size_t(e.np) * sizeof(float);
+    e.Gp = a.take(gbytes);
+    e.GpT = a.take(gbytes);
+    e.Y = a.take(gbytes);
+    plan_side(e.L, e.m, a);
+    plan_side(e.R, e.n, a);
+    e.L.out = en[i].PL;
+    e.R.out = en[i].PR;
+    e.L.has_out = e.R.has_out = true;
+  }
+  desc_at = a.off;
+  const bool refresh = hp->refresh != 0;
+  const int iters = hp->root_iters;
+  const int fin = refresh ? (iters & 1) : 0;
+
+  std::vector<ShCopyDesc> cin;
+  int ct = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    EntryPlan& e = P[size_t(i)];
+    cin.push_back(copy_desc(en[i].grad, en[i].grad_dtype, b.ptr<float>(e.Gp), b.ptr<float>(e.GpT), e.m,
+                            e.n, e.n, e.np, e.mp, e.mp, e.np, ct));
+    cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.L.M), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp,
+                            e.mp, ct));
+    cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.R.M), nullptr, e.n, e.n, e.n, e.np, 0, e.np,
+                            e.np, ct));
+    if (!refresh) {
+      cin.push_back(copy_desc(en[i].PL, kDtF32, b.ptr<float>(e.L.X[0]), nullptr, e.m, e.m, e.m, e.mp, 0,
+                              e.mp, e.mp, ct));
+      cin.push_back(copy_desc(en[i].PR, kDtF32, b.ptr<float>(e.R.X[0]), nullptr, e.n, e.n, e.n, e.np, 0,
+                              e.np, e.np, ct));
+    }
+  }
+  b.op(kOpCopyIn, cin, ct);
+
+  std::vector<ShGemmDesc> gs;
+  int gt = 0;
+  for (auto& e : P) {
+    gs.push_back(gemm_desc(b.ptr<float>(e.Gp), b.ptr<float>(e.Gp), b.ptr<float>(e.L.M), b.ptr<float>(e.L.M),
+                           e.np, e.np, e.mp, e.mp, e.mp, e.mp, e.np, 1, float(hp->weight),
+                           float(hp->beta), 0.0f, gt));
+    gs.push_back(gemm_desc(b.ptr<float>(e.GpT), b.ptr<float>(e.GpT), b.ptr<float>(e.R.M),
+                           b.ptr<float>(e.R.M), e.mp, e.mp, e.np, e.np, e.np, e.np, e.mp, 1,
+                           float(hp->weight), float(hp->beta), 0.0f, gt));
+  }
+  b.op(kOpGemm, gs, gt);
+
+  std::vector<ShCopyDesc> cst;
+  ct = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    EntryPlan& e = P[size_t(i)];
+    cst.push_back(copy_desc(b.ptr<float>(e.L.M), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m,
+                            e.m, ct));
+    cst.push_back(copy_desc(b.ptr<float>(e.R.M), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n,
+                            e.n, ct));
+  }
+  b.op(kOpCopyOut, cst, ct);
+
+  if (refresh) {
+    std::vector<Side*> sides;
+    for (auto& e : P) {
+      sides.push_back(&e.L);
+      sides.push_back(&e.R);
+    }
+    add_root_ops(b, sides, 4, iters);
+  }
+
+  std::vector<ShGemmDesc> gy, gu;
+  int ty = 0, tu = 0;
+  for (auto& e : P) {
+    gy.push_back(gemm_desc(b.ptr<float>(e.L.X[fin]), b.ptr<float>(e.GpT), nullptr, b.ptr<float>(e.Y),
+                           e.mp, e.mp, 0, e.np, e.mp, e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
+    gu.push_back(gemm_desc(b.ptr<float>(e.Y), b.ptr<float>(e.R.X[fin]), nullptr, b.ptr<float>(e.Gp),
+                           e.np, e.np, 0, e.np, e.mp, e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
+  }
+  b.op(kOpGemm, gy, ty);
+  b.op(kOpGemm, gu, tu);
+
+  std::vector<ShApplyDesc> ap;
+  int at = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    EntryPlan& e = P[size_t(i)];
+    ShApplyDesc d{};
+    d.U = b.ptr<float>(e.Gp);
+    d.ldu = e.np;
+    d.param = en[i].param;
+    d.update_out = en[i].update_out;
+    d.m = e.m;
+    d.n = e.n;
+    d.param_dtype = en[i].param_dtype == MFSDP_BF16 ? kDtBF16 : kDtF32;
+    const int64_t tn = (e.n + kShCopyTile - 1) / kShCopyTile, tm = (e.m + kShCopyTile - 1) / kShCopyTile;
+    d.tiles_n = int32_t(tn);
+    d.tile_begin = at;
+    at += int(tm * tn);
+    ap.push_back(d);
+  }
+  b.op(kOpApply, ap, at);
+  return desc_at + al(b.h.size());
+}
+
+size_t build_root(int64_t d, int p, int iters, const float* a, float* out, char* ws, Build& b,
+                  size_t& desc_at) {
+  b.base = ws;
+  Arena ar;
+  Side s;
+  plan_side(s, d, ar);
+  s.out = out;
+  s.has_out = true;
+  desc_at = ar.off;
+  std::vector<ShCopyDesc> cin;
+  int ct = 0;
+  cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.M), nullptr, d, d, d, s.dp, 0, s.dp, s.dp, ct));
+  b.op(kOpCopyIn, cin, ct);
+  std::vector<Side*> sides{&s};
+  add_root_ops(b, sides, p, iters);
+  return desc_at + al(b.h.size());
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mfsdp_shampoo_workspace_size(const mfsdp_shampoo_entry* entries, int64_t count,
+                                    const mfsdp_shampoo_hparams* hp) {
+  if (check_shampoo_entries(entries, count, false) != MFSDP_OK) return 0;
+  if (check_shampoo_hp(hp) != MFSDP_OK) return 0;
+  if (count == 0) return 0;
+  Build b;
+  size_t desc_at = 0;
+  return build_shampoo(entries, count, hp, nullptr, b, desc_at);
+}
+
+int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count, const mfsdp_shampoo_hparams* hp,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_shampoo_entries(entries, count, true);
+  if (rc != MFSDP_OK) return rc;
+  rc = check_shampoo_hp(hp);
+  if (rc != MFSDP_OK) return rc;
+  if (count == 0) return MFSDP_OK;
+  Build b;
+  size_t desc_at = 0;
+  const size_t need = build_shampoo(entries, count, hp, static_cast<char*>(workspace), b, desc_at);
+  if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
+    return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
+                                             "mfsdp_shampoo_workspace_size (" + std::to_string(need) + " bytes)");
+  const double decay = 1.0 - hp->lr * hp->weight_decay;
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), hp->eps,
+             hp->eps_rel, 4, float(decay), float(hp->lr));
+}
+
+size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters) {
+  if (d < 1 || d > kMaxDim || (p != 1 && p != 2 && p != 4) || iters < 1 || iters > 100) return 0;
+  Build b;
+  size_t desc_at = 0;
+  return build_root(d, p, iters, nullptr, nullptr, nullptr, b, desc_at);
+}
+
+int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double eps, double eps_rel,
+                       int32_t iters, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!a || !out) return bad("a and out must be non-NULL");
+  if (!aligned(a, 4) || !aligned(out, 4)) return bad("misaligned pointer");
+  if (d < 1 || d > kMaxDim) return bad("d must be in [1, 65536]");
+  if (p != 1 && p != 2 && p != 4) return bad("p must be 1, 2 or 4");
+  if (!(eps > 0.0) || !std::isfinite(eps)) return bad("eps must be finite and > 0");
+  if (!(eps_rel >= 0.0) || !std::isfinite(eps_rel)) return bad("eps_rel must be finite and >= 0");
+  if (iters < 1 || iters > 100) return bad("iters must be in [1, 100]");
+  Build b;
+  size_t desc_at = 0;
+  const size_t need = build_root(d, p, iters, a, out, static_cast<char*>(workspace), b, desc_at);
+  if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
+    return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
+                                             "mfsdp_inverse_root_workspace_size (" + std::to_string(need) + " bytes)");
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), eps, eps_rel, p,
+             1.0f, 0.0f);
+}
+
+}  // extern "C"

@@ -20,9 +20,11 @@ _NS_DT = {"bf16": BF16, "f32": F32}
 _LR_MODES = {"none": LR_NONE, "original": LR_ORIGINAL, "match_rms_adamw": LR_MATCH_RMS_ADAMW}
 EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_timed", "mfsdp_ns_workspace_size",
            "mfsdp_newton_schulz", "mfsdp_newton_schulz_schedule", "mfsdp_adamw_step", "mfsdp_last_error",
-           "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners")
+           "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners",
+           "mfsdp_shampoo_workspace_size", "mfsdp_shampoo_step", "mfsdp_inverse_root_workspace_size",
+           "mfsdp_inverse_root")
 MAX_GRAD_PARTS = 64
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 
 class MuonEntry(ctypes.Structure):
@@ -46,6 +48,19 @@ class AdamWEntry(ctypes.Structure):
                 ("exp_avg", ctypes.c_void_p), ("exp_avg_sq", ctypes.c_void_p),
                 ("numel", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
                 ("grad_dtype", ctypes.c_int32)]
+
+
+class ShampooEntry(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("L", ctypes.c_void_p),
+                ("R", ctypes.c_void_p), ("PL", ctypes.c_void_p), ("PR", ctypes.c_void_p),
+                ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("param_dtype", ctypes.c_int32),
+                ("grad_dtype", ctypes.c_int32), ("update_out", ctypes.c_void_p)]
+
+
+class ShampooHParams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("weight_decay", ctypes.c_double), ("beta", ctypes.c_double),
+                ("weight", ctypes.c_double), ("eps", ctypes.c_double), ("eps_rel", ctypes.c_double),
+                ("refresh", ctypes.c_int32), ("root_iters", ctypes.c_int32)]
 
 
 class PlanParam(ctypes.Structure):
@@ -107,6 +122,15 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_plan_owners.argtypes = [ctypes.POINTER(PlanParam), i64, i32, i32, f64, ctypes.POINTER(i32),
                                         ctypes.POINTER(i64), ctypes.POINTER(f64), ctypes.POINTER(i32)]
         L.mfsdp_plan_owners.restype = ctypes.c_int
+        L.mfsdp_shampoo_workspace_size.argtypes = [ctypes.POINTER(ShampooEntry), i64, ctypes.POINTER(ShampooHParams)]
+        L.mfsdp_shampoo_workspace_size.restype = sz
+        L.mfsdp_shampoo_step.argtypes = [ctypes.POINTER(ShampooEntry), i64, ctypes.POINTER(ShampooHParams), vp,
+                                         sz, vp]
+        L.mfsdp_shampoo_step.restype = ctypes.c_int
+        L.mfsdp_inverse_root_workspace_size.argtypes = [i64, i32, i32]
+        L.mfsdp_inverse_root_workspace_size.restype = sz
+        L.mfsdp_inverse_root.argtypes = [vp, vp, i64, i32, f64, f64, i32, vp, sz, vp]
+        L.mfsdp_inverse_root.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -148,6 +172,26 @@ def mfsdp_plan_owners(params, world: int, policy: int, gamma_cap: float = 0.0):
     _check(lib().mfsdp_plan_owners(arr, len(params), world, policy, gamma_cap, owner, loads, gam,
                                    ctypes.byref(used)))
     return list(owner[:len(params)]), list(loads[:world]), list(gam[:nblocks]), used.value
+
+
+def mfsdp_shampoo_workspace_size(entries: Sequence[ShampooEntry], hp: ShampooHParams) -> int:
+    arr, n = _entries(entries, ShampooEntry)
+    return lib().mfsdp_shampoo_workspace_size(arr, n, ctypes.byref(hp))
+
+
+def mfsdp_shampoo_step(entries: Sequence[ShampooEntry], hp: ShampooHParams, workspace: int,
+                       workspace_bytes: int, stream: int) -> None:
+    arr, n = _entries(entries, ShampooEntry)
+    _check(lib().mfsdp_shampoo_step(arr, n, ctypes.byref(hp), workspace, workspace_bytes, stream))
+
+
+def mfsdp_inverse_root_workspace_size(d: int, p: int, iters: int) -> int:
+    return lib().mfsdp_inverse_root_workspace_size(d, p, iters)
+
+
+def mfsdp_inverse_root(a: int, out: int, d: int, p: int, eps: float, eps_rel: float, iters: int,
+                       workspace: int, workspace_bytes: int, stream: int) -> None:
+    _check(lib().mfsdp_inverse_root(a, out, d, p, eps, eps_rel, iters, workspace, workspace_bytes, stream))
 
 
 def mfsdp_muon_workspace_size(entries: Sequence[MuonEntry], hp: MuonHParams) -> int:
@@ -303,3 +347,35 @@ def adamw_entry_t(param, grad, exp_avg, exp_avg_sq) -> AdamWEntry:
 def adamw_step_t(entries: Sequence[AdamWEntry], lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
                  weight_decay=1e-2, step=1) -> None:
     mfsdp_adamw_step(entries, lr, beta1, beta2, eps, weight_decay, step, _stream())
+
+
+def shampoo_hparams(lr=1e-3, weight_decay=0.0, beta=1.0, weight=1.0, eps=1e-12, eps_rel=1e-6,
+                    refresh=True, root_iters=20) -> ShampooHParams:
+    return ShampooHParams(lr, weight_decay, beta, weight, eps, eps_rel, int(bool(refresh)), root_iters)
+
+
+def shampoo_entry_t(param, grad, L, R, PL, PR, update_out=None) -> ShampooEntry:
+    m, n = param.shape
+    return ShampooEntry(param.data_ptr(), grad.data_ptr(), L.data_ptr(), R.data_ptr(), PL.data_ptr(),
+                        PR.data_ptr(), m, n, _dt(param), _dt(grad),
+                        update_out.data_ptr() if update_out is not None else None)
+
+
+def shampoo_workspace_t(entries: Sequence[ShampooEntry], hp: ShampooHParams, device="cuda"):
+    import torch
+    size = mfsdp_shampoo_workspace_size(entries, hp)
+    return torch.empty(max(size, 256), dtype=torch.uint8, device=device)
+
+
+def shampoo_step_t(entries: Sequence[ShampooEntry], hp: ShampooHParams, workspace) -> None:
+    mfsdp_shampoo_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def inverse_root_t(a, out, p=4, eps=1e-12, eps_rel=1e-6, iters=20, workspace=None) -> None:
+    import torch
+    d = a.shape[0]
+    if workspace is None:
+        workspace = torch.empty(mfsdp_inverse_root_workspace_size(d, p, iters), dtype=torch.uint8,
+                                device=a.device)
+    mfsdp_inverse_root(a.data_ptr(), out.data_ptr(), d, p, eps, eps_rel, iters, workspace.data_ptr(),
+                       workspace.numel(), _stream())

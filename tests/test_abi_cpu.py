@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert native.mfsdp_abi_version() == native.ABI_VERSION == 3
+    assert native.mfsdp_abi_version() == native.ABI_VERSION == 4
     assert native.mfsdp_status_string(0) == "MFSDP_OK"
     assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
     assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
@@ -193,3 +193,103 @@ def test_adamw_rejects_bad_entries(bad):
     with pytest.raises(native.MfsdpError) as ei:
         native.mfsdp_adamw_step([good, native.AdamWEntry(**d)], 1e-3, 0.9, 0.999, 1e-8, 0.0, 1, 0)
     assert ei.value.status == native.E_INVALID
+
+
+# ---------------------------------------------------------------------------------------------
+# Shampoo and the inverse root
+
+def _sh_entry(**kw):
+    d = dict(param=FAKE, grad=FAKE * 2, L=FAKE * 3, R=FAKE * 4, PL=FAKE * 5, PR=FAKE * 6, m=96,
+             n=200, param_dtype=1, grad_dtype=1, update_out=None)
+    d.update(kw)
+    return native.ShampooEntry(**d)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(m=0), dict(n=70000), dict(param=None), dict(grad=None), dict(L=None), dict(R=None),
+    dict(PL=None), dict(PR=None), dict(param_dtype=3), dict(grad_dtype=-1), dict(L=FAKE * 3 + 2),
+    dict(param=FAKE + 1), dict(update_out=FAKE + 2),
+])
+def test_shampoo_rejects_bad_entries(bad):
+    hp = native.shampoo_hparams()
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_shampoo_step([_sh_entry(), _sh_entry(**bad)], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+@pytest.mark.parametrize("bad", [
+    dict(lr=-1.0), dict(weight_decay=-1.0), dict(beta=-0.1), dict(weight=float("nan")), dict(eps=0.0),
+    dict(eps_rel=-1e-6), dict(root_iters=0), dict(root_iters=101), dict(lr=float("inf")),
+])
+def test_shampoo_rejects_bad_hparams(bad):
+    hp = native.shampoo_hparams(**bad)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_shampoo_step([_sh_entry()], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+    assert native.mfsdp_shampoo_workspace_size([_sh_entry()], hp) == 0
+
+
+def test_shampoo_refresh_flag_and_workspace_checks():
+    hp = native.shampoo_hparams()
+    hp.refresh = 2
+    with pytest.raises(native.MfsdpError):
+        native.mfsdp_shampoo_step([_sh_entry()], hp, FAKE * 16, 1 << 40, 0)
+    hp = native.shampoo_hparams()
+    need = native.mfsdp_shampoo_workspace_size([_sh_entry()], hp)
+    # padded to 128: G, G^T and P_L G (3 x 128 x 256) plus 5 matrices per side (128^2 + 256^2)
+    assert need >= 4 * (3 * 128 * 256 + 5 * (128 ** 2 + 256 ** 2))
+    for ws, nb in ((None, need), (FAKE * 16 + 8, need), (FAKE * 16, need - 1)):
+        with pytest.raises(native.MfsdpError) as ei:
+            native.mfsdp_shampoo_step([_sh_entry()], hp, ws, nb, 0)
+        assert ei.value.status == native.E_WORKSPACE
+    # the size query does not depend on the data pointers, and count == 0 is a no-op
+    assert native.mfsdp_shampoo_workspace_size([_sh_entry(param=None, L=None)], hp) == need
+    assert native.mfsdp_shampoo_workspace_size([], hp) == 0
+    native.mfsdp_shampoo_step([], hp, None, 0, 0)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(d=0), dict(d=70000), dict(p=3), dict(p=0), dict(eps=0.0), dict(eps_rel=-1.0), dict(iters=0),
+    dict(iters=101), dict(a=None), dict(out=None), dict(a=FAKE + 2),
+])
+def test_inverse_root_rejects_bad_arguments(bad):
+    args = dict(a=FAKE, out=FAKE * 2, d=100, p=4, eps=1e-9, eps_rel=1e-6, iters=20)
+    args.update(bad)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_inverse_root(args["a"], args["out"], args["d"], args["p"], args["eps"],
+                                  args["eps_rel"], args["iters"], FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+def test_inverse_root_workspace_query():
+    assert native.mfsdp_inverse_root_workspace_size(100, 4, 20) >= 5 * 128 * 128 * 4
+    assert native.mfsdp_inverse_root_workspace_size(100, 3, 20) == 0
+    assert native.mfsdp_inverse_root_workspace_size(0, 4, 20) == 0
+    need = native.mfsdp_inverse_root_workspace_size(300, 2, 7)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_inverse_root(FAKE, FAKE * 2, 300, 2, 1e-9, 0.0, 7, FAKE * 16, need - 1, 0)
+    assert ei.value.status == native.E_WORKSPACE
+
+
+def _needed_bytes(fn):
+    with pytest.raises(native.MfsdpError) as ei:
+        fn()
+    assert ei.value.status == native.E_WORKSPACE
+    return int(re.search(r"\((\d+) bytes\)", str(ei.value)).group(1))
+
+
+@pytest.mark.parametrize("refresh", [0, 1])
+def test_shampoo_size_query_equals_what_the_call_needs(refresh):
+    ents = [_sh_entry(), _sh_entry(m=1, n=50, param_dtype=0), _sh_entry(m=300, n=129)]
+    hp = native.shampoo_hparams(refresh=bool(refresh), root_iters=7)
+    q = native.mfsdp_shampoo_workspace_size([native.ShampooEntry(m=e.m, n=e.n, param_dtype=e.param_dtype,
+                                                                 grad_dtype=e.grad_dtype) for e in ents], hp)
+    assert q > 0
+    assert _needed_bytes(lambda: native.mfsdp_shampoo_step(ents, hp, FAKE * 16, 0, 0)) == q
+
+
+@pytest.mark.parametrize("p,iters", [(1, 1), (2, 8), (4, 20)])
+def test_inverse_root_size_query_equals_what_the_call_needs(p, iters):
+    q = native.mfsdp_inverse_root_workspace_size(257, p, iters)
+    assert _needed_bytes(lambda: native.mfsdp_inverse_root(FAKE, FAKE * 2, 257, p, 1e-9, 1e-6, iters,
+                                                           FAKE * 16, 0, 0)) == q
