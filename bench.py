@@ -267,6 +267,63 @@ def planner_report(native, spans, gpu_span, ctx=None) -> dict:
     return out
 
 
+PEAK_F32_MFMA_TFLOPS = 157.3  # dense fp32 MFMA
+
+
+def shampoo_nominal_flop(shapes, iters: int, refresh: bool) -> float:
+    """Nominal flop of one Shampoo step: statistics G G^T and G^T G, P_L G and (P_L G) P_R, and on
+    refresh 4 iters - 3 products of d x d per side (the last iteration forms X only)."""
+    tot = 0.0
+    for m, n in shapes:
+        tot += 2.0 * m * m * n + 2.0 * m * n * n          # statistics
+        tot += 2.0 * m * m * n + 2.0 * m * n * n          # U = P_L G P_R
+        if refresh:
+            tot += (4 * iters - 3) * 2.0 * (m ** 3 + n ** 3)
+    return tot
+
+
+def time_shampoo(native, torch, dev, hev, stream, steps, warmup, iters=20) -> dict:
+    """The Shampoo owner step (Section 5.7) on the GPT-2-small share's 12 matrices, fp32 math."""
+    import synth
+    wl = synth.workload(2)
+    shapes = [(e.m, e.n) for e in wl.muon]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2)
+    keep, ents = [], []
+    for m, n in shapes:
+        t = ((torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
+             (torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
+             torch.zeros(m, m, device=dev), torch.zeros(n, n, device=dev),
+             torch.zeros(m, m, device=dev), torch.zeros(n, n, device=dev))
+        keep.append(t)
+        ents.append(native.shampoo_entry_t(*t))
+    out = {"workload": wl.name + " (12 matrices: 8 x 768x768, 2 x 3072x768, 2 x 768x3072)",
+           "root_iters": iters, "ridge": "1e-12 + 1e-6 ||S||_F", "dtype": "f32"}
+    for refresh in (True, False):
+        hp = native.shampoo_hparams(lr=1e-3, weight_decay=0.01, beta=0.95, weight=0.05, eps=1e-12,
+                                    eps_rel=1e-6, refresh=refresh, root_iters=iters)
+        ws = native.shampoo_workspace_t(ents, hp, device=dev)
+        for _ in range(warmup):
+            native.shampoo_step_t(ents, hp, ws)
+        torch.cuda.synchronize()
+        a, b = hev.create(), hev.create()
+        hev.record(a, stream)
+        for _ in range(steps):
+            native.shampoo_step_t(ents, hp, ws)
+        hev.record(b, stream)
+        torch.cuda.synchronize()
+        ms = hev.elapsed_ms(a, b) / steps
+        fl = shampoo_nominal_flop(shapes, iters, refresh)
+        key = "refresh" if refresh else "stale_preconditioners"
+        out[key] = {"ms_per_step": round(ms, 4), "nominal_flop_per_step": fl,
+                    "nominal_tflops": round(fl / (ms * 1e-3) / 1e12, 2),
+                    "frac_fp32_mfma_peak": round(fl / (ms * 1e-3) / 1e12 / PEAK_F32_MFMA_TFLOPS, 4),
+                    "workspace_gib": round(ws.numel() / 2 ** 30, 3)}
+        log(f"shampoo ({key}): {ms:.3f} ms per step, {fl / (ms * 1e-3) / 1e12:.1f} nominal TFLOP/s")
+        del ws
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,6 +340,8 @@ def main() -> int:
     ap.add_argument("--plan-span", type=int, default=0, choices=[0] + sorted(PLAN_SWEEP),
                     help="also run every rank's owner share of the planned decoder sweep model at this "
                          "shard span on the GPU and report the step-time imbalance over ranks")
+    ap.add_argument("--shampoo", action="store_true",
+                    help="also time the Shampoo owner step (fp32 MFMA) on the GPT-2-small share")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -456,6 +515,8 @@ def main() -> int:
                                                   if args.plan_span else ""))
     pctx = (torch, dev, hev, stream, h, ah, 5, 2) if args.plan_span else None
     out["planner"] = planner_report(native, sorted(PLAN_SWEEP), args.plan_span, pctx)
+    if args.shampoo:
+        out["shampoo"] = time_shampoo(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])

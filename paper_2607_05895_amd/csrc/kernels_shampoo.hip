@@ -54,6 +54,7 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
   const int e = find_desc(descs, count, blockIdx.x);
   const ShGemmDesc& d = descs[e];
   int lt = blockIdx.x - d.tile_begin;
+  if (d.clear && lt == 0 && threadIdx.x == 0) *d.clear = 0.0f;
   int bi, bj;
   if (d.sym) {
     bi = 0;
@@ -70,6 +71,22 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
   }
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wr = w >> 1, wc = w & 1;
+  if (d.conv_in && *d.conv_in < kShConvTol) {  // converged side: the iterate no longer changes
+    if (d.copy_on_skip) {
+      const g_cf32* src = (const g_cf32*)(d.E);
+      g_f32* dst = (g_f32*)(d.C);
+#pragma unroll 4
+      for (int it = 0; it < 64; ++it) {
+        const int r = (t >> 7) + 2 * it, c = t & 127;
+        dst[(int64_t(bi) * kShTile + r) * d.ldc + int64_t(bj) * kShTile + c] =
+            src[(int64_t(bi) * kShTile + r) * d.lde + int64_t(bj) * kShTile + c];
+        if (bi != bj)
+          dst[(int64_t(bj) * kShTile + r) * d.ldc + int64_t(bi) * kShTile + c] =
+              src[(int64_t(bj) * kShTile + r) * d.lde + int64_t(bi) * kShTile + c];
+      }
+    }
+    return;
+  }
   const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
   const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
   const int lrow = t >> 3, lch = t & 7;
@@ -133,6 +150,7 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
   const bool diag_tile = d.sym && bi == bj;
   float* tl = reinterpret_cast<float*>(&lds[0][0][0]);  // 128 x 128 floats, element (r, c) at r*128 + (c ^ r)
   const int64_t r0 = int64_t(bi) * kShTile, c0 = int64_t(bj) * kShTile;
+  float res = 0.0f;  // max |C - I| over this thread's elements of the real block
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
@@ -148,7 +166,18 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
         if (gr == gc) x += d.diag;
         C[gr * d.ldc + gc] = x;
         if (d.sym) tl[r * kShTile + (c ^ r)] = x;
+        if (gr < d.valid && gc < d.valid) {
+          const float dv = fabsf(x - (gr == gc ? 1.0f : 0.0f));
+          res = (dv > res || dv != dv) ? dv : res;  // keeps a NaN
+        }
       }
+  if (d.resid_out) {
+    // NaN propagates as the largest bit pattern, so a diverged side never counts as converged
+    uint32_t rb = __float_as_uint(res);
+    if (res != res) rb = 0x7fc00000u;
+    for (int o = 32; o > 0; o >>= 1) rb = max(rb, uint32_t(__shfl_xor(int(rb), o)));
+    if (lane == 0) atomicMax(reinterpret_cast<unsigned int*>(d.resid_out), rb);
+  }
   if (d.sym) {
     __syncthreads();
 #pragma unroll 4
@@ -269,6 +298,7 @@ __global__ __launch_bounds__(256) void sh_init_kernel(const ShInitDesc* __restri
   const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
   const float rho = d.sc[0], z = d.sc[1], zp = d.sc[2];
   const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  if (lt == 0 && t < 2) d.resid[t] = t == 0 ? 0.0f : 3.0e38f;
   const int64_t gc = int64_t(tj) * kShCopyTile + c;
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {

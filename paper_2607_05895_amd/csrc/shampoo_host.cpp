@@ -6,6 +6,9 @@
 //   refresh: P_L = (L + rho_L I)^(-1/4), P_R = (R + rho_R I)^(-1/4), rho = eps + eps_rel ||S||_F
 //   U = P_L G P_R,  p <- p (1 - lr wd) - lr U
 //
+// Convergence: the M product of every iteration also records max |M - I| over the real block; once
+// it is below kShConvTol, the side's later products are skipped and its X products become copies.
+//
 // Inverse p-th root by the coupled Newton iteration (Guo and Higham, SIAM J. Matrix Anal. Appl.
 // 2006; the form used for Shampoo by Anil et al. 2020): with z = (1 + p) / (2 ||A||_F),
 //   X_0 = z^(1/p) I,  M_0 = z A,  T_k = ((p + 1) I - M_k) / p,
@@ -20,6 +23,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -62,7 +66,7 @@ struct Arena {
 // One inverse-root problem on a padded d_pad x d_pad statistic held in M.
 struct Side {
   int64_t d = 0, dp = 0;
-  size_t M = 0, T2 = 0, T4 = 0, X[2] = {0, 0}, partials = 0, sc = 0;
+  size_t M = 0, T2 = 0, T4 = 0, X[2] = {0, 0}, partials = 0, sc = 0, resid = 0;
   float* out = nullptr;  // caller destination of the root (d x d, row stride d)
   bool has_out = false;  // copy the root out (decided by the call, not by the pointer value,
                          // so that the size query, which sees no pointers, builds the same ops)
@@ -79,6 +83,7 @@ void plan_side(Side& s, int64_t d, Arena& a) {
   s.X[1] = a.take(mat);
   s.partials = a.take(size_t(s.dp / kNormChunkRows) * 2 * sizeof(double));
   s.sc = a.take(4 * sizeof(float));
+  s.resid = a.take(2 * sizeof(float));
 }
 
 struct EntryPlan {
@@ -165,7 +170,10 @@ ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, float* C, i
 }
 
 // Root ops for every side: norms, scalars, init, the iterations and the copy of X to side.out.
-void add_root_ops(Build& b, std::vector<Side*>& sides, int p, int iters) {
+// In every grouped launch the larger problems come first (their tiles run longest), so the
+// hardware's in-order dispatch fills the tail of the launch with the short tiles.
+void add_root_ops(Build& b, std::vector<Side*> sides, int p, int iters) {
+  std::stable_sort(sides.begin(), sides.end(), [](const Side* x, const Side* y) { return x->dp > y->dp; });
   std::vector<ShNormDesc> nd;
   std::vector<ShScalarDesc> sd;
   std::vector<ShInitDesc> idesc;
@@ -191,6 +199,7 @@ void add_root_ops(Build& b, std::vector<Side*>& sides, int p, int iters) {
     in.S = b.ptr<float>(s->M);
     in.M = b.ptr<float>(s->M);
     in.X = b.ptr<float>(s->X[0]);
+    in.resid = b.ptr<float>(s->resid);
     in.ld = s->dp;
     in.sc = c.out;
     in.tiles_n = int32_t(s->dp / kShCopyTile);
@@ -203,16 +212,25 @@ void add_root_ops(Build& b, std::vector<Side*>& sides, int p, int iters) {
   b.op(kOpInit, idesc, itiles);
 
   const float fp = float(p);
-  // per parity q: A holds M_k, B receives M_{k+1}; X[q] -> X[q ^ 1]
+  // per parity q: A holds M_k, B receives M_{k+1}; X[q] -> X[q ^ 1]; residual slots q^1 (read)
+  // and q (cleared by the first launch of the iteration, written by the M product)
   std::vector<ShGemmDesc> l1[2], l2[2], l3[2];
   int t1[2] = {0, 0}, t1x[2] = {0, 0}, t2[2] = {0, 0}, t3[2] = {0, 0};
+  auto roots = [&](ShGemmDesc g, const Side* s, int q) {
+    g.conv_in = b.ptr<float>(s->resid + sizeof(float) * (q ^ 1));
+    g.valid = int32_t(s->d);
+    return g;
+  };
   for (int q = 0; q < 2; ++q) {
     for (Side* s : sides) {  // X products first, so the last iteration launches a prefix
       const int64_t dp = s->dp;
       float* A = b.ptr<float>(q == 0 ? s->M : s->T2);
-      l1[q].push_back(gemm_desc(b.ptr<float>(s->X[q]), A, b.ptr<float>(s->X[q]),
-                                b.ptr<float>(s->X[q ^ 1]), dp, dp, dp, dp, dp, dp, dp, 1,
-                                -1.0f / fp, (fp + 1.0f) / fp, 0.0f, t1[q]));
+      ShGemmDesc g = roots(gemm_desc(b.ptr<float>(s->X[q]), A, b.ptr<float>(s->X[q]),
+                                     b.ptr<float>(s->X[q ^ 1]), dp, dp, dp, dp, dp, dp, dp, 1,
+                                     -1.0f / fp, (fp + 1.0f) / fp, 0.0f, t1[q]), s, q);
+      g.copy_on_skip = 1;
+      g.clear = b.ptr<float>(s->resid + sizeof(float) * q);
+      l1[q].push_back(g);
     }
     t1x[q] = t1[q];
     for (Side* s : sides) {
@@ -220,16 +238,21 @@ void add_root_ops(Build& b, std::vector<Side*>& sides, int p, int iters) {
       float* A = b.ptr<float>(q == 0 ? s->M : s->T2);
       float* B = b.ptr<float>(q == 0 ? s->T2 : s->M);
       float* T4 = b.ptr<float>(s->T4);
+      ShGemmDesc mupd;
       if (p == 1) {
-        l1[q].push_back(gemm_desc(A, A, A, B, dp, dp, dp, dp, dp, dp, dp, 1, -1.0f, 2.0f, 0.0f, t1[q]));
-        continue;
+        mupd = roots(gemm_desc(A, A, A, B, dp, dp, dp, dp, dp, dp, dp, 1, -1.0f, 2.0f, 0.0f, t3[q]), s, q);
+      } else {
+        const float ip2 = 1.0f / (fp * fp);
+        l1[q].push_back(roots(gemm_desc(A, A, A, p == 4 ? B : T4, dp, dp, dp, dp, dp, dp, dp, 1, ip2,
+                                        -2.0f * (fp + 1.0f) * ip2, (fp + 1.0f) * (fp + 1.0f) * ip2, t1[q]),
+                              s, q));
+        if (p == 4)
+          l2[q].push_back(roots(gemm_desc(B, B, nullptr, T4, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f,
+                                          t2[q]), s, q));
+        mupd = roots(gemm_desc(T4, A, nullptr, B, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f, t3[q]), s, q);
       }
-      const float ip2 = 1.0f / (fp * fp);
-      l1[q].push_back(gemm_desc(A, A, A, p == 4 ? B : T4, dp, dp, dp, dp, dp, dp, dp, 1, ip2,
-                                -2.0f * (fp + 1.0f) * ip2, (fp + 1.0f) * (fp + 1.0f) * ip2, t1[q]));
-      if (p == 4)
-        l2[q].push_back(gemm_desc(B, B, nullptr, T4, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f, t2[q]));
-      l3[q].push_back(gemm_desc(T4, A, nullptr, B, dp, dp, 0, dp, dp, dp, dp, 1, 1.0f, 0.0f, 0.0f, t3[q]));
+      mupd.resid_out = b.ptr<float>(s->resid + sizeof(float) * q);
+      l3[q].push_back(mupd);
     }
   }
   size_t o1[2], o2[2] = {0, 0}, o3[2] = {0, 0};
@@ -371,9 +394,16 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   }
   b.op(kOpCopyIn, cin, ct);
 
+  // grouped products over the entries, largest first (see add_root_ops)
+  std::vector<EntryPlan*> order;
+  for (auto& e : P) order.push_back(&e);
+  std::stable_sort(order.begin(), order.end(), [](const EntryPlan* x, const EntryPlan* y) {
+    return std::max(x->mp, x->np) > std::max(y->mp, y->np);
+  });
   std::vector<ShGemmDesc> gs;
   int gt = 0;
-  for (auto& e : P) {
+  for (EntryPlan* ep : order) {
+    EntryPlan& e = *ep;
     gs.push_back(gemm_desc(b.ptr<float>(e.Gp), b.ptr<float>(e.Gp), b.ptr<float>(e.L.M), b.ptr<float>(e.L.M),
                            e.np, e.np, e.mp, e.mp, e.mp, e.mp, e.np, 1, float(hp->weight),
                            float(hp->beta), 0.0f, gt));
@@ -405,7 +435,8 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
 
   std::vector<ShGemmDesc> gy, gu;
   int ty = 0, tu = 0;
-  for (auto& e : P) {
+  for (EntryPlan* ep : order) {
+    EntryPlan& e = *ep;
     gy.push_back(gemm_desc(b.ptr<float>(e.L.X[fin]), b.ptr<float>(e.GpT), nullptr, b.ptr<float>(e.Y),
                            e.mp, e.mp, 0, e.np, e.mp, e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
     gu.push_back(gemm_desc(b.ptr<float>(e.Y), b.ptr<float>(e.R.X[fin]), nullptr, b.ptr<float>(e.Gp),

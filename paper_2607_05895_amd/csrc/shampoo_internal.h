@@ -17,6 +17,10 @@ namespace mfsdp {
 
 constexpr int kShTile = 128;     // GEMM output tile and padding granularity
 constexpr int kShCopyTile = 64;  // copy / init / apply tile
+// Convergence of the inverse-root iteration: once max |M_k - I| over the real block is below this,
+// the remaining change of X is below 2.5e-6 relative (T_k = I - (M_k - I)/p, then quadratic), and
+// the side's remaining products are skipped.
+constexpr float kShConvTol = 1e-5f;
 
 // C = alpha * P Q^T + beta * E + diag * I over one padded problem (P: M x K, Q: N x K, all
 // row-major with the given row strides). sym: only tiles bi <= bj are computed; each is stored at
@@ -33,6 +37,14 @@ struct ShGemmDesc {
   int32_t sym;
   int32_t tile_begin;  // prefix over the problems of one launch
   float alpha, beta, diag;
+  // inverse-root iteration only (null otherwise). Each side has two residual slots; iteration k
+  // (parity q) reads slot q^1 (written by iteration k-1) and writes slot q:
+  const float* conv_in;  // skip the product when this residual is below kShConvTol (and, with
+                         // copy_on_skip, copy the tile of E into C instead)
+  float* clear;          // set to 0 by the problem's first block before anything else
+  float* resid_out;      // max |C - I| over the real block (rows, cols < valid), atomic max
+  int32_t copy_on_skip;
+  int32_t valid;
 };
 
 // Boundary copies over 64 x 64 tiles of a padded rows_pad x cols_pad domain.
@@ -74,6 +86,7 @@ struct ShInitDesc {
   const float* S;
   float* M;
   float* X;
+  float* resid;        // the two residual slots: {0, not converged}
   int64_t ld;
   const float* sc;     // {rho, z, z^(1/p)}
   int32_t tiles_n;

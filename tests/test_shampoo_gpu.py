@@ -256,3 +256,26 @@ def test_shampoo_lr_zero_and_determinism(native):
     _sync()
     for x, u in zip(mats, u1):
         assert bool((x.dU == u).all())
+
+
+@pytest.mark.parametrize("p", [1, 2, 4])
+def test_inverse_root_iteration_cap_beyond_convergence(native, p):
+    """Iterations after convergence are skipped (the iterate is copied): a cap of 100 gives the
+    result of 30 to within the convergence threshold's effect (2.5e-6 relative), and both match
+    the oracle."""
+    import torch
+    _say(f"inverse root cap p={p}")
+    d = 257
+    rng = np.random.default_rng(7000 + p)
+    a = _spd(rng, d, 1e4).astype(np.float32)
+    ad = to_dev(a, synth.F32)
+    outs = []
+    for iters in (30, 100):
+        out = torch.empty((d, d), dtype=torch.float32, device="cuda")
+        native.inverse_root_t(ad, out, p=p, eps=1e-9, eps_rel=1e-6, iters=iters)
+        _sync()
+        outs.append(from_dev(out))
+    ref = OS.inverse_root(a.astype(np.float64), p, 1e-9, 1e-6)
+    assert rel_fro(outs[1], outs[0]) <= 5e-6
+    assert rel_fro(outs[1], ref) <= 1e-4
+    np.testing.assert_array_equal(outs[1], outs[1].T)   # stored exactly symmetric
