@@ -10,8 +10,10 @@ iterations, ridge 1e-6 ||S||_F), which the GPU reproduces to two digits:
   resolves only coarsely: emulation 2.4e-4, bar 5e-4.
 * P restricted to the gradient's range (P_L G, G P_R): 1e-4 (emulation <= 1.3e-5).
 * The whole P: 1e-4 for the well-conditioned side (the shorter side of a rectangular gradient);
-  else 1e-2, since there the root is known to about 2.5e-3 in directions the gradient does not
-  reach (where it equals rho^(-1/4)) and that never enter U.
+  else 5e-2. On a rank-deficient side the ridge directions carry rho^(-1/4), the largest
+  eigenvalues of P, and dominate ||P||_F; float32 resolves M's eigenvalue there (z rho ~ 2.5e-6)
+  against rounding noise that grows with sqrt(d), to a few percent (emulated 2.5e-3 at d = 256,
+  measured 1.4e-2 at d = 3072). Those directions never enter U of the same statistics.
 * Statistics 1e-5 (fp32 sums). Parameters: bf16 rounding-aware (half an ulp plus the U bar times
   lr ||U||); fp32 parameters the U bar times lr ||U|| + 1e-6 ||p||.
 """
@@ -148,8 +150,8 @@ def _check(mat, hp, check_p=True):
         PL, PR = from_dev(mat.dPL), from_dev(mat.dPR)
         assert rel_fro(PL @ G, mat.PL @ G) <= U_TOL, ("PL G", rel_fro(PL @ G, mat.PL @ G))
         assert rel_fro(G @ PR, G @ mat.PR) <= U_TOL, ("G PR", rel_fro(G @ PR, G @ mat.PR))
-        tol_l = 1e-4 if mat.m <= 0.75 * mat.n else 1e-2
-        tol_r = 1e-4 if mat.n <= 0.75 * mat.m else 1e-2
+        tol_l = 1e-4 if mat.m <= 0.75 * mat.n else 5e-2
+        tol_r = 1e-4 if mat.n <= 0.75 * mat.m else 5e-2
         assert rel_fro(PL, mat.PL) <= tol_l, ("PL", rel_fro(PL, mat.PL))
         assert rel_fro(PR, mat.PR) <= tol_r, ("PR", rel_fro(PR, mat.PR))
     if check_p:
@@ -279,3 +281,28 @@ def test_inverse_root_iteration_cap_beyond_convergence(native, p):
     assert rel_fro(outs[1], outs[0]) <= 5e-6
     assert rel_fro(outs[1], ref) <= 1e-4
     np.testing.assert_array_equal(outs[1], outs[1].T)   # stored exactly symmetric
+
+
+def test_shampoo_benchmark_configuration_full_size(native):
+    """The configuration bench.py --shampoo times: the GPT-2-small share's 12 matrices in one call,
+    EMA statistics (beta 0.95, weight 0.05), ridge 1e-12 + 1e-6 ||S||_F, 20 root iterations, bf16
+    parameters and gradients; every matrix against the oracle (two steps, so the second sees EMA
+    statistics)."""
+    _say("shampoo benchmark configuration")
+    wl = synth.workload(2)
+    rng = np.random.default_rng(8000)
+    mats = [_Mat(rng, e.m, e.n, synth.BF16, synth.BF16, g_std=0.02).device() for e in wl.muon]
+    hpn, hpo = _hp(native, lr=1e-3, weight_decay=0.01, beta=0.95, weight=0.05)
+    ents = [x.entry(native) for x in mats]
+    ws = native.shampoo_workspace_t(ents, hpn)
+    for step in range(2):
+        if step == 1:
+            for x in mats:
+                x.g = synth.random_muon_tensors(rng, x.m, x.n, x.pdt, x.gdt, g_std=0.02).grad
+                x.dg.copy_(to_dev(x.g, x.gdt))
+        native.shampoo_step_t(ents, hpn, ws)
+        _sync()
+        for x in mats:
+            _oracle_step(x, hpo)
+    for x in mats:
+        _check(x, hpo)
