@@ -267,12 +267,16 @@ int check_entries(const mfsdp_muon_entry* entries, int64_t count, bool need_grad
   if (count < 0) return fail(MFSDP_E_INVALID, "count must be >= 0");
   if (count > 0 && !entries) return fail(MFSDP_E_INVALID, "entries is NULL");
   if (count > (1 << 20)) return fail(MFSDP_E_INVALID, "too many entries");
+  int64_t units = 0;  // bound on the 64 x 64 tiles of any one grouped launch (grid and int32 counters)
   for (int64_t i = 0; i < count; ++i) {
     const mfsdp_muon_entry& e = entries[i];
     if (!e.param || (need_grad && !e.grad) || !e.momentum)
       return fail(MFSDP_E_INVALID, "entry %lld: NULL pointer", (long long)i);
     int st = check_shape(e.m, e.n, "entry", i);
     if (st) return st;
+    units += (round_up(e.m, kTileBF16) / 64) * (round_up(e.n, kTileBF16) / 64);
+    if (units > (int64_t(1) << 30))
+      return fail(MFSDP_E_INVALID, "the entries of one call exceed 2^30 tiles per launch");
     if (!valid_dtype(e.param_dtype) || !valid_dtype(e.grad_dtype))
       return fail(MFSDP_E_INVALID, "entry %lld: unsupported dtype", (long long)i);
     if (!aligned16(e.param) || (need_grad && !aligned16(e.grad)) || !aligned16(e.momentum) ||

@@ -332,10 +332,14 @@ int check_shampoo_entries(const mfsdp_shampoo_entry* en, int64_t count, bool dat
   if (count < 0) return bad("count must be >= 0");
   if (count > 0 && !en) return bad("entries is NULL");
   if (count > 4096) return bad("at most 4096 entries per call");
+  int64_t units = 0;  // bound on the 64 x 64 tiles of any one grouped launch (grid and int32 counters)
   for (int64_t i = 0; i < count; ++i) {
     const mfsdp_shampoo_entry& e = en[i];
     const std::string w = "entry " + std::to_string(i) + ": ";
     if (e.m < 1 || e.n < 1 || e.m > kMaxDim || e.n > kMaxDim) return bad(w + "m and n must be in [1, 65536]");
+    const int64_t s = rup(e.m, kShTile) + rup(e.n, kShTile);
+    units += 3 * (s / kShCopyTile) * (s / kShCopyTile);
+    if (units > (int64_t(1) << 30)) return bad("the entries of one call exceed 2^30 tiles per launch");
     if (!dtype_ok(e.param_dtype) || !dtype_ok(e.grad_dtype)) return bad(w + "dtype must be F32 or BF16");
     if (!data) continue;
     if (!e.param || !e.grad || !e.L || !e.R || !e.PL || !e.PR) return bad(w + "NULL pointer");

@@ -293,3 +293,16 @@ def test_inverse_root_size_query_equals_what_the_call_needs(p, iters):
     q = native.mfsdp_inverse_root_workspace_size(257, p, iters)
     assert _needed_bytes(lambda: native.mfsdp_inverse_root(FAKE, FAKE * 2, 257, p, 1e-9, 1e-6, iters,
                                                            FAKE * 16, 0, 0)) == q
+
+
+def test_shampoo_rejects_calls_beyond_the_launch_size_limit():
+    big = [_sh_entry(m=65536, n=65536) for _ in range(300)]
+    with pytest.raises(native.MfsdpError, match="2\\^30 tiles"):
+        native.mfsdp_shampoo_step(big, native.shampoo_hparams(), FAKE * 16, 1 << 62, 0)
+    assert native.mfsdp_shampoo_workspace_size(big, native.shampoo_hparams()) == 0
+
+
+def test_muon_rejects_calls_beyond_the_launch_size_limit():
+    big = [_entry(m=65536, n=65536) for _ in range(1100)]
+    with pytest.raises(native.MfsdpError, match="2\\^30 tiles"):
+        native.mfsdp_muon_step(big, native.muon_hparams(), FAKE * 16, 1 << 62, 0)
