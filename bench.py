@@ -14,6 +14,8 @@ Prints ONE JSON line. `value` is nominal NS TFLOP/s over the whole step (NS flop
 sample of the same share on the host cores. `planner` reports the owner planner (Algorithm 1) on the
 paper's decoder sweep (planner time, rank-load imbalance, gamma_B per policy); with --plan-span W it
 also runs every rank's planned share on the GPU and reports the step-time imbalance over ranks.
+`shampoo` times the Shampoo owner step (fp32 MFMA) on the GPT-2-small share, with and without
+preconditioner refresh.
 """
 from __future__ import annotations
 
@@ -340,8 +342,9 @@ def main() -> int:
     ap.add_argument("--plan-span", type=int, default=0, choices=[0] + sorted(PLAN_SWEEP),
                     help="also run every rank's owner share of the planned decoder sweep model at this "
                          "shard span on the GPU and report the step-time imbalance over ranks")
-    ap.add_argument("--shampoo", action="store_true",
-                    help="also time the Shampoo owner step (fp32 MFMA) on the GPT-2-small share")
+    ap.add_argument("--no-shampoo", action="store_true",
+                    help="skip timing the Shampoo owner step (fp32 MFMA) on the GPT-2-small share")
+    ap.add_argument("--shampoo", action="store_true", help=argparse.SUPPRESS)  # (the default)
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -515,7 +518,9 @@ def main() -> int:
                                                   if args.plan_span else ""))
     pctx = (torch, dev, hev, stream, h, ah, 5, 2) if args.plan_span else None
     out["planner"] = planner_report(native, sorted(PLAN_SWEEP), args.plan_span, pctx)
-    if args.shampoo:
+    if not args.no_shampoo:
+        # nominal_flop counts every product of all root iterations in full; iterations skipped
+        # after convergence and the upper-tile-only symmetric products execute less
         out["shampoo"] = time_shampoo(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
