@@ -1,0 +1,26 @@
+"""The torch.optim front ends refuse anything but CUDA tensors (there is no CPU path) and unknown
+hyperparameters, before touching the library."""
+import pytest
+import torch
+
+from paper_2607_05895_amd.optim import OwnerMuon, OwnerShampoo
+
+
+@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo])
+def test_cpu_tensors_are_refused(cls):
+    p = torch.zeros(8, 8, requires_grad=True)
+    p.grad = torch.ones(8, 8)
+    opt = cls([p])
+    with pytest.raises(ValueError, match="GPU only"):
+        opt.step()
+
+
+@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo])
+def test_unknown_hyperparameters_are_refused(cls):
+    with pytest.raises(TypeError, match="unknown"):
+        cls([torch.zeros(2, 2, requires_grad=True)], betas=(0.9, 0.99))
+
+
+def test_shampoo_frequency_must_be_positive():
+    with pytest.raises(ValueError):
+        OwnerShampoo([torch.zeros(2, 2, requires_grad=True)], precondition_frequency=0)

@@ -1,0 +1,124 @@
+"""The torch.optim front ends (paper_2607_05895_amd.optim) against the fp64 oracle: two steps of a
+small owner share (2D weights on Muon or Shampoo, vectors on AdamW) with state carried by the
+optimizer, and a state_dict round trip. Tolerances as in the kernel parity tests."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from oracle import shampoo as OS
+from tests.helpers import check_bf16_param, from_dev, rel_fro, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _model(rng):
+    """(name, param bits/array, dtype) of a tiny decoder block: 3 matrices and 3 vectors."""
+    out = []
+    for name, shape in (("q", (256, 256)), ("up", (512, 256)), ("down", (256, 512))):
+        t = synth.random_muon_tensors(rng, *shape, synth.BF16, synth.BF16, g_std=1e-3)
+        out.append((name, t.param, [t.grad, synth.random_muon_tensors(rng, *shape).grad], synth.BF16))
+    for name, n in (("ln.w", 256), ("ln.b", 256), ("bias", 512)):
+        p = rng.standard_normal(n).astype(np.float32)
+        out.append((name, p, [(rng.standard_normal(n) * 1e-2).astype(np.float32) for _ in range(2)],
+                    synth.F32))
+    return out
+
+
+def _torch_params(model):
+    import torch
+    ps, grads = [], []
+    for name, p, gs, dt in model:
+        t = to_dev(p, dt).clone()
+        t.requires_grad_(True)
+        ps.append(t)
+        grads.append([to_dev(g, dt) for g in gs])
+    return ps, grads
+
+
+def test_owner_muon_two_steps_match_oracle():
+    from paper_2607_05895_amd.optim import OwnerMuon
+    rng = np.random.default_rng(11)
+    model = _model(rng)
+    ps, grads = _torch_params(model)
+    opt = OwnerMuon(ps, lr=0.02, weight_decay=0.01, momentum=0.95, adamw_lr=1e-3, adamw_weight_decay=0.01)
+    for step in range(2):
+        for p, g in zip(ps, grads):
+            p.grad = g[step]
+        opt.step()
+    import torch
+    torch.cuda.synchronize()
+    for (name, p0, gs, dt), p in zip(model, ps):
+        if p.dim() == 2:
+            buf = np.zeros(p0.shape)
+            pin = p0
+            for step in range(2):
+                pout, buf, O = oracle.muon_step(pin, gs[step], buf, lr=0.02, weight_decay=0.01, momentum=0.95,
+                                                nesterov=True, a=3.4445, b=-4.7750, c=2.0315, ns_steps=5)
+                pin = synth.f32_to_bf16_bits(pout.astype(np.float32))
+            assert rel_fro(from_dev(opt.state[p]["momentum_buffer"]), buf) <= 1e-6, name
+            f = max(1.0, p0.shape[0] / p0.shape[1]) ** 0.5
+            assert check_bf16_param(from_dev(p.detach()), pout, 0.02 * f * np.linalg.norm(O), 2e-2) <= 1.0, name
+        else:
+            pin, m, v = p0.astype(np.float64), np.zeros(p0.shape), np.zeros(p0.shape)
+            for step in range(2):
+                pin, m, v = oracle.adamw_step(pin.astype(np.float32), gs[step], m, v, lr=1e-3, beta1=0.9,
+                                              beta2=0.999, eps=1e-8, weight_decay=0.01, step=step + 1)
+            assert opt.state[p]["step"] == 2
+            assert rel_fro(from_dev(opt.state[p]["exp_avg"]), m) <= 1e-6, name
+            assert rel_fro(from_dev(opt.state[p]["exp_avg_sq"]), v) <= 1e-6, name
+            assert np.abs(from_dev(p.detach()) - pin).max() <= 1e-6 * np.abs(pin).max() + 1e-7, name
+
+
+def test_owner_shampoo_refresh_then_stale_matches_oracle():
+    from paper_2607_05895_amd.optim import OwnerShampoo
+    import torch
+    rng = np.random.default_rng(12)
+    # the same gradient at both steps: it stays in the range of the step-0 statistics, where the
+    # stale preconditioners are accurate; recomputing them at step 1 (from twice the statistic)
+    # would scale U by 2^(-1/2), so the refresh schedule is checked
+    model = [(n, p, [gs[0], gs[0]], dt) for n, p, gs, dt in _model(rng) if dt == synth.BF16]
+    ps, grads = _torch_params(model)
+    opt = OwnerShampoo(ps, lr=0.05, weight_decay=0.01, beta=1.0, weight=1.0, precondition_frequency=2)
+    for step in range(2):
+        for p, g in zip(ps, grads):
+            p.grad = g[step]
+        opt.step()
+    torch.cuda.synchronize()
+    for (name, p0, gs, dt), p in zip(model, ps):
+        m, n = p0.shape
+        L, R, PL, PR, pin = np.zeros((m, m)), np.zeros((n, n)), None, None, p0
+        for step in range(2):
+            hp = OS.ShampooHParams(lr=0.05, weight_decay=0.01, beta=1.0, weight=1.0, eps=1e-12, eps_rel=1e-6,
+                                   refresh=step == 0)
+            pout, L, R, PL, PR, U = OS.shampoo_step(pin, gs[step], L, R, PL, PR, hp)
+            pin = synth.f32_to_bf16_bits(pout.astype(np.float32))
+        st = opt.state[p]
+        assert rel_fro(from_dev(st["L"]), L) <= 1e-5 and rel_fro(from_dev(st["R"]), R) <= 1e-5, name
+        tol = 1e-4 if min(m, n) <= 0.75 * max(m, n) else 5e-4
+        assert check_bf16_param(from_dev(p.detach()), pout, 0.05 * np.linalg.norm(U), tol) <= 1.0, name
+
+
+def test_state_dict_round_trip_continues_identically():
+    from paper_2607_05895_amd.optim import OwnerMuon
+    import torch
+    rng = np.random.default_rng(13)
+    model = _model(rng)
+    runs = []
+    for resume in (False, True):
+        ps, grads = _torch_params(model)
+        opt = OwnerMuon(ps, lr=0.02)
+        for p, g in zip(ps, grads):
+            p.grad = g[0]
+        opt.step()
+        if resume:
+            sd = opt.state_dict()
+            opt = OwnerMuon(ps, lr=0.02)
+            opt.load_state_dict(sd)
+        for p, g in zip(ps, grads):
+            p.grad = g[1]
+        opt.step()
+        torch.cuda.synchronize()
+        runs.append([p.detach().clone() for p in ps])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
