@@ -631,80 +631,114 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
 #undef MFSDP_WAIT_VMCNT
 #undef MFSDP_WAIT_LGKM0
 
-// ---------------------------------------------------------------------------------------------
-// fp32 kernel: 64 x 64 tile, 256 threads of 4 x 4 outputs, K step 16 through LDS.
+// fp32 NS products on fp32 MFMA. One 64 x 64 output tile per 256-thread workgroup: 4 waves of
+// 32 x 32 (v_mfma_f32_32x32x2f32), K steps of 32 double-buffered in LDS with the next step's 16-byte
+// global loads held in registers. The K index inside a step is permuted identically on both
+// operands (lane half h of MFMA q in group g takes k = 8 g + 4 h + q), so each lane reads its
+// fragments as 16-byte vectors; rows' eight 16-byte chunks are XOR-permuted by
+// (r & 7) ^ ((r >> 3) & 1) in LDS (conflict-free for 32 and 64 banks). The epilogue follows the
+// problem description: C = alpha P Q^T + beta E (+ the square's diagonal term), upper tiles of
+// symmetric products with mirrored stores, the transposed output CT; transposed stores go through
+// an LDS tile so that they are row-contiguous.
+__device__ __forceinline__ int f32_slot(int r, int chunk) {
+  return r * 8 + (chunk ^ ((r & 7) ^ ((r >> 3) & 1)));
+}
+
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restrict__ descs, int count,
                                                        int parity, int first, int last, float ca,
                                                        float cb, float cc) {
-  __shared__ float Ps[16][68];
-  __shared__ float Qs[16][68];
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  typedef float f32x16 __attribute__((ext_vector_type(16)));
+  typedef __attribute__((address_space(1))) float gf32;
+  typedef __attribute__((address_space(1))) const f32x4 gcf4;
+  __shared__ f32x4 lds[2][2][64 * 8];  // [stage][P, Q][slot]: 32 KiB
+  __shared__ float tt[64][65];          // transposition tile
   const int e = find_entry(descs, count, blockIdx.x);
   const GemmDesc& dd = descs[e];
   const int lt = blockIdx.x - dd.tile_begin;
   int bi, bj;
   tile_coords(dd, lt, bi, bj);
-  const float* __restrict__ P = static_cast<const float*>(dd.P[parity]);
-  const float* __restrict__ Q = static_cast<const float*>(dd.Q[parity]);
-  const int t = threadIdx.x;
-  const int tx = t & 15, ty = t >> 4;
-  const int lr = t >> 2, lk = (t & 3) * 4;
-  const int64_t prow = int64_t(bi) * 64 + lr, qrow = int64_t(bj) * 64 + lr;
-  float acc[4][4] = {};
-  for (int k0 = 0; k0 < dd.K; k0 += 16) {
-    const float4 pv = *reinterpret_cast<const float4*>(P + blk_index(prow, k0 + lk, dd.ldp));
-    const float4 qv = *reinterpret_cast<const float4*>(Q + blk_index(qrow, k0 + lk, dd.ldq));
-    Ps[lk + 0][lr] = pv.x; Ps[lk + 1][lr] = pv.y; Ps[lk + 2][lr] = pv.z; Ps[lk + 3][lr] = pv.w;
-    Qs[lk + 0][lr] = qv.x; Qs[lk + 1][lr] = qv.y; Qs[lk + 2][lr] = qv.z; Qs[lk + 3][lr] = qv.w;
-    __syncthreads();
+  const gf32* P = (const gf32*)dd.P[parity];
+  const gf32* Q = (const gf32*)dd.Q[parity];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wr = w >> 1, wc = w & 1;
+  const int fr = lane & 31, fh = lane >> 5;
+  // global loads of one K step: the 64 x 32 slice of a panel-blocked operand is four 16 x 32 blocks
+  // (2 KiB each); float4 f = t + 256 j covers block f >> 7, row (f >> 3) & 15, chunk f & 7
+  const int64_t prow0 = int64_t(bi) * 64, qrow0 = int64_t(bj) * 64;
+  f32x4 ra[2], rb[2];
+  auto gload = [&](int k0) {
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const float4 a = *reinterpret_cast<const float4*>(&Ps[k][ty * 4]);
-      const float4 b = *reinterpret_cast<const float4*>(&Qs[k][tx * 4]);
-      const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(av[r], bv[c], acc[r][c]);
+    for (int j = 0; j < 2; ++j) {
+      const int f = t + 256 * j;
+      const int r = (f >> 7) * 16 + ((f >> 3) & 15), c = f & 7;
+      ra[j] = *(gcf4*)(P + blk_index(prow0 + r, k0 + 4 * c, dd.ldp));
+      rb[j] = *(gcf4*)(Q + blk_index(qrow0 + r, k0 + 4 * c, dd.ldq));
     }
+  };
+  auto lstore = [&](int s) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int f = t + 256 * j;
+      const int slot = f32_slot((f >> 7) * 16 + ((f >> 3) & 15), f & 7);
+      lds[s][0][slot] = ra[j];
+      lds[s][1][slot] = rb[j];
+    }
+  };
+  f32x16 acc = f32x16{};
+  const int nk = dd.K / 32;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int s = kt & 1;
+    if (kt + 1 < nk) gload((kt + 1) * 32);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 a = lds[s][0][f32_slot(wr * 32 + fr, 2 * g + fh)];
+      const f32x4 b = lds[s][1][f32_slot(wc * 32 + fr, 2 * g + fh)];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[q], b[q], acc, 0, 0, 0);
+    }
+    if (kt + 1 < nk) lstore(s ^ 1);
     __syncthreads();
   }
   // the square product (the only one with an addend) takes this step's coefficients
   const bool square = dd.E[parity] != nullptr;
   const float alpha = square ? cc : dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
   const float beta = square ? cb : dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
-  const float diag = square ? ca : 0.0f;
-  const float* E = static_cast<const float*>(dd.E[parity]);
-  float* C = static_cast<float*>(dd.C[parity]);
-  float* CT = static_cast<float*>(dd.CT[parity]);
+  const float diag = (square && dd.sym && bi == bj) ? ca : 0.0f;
+  const gf32* E = (const gf32*)dd.E[parity];
+  gf32* C = (gf32*)dd.C[parity];
+  gf32* CT = (gf32*)dd.CT[parity];
   if (last) {
     if (!dd.last_c) C = nullptr;
     if (!dd.last_ct) CT = nullptr;
   }
   const bool mirror = dd.sym && bi != bj && C;
+  // accumulator element v is tile row wr*32 + 8 (v / 4) + 4 h + v % 4, column wc*32 + lane % 32
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t i = int64_t(bi) * 64 + ty * 4 + r;
-    const int64_t j = int64_t(bj) * 64 + tx * 4;
-    float v[4];
-#pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = alpha * acc[r][c];
-    if (E) {
-      const float4 ev = *reinterpret_cast<const float4*>(E + blk_index(i, j, dd.lde));
-      v[0] += beta * ev.x; v[1] += beta * ev.y; v[2] += beta * ev.z; v[3] += beta * ev.w;
+  for (int v = 0; v < 16; ++v) {
+    const int i = wr * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+    const int j = wc * 32 + fr;
+    const int64_t gi = prow0 + i, gj = qrow0 + j;
+    float x = alpha * acc[v];
+    if (E) x += beta * E[blk_index(gi, gj, dd.lde)];
+    if (gi == gj) x += diag;
+    if (C) C[blk_index(gi, gj, dd.ldc)] = x;
+    tt[i][j] = x;
+  }
+  if (mirror || CT) {
+    __syncthreads();
+    // transposed tile: row qrow0 + j, columns prow0 + i (i across lanes)
+    const int i = t & 63;
+#pragma unroll 4
+    for (int it = 0; it < 16; ++it) {
+      const int j = (t >> 6) + 4 * it;
+      const float x = tt[i][j];
+      if (mirror) C[blk_index(qrow0 + j, prow0 + i, dd.ldc)] = x;
+      if (CT) CT[blk_index(qrow0 + j, prow0 + i, dd.ldct)] = x;
     }
-    if (dd.sym && bi == bj)
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (i == j + c) v[c] += diag;
-    if (C) {
-      *reinterpret_cast<float4*>(C + blk_index(i, j, dd.ldc)) = make_float4(v[0], v[1], v[2], v[3]);
-      if (mirror)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) C[blk_index(j + c, i, dd.ldc)] = v[c];
-    }
-    if (CT)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) CT[blk_index(j + c, i, dd.ldct)] = v[c];
   }
 }
 
