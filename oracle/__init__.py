@@ -18,10 +18,11 @@ What it computes follows the paper (MatrixFSDP, arxiv 2607.05895):
 Where the paper is silent, the readings used are the ones stated in each function's docstring.
 
 * Section 5.7 (Generality beyond Muon): the owner runs Shampoo (full left/right preconditioners,
-  inverse fourth root) on the same whole matrices (``shampoo.py``).
+  inverse fourth root, ``shampoo.py``) and SOAP (Adam in the eigenbasis of Shampoo's statistics,
+  ``soap.py``) on the same whole matrices.
 
 Parity status: every function here is pinned by tests in ``tests/test_oracle_pins.py``,
-``tests/test_planner_pins.py`` and ``tests/test_shampoo_pins.py``.
+``tests/test_planner_pins.py``, ``tests/test_shampoo_pins.py`` and ``tests/test_soap_pins.py``.
 """
 from .muon import (  # noqa: F401
     bf16_widen,
@@ -39,3 +40,4 @@ from .muon import (  # noqa: F401
 from .adamw import adamw_step  # noqa: F401
 from . import planner  # noqa: F401
 from . import shampoo  # noqa: F401
+from . import soap  # noqa: F401

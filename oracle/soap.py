@@ -1,0 +1,103 @@
+"""fp64 reference of the owner's SOAP update (test infrastructure only; see package docstring).
+
+Paper passage followed: Section 5.7 ("Generality beyond Muon"): the owner, holding each 2D matrix
+whole, runs a single-device matrix optimizer on it unchanged; besides Shampoo the paper runs SOAP,
+which it describes as Adam run in the eigenbasis of Shampoo's preconditioner statistics. The paper
+does not restate SOAP, so the published algorithm is followed: Vyas, Morwani, Zhao, Shapira,
+Brandfonbrener, Janson and Kakade, "SOAP: Improving and Stabilizing Shampoo using Adam" (2024), the
+matrix case, whose eigenbasis is refreshed by one step of power iteration followed by a QR
+decomposition. Per step, with the bases Q_L (m x m) and Q_R (n x n) of the previous refresh:
+
+    G' = Q_L^T G Q_R                        gradient in the eigenbasis
+    M  <- beta1 M + (1 - beta1) G           first moment, kept in the original coordinates
+    M' = Q_L^T M Q_R
+    V  <- beta2 V + (1 - beta2) G' * G'     second moment, kept in the eigenbasis coordinates
+    N' = Adam direction from M', V          (bias-corrected, below)
+    N  = Q_L N' Q_R^T                       back to the original coordinates
+    p  <- p (1 - lr wd) - lr N
+    L  <- beta_s L + w_s G G^T,  R <- beta_s R + w_s G^T G          (Shampoo statistics)
+    refresh: Q_L <- orthonormal factor of QR(L Q_L), Q_R <- of QR(R Q_R)
+
+Readings (the paper fixes none of them):
+* bias correction as PyTorch AdamW: N' = (M'/(1 - beta1^t)) / (sqrt(V)/sqrt(1 - beta2^t) + eps), so
+  that with Q_L = Q_R = I one SOAP step is exactly one AdamW step.
+* decoupled weight decay on the old parameter (as AdamW and the Muon/Shampoo steps here).
+* the statistics use the Shampoo update of ``shampoo.update_statistics`` (beta_s L + w_s G G^T;
+  the published SOAP uses the EMA w_s = 1 - beta_s) and start at zero; the bases start at the
+  identity, so the first steps are AdamW and the first refresh begins the power iteration (the
+  published code starts from a full eigendecomposition instead; ``refresh_iters`` > 1 repeats the
+  power step + QR, i.e. runs orthogonal iteration towards the eigenvectors).
+* V is left unchanged when the basis is refreshed, as in the published algorithm.
+* the QR factor is the Householder one with LAPACK's sign convention (numpy.linalg.qr). Column
+  signs of a basis do not change N (each column enters N twice).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Tuple
+
+import numpy as np
+
+from .muon import _f64
+from .shampoo import update_statistics
+
+
+@dataclasses.dataclass
+class SoapHParams:
+    lr: float = 3e-3
+    weight_decay: float = 0.0
+    beta1: float = 0.95
+    beta2: float = 0.95
+    eps: float = 1e-8
+    shampoo_beta: float = 0.95
+    shampoo_weight: float = 0.05
+    refresh: bool = False
+    refresh_iters: int = 1
+
+
+def orthonormal_factor(A: np.ndarray) -> np.ndarray:
+    """Q of the Householder QR decomposition A = Q R (square A; numpy.linalg.qr, LAPACK signs)."""
+    Q, _ = np.linalg.qr(np.asarray(A, dtype=np.float64))
+    return Q
+
+
+def refresh_basis(S: np.ndarray, Q: np.ndarray, iters: int = 1) -> np.ndarray:
+    """`iters` steps of power iteration with QR on the statistic S, from the basis Q."""
+    S = np.asarray(S, dtype=np.float64)
+    Q = np.asarray(Q, dtype=np.float64)
+    for _ in range(int(iters)):
+        Q = orthonormal_factor(S @ Q)
+    return Q
+
+
+def adam_direction(Mp: np.ndarray, V: np.ndarray, beta1: float, beta2: float, eps: float,
+                   step: int) -> np.ndarray:
+    """Bias-corrected Adam direction (M/(1 - beta1^t)) / (sqrt(V)/sqrt(1 - beta2^t) + eps)."""
+    if step < 1:
+        raise ValueError("step is counted from 1")
+    bc1 = 1.0 - beta1 ** step
+    bc2 = 1.0 - beta2 ** step
+    return (Mp / bc1) / (np.sqrt(V) / math.sqrt(bc2) + eps)
+
+
+def soap_step(param: np.ndarray, grad: np.ndarray, exp_avg: np.ndarray, exp_avg_sq: np.ndarray,
+              L: np.ndarray, R: np.ndarray, QL: np.ndarray, QR: np.ndarray, step: int,
+              hp: SoapHParams):
+    """One owner-local SOAP step on one whole m x n matrix at step number ``step`` (t >= 1).
+    Returns (param', M', V', L', R', Q_L', Q_R', N) in float64."""
+    G = _f64(grad)
+    QL = np.asarray(QL, dtype=np.float64)
+    QR = np.asarray(QR, dtype=np.float64)
+    Gp = QL.T @ G @ QR
+    M = hp.beta1 * _f64(exp_avg) + (1.0 - hp.beta1) * G
+    Mp = QL.T @ M @ QR
+    V = hp.beta2 * _f64(exp_avg_sq) + (1.0 - hp.beta2) * Gp * Gp
+    Np = adam_direction(Mp, V, hp.beta1, hp.beta2, hp.eps, step)
+    N = QL @ Np @ QR.T
+    p_new = _f64(param) * (1.0 - hp.lr * hp.weight_decay) - hp.lr * N
+    L2, R2 = update_statistics(L, R, G, hp.shampoo_beta, hp.shampoo_weight)
+    if hp.refresh:
+        QL = refresh_basis(L2, QL, hp.refresh_iters)
+        QR = refresh_basis(R2, QR, hp.refresh_iters)
+    return p_new, M, V, L2, R2, QL, QR, N
