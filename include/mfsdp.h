@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MFSDP_ABI_VERSION 4
+#define MFSDP_ABI_VERSION 5
 
 typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
 
@@ -269,6 +269,88 @@ size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters);
 int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double eps,
                        double eps_rel, int32_t iters, void* workspace, size_t workspace_bytes,
                        void* stream);
+
+/* ---- SOAP owner step (Section 5.7: Adam in the eigenbasis of Shampoo's statistics) ---------- */
+
+/* One whole matrix the rank owns, for SOAP (Vyas et al. 2024, the matrix case).
+ *   param       m x n, param_dtype (F32 or BF16), updated in place (fp32 math, bf16 rounded to
+ *               nearest even)
+ *   grad        m x n, grad_dtype (F32 or BF16), read only
+ *   exp_avg     m x n fp32 first moment M in the original coordinates, updated in place
+ *   exp_avg_sq  m x n fp32 second moment V in the eigenbasis coordinates, updated in place
+ *   L, R        m x m and n x n fp32 Shampoo statistics (row-major), updated in place
+ *   QL, QR      m x m and n x n fp32 orthogonal bases (row-major; columns are the basis vectors):
+ *               read; overwritten by the refreshed bases when hp->refresh is 1. Start them at the
+ *               identity (then the first steps are AdamW steps).
+ *   m, n        1 .. 4096 (each side's basis is refreshed by a QR whose panels are held in
+ *               registers, at most 4096 rows)
+ *   update_out  optional m x n fp32: receives the direction N. NULL = off.
+ * All buffers are distinct device allocations (no aliasing), naturally aligned. */
+typedef struct {
+  void* param;
+  const void* grad;
+  float* exp_avg;
+  float* exp_avg_sq;
+  float* L;
+  float* R;
+  float* QL;
+  float* QR;
+  int64_t m;
+  int64_t n;
+  int32_t param_dtype;
+  int32_t grad_dtype;
+  float* update_out;
+} mfsdp_soap_entry;
+
+/* SOAP hyperparameters, shared by every entry of one call (doubles; fp32 math on the GPU). Per
+ * step, with the bases of the previous refresh:
+ *   G' = QL^T G QR;  M <- beta1 M + (1 - beta1) G;  M' = QL^T M QR;  V <- beta2 V + (1 - beta2) G'^2
+ *   N' = (M' / (1 - beta1^t)) / (sqrt(V) / sqrt(1 - beta2^t) + eps);  N = QL N' QR^T
+ *   p <- p (1 - lr wd) - lr N      (decoupled decay, both terms on the old p)
+ *   L <- shampoo_beta L + shampoo_weight G G^T;  R <- shampoo_beta R + shampoo_weight G^T G
+ *   refresh 1: refresh_iters times QL <- Q factor of the Householder QR of L QL (and R, QR alike),
+ *   with LAPACK's sign convention; refresh 0: the bases are read only.
+ *   lr, weight_decay, shampoo_beta, shampoo_weight >= 0; beta1, beta2 in [0, 1); eps > 0;
+ *   step t >= 1 (the bias-correction count); refresh 0/1; refresh_iters 1 .. 100. */
+typedef struct {
+  double lr;
+  double weight_decay;
+  double beta1;
+  double beta2;
+  double eps;
+  double shampoo_beta;
+  double shampoo_weight;
+  int32_t step;
+  int32_t refresh;
+  int32_t refresh_iters;
+} mfsdp_soap_hparams;
+
+/* Bytes of device workspace mfsdp_soap_step needs for these entries and hyperparameters: per
+ * matrix, zero-padded fp32 buffers of 8 mp np + 3 (mp^2 + np^2) floats (mp, np = m, n rounded up
+ * to 128) and 16 (m + n) + 512 floats for the QR panels; plus launch descriptors. Data pointers are
+ * not used. 0 on invalid arguments; count == 0 returns 0 with no error. */
+size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
+                                 const mfsdp_soap_hparams* hp);
+
+/* One SOAP step on every entry (host array of count entries), enqueued on `stream` (hipStream_t,
+ * NULL = default stream); no host synchronisation. Every product runs on fp32 MFMA (grouped over
+ * the entries); the refresh QR is a blocked Householder factorization (panels of 16 columns).
+ * The workspace (device, 256-byte aligned, >= the size query) must not be in use by another call
+ * still running. Returns MFSDP_OK, MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an
+ * argument error nothing is enqueued. At most 4096 entries per call. */
+int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes for mfsdp_orthonormal_factor (0 on invalid arguments). */
+size_t mfsdp_orthonormal_factor_workspace_size(int64_t d);
+
+/* q = Q of the Householder QR decomposition a = Q R of a d x d fp32 matrix (row-major, device,
+ * read only), with LAPACK's sign convention (the diagonal of R is -sign(pivot) times the column
+ * norm; a column with nothing below its pivot gets the identity reflector): the factorization that
+ * SOAP's basis refresh uses. 1 <= d <= 4096. `q` (d x d fp32, device) must not overlap `a`. Same
+ * stream, workspace and error rules as mfsdp_soap_step. */
+int mfsdp_orthonormal_factor(const float* a, float* q, int64_t d, void* workspace,
+                             size_t workspace_bytes, void* stream);
 
 /* ---- Owner planning (host only; no GPU, no stream) ---------------------------------------- */
 

@@ -13,8 +13,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmfsdp.so")
-SOURCES = ["mfsdp_host.cpp", "planner.cpp", "shampoo_host.cpp", "kernels_elementwise.hip",
-           "kernels_gemm.hip", "kernels_shampoo.hip"]
+SOURCES = ["mfsdp_host.cpp", "planner.cpp", "shampoo_host.cpp", "soap_host.cpp", "kernels_elementwise.hip",
+           "kernels_gemm.hip", "kernels_shampoo.hip", "kernels_soap.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

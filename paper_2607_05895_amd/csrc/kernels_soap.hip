@@ -1,0 +1,386 @@
+// HIP kernels specific to the SOAP owner step (fp32): the first-moment pass that also lays out the
+// gradient for the products, Adam in the eigenbasis, and the blocked Householder QR that refreshes
+// a basis. The products themselves run on the Shampoo GEMM.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <utility>
+
+#include "mfsdp_internal.h"
+#include "soap_internal.h"
+
+namespace mfsdp {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) float g_f32;
+typedef __attribute__((address_space(1))) const float g_cf32;
+typedef __attribute__((address_space(1))) f32x4 g_f32x4;
+typedef __attribute__((address_space(1))) const f32x4 g_cf32x4;
+
+constexpr int kTile = kShCopyTile;  // 64 x 64 tiles of the elementwise passes
+
+template <typename D>
+__device__ __forceinline__ int find_desc(const D* d, int count, int b) {
+  int lo = 0, hi = count - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (d[mid].tile_begin <= b) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Compile-time loop: f(integral_constant<int, 0>) ... f(integral_constant<int, N - 1>), so that
+// register arrays indexed by the loop variable stay in registers.
+template <typename F, int... I>
+__device__ __forceinline__ void unrolled_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void unrolled(F&& f) {
+  unrolled_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+__global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __restrict__ descs, int count,
+                                                        float beta1) {
+  __shared__ float tg[kTile][kTile + 1];
+  __shared__ float tm[kTile][kTile + 1];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const SoapPrepDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const int64_t gc = int64_t(tj) * kTile + c;
+  g_f32* Gp = (g_f32*)(d.Gp);
+  g_f32* GMt = (g_f32*)(d.GMt);
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;
+    const int64_t gr = int64_t(ti) * kTile + r;
+    float g = 0.0f, mo = 0.0f;
+    if (gr < d.m && gc < d.n) {
+      const int64_t o = gr * d.n + gc;
+      g = d.grad_dtype == kDtBF16
+              ? __uint_as_float(uint32_t(static_cast<const uint16_t*>(d.grad)[o]) << 16)
+              : static_cast<const float*>(d.grad)[o];
+      mo = beta1 * d.exp_avg[o] + (1.0f - beta1) * g;
+      d.exp_avg[o] = mo;
+    }
+    Gp[gr * d.np + gc] = g;
+    tg[r][c] = g;
+    tm[r][c] = mo;
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;  // row of the transposed tile = column of the source tile
+    const int64_t o = (int64_t(tj) * kTile + r) * d.mp + int64_t(ti) * kTile + c;
+    GMt[o] = tg[c][r];
+    GMt[o + d.np * d.mp] = tm[c][r];
+  }
+}
+
+__global__ __launch_bounds__(256) void soap_adam_kernel(const SoapAdamDesc* __restrict__ descs, int count,
+                                                        float beta2, float eps, float inv_bc1,
+                                                        float inv_sqrt_bc2) {
+  __shared__ float tn[kTile][kTile + 1];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const SoapAdamDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const int64_t gc = int64_t(tj) * kTile + c;
+  const g_cf32* GMr = (const g_cf32*)(d.GMr);
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;
+    const int64_t gr = int64_t(ti) * kTile + r;
+    float np_ = 0.0f;
+    if (gr < d.m && gc < d.n) {
+      const float gq = GMr[gr * 2 * d.np + gc];
+      const float mq = GMr[gr * 2 * d.np + d.np + gc];
+      const int64_t o = gr * d.n + gc;
+      const float v = beta2 * d.exp_avg_sq[o] + (1.0f - beta2) * (gq * gq);
+      d.exp_avg_sq[o] = v;
+      np_ = (mq * inv_bc1) / (sqrtf(v) * inv_sqrt_bc2 + eps);
+    }
+    tn[r][c] = np_;
+  }
+  __syncthreads();
+  g_f32* NpT = (g_f32*)(d.NpT);
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;
+    NpT[(int64_t(tj) * kTile + r) * d.mp + int64_t(ti) * kTile + c] = tn[c][r];
+  }
+}
+
+__global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __restrict__ descs, int count) {
+  const int e = find_desc(descs, count, blockIdx.x);
+  const SoapEyeDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const int64_t gc = int64_t(tj) * kTile + c;
+  if (gc >= d.d) return;
+  g_f32* X = (g_f32*)(d.X);
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int64_t gr = int64_t(ti) * kTile + rr + 4 * i;
+    if (gr < d.d) X[gr * d.ld + gc] = gr == gc ? 1.0f : 0.0f;
+  }
+}
+
+// Householder factorization of one 16-column panel (LAPACK's convention: for the column x below and
+// on the pivot, beta = -sign(x_0) ||x||, tau = (beta - x_0) / beta, v = x / (x_0 - beta) with v_0 = 1;
+// tau = 0 when nothing below the pivot is non-zero) and the compact-WY factor T of the panel
+// (T_kk = tau_k, T_{0:k,k} = -tau_k T_{0:k,0:k} V_{:,0:k}^T v_k), so that H_1 ... H_jb = I - V T V^T.
+// One 512-thread workgroup per panel; thread t holds rows t + 512 i (i < 8) of the panel in
+// registers. Per column: one block reduction for the norm below the pivot, one for the 15 dot
+// products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k, for T). Every sum is
+// taken in a fixed order.
+__global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanelDesc* __restrict__ descs) {
+  __shared__ float red1[kQrPanelThreads / 64];
+  __shared__ float red2[kQrPanelThreads / 64][kQrPanel];
+  __shared__ float alpha_s;
+  __shared__ float Ts[kQrPanel][kQrPanel];
+  const QrPanelDesc& d = descs[blockIdx.x];
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int jb = d.jb;
+  float a[kQrRowsPerThread][kQrPanel];
+#pragma unroll
+  for (int i = 0; i < kQrRowsPerThread; ++i) {
+    const int lr = t + kQrPanelThreads * i;
+    if (lr < d.rows) {
+      const g_cf32x4* row = (const g_cf32x4*)(d.A + (int64_t(d.j0) + lr) * d.lda + d.j0);
+#pragma unroll
+      for (int q = 0; q < kQrPanel / 4; ++q) {
+        const f32x4 v = row[q];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) a[i][4 * q + j] = (4 * q + j < jb) ? v[j] : 0.0f;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kQrPanel; ++k) a[i][k] = 0.0f;
+    }
+  }
+  if (t < kQrPanel * kQrPanel) Ts[t / kQrPanel][t % kQrPanel] = 0.0f;
+
+  unrolled<kQrPanel>([&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    if (k >= jb) return;  // (uniform: jb is the panel's width)
+    // norm of the column below the pivot (local row k), and the pivot itself
+    float s = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kQrRowsPerThread; ++i) {
+      const int lr = t + kQrPanelThreads * i;
+      if (lr > k) s += a[i][k] * a[i][k];
+    }
+    s = wave_sum(s);
+    if (lane == 0) red1[w] = s;
+    if (t == k) alpha_s = a[0][k];
+    __syncthreads();
+    float sigma = 0.0f;
+#pragma unroll
+    for (int j = 0; j < kQrPanelThreads / 64; ++j) sigma += red1[j];
+    const float alpha = alpha_s;
+    float tau = 0.0f, scale = 0.0f;
+    if (sigma != 0.0f) {
+      const float beta = -copysignf(sqrtf(alpha * alpha + sigma), alpha);
+      tau = (beta - alpha) / beta;
+      scale = 1.0f / (alpha - beta);
+    }
+#pragma unroll
+    for (int i = 0; i < kQrRowsPerThread; ++i) {
+      const int lr = t + kQrPanelThreads * i;
+      a[i][k] = lr > k ? a[i][k] * scale : (lr == k ? 1.0f : 0.0f);
+    }
+    // slot s < k: v_s . v_k (for T); slot s >= k: v_k . a_{s+1} (to update column s + 1)
+#pragma unroll
+    for (int sl = 0; sl < kQrPanel - 1; ++sl) {
+      const int col = sl < k ? sl : sl + 1;
+      float acc = 0.0f;
+      if (col < jb) {
+#pragma unroll
+        for (int i = 0; i < kQrRowsPerThread; ++i) acc += a[i][k] * a[i][col];
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) red2[w][sl] = acc;
+    }
+    __syncthreads();
+    auto total = [&](int sl) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int j = 0; j < kQrPanelThreads / 64; ++j) acc += red2[j][sl];
+      return acc;
+    };
+#pragma unroll
+    for (int l = k + 1; l < kQrPanel; ++l) {
+      if (l < jb) {
+        const float f = tau * total(l - 1);
+#pragma unroll
+        for (int i = 0; i < kQrRowsPerThread; ++i) a[i][l] -= f * a[i][k];
+      }
+    }
+    if (t < k) {
+      float acc = 0.0f;
+#pragma unroll
+      for (int j = 0; j < k; ++j)
+        if (j >= t) acc += Ts[t][j] * total(j);
+      Ts[t][k] = -tau * acc;
+    } else if (t == k) {
+      Ts[k][k] = tau;
+    }
+  });
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kQrRowsPerThread; ++i) {
+    const int lr = t + kQrPanelThreads * i;
+    if (lr < d.rows) {
+      g_f32x4* vrow = (g_f32x4*)(d.V + int64_t(lr) * kQrPanel);
+#pragma unroll
+      for (int q = 0; q < kQrPanel / 4; ++q)
+        vrow[q] = f32x4{a[i][4 * q], a[i][4 * q + 1], a[i][4 * q + 2], a[i][4 * q + 3]};
+    }
+  }
+  if (t < kQrPanel * kQrPanel) ((g_f32*)d.T)[t] = Ts[t / kQrPanel][t % kQrPanel];
+}
+
+// X <- X - V (T^T (V^T X)) on one block of 64 columns, all `rows` rows: a first pass forms the 16
+// column sums W = V^T X (4 row groups of one wave each, combined in a fixed order), one wave forms
+// Y = T^T W, a second pass subtracts V Y.
+__global__ __launch_bounds__(256) void qr_apply_kernel(const QrApplyDesc* __restrict__ descs, int count) {
+  __shared__ float red[4][kQrPanel][kQrApplyCols];
+  __shared__ float ys[kQrPanel][kQrApplyCols];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const QrApplyDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int t = threadIdx.x, c = t & 63, rg = t >> 6;
+  const int lc = lt * kQrApplyCols + c;
+  const bool live = lc < d.cols;
+  g_f32* X = (g_f32*)(d.X) + int64_t(d.row0) * d.ldx + d.c0 + (live ? lc : 0);
+  const g_cf32x4* V = (const g_cf32x4*)(d.V);
+  float wk[kQrPanel];
+#pragma unroll
+  for (int k = 0; k < kQrPanel; ++k) wk[k] = 0.0f;
+  if (live) {
+#pragma unroll 4
+    for (int r = rg; r < d.rows; r += 4) {
+      const float x = X[int64_t(r) * d.ldx];
+#pragma unroll
+      for (int q = 0; q < kQrPanel / 4; ++q) {
+        const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + q];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wk[4 * q + j] += v[j] * x;
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < kQrPanel; ++k) red[rg][k][c] = wk[k];
+  __syncthreads();
+  if (rg == 0) {
+    const g_cf32* T = (const g_cf32*)(d.T);
+    float W[kQrPanel];
+#pragma unroll
+    for (int k = 0; k < kQrPanel; ++k) W[k] = ((red[0][k][c] + red[1][k][c]) + red[2][k][c]) + red[3][k][c];
+#pragma unroll
+    for (int i = 0; i < kQrPanel; ++i) {
+      float y = 0.0f;
+#pragma unroll
+      for (int k = 0; k <= i; ++k) y += T[k * kQrPanel + i] * W[k];
+      ys[i][c] = y;
+    }
+  }
+  __syncthreads();
+  if (!live) return;
+  float y[kQrPanel];
+#pragma unroll
+  for (int k = 0; k < kQrPanel; ++k) y[k] = ys[k][c];
+#pragma unroll 4
+  for (int r = rg; r < d.rows; r += 4) {
+    float s = 0.0f;
+#pragma unroll
+    for (int q = 0; q < kQrPanel / 4; ++q) {
+      const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + q];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) s += v[j] * y[4 * q + j];
+    }
+    const int64_t o = int64_t(r) * d.ldx;
+    X[o] = X[o] - s;
+  }
+}
+
+// Transposed boundary copy: dst[c][r] = src[r][c] for r < rows, c < cols (64 x 64 tiles over the
+// real block, through a padded LDS tile).
+__global__ __launch_bounds__(256) void copy_out_t_kernel(const ShCopyDesc* __restrict__ descs, int count) {
+  __shared__ float tt[kTile][kTile + 1];
+  const int e = find_desc(descs, count, blockIdx.x);
+  const ShCopyDesc& d = descs[e];
+  const int lt = blockIdx.x - d.tile_begin;
+  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
+  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
+  const g_cf32* src = (const g_cf32*)(d.src);
+  g_f32* dst = (g_f32*)(d.dst);
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;
+    const int64_t gr = int64_t(ti) * kTile + r, gc = int64_t(tj) * kTile + c;
+    tt[r][c] = (gr < d.rows && gc < d.cols) ? src[gr * d.ld_src + gc] : 0.0f;
+  }
+  __syncthreads();
+#pragma unroll 4
+  for (int i = 0; i < 16; ++i) {
+    const int r = rr + 4 * i;  // destination row = source column
+    const int64_t dr = int64_t(tj) * kTile + r, dc = int64_t(ti) * kTile + c;
+    if (dr < d.cols && dc < d.rows) dst[dr * d.ld_dst + dc] = tt[c][r];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_soap_prep(const SoapPrepDesc* d, int count, int total_tiles, float beta1, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(soap_prep_kernel, dim3(total_tiles), dim3(256), 0, st, d, count, beta1);
+  return hipGetLastError();
+}
+
+hipError_t launch_soap_adam(const SoapAdamDesc* d, int count, int total_tiles, float beta2, float eps,
+                            float inv_bc1, float inv_sqrt_bc2, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(soap_adam_kernel, dim3(total_tiles), dim3(256), 0, st, d, count, beta2, eps, inv_bc1,
+                     inv_sqrt_bc2);
+  return hipGetLastError();
+}
+
+hipError_t launch_soap_eye(const SoapEyeDesc* d, int count, int total_tiles, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(soap_eye_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_qr_panel(const QrPanelDesc* d, int count, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(qr_panel_kernel, dim3(count), dim3(kQrPanelThreads), 0, st, d);
+  return hipGetLastError();
+}
+
+hipError_t launch_qr_apply(const QrApplyDesc* d, int count, int total_blocks, hipStream_t st) {
+  if (total_blocks <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(qr_apply_kernel, dim3(total_blocks), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_out_transposed(const ShCopyDesc* d, int count, int total_tiles, hipStream_t st) {
+  if (total_tiles <= 0 || count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(copy_out_t_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+  return hipGetLastError();
+}
+
+}  // namespace mfsdp

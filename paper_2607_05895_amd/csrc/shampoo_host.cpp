@@ -29,39 +29,15 @@
 #include <string>
 #include <vector>
 
-#include "../../include/mfsdp.h"
-#include "mfsdp_internal.h"
-#include "shampoo_internal.h"
-
-namespace mfsdp {
-int set_last_error(int status, const std::string& msg);
-int staging_acquire(size_t bytes, void** host);
-int staging_upload(int slot, void* dst, size_t bytes, hipStream_t st);
-}  // namespace mfsdp
+#include "shampoo_build.h"
 
 using namespace mfsdp;
+using namespace mfsdp::shb;
 
 namespace {
 
-constexpr size_t kAl = 256;
 constexpr int kNormChunkRows = 16;
 constexpr int64_t kMaxDim = 1 << 16;
-size_t al(size_t x) { return (x + kAl - 1) / kAl * kAl; }
-int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
-int bad(const std::string& m) { return set_last_error(MFSDP_E_INVALID, m); }
-int hip_err(hipError_t e, const char* what) {
-  return set_last_error(MFSDP_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
-}
-
-// Workspace bump allocator (offsets only; the base is added when the workspace is known).
-struct Arena {
-  size_t off = 0;
-  size_t take(size_t bytes) {
-    const size_t o = off;
-    off = al(off + bytes);
-    return o;
-  }
-};
 
 // One inverse-root problem on a padded d_pad x d_pad statistic held in M.
 struct Side {
@@ -91,83 +67,6 @@ struct EntryPlan {
   size_t Gp, GpT, Y;
   Side L, R;
 };
-
-// The launch sequence: descriptor arrays packed in one host buffer (uploaded once into the
-// workspace) and the ops that consume them.
-enum OpKind { kOpCopyIn, kOpCopyOut, kOpGemm, kOpNorm, kOpScalars, kOpInit, kOpApply };
-struct Op {
-  OpKind kind;
-  size_t desc_off;
-  int count;
-  int total;  // grid blocks
-};
-
-struct Build {
-  char* base = nullptr;  // workspace base (nullptr while sizing)
-  std::vector<char> h;
-  std::vector<Op> ops;
-  template <class T>
-  T* ptr(size_t off) const {  // integer arithmetic: base is null while only sizing
-    return reinterpret_cast<T*>(reinterpret_cast<uintptr_t>(base) + off);
-  }
-  template <class T>
-  size_t put(const std::vector<T>& v) {
-    const size_t o = al(h.size());
-    h.resize(o + v.size() * sizeof(T));
-    std::memcpy(h.data() + o, v.data(), v.size() * sizeof(T));
-    return o;
-  }
-  template <class T>
-  void op(OpKind k, const std::vector<T>& v, int total) {
-    if (v.empty() || total <= 0) return;
-    ops.push_back(Op{k, put(v), int(v.size()), total});
-  }
-};
-
-ShCopyDesc copy_desc(const void* src, int dt, void* dst, float* dstT, int64_t rows, int64_t cols,
-                     int64_t ld_src, int64_t ld_dst, int64_t ld_dstT, int64_t dom_rows,
-                     int64_t dom_cols, int& tiles) {
-  ShCopyDesc c{};
-  c.src = src;
-  c.dst = dst;
-  c.dstT = dstT;
-  c.rows = rows;
-  c.cols = cols;
-  c.ld_src = ld_src;
-  c.ld_dst = ld_dst;
-  c.ld_dstT = ld_dstT;
-  c.src_dtype = dt;
-  const int64_t tm = (dom_rows + kShCopyTile - 1) / kShCopyTile;
-  const int64_t tn = (dom_cols + kShCopyTile - 1) / kShCopyTile;
-  c.tiles_n = int32_t(tn);
-  c.tile_begin = tiles;
-  tiles += int(tm * tn);
-  return c;
-}
-
-ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, float* C, int64_t ldp,
-                     int64_t ldq, int64_t lde, int64_t ldc, int64_t M, int64_t N, int64_t K,
-                     int sym, float alpha, float beta, float diag, int& tiles) {
-  ShGemmDesc g{};
-  g.P = P;
-  g.Q = Q;
-  g.E = E;
-  g.C = C;
-  g.ldp = ldp;
-  g.ldq = ldq;
-  g.lde = lde;
-  g.ldc = ldc;
-  g.K = int32_t(K);
-  g.tiles_n = int32_t(N / kShTile);
-  g.sym = sym;
-  g.alpha = alpha;
-  g.beta = beta;
-  g.diag = diag;
-  g.tile_begin = tiles;
-  const int64_t tm = M / kShTile, tn = N / kShTile;
-  tiles += int(sym ? tn * (tn + 1) / 2 : tm * tn);
-  return g;
-}
 
 // Root ops for every side: norms, scalars, init, the iterations and the copy of X to side.out.
 // In every grouped launch the larger problems come first (their tiles run longest), so the
@@ -279,40 +178,6 @@ void add_root_ops(Build& b, std::vector<Side*> sides, int p, int iters) {
   }
   b.op(kOpCopyOut, co, ct);
 }
-
-int run(Build& b, char* ws, size_t desc_at, hipStream_t st, double eps, double eps_rel, int p,
-        float decay, float step) {
-  if (!b.h.empty()) {
-    void* host = nullptr;
-    const int slot = staging_acquire(b.h.size(), &host);
-    if (slot < 0) return slot;
-    std::memcpy(host, b.h.data(), b.h.size());
-    const int rc = staging_upload(slot, ws + desc_at, b.h.size(), st);
-    if (rc != MFSDP_OK) return rc;
-  }
-  for (const Op& o : b.ops) {
-    char* dp = ws + desc_at + o.desc_off;
-    hipError_t e = hipSuccess;
-    switch (o.kind) {
-      case kOpCopyIn: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 0, st); break;
-      case kOpCopyOut: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 1, st); break;
-      case kOpGemm: e = launch_sh_gemm(reinterpret_cast<ShGemmDesc*>(dp), o.count, o.total, st); break;
-      case kOpNorm: e = launch_sh_norm(reinterpret_cast<ShNormDesc*>(dp), o.count, o.total, st); break;
-      case kOpScalars:
-        e = launch_sh_scalars(reinterpret_cast<ShScalarDesc*>(dp), o.count, eps, eps_rel, p, st);
-        break;
-      case kOpInit: e = launch_sh_init(reinterpret_cast<ShInitDesc*>(dp), o.count, o.total, st); break;
-      case kOpApply:
-        e = launch_sh_apply(reinterpret_cast<ShApplyDesc*>(dp), o.count, o.total, decay, step, st);
-        break;
-    }
-    if (e != hipSuccess) return hip_err(e, "Shampoo kernel launch");
-  }
-  return MFSDP_OK;
-}
-
-bool dtype_ok(int32_t dt) { return dt == MFSDP_F32 || dt == MFSDP_BF16; }
-bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 int check_shampoo_hp(const mfsdp_shampoo_hparams* hp) {
   if (!hp) return bad("hparams is NULL");
@@ -516,9 +381,13 @@ int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count, const 
   if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
     return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
                                              "mfsdp_shampoo_workspace_size (" + std::to_string(need) + " bytes)");
-  const double decay = 1.0 - hp->lr * hp->weight_decay;
-  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), hp->eps,
-             hp->eps_rel, 4, float(decay), float(hp->lr));
+  RunScalars rs;
+  rs.eps = hp->eps;
+  rs.eps_rel = hp->eps_rel;
+  rs.p = 4;
+  rs.decay = float(1.0 - hp->lr * hp->weight_decay);
+  rs.step = float(hp->lr);
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), rs);
 }
 
 size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters) {
@@ -543,8 +412,11 @@ int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double 
   if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
     return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
                                              "mfsdp_inverse_root_workspace_size (" + std::to_string(need) + " bytes)");
-  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), eps, eps_rel, p,
-             1.0f, 0.0f);
+  RunScalars rs;
+  rs.eps = eps;
+  rs.eps_rel = eps_rel;
+  rs.p = p;
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), rs);
 }
 
 }  // extern "C"

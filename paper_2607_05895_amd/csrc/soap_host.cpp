@@ -1,0 +1,433 @@
+// Host side of the SOAP owner step and of the standalone orthonormal factor: argument checks,
+// workspace plan, descriptor build and the launch sequence (all on the caller's stream).
+//
+// SOAP (Section 5.7 of the paper: Adam in the eigenbasis of Shampoo's statistics; Vyas et al. 2024,
+// matrix case) per owned m x n matrix, with the bases Q_L, Q_R of the previous refresh:
+//   G' = Q_L^T G Q_R,  M <- beta1 M + (1 - beta1) G,  M' = Q_L^T M Q_R
+//   V <- beta2 V + (1 - beta2) G'^2,  N' = bias-corrected M' / (sqrt(V) + eps),  N = Q_L N' Q_R^T
+//   p <- p (1 - lr wd) - lr N;  L <- beta_s L + w_s G G^T, R <- beta_s R + w_s G^T G
+//   refresh: Q_L <- Q of QR(L Q_L), Q_R <- Q of QR(R Q_R)   (refresh_iters times)
+//
+// Every product is an NT product C = alpha P Q^T (+ beta E) on the Shampoo GEMM, over padded
+// row-major buffers (mp, np = m, n rounded up to 128), grouped over the entries:
+//   X1      = Q_L^T [G | M]      P = Q_L^T,  Q = [G^T ; M^T]        (mp x 2np, K = mp)
+//   [G'|M'] = X1 halves . Q_R    P = X1 half, Q = Q_R^T              (two mp x np, K = np)
+//   Z       = Q_L N'             P = Q_L,    Q = N'^T               (mp x np, K = mp)
+//   N       = Z Q_R^T            P = Z,      Q = Q_R                (mp x np, K = np)
+//   L, R statistics              P = Q = G (sym, K = np), P = Q = G^T (sym, K = mp)
+//   refresh S = L Q_L            P = L,      Q = Q_L^T              (mp x mp, K = mp)
+// The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
+// with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
+// block: per 16-column panel one panel launch (V, T) and one launch that applies the block
+// reflector to the trailing columns of S and to the accumulated Q^T (started at the identity).
+// Zero padding is exact: padded rows and columns of G, M, the bases and the statistics are zero, so
+// every product's real block is unaffected and its padded part is zero.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <string>
+#include <vector>
+
+#include "shampoo_build.h"
+
+using namespace mfsdp;
+using namespace mfsdp::shb;
+
+namespace {
+
+// One basis refresh problem: S (d_pad x d_pad, real block d x d) is factored in place, Qt
+// accumulates Q^T.
+struct QrSide {
+  int64_t d = 0, dp = 0;
+  size_t S = 0, Qt = 0, V = 0, T = 0;
+};
+
+void plan_qr_buffers(QrSide& s, Arena& a) {
+  s.V = a.take(size_t(s.d) * kQrPanel * sizeof(float));
+  s.T = a.take(size_t(kQrPanel) * kQrPanel * sizeof(float));
+}
+
+// Qt = I, then per panel: factor it, apply its reflector to S's trailing columns and to Qt.
+// Sides are listed largest first in every grouped launch.
+void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
+  if (sides.empty()) return;
+  std::stable_sort(sides.begin(), sides.end(), [](const QrSide* x, const QrSide* y) { return x->d > y->d; });
+  std::vector<SoapEyeDesc> ey;
+  int et = 0;
+  for (QrSide* s : sides) {
+    SoapEyeDesc e{};
+    e.X = b.ptr<float>(s->Qt);
+    e.ld = s->dp;
+    e.d = s->d;
+    const int64_t tn = (s->d + kShCopyTile - 1) / kShCopyTile;
+    e.tiles_n = int32_t(tn);
+    e.tile_begin = et;
+    et += int(tn * tn);
+    ey.push_back(e);
+  }
+  b.op(kOpEye, ey, et);
+  for (int64_t j0 = 0; j0 < sides[0]->d; j0 += kQrPanel) {
+    std::vector<QrPanelDesc> pd;
+    std::vector<QrApplyDesc> ad;
+    int at = 0;
+    for (QrSide* s : sides) {
+      if (s->d <= j0) continue;
+      QrPanelDesc p{};
+      p.A = b.ptr<float>(s->S);
+      p.lda = s->dp;
+      p.V = b.ptr<float>(s->V);
+      p.T = b.ptr<float>(s->T);
+      p.j0 = int32_t(j0);
+      p.jb = int32_t(std::min<int64_t>(kQrPanel, s->d - j0));
+      p.rows = int32_t(s->d - j0);
+      pd.push_back(p);
+      auto apply = [&](size_t X, int64_t c0, int64_t cols) {
+        if (cols <= 0) return;
+        QrApplyDesc a{};
+        a.X = b.ptr<float>(X);
+        a.ldx = s->dp;
+        a.V = p.V;
+        a.T = p.T;
+        a.row0 = p.j0;
+        a.rows = p.rows;
+        a.c0 = int32_t(c0);
+        a.cols = int32_t(cols);
+        a.tile_begin = at;
+        at += int((cols + kQrApplyCols - 1) / kQrApplyCols);
+        ad.push_back(a);
+      };
+      apply(s->S, j0 + p.jb, s->d - j0 - p.jb);
+      apply(s->Qt, 0, s->d);
+    }
+    b.op(kOpQrPanel, pd, int(pd.size()));
+    b.op(kOpQrApply, ad, at);
+  }
+}
+
+// A grouped product before its tile offset is known (so that a launch can be ordered by cost).
+struct Prod {
+  const float *P, *Q, *E;
+  float* C;
+  int64_t ldp, ldq, lde, ldc, M, N, K;
+  int sym;
+  float alpha, beta;
+};
+
+void add_gemm(Build& b, std::vector<Prod> ps) {
+  // longest tiles (largest K) first: the hardware dispatches blocks in order
+  std::stable_sort(ps.begin(), ps.end(), [](const Prod& x, const Prod& y) { return x.K > y.K; });
+  std::vector<ShGemmDesc> gs;
+  int gt = 0;
+  for (const Prod& p : ps)
+    gs.push_back(gemm_desc(p.P, p.Q, p.E, p.C, p.ldp, p.ldq, p.lde, p.ldc, p.M, p.N, p.K, p.sym, p.alpha,
+                           p.beta, 0.0f, gt));
+  b.op(kOpGemm, gs, gt);
+}
+
+struct SoapPlan {
+  int64_t m = 0, n = 0, mp = 0, np = 0;
+  size_t Gp = 0, GMt = 0, X1 = 0, GMr = 0, NpT = 0, QLp = 0, QLt = 0, QRp = 0, QRt = 0, Lp = 0, Rp = 0;
+  QrSide L, R;
+};
+
+int check_soap_hp(const mfsdp_soap_hparams* hp) {
+  if (!hp) return bad("hparams is NULL");
+  auto fin = [](double x) { return std::isfinite(x); };
+  if (!(hp->lr >= 0.0) || !fin(hp->lr)) return bad("lr must be finite and >= 0");
+  if (!(hp->weight_decay >= 0.0) || !fin(hp->weight_decay)) return bad("weight_decay must be finite and >= 0");
+  if (!(hp->beta1 >= 0.0 && hp->beta1 < 1.0)) return bad("beta1 must be in [0, 1)");
+  if (!(hp->beta2 >= 0.0 && hp->beta2 < 1.0)) return bad("beta2 must be in [0, 1)");
+  if (!(hp->eps > 0.0) || !fin(hp->eps)) return bad("eps must be finite and > 0");
+  if (!(hp->shampoo_beta >= 0.0) || !fin(hp->shampoo_beta)) return bad("shampoo_beta must be finite and >= 0");
+  if (!(hp->shampoo_weight >= 0.0) || !fin(hp->shampoo_weight))
+    return bad("shampoo_weight must be finite and >= 0");
+  if (hp->step < 1) return bad("step must be >= 1");
+  if (hp->refresh != 0 && hp->refresh != 1) return bad("refresh must be 0 or 1");
+  if (hp->refresh_iters < 1 || hp->refresh_iters > 100) return bad("refresh_iters must be in [1, 100]");
+  return MFSDP_OK;
+}
+
+int check_soap_entries(const mfsdp_soap_entry* en, int64_t count, bool data) {
+  if (count < 0) return bad("count must be >= 0");
+  if (count > 0 && !en) return bad("entries is NULL");
+  if (count > 4096) return bad("at most 4096 entries per call");
+  int64_t units = 0;  // bound on the 64 x 64 tiles of any one grouped launch (grid and int32 counters)
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_soap_entry& e = en[i];
+    const std::string w = "entry " + std::to_string(i) + ": ";
+    if (e.m < 1 || e.n < 1 || e.m > kQrMaxDim || e.n > kQrMaxDim) return bad(w + "m and n must be in [1, 4096]");
+    const int64_t s = rup(e.m, kShTile) + 2 * rup(e.n, kShTile);
+    units += 3 * (s / kShCopyTile) * (s / kShCopyTile);
+    if (units > (int64_t(1) << 30)) return bad("the entries of one call exceed 2^30 tiles per launch");
+    if (!dtype_ok(e.param_dtype) || !dtype_ok(e.grad_dtype)) return bad(w + "dtype must be F32 or BF16");
+    if (!data) continue;
+    if (!e.param || !e.grad || !e.exp_avg || !e.exp_avg_sq || !e.L || !e.R || !e.QL || !e.QR)
+      return bad(w + "NULL pointer");
+    const size_t pa = e.param_dtype == MFSDP_BF16 ? 2 : 4, ga = e.grad_dtype == MFSDP_BF16 ? 2 : 4;
+    if (!aligned(e.param, pa) || !aligned(e.grad, ga) || !aligned(e.exp_avg, 4) || !aligned(e.exp_avg_sq, 4) ||
+        !aligned(e.L, 4) || !aligned(e.R, 4) || !aligned(e.QL, 4) || !aligned(e.QR, 4) ||
+        !aligned(e.update_out, 4))
+      return bad(w + "misaligned pointer");
+  }
+  return MFSDP_OK;
+}
+
+size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hparams* hp, char* ws,
+                  Build& b, size_t& desc_at) {
+  b.base = ws;
+  Arena a;
+  std::vector<SoapPlan> P(static_cast<size_t>(count));
+  for (int64_t i = 0; i < count; ++i) {
+    SoapPlan& e = P[size_t(i)];
+    e.m = en[i].m;
+    e.n = en[i].n;
+    e.mp = rup(e.m, kShTile);
+    e.np = rup(e.n, kShTile);
+    const size_t f = sizeof(float), mn = size_t(e.mp) * size_t(e.np) * f;
+    e.Gp = a.take(mn);
+    e.GMt = a.take(2 * mn);
+    e.X1 = a.take(2 * mn);   // later Z = Q_L N' (mp x np)
+    e.GMr = a.take(2 * mn);  // later N (mp x np)
+    e.NpT = a.take(mn);
+    const size_t mm = size_t(e.mp) * size_t(e.mp) * f, nn = size_t(e.np) * size_t(e.np) * f;
+    e.QLp = a.take(mm);  // later the refresh product S = L Q_L
+    e.QLt = a.take(mm);  // later the accumulated Q_L^T of the refresh
+    e.Lp = a.take(mm);
+    e.QRp = a.take(nn);
+    e.QRt = a.take(nn);
+    e.Rp = a.take(nn);
+    e.L.d = e.m;
+    e.L.dp = e.mp;
+    e.L.S = e.QLp;
+    e.L.Qt = e.QLt;
+    plan_qr_buffers(e.L, a);
+    e.R.d = e.n;
+    e.R.dp = e.np;
+    e.R.S = e.QRp;
+    e.R.Qt = e.QRt;
+    plan_qr_buffers(e.R, a);
+  }
+  desc_at = a.off;
+
+  std::vector<ShCopyDesc> cin;
+  std::vector<SoapPrepDesc> prep;
+  int ct = 0, pt = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    SoapPlan& e = P[size_t(i)];
+    cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.Lp), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp, e.mp, ct));
+    cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.Rp), nullptr, e.n, e.n, e.n, e.np, 0, e.np, e.np, ct));
+    cin.push_back(copy_desc(en[i].QL, kDtF32, b.ptr<float>(e.QLp), b.ptr<float>(e.QLt), e.m, e.m, e.m, e.mp,
+                            e.mp, e.mp, e.mp, ct));
+    cin.push_back(copy_desc(en[i].QR, kDtF32, b.ptr<float>(e.QRp), b.ptr<float>(e.QRt), e.n, e.n, e.n, e.np,
+                            e.np, e.np, e.np, ct));
+    SoapPrepDesc d{};
+    d.grad = en[i].grad;
+    d.exp_avg = en[i].exp_avg;
+    d.Gp = b.ptr<float>(e.Gp);
+    d.GMt = b.ptr<float>(e.GMt);
+    d.m = e.m;
+    d.n = e.n;
+    d.mp = e.mp;
+    d.np = e.np;
+    d.grad_dtype = en[i].grad_dtype == MFSDP_BF16 ? kDtBF16 : kDtF32;
+    d.tiles_n = int32_t(e.np / kShCopyTile);
+    d.tile_begin = pt;
+    pt += int((e.mp / kShCopyTile) * (e.np / kShCopyTile));
+    prep.push_back(d);
+  }
+  b.op(kOpCopyIn, cin, ct);
+  b.op(kOpSoapPrep, prep, pt);
+
+  const float ws_ = float(hp->shampoo_weight), bs_ = float(hp->shampoo_beta);
+  std::vector<Prod> p1, p2, p3, p4;
+  for (SoapPlan& e : P) {
+    float* X1 = b.ptr<float>(e.X1);
+    float* GMr = b.ptr<float>(e.GMr);
+    const float* GMt = b.ptr<float>(e.GMt);
+    const float* Gp = b.ptr<float>(e.Gp);
+    const int64_t mp = e.mp, np = e.np;
+    p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, 2 * np, mp, 0, 1.0f, 0.0f});
+    // the statistics read only G and G^T: they join the first launch
+    p1.push_back(Prod{Gp, Gp, b.ptr<float>(e.Lp), b.ptr<float>(e.Lp), np, np, mp, mp, mp, mp, np, 1, ws_, bs_});
+    p1.push_back(Prod{GMt, GMt, b.ptr<float>(e.Rp), b.ptr<float>(e.Rp), mp, mp, np, np, np, np, mp, 1, ws_, bs_});
+    for (int h = 0; h < 2; ++h)
+      p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np, np,
+                        0, 1.0f, 0.0f});
+    p3.push_back(Prod{b.ptr<float>(e.QLp), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f,
+                      0.0f});
+    p4.push_back(Prod{X1, b.ptr<float>(e.QRp), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
+  }
+  add_gemm(b, p1);
+  add_gemm(b, p2);
+
+  std::vector<SoapAdamDesc> ad;
+  int at = 0;
+  for (SoapPlan& e : P) {
+    SoapAdamDesc d{};
+    d.GMr = b.ptr<float>(e.GMr);
+    d.exp_avg_sq = en[&e - P.data()].exp_avg_sq;
+    d.NpT = b.ptr<float>(e.NpT);
+    d.m = e.m;
+    d.n = e.n;
+    d.mp = e.mp;
+    d.np = e.np;
+    d.tiles_n = int32_t(e.np / kShCopyTile);
+    d.tile_begin = at;
+    at += int((e.mp / kShCopyTile) * (e.np / kShCopyTile));
+    ad.push_back(d);
+  }
+  b.op(kOpSoapAdam, ad, at);
+  add_gemm(b, p3);
+  add_gemm(b, p4);
+
+  std::vector<ShApplyDesc> ap;
+  int apt = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    SoapPlan& e = P[size_t(i)];
+    ShApplyDesc d{};
+    d.U = b.ptr<float>(e.GMr);
+    d.ldu = e.np;
+    d.param = en[i].param;
+    d.update_out = en[i].update_out;
+    d.m = e.m;
+    d.n = e.n;
+    d.param_dtype = en[i].param_dtype == MFSDP_BF16 ? kDtBF16 : kDtF32;
+    const int64_t tn = (e.n + kShCopyTile - 1) / kShCopyTile, tm = (e.m + kShCopyTile - 1) / kShCopyTile;
+    d.tiles_n = int32_t(tn);
+    d.tile_begin = apt;
+    apt += int(tm * tn);
+    ap.push_back(d);
+  }
+  b.op(kOpApply, ap, apt);
+
+  std::vector<ShCopyDesc> cst;
+  ct = 0;
+  for (int64_t i = 0; i < count; ++i) {
+    SoapPlan& e = P[size_t(i)];
+    cst.push_back(copy_desc(b.ptr<float>(e.Lp), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, ct));
+    cst.push_back(copy_desc(b.ptr<float>(e.Rp), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, ct));
+  }
+  b.op(kOpCopyOut, cst, ct);
+
+  if (hp->refresh) {
+    std::vector<Prod> ps;
+    std::vector<QrSide*> sides;
+    for (SoapPlan& e : P) {
+      ps.push_back(Prod{b.ptr<float>(e.Lp), b.ptr<float>(e.QLt), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
+                        e.mp, e.mp, e.mp, 0, 1.0f, 0.0f});
+      ps.push_back(Prod{b.ptr<float>(e.Rp), b.ptr<float>(e.QRt), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
+                        e.np, e.np, e.np, 0, 1.0f, 0.0f});
+      sides.push_back(&e.L);
+      sides.push_back(&e.R);
+    }
+    // one refresh = the power step S = statistic * basis, then the QR of S; later repetitions reuse
+    // the first one's descriptors
+    const size_t first = b.ops.size();
+    add_gemm(b, ps);
+    add_qr_ops(b, sides);
+    const size_t last = b.ops.size();
+    for (int it = 1; it < hp->refresh_iters; ++it)
+      for (size_t k = first; k < last; ++k) {
+        const Op o = b.ops[k];
+        b.ops.push_back(o);
+      }
+    std::vector<ShCopyDesc> co;
+    int cot = 0;
+    for (int64_t i = 0; i < count; ++i) {
+      SoapPlan& e = P[size_t(i)];
+      co.push_back(copy_desc(b.ptr<float>(e.QLt), kDtF32, en[i].QL, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, cot));
+      co.push_back(copy_desc(b.ptr<float>(e.QRt), kDtF32, en[i].QR, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, cot));
+    }
+    b.op(kOpCopyOutT, co, cot);
+  }
+  return desc_at + al(b.h.size());
+}
+
+size_t build_factor(int64_t d, const float* a, float* q, char* ws, Build& b, size_t& desc_at) {
+  b.base = ws;
+  Arena ar;
+  QrSide s;
+  s.d = d;
+  s.dp = rup(d, kShTile);
+  const size_t mat = size_t(s.dp) * size_t(s.dp) * sizeof(float);
+  s.S = ar.take(mat);
+  s.Qt = ar.take(mat);
+  plan_qr_buffers(s, ar);
+  desc_at = ar.off;
+  std::vector<ShCopyDesc> cin;
+  int ct = 0;
+  cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.S), nullptr, d, d, d, s.dp, 0, s.dp, s.dp, ct));
+  b.op(kOpCopyIn, cin, ct);
+  std::vector<QrSide*> sides{&s};
+  add_qr_ops(b, sides);
+  std::vector<ShCopyDesc> co;
+  int cot = 0;
+  co.push_back(copy_desc(b.ptr<float>(s.Qt), kDtF32, q, nullptr, d, d, s.dp, d, 0, d, d, cot));
+  b.op(kOpCopyOutT, co, cot);
+  return desc_at + al(b.h.size());
+}
+
+int workspace_error(size_t need, const char* query) {
+  return set_last_error(MFSDP_E_WORKSPACE, std::string("workspace NULL, not 256-byte aligned or smaller than ") +
+                                               query + " (" + std::to_string(need) + " bytes)");
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp) {
+  if (check_soap_entries(entries, count, false) != MFSDP_OK) return 0;
+  if (check_soap_hp(hp) != MFSDP_OK) return 0;
+  if (count == 0) return 0;
+  Build b;
+  size_t desc_at = 0;
+  return build_soap(entries, count, hp, nullptr, b, desc_at);
+}
+
+int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
+                    void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_soap_entries(entries, count, true);
+  if (rc != MFSDP_OK) return rc;
+  rc = check_soap_hp(hp);
+  if (rc != MFSDP_OK) return rc;
+  if (count == 0) return MFSDP_OK;
+  Build b;
+  size_t desc_at = 0;
+  const size_t need = build_soap(entries, count, hp, static_cast<char*>(workspace), b, desc_at);
+  if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
+    return workspace_error(need, "mfsdp_soap_workspace_size");
+  RunScalars rs;
+  rs.decay = float(1.0 - hp->lr * hp->weight_decay);
+  rs.step = float(hp->lr);
+  rs.beta1 = float(hp->beta1);
+  rs.beta2 = float(hp->beta2);
+  rs.adam_eps = float(hp->eps);
+  rs.inv_bc1 = float(1.0 / (1.0 - std::pow(hp->beta1, double(hp->step))));
+  rs.inv_sqrt_bc2 = float(1.0 / std::sqrt(1.0 - std::pow(hp->beta2, double(hp->step))));
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), rs);
+}
+
+size_t mfsdp_orthonormal_factor_workspace_size(int64_t d) {
+  if (d < 1 || d > kQrMaxDim) return 0;
+  Build b;
+  size_t desc_at = 0;
+  return build_factor(d, nullptr, nullptr, nullptr, b, desc_at);
+}
+
+int mfsdp_orthonormal_factor(const float* a, float* q, int64_t d, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  if (!a || !q) return bad("a and q must be non-NULL");
+  if (!aligned(a, 4) || !aligned(q, 4)) return bad("misaligned pointer");
+  if (d < 1 || d > kQrMaxDim) return bad("d must be in [1, 4096]");
+  Build b;
+  size_t desc_at = 0;
+  const size_t need = build_factor(d, a, q, static_cast<char*>(workspace), b, desc_at);
+  if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
+    return workspace_error(need, "mfsdp_orthonormal_factor_workspace_size");
+  return run(b, static_cast<char*>(workspace), desc_at, static_cast<hipStream_t>(stream), RunScalars{});
+}
+
+}  // extern "C"

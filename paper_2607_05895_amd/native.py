@@ -22,9 +22,11 @@ EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_time
            "mfsdp_newton_schulz", "mfsdp_newton_schulz_schedule", "mfsdp_adamw_step", "mfsdp_last_error",
            "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners",
            "mfsdp_shampoo_workspace_size", "mfsdp_shampoo_step", "mfsdp_inverse_root_workspace_size",
-           "mfsdp_inverse_root")
+           "mfsdp_inverse_root", "mfsdp_soap_workspace_size", "mfsdp_soap_step",
+           "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor")
 MAX_GRAD_PARTS = 64
-ABI_VERSION = 4
+ABI_VERSION = 5
+SOAP_MAX_DIM = 4096
 
 
 class MuonEntry(ctypes.Structure):
@@ -61,6 +63,20 @@ class ShampooHParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("weight_decay", ctypes.c_double), ("beta", ctypes.c_double),
                 ("weight", ctypes.c_double), ("eps", ctypes.c_double), ("eps_rel", ctypes.c_double),
                 ("refresh", ctypes.c_int32), ("root_iters", ctypes.c_int32)]
+
+
+class SoapEntry(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("exp_avg", ctypes.c_void_p),
+                ("exp_avg_sq", ctypes.c_void_p), ("L", ctypes.c_void_p), ("R", ctypes.c_void_p),
+                ("QL", ctypes.c_void_p), ("QR", ctypes.c_void_p), ("m", ctypes.c_int64), ("n", ctypes.c_int64),
+                ("param_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32), ("update_out", ctypes.c_void_p)]
+
+
+class SoapHParams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("weight_decay", ctypes.c_double), ("beta1", ctypes.c_double),
+                ("beta2", ctypes.c_double), ("eps", ctypes.c_double), ("shampoo_beta", ctypes.c_double),
+                ("shampoo_weight", ctypes.c_double), ("step", ctypes.c_int32), ("refresh", ctypes.c_int32),
+                ("refresh_iters", ctypes.c_int32)]
 
 
 class PlanParam(ctypes.Structure):
@@ -131,6 +147,14 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_inverse_root_workspace_size.restype = sz
         L.mfsdp_inverse_root.argtypes = [vp, vp, i64, i32, f64, f64, i32, vp, sz, vp]
         L.mfsdp_inverse_root.restype = ctypes.c_int
+        L.mfsdp_soap_workspace_size.argtypes = [ctypes.POINTER(SoapEntry), i64, ctypes.POINTER(SoapHParams)]
+        L.mfsdp_soap_workspace_size.restype = sz
+        L.mfsdp_soap_step.argtypes = [ctypes.POINTER(SoapEntry), i64, ctypes.POINTER(SoapHParams), vp, sz, vp]
+        L.mfsdp_soap_step.restype = ctypes.c_int
+        L.mfsdp_orthonormal_factor_workspace_size.argtypes = [i64]
+        L.mfsdp_orthonormal_factor_workspace_size.restype = sz
+        L.mfsdp_orthonormal_factor.argtypes = [vp, vp, i64, vp, sz, vp]
+        L.mfsdp_orthonormal_factor.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -183,6 +207,26 @@ def mfsdp_shampoo_step(entries: Sequence[ShampooEntry], hp: ShampooHParams, work
                        workspace_bytes: int, stream: int) -> None:
     arr, n = _entries(entries, ShampooEntry)
     _check(lib().mfsdp_shampoo_step(arr, n, ctypes.byref(hp), workspace, workspace_bytes, stream))
+
+
+def mfsdp_soap_workspace_size(entries: Sequence[SoapEntry], hp: SoapHParams) -> int:
+    arr, n = _entries(entries, SoapEntry)
+    return lib().mfsdp_soap_workspace_size(arr, n, ctypes.byref(hp))
+
+
+def mfsdp_soap_step(entries: Sequence[SoapEntry], hp: SoapHParams, workspace: int, workspace_bytes: int,
+                    stream: int = 0) -> None:
+    arr, n = _entries(entries, SoapEntry)
+    _check(lib().mfsdp_soap_step(arr, n, ctypes.byref(hp), workspace, workspace_bytes, stream))
+
+
+def mfsdp_orthonormal_factor_workspace_size(d: int) -> int:
+    return lib().mfsdp_orthonormal_factor_workspace_size(d)
+
+
+def mfsdp_orthonormal_factor(a: int, q: int, d: int, workspace: int, workspace_bytes: int,
+                             stream: int = 0) -> None:
+    _check(lib().mfsdp_orthonormal_factor(a, q, d, workspace, workspace_bytes, stream))
 
 
 def mfsdp_inverse_root_workspace_size(d: int, p: int, iters: int) -> int:
@@ -379,3 +423,35 @@ def inverse_root_t(a, out, p=4, eps=1e-12, eps_rel=1e-6, iters=20, workspace=Non
                                 device=a.device)
     mfsdp_inverse_root(a.data_ptr(), out.data_ptr(), d, p, eps, eps_rel, iters, workspace.data_ptr(),
                        workspace.numel(), _stream())
+
+
+def soap_hparams(lr=3e-3, weight_decay=0.0, beta1=0.95, beta2=0.95, eps=1e-8, shampoo_beta=0.95,
+                 shampoo_weight=0.05, step=1, refresh=False, refresh_iters=1) -> SoapHParams:
+    return SoapHParams(lr, weight_decay, beta1, beta2, eps, shampoo_beta, shampoo_weight, int(step),
+                       int(bool(refresh)), int(refresh_iters))
+
+
+def soap_entry_t(param, grad, exp_avg, exp_avg_sq, L, R, QL, QR, update_out=None) -> SoapEntry:
+    m, n = param.shape
+    return SoapEntry(param.data_ptr(), grad.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), L.data_ptr(),
+                     R.data_ptr(), QL.data_ptr(), QR.data_ptr(), m, n, _dt(param), _dt(grad),
+                     update_out.data_ptr() if update_out is not None else None)
+
+
+def soap_workspace_t(entries: Sequence[SoapEntry], hp: SoapHParams, device="cuda"):
+    import torch
+    size = mfsdp_soap_workspace_size(entries, hp)
+    return torch.empty(max(size, 256), dtype=torch.uint8, device=device)
+
+
+def soap_step_t(entries: Sequence[SoapEntry], hp: SoapHParams, workspace) -> None:
+    mfsdp_soap_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+
+
+def orthonormal_factor_t(a, q, workspace=None) -> None:
+    import torch
+    d = a.shape[0]
+    if workspace is None:
+        workspace = torch.empty(max(mfsdp_orthonormal_factor_workspace_size(d), 256), dtype=torch.uint8,
+                                device=a.device)
+    mfsdp_orthonormal_factor(a.data_ptr(), q.data_ptr(), d, workspace.data_ptr(), workspace.numel(), _stream())

@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert native.mfsdp_abi_version() == native.ABI_VERSION == 4
+    assert native.mfsdp_abi_version() == native.ABI_VERSION == 5
     assert native.mfsdp_status_string(0) == "MFSDP_OK"
     assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
     assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
@@ -306,3 +306,85 @@ def test_muon_rejects_calls_beyond_the_launch_size_limit():
     big = [_entry(m=65536, n=65536) for _ in range(1100)]
     with pytest.raises(native.MfsdpError, match="2\\^30 tiles"):
         native.mfsdp_muon_step(big, native.muon_hparams(), FAKE * 16, 1 << 62, 0)
+
+
+# ---------------------------------------------------------------------------------------------
+# SOAP and the orthonormal factor
+
+def _soap_entry(**kw):
+    d = dict(param=FAKE, grad=FAKE * 2, exp_avg=FAKE * 3, exp_avg_sq=FAKE * 4, L=FAKE * 5, R=FAKE * 6,
+             QL=FAKE * 7, QR=FAKE * 8, m=96, n=200, param_dtype=1, grad_dtype=1, update_out=None)
+    d.update(kw)
+    return native.SoapEntry(**d)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(m=0), dict(n=4097), dict(m=5000), dict(param=None), dict(grad=None), dict(exp_avg=None),
+    dict(exp_avg_sq=None), dict(L=None), dict(R=None), dict(QL=None), dict(QR=None), dict(param_dtype=3),
+    dict(grad_dtype=-1), dict(QL=FAKE * 7 + 2), dict(exp_avg_sq=FAKE * 4 + 1), dict(update_out=FAKE + 2),
+])
+def test_soap_rejects_bad_entries(bad):
+    hp = native.soap_hparams()
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_soap_step([_soap_entry(), _soap_entry(**bad)], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+@pytest.mark.parametrize("bad", [
+    dict(lr=-1.0), dict(weight_decay=-1.0), dict(beta1=1.0), dict(beta2=-0.1), dict(beta1=float("nan")),
+    dict(eps=0.0), dict(shampoo_beta=-1.0), dict(shampoo_weight=float("inf")), dict(step=0),
+    dict(refresh_iters=0), dict(refresh_iters=101), dict(lr=float("inf")),
+])
+def test_soap_rejects_bad_hparams(bad):
+    hp = native.soap_hparams(**bad)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_soap_step([_soap_entry()], hp, FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+    assert native.mfsdp_soap_workspace_size([_soap_entry()], hp) == 0
+
+
+def test_soap_refresh_flag_and_workspace_checks():
+    hp = native.soap_hparams()
+    hp.refresh = 2
+    with pytest.raises(native.MfsdpError):
+        native.mfsdp_soap_step([_soap_entry()], hp, FAKE * 16, 1 << 40, 0)
+    hp = native.soap_hparams(refresh=True)
+    need = native.mfsdp_soap_workspace_size([_soap_entry()], hp)
+    # padded to 128: 8 mp np + 3 (mp^2 + np^2) floats, plus the QR panels 16 (m + n) + 512 floats
+    assert need >= 4 * (8 * 128 * 256 + 3 * (128 ** 2 + 256 ** 2) + 16 * (96 + 200) + 512)
+    for ws, nb in ((None, need), (FAKE * 16 + 8, need), (FAKE * 16, need - 1)):
+        with pytest.raises(native.MfsdpError) as ei:
+            native.mfsdp_soap_step([_soap_entry()], hp, ws, nb, 0)
+        assert ei.value.status == native.E_WORKSPACE
+    assert native.mfsdp_soap_workspace_size([_soap_entry(param=None, QL=None)], hp) == need
+    assert native.mfsdp_soap_workspace_size([], hp) == 0
+    native.mfsdp_soap_step([], hp, None, 0, 0)
+
+
+@pytest.mark.parametrize("refresh,iters", [(0, 1), (1, 1), (1, 4)])
+def test_soap_size_query_equals_what_the_call_needs(refresh, iters):
+    ents = [_soap_entry(), _soap_entry(m=1, n=50, param_dtype=0), _soap_entry(m=300, n=129)]
+    hp = native.soap_hparams(refresh=bool(refresh), refresh_iters=iters, step=4)
+    q = native.mfsdp_soap_workspace_size([native.SoapEntry(m=e.m, n=e.n, param_dtype=e.param_dtype,
+                                                           grad_dtype=e.grad_dtype) for e in ents], hp)
+    assert q > 0
+    assert _needed_bytes(lambda: native.mfsdp_soap_step(ents, hp, FAKE * 16, 0, 0)) == q
+
+
+@pytest.mark.parametrize("bad", [dict(d=0), dict(d=4097), dict(a=None), dict(q=None), dict(a=FAKE + 2)])
+def test_orthonormal_factor_rejects_bad_arguments(bad):
+    args = dict(a=FAKE, q=FAKE * 2, d=100)
+    args.update(bad)
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_orthonormal_factor(args["a"], args["q"], args["d"], FAKE * 16, 1 << 40, 0)
+    assert ei.value.status == native.E_INVALID
+
+
+def test_orthonormal_factor_workspace_query():
+    assert native.mfsdp_orthonormal_factor_workspace_size(0) == 0
+    assert native.mfsdp_orthonormal_factor_workspace_size(4097) == 0
+    for d in (1, 100, 4096):
+        q = native.mfsdp_orthonormal_factor_workspace_size(d)
+        dp = -(-d // 128) * 128
+        assert q >= 4 * (2 * dp * dp + 16 * d + 256)
+        assert _needed_bytes(lambda: native.mfsdp_orthonormal_factor(FAKE, FAKE * 2, d, FAKE * 16, 0, 0)) == q
