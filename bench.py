@@ -15,7 +15,8 @@ sample of the same share on the host cores. `planner` reports the owner planner 
 paper's decoder sweep (planner time, rank-load imbalance, gamma_B per policy); with --plan-span W it
 also runs every rank's planned share on the GPU and reports the step-time imbalance over ranks.
 `shampoo` times the Shampoo owner step (fp32 MFMA) on the GPT-2-small share, with and without
-preconditioner refresh.
+preconditioner refresh; `soap` times the SOAP owner step (Adam in the eigenbasis of the Shampoo
+statistics) on the same share, with and without the basis refresh (power step + Householder QR).
 """
 from __future__ import annotations
 
@@ -326,6 +327,69 @@ def time_shampoo(native, torch, dev, hev, stream, steps, warmup, iters=20) -> di
     return out
 
 
+def soap_nominal_flop(shapes, refresh_iters: int, refresh: bool) -> float:
+    """Nominal flop of one SOAP step: Q_L^T [G | M] (4 m^2 n), its two halves times Q_R (4 m n^2),
+    Q_L N' (2 m^2 n), (Q_L N') Q_R^T (2 m n^2) and the statistics (2 m^2 n + 2 m n^2); per refresh
+    iteration the power step S Q (2 d^3 per side) and a Householder QR with the explicit Q
+    (LAPACK's count, 4/3 d^3 for the factorization and 4/3 d^3 for forming Q)."""
+    tot = 0.0
+    for m, n in shapes:
+        tot += 8.0 * m * n * (m + n)
+        if refresh:
+            tot += refresh_iters * (2.0 + 8.0 / 3.0) * (m ** 3 + n ** 3)
+    return tot
+
+
+def time_soap(native, torch, dev, hev, stream, steps, warmup) -> dict:
+    """The SOAP owner step (Section 5.7) on the GPT-2-small share's 12 matrices, fp32 math, bases
+    starting at the identity and statistics at zero (the cost does not depend on the values)."""
+    import synth
+    wl = synth.workload(2)
+    shapes = [(e.m, e.n) for e in wl.muon]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3)
+    keep, ents = [], []
+    for m, n in shapes:
+        t = ((torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
+             (torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
+             torch.zeros(m, n, device=dev), torch.zeros(m, n, device=dev),
+             torch.zeros(m, m, device=dev), torch.zeros(n, n, device=dev),
+             torch.eye(m, device=dev), torch.eye(n, device=dev))
+        keep.append(t)
+        ents.append(native.soap_entry_t(*t))
+    out = {"workload": wl.name + " (12 matrices: 8 x 768x768, 2 x 3072x768, 2 x 768x3072)",
+           "dtype": "f32", "betas": [0.95, 0.95], "shampoo_beta": 0.95}
+    step_no = 1
+    for refresh in (True, False):
+        hp = native.soap_hparams(lr=3e-3, weight_decay=0.01, refresh=refresh, refresh_iters=1)
+        ws = native.soap_workspace_t(ents, hp, device=dev)
+
+        def one():
+            nonlocal step_no
+            hp.step = step_no
+            native.soap_step_t(ents, hp, ws)
+            step_no += 1
+        for _ in range(warmup):
+            one()
+        torch.cuda.synchronize()
+        a, b = hev.create(), hev.create()
+        hev.record(a, stream)
+        for _ in range(steps):
+            one()
+        hev.record(b, stream)
+        torch.cuda.synchronize()
+        ms = hev.elapsed_ms(a, b) / steps
+        fl = soap_nominal_flop(shapes, 1, refresh)
+        key = "refresh" if refresh else "no_refresh"
+        out[key] = {"ms_per_step": round(ms, 4), "nominal_flop_per_step": fl,
+                    "nominal_tflops": round(fl / (ms * 1e-3) / 1e12, 2),
+                    "frac_fp32_mfma_peak": round(fl / (ms * 1e-3) / 1e12 / PEAK_F32_MFMA_TFLOPS, 4),
+                    "workspace_gib": round(ws.numel() / 2 ** 30, 3)}
+        log(f"soap ({key}): {ms:.3f} ms per step, {fl / (ms * 1e-3) / 1e12:.1f} nominal TFLOP/s")
+        del ws
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -345,6 +409,7 @@ def main() -> int:
     ap.add_argument("--no-shampoo", action="store_true",
                     help="skip timing the Shampoo owner step (fp32 MFMA) on the GPT-2-small share")
     ap.add_argument("--shampoo", action="store_true", help=argparse.SUPPRESS)  # (the default)
+    ap.add_argument("--no-soap", action="store_true", help="skip the SOAP owner-step timing")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -522,6 +587,8 @@ def main() -> int:
         # nominal_flop counts every product of all root iterations in full; iterations skipped
         # after convergence and the upper-tile-only symmetric products execute less
         out["shampoo"] = time_shampoo(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
+    if not args.no_soap:
+        out["soap"] = time_soap(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])

@@ -1,9 +1,10 @@
 """torch.optim front ends of the owner-local step.
 
-`OwnerMuon` and `OwnerShampoo` take the parameters a rank owns (whole tensors, as owner placement
-gives them). Each step makes one grouped library call per parameter group for the 2D matrices
-(Muon or Shampoo) and one for the remaining tensors (AdamW), on torch's current stream. Optimizer
-state (fp32 momentum, Shampoo statistics and preconditioners, AdamW moments) lives in
+`OwnerMuon`, `OwnerShampoo` and `OwnerSOAP` take the parameters a rank owns (whole tensors, as owner
+placement gives them). Each step makes one grouped library call per parameter group for the 2D
+matrices (Muon, Shampoo or SOAP) and one for the remaining tensors (AdamW), on torch's current
+stream. Optimizer state (fp32 momentum, Shampoo statistics and preconditioners, SOAP moments and
+bases, AdamW moments) lives in
 `self.state` like torch's own optimizers, so `state_dict()` / `load_state_dict()` work unchanged.
 These classes only marshal arguments: every arithmetic step runs in libmfsdp.so, and there is no
 CPU path (CUDA tensors are required).
@@ -23,6 +24,10 @@ _MUON_DEFAULTS = dict(lr=1e-3, weight_decay=0.1, momentum=0.95, nesterov=True,
 _SHAMPOO_DEFAULTS = dict(lr=1e-3, weight_decay=0.0, beta=1.0, weight=1.0, eps=1e-12, eps_rel=1e-6,
                          root_iters=20, precondition_frequency=1, adamw_lr=1e-3,
                          adamw_betas=(0.9, 0.999), adamw_eps=1e-8, adamw_weight_decay=0.01)
+
+_SOAP_DEFAULTS = dict(lr=3e-3, weight_decay=0.01, beta1=0.95, beta2=0.95, eps=1e-8, shampoo_beta=0.95,
+                      precondition_frequency=10, refresh_iters=1, adamw_lr=1e-3, adamw_betas=(0.9, 0.999),
+                      adamw_eps=1e-8, adamw_weight_decay=0.01)
 
 
 def _check_tensor(p: torch.Tensor, what: str) -> None:
@@ -192,6 +197,72 @@ class OwnerShampoo(_OwnerOptimizer):
                 ws = self._workspace(gi, "shampoo" + ("+" if refresh else "-"), key,
                                      lambda: native.mfsdp_shampoo_workspace_size(ents, hp), ps[0].device)
                 native.shampoo_step_t(ents, hp, ws)
+            if tails:
+                self._adamw(group, tails)
+        return loss
+
+
+class OwnerSOAP(_OwnerOptimizer):
+    """SOAP on the owned 2D matrices (Adam in the eigenbasis of the Shampoo statistics; the bases
+    start at the identity and are refreshed by a power step + QR after the first step and then
+    every `precondition_frequency` steps) and AdamW on the other tensors. fp32 math on the GPU;
+    matrix sides up to 4096.
+
+    Hyperparameters: lr, weight_decay, beta1, beta2, eps (Adam in the eigenbasis), shampoo_beta
+    (statistics S <- shampoo_beta S + (1 - shampoo_beta) G G^T), precondition_frequency,
+    refresh_iters; adamw_lr, adamw_betas, adamw_eps, adamw_weight_decay.
+    """
+
+    def __init__(self, params, **kw):
+        d = dict(_SOAP_DEFAULTS)
+        unknown = set(kw) - set(d)
+        if unknown:
+            raise TypeError(f"unknown hyperparameters: {sorted(unknown)}")
+        d.update(kw)
+        if int(d["precondition_frequency"]) < 1:
+            raise ValueError("precondition_frequency must be >= 1")
+        super().__init__(params, d)
+
+    @torch.no_grad()
+    def step(self, closure=None):
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for gi, group in enumerate(self.param_groups):
+            mats, tails = self._split(group)
+            # the library takes one step count and one refresh decision per call
+            calls: Dict[Tuple[int, bool], list] = {}
+            for p in mats:
+                if max(p.shape) > native.SOAP_MAX_DIM:
+                    raise ValueError(f"SOAP supports matrix sides up to {native.SOAP_MAX_DIM}, got {tuple(p.shape)}")
+                st = self.state[p]
+                if "QL" not in st:
+                    m, n = p.shape
+                    st["exp_avg"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
+                    st["exp_avg_sq"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
+                    st["L"] = torch.zeros((m, m), dtype=torch.float32, device=p.device)
+                    st["R"] = torch.zeros((n, n), dtype=torch.float32, device=p.device)
+                    st["QL"] = torch.eye(m, dtype=torch.float32, device=p.device)
+                    st["QR"] = torch.eye(n, dtype=torch.float32, device=p.device)
+                    st["step"] = 0
+                st["step"] += 1
+                t = st["step"]
+                refresh = t == 1 or t % int(group["precondition_frequency"]) == 0
+                calls.setdefault((t, refresh), []).append(p)
+            for (t, refresh), ps in calls.items():
+                ents = [native.soap_entry_t(p, p.grad, self.state[p]["exp_avg"], self.state[p]["exp_avg_sq"],
+                                            self.state[p]["L"], self.state[p]["R"], self.state[p]["QL"],
+                                            self.state[p]["QR"]) for p in ps]
+                beta_s = float(group["shampoo_beta"])
+                hp = native.soap_hparams(lr=group["lr"], weight_decay=group["weight_decay"], beta1=group["beta1"],
+                                         beta2=group["beta2"], eps=group["eps"], shampoo_beta=beta_s,
+                                         shampoo_weight=1.0 - beta_s, step=t, refresh=refresh,
+                                         refresh_iters=group["refresh_iters"])
+                key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh, group["refresh_iters"])
+                ws = self._workspace(gi, "soap" + ("+" if refresh else "-"), key,
+                                     lambda: native.mfsdp_soap_workspace_size(ents, hp), ps[0].device)
+                native.soap_step_t(ents, hp, ws)
             if tails:
                 self._adamw(group, tails)
         return loss

@@ -3,10 +3,10 @@ hyperparameters, before touching the library."""
 import pytest
 import torch
 
-from paper_2607_05895_amd.optim import OwnerMuon, OwnerShampoo
+from paper_2607_05895_amd.optim import OwnerMuon, OwnerShampoo, OwnerSOAP
 
 
-@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo])
+@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo, OwnerSOAP])
 def test_cpu_tensors_are_refused(cls):
     p = torch.zeros(8, 8, requires_grad=True)
     p.grad = torch.ones(8, 8)
@@ -15,12 +15,13 @@ def test_cpu_tensors_are_refused(cls):
         opt.step()
 
 
-@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo])
+@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo, OwnerSOAP])
 def test_unknown_hyperparameters_are_refused(cls):
     with pytest.raises(TypeError, match="unknown"):
         cls([torch.zeros(2, 2, requires_grad=True)], betas=(0.9, 0.99))
 
 
-def test_shampoo_frequency_must_be_positive():
+@pytest.mark.parametrize("cls", [OwnerShampoo, OwnerSOAP])
+def test_refresh_frequency_must_be_positive(cls):
     with pytest.raises(ValueError):
-        OwnerShampoo([torch.zeros(2, 2, requires_grad=True)], precondition_frequency=0)
+        cls([torch.zeros(2, 2, requires_grad=True)], precondition_frequency=0)

@@ -1,12 +1,13 @@
 """The torch.optim front ends (paper_2607_05895_amd.optim) against the fp64 oracle: two steps of a
-small owner share (2D weights on Muon or Shampoo, vectors on AdamW) with state carried by the
-optimizer, and a state_dict round trip. Tolerances as in the kernel parity tests."""
+small owner share (2D weights on Muon, Shampoo or SOAP, vectors on AdamW) with state carried by
+the optimizer, and a state_dict round trip. Tolerances as in the kernel parity tests."""
 import numpy as np
 import pytest
 
 import oracle
 import synth
 from oracle import shampoo as OS
+from oracle import soap as OSP
 from tests.helpers import check_bf16_param, from_dev, rel_fro, to_dev
 
 pytestmark = pytest.mark.gpu
@@ -99,21 +100,82 @@ def test_owner_shampoo_refresh_then_stale_matches_oracle():
         assert check_bf16_param(from_dev(p.detach()), pout, 0.05 * np.linalg.norm(U), tol) <= 1.0, name
 
 
-def test_state_dict_round_trip_continues_identically():
-    from paper_2607_05895_amd.optim import OwnerMuon
+def _well_conditioned_grads(rng, d, k):
+    """k gradients U diag(s) V^T with s in [0.5, 1] 1e-3: square and well conditioned, so every
+    statistic and every refreshed basis is fully determined (float32 resolves it to ~1e-6)."""
+    out = []
+    for _ in range(k):
+        U, _r = np.linalg.qr(rng.standard_normal((d, d)))
+        V, _r = np.linalg.qr(rng.standard_normal((d, d)))
+        g = (U * (1e-3 * rng.uniform(0.5, 1.0, d))) @ V.T
+        out.append(g.astype(np.float32))
+    return out
+
+
+def test_owner_soap_three_steps_match_oracle():
+    """Refresh after step 1 and step 3 (precondition_frequency 3), AdamW on the vectors."""
+    from paper_2607_05895_amd.optim import OwnerSOAP
+    import torch
+    rng = np.random.default_rng(14)
+    model = []
+    for name, d in (("q", 256), ("o", 128)):
+        p = synth.random_muon_tensors(rng, d, d, synth.BF16, synth.BF16).param
+        model.append((name, p, [synth.f32_to_bf16_bits(g) for g in _well_conditioned_grads(rng, d, 3)],
+                      synth.BF16))
+    for name, n in (("ln.w", 256), ("bias", 128)):
+        p = rng.standard_normal(n).astype(np.float32)
+        model.append((name, p, [(rng.standard_normal(n) * 1e-2).astype(np.float32) for _ in range(3)],
+                      synth.F32))
+    ps, grads = _torch_params(model)
+    opt = OwnerSOAP(ps, lr=3e-3, weight_decay=0.01, precondition_frequency=3)
+    for step in range(3):
+        for p, g in zip(ps, grads):
+            p.grad = g[step]
+        opt.step()
+    torch.cuda.synchronize()
+    for (name, p0, gs, dt), p in zip(model, ps):
+        if p0.ndim == 1:
+            pin, m_, v_ = p0, np.zeros_like(p0), np.zeros_like(p0)
+            for step in range(3):
+                pin, m_, v_ = oracle.adamw_step(pin, gs[step], m_, v_, lr=1e-3, beta1=0.9, beta2=0.999,
+                                                eps=1e-8, weight_decay=0.01, step=step + 1)
+                pin = pin.astype(np.float32)
+            assert np.abs(from_dev(p.detach()) - pin).max() <= 1e-6, name
+            continue
+        d = p0.shape[0]
+        M, V, L, R = np.zeros((d, d)), np.zeros((d, d)), np.zeros((d, d)), np.zeros((d, d))
+        QL, QR, pin = np.eye(d), np.eye(d), p0
+        for step in range(3):
+            hp = OSP.SoapHParams(lr=3e-3, weight_decay=0.01, refresh=step in (0, 2))
+            pout, M, V, L, R, QL, QR, N = OSP.soap_step(pin, gs[step], M, V, L, R, QL, QR, step + 1, hp)
+            pin = synth.f32_to_bf16_bits(pout.astype(np.float32))
+        st = opt.state[p]
+        assert st["step"] == 3
+        assert rel_fro(from_dev(st["exp_avg"]), M) <= 1e-5, name
+        assert rel_fro(from_dev(st["L"]), L) <= 1e-5 and rel_fro(from_dev(st["R"]), R) <= 1e-5, name
+        for q, qo in ((from_dev(st["QL"]), QL), (from_dev(st["QR"]), QR)):
+            s_ = np.sign(np.sum(q * qo, axis=0))
+            assert rel_fro(q * s_, qo) <= 1e-4, name
+        assert check_bf16_param(from_dev(p.detach()), pout, 3e-3 * np.linalg.norm(N), 1e-4) <= 1.0, name
+
+
+@pytest.mark.parametrize("which", ["muon", "soap"])
+def test_state_dict_round_trip_continues_identically(which):
+    from paper_2607_05895_amd.optim import OwnerMuon, OwnerSOAP
     import torch
     rng = np.random.default_rng(13)
     model = _model(rng)
+    cls, kw = (OwnerMuon, dict(lr=0.02)) if which == "muon" else (OwnerSOAP, dict(precondition_frequency=2))
     runs = []
     for resume in (False, True):
         ps, grads = _torch_params(model)
-        opt = OwnerMuon(ps, lr=0.02)
+        opt = cls(ps, **kw)
         for p, g in zip(ps, grads):
             p.grad = g[0]
         opt.step()
         if resume:
             sd = opt.state_dict()
-            opt = OwnerMuon(ps, lr=0.02)
+            opt = cls(ps, **kw)
             opt.load_state_dict(sd)
         for p, g in zip(ps, grads):
             p.grad = g[1]
