@@ -42,10 +42,27 @@ __device__ __forceinline__ void unrolled(F&& f) {
   unrolled_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes of a wave (all lanes active), the same value in every lane, in a fixed
+// order: DPP butterflies within each 16-lane row (quad_perm [1,0,3,2], quad_perm [2,3,0,1],
+// row_half_mirror, row_mirror: every lane of a row then holds the row sum; the partners' adds are
+// commutative, so all lanes agree bit for bit), then the four row sums read from lanes 0, 16, 32,
+// 48 and added in that order.
 __device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-  return x;
+  x += dpp<0xB1>(x);
+  x += dpp<0x4E>(x);
+  x += dpp<0x141>(x);
+  x += dpp<0x140>(x);
+  const int xi = __float_as_int(x);
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(xi, 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(xi, 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(xi, 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(xi, 48));
+  return ((r0 + r1) + r2) + r3;
 }
 
 __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __restrict__ descs, int count,
@@ -253,67 +270,107 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
   if (t < kQrPanel * kQrPanel) ((g_f32*)d.T)[t] = Ts[t / kQrPanel][t % kQrPanel];
 }
 
-// X <- X - V (T^T (V^T X)) on one block of 64 columns, all `rows` rows: a first pass forms the 16
-// column sums W = V^T X (4 row groups of one wave each, combined in a fixed order), one wave forms
-// Y = T^T W, a second pass subtracts V Y.
+// X <- X - V (T^T (V^T X)) on one block of 64 columns, all `rows` rows. Thread (q, g) = (t % 16,
+// t / 16) owns the column quad 4q .. 4q + 3 and the rows g, g + 16, ... (16-byte loads and stores).
+// A first pass forms the 16 column sums W = V^T X: per thread, then over the four row groups of a
+// wave (lanes 16 and 32 apart), then over the four waves through LDS, in a fixed order; one wave
+// forms Y = T^T W; a second pass subtracts V Y.
 __global__ __launch_bounds__(256) void qr_apply_kernel(const QrApplyDesc* __restrict__ descs, int count) {
   __shared__ float red[4][kQrPanel][kQrApplyCols];
   __shared__ float ys[kQrPanel][kQrApplyCols];
   const int e = find_desc(descs, count, blockIdx.x);
   const QrApplyDesc& d = descs[e];
   const int lt = blockIdx.x - d.tile_begin;
-  const int t = threadIdx.x, c = t & 63, rg = t >> 6;
-  const int lc = lt * kQrApplyCols + c;
-  const bool live = lc < d.cols;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int q = t & 15, g = t >> 4;
+  const int lc = lt * kQrApplyCols + 4 * q;  // first column of this thread's quad, within [0, cols)
+  const bool live = lc < d.cols, full = lc + 4 <= d.cols;
   g_f32* X = (g_f32*)(d.X) + int64_t(d.row0) * d.ldx + d.c0 + (live ? lc : 0);
   const g_cf32x4* V = (const g_cf32x4*)(d.V);
-  float wk[kQrPanel];
+  auto load4 = [&](int64_t o) -> f32x4 {
+    if (full) return *(const g_cf32x4*)(X + o);
+    f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int k = 0; k < kQrPanel; ++k) wk[k] = 0.0f;
+    for (int j = 0; j < 4; ++j)
+      if (lc + j < d.cols) x[j] = X[o + j];
+    return x;
+  };
+  float wk[4][kQrPanel];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int k = 0; k < kQrPanel; ++k) wk[j][k] = 0.0f;
   if (live) {
-#pragma unroll 4
-    for (int r = rg; r < d.rows; r += 4) {
-      const float x = X[int64_t(r) * d.ldx];
+#pragma unroll 2
+    for (int r = g; r < d.rows; r += 16) {
+      const f32x4 x = load4(int64_t(r) * d.ldx);
 #pragma unroll
-      for (int q = 0; q < kQrPanel / 4; ++q) {
-        const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + q];
+      for (int qq = 0; qq < kQrPanel / 4; ++qq) {
+        const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + qq];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) wk[4 * q + j] += v[j] * x;
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) wk[j][4 * qq + i] += v[i] * x[j];
       }
     }
   }
+  // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns (row groups 4w .. 4w + 3)
 #pragma unroll
-  for (int k = 0; k < kQrPanel; ++k) red[rg][k][c] = wk[k];
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int k = 0; k < kQrPanel; ++k) {
+      float v = wk[j][k];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      wk[j][k] = v;
+    }
+  if (lane < 16) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int k = 0; k < kQrPanel; ++k) red[w][k][4 * q + j] = wk[j][k];
+  }
   __syncthreads();
-  if (rg == 0) {
+  if (t < kQrApplyCols) {
     const g_cf32* T = (const g_cf32*)(d.T);
     float W[kQrPanel];
 #pragma unroll
-    for (int k = 0; k < kQrPanel; ++k) W[k] = ((red[0][k][c] + red[1][k][c]) + red[2][k][c]) + red[3][k][c];
+    for (int k = 0; k < kQrPanel; ++k) W[k] = ((red[0][k][t] + red[1][k][t]) + red[2][k][t]) + red[3][k][t];
 #pragma unroll
     for (int i = 0; i < kQrPanel; ++i) {
       float y = 0.0f;
 #pragma unroll
       for (int k = 0; k <= i; ++k) y += T[k * kQrPanel + i] * W[k];
-      ys[i][c] = y;
+      ys[i][t] = y;
     }
   }
   __syncthreads();
   if (!live) return;
-  float y[kQrPanel];
+  float y[4][kQrPanel];
 #pragma unroll
-  for (int k = 0; k < kQrPanel; ++k) y[k] = ys[k][c];
-#pragma unroll 4
-  for (int r = rg; r < d.rows; r += 4) {
-    float s = 0.0f;
+  for (int j = 0; j < 4; ++j)
 #pragma unroll
-    for (int q = 0; q < kQrPanel / 4; ++q) {
-      const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + q];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) s += v[j] * y[4 * q + j];
-    }
+    for (int k = 0; k < kQrPanel; ++k) y[j][k] = ys[k][4 * q + j];
+#pragma unroll 2
+  for (int r = g; r < d.rows; r += 16) {
     const int64_t o = int64_t(r) * d.ldx;
-    X[o] = X[o] - s;
+    f32x4 x = load4(o);
+    f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int qq = 0; qq < kQrPanel / 4; ++qq) {
+      const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + qq];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) s[j] += v[i] * y[j][4 * qq + i];
+    }
+    if (full) {
+      *(g_f32x4*)(X + o) = x - s;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (lc + j < d.cols) X[o + j] = x[j] - s[j];
+    }
   }
 }
 
