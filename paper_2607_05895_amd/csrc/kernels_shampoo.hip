@@ -41,6 +41,31 @@ __device__ __forceinline__ int op_slot(int r, int chunk) {
   return r * 8 + (chunk ^ ((r & 7) ^ ((r >> 3) & 1)));
 }
 
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Exact three-way split of eight fp32 values into bf16 parts, x = hi + mid + lo: hi is x rounded
+// to bf16 (nearest even), mid the rounded remainder, lo the rounded second remainder. Each
+// remainder is exact in fp32 (it is x's lower bits), so only lo rounds, at about 2^-25 |x|.
+__device__ __forceinline__ void split3(const f32x4& x0, const f32x4& x1, bf16x8_t& hi, bf16x8_t& mid,
+                                       bf16x8_t& lo) {
+  float r[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+  u32x4 ph, pm, pl;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t h = pack_bf16x2(r[2 * j], r[2 * j + 1]);
+    ph[j] = h;
+    const float a = r[2 * j] - __uint_as_float(h << 16);
+    const float b = r[2 * j + 1] - __uint_as_float(h & 0xffff0000u);
+    const uint32_t m = pack_bf16x2(a, b);
+    pm[j] = m;
+    pl[j] = pack_bf16x2(a - __uint_as_float(m << 16), b - __uint_as_float(m & 0xffff0000u));
+  }
+  hi = __builtin_bit_cast(bf16x8_t, ph);
+  mid = __builtin_bit_cast(bf16x8_t, pm);
+  lo = __builtin_bit_cast(bf16x8_t, pl);
+}
+
 // C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup.
 // 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of v_mfma_f32_32x32x2f32. K steps of
 // 32, double-buffered in LDS with the next step's global loads in registers during the current
@@ -48,6 +73,12 @@ __device__ __forceinline__ int op_slot(int r, int chunk) {
 // instruction q within group g takes k = 8g + 4h + q), so each lane reads its operands as 16-byte
 // vectors. Symmetric problems compute the upper tiles only and store each tile transposed as well,
 // through LDS, with coalesced row stores.
+// SPLIT: the products run on the bf16 MFMA instead (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
+// each lane takes 8 consecutive k of its row from the same LDS tiles, splits them exactly into
+// hi + mid + lo bf16 parts, and accumulates the six partial products above 2^-24 relative
+// (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo, lo.mid, lo.lo are below
+// 2^-32). Six bf16 MFMAs per 16 k cost 192 cycles against 512 for the fp32 MFMA, at fp32 accuracy.
+template <bool SPLIT>
 __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs,
                                                          int count) {
   __shared__ f32x4 lds[2][2][kShTile * 8];  // [stage][P, Q][slot]: 64 KiB
@@ -120,20 +151,52 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
   for (int kt = 0; kt < nk; ++kt) {
     const int s = kt & 1;
     if (kt + 1 < nk) gload((kt + 1) * 32);
+    if constexpr (SPLIT) {
+      // lane half fh of 16-k group g takes k = 16 g + 8 fh .. + 7: chunks 4 g + 2 fh and + 1
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      f32x4 a[2], b[2];
+      for (int g = 0; g < 2; ++g) {
+        bf16x8_t ah[2], am[2], al[2], bh[2], bm[2], bl[2];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = lds[s][0][op_slot(wr * 64 + i * 32 + fr, 2 * g + fh)];
+        for (int i = 0; i < 2; ++i) {
+          const int r = wr * 64 + i * 32 + fr;
+          split3(lds[s][0][op_slot(r, 4 * g + 2 * fh)], lds[s][0][op_slot(r, 4 * g + 2 * fh + 1)], ah[i], am[i],
+                 al[i]);
+        }
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = lds[s][1][op_slot(wc * 64 + j * 32 + fr, 2 * g + fh)];
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
+        for (int j = 0; j < 2; ++j) {
+          const int r = wc * 64 + j * 32 + fr;
+          split3(lds[s][1][op_slot(r, 4 * g + 2 * fh)], lds[s][1][op_slot(r, 4 * g + 2 * fh + 1)], bh[j], bm[j],
+                 bl[j]);
+        }
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+          for (int j = 0; j < 2; ++j) {
+            f32x16 c = acc[i][j];
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bh[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bl[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bm[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bh[j], c, 0, 0, 0);
+            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bm[j], c, 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bh[j], c, 0, 0, 0);
+          }
+      }
+    } else {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        f32x4 a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = lds[s][0][op_slot(wr * 64 + i * 32 + fr, 2 * g + fh)];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) b[j] = lds[s][1][op_slot(wc * 64 + j * 32 + fr, 2 * g + fh)];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+      }
     }
     if (kt + 1 < nk) lstore(s ^ 1);
     __syncthreads();
@@ -341,7 +404,11 @@ __global__ __launch_bounds__(256) void sh_apply_kernel(const ShApplyDesc* __rest
 
 hipError_t launch_sh_gemm(const ShGemmDesc* d, int count, int total_tiles, hipStream_t st) {
   if (total_tiles <= 0 || count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(sh_gemm_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+#ifdef MFSDP_SH_GEMM_F32
+  hipLaunchKernelGGL(sh_gemm_kernel<false>, dim3(total_tiles), dim3(256), 0, st, d, count);
+#else
+  hipLaunchKernelGGL(sh_gemm_kernel<true>, dim3(total_tiles), dim3(256), 0, st, d, count);
+#endif
   return hipGetLastError();
 }
 
