@@ -42,46 +42,51 @@ __device__ __forceinline__ int op_slot(int r, int chunk) {
 }
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Exact three-way split of eight fp32 values into bf16 parts, x = hi + mid + lo: hi is x rounded
-// to bf16 (nearest even), mid the rounded remainder, lo the rounded second remainder. Each
-// remainder is exact in fp32 (it is x's lower bits), so only lo rounds, at about 2^-25 |x|.
-__device__ __forceinline__ void split3(const f32x4& x0, const f32x4& x1, bf16x8_t& hi, bf16x8_t& mid,
-                                       bf16x8_t& lo) {
-  float r[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-  u32x4 ph, pm, pl;
+// Exact three-way split of four fp32 values into bf16 parts, x = hi + mid + lo (4 bf16 each, packed
+// in two dwords): hi is x rounded to bf16 (nearest even), mid the rounded remainder, lo the rounded
+// second remainder. Each remainder is exact in fp32 (it is x's lower bits), so only lo rounds, at
+// about 2^-25 |x|.
+__device__ __forceinline__ void split3x4(const f32x4& x, u32x2& hi, u32x2& mid, u32x2& lo) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const uint32_t h = pack_bf16x2(r[2 * j], r[2 * j + 1]);
-    ph[j] = h;
-    const float a = r[2 * j] - __uint_as_float(h << 16);
-    const float b = r[2 * j + 1] - __uint_as_float(h & 0xffff0000u);
+  for (int j = 0; j < 2; ++j) {
+    const uint32_t h = pack_bf16x2(x[2 * j], x[2 * j + 1]);
+    hi[j] = h;
+    const float a = x[2 * j] - __uint_as_float(h << 16);
+    const float b = x[2 * j + 1] - __uint_as_float(h & 0xffff0000u);
     const uint32_t m = pack_bf16x2(a, b);
-    pm[j] = m;
-    pl[j] = pack_bf16x2(a - __uint_as_float(m << 16), b - __uint_as_float(m & 0xffff0000u));
+    mid[j] = m;
+    lo[j] = pack_bf16x2(a - __uint_as_float(m << 16), b - __uint_as_float(m & 0xffff0000u));
   }
-  hi = __builtin_bit_cast(bf16x8_t, ph);
-  mid = __builtin_bit_cast(bf16x8_t, pm);
-  lo = __builtin_bit_cast(bf16x8_t, pl);
 }
 
+// 16-byte slot of (row r, k-chunk c) in a split operand plane (rows of 16 bf16 = two 16-byte
+// chunks): c ^ ((r >> 3) & 1), so that 16 consecutive rows at one chunk (a quarter wave's fragment
+// reads) fall in 16 distinct 16-byte bank groups, and a wave's 8-byte stores (4 lanes per row) in 32.
+__device__ __forceinline__ int split_slot(int r, int c) { return r * 2 + (c ^ ((r >> 3) & 1)); }
+
 // C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup.
-// 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of v_mfma_f32_32x32x2f32. K steps of
-// 32, double-buffered in LDS with the next step's global loads in registers during the current
-// step's MFMAs. The K index inside a step is permuted identically on both operands (lane half h of
-// instruction q within group g takes k = 8g + 4h + q), so each lane reads its operands as 16-byte
-// vectors. Symmetric problems compute the upper tiles only and store each tile transposed as well,
-// through LDS, with coalesced row stores.
-// SPLIT: the products run on the bf16 MFMA instead (v_mfma_f32_32x32x16_bf16, fp32 accumulation):
-// each lane takes 8 consecutive k of its row from the same LDS tiles, splits them exactly into
-// hi + mid + lo bf16 parts, and accumulates the six partial products above 2^-24 relative
-// (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo, lo.mid, lo.lo are below
-// 2^-32). Six bf16 MFMAs per 16 k cost 192 cycles against 512 for the fp32 MFMA, at fp32 accuracy.
+// 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The next K step's
+// global loads are held in registers during the current step's products (LDS double buffer).
+// SPLIT (the default): the products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32
+// accumulation) at fp32 accuracy. K steps of 16; when a step is staged into LDS every element is
+// split once into hi + mid + lo bf16 parts (three planes per operand, 24 KiB per stage); a lane's
+// fragment is 8 consecutive k of one row from each plane, and the six partial products above 2^-24
+// relative are accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo,
+// lo.mid, lo.lo are below 2^-32). Six bf16 MFMAs per 16 k take 192 cycles against 512 for the fp32
+// MFMA. 48 KiB of LDS lets three workgroups share a CU.
+// !SPLIT: v_mfma_f32_32x32x2f32 on fp32 tiles, K steps of 32 (64 KiB of LDS, two per CU); the K
+// index inside a step is permuted identically on both operands (lane half h of instruction q within
+// group g takes k = 8g + 4h + q), so each lane reads its operands as 16-byte vectors.
+// Symmetric problems compute the upper tiles only and store each tile transposed as well, through
+// LDS, with coalesced row stores.
 template <bool SPLIT>
-__global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs,
-                                                         int count) {
-  __shared__ f32x4 lds[2][2][kShTile * 8];  // [stage][P, Q][slot]: 64 KiB
+__global__ __launch_bounds__(256, SPLIT ? 3 : 2) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs,
+                                                                      int count) {
+  constexpr int kPlane = kShTile * 32;                        // bytes of one split plane (128 x 16 bf16)
+  constexpr int kStage = SPLIT ? 6 * kPlane : 2 * kShTile * 128;  // both operands of one K step
+  __shared__ __attribute__((aligned(16))) uint8_t lds_raw[2 * kStage];
   const int e = find_desc(descs, count, blockIdx.x);
   const ShGemmDesc& d = descs[e];
   int lt = blockIdx.x - d.tile_begin;
@@ -120,68 +125,102 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
   }
   const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
   const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
-  const int lrow = t >> 3, lch = t & 7;
-  f32x4 ra[4], rb[4];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = lrow + 32 * j;
-      ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
-      rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
-    }
-  };
-  auto lstore = [&](int s) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int slot = op_slot(lrow + 32 * j, lch);
-      lds[s][0][slot] = ra[j];
-      lds[s][1][slot] = rb[j];
-    }
-  };
   f32x16 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  const int nk = d.K / 32;
   const int fr = lane & 31, fh = lane >> 5;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    const int s = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * 32);
-    if constexpr (SPLIT) {
-      // lane half fh of 16-k group g takes k = 16 g + 8 fh .. + 7: chunks 4 g + 2 fh and + 1
+  if constexpr (SPLIT) {
+    // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
+    const int lrow = t >> 2, lch = t & 3;
+    f32x4 ra[2], rb[2];
+    auto gload = [&](int k0) {
 #pragma unroll
-      for (int g = 0; g < 2; ++g) {
-        bf16x8_t ah[2], am[2], al[2], bh[2], bm[2], bl[2];
+      for (int j = 0; j < 2; ++j) {
+        const int r = lrow + 64 * j;
+        ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
+        rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
+      }
+    };
+    // plane (operand o, part p) of stage s; the 8-byte piece of row r holding k 4 lch .. + 3
+    auto lstore = [&](int s) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-          const int r = wr * 64 + i * 32 + fr;
-          split3(lds[s][0][op_slot(r, 4 * g + 2 * fh)], lds[s][0][op_slot(r, 4 * g + 2 * fh + 1)], ah[i], am[i],
-                 al[i]);
+      for (int j = 0; j < 2; ++j) {
+        const int r = lrow + 64 * j;
+        const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
+        u32x2 h, m, l;
+        split3x4(ra[j], h, m, l);
+        uint8_t* base = lds_raw + s * kStage;
+        *reinterpret_cast<u32x2*>(base + 0 * kPlane + off) = h;
+        *reinterpret_cast<u32x2*>(base + 1 * kPlane + off) = m;
+        *reinterpret_cast<u32x2*>(base + 2 * kPlane + off) = l;
+        split3x4(rb[j], h, m, l);
+        *reinterpret_cast<u32x2*>(base + 3 * kPlane + off) = h;
+        *reinterpret_cast<u32x2*>(base + 4 * kPlane + off) = m;
+        *reinterpret_cast<u32x2*>(base + 5 * kPlane + off) = l;
+      }
+    };
+    auto frag = [&](int s, int plane, int r) {
+      return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kStage + plane * kPlane + split_slot(r, fh) * 16);
+    };
+    const int nk = d.K / 16;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int s = kt & 1;
+      if (kt + 1 < nk) gload((kt + 1) * 16);
+      // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid,
+      // hi.hi) term by term over the four blocks, so that consecutive MFMAs use different
+      // accumulators
+      bf16x8_t af[2][3], bf[2][3];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int pt = 0; pt < 3; ++pt) {
+          af[i][pt] = frag(s, pt, wr * 64 + i * 32 + fr);
+          bf[i][pt] = frag(s, 3 + pt, wc * 64 + i * 32 + fr);
         }
+      constexpr int kTerm[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int r = wc * 64 + j * 32 + fr;
-          split3(lds[s][1][op_slot(r, 4 * g + 2 * fh)], lds[s][1][op_slot(r, 4 * g + 2 * fh + 1)], bh[j], bm[j],
-                 bl[j]);
-        }
+      for (int tm = 0; tm < 6; ++tm)
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            f32x16 c = acc[i][j];
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(al[i], bh[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bl[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bm[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(am[i], bh[j], c, 0, 0, 0);
-            c = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bm[j], c, 0, 0, 0);
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ah[i], bh[j], c, 0, 0, 0);
-          }
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]], acc[i][j],
+                                                                0, 0, 0);
+      if (kt + 1 < nk) lstore(s ^ 1);
+      __syncthreads();
+    }
+  } else {
+    f32x4(*lds)[2][kShTile * 8] = reinterpret_cast<f32x4(*)[2][kShTile * 8]>(lds_raw);
+    const int lrow = t >> 3, lch = t & 7;
+    f32x4 ra[4], rb[4];
+    auto gload = [&](int k0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = lrow + 32 * j;
+        ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
+        rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
       }
-    } else {
+    };
+    auto lstore = [&](int s) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int slot = op_slot(lrow + 32 * j, lch);
+        lds[s][0][slot] = ra[j];
+        lds[s][1][slot] = rb[j];
+      }
+    };
+    const int nk = d.K / 32;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int s = kt & 1;
+      if (kt + 1 < nk) gload((kt + 1) * 32);
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         f32x4 a[2], b[2];
@@ -197,21 +236,21 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
             for (int j = 0; j < 2; ++j)
               acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
       }
+      if (kt + 1 < nk) lstore(s ^ 1);
+      __syncthreads();
     }
-    if (kt + 1 < nk) lstore(s ^ 1);
-    __syncthreads();
   }
 
   // Epilogue. Accumulator element v of block (i, j) is C row 8 (v / 4) + 4 h + v % 4, column
   // lane % 32 of that 32 x 32 block (h = lane / 32). E may alias C: each element is read and then
-  // written by the same thread. Symmetric problems are stored exactly symmetric: an upper tile is
-  // also stored transposed, and a diagonal tile keeps its upper triangle and mirrors it into the
-  // lower one (in floating point the two triangles of a product of two different symmetric
-  // matrices differ; kept, that antisymmetric part is amplified by the NT form of the iteration).
+  // written by the same thread; the final values stay in acc for the transposed stores.
+  // Symmetric problems are stored exactly symmetric: an upper tile is also stored transposed, and a
+  // diagonal tile keeps its upper triangle and mirrors it into the lower one (in floating point the
+  // two triangles of a product of two different symmetric matrices differ; kept, that
+  // antisymmetric part is amplified by the NT form of the iteration).
   g_f32* C = (g_f32*)(d.C);
   const g_cf32* E = (const g_cf32*)(d.E);
   const bool diag_tile = d.sym && bi == bj;
-  float* tl = reinterpret_cast<float*>(&lds[0][0][0]);  // 128 x 128 floats, element (r, c) at r*128 + (c ^ r)
   const int64_t r0 = int64_t(bi) * kShTile, c0 = int64_t(bj) * kShTile;
   float res = 0.0f;  // max |C - I| over this thread's elements of the real block
 #pragma unroll
@@ -228,7 +267,7 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
         if (E) x += d.beta * E[gr * d.lde + gc];
         if (gr == gc) x += d.diag;
         C[gr * d.ldc + gc] = x;
-        if (d.sym) tl[r * kShTile + (c ^ r)] = x;
+        acc[i][j][v] = x;
         if (gr < d.valid && gc < d.valid) {
           const float dv = fabsf(x - (gr == gc ? 1.0f : 0.0f));
           res = (dv > res || dv != dv) ? dv : res;  // keeps a NaN
@@ -242,15 +281,31 @@ __global__ __launch_bounds__(256, 2) void sh_gemm_kernel(const ShGemmDesc* __res
     if (lane == 0) atomicMax(reinterpret_cast<unsigned int*>(d.resid_out), rb);
   }
   if (d.sym) {
-    __syncthreads();
-#pragma unroll 4
-    for (int it = 0; it < 32; ++it) {
-      const int c = (t >> 6) + 4 * it;
+    // two passes over the tile's row halves (the waves with wr = h own rows 64 h .. 64 h + 63),
+    // each through a 64 x 128 LDS tile (32 KiB): element (rl, c) at rl * 128 + (c ^ rl)
+    float* tl = reinterpret_cast<float*>(lds_raw);
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int r = lane + 64 * h;
+    for (int h = 0; h < 2; ++h) {
+      if (h == 1) __syncthreads();  // the first half's transposed reads are done
+      if (wr == h) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+              const int rl = i * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+              const int c = wc * 64 + j * 32 + fr;
+              tl[rl * kShTile + (c ^ rl)] = acc[i][j][v];
+            }
+      }
+      __syncthreads();
+      const int r = 64 * h + lane;
+#pragma unroll 4
+      for (int it = 0; it < 32; ++it) {
+        const int c = (t >> 6) + 4 * it;
         // position (c, r) of the tile's transpose; on a diagonal tile only below the diagonal
-        if (!diag_tile || c > r) C[(c0 + c) * d.ldc + r0 + r] = tl[r * kShTile + (c ^ r)];
+        if (!diag_tile || c > r) C[(c0 + c) * d.ldc + r0 + r] = tl[lane * kShTile + (c ^ lane)];
       }
     }
   }
