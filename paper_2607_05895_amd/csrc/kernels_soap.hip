@@ -65,6 +65,35 @@ __device__ __forceinline__ float wave_sum(float x) {
   return ((r0 + r1) + r2) + r3;
 }
 
+// Reduce-scatter of 16 values over the 16 lanes of a DPP row (all lanes active): afterwards lane l
+// of each row holds that row's sum of value l (l = lane mod 16). Four exchange rounds with the lane
+// at distance 1, 2, 4 and 8 (quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_shl/row_shr 4,
+// row_ror 8): each lane keeps the half of its values whose index bit matches its own lane bit and
+// adds the partner's copy of them; every sum is formed by exactly one lane, in a fixed order.
+__device__ __forceinline__ float row_reduce_scatter16(const float (&v)[16], int l16) {
+  const bool b0 = l16 & 1, b1 = (l16 >> 1) & 1, b2 = (l16 >> 2) & 1, b3 = (l16 >> 3) & 1;
+  float s1[8], s2[4], s3[2];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float keep = b0 ? v[2 * j + 1] : v[2 * j], send = b0 ? v[2 * j] : v[2 * j + 1];
+    s1[j] = keep + dpp<0xB1>(send);
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float keep = b1 ? s1[2 * j + 1] : s1[2 * j], send = b1 ? s1[2 * j] : s1[2 * j + 1];
+    s2[j] = keep + dpp<0x4E>(send);
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const float keep = b2 ? s2[2 * j + 1] : s2[2 * j], send = b2 ? s2[2 * j] : s2[2 * j + 1];
+    const float from_up = dpp<0x104>(send);    // row_shl 4: lane l reads lane l + 4
+    const float from_down = dpp<0x114>(send);  // row_shr 4: lane l reads lane l - 4
+    s3[j] = keep + (b2 ? from_down : from_up);
+  }
+  const float keep = b3 ? s3[1] : s3[0], send = b3 ? s3[0] : s3[1];
+  return keep + dpp<0x128>(send);  // row_ror 8: lane l reads lane l ^ 8
+}
+
 __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __restrict__ descs, int count,
                                                         float beta1) {
   __shared__ float tg[kTile][kTile + 1];
@@ -220,16 +249,25 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
       a[i][k] = lr > k ? a[i][k] * scale : (lr == k ? 1.0f : 0.0f);
     }
     // slot s < k: v_s . v_k (for T); slot s >= k: v_k . a_{s+1} (to update column s + 1)
+    {
+      float part[kQrPanel];
 #pragma unroll
-    for (int sl = 0; sl < kQrPanel - 1; ++sl) {
-      const int col = sl < k ? sl : sl + 1;
-      float acc = 0.0f;
-      if (col < jb) {
+      for (int sl = 0; sl < kQrPanel - 1; ++sl) {
+        const int col = sl < k ? sl : sl + 1;
+        float acc = 0.0f;
+        if (col < jb) {
 #pragma unroll
-        for (int i = 0; i < kQrRowsPerThread; ++i) acc += a[i][k] * a[i][col];
+          for (int i = 0; i < kQrRowsPerThread; ++i) acc += a[i][k] * a[i][col];
+        }
+        part[sl] = acc;
       }
-      acc = wave_sum(acc);
-      if (lane == 0) red2[w][sl] = acc;
+      part[kQrPanel - 1] = 0.0f;
+      // lane l of every row: the row's sum of slot l; then over the four rows of the wave (the
+      // adds are commutative pairs, so every lane of a column l agrees bit for bit)
+      float r = row_reduce_scatter16(part, lane & 15);
+      r += __shfl_xor(r, 16);
+      r += __shfl_xor(r, 32);
+      if (lane < kQrPanel - 1) red2[w][lane] = r;
     }
     __syncthreads();
     auto total = [&](int sl) {
@@ -301,7 +339,7 @@ __global__ __launch_bounds__(256) void qr_apply_kernel(const QrApplyDesc* __rest
 #pragma unroll
     for (int k = 0; k < kQrPanel; ++k) wk[j][k] = 0.0f;
   if (live) {
-#pragma unroll 2
+#pragma unroll 4
     for (int r = g; r < d.rows; r += 16) {
       const f32x4 x = load4(int64_t(r) * d.ldx);
 #pragma unroll
@@ -351,7 +389,7 @@ __global__ __launch_bounds__(256) void qr_apply_kernel(const QrApplyDesc* __rest
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int k = 0; k < kQrPanel; ++k) y[j][k] = ys[k][4 * q + j];
-#pragma unroll 2
+#pragma unroll 4
   for (int r = g; r < d.rows; r += 16) {
     const int64_t o = int64_t(r) * d.ldx;
     f32x4 x = load4(o);
