@@ -218,6 +218,9 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
     }
   }
   if (t < kQrPanel * kQrPanel) Ts[t / kQrPanel][t % kQrPanel] = 0.0f;
+  // register rows that hold panel rows (uniform); the others are zero and are skipped. Columns
+  // >= jb are zero as well: their dot products are exactly 0 and they stay 0.
+  const int used = (d.rows + kQrPanelThreads - 1) / kQrPanelThreads;
 
   unrolled<kQrPanel>([&](auto kc) {
     constexpr int k = decltype(kc)::value;
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
 #pragma unroll
     for (int i = 0; i < kQrRowsPerThread; ++i) {
       const int lr = t + kQrPanelThreads * i;
-      if (lr > k) s += a[i][k] * a[i][k];
+      if (i < used && lr > k) s += a[i][k] * a[i][k];
     }
     s = wave_sum(s);
     if (lane == 0) red1[w] = s;
@@ -245,23 +248,24 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
     }
 #pragma unroll
     for (int i = 0; i < kQrRowsPerThread; ++i) {
-      const int lr = t + kQrPanelThreads * i;
-      a[i][k] = lr > k ? a[i][k] * scale : (lr == k ? 1.0f : 0.0f);
+      if (i < used) {
+        const int lr = t + kQrPanelThreads * i;
+        a[i][k] = lr > k ? a[i][k] * scale : (lr == k ? 1.0f : 0.0f);
+      }
     }
     // slot s < k: v_s . v_k (for T); slot s >= k: v_k . a_{s+1} (to update column s + 1)
     {
       float part[kQrPanel];
 #pragma unroll
-      for (int sl = 0; sl < kQrPanel - 1; ++sl) {
-        const int col = sl < k ? sl : sl + 1;
-        float acc = 0.0f;
-        if (col < jb) {
+      for (int sl = 0; sl < kQrPanel; ++sl) part[sl] = 0.0f;
 #pragma unroll
-          for (int i = 0; i < kQrRowsPerThread; ++i) acc += a[i][k] * a[i][col];
+      for (int i = 0; i < kQrRowsPerThread; ++i) {
+        if (i < used) {
+          const float vk = a[i][k];
+#pragma unroll
+          for (int sl = 0; sl < kQrPanel - 1; ++sl) part[sl] += vk * a[i][sl < k ? sl : sl + 1];
         }
-        part[sl] = acc;
       }
-      part[kQrPanel - 1] = 0.0f;
       // lane l of every row: the row's sum of slot l; then over the four rows of the wave (the
       // adds are commutative pairs, so every lane of a column l agrees bit for bit)
       float r = row_reduce_scatter16(part, lane & 15);
@@ -276,12 +280,14 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
       for (int j = 0; j < kQrPanelThreads / 64; ++j) acc += red2[j][sl];
       return acc;
     };
+    float f[kQrPanel];
 #pragma unroll
-    for (int l = k + 1; l < kQrPanel; ++l) {
-      if (l < jb) {
-        const float f = tau * total(l - 1);
+    for (int l = k + 1; l < kQrPanel; ++l) f[l] = tau * total(l - 1);
 #pragma unroll
-        for (int i = 0; i < kQrRowsPerThread; ++i) a[i][l] -= f * a[i][k];
+    for (int i = 0; i < kQrRowsPerThread; ++i) {
+      if (i < used) {
+#pragma unroll
+        for (int l = k + 1; l < kQrPanel; ++l) a[i][l] -= f[l] * a[i][k];
       }
     }
     if (t < k) {
