@@ -84,6 +84,25 @@ def _to_dev(arr, dtype, torch, dev):
     return torch.from_numpy(arr).to(dev)
 
 
+def device_info(torch) -> dict:
+    """The device the numbers come from: name, architecture and CU count from the runtime, and the
+    shader clock rocm-smi reports right after the timed region (a child process; null when the tool
+    is not available). Under a long MFMA load the clock settles below its maximum."""
+    import subprocess
+    pr = torch.cuda.get_device_properties(0)
+    info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "compute_units": pr.multi_processor_count,
+            "sclk_after_timing": None}
+    try:
+        res = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
+        for line in res.stdout.splitlines():
+            if "sclk" in line.lower():
+                info["sclk_after_timing"] = line.split(":", 2)[-1].strip()
+                break
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return info
+
+
 def cpu_baseline(wl, sample_idx, pool) -> dict:
     """Time the fp64 oracle on a bounded sample of the share (host cores)."""
     import numpy as np
@@ -566,6 +585,7 @@ def main() -> int:
         },
         "step_ms_stats": {"median": round(step_ms[len(step_ms) // 2], 4), "min": round(step_ms[0], 4),
                           "max": round(step_ms[-1], 4)},
+        "device": device_info(torch),
         # (nominal NS flop / MFMA peak + algorithmic elementwise bytes / HBM peak) / step time
         "step_roofline_frac": round((flops / (peak * 1e12) + (alg_bytes + adamw_bytes) / (PEAK_HBM_GBS * 1e9))
                                     / (ms_per_step * 1e-3), 4),
