@@ -1,7 +1,7 @@
 // Descriptors and launchers of the Shampoo owner step (fp32 throughout).
 //
 // Every matrix the step works on lives in the workspace as a zero-padded row-major fp32 buffer
-// whose row and column counts are multiples of kShTile (128), so the fp32 MFMA GEMM needs no edge
+// whose row and column counts are multiples of kShTile (128), so the GEMM needs no edge
 // handling. Caller buffers (gradient, parameter, statistics, preconditioners) keep their natural
 // m x n / m x m / n x n row-major layout; small copy kernels move data across that boundary.
 //
