@@ -251,8 +251,8 @@ size_t mfsdp_shampoo_workspace_size(const mfsdp_shampoo_entry* entries, int64_t 
  * fourth roots (on refresh), U = P_L G P_R, every product at fp32 accuracy on the bf16 MFMA
  * (each fp32 operand split exactly into three bf16 parts, fp32 accumulation), then the parameter
  * update. The workspace (device, 256-byte aligned, >= the size query) must not be in use by
- * another call still running. Returns MFSDP_OK, MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an
- * argument error nothing is enqueued. At most 4096 entries per call. */
+ * another call still running. Returns MFSDP_OK, MFSDP_E_INVALID, MFSDP_E_WORKSPACE or
+ * MFSDP_E_HIP; on an argument error nothing is enqueued. At most 4096 entries per call. */
 int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count,
                        const mfsdp_shampoo_hparams* hp, void* workspace, size_t workspace_bytes,
                        void* stream);
@@ -263,7 +263,8 @@ size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters);
 /* out = (a + rho I)^(-1/p), rho = eps + eps_rel ||a||_F, for a symmetric positive semidefinite
  * d x d fp32 matrix `a` (row-major, device; read only; not checked for symmetry), by `iters`
  * steps of the coupled Newton iteration (Guo and Higham 2006), the iteration the Shampoo step
- * uses (products as there). p in {1, 2, 4}; 1 <= d <= 65536; eps > 0; eps_rel >= 0; 1 <= iters <= 100.
+ * uses (products as there). p in {1, 2, 4}; 1 <= d <= 65536; eps > 0; eps_rel >= 0;
+ * 1 <= iters <= 100.
  * `out` (d x d fp32, device) must not overlap `a`. In fp32 the iteration is stable while rho is
  * at least about 1e-6 ||a||_F; a smaller ridge can diverge. Same stream, workspace and error
  * rules as mfsdp_shampoo_step. */
@@ -335,10 +336,11 @@ size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
 
 /* One SOAP step on every entry (host array of count entries), enqueued on `stream` (hipStream_t,
  * NULL = default stream); no host synchronisation. Every product runs at fp32 accuracy on the
- * bf16 MFMA as in mfsdp_shampoo_step (grouped over the entries); the refresh QR is a blocked Householder factorization (panels of 16 columns).
- * The workspace (device, 256-byte aligned, >= the size query) must not be in use by another call
- * still running. Returns MFSDP_OK, MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an
- * argument error nothing is enqueued. At most 4096 entries per call. */
+ * bf16 MFMA as in mfsdp_shampoo_step (grouped over the entries); the refresh QR is a blocked
+ * Householder factorization (panels of 16 columns). The workspace (device, 256-byte aligned,
+ * >= the size query) must not be in use by another call still running. Returns MFSDP_OK,
+ * MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an argument error nothing is enqueued.
+ * At most 4096 entries per call. */
 int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
                     void* workspace, size_t workspace_bytes, void* stream);
 
