@@ -134,6 +134,48 @@ def cpu_baseline(wl, sample_idx, pool) -> dict:
                       f"{elapsed * wl.ns_flops_nominal() / flops:.0f} s"}
 
 
+def _oracle_threads() -> int:
+    try:
+        import threadpoolctl
+        return max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def cpu_baseline_matrix_opt(which: str, refresh: bool) -> dict:
+    """The fp64 oracle's Shampoo or SOAP step with refresh on the GPT-2-small share, timed on one
+    matrix of each distinct shape and extrapolated to the share by the shape counts (host cores)."""
+    import numpy as np
+    import oracle
+    import synth
+    shapes = [(e.m, e.n) for e in synth.workload(2).muon]
+    counts = {}
+    for sh in shapes:
+        counts[sh] = counts.get(sh, 0) + 1
+    rng = np.random.default_rng(11)
+    total, sample = 0.0, 0.0
+    for (m, n), c in counts.items():
+        g = rng.standard_normal((m, n)) * 0.02
+        p = rng.standard_normal((m, n)) * 0.02
+        t0 = time.perf_counter()
+        if which == "shampoo":
+            oracle.shampoo.shampoo_step(p, g, np.zeros((m, m)), np.zeros((n, n)), None, None,
+                                        oracle.shampoo.ShampooHParams(lr=1e-3, weight_decay=0.01, beta=0.95,
+                                                                      weight=0.05, eps=1e-12, eps_rel=1e-6,
+                                                                      refresh=refresh))
+        else:
+            oracle.soap.soap_step(p, g, np.zeros((m, n)), np.zeros((m, n)), np.zeros((m, m)), np.zeros((n, n)),
+                                  np.eye(m), np.eye(n), 1, oracle.soap.SoapHParams(lr=3e-3, weight_decay=0.01,
+                                                                                  refresh=refresh))
+        dt = time.perf_counter() - t0
+        sample += dt
+        total += c * dt
+    return {"ms_per_step": round(total * 1e3, 1), "cores": _oracle_threads(), "kind": "oracle",
+            "sample": f"fp64 oracle {which} step with refresh on one matrix of each shape "
+                      f"({', '.join(f'{m}x{n}' for (m, n) in counts)}): {sample:.1f} s, extrapolated to "
+                      f"the share's {len(shapes)} matrices by shape counts"}
+
+
 def traffic_record(workload_name: str):
     """HBM traffic of the NS GEMM kernel per launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE runs (scaled by the plain-copy calibration), if they were taken on the current
@@ -620,6 +662,10 @@ def main() -> int:
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])
         log("timing the fp64 oracle on a bounded sample (cpu_baseline)")
         out["cpu_baseline"] = cpu_baseline(wl, sample, pool)
+        for key in ("shampoo", "soap"):
+            if key in out:
+                log(f"timing the fp64 {key} oracle on one matrix of each shape")
+                out[key]["cpu_baseline"] = cpu_baseline_matrix_opt(key, True)
     print(json.dumps(out), flush=True)
     return 0
 
