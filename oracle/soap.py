@@ -28,8 +28,8 @@ Readings (the paper fixes none of them):
   published code starts from a full eigendecomposition instead; ``refresh_iters`` > 1 repeats the
   power step + QR, i.e. runs orthogonal iteration towards the eigenvectors).
 * V is left unchanged when the basis is refreshed, as in the published algorithm.
-* the QR factor is the Householder one with LAPACK's sign convention (numpy.linalg.qr). Column
-  signs of a basis do not change N (each column enters N twice).
+* the QR factor is the Householder one with LAPACK's sign convention (LAPACK's geqrf/orgqr through
+  scipy.linalg.qr). Column signs of a basis do not change N (each column enters N twice).
 """
 from __future__ import annotations
 
@@ -38,6 +38,7 @@ import math
 from typing import Tuple
 
 import numpy as np
+import scipy.linalg
 
 from .muon import _f64
 from .shampoo import update_statistics
@@ -57,8 +58,9 @@ class SoapHParams:
 
 
 def orthonormal_factor(A: np.ndarray) -> np.ndarray:
-    """Q of the Householder QR decomposition A = Q R (square A; numpy.linalg.qr, LAPACK signs)."""
-    Q, _ = np.linalg.qr(np.asarray(A, dtype=np.float64))
+    """Q of the Householder QR decomposition A = Q R (square A; LAPACK's geqrf/orgqr with their sign
+    convention, as numpy.linalg.qr, through scipy.linalg.qr)."""
+    Q, _ = scipy.linalg.qr(np.asarray(A, dtype=np.float64), mode="economic", check_finite=False)
     return Q
 
 

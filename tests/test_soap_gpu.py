@@ -22,6 +22,7 @@ import sys
 
 import numpy as np
 import pytest
+import scipy.linalg
 
 import synth
 from oracle import soap as OS
@@ -53,7 +54,7 @@ def _sync():
 
 
 def _orth(rng, d):
-    q, r = np.linalg.qr(rng.standard_normal((d, d)))
+    q, r = scipy.linalg.qr(rng.standard_normal((d, d)), check_finite=False)
     return q * np.sign(np.diag(r))
 
 
@@ -106,6 +107,24 @@ def test_orthonormal_factor_rank_deficient_and_signs(native):
     native.orthonormal_factor_t(to_dev(a, synth.F32), q)
     _sync()
     assert rel_fro(from_dev(q), OS.orthonormal_factor(a.astype(np.float64))) <= Q_TOL
+
+
+def test_orthonormal_factor_at_the_largest_side(native):
+    """d = 4096, the largest side: every thread of the panel kernel holds 8 rows of the first panel."""
+    import torch
+    _say("orthonormal factor d=4096")
+    d = 4096
+    rng = np.random.default_rng(4096)
+    A = rng.standard_normal((d, d)) + 0.5 * d ** 0.5 * np.eye(d)   # well conditioned
+    a = A.astype(np.float32)
+    q = torch.empty((d, d), dtype=torch.float32, device="cuda")
+    native.orthonormal_factor_t(to_dev(a, synth.F32), q)
+    _sync()
+    qg = from_dev(q)
+    ref = OS.orthonormal_factor(a.astype(np.float64))
+    assert _sign_aligned_err(qg, ref) <= Q_TOL
+    d_orth = np.abs(qg.T @ qg - np.eye(d)).max()
+    assert d_orth <= 2e-5, d_orth
 
 
 # ------------------------------------------------------------------ SOAP step
@@ -295,6 +314,19 @@ def test_soap_lr_zero_and_determinism(native):
     for x, o in zip(mats, out1):
         for a, b in zip((x.dN, x.dQL, x.dQR), o):
             assert bool((a == b).all())
+
+
+def test_soap_step_with_a_4096_side(native):
+    """A 64 x 4096 matrix: the right basis is 4096 x 4096 (the largest side), refreshed by the QR."""
+    _say("soap 64x4096")
+    rng = np.random.default_rng(9600)
+    mat = _Mat(rng, 64, 4096, synth.BF16, synth.BF16).device()
+    hpn, hpo, step = _hp(native)
+    ents = [mat.entry(native)]
+    native.soap_step_t(ents, hpn, native.soap_workspace_t(ents, hpn))
+    _sync()
+    _oracle_step(mat, step, hpo)
+    _check(mat, hpo)
 
 
 def test_soap_benchmark_configuration_full_size(native):
