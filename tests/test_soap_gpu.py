@@ -86,6 +86,22 @@ def test_orthonormal_factor_matches_numpy_qr(native, d):
     np.testing.assert_allclose(qg.T @ qg, np.eye(d), atol=2e-5)
 
 
+@pytest.mark.parametrize("d", sorted(int(x) for x in np.random.default_rng(77).integers(2, 1000, 8)))
+def test_orthonormal_factor_random_sizes(native, d):
+    """Seeded random sizes: ragged last panels (d mod 16) and row counts that are not multiples of
+    the 512 panel threads."""
+    import torch
+    _say(f"orthonormal factor random d={d}")
+    rng = np.random.default_rng(200 + d)
+    a = (rng.standard_normal((d, d)) + 0.5 * d ** 0.5 * np.eye(d)).astype(np.float32)
+    q = torch.empty((d, d), dtype=torch.float32, device="cuda")
+    native.orthonormal_factor_t(to_dev(a, synth.F32), q)
+    _sync()
+    qg = from_dev(q)
+    assert _sign_aligned_err(qg, OS.orthonormal_factor(a.astype(np.float64))) <= Q_TOL
+    np.testing.assert_allclose(qg.T @ qg, np.eye(d), atol=2e-5)
+
+
 def test_orthonormal_factor_rank_deficient_and_signs(native):
     """A rank-deficient input still gives an orthogonal factor with Q^T A upper triangular; on a
     full-rank input LAPACK's signs are reproduced (no column flips)."""
@@ -245,6 +261,23 @@ def test_soap_grouped_three_steps_with_refresh_iterations(native):
         for x in mats:
             _oracle_step(x, step, hpo)
             _check(x, hpo)
+
+
+def test_soap_many_entries_in_one_call(native):
+    """24 seeded random shapes (sides 1 .. 300, mixed dtypes) in one call with the refresh: the
+    grouped launches' tile prefixes and the sides' different panel counts."""
+    _say("soap 24 entries")
+    rng = np.random.default_rng(9700)
+    dts = (synth.BF16, synth.F32)
+    mats = [_Mat(rng, int(rng.integers(1, 301)), int(rng.integers(1, 301)), dts[i % 2], dts[(i // 2) % 2]).device()
+            for i in range(24)]
+    hpn, hpo, step = _hp(native)
+    ents = [x.entry(native) for x in mats]
+    native.soap_step_t(ents, hpn, native.soap_workspace_t(ents, hpn))
+    _sync()
+    for x in mats:
+        _oracle_step(x, step, hpo)
+        _check(x, hpo)
 
 
 def test_soap_identity_bases_is_adamw(native):
