@@ -159,27 +159,30 @@ def test_owner_soap_three_steps_match_oracle():
         assert check_bf16_param(from_dev(p.detach()), pout, 3e-3 * np.linalg.norm(N), 1e-4) <= 1.0, name
 
 
-@pytest.mark.parametrize("which", ["muon", "soap"])
+@pytest.mark.parametrize("which", ["muon", "shampoo", "soap"])
 def test_state_dict_round_trip_continues_identically(which):
-    from paper_2607_05895_amd.optim import OwnerMuon, OwnerSOAP
+    """Three steps, the optimizer rebuilt from its state_dict after the first: the parameters end
+    bitwise the same. With precondition_frequency 2 the Shampoo steps after the resume are a stale
+    one (it needs the saved preconditioners) and a refresh; the SOAP ones a refresh and a stale one."""
+    from paper_2607_05895_amd.optim import OwnerMuon, OwnerShampoo, OwnerSOAP
     import torch
     rng = np.random.default_rng(13)
     model = _model(rng)
-    cls, kw = (OwnerMuon, dict(lr=0.02)) if which == "muon" else (OwnerSOAP, dict(precondition_frequency=2))
+    cls, kw = {"muon": (OwnerMuon, dict(lr=0.02)),
+               "shampoo": (OwnerShampoo, dict(precondition_frequency=2)),
+               "soap": (OwnerSOAP, dict(precondition_frequency=2))}[which]
     runs = []
     for resume in (False, True):
         ps, grads = _torch_params(model)
         opt = cls(ps, **kw)
-        for p, g in zip(ps, grads):
-            p.grad = g[0]
-        opt.step()
-        if resume:
-            sd = opt.state_dict()
-            opt = cls(ps, **kw)
-            opt.load_state_dict(sd)
-        for p, g in zip(ps, grads):
-            p.grad = g[1]
-        opt.step()
+        for k in range(3):
+            for p, g in zip(ps, grads):
+                p.grad = g[k % len(g)]
+            opt.step()
+            if resume and k == 0:
+                sd = opt.state_dict()
+                opt = cls(ps, **kw)
+                opt.load_state_dict(sd)
         torch.cuda.synchronize()
         runs.append([p.detach().clone() for p in ps])
     for a, b in zip(*runs):

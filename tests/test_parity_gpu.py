@@ -387,7 +387,7 @@ def _parts(rng, W, m, n, dtype):
             for _ in range(W)]
 
 
-@pytest.mark.parametrize("W", [1, 3, 8])
+@pytest.mark.parametrize("W", [1, 3, 8, 64])
 @pytest.mark.parametrize("gdt", [synth.BF16, synth.F32])
 def test_muon_reduce_matches_oracle(native, W, gdt):
     import torch
