@@ -14,8 +14,8 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run in one process on the GPU machine; on a machine without a GPU they are skipped
-    # rather than failing, so `-m "not gpu"` and a plain run behave the same here.
+    # GPU tests run in one process on an MI355X; on a machine without a GPU they are skipped
+    # rather than failing, so `-m "not gpu"` and a plain run behave the same there.
     try:
         import torch
         has_gpu = torch.cuda.is_available()
