@@ -86,19 +86,21 @@ def _to_dev(arr, dtype, torch, dev):
 
 def device_info(torch) -> dict:
     """The device the numbers come from: name, architecture and CU count from the runtime, and the
-    shader clock rocm-smi reports right after the timed region (a child process; null when the tool
-    is not available). Under a long MFMA load the clock settles below its maximum."""
-    import subprocess
+    shader clock level the driver marks as current right after the timed region (read from the
+    device's sysfs `pp_dpm_sclk`, no child process; null where the file is not readable). Under a long
+    MFMA load the clock settles below its maximum."""
     pr = torch.cuda.get_device_properties(0)
     info = {"name": pr.name, "arch": getattr(pr, "gcnArchName", None), "compute_units": pr.multi_processor_count,
             "sclk_after_timing": None}
     try:
-        res = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20)
-        for line in res.stdout.splitlines():
-            if "sclk" in line.lower():
-                info["sclk_after_timing"] = line.split(":", 2)[-1].strip()
-                break
-    except (OSError, subprocess.SubprocessError):
+        path = (f"/sys/bus/pci/devices/{pr.pci_domain_id:04x}:{pr.pci_bus_id:02x}:"
+                f"{pr.pci_device_id:02x}.0/pp_dpm_sclk")
+        with open(path) as f:
+            for line in f:
+                if line.rstrip().endswith("*"):
+                    info["sclk_after_timing"] = line.rstrip().rstrip("*").strip()
+                    break
+    except (OSError, AttributeError, TypeError, ValueError):
         pass
     return info
 
