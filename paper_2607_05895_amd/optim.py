@@ -35,6 +35,8 @@ def _check_tensor(p: torch.Tensor, what: str) -> None:
         raise ValueError(f"{what}: the owner step runs on the GPU only; got a {p.device} tensor")
     if p.dtype not in (torch.float32, torch.bfloat16):
         raise TypeError(f"{what}: dtype must be float32 or bfloat16, got {p.dtype}")
+    if p.layout != torch.strided:
+        raise ValueError(f"{what}: must be a dense (strided) tensor, got {p.layout}")
     if not p.is_contiguous():
         raise ValueError(f"{what}: must be contiguous")
 
@@ -47,14 +49,41 @@ class _OwnerOptimizer(torch.optim.Optimizer):
         self._ws: Dict[Tuple[int, str], Tuple[tuple, torch.Tensor]] = {}
 
     def _split(self, group) -> Tuple[List[torch.Tensor], List[torch.Tensor]]:
+        """The group's parameters with a gradient, 2D matrices and the rest; empty tensors have
+        nothing to update and are left out. Every tensor must be a dense CUDA tensor on one device."""
         mats, tails = [], []
+        device = None
         for p in group["params"]:
-            if p.grad is None:
+            if p.grad is None or p.numel() == 0:
                 continue
             _check_tensor(p, "parameter")
             _check_tensor(p.grad, "gradient")
+            if p.grad.device != p.device or p.grad.shape != p.shape:
+                raise ValueError("gradient: must have the parameter's shape and device")
+            if device is None:
+                device = p.device
+            elif p.device != device:
+                raise ValueError(f"parameters of one group must be on one GPU; got {device} and {p.device}")
             (mats if p.dim() == 2 else tails).append(p)
         return mats, tails
+
+    @torch.no_grad()
+    def step(self, closure=None):
+        loss = None
+        if closure is not None:
+            with torch.enable_grad():
+                loss = closure()
+        for gi, group in enumerate(self.param_groups):
+            mats, tails = self._split(group)
+            if not mats and not tails:
+                continue
+            # the library launches on the current device's stream: make it the parameters' device
+            with torch.cuda.device((mats or tails)[0].device):
+                self._step_group(gi, group, mats, tails)
+        return loss
+
+    def _step_group(self, gi: int, group: dict, mats: List[torch.Tensor], tails: List[torch.Tensor]) -> None:
+        raise NotImplementedError
 
     def load_state_dict(self, state_dict) -> None:
         """As torch.optim.Optimizer.load_state_dict, except that the state tensors keep float32:
@@ -112,35 +141,27 @@ class OwnerMuon(_OwnerOptimizer):
         d.update(kw)
         super().__init__(params, d)
 
-    @torch.no_grad()
-    def step(self, closure=None):
-        loss = None
-        if closure is not None:
-            with torch.enable_grad():
-                loss = closure()
-        for gi, group in enumerate(self.param_groups):
-            mats, tails = self._split(group)
-            if mats:
-                ents = []
-                for p in mats:
-                    st = self.state[p]
-                    if "momentum_buffer" not in st:
-                        st["momentum_buffer"] = torch.zeros_like(p, dtype=torch.float32)
-                    ents.append(native.muon_entry_t(p, p.grad, st["momentum_buffer"]))
-                a, b, c = group["ns_coefficients"]
-                hp = native.muon_hparams(lr=group["lr"], weight_decay=group["weight_decay"],
-                                         momentum=group["momentum"], nesterov=group["nesterov"], a=a, b=b,
-                                         c=c, ns_steps=group["ns_steps"], eps=group["eps"],
-                                         lr_adjust=group["lr_adjust"], ns_dtype=group["ns_dtype"],
-                                         ns_schedule=group["ns_schedule"])
-                key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in mats), group["ns_steps"],
-                       group["ns_dtype"])
-                ws = self._workspace(gi, "muon", key, lambda: native.mfsdp_muon_workspace_size(ents, hp),
-                                     mats[0].device)
-                native.muon_step_t(ents, hp, ws)
-            if tails:
-                self._adamw(group, tails)
-        return loss
+    def _step_group(self, gi: int, group: dict, mats: List[torch.Tensor], tails: List[torch.Tensor]) -> None:
+        if mats:
+            ents = []
+            for p in mats:
+                st = self.state[p]
+                if "momentum_buffer" not in st:
+                    st["momentum_buffer"] = torch.zeros_like(p, dtype=torch.float32)
+                ents.append(native.muon_entry_t(p, p.grad, st["momentum_buffer"]))
+            a, b, c = group["ns_coefficients"]
+            hp = native.muon_hparams(lr=group["lr"], weight_decay=group["weight_decay"],
+                                     momentum=group["momentum"], nesterov=group["nesterov"], a=a, b=b,
+                                     c=c, ns_steps=group["ns_steps"], eps=group["eps"],
+                                     lr_adjust=group["lr_adjust"], ns_dtype=group["ns_dtype"],
+                                     ns_schedule=group["ns_schedule"])
+            key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in mats), group["ns_steps"],
+                   group["ns_dtype"])
+            ws = self._workspace(gi, "muon", key, lambda: native.mfsdp_muon_workspace_size(ents, hp),
+                                 mats[0].device)
+            native.muon_step_t(ents, hp, ws)
+        if tails:
+            self._adamw(group, tails)
 
 
 class OwnerShampoo(_OwnerOptimizer):
@@ -163,43 +184,35 @@ class OwnerShampoo(_OwnerOptimizer):
             raise ValueError("precondition_frequency must be >= 1")
         super().__init__(params, d)
 
-    @torch.no_grad()
-    def step(self, closure=None):
-        loss = None
-        if closure is not None:
-            with torch.enable_grad():
-                loss = closure()
-        for gi, group in enumerate(self.param_groups):
-            mats, tails = self._split(group)
-            # one call per refresh decision: matrices whose preconditioners are due, and the rest
-            due: Dict[bool, list] = {True: [], False: []}
-            for p in mats:
-                st = self.state[p]
-                if "L" not in st:
-                    m, n = p.shape
-                    for name, d in (("L", m), ("R", n), ("PL", m), ("PR", n)):
-                        st[name] = torch.zeros((d, d), dtype=torch.float32, device=p.device)
-                    st["step"] = 0
-                refresh = st["step"] % int(group["precondition_frequency"]) == 0
-                st["step"] += 1
-                due[refresh].append(p)
-            for refresh, ps in due.items():
-                if not ps:
-                    continue
-                ents = [native.shampoo_entry_t(p, p.grad, self.state[p]["L"], self.state[p]["R"],
-                                               self.state[p]["PL"], self.state[p]["PR"]) for p in ps]
-                hp = native.shampoo_hparams(lr=group["lr"], weight_decay=group["weight_decay"],
-                                            beta=group["beta"], weight=group["weight"], eps=group["eps"],
-                                            eps_rel=group["eps_rel"], refresh=refresh,
-                                            root_iters=group["root_iters"])
-                key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh,
-                       group["root_iters"])
-                ws = self._workspace(gi, "shampoo" + ("+" if refresh else "-"), key,
-                                     lambda: native.mfsdp_shampoo_workspace_size(ents, hp), ps[0].device)
-                native.shampoo_step_t(ents, hp, ws)
-            if tails:
-                self._adamw(group, tails)
-        return loss
+    def _step_group(self, gi: int, group: dict, mats: List[torch.Tensor], tails: List[torch.Tensor]) -> None:
+        # one call per refresh decision: matrices whose preconditioners are due, and the rest
+        due: Dict[bool, list] = {True: [], False: []}
+        for p in mats:
+            st = self.state[p]
+            if "L" not in st:
+                m, n = p.shape
+                for name, d in (("L", m), ("R", n), ("PL", m), ("PR", n)):
+                    st[name] = torch.zeros((d, d), dtype=torch.float32, device=p.device)
+                st["step"] = 0
+            refresh = st["step"] % int(group["precondition_frequency"]) == 0
+            st["step"] += 1
+            due[refresh].append(p)
+        for refresh, ps in due.items():
+            if not ps:
+                continue
+            ents = [native.shampoo_entry_t(p, p.grad, self.state[p]["L"], self.state[p]["R"],
+                                           self.state[p]["PL"], self.state[p]["PR"]) for p in ps]
+            hp = native.shampoo_hparams(lr=group["lr"], weight_decay=group["weight_decay"],
+                                        beta=group["beta"], weight=group["weight"], eps=group["eps"],
+                                        eps_rel=group["eps_rel"], refresh=refresh,
+                                        root_iters=group["root_iters"])
+            key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh,
+                   group["root_iters"])
+            ws = self._workspace(gi, "shampoo" + ("+" if refresh else "-"), key,
+                                 lambda: native.mfsdp_shampoo_workspace_size(ents, hp), ps[0].device)
+            native.shampoo_step_t(ents, hp, ws)
+        if tails:
+            self._adamw(group, tails)
 
 
 class OwnerSOAP(_OwnerOptimizer):
@@ -223,46 +236,38 @@ class OwnerSOAP(_OwnerOptimizer):
             raise ValueError("precondition_frequency must be >= 1")
         super().__init__(params, d)
 
-    @torch.no_grad()
-    def step(self, closure=None):
-        loss = None
-        if closure is not None:
-            with torch.enable_grad():
-                loss = closure()
-        for gi, group in enumerate(self.param_groups):
-            mats, tails = self._split(group)
-            # the library takes one step count and one refresh decision per call
-            calls: Dict[Tuple[int, bool], list] = {}
-            for p in mats:
-                if max(p.shape) > native.SOAP_MAX_DIM:
-                    raise ValueError(f"SOAP supports matrix sides up to {native.SOAP_MAX_DIM}, got {tuple(p.shape)}")
-                st = self.state[p]
-                if "QL" not in st:
-                    m, n = p.shape
-                    st["exp_avg"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
-                    st["exp_avg_sq"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
-                    st["L"] = torch.zeros((m, m), dtype=torch.float32, device=p.device)
-                    st["R"] = torch.zeros((n, n), dtype=torch.float32, device=p.device)
-                    st["QL"] = torch.eye(m, dtype=torch.float32, device=p.device)
-                    st["QR"] = torch.eye(n, dtype=torch.float32, device=p.device)
-                    st["step"] = 0
-                st["step"] += 1
-                t = st["step"]
-                refresh = t == 1 or t % int(group["precondition_frequency"]) == 0
-                calls.setdefault((t, refresh), []).append(p)
-            for (t, refresh), ps in calls.items():
-                ents = [native.soap_entry_t(p, p.grad, self.state[p]["exp_avg"], self.state[p]["exp_avg_sq"],
-                                            self.state[p]["L"], self.state[p]["R"], self.state[p]["QL"],
-                                            self.state[p]["QR"]) for p in ps]
-                beta_s = float(group["shampoo_beta"])
-                hp = native.soap_hparams(lr=group["lr"], weight_decay=group["weight_decay"], beta1=group["beta1"],
-                                         beta2=group["beta2"], eps=group["eps"], shampoo_beta=beta_s,
-                                         shampoo_weight=1.0 - beta_s, step=t, refresh=refresh,
-                                         refresh_iters=group["refresh_iters"])
-                key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh, group["refresh_iters"])
-                ws = self._workspace(gi, "soap" + ("+" if refresh else "-"), key,
-                                     lambda: native.mfsdp_soap_workspace_size(ents, hp), ps[0].device)
-                native.soap_step_t(ents, hp, ws)
-            if tails:
-                self._adamw(group, tails)
-        return loss
+    def _step_group(self, gi: int, group: dict, mats: List[torch.Tensor], tails: List[torch.Tensor]) -> None:
+        # the library takes one step count and one refresh decision per call
+        calls: Dict[Tuple[int, bool], list] = {}
+        for p in mats:
+            if max(p.shape) > native.SOAP_MAX_DIM:
+                raise ValueError(f"SOAP supports matrix sides up to {native.SOAP_MAX_DIM}, got {tuple(p.shape)}")
+            st = self.state[p]
+            if "QL" not in st:
+                m, n = p.shape
+                st["exp_avg"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
+                st["exp_avg_sq"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
+                st["L"] = torch.zeros((m, m), dtype=torch.float32, device=p.device)
+                st["R"] = torch.zeros((n, n), dtype=torch.float32, device=p.device)
+                st["QL"] = torch.eye(m, dtype=torch.float32, device=p.device)
+                st["QR"] = torch.eye(n, dtype=torch.float32, device=p.device)
+                st["step"] = 0
+            st["step"] += 1
+            t = st["step"]
+            refresh = t == 1 or t % int(group["precondition_frequency"]) == 0
+            calls.setdefault((t, refresh), []).append(p)
+        for (t, refresh), ps in calls.items():
+            ents = [native.soap_entry_t(p, p.grad, self.state[p]["exp_avg"], self.state[p]["exp_avg_sq"],
+                                        self.state[p]["L"], self.state[p]["R"], self.state[p]["QL"],
+                                        self.state[p]["QR"]) for p in ps]
+            beta_s = float(group["shampoo_beta"])
+            hp = native.soap_hparams(lr=group["lr"], weight_decay=group["weight_decay"], beta1=group["beta1"],
+                                     beta2=group["beta2"], eps=group["eps"], shampoo_beta=beta_s,
+                                     shampoo_weight=1.0 - beta_s, step=t, refresh=refresh,
+                                     refresh_iters=group["refresh_iters"])
+            key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh, group["refresh_iters"])
+            ws = self._workspace(gi, "soap" + ("+" if refresh else "-"), key,
+                                 lambda: native.mfsdp_soap_workspace_size(ents, hp), ps[0].device)
+            native.soap_step_t(ents, hp, ws)
+        if tails:
+            self._adamw(group, tails)

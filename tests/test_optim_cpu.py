@@ -1,5 +1,5 @@
 """The torch.optim front ends refuse anything but CUDA tensors (there is no CPU path) and unknown
-hyperparameters, before touching the library."""
+hyperparameters, before touching the library; empty and gradient-less parameters are skipped."""
 import pytest
 import torch
 
@@ -25,3 +25,16 @@ def test_unknown_hyperparameters_are_refused(cls):
 def test_refresh_frequency_must_be_positive(cls):
     with pytest.raises(ValueError):
         cls([torch.zeros(2, 2, requires_grad=True)], precondition_frequency=0)
+
+
+@pytest.mark.parametrize("cls", [OwnerMuon, OwnerShampoo, OwnerSOAP])
+def test_empty_and_gradless_parameters_are_skipped(cls):
+    # nothing to update: no library call is made, so this runs without a GPU
+    empty = torch.zeros(0, 8, requires_grad=True)
+    empty.grad = torch.zeros(0, 8)
+    no_grad = torch.zeros(4, 4, requires_grad=True)
+    opt = cls([empty, no_grad])
+    assert opt.step() is None
+    assert opt.step(closure=lambda: 3.5) == 3.5
+    assert len(opt.state) == 0
+

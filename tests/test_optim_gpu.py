@@ -187,3 +187,33 @@ def test_state_dict_round_trip_continues_identically(which):
         runs.append([p.detach().clone() for p in ps])
     for a, b in zip(*runs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("which", ["muon", "shampoo", "soap"])
+def test_empty_parameters_change_nothing(which):
+    """An empty matrix and an empty vector in the group (nothing to update) leave the other
+    parameters' updates bitwise as without them, and get no state."""
+    from paper_2607_05895_amd.optim import OwnerMuon, OwnerShampoo, OwnerSOAP
+    import torch
+    rng = np.random.default_rng(17)
+    model = _model(rng)
+    cls = {"muon": OwnerMuon, "shampoo": OwnerShampoo, "soap": OwnerSOAP}[which]
+    runs = []
+    for with_empty in (False, True):
+        ps, grads = _torch_params(model)
+        extra = []
+        if with_empty:
+            for shape in ((0, 256), (0,)):
+                e = torch.zeros(shape, dtype=torch.bfloat16, device="cuda", requires_grad=True)
+                e.grad = torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+                extra.append(e)
+        opt = cls(extra + ps)
+        for k in range(2):
+            for p, g in zip(ps, grads):
+                p.grad = g[k]
+            opt.step()
+        torch.cuda.synchronize()
+        assert all(e not in opt.state for e in extra)
+        runs.append([p.detach().clone() for p in ps])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
