@@ -8,7 +8,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from typing import Optional, Sequence
+from typing import Optional, Sequence, Tuple
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmfsdp.so")
@@ -323,6 +323,34 @@ def _stream() -> int:
     return torch.cuda.current_stream().cuda_stream
 
 
+_FLOAT = ("bfloat16", "float32")
+
+
+def _ptr(t, what: str, shape=None, dtypes=_FLOAT) -> int:
+    """Data pointer of a tensor handed to the library, after checking what the C ABI cannot: that it
+    is a dense, contiguous tensor on the current GPU (the calls run on that GPU's current stream)
+    with the shape and dtype the call reads and writes. The library trusts pointers and sizes, so a
+    tensor that is smaller than the call assumes would be written past its end."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what}: expected a torch.Tensor, got {type(t).__name__}")
+    if not t.is_cuda or t.layout != torch.strided:
+        raise ValueError(f"{what}: must be a dense CUDA tensor, got {t.layout} on {t.device}")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{what}: is on {t.device} but the current device is cuda:{torch.cuda.current_device()}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: must be contiguous")
+    if str(t.dtype).replace("torch.", "") not in dtypes:
+        raise TypeError(f"{what}: dtype must be one of {dtypes}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{what}: shape {tuple(t.shape)} where {tuple(shape)} is required")
+    return t.data_ptr()
+
+
+def _ws(workspace) -> Tuple[int, int]:
+    return _ptr(workspace, "workspace", dtypes=("uint8",)), workspace.numel()
+
+
 def muon_hparams(lr=0.02, weight_decay=0.0, momentum=0.95, nesterov=True, a=3.4445, b=-4.7750,
                  c=2.0315, ns_steps=5, eps=1e-7, lr_adjust="original", ns_dtype="bf16",
                  ns_schedule=None) -> MuonHParams:
@@ -337,9 +365,12 @@ def muon_hparams(lr=0.02, weight_decay=0.0, momentum=0.95, nesterov=True, a=3.44
 
 
 def muon_entry_t(param, grad, momentum, update_out=None) -> MuonEntry:
+    if param.dim() != 2:
+        raise ValueError(f"param: a Muon entry is a 2D matrix, got shape {tuple(param.shape)}")
     m, n = param.shape
-    return MuonEntry(param.data_ptr(), grad.data_ptr(), momentum.data_ptr(), m, n, _dt(param),
-                     _dt(grad), update_out.data_ptr() if update_out is not None else None)
+    return MuonEntry(_ptr(param, "param"), _ptr(grad, "grad", (m, n)),
+                     _ptr(momentum, "momentum", (m, n), ("float32",)), m, n, _dt(param), _dt(grad),
+                     _ptr(update_out, "update_out", (m, n), ("float32",)) if update_out is not None else None)
 
 
 def muon_workspace_t(entries: Sequence[MuonEntry], hp: MuonHParams, device="cuda"):
@@ -349,17 +380,21 @@ def muon_workspace_t(entries: Sequence[MuonEntry], hp: MuonHParams, device="cuda
 
 
 def muon_step_t(entries: Sequence[MuonEntry], hp: MuonHParams, workspace) -> None:
-    mfsdp_muon_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+    mfsdp_muon_step(entries, hp, *_ws(workspace), _stream())
 
 
 def muon_step_reduce_t(entries: Sequence[MuonEntry], parts, grad_scale: float, hp: MuonHParams,
                        workspace, reduced_out=None) -> None:
     """parts[i]: list of gradient-part tensors of entry i; reduced_out: None or a list of tensors
     (or None) receiving the reduced gradients."""
-    mfsdp_muon_step_reduce(entries, [[t.data_ptr() for t in ps] for ps in parts], grad_scale,
-                           [t.data_ptr() if t is not None else None for t in reduced_out]
-                           if reduced_out is not None else None,
-                           hp, workspace.data_ptr(), workspace.numel(), _stream())
+    if len(parts) != len(entries) or (reduced_out is not None and len(reduced_out) != len(entries)):
+        raise ValueError("parts (and reduced_out) need one item per entry")
+    dts = {BF16: ("bfloat16",), F32: ("float32",)}
+    ptrs = [[_ptr(t, f"parts[{i}]", (e.m, e.n), dts.get(e.grad_dtype, ())) for t in ps]
+            for i, (e, ps) in enumerate(zip(entries, parts))]
+    outs = ([_ptr(t, f"reduced_out[{i}]", (e.m, e.n), dts.get(e.grad_dtype, ())) if t is not None else None
+             for i, (e, t) in enumerate(zip(entries, reduced_out))] if reduced_out is not None else None)
+    mfsdp_muon_step_reduce(entries, ptrs, grad_scale, outs, hp, *_ws(workspace), _stream())
 
 
 def newton_schulz_t(x, out, a=3.4445, b=-4.7750, c=2.0315, steps=5, eps=1e-7, ns_dtype="bf16",
@@ -369,8 +404,8 @@ def newton_schulz_t(x, out, a=3.4445, b=-4.7750, c=2.0315, steps=5, eps=1e-7, ns
     nsd = BF16 if ns_dtype in ("bf16", BF16) else F32
     if workspace is None:
         workspace = torch.empty(mfsdp_ns_workspace_size(m, n, nsd), dtype=torch.uint8, device=x.device)
-    mfsdp_newton_schulz(x.data_ptr(), _dt(x), out.data_ptr(), _dt(out), m, n, a, b, c, steps, eps,
-                        nsd, workspace.data_ptr(), workspace.numel(), _stream())
+    mfsdp_newton_schulz(_ptr(x, "x"), _dt(x), _ptr(out, "out", (m, n)), _dt(out), m, n, a, b, c, steps, eps,
+                        nsd, *_ws(workspace), _stream())
 
 
 def newton_schulz_schedule_t(x, out, schedule, eps=1e-7, ns_dtype="bf16", workspace=None) -> None:
@@ -379,12 +414,14 @@ def newton_schulz_schedule_t(x, out, schedule, eps=1e-7, ns_dtype="bf16", worksp
     nsd = BF16 if ns_dtype in ("bf16", BF16) else F32
     if workspace is None:
         workspace = torch.empty(mfsdp_ns_workspace_size(m, n, nsd), dtype=torch.uint8, device=x.device)
-    mfsdp_newton_schulz_schedule(x.data_ptr(), _dt(x), out.data_ptr(), _dt(out), m, n, schedule, eps,
-                                 nsd, workspace.data_ptr(), workspace.numel(), _stream())
+    mfsdp_newton_schulz_schedule(_ptr(x, "x"), _dt(x), _ptr(out, "out", (m, n)), _dt(out), m, n, schedule,
+                                 eps, nsd, *_ws(workspace), _stream())
 
 
 def adamw_entry_t(param, grad, exp_avg, exp_avg_sq) -> AdamWEntry:
-    return AdamWEntry(param.data_ptr(), grad.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(),
+    sh = tuple(param.shape)
+    return AdamWEntry(_ptr(param, "param"), _ptr(grad, "grad", sh),
+                      _ptr(exp_avg, "exp_avg", sh, ("float32",)), _ptr(exp_avg_sq, "exp_avg_sq", sh, ("float32",)),
                       param.numel(), _dt(param), _dt(grad))
 
 
@@ -399,10 +436,14 @@ def shampoo_hparams(lr=1e-3, weight_decay=0.0, beta=1.0, weight=1.0, eps=1e-12, 
 
 
 def shampoo_entry_t(param, grad, L, R, PL, PR, update_out=None) -> ShampooEntry:
+    if param.dim() != 2:
+        raise ValueError(f"param: a Shampoo entry is a 2D matrix, got shape {tuple(param.shape)}")
     m, n = param.shape
-    return ShampooEntry(param.data_ptr(), grad.data_ptr(), L.data_ptr(), R.data_ptr(), PL.data_ptr(),
-                        PR.data_ptr(), m, n, _dt(param), _dt(grad),
-                        update_out.data_ptr() if update_out is not None else None)
+    f = ("float32",)
+    return ShampooEntry(_ptr(param, "param"), _ptr(grad, "grad", (m, n)), _ptr(L, "L", (m, m), f),
+                        _ptr(R, "R", (n, n), f), _ptr(PL, "PL", (m, m), f), _ptr(PR, "PR", (n, n), f),
+                        m, n, _dt(param), _dt(grad),
+                        _ptr(update_out, "update_out", (m, n), f) if update_out is not None else None)
 
 
 def shampoo_workspace_t(entries: Sequence[ShampooEntry], hp: ShampooHParams, device="cuda"):
@@ -412,7 +453,7 @@ def shampoo_workspace_t(entries: Sequence[ShampooEntry], hp: ShampooHParams, dev
 
 
 def shampoo_step_t(entries: Sequence[ShampooEntry], hp: ShampooHParams, workspace) -> None:
-    mfsdp_shampoo_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+    mfsdp_shampoo_step(entries, hp, *_ws(workspace), _stream())
 
 
 def inverse_root_t(a, out, p=4, eps=1e-12, eps_rel=1e-6, iters=20, workspace=None) -> None:
@@ -421,8 +462,9 @@ def inverse_root_t(a, out, p=4, eps=1e-12, eps_rel=1e-6, iters=20, workspace=Non
     if workspace is None:
         workspace = torch.empty(mfsdp_inverse_root_workspace_size(d, p, iters), dtype=torch.uint8,
                                 device=a.device)
-    mfsdp_inverse_root(a.data_ptr(), out.data_ptr(), d, p, eps, eps_rel, iters, workspace.data_ptr(),
-                       workspace.numel(), _stream())
+    f = ("float32",)
+    mfsdp_inverse_root(_ptr(a, "a", (d, d), f), _ptr(out, "out", (d, d), f), d, p, eps, eps_rel, iters,
+                       *_ws(workspace), _stream())
 
 
 def soap_hparams(lr=3e-3, weight_decay=0.0, beta1=0.95, beta2=0.95, eps=1e-8, shampoo_beta=0.95,
@@ -432,10 +474,14 @@ def soap_hparams(lr=3e-3, weight_decay=0.0, beta1=0.95, beta2=0.95, eps=1e-8, sh
 
 
 def soap_entry_t(param, grad, exp_avg, exp_avg_sq, L, R, QL, QR, update_out=None) -> SoapEntry:
+    if param.dim() != 2:
+        raise ValueError(f"param: a SOAP entry is a 2D matrix, got shape {tuple(param.shape)}")
     m, n = param.shape
-    return SoapEntry(param.data_ptr(), grad.data_ptr(), exp_avg.data_ptr(), exp_avg_sq.data_ptr(), L.data_ptr(),
-                     R.data_ptr(), QL.data_ptr(), QR.data_ptr(), m, n, _dt(param), _dt(grad),
-                     update_out.data_ptr() if update_out is not None else None)
+    f = ("float32",)
+    return SoapEntry(_ptr(param, "param"), _ptr(grad, "grad", (m, n)), _ptr(exp_avg, "exp_avg", (m, n), f),
+                     _ptr(exp_avg_sq, "exp_avg_sq", (m, n), f), _ptr(L, "L", (m, m), f), _ptr(R, "R", (n, n), f),
+                     _ptr(QL, "QL", (m, m), f), _ptr(QR, "QR", (n, n), f), m, n, _dt(param), _dt(grad),
+                     _ptr(update_out, "update_out", (m, n), f) if update_out is not None else None)
 
 
 def soap_workspace_t(entries: Sequence[SoapEntry], hp: SoapHParams, device="cuda"):
@@ -445,7 +491,7 @@ def soap_workspace_t(entries: Sequence[SoapEntry], hp: SoapHParams, device="cuda
 
 
 def soap_step_t(entries: Sequence[SoapEntry], hp: SoapHParams, workspace) -> None:
-    mfsdp_soap_step(entries, hp, workspace.data_ptr(), workspace.numel(), _stream())
+    mfsdp_soap_step(entries, hp, *_ws(workspace), _stream())
 
 
 def orthonormal_factor_t(a, q, workspace=None) -> None:
@@ -454,4 +500,5 @@ def orthonormal_factor_t(a, q, workspace=None) -> None:
     if workspace is None:
         workspace = torch.empty(max(mfsdp_orthonormal_factor_workspace_size(d), 256), dtype=torch.uint8,
                                 device=a.device)
-    mfsdp_orthonormal_factor(a.data_ptr(), q.data_ptr(), d, workspace.data_ptr(), workspace.numel(), _stream())
+    f = ("float32",)
+    mfsdp_orthonormal_factor(_ptr(a, "a", (d, d), f), _ptr(q, "q", (d, d), f), d, *_ws(workspace), _stream())
