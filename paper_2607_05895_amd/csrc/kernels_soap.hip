@@ -190,11 +190,13 @@ __global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __rest
 // (T_kk = tau_k, T_{0:k,k} = -tau_k T_{0:k,0:k} V_{:,0:k}^T v_k), so that H_1 ... H_jb = I - V T V^T.
 // One 512-thread workgroup per panel; thread t holds rows t + 512 i (i < 8) of the panel in
 // registers. Per column: one block reduction for the norm below the pivot, one for the 15 dot
-// products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k, for T). Every sum is
+// products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k, for T), whose 15
+// totals are formed once in LDS and then read by every thread. Every sum is
 // taken in a fixed order.
 __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanelDesc* __restrict__ descs) {
   __shared__ float red1[kQrPanelThreads / 64];
   __shared__ float red2[kQrPanelThreads / 64][kQrPanel];
+  __shared__ float tot[kQrPanel];
   __shared__ float alpha_s;
   __shared__ float Ts[kQrPanel][kQrPanel];
   const QrPanelDesc& d = descs[blockIdx.x];
@@ -274,12 +276,15 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
       if (lane < kQrPanel - 1) red2[w][lane] = r;
     }
     __syncthreads();
-    auto total = [&](int sl) {
+    // the 15 block totals, each summed once over the waves in wave order
+    if (t < kQrPanel - 1) {
       float acc = 0.0f;
 #pragma unroll
-      for (int j = 0; j < kQrPanelThreads / 64; ++j) acc += red2[j][sl];
-      return acc;
-    };
+      for (int j = 0; j < kQrPanelThreads / 64; ++j) acc += red2[j][t];
+      tot[t] = acc;
+    }
+    __syncthreads();
+    auto total = [&](int sl) { return tot[sl]; };
     float f[kQrPanel];
 #pragma unroll
     for (int l = k + 1; l < kQrPanel; ++l) f[l] = tau * total(l - 1);
