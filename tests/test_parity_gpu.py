@@ -257,6 +257,21 @@ def test_muon_update_out_optional_and_deterministic(native):
         assert torch.equal(m1, m2)
 
 
+@pytest.mark.parametrize("ns_dtype", ["bf16", "f32"])
+def test_muon_tiny_degenerate_shapes(native, ns_dtype):
+    """Matrices far below one tile (1x1, single rows and columns, 2x2, 3x3, 16x16) grouped in one
+    call: zero padding must leave their NS iterates exact on the padded tiles. A 1x1 or single-row
+    matrix has one normalised singular value, 1, so its update is the scalar quintic iterated on 1."""
+    _say(f"muon tiny shapes {ns_dtype}")
+    rng = np.random.default_rng(16)
+    shapes = [(1, 1), (1, 2), (2, 1), (2, 2), (3, 3), (1, 257), (257, 1), (16, 16)]
+    specs = [synth.MuonSpec(m, n, f"t{m}x{n}", synth.BF16, synth.BF16) for (m, n) in shapes]
+    tensors = [synth.random_muon_tensors(rng, m, n) for (m, n) in shapes]
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01, ns_dtype=ns_dtype)
+    dev = _run_muon(native, tensors, specs, hp)
+    _check_muon(tensors, specs, dev, hp, 2e-2 if ns_dtype == "bf16" else 1e-4)
+
+
 def test_muon_two_consecutive_steps(native):
     # state carried across calls on the same workspace
     import torch
