@@ -100,6 +100,7 @@ def test_inverse_root_of_diagonal_and_scaled_identity(native):
 # ------------------------------------------------------------------ Shampoo step
 
 SHAPES = [(1, 50), (65, 129), (200, 96), (256, 512), (300, 300), (640, 1152)]
+TINY = [(1, 1), (2, 3), (3, 2)]  # far below one tile: padding and 1x1 / 2x2 / 3x3 statistics
 
 
 class _Mat:
@@ -172,7 +173,7 @@ def _hp(native, **kw):
                                                          eps_rel=d["eps_rel"], refresh=d["refresh"])
 
 
-@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("shape", SHAPES + TINY)
 @pytest.mark.parametrize("dts", [(synth.BF16, synth.BF16), (synth.F32, synth.F32)])
 def test_shampoo_step_matches_oracle(native, shape, dts):
     m, n = shape

@@ -146,6 +146,7 @@ def test_orthonormal_factor_at_the_largest_side(native):
 # ------------------------------------------------------------------ SOAP step
 
 SHAPES = [(1, 50), (65, 129), (200, 96), (256, 512), (300, 300), (640, 1152)]
+TINY = [(1, 1), (2, 3), (3, 2)]  # far below one tile: padding and 1x1 / 2x2 / 3x3 statistics
 
 
 class _Mat:
@@ -223,7 +224,7 @@ def _hp(native, **kw):
     return (native.soap_hparams(step=step, **d), OS.SoapHParams(**d), step)
 
 
-@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("shape", SHAPES + TINY)
 @pytest.mark.parametrize("dts", [(synth.BF16, synth.BF16), (synth.F32, synth.F32)])
 def test_soap_step_matches_oracle(native, shape, dts):
     m, n = shape
