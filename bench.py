@@ -34,7 +34,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6   # dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk/CU
 PEAK_HBM_GBS = 8000.0       # HBM3E
-PEAK_F32_TFLOPS = 157.3     # fp32 vector (the fp32 NS path runs on the vector ALUs)
+PEAK_F32_TFLOPS = 157.3     # dense fp32 MFMA (the fp32 NS path runs v_mfma_f32_32x32x2f32)
 METRIC = "owner Muon-step latency (ms) and NS TFLOP/s (% MFMA bf16 peak) at 1 MI355X"
 GEMM_KERNEL = "gemm_bf16_kernel"
 GEMM_SOURCE = os.path.join(ROOT, "paper_2607_05895_amd", "csrc", "kernels_gemm.hip")
@@ -615,7 +615,7 @@ def main() -> int:
                    "nominal_ns_flop_per_step": flops},
         "roofline": {
             "kernel": GEMM_KERNEL if bf16_ns else "gemm_f32_kernel",
-            "bound": "mfma" if bf16_ns else "alu",
+            "bound": "mfma",
             "achieved": round(ns_tflops, 2),
             "peak": peak,
             "unit": "TFLOP/s",

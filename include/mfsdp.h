@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define MFSDP_ABI_VERSION 5
+#define MFSDP_ABI_VERSION 6
 
 typedef enum { MFSDP_F32 = 0, MFSDP_BF16 = 1 } mfsdp_dtype;
 
@@ -404,6 +404,10 @@ const char* mfsdp_last_error(void);
 const char* mfsdp_status_string(int status);
 /* MFSDP_ABI_VERSION of the built library. */
 int mfsdp_abi_version(void);
+/* Identifier of the sources the library was built from (16 hex digits of a SHA-256 over its source
+ * files, this header and the compiler flags, fixed at build time; "unknown" if the build did not set
+ * it). Bindings compare it with the sources they ship to refuse a stale binary. Static string. */
+const char* mfsdp_build_id(void);
 
 #ifdef __cplusplus
 }

@@ -33,7 +33,6 @@ from .muon import (  # noqa: F401
     lr_factor,
     apply_update,
     muon_step,
-    scalar_ns_map,
     reduce_gradients,
     step_coefficients,
 )

@@ -121,19 +121,6 @@ def newton_schulz(u: np.ndarray, a: float, b: float, c: float, steps: int,
     return np.ascontiguousarray(x.T if tall else x)
 
 
-def scalar_ns_map(sigma: float, a: float, b: float, c: float, steps: int,
-                  schedule=None) -> float:
-    """The scalar polynomial p(s) = a s + b s^3 + c s^5 iterated ``steps`` times (p_k with the
-    step's coefficients under a schedule).
-
-    NS acts on each singular value of the normalised input by this map; used by the pins.
-    """
-    s = float(sigma)
-    for ak, bk, ck in step_coefficients(a, b, c, steps, schedule):
-        s = ak * s + bk * s ** 3 + ck * s ** 5
-    return s
-
-
 def lr_factor(m: int, n: int, mode: str) -> float:
     """Shape adjustment of the learning rate (Section 5.1 names ``match_rms_adamw``).
 

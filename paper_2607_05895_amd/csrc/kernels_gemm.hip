@@ -11,7 +11,7 @@
 // v_mfma_f32_32x32x16_bf16 with fp32 accumulation. K advances 32 elements per step through a
 // five-stage LDS ring filled by direct global->LDS loads; the next tile's first loads overlap the
 // current tile's epilogue.
-// fp32 path: 64 x 64 tiles on the vector ALUs (a correctness path for fp32 NS).
+// fp32 path: 64 x 64 tiles on the fp32 MFMA (v_mfma_f32_32x32x2f32).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -163,9 +163,7 @@ __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((
 // are not waited for)
 #define MFSDP_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (0 << 8) | (3 << 14))
 
-#ifndef MFSDP_GEMM_WAVES
-#define MFSDP_GEMM_WAVES 8
-#endif
+constexpr int kGemmWaves = 8;  // waves per workgroup of the bf16 kernel
 // NW waves per workgroup arranged WM x WN over the 256 x 256 tile; each wave owns
 // (256 / WM) x (256 / WN) outputs as MI x NI blocks of 32 x 32. With 8 waves two share each SIMD,
 // so one can issue while the other waits.
@@ -749,15 +747,15 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, cons
                        int last_step, float ca, float cb, float cc, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16) {
-    const dim3 grid(kGemmXcds * kGemmSlots), block(MFSDP_GEMM_WAVES * 64);
+    const dim3 grid(kGemmXcds * kGemmSlots), block(kGemmWaves * 64);
     if (product == kProdGram)
-      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdGram>), grid, block, 0, st,
+      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdGram>), grid, block, 0, st,
                          d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
     else if (product == kProdSquare)
-      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdSquare>), grid, block, 0, st,
+      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdSquare>), grid, block, 0, st,
                          d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
     else
-      hipLaunchKernelGGL((gemm_bf16_kernel<MFSDP_GEMM_WAVES, kProdUpdate>), grid, block, 0, st,
+      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdUpdate>), grid, block, 0, st,
                          d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
   } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,

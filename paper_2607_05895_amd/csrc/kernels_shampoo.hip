@@ -34,13 +34,6 @@ __device__ __forceinline__ float ld_any(const void* p, int64_t i, int dt) {
   return static_cast<const float*>(p)[i];
 }
 
-// LDS slot permutation of the GEMM operand tiles: row r's eight 16-byte chunks are XOR-permuted by
-// (r & 7) ^ ((r >> 3) & 1). The fragment reads (32 consecutive rows at one chunk per half wave) and
-// the tile stores (8 lanes per row) are then free of bank conflicts for 32 and for 64 banks.
-__device__ __forceinline__ int op_slot(int r, int chunk) {
-  return r * 8 + (chunk ^ ((r & 7) ^ ((r >> 3) & 1)));
-}
-
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -69,23 +62,17 @@ __device__ __forceinline__ int split_slot(int r, int c) { return r * 2 + (c ^ ((
 // C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup.
 // 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The next K step's
 // global loads are held in registers during the current step's products (LDS double buffer).
-// SPLIT (the default): the products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32
-// accumulation) at fp32 accuracy. K steps of 16; when a step is staged into LDS every element is
+// The products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32 accuracy. K steps of 16; when a step is staged into LDS every element is
 // split once into hi + mid + lo bf16 parts (three planes per operand, 24 KiB per stage); a lane's
 // fragment is 8 consecutive k of one row from each plane, and the six partial products above 2^-24
 // relative are accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo,
 // lo.mid, lo.lo are below 2^-32). Six bf16 MFMAs per 16 k take 192 cycles against 512 for the fp32
 // MFMA. 48 KiB of LDS lets three workgroups share a CU.
-// !SPLIT: v_mfma_f32_32x32x2f32 on fp32 tiles, K steps of 32 (64 KiB of LDS, two per CU); the K
-// index inside a step is permuted identically on both operands (lane half h of instruction q within
-// group g takes k = 8g + 4h + q), so each lane reads its operands as 16-byte vectors.
 // Symmetric problems compute the upper tiles only and store each tile transposed as well, through
 // LDS, with coalesced row stores.
-template <bool SPLIT>
-__global__ __launch_bounds__(256, SPLIT ? 3 : 2) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs,
-                                                                      int count) {
+__global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs, int count) {
   constexpr int kPlane = kShTile * 32;                        // bytes of one split plane (128 x 16 bf16)
-  constexpr int kStage = SPLIT ? 6 * kPlane : 2 * kShTile * 128;  // both operands of one K step
+  constexpr int kStage = 6 * kPlane;  // both operands of one K step, three planes each
   __shared__ __attribute__((aligned(16))) uint8_t lds_raw[2 * kStage];
   const int e = find_desc(descs, count, blockIdx.x);
   const ShGemmDesc& d = descs[e];
@@ -131,7 +118,7 @@ __global__ __launch_bounds__(256, SPLIT ? 3 : 2) void sh_gemm_kernel(const ShGem
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
   const int fr = lane & 31, fh = lane >> 5;
-  if constexpr (SPLIT) {
+  {
     // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
     const int lrow = t >> 2, lch = t & 3;
     f32x4 ra[2], rb[2];
@@ -191,51 +178,6 @@ __global__ __launch_bounds__(256, SPLIT ? 3 : 2) void sh_gemm_kernel(const ShGem
           for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]], acc[i][j],
                                                                 0, 0, 0);
-      if (kt + 1 < nk) lstore(s ^ 1);
-      __syncthreads();
-    }
-  } else {
-    f32x4(*lds)[2][kShTile * 8] = reinterpret_cast<f32x4(*)[2][kShTile * 8]>(lds_raw);
-    const int lrow = t >> 3, lch = t & 7;
-    f32x4 ra[4], rb[4];
-    auto gload = [&](int k0) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = lrow + 32 * j;
-        ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
-        rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
-      }
-    };
-    auto lstore = [&](int s) {
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int slot = op_slot(lrow + 32 * j, lch);
-        lds[s][0][slot] = ra[j];
-        lds[s][1][slot] = rb[j];
-      }
-    };
-    const int nk = d.K / 32;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int s = kt & 1;
-      if (kt + 1 < nk) gload((kt + 1) * 32);
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        f32x4 a[2], b[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = lds[s][0][op_slot(wr * 64 + i * 32 + fr, 2 * g + fh)];
-#pragma unroll
-        for (int j = 0; j < 2; ++j) b[j] = lds[s][1][op_slot(wc * 64 + j * 32 + fr, 2 * g + fh)];
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
-      }
       if (kt + 1 < nk) lstore(s ^ 1);
       __syncthreads();
     }
@@ -459,11 +401,7 @@ __global__ __launch_bounds__(256) void sh_apply_kernel(const ShApplyDesc* __rest
 
 hipError_t launch_sh_gemm(const ShGemmDesc* d, int count, int total_tiles, hipStream_t st) {
   if (total_tiles <= 0 || count <= 0) return hipSuccess;
-#ifdef MFSDP_SH_GEMM_F32
-  hipLaunchKernelGGL(sh_gemm_kernel<false>, dim3(total_tiles), dim3(256), 0, st, d, count);
-#else
-  hipLaunchKernelGGL(sh_gemm_kernel<true>, dim3(total_tiles), dim3(256), 0, st, d, count);
-#endif
+  hipLaunchKernelGGL(sh_gemm_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
   return hipGetLastError();
 }
 

@@ -549,6 +549,11 @@ extern "C" {
 
 int mfsdp_abi_version(void) { return MFSDP_ABI_VERSION; }
 
+#ifndef MFSDP_BUILD_ID
+#define MFSDP_BUILD_ID "unknown"
+#endif
+const char* mfsdp_build_id(void) { return MFSDP_BUILD_ID; }
+
 const char* mfsdp_last_error(void) { return g_last_error.c_str(); }
 
 const char* mfsdp_status_string(int status) {

@@ -167,16 +167,10 @@ hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t s
 // NS tile sizes (padding granularity of the workspace buffers).
 constexpr int kTileBF16 = 256;
 constexpr int kTileF32 = 64;
-#ifndef MFSDP_PREP_COLS
-#define MFSDP_PREP_COLS 256
-#endif
-#ifndef MFSDP_APPLY_COLS
-#define MFSDP_APPLY_COLS 128
-#endif
 constexpr int kPrepRows = 64;                    // prep tile rows
-constexpr int kPrepColsBF16 = MFSDP_PREP_COLS;   // prep tile columns on the bf16 path (divides 256)
+constexpr int kPrepColsBF16 = 256;              // prep tile columns on the bf16 path (divides 256)
 constexpr int kPrepColsF32 = 64;                 // prep tile columns on the fp32 path
-constexpr int kApplyCols = MFSDP_APPLY_COLS;     // apply tile columns (8 per thread per row)
-constexpr int kApplyRows = 16384 / MFSDP_APPLY_COLS;  // 16 K elements per tile: 64 per thread
+constexpr int kApplyCols = 128;                 // apply tile columns (8 per thread per row)
+constexpr int kApplyRows = 16384 / kApplyCols;  // 16 K elements per tile: 64 per thread
 
 }  // namespace mfsdp

@@ -23,9 +23,9 @@ EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_time
            "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners",
            "mfsdp_shampoo_workspace_size", "mfsdp_shampoo_step", "mfsdp_inverse_root_workspace_size",
            "mfsdp_inverse_root", "mfsdp_soap_workspace_size", "mfsdp_soap_step",
-           "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor")
+           "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor", "mfsdp_build_id")
 MAX_GRAD_PARTS = 64
-ABI_VERSION = 5
+ABI_VERSION = 6
 SOAP_MAX_DIM = 4096
 
 
@@ -96,7 +96,8 @@ _lib = None
 
 
 def lib() -> ctypes.CDLL:
-    """Load libmfsdp.so once. Raises if it is missing: there is no fallback path."""
+    """Load libmfsdp.so once. Raises if it is missing, or if it was built from other sources than the
+    ones in the tree (its embedded build identifier differs): there is no fallback path."""
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
@@ -155,6 +156,13 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_orthonormal_factor_workspace_size.restype = sz
         L.mfsdp_orthonormal_factor.argtypes = [vp, vp, i64, vp, sz, vp]
         L.mfsdp_orthonormal_factor.restype = ctypes.c_int
+        L.mfsdp_build_id.argtypes = []
+        L.mfsdp_build_id.restype = ctypes.c_char_p
+        from . import build_lib
+        built, tree = L.mfsdp_build_id().decode(), build_lib.source_id()
+        if built != tree:
+            raise ImportError(f"{LIB_PATH} was built from other sources (build id {built}, sources {tree}); "
+                              "rebuild it with `python -m paper_2607_05895_amd.build_lib`")
         _lib = L
     return _lib
 
@@ -173,6 +181,10 @@ def _entries(arr, cls):
 
 def mfsdp_abi_version() -> int:
     return lib().mfsdp_abi_version()
+
+
+def mfsdp_build_id() -> str:
+    return lib().mfsdp_build_id().decode()
 
 
 def mfsdp_last_error() -> str:

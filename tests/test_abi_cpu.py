@@ -25,7 +25,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_abi_version_and_status_strings():
-    assert native.mfsdp_abi_version() == native.ABI_VERSION == 5
+    assert native.mfsdp_abi_version() == native.ABI_VERSION == 6
     assert native.mfsdp_status_string(0) == "MFSDP_OK"
     assert native.mfsdp_status_string(-1) == "MFSDP_E_INVALID"
     assert native.mfsdp_status_string(-2) == "MFSDP_E_WORKSPACE"
@@ -388,3 +388,21 @@ def test_orthonormal_factor_workspace_query():
         dp = -(-d // 128) * 128
         assert q >= 4 * (2 * dp * dp + 16 * d + 256)
         assert _needed_bytes(lambda: native.mfsdp_orthonormal_factor(FAKE, FAKE * 2, d, FAKE * 16, 0, 0)) == q
+
+
+def test_library_build_id_matches_the_sources():
+    from paper_2607_05895_amd import build_lib
+    assert native.mfsdp_build_id() == build_lib.source_id()
+    assert re.fullmatch(r"[0-9a-f]{16}", native.mfsdp_build_id())
+
+
+def test_stale_library_is_refused(monkeypatch):
+    """A library built from other sources than the tree's is not loaded (no silent stale binary)."""
+    from paper_2607_05895_amd import build_lib
+    native.lib()
+    monkeypatch.setattr(native, "_lib", None)
+    monkeypatch.setattr(build_lib, "source_id", lambda: "0" * 16)
+    with pytest.raises(ImportError, match="other sources"):
+        native.lib()
+    monkeypatch.undo()
+    assert native.lib() is not None
