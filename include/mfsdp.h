@@ -141,6 +141,29 @@ int mfsdp_muon_step_timed(const mfsdp_muon_entry* entries, int64_t count,
                           const mfsdp_muon_hparams* hp, void* workspace, size_t workspace_bytes,
                           void* stream, void* const* events);
 
+/* Size of the static device array mfsdp_muon_step_noalloc works in: 64 MiB per GPU the library runs
+ * on, held until the process ends. It fits, e.g., one 2048 x 2048 or one 1024 x 4096 matrix, or eight
+ * 768 x 768 matrices (mfsdp_muon_workspace_size gives what a list of entries needs). */
+#define MFSDP_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* mfsdp_muon_step for callers that cannot allocate memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation. Same entries, hyperparameters, results (bitwise
+ * those of mfsdp_muon_step) and error rules, but no workspace argument and no allocation of any kind
+ * by the library (no hipMalloc / hipFree / hipHostMalloc; the launch descriptors are passed to the
+ * device as kernel arguments, a few small launches per call, instead of through pinned staging).
+ *   - The workspace is a file-scope device array of MFSDP_NOALLOC_SCRATCH_BYTES, one per GPU. Entries
+ *     whose mfsdp_muon_workspace_size exceeds it are rejected with MFSDP_E_INVALID before anything is
+ *     enqueued; use mfsdp_muon_step with a caller workspace for them.
+ *   - The call runs on the current device; `stream` (hipStream_t, NULL = null stream) must belong to
+ *     it. The first call on a device looks up that device's copy of the array (hipGetSymbolAddress);
+ *     make one call before capturing a graph so that the lookup is not part of the capture.
+ *   - Every call on one GPU shares that GPU's array, which keeps the last call's contents (nothing in
+ *     it needs to start at zero: each call writes every byte it reads). Calls that overlap on one
+ *     GPU (different streams, threads, or graph replays running concurrently) race on it and give
+ *     wrong results: order them on one stream or with events. */
+int mfsdp_muon_step_noalloc(const mfsdp_muon_entry* entries, int64_t count,
+                            const mfsdp_muon_hparams* hp, void* stream);
+
 /* Most gradient parts one entry of mfsdp_muon_step_reduce may have (the paper's largest shard
  * span is 64 ranks). */
 #define MFSDP_MAX_GRAD_PARTS 64

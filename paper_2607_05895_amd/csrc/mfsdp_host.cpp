@@ -494,13 +494,18 @@ int record(void* const* events, int k, hipStream_t st) {
   return e == hipSuccess ? MFSDP_OK : hip_fail(e, "hipEventRecord");
 }
 
+int upload_as_kernel_args(const uint8_t* host, size_t bytes, uint8_t* dst, hipStream_t st);
+
 // coeffs: 3 * steps doubles, (a_k, b_k, c_k) of NS step k.
+// Descriptors: slot >= 0 uploads them from that pinned staging slot; slot < 0 passes them from the
+// host buffer `host_descs` as kernel arguments (the allocation-free step).
 int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const double* coeffs,
                      int ns_dtype, double beta, int nesterov, double eps, int prep_tiles,
-                     int apply_tiles, hipStream_t st, void* const* events, bool reduce = false) {
+                     int apply_tiles, hipStream_t st, void* const* events, bool reduce = false,
+                     const uint8_t* host_descs = nullptr) {
   const int count = int(P.ns.size());
   const DescLayout& dl = P.dl;
-  int rc = ring().upload(slot, ws, dl.bytes, st);
+  int rc = slot >= 0 ? ring().upload(slot, ws, dl.bytes, st) : upload_as_kernel_args(host_descs, dl.bytes, ws, st);
   if (rc) return rc;
   if ((rc = record(events, 0, st))) return rc;
   hipError_t e;
@@ -541,7 +546,7 @@ struct ReduceArgs {
 };
 int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
               void* workspace, size_t workspace_bytes, void* stream, void* const* events,
-              const ReduceArgs* ra);
+              const ReduceArgs* ra, bool in_scratch = false);
 
 }  // namespace
 
@@ -615,9 +620,14 @@ int mfsdp_muon_step_reduce(const mfsdp_muon_entry* entries, int64_t count,
 
 namespace {
 
+int scratch_address(void** out);
+
+// in_scratch: the allocation-free step. The workspace is this device's static scratch array
+// (`workspace` and `workspace_bytes` are ignored) and the descriptors travel as kernel arguments
+// from ordinary host memory instead of through the pinned staging ring.
 int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_hparams* hp,
               void* workspace, size_t workspace_bytes, void* stream, void* const* events,
-              const ReduceArgs* ra) {
+              const ReduceArgs* ra, bool in_scratch) {
   int rc = check_hp(hp);
   if (rc) return rc;
   rc = check_entries(entries, count, ra == nullptr);
@@ -629,6 +639,15 @@ int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_h
   });
   const std::vector<NsPlan>& plans = P.ns;
   const size_t need = P.bytes;
+  if (in_scratch) {
+    if (need > size_t(MFSDP_NOALLOC_SCRATCH_BYTES))
+      return fail(MFSDP_E_INVALID,
+                  "these entries need %zu bytes of workspace; the allocation-free step holds at most "
+                  "%zu (MFSDP_NOALLOC_SCRATCH_BYTES): use mfsdp_muon_step with a caller workspace",
+                  need, size_t(MFSDP_NOALLOC_SCRATCH_BYTES));
+    if ((rc = scratch_address(&workspace))) return rc;
+    workspace_bytes = MFSDP_NOALLOC_SCRATCH_BYTES;
+  }
   if (!workspace || (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
     return fail(MFSDP_E_WORKSPACE, "workspace must be non-NULL and 256-byte aligned");
   if (workspace_bytes < need)
@@ -637,11 +656,19 @@ int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_h
   hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   const DescLayout& dl = P.dl;
-  void* hptr = nullptr;
-  const int slot = ring().acquire(dl.bytes, &hptr, st);
-  if (slot < 0) return slot;
-  uint8_t* h = static_cast<uint8_t*>(hptr);
-  std::memset(h, 0, dl.bytes);
+  int slot = -1;
+  std::vector<uint8_t> host_descs;
+  uint8_t* h = nullptr;
+  if (in_scratch) {
+    host_descs.assign(dl.bytes, 0);
+    h = host_descs.data();
+  } else {
+    void* hptr = nullptr;
+    slot = ring().acquire(dl.bytes, &hptr, st);
+    if (slot < 0) return slot;
+    h = static_cast<uint8_t*>(hptr);
+    std::memset(h, 0, dl.bytes);
+  }
 
   auto* prep = reinterpret_cast<PrepDesc*>(h + dl.off_prep);
   auto* norm = reinterpret_cast<NormDesc*>(h + dl.off_norm);
@@ -670,7 +697,8 @@ int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_h
   fill_gemm_descs(P, ws, *hp, h, tile);
   const std::vector<double> coeffs = step_coeffs(hp->a, hp->b, hp->c, hp->ns_steps, hp->ns_schedule);
   return enqueue_pipeline(P, ws, slot, hp->ns_steps, coeffs.data(), hp->ns_dtype, hp->momentum,
-                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events, ra != nullptr);
+                          hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events, ra != nullptr,
+                          h);
 }
 
 }  // namespace
@@ -828,6 +856,74 @@ int mfsdp_adamw_step(const mfsdp_adamw_entry* entries, int64_t count, double lr,
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------------------------
+// Allocation-free Muon step (mfsdp_muon_step_noalloc): its workspace is this static device array,
+// one copy per GPU the library runs on, held until the process ends. In host code `scratch` is
+// only a host-side stand-in for the symbol; the device address of each GPU's copy comes from
+// hipGetSymbolAddress, looked up once per device with that device current and cached here, and
+// only that address is handed to kernels. Every call on one GPU shares that GPU's copy.
+static __device__ __align__(256) uint8_t scratch[MFSDP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 256;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxScratchDevices] = {};
+
+// Device address of the current device's scratch array (looked up on the first call per device).
+int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(MFSDP_E_HIP, "device ordinal %d outside [0, %d)", dev, kMaxScratchDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (!p || (reinterpret_cast<uintptr_t>(p) % kAlign) != 0)
+      return fail(MFSDP_E_HIP, "scratch array of device %d is not 256-byte aligned", dev);
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return MFSDP_OK;
+}
+
+// Descriptor bytes handed over as kernel arguments, one launch per chunk (vector stores only).
+constexpr int kArgChunkWords = 448;  // 1792 bytes of payload per launch
+struct ArgChunk {
+  uint32_t w[kArgChunkWords];
+  uint32_t words;
+};
+
+__global__ __launch_bounds__(256) void arg_copy_kernel(ArgChunk c, uint32_t* __restrict__ dst) {
+  for (uint32_t i = threadIdx.x; i < c.words; i += blockDim.x) dst[i] = c.w[i];
+}
+
+int upload_as_kernel_args(const uint8_t* host, size_t bytes, uint8_t* dst, hipStream_t st) {
+  if (bytes % 4) return fail(MFSDP_E_INVALID, "descriptor region of %zu bytes is not whole words", bytes);
+  const size_t words = bytes / 4;
+  for (size_t w0 = 0; w0 < words; w0 += kArgChunkWords) {
+    ArgChunk c;
+    c.words = uint32_t(std::min<size_t>(kArgChunkWords, words - w0));
+    std::memcpy(c.w, host + 4 * w0, 4 * size_t(c.words));
+    hipLaunchKernelGGL(arg_copy_kernel, dim3(1), dim3(256), 0, st, c,
+                       reinterpret_cast<uint32_t*>(dst + 4 * w0));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "descriptor launch");
+  }
+  return MFSDP_OK;
+}
+
+}  // namespace
+
+extern "C" int mfsdp_muon_step_noalloc(const mfsdp_muon_entry* entries, int64_t count,
+                                       const mfsdp_muon_hparams* hp, void* stream) {
+  g_last_error.clear();
+  return muon_impl(entries, count, hp, nullptr, 0, stream, nullptr, nullptr, true);
+}
 
 namespace mfsdp {
 // Descriptor staging shared with the other host modules of the library.

@@ -23,7 +23,9 @@ EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_time
            "mfsdp_status_string", "mfsdp_abi_version", "mfsdp_muon_step_reduce", "mfsdp_plan_owners",
            "mfsdp_shampoo_workspace_size", "mfsdp_shampoo_step", "mfsdp_inverse_root_workspace_size",
            "mfsdp_inverse_root", "mfsdp_soap_workspace_size", "mfsdp_soap_step",
-           "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor", "mfsdp_build_id")
+           "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor", "mfsdp_build_id",
+           "mfsdp_muon_step_noalloc")
+NOALLOC_SCRATCH_BYTES = 64 << 20
 MAX_GRAD_PARTS = 64
 ABI_VERSION = 6
 SOAP_MAX_DIM = 4096
@@ -117,6 +119,8 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_muon_step_timed.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams),
                                             vp, sz, vp, ctypes.POINTER(ctypes.c_void_p)]
         L.mfsdp_muon_step_timed.restype = ctypes.c_int
+        L.mfsdp_muon_step_noalloc.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(MuonHParams), vp]
+        L.mfsdp_muon_step_noalloc.restype = ctypes.c_int
         L.mfsdp_muon_step_reduce.argtypes = [ctypes.POINTER(MuonEntry), i64, ctypes.POINTER(ctypes.c_void_p),
                                              i32, f64, ctypes.POINTER(ctypes.c_void_p),
                                              ctypes.POINTER(MuonHParams), vp, sz, vp]
@@ -264,6 +268,11 @@ def mfsdp_muon_step(entries: Sequence[MuonEntry], hp: MuonHParams, workspace: in
     _check(lib().mfsdp_muon_step(arr, n, ctypes.byref(hp), workspace, workspace_bytes, stream))
 
 
+def mfsdp_muon_step_noalloc(entries: Sequence[MuonEntry], hp: MuonHParams, stream: int = 0) -> None:
+    arr, n = _entries(entries, MuonEntry)
+    _check(lib().mfsdp_muon_step_noalloc(arr, n, ctypes.byref(hp), stream))
+
+
 def mfsdp_muon_step_timed(entries: Sequence[MuonEntry], hp: MuonHParams, workspace: int,
                           workspace_bytes: int, stream: int, events: Sequence[int]) -> None:
     arr, n = _entries(entries, MuonEntry)
@@ -393,6 +402,11 @@ def muon_workspace_t(entries: Sequence[MuonEntry], hp: MuonHParams, device="cuda
 
 def muon_step_t(entries: Sequence[MuonEntry], hp: MuonHParams, workspace) -> None:
     mfsdp_muon_step(entries, hp, *_ws(workspace), _stream())
+
+
+def muon_step_noalloc_t(entries: Sequence[MuonEntry], hp: MuonHParams) -> None:
+    """The allocation-free step on the current device's torch stream (no workspace tensor)."""
+    mfsdp_muon_step_noalloc(entries, hp, _stream())
 
 
 def muon_step_reduce_t(entries: Sequence[MuonEntry], parts, grad_scale: float, hp: MuonHParams,

@@ -406,3 +406,20 @@ def test_stale_library_is_refused(monkeypatch):
         native.lib()
     monkeypatch.undo()
     assert native.lib() is not None
+
+
+def test_noalloc_rejects_entries_beyond_the_scratch_before_any_gpu_work():
+    """A list that needs more workspace than the allocation-free step's static array is refused by
+    the argument checks (no device is touched: the pointers here are never dereferenced)."""
+    hp = native.muon_hparams()
+    big = [_entry(m=4096, n=4096)]
+    need = native.mfsdp_muon_workspace_size(big, hp)
+    assert need > native.NOALLOC_SCRATCH_BYTES
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step_noalloc(big, hp, 0)
+    assert ei.value.status == native.E_INVALID
+    assert "MFSDP_NOALLOC_SCRATCH_BYTES" in native.mfsdp_last_error()
+    with pytest.raises(native.MfsdpError) as ei:
+        native.mfsdp_muon_step_noalloc([_entry(m=0)], hp, 0)
+    assert ei.value.status == native.E_INVALID
+    native.mfsdp_muon_step_noalloc([], hp, 0)  # count == 0 is a no-op
