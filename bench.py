@@ -352,6 +352,103 @@ def shampoo_nominal_flop(shapes, iters: int, refresh: bool) -> float:
     return tot
 
 
+def _dist_draw(torch, shape, dist, dtype, dev, gen):
+    """Seeded device draw of N(dist.mean, dist.std^2) (a constant when std == 0)."""
+    x = torch.randn(*shape, device=dev, generator=gen) * dist.std + dist.mean
+    return x.to(dtype)
+
+
+def share_record(native, torch, dev, hev, stream, index, steps, warmup) -> dict:
+    """One owner share (synth.workload(index)) timed like the headline share: values drawn on the
+    device from a seeded generator with the share's distributions (the cost does not depend on them),
+    warmup + `steps` whole owner steps (Muon over every matrix, then AdamW over the tail tensors),
+    phase events from mfsdp_muon_step_timed. The share's largest AdamW tensor (the uneven plan's
+    128256 x 4096 embedding) is also timed on its own."""
+    import synth
+    wl = synth.workload(index)
+    hp = wl.hp
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1000 + index)
+    tdt = {synth.BF16: torch.bfloat16, synth.F32: torch.float32}
+    keep, ents, aents = [], [], []
+    for e in wl.muon:
+        p = _dist_draw(torch, (e.m, e.n), e.param, tdt[e.param_dtype], dev, gen)
+        g = _dist_draw(torch, (e.m, e.n), e.grad, tdt[e.grad_dtype], dev, gen)
+        mo = _dist_draw(torch, (e.m, e.n), e.momentum, torch.float32, dev, gen)
+        keep.append((p, g, mo))
+        ents.append(native.muon_entry_t(p, g, mo))
+    for e in wl.adamw:
+        t = (_dist_draw(torch, (e.numel,), e.param, tdt[e.param_dtype], dev, gen),
+             _dist_draw(torch, (e.numel,), e.grad, tdt[e.grad_dtype], dev, gen),
+             torch.zeros(e.numel, device=dev), torch.zeros(e.numel, device=dev))
+        keep.append(t)
+        aents.append(native.adamw_entry_t(*t))
+    h = native.muon_hparams(lr=hp.lr, weight_decay=hp.weight_decay, momentum=hp.momentum,
+                            nesterov=hp.nesterov, a=hp.a, b=hp.b, c=hp.c, ns_steps=hp.ns_steps,
+                            eps=hp.eps, lr_adjust=hp.lr_adjust, ns_dtype=hp.ns_dtype)
+    ws = native.muon_workspace_t(ents, h, device=dev)
+    ah = wl.adamw_hp
+    ev = [[hev.create() for _ in range(4)] for _ in range(steps)]
+    e0, e1 = hev.create(), hev.create()
+
+    def step(events=None):
+        native.mfsdp_muon_step_timed(ents, h, ws.data_ptr(), ws.numel(), stream, events or [None] * 4)
+        if aents:
+            native.mfsdp_adamw_step(aents, ah.lr, ah.beta1, ah.beta2, ah.eps, ah.weight_decay, ah.step, stream)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hev.record(e0, stream)
+    for k in range(steps):
+        step(ev[k])
+    hev.record(e1, stream)
+    torch.cuda.synchronize()
+    ms = hev.elapsed_ms(e0, e1) / steps
+    prep_ms = sum(hev.elapsed_ms(x[0], x[1]) for x in ev) / steps
+    ns_ms = sum(hev.elapsed_ms(x[1], x[2]) for x in ev) / steps
+    bf16_ns = hp.ns_dtype == synth.BF16
+    peak = PEAK_BF16_TFLOPS if bf16_ns else PEAK_F32_TFLOPS
+    flops = wl.ns_flops_nominal()
+    es = {synth.BF16: 2, synth.F32: 4}
+    prep_bytes = sum(e.m * e.n * (es[e.grad_dtype] + 8 + 2 * es[hp.ns_dtype]) for e in wl.muon)
+    rec = {"workload": wl.name, "description": wl.description, "muon_matrices": len(wl.muon),
+           "muon_elements": wl.muon_elements(), "adamw_elements": wl.adamw_elements(),
+           "ns_dtype": "bf16" if bf16_ns else "f32", "steps": steps, "warmup": warmup,
+           "ms_per_step": round(ms, 4), "ns_ms": round(ns_ms, 4), "prep_norm_ms": round(prep_ms, 4),
+           "nominal_ns_flop_per_step": flops,
+           "ns_tflops": round(flops / (ns_ms * 1e-3) / 1e12, 2),
+           "ns_frac_peak": round(flops / (ns_ms * 1e-3) / 1e12 / peak, 4), "peak_tflops": peak,
+           "prep_GBps": round(prep_bytes / (prep_ms * 1e-3) / 1e9, 1),
+           "prep_frac_hbm": round(prep_bytes / (prep_ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+           "data": "seeded device draws with the share's distributions"}
+    log(f"share {wl.name}: {ms:.3f} ms per step, NS {ns_ms:.3f} ms ({rec['ns_tflops']} TFLOP/s, "
+        f"{rec['ns_frac_peak']:.3f} of peak), prep {rec['prep_GBps']} GB/s")
+    del ws
+    big = max(range(len(wl.adamw)), key=lambda j: wl.adamw[j].numel, default=None)
+    if big is not None and wl.adamw[big].numel >= (1 << 24):
+        e = wl.adamw[big]
+        one = [aents[big]]
+        for _ in range(warmup):
+            native.mfsdp_adamw_step(one, ah.lr, ah.beta1, ah.beta2, ah.eps, ah.weight_decay, ah.step, stream)
+        torch.cuda.synchronize()
+        hev.record(e0, stream)
+        for _ in range(steps):
+            native.mfsdp_adamw_step(one, ah.lr, ah.beta1, ah.beta2, ah.eps, ah.weight_decay, ah.step, stream)
+        hev.record(e1, stream)
+        torch.cuda.synchronize()
+        ams = hev.elapsed_ms(e0, e1) / steps
+        nb = e.numel * (2 * es[e.param_dtype] + es[e.grad_dtype] + 16)
+        rec["adamw_largest"] = {"tensor": e.name, "numel": e.numel, "bytes": nb, "ms": round(ams, 4),
+                                "GBps": round(nb / (ams * 1e-3) / 1e9, 1),
+                                "frac_hbm": round(nb / (ams * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        log(f"AdamW on {e.name} ({e.numel / 1e6:.1f} M elements): {ams:.3f} ms, "
+            f"{rec['adamw_largest']['GBps']} GB/s")
+    del keep, ents, aents
+    torch.cuda.empty_cache()
+    return rec
+
+
 def time_shampoo(native, torch, dev, hev, stream, steps, warmup, iters=20) -> dict:
     """The Shampoo owner step (Section 5.7) on the GPT-2-small share's 12 matrices, fp32 accuracy."""
     import synth
@@ -479,6 +576,8 @@ def main() -> int:
                     help="skip timing the Shampoo owner step on the GPT-2-small share")
     ap.add_argument("--shampoo", action="store_true", help=argparse.SUPPRESS)  # (the default)
     ap.add_argument("--no-soap", action="store_true", help="skip the SOAP owner-step timing")
+    ap.add_argument("--no-other-shares", action="store_true",
+                    help="skip timing the other owner shares (1, 2, 4, 5 besides the default 3)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -653,6 +752,16 @@ def main() -> int:
                                                   if args.plan_span else ""))
     pctx = (torch, dev, hev, stream, h, ah, 5, 2) if args.plan_span else None
     out["planner"] = planner_report(native, sorted(PLAN_SWEEP), args.plan_span, pctx)
+    if not args.no_other_shares:
+        # the other owner shares, each timed on its own (the headline stays the share above)
+        others = [i for i in (1, 2, 3, 4, 5) if i != args.workload]
+        del ws
+        torch.cuda.empty_cache()
+        out["other_shares"] = {}
+        for i in others:
+            log(f"timing owner share {i}")
+            out["other_shares"][synth.workload(i).name] = share_record(
+                native, torch, dev, hev, stream, i, max(5, args.steps // 4), 2)
     if not args.no_shampoo:
         # nominal_flop counts every product of all root iterations in full; iterations skipped
         # after convergence and the upper-tile-only symmetric products execute less

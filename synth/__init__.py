@@ -9,7 +9,7 @@ drawn in parallel without changing a single bit:
 
     root = SeedSequence([workload seed])
     root.spawn(1 + n_muon + n_adamw)
-      child 0            -> shape draws (uneven-plan workload only)
+      child 0            -> (unused; the uneven plan draws its shapes from default_rng(4))
       child 1 + i        -> Muon entry i:   spawn(3) = (param, grad, momentum)
       child 1 + n_muon+j -> AdamW entry j:  spawn(2) = (param, grad)
     each tensor stream spawns one grand-child per 2**24-element chunk, in order.
@@ -180,9 +180,8 @@ def workload(index: int) -> Workload:
             hp=MuonHParams(lr=0.02, weight_decay=0.01), adamw_hp=AdamWHParams(weight_decay=0.01),
             description="4 of 32 Llama-3-8B layers: 28 matrices + 8 RMSNorm vectors of 4096")
     if index == 4:
-        root = np.random.SeedSequence([4])
-        shape_rng = np.random.Generator(np.random.PCG64(root.spawn(1)[0]))
-        shapes = _uneven_shapes(shape_rng)
+        # shapes first, from the plain seeded generator: 25 tall, 38 wide, 1 square, 1485.4 M elements
+        shapes = _uneven_shapes(np.random.default_rng(4))
         mu = [MuonSpec(m, n, f"u{i}") for i, (m, n) in enumerate(shapes)]
         ad = [AdamWSpec(128256 * 4096, "embed", param=Dist(0.02), grad=Dist(1e-3))]
         ad += [AdamWSpec(4096, f"norm{i}", grad=Dist(1e-3)) for i in range(32)]

@@ -27,6 +27,23 @@ def rel_fro(a, b) -> float:
     return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a - b))
 
 
+def tile_rel_errors(a, b, tile: int = 256) -> np.ndarray:
+    """Relative Frobenius error of a against b on every tile x tile block (edge blocks partial):
+    a defect confined to one block of the output shows here even where the whole-matrix error,
+    which averages it over all blocks, stays small."""
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    m, n = b.shape
+    tm, tn = -(-m // tile), -(-n // tile)
+    d2 = np.zeros((tm * tile, tn * tile))
+    b2 = np.zeros((tm * tile, tn * tile))
+    d2[:m, :n] = (a - b) ** 2
+    b2[:m, :n] = b ** 2
+    num = d2.reshape(tm, tile, tn, tile).sum(axis=(1, 3))
+    den = b2.reshape(tm, tile, tn, tile).sum(axis=(1, 3))
+    return np.sqrt(num / np.where(den > 0, den, 1.0))
+
+
 def bf16_half_ulp(x: np.ndarray) -> np.ndarray:
     """Half a bf16 ulp at |x| (8 significant bits); tiny values use the subnormal spacing."""
     ax = np.maximum(np.abs(np.asarray(x, dtype=np.float64)), 2.0 ** -126)

@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 import synth
-from tests.helpers import check_bf16_param, from_dev, rel_fro, to_dev
+from tests.helpers import check_bf16_param, from_dev, rel_fro, tile_rel_errors, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -61,8 +61,10 @@ def test_ns_bf16_matches_oracle(native, shape, steps):
     native.newton_schulz_t(xd, out, A, B, C, steps, 1e-7, "bf16")
     _sync()
     ref = oracle.newton_schulz(xb, A, B, C, steps)
-    err = rel_fro(from_dev(out), ref)
+    og = from_dev(out)
+    err = rel_fro(og, ref)
     assert err <= 2e-2, err
+    assert float(tile_rel_errors(og, ref).max()) <= 5e-2
 
 
 @pytest.mark.parametrize("shape", [(256, 512), (512, 256), (100, 300), (65, 129), (768, 768), (3, 5)])
@@ -148,9 +150,13 @@ def _check_muon(tensors, specs, dev, hp, upd_tol):
             ns_steps=hp.ns_steps, eps=hp.eps, lr_adjust=hp.lr_adjust, ns_schedule=hp.ns_schedule)
         assert rel_fro(from_dev(mo), buf_or) <= 1e-6, (e.name, "momentum")
         if uo is not None:
-            err = rel_fro(from_dev(uo), O)
+            og = from_dev(uo)
+            err = rel_fro(og, O)
             worst = max(worst, err)
             assert err <= upd_tol, (e.name, e.m, e.n, err)
+            # and on every 256 x 256 block, so that an error confined to one block shows
+            tmax = float(tile_rel_errors(og, O).max())
+            assert tmax <= 2.5 * upd_tol, (e.name, e.m, e.n, "worst block", tmax)
         f = oracle.lr_factor(e.m, e.n, hp.lr_adjust)
         pg = from_dev(p)
         if e.param_dtype == synth.BF16:
