@@ -10,10 +10,18 @@ iterations, ridge 1e-6 ||S||_F), which the GPU reproduces to two digits:
   resolves only coarsely: emulation 2.4e-4, bar 5e-4.
 * P restricted to the gradient's range (P_L G, G P_R): 1e-4 (emulation <= 1.3e-5).
 * The whole P: 1e-4 for the well-conditioned side (the shorter side of a rectangular gradient);
-  else 5e-2. On a rank-deficient side the ridge directions carry rho^(-1/4), the largest
-  eigenvalues of P, and dominate ||P||_F; float32 resolves M's eigenvalue there (z rho ~ 2.5e-6)
-  against rounding noise that grows with sqrt(d), to a few percent (emulated 2.5e-3 at d = 256,
-  measured 1.4e-2 at d = 3072). Those directions never enter U of the same statistics.
+  else the ridge bar 2e-8 / eps_rel. On a rank-deficient side the null directions of S carry
+  rho^(-1/4), the largest eigenvalues of P, and dominate ||P||_F. The coupled iteration works on
+  M = z (S + rho I), whose eigenvalue there starts at z rho ~ eps_rel, so float32 rounding of M
+  (absolute, ~2^-24 ||M||) perturbs it by ~2^-24 / eps_rel relative: the condition number of
+  S + rho I is ~1 / eps_rel. A float32 emulation of the iteration gives a relative error of
+  (6.0-7.3e-9) / eps_rel in P there, independent of d from 256 to 1536 (6.7e-3 at eps_rel 1e-6,
+  6.6e-4 at 1e-5, 7e-5 at 1e-4); the GPU measured 1.4e-2 at d = 3072 and eps_rel 1e-6. The exact root
+  of the same float32-stored statistic is within 2-4e-4, so the limit is the iteration's float32
+  arithmetic at that condition number, not the statistic's storage. Those directions never enter
+  U of the same statistics; a stale step on a new gradient with components outside the statistic's
+  range does take them into U: its bar is the same ridge bar (emulation: the U error equals the
+  P error in those directions).
 * Statistics 1e-5 (fp32 sums). Parameters: bf16 rounding-aware (half an ulp plus the U bar times
   lr ||U||); fp32 parameters the U bar times lr ||U|| + 1e-6 ||p||.
 """
@@ -34,6 +42,12 @@ STAT_TOL = 1e-5
 
 def _u_tol(m, n):
     return U_TOL if min(m, n) <= 0.75 * max(m, n) else 5e-4
+
+
+def _ridge_tol(eps_rel):
+    """Relative accuracy of P in the null directions of a rank-deficient statistic (float32
+    iteration at condition number ~1 / eps_rel; see the module docstring)."""
+    return max(U_TOL, 2e-8 / eps_rel)
 
 
 def _say(msg):
@@ -151,8 +165,8 @@ def _check(mat, hp, check_p=True):
         PL, PR = from_dev(mat.dPL), from_dev(mat.dPR)
         assert rel_fro(PL @ G, mat.PL @ G) <= U_TOL, ("PL G", rel_fro(PL @ G, mat.PL @ G))
         assert rel_fro(G @ PR, G @ mat.PR) <= U_TOL, ("G PR", rel_fro(G @ PR, G @ mat.PR))
-        tol_l = 1e-4 if mat.m <= 0.75 * mat.n else 5e-2
-        tol_r = 1e-4 if mat.n <= 0.75 * mat.m else 5e-2
+        tol_l = 1e-4 if mat.m <= 0.75 * mat.n else _ridge_tol(hp.eps_rel)
+        tol_r = 1e-4 if mat.n <= 0.75 * mat.m else _ridge_tol(hp.eps_rel)
         assert rel_fro(PL, mat.PL) <= tol_l, ("PL", rel_fro(PL, mat.PL))
         assert rel_fro(PR, mat.PR) <= tol_r, ("PR", rel_fro(PR, mat.PR))
     if check_p:
@@ -237,6 +251,52 @@ def test_shampoo_stale_preconditioners(native):
         assert rel_fro(from_dev(x.dU), x.U_or) <= 1e-5
         assert bool((x.dPL == kl).all()) and bool((x.dPR == kr).all())
         _check(x, hpo)
+
+
+@pytest.mark.parametrize("eps_rel", [1e-6, 1e-4])
+@pytest.mark.parametrize("dts", [(synth.BF16, synth.BF16), (synth.F32, synth.F32)])
+def test_shampoo_stale_step_on_new_gradient_after_rank_deficient_refresh(native, eps_rel, dts):
+    """Refresh from a rank-deficient left statistic (768 x 768 of rank 192), then a stale step
+    (refresh = 0) on a new gradient whose columns lie mostly outside that statistic's range, so
+    that P_L's null directions (eigenvalue rho^(-1/4)) dominate U. Compared with the oracle's stale
+    step from its own fp64 preconditioners; U within the ridge bar."""
+    import torch
+    m, n = 768, 192
+    _say(f"shampoo stale step on a new gradient, eps_rel {eps_rel:g}, {dts}")
+    rng = np.random.default_rng(4100 + int(-np.log10(eps_rel)) + 10 * (dts[0] == synth.F32))
+    mat = _Mat(rng, m, n, *dts).device()
+    hpn, hpo = _hp(native, eps_rel=eps_rel, beta=0.95, weight=0.05)
+    ws = native.shampoo_workspace_t([mat.entry(native)], hpn)
+    native.shampoo_step_t([mat.entry(native)], hpn, ws)
+    _sync()
+    _oracle_step(mat, hpo)
+    _check(mat, hpo)
+    # the new gradient: its share of U that comes from outside the first statistic's range
+    g2 = synth.random_muon_tensors(rng, m, n, dts[0], dts[1]).grad
+    G1, G2 = OS._f64(mat.g), OS._f64(g2)
+    Q, _ = np.linalg.qr(G1)
+    outside = G2 - Q @ (Q.T @ G2)
+    share = np.linalg.norm(mat.PL @ outside @ mat.PR) / np.linalg.norm(mat.PL @ G2 @ mat.PR)
+    assert share > 0.9, share
+    mat.g = g2
+    mat.dg.copy_(to_dev(g2, mat.gdt))
+    hpn2, hpo2 = _hp(native, eps_rel=eps_rel, beta=0.95, weight=0.05, refresh=False)
+    pl0, pr0 = mat.dPL.clone(), mat.dPR.clone()
+    native.shampoo_step_t([mat.entry(native)], hpn2, ws)
+    _sync()
+    _oracle_step(mat, hpo2)
+    eu = rel_fro(from_dev(mat.dU), mat.U_or)
+    bar = _ridge_tol(eps_rel)
+    _say(f"  stale U rel err {eu:.3e} (bar {bar:.1e}; share of U outside the old range {share:.3f})")
+    assert eu <= bar, eu
+    assert torch.equal(pl0, mat.dPL) and torch.equal(pr0, mat.dPR)   # read, not written
+    assert rel_fro(from_dev(mat.dL), mat.L) <= STAT_TOL
+    assert rel_fro(from_dev(mat.dR), mat.R) <= STAT_TOL
+    pg, un = from_dev(mat.dp), hpo2.lr * np.linalg.norm(mat.U_or)
+    if mat.pdt == synth.BF16:
+        assert check_bf16_param(pg, mat.p_or, un, bar) <= 1.0
+    else:
+        assert np.linalg.norm(pg - mat.p_or) <= bar * un + 1e-6 * np.linalg.norm(mat.p_or)
 
 
 def test_shampoo_lr_zero_and_determinism(native):
