@@ -1,0 +1,80 @@
+// Tile schedules of the grouped NS products (host side; plain C++ with no HIP dependency, so that
+// the CPU tests can build and check it on its own).
+#pragma once
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+namespace mfsdp {
+
+// One output tile of a grouped NS product: problem (matrix) index and 256 x 256 block coordinates;
+// e < 0 marks an idle slot. The bf16 NS kernels run a persistent grid of kGemmXcds x
+// kGemmSlots workgroups; workgroup b serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes
+// tile sched[g * kGemmSlots + slot] of every group g = xcd, xcd + kGemmXcds, ...
+struct TileRef {
+  int32_t e;
+  int16_t bi, bj;
+};
+constexpr int kGemmXcds = 8;    // MI355X: 8 XCDs (workgroups are dealt to them round robin)
+constexpr int kGemmSlots = 32;  // CUs per XCD = tiles per group
+constexpr int kGroupRows = 4;   // a group covers 4 block rows x 8 block columns of one matrix
+
+// Per-problem tile grid of one NS product (256 x 256 tiles on the bf16 path).
+struct TileGrid {
+  int tm, tn;
+  bool sym;
+};
+
+// Tile schedule of one product for the persistent bf16 kernel. Tiles are put in locality order
+// (bands of kGroupRows block rows, within a band column by column, upper triangle only for
+// symmetric products) and cut into groups of kGemmSlots tiles, so that the workgroups of one XCD
+// run the tiles of a group together and share its operand blocks in L2. Groups are then dealt to
+// the XCDs longest first, each to the XCD with the least work so far (a group's cost is the
+// largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
+// g % kGemmXcds; XCDs with fewer groups get empty ones (every slot e = -1).
+inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
+                                           const std::vector<int64_t>& cost) {
+  std::vector<TileRef> flat;
+  for (int e : order) {
+    const TileGrid& g = grids[e];
+    for (int r0 = 0; r0 < g.tm; r0 += kGroupRows) {
+      const int r1 = std::min(g.tm, r0 + kGroupRows);
+      for (int c = g.sym ? r0 : 0; c < g.tn; ++c)
+        for (int r = r0; r < r1; ++r)
+          if (!g.sym || r <= c) flat.push_back(TileRef{e, int16_t(r), int16_t(c)});
+    }
+  }
+  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0});
+  const size_t ng = flat.size() / kGemmSlots;
+  std::vector<int64_t> gcost(ng, 0);
+  for (size_t g = 0; g < ng; ++g)
+    for (int s = 0; s < kGemmSlots; ++s) {
+      const TileRef& t = flat[g * kGemmSlots + s];
+      if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e]);
+    }
+  std::vector<size_t> by(ng);
+  for (size_t g = 0; g < ng; ++g) by[g] = g;
+  std::stable_sort(by.begin(), by.end(), [&](size_t x, size_t y) { return gcost[x] > gcost[y]; });
+  std::vector<std::vector<size_t>> lists(kGemmXcds);
+  int64_t load[kGemmXcds] = {};
+  for (size_t g : by) {
+    int best = 0;
+    for (int x = 1; x < kGemmXcds; ++x)
+      if (load[x] < load[best]) best = x;
+    lists[best].push_back(g);
+    load[best] += gcost[g];
+  }
+  size_t rounds = 0;
+  for (const auto& l : lists) rounds = std::max(rounds, l.size());
+  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0});
+  for (int x = 0; x < kGemmXcds; ++x)
+    for (size_t i = 0; i < lists[x].size(); ++i)
+      std::memcpy(&s[(i * kGemmXcds + x) * kGemmSlots], &flat[lists[x][i] * kGemmSlots],
+                  kGemmSlots * sizeof(TileRef));
+  return s;
+}
+
+}  // namespace mfsdp

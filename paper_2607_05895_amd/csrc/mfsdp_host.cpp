@@ -104,60 +104,6 @@ struct DescLayout {
   int ngroups[3];
 };
 
-// Per-problem tile shape of the three NS products (tiles of kTileBF16 / kTileF32).
-struct TileGrid {
-  int tm, tn;
-  bool sym;
-};
-
-// Tile schedule of one product for the persistent bf16 kernel. Tiles are put in locality order
-// (bands of kGroupRows block rows, within a band column by column, upper triangle only for
-// symmetric products) and cut into groups of kGemmSlots tiles, so that the workgroups of one XCD
-// run the tiles of a group together and share its operand blocks in L2. Groups are then dealt to
-// the XCDs longest first, each to the XCD with the least work so far (a group's cost is the
-// largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
-// g % kGemmXcds; XCDs with fewer groups get empty ones (every slot e = -1).
-std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
-                                    const std::vector<int64_t>& cost) {
-  std::vector<TileRef> flat;
-  for (int e : order) {
-    const TileGrid& g = grids[e];
-    for (int r0 = 0; r0 < g.tm; r0 += kGroupRows) {
-      const int r1 = std::min(g.tm, r0 + kGroupRows);
-      for (int c = g.sym ? r0 : 0; c < g.tn; ++c)
-        for (int r = r0; r < r1; ++r)
-          if (!g.sym || r <= c) flat.push_back(TileRef{e, int16_t(r), int16_t(c)});
-    }
-  }
-  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0});
-  const size_t ng = flat.size() / kGemmSlots;
-  std::vector<int64_t> gcost(ng, 0);
-  for (size_t g = 0; g < ng; ++g)
-    for (int s = 0; s < kGemmSlots; ++s) {
-      const TileRef& t = flat[g * kGemmSlots + s];
-      if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e]);
-    }
-  std::vector<size_t> by(ng);
-  for (size_t g = 0; g < ng; ++g) by[g] = g;
-  std::stable_sort(by.begin(), by.end(), [&](size_t x, size_t y) { return gcost[x] > gcost[y]; });
-  std::vector<std::vector<size_t>> lists(kGemmXcds);
-  int64_t load[kGemmXcds] = {};
-  for (size_t g : by) {
-    int best = 0;
-    for (int x = 1; x < kGemmXcds; ++x)
-      if (load[x] < load[best]) best = x;
-    lists[best].push_back(g);
-    load[best] += gcost[g];
-  }
-  size_t rounds = 0;
-  for (const auto& l : lists) rounds = std::max(rounds, l.size());
-  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0});
-  for (int x = 0; x < kGemmXcds; ++x)
-    for (size_t i = 0; i < lists[x].size(); ++i)
-      std::memcpy(&s[(i * kGemmXcds + x) * kGemmSlots], &flat[lists[x][i] * kGemmSlots],
-                  kGemmSlots * sizeof(TileRef));
-  return s;
-}
 
 DescLayout plan_descs(int64_t count, const size_t sched_bytes[3]) {
   DescLayout d{};

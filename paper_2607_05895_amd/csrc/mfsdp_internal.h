@@ -25,6 +25,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "gemm_schedule.h"
+
 namespace mfsdp {
 
 // Element (r, k) of a panel-blocked buffer with K columns (K a multiple of 32, rows a multiple of
@@ -115,18 +117,6 @@ struct GemmDesc {
   // standalone NS output) from the fp32 accumulators instead of storing the final iterate
   const ApplyDesc* fused;
 };
-
-// One output tile of a grouped NS product: problem (matrix) index and 256 x 256 block coordinates;
-// e < 0 marks an idle slot. The bf16 NS kernels run a persistent grid of kGemmXcds x
-// kGemmSlots workgroups; workgroup b serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes
-// tile sched[g * kGemmSlots + slot] of every group g = xcd, xcd + kGemmXcds, ...
-struct TileRef {
-  int32_t e;
-  int16_t bi, bj;
-};
-constexpr int kGemmXcds = 8;    // MI355X: 8 XCDs (workgroups are dealt to them round robin)
-constexpr int kGemmSlots = 32;  // CUs per XCD = tiles per group
-constexpr int kGroupRows = 4;   // a group covers 4 block rows x 8 block columns of one matrix
 
 constexpr int kAdamWMaxPerLaunch = 32;
 struct AdamWDesc {

@@ -186,6 +186,25 @@ def test_muon_gpt2_small_share(native):
     _check_muon(tensors, wl.muon, dev, wl.hp, 2e-2)
 
 
+@pytest.mark.parametrize("shape", [(2048, 4096), (4096, 2048), (1024, 4096), (2048, 2048)])
+def test_muon_single_matrix_few_tiles(native, shape):
+    """One matrix alone in a call, so that each launch has fewer tiles than the GPU has CUs
+    (2048 x 4096: 36 / 36 / 128 tiles, wide and tall, the last update with the fused parameter
+    update). Matches the oracle and is bitwise reproducible."""
+    import torch
+    m, n = shape
+    _say(f"muon single matrix {m}x{n}")
+    rng = np.random.default_rng(5000 + m + n)
+    specs = [synth.MuonSpec(m, n, f"s{m}x{n}")]
+    tensors = [synth.random_muon_tensors(rng, m, n)]
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
+    dev = _run_muon(native, tensors, specs, hp)
+    _check_muon(tensors, specs, dev, hp, 2e-2)
+    dev2 = _run_muon(native, tensors, specs, hp)
+    for a, b in zip(dev[0], dev2[0]):
+        assert torch.equal(a, b)
+
+
 MIXED = [(256, 512), (512, 256), (384, 384), (100, 700), (700, 100), (130, 1000), (1, 50),
          (50, 1), (768, 3072), (3072, 768)]
 
