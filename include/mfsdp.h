@@ -421,6 +421,29 @@ int mfsdp_plan_owners(const mfsdp_plan_param* params, int64_t count, int32_t wor
                       double gamma_cap, int32_t* owner, int64_t* rank_load, double* block_gamma,
                       int32_t* policy_used);
 
+/* Per-block MatrixShard layouts of an owner plan (Section 4.1: a rank-indexed placement of each
+ * flattened parameter interval; the last step of Algorithm 1: one layout per block, each validated
+ * for one contiguous local segment per parameter). Layout rules (the paper fixes no packing order):
+ * a block's canonical axis concatenates its parameters' elements in parameter order; rank r's
+ * local buffer for block b holds the roles of b that r owns, ordered by each role's first parameter
+ * index, a matrix whole and the block's tail as its non-2D tensors packed in parameter order; every
+ * other rank's segment of a parameter is empty.
+ *   params, count   as for mfsdp_plan_owners (host memory, read only); count == 0 is valid
+ *   world           shard span, 1 .. 65536
+ *   owner           count owner ranks (host, read only), e.g. from mfsdp_plan_owners
+ *   global_offset   out, count int64: parameter i's offset on its block's canonical axis
+ *   local_offset    out, count int64: parameter i's offset in its owner's local buffer of its block
+ *   block_rank_len  optional out (NULL = off), (1 + max block index) * world int64: entry
+ *                   b * world + r is rank r's local buffer length in block b
+ * The emitted layout is validated (every rank's segments tile its local buffer of every block with
+ * no gap or overlap, the tail is one packed segment, a block's local buffers add up to its
+ * canonical axis). Returns MFSDP_OK or MFSDP_E_INVALID (NULL, world out of range, bad parameter,
+ * owner out of range, a block's non-2D tensors with different owners, a failed validation); the
+ * outputs are unspecified on error. Thread safe; deterministic; host only. */
+int mfsdp_plan_layouts(const mfsdp_plan_param* params, int64_t count, int32_t world,
+                       const int32_t* owner, int64_t* global_offset, int64_t* local_offset,
+                       int64_t* block_rank_len);
+
 /* Text for the last failure on the calling thread ("" if none). */
 const char* mfsdp_last_error(void);
 /* Name of a status code. */

@@ -19,6 +19,15 @@ Readings (the paper gives no tie rules and no cap definition):
 * RoleGreedy visits blocks in increasing block index;
 * "balance improves" means a strictly smaller maximum rank load; the workspace cap bounds gamma_B
   of every block (cap <= 0: no cap).
+
+Layouts (Section 4.1, "MatrixShard": a rank-indexed placement of each flattened parameter interval;
+Algorithm 1's last step: one layout per block, validated for one contiguous local segment per
+parameter). Readings (the paper does not fix the packing order):
+* a block's canonical axis is its parameters' flattened elements concatenated in parameter order;
+* a rank's local buffer for a block holds the roles of that block it owns, ordered by each role's
+  first parameter index; a matrix role is the whole matrix, the tail role the block's non-2D
+  tensors packed in parameter order (one whole segment on the tail owner);
+* a parameter's local segment on any other rank is empty.
 """
 from __future__ import annotations
 
@@ -119,3 +128,69 @@ def validate(params, owner: Sequence[int], world: int) -> None:
         if not is_matrix:
             if tails.setdefault(blk, r) != r:
                 raise ValueError("a block's tail is split across ranks")
+
+
+def layouts(params, owner: Sequence[int], world: int):
+    """Per-block MatrixShard layouts of a plan. Returns (global_offset, local_offset, lengths):
+    global_offset[i] and local_offset[i] are parameter i's offsets on its block's canonical axis and
+    in its owner's local buffer of that block; lengths[b][r] is rank r's local buffer length in
+    block b (blocks 0 .. max block)."""
+    validate(params, owner, world)
+    nblocks = 1 + max((p[0] for p in params), default=-1)
+    lengths = [[0] * world for _ in range(nblocks)]
+    canon = [0] * nblocks
+    global_offset = [0] * len(params)
+    local_offset = [0] * len(params)
+    # canonical axis: parameter order within each block
+    for i, (blk, numel, _) in enumerate(params):
+        global_offset[i] = canon[blk]
+        canon[blk] += numel
+    # local buffers: roles in the order of their first parameter index
+    roles = sorted(build_roles(params), key=lambda r: r[3][0])
+    for blk, numel, _, idx in roles:
+        r = owner[idx[0]]
+        pos = lengths[blk][r]
+        for i in idx:                 # one parameter (a matrix), or the tail in parameter order
+            local_offset[i] = pos
+            pos += params[i][1]
+        lengths[blk][r] = pos
+    return global_offset, local_offset, lengths
+
+
+def validate_layouts(params, owner: Sequence[int], world: int, global_offset, local_offset, lengths) -> None:
+    """Algorithm 1's last step: every parameter is one contiguous segment of its numel on its owner
+    (empty elsewhere); every rank's segments tile its local buffer of each block exactly; a block's
+    tail is one contiguous segment in parameter order; the local buffers of a block hold its whole
+    canonical axis, whose intervals tile [0, P_B) in parameter order."""
+    validate(params, owner, world)
+    nblocks = 1 + max((p[0] for p in params), default=-1)
+    if len(lengths) != nblocks or any(len(row) != world for row in lengths):
+        raise ValueError("one row of rank lengths per block")
+    canon = [0] * nblocks
+    segs = {}
+    for i, (blk, numel, _) in enumerate(params):
+        if global_offset[i] != canon[blk]:
+            raise ValueError(f"parameter {i}: canonical interval out of order")
+        canon[blk] += numel
+        segs.setdefault((blk, owner[i]), []).append((local_offset[i], numel, i))
+    for b in range(nblocks):
+        if sum(lengths[b]) != canon[b]:
+            raise ValueError(f"block {b}: local buffers hold {sum(lengths[b])} of {canon[b]} elements")
+        for r in range(world):
+            pos = 0
+            # at one offset, empty segments first (an empty tail tensor may share its offset with
+            # the role that follows the tail)
+            for off, numel, i in sorted(segs.get((b, r), []), key=lambda t: (t[0], t[1] > 0, t[2])):
+                if off != pos:
+                    raise ValueError(f"block {b} rank {r}: parameter {i} at {off}, expected {pos}")
+                pos += numel
+            if pos != lengths[b][r]:
+                raise ValueError(f"block {b} rank {r}: segments cover {pos} of {lengths[b][r]}")
+    tails = {}
+    for i, (blk, numel, is_matrix) in enumerate(params):
+        if not is_matrix:
+            tails.setdefault(blk, []).append(i)
+    for blk, idx in tails.items():
+        for a, b in zip(idx, idx[1:]):
+            if local_offset[b] != local_offset[a] + params[a][1]:
+                raise ValueError(f"block {blk}: tail not packed in parameter order")

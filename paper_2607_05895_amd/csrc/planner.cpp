@@ -186,3 +186,93 @@ extern "C" int mfsdp_plan_owners(const mfsdp_plan_param* params, int64_t count, 
   if (policy_used) *policy_used = used;
   return MFSDP_OK;
 }
+
+// Per-block MatrixShard layouts of a plan (Section 4.1; the last step of Algorithm 1). A block's
+// canonical axis concatenates its parameters in parameter order; a rank's local buffer for a block
+// holds the roles of that block it owns in the order of each role's first parameter index (a
+// matrix whole, the tail's tensors packed in parameter order). The emitted layout is then
+// validated: per rank and block the segments tile the local buffer exactly, the tail is packed in
+// parameter order, and the block's local buffers hold its whole canonical axis.
+extern "C" int mfsdp_plan_layouts(const mfsdp_plan_param* params, int64_t count, int32_t world,
+                                  const int32_t* owner, int64_t* global_offset, int64_t* local_offset,
+                                  int64_t* block_rank_len) {
+  using mfsdp::set_last_error;
+  if (count < 0) return set_last_error(MFSDP_E_INVALID, "count must be >= 0");
+  if (count > 0 && (!params || !owner || !global_offset || !local_offset))
+    return set_last_error(MFSDP_E_INVALID, "params, owner and the offset arrays must be non-NULL");
+  if (world < 1 || world > (1 << 16)) return set_last_error(MFSDP_E_INVALID, "world must be in [1, 65536]");
+  int32_t nblocks = 0;
+  std::unordered_map<int32_t, int32_t> tail_owner;
+  std::unordered_map<int32_t, int64_t> tail_numel;
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_plan_param& p = params[i];
+    if (p.block < 0 || p.numel < 0 || (p.is_matrix != 0 && p.is_matrix != 1))
+      return set_last_error(MFSDP_E_INVALID, "param " + std::to_string(i) + ": block and numel must be >= 0, is_matrix 0 or 1");
+    if (owner[i] < 0 || owner[i] >= world)
+      return set_last_error(MFSDP_E_INVALID, "param " + std::to_string(i) + ": owner out of range");
+    if (!p.is_matrix) {
+      auto it = tail_owner.emplace(p.block, owner[i]).first;
+      if (it->second != owner[i])
+        return set_last_error(MFSDP_E_INVALID, "block " + std::to_string(p.block) + ": its tail is split across ranks");
+      tail_numel[p.block] += p.numel;
+    }
+    nblocks = std::max(nblocks, p.block + 1);
+  }
+  std::unordered_map<int32_t, int64_t> canon;                 // block -> canonical length so far
+  std::unordered_map<int64_t, int64_t> len;                   // block * world + rank -> local length
+  std::unordered_map<int32_t, int64_t> tail_pos;              // block -> next tail offset
+  for (int64_t i = 0; i < count; ++i) {
+    const mfsdp_plan_param& p = params[i];
+    global_offset[i] = canon[p.block];
+    canon[p.block] += p.numel;
+    const int64_t key = int64_t(p.block) * world + owner[i];
+    if (p.is_matrix) {
+      local_offset[i] = len[key];
+      len[key] += p.numel;
+    } else {
+      auto it = tail_pos.find(p.block);
+      if (it == tail_pos.end()) {  // the tail role starts at its first tensor: reserve all of it
+        it = tail_pos.emplace(p.block, len[key]).first;
+        len[key] += tail_numel[p.block];
+      }
+      local_offset[i] = it->second;
+      it->second += p.numel;
+    }
+  }
+  // validation: segments tile every local buffer, the tail is packed in parameter order, and the
+  // local buffers of a block add up to its canonical axis
+  std::unordered_map<int64_t, std::vector<std::pair<std::pair<int64_t, int>, int64_t>>> segs;
+  for (int64_t i = 0; i < count; ++i)
+    segs[int64_t(params[i].block) * world + owner[i]].push_back({{local_offset[i], params[i].numel > 0 ? 1 : 0}, i});
+  for (auto& kv : segs) {
+    auto& v = kv.second;
+    std::sort(v.begin(), v.end());
+    int64_t pos = 0;
+    for (const auto& sg : v) {
+      if (sg.first.first != pos)
+        return set_last_error(MFSDP_E_INVALID, "layout: parameter " + std::to_string(sg.second) + " leaves a gap or overlaps");
+      pos += params[sg.second].numel;
+    }
+    if (pos != len[kv.first]) return set_last_error(MFSDP_E_INVALID, "layout: local buffer not covered");
+  }
+  std::unordered_map<int32_t, int64_t> last_tail;  // block -> index of the previous tail tensor
+  std::unordered_map<int32_t, int64_t> local_sum;
+  for (const auto& kv : len) local_sum[int32_t(kv.first / world)] += kv.second;
+  for (int64_t i = 0; i < count; ++i) {
+    if (params[i].is_matrix) continue;
+    auto it = last_tail.find(params[i].block);
+    if (it != last_tail.end() && local_offset[i] != local_offset[it->second] + params[it->second].numel)
+      return set_last_error(MFSDP_E_INVALID, "layout: tail of block " + std::to_string(params[i].block) + " not packed");
+    last_tail[params[i].block] = i;
+  }
+  for (const auto& kv : canon)
+    if (local_sum[kv.first] != kv.second) return set_last_error(MFSDP_E_INVALID, "layout: block not covered");
+  if (block_rank_len) {
+    for (int64_t b = 0; b < nblocks; ++b)
+      for (int32_t r = 0; r < world; ++r) {
+        auto it = len.find(b * world + r);
+        block_rank_len[b * world + r] = it == len.end() ? 0 : it->second;
+      }
+  }
+  return MFSDP_OK;
+}

@@ -24,7 +24,7 @@ EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_time
            "mfsdp_shampoo_workspace_size", "mfsdp_shampoo_step", "mfsdp_inverse_root_workspace_size",
            "mfsdp_inverse_root", "mfsdp_soap_workspace_size", "mfsdp_soap_step",
            "mfsdp_orthonormal_factor_workspace_size", "mfsdp_orthonormal_factor", "mfsdp_build_id",
-           "mfsdp_muon_step_noalloc")
+           "mfsdp_muon_step_noalloc", "mfsdp_plan_layouts")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 MAX_GRAD_PARTS = 64
 ABI_VERSION = 6
@@ -143,6 +143,9 @@ def lib() -> ctypes.CDLL:
         L.mfsdp_plan_owners.argtypes = [ctypes.POINTER(PlanParam), i64, i32, i32, f64, ctypes.POINTER(i32),
                                         ctypes.POINTER(i64), ctypes.POINTER(f64), ctypes.POINTER(i32)]
         L.mfsdp_plan_owners.restype = ctypes.c_int
+        L.mfsdp_plan_layouts.argtypes = [ctypes.POINTER(PlanParam), i64, i32, ctypes.POINTER(i32),
+                                         ctypes.POINTER(i64), ctypes.POINTER(i64), ctypes.POINTER(i64)]
+        L.mfsdp_plan_layouts.restype = ctypes.c_int
         L.mfsdp_shampoo_workspace_size.argtypes = [ctypes.POINTER(ShampooEntry), i64, ctypes.POINTER(ShampooHParams)]
         L.mfsdp_shampoo_workspace_size.restype = sz
         L.mfsdp_shampoo_step.argtypes = [ctypes.POINTER(ShampooEntry), i64, ctypes.POINTER(ShampooHParams), vp,
@@ -212,6 +215,21 @@ def mfsdp_plan_owners(params, world: int, policy: int, gamma_cap: float = 0.0):
     _check(lib().mfsdp_plan_owners(arr, len(params), world, policy, gamma_cap, owner, loads, gam,
                                    ctypes.byref(used)))
     return list(owner[:len(params)]), list(loads[:world]), list(gam[:nblocks]), used.value
+
+
+def mfsdp_plan_layouts(params, world: int, owner):
+    """params: (block, numel, is_matrix) per parameter; owner: one rank per parameter. Returns
+    (global offsets, local offsets, per-block lists of the ranks' local buffer lengths). Host only."""
+    params = list(params)
+    n = len(params)
+    arr = (PlanParam * max(1, n))(*[PlanParam(int(b), int(bool(mx)), int(k)) for b, k, mx in params])
+    own = (ctypes.c_int32 * max(1, n))(*[int(o) for o in owner])
+    nblocks = 1 + max((int(b) for b, _, _ in params), default=-1)
+    g = (ctypes.c_int64 * max(1, n))()
+    loc = (ctypes.c_int64 * max(1, n))()
+    lens = (ctypes.c_int64 * max(1, nblocks * world))()
+    _check(lib().mfsdp_plan_layouts(arr, n, world, own, g, loc, lens))
+    return list(g[:n]), list(loc[:n]), [list(lens[b * world:(b + 1) * world]) for b in range(nblocks)]
 
 
 def mfsdp_shampoo_workspace_size(entries: Sequence[ShampooEntry], hp: ShampooHParams) -> int:

@@ -30,6 +30,10 @@ def _check(params, world, policy, cap=0.0):
     assert got[2] == exp[2], "gamma_B (bitwise: same evaluation order in double)"
     assert got[3] == exp[3], "policy used"
     P.validate(params, got[0], world)
+    # the per-block layouts of the plan, bit for bit, and valid
+    lay = native.mfsdp_plan_layouts(params, world, got[0])
+    assert lay == tuple(P.layouts(params, got[0], world)), "layouts"
+    P.validate_layouts(params, got[0], world, *lay)
     return got
 
 
@@ -104,3 +108,20 @@ def test_invalid_arguments_rejected():
     arr = (native.PlanParam * 1)(native.PlanParam(0, 1, 1))
     st = native.lib().mfsdp_plan_owners(arr, 1, 2, 0, 0.0, None, None, None, None)
     assert st == native.E_INVALID
+
+
+def test_layouts_hand_worked_and_rejections():
+    params = [(0, 4, False), (0, 6, True), (0, 2, False), (0, 8, True)]
+    assert native.mfsdp_plan_layouts(params, 2, [1, 1, 1, 0]) == ([0, 4, 10, 12], [0, 6, 4, 0], [[8, 12]])
+    assert native.mfsdp_plan_layouts([], 3, []) == ([], [], [])
+    with pytest.raises(native.MfsdpError, match="tail is split"):
+        native.mfsdp_plan_layouts(params, 2, [1, 1, 0, 0])
+    with pytest.raises(native.MfsdpError, match="owner out of range"):
+        native.mfsdp_plan_layouts(params, 2, [1, 1, 1, 2])
+    with pytest.raises(native.MfsdpError, match="world"):
+        native.mfsdp_plan_layouts(params, 0, [0, 0, 0, 0])
+    # sparse block indices and empty tensors: blocks without parameters get all-zero rows
+    params = [(3, 5, True), (3, 0, False), (1, 2, False), (1, 0, True)]
+    lay = native.mfsdp_plan_layouts(params, 2, [1, 0, 0, 1])
+    assert lay == tuple(P.layouts(params, [1, 0, 0, 1], 2))
+    assert lay[2][0] == [0, 0] and lay[2][2] == [0, 0]

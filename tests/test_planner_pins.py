@@ -94,3 +94,72 @@ def test_cost_aware_respects_the_cap():
     worst = max(P.block_gamma(params, sg, 2).values())
     assert P.plan(params, 2, P.COST_AWARE, cap=worst)[1] == P.SCOPE_GREEDY
     assert P.plan(params, 2, P.COST_AWARE, cap=worst * 0.99)[1] == P.ROLE_GREEDY
+
+
+# ------------------------------------------------------------------ per-block layouts (Section 4.1)
+
+def test_layouts_hand_worked():
+    params = [(0, 10, True), (0, 5, True), (0, 3, False), (1, 7, True)]
+    owner = [0, 1, 0, 1]                      # the ScopeGreedy plan worked above
+    g, l, lens = P.layouts(params, owner, 2)
+    # block 0 canonical: [0, 10) [10, 15) [15, 18); block 1: [0, 7)
+    assert g == [0, 10, 15, 0]
+    # rank 0 holds the matrix of 10 (first index 0) then the tail (first index 2); rank 1 the 5
+    assert l == [0, 0, 10, 0]
+    assert lens == [[13, 5], [0, 7]]
+    P.validate_layouts(params, owner, 2, g, l, lens)
+
+
+def test_layouts_tail_packed_before_a_later_matrix():
+    # non-2D tensors at indices 0 and 2 around a matrix: the tail (first index 0) comes first in its
+    # owner's buffer and its two tensors are packed next to each other
+    params = [(0, 4, False), (0, 6, True), (0, 2, False), (0, 8, True)]
+    owner, _ = P.plan(params, 2, P.SCOPE_GREEDY)
+    assert owner == [1, 1, 1, 0]              # 8 -> r0; matrix 6 (before the tail of 6 on ties) -> r1; tail -> r1
+    g, l, lens = P.layouts(params, owner, 2)
+    assert g == [0, 4, 10, 12]
+    assert l == [0, 6, 4, 0]
+    assert lens == [[8, 12]]
+    P.validate_layouts(params, owner, 2, g, l, lens)
+
+
+def test_layouts_of_random_plans_are_valid():
+    rng = np.random.default_rng(70)
+    for _ in range(200):
+        n = int(rng.integers(0, 25))
+        params = [(int(rng.integers(0, 5)), int(rng.integers(0, 50)), bool(rng.integers(0, 2))) for _ in range(n)]
+        world = int(rng.integers(1, 7))
+        for pol in (P.ROLE_GREEDY, P.SCOPE_GREEDY):
+            owner, _ = P.plan(params, world, pol)
+            g, l, lens = P.layouts(params, owner, world)
+            P.validate_layouts(params, owner, world, g, l, lens)
+            # rank r's buffers over all blocks hold exactly its load
+            assert [sum(lens[b][r] for b in range(len(lens))) for r in range(world)] == P.rank_loads(params, owner, world)
+
+
+def test_layout_validation_rejects_broken_layouts():
+    params = [(0, 10, True), (0, 5, True), (0, 3, False), (0, 2, False), (1, 7, True)]
+    owner = [0, 1, 0, 0, 1]
+    g, l, lens = P.layouts(params, owner, 2)
+    P.validate_layouts(params, owner, 2, g, l, lens)
+    bad = list(l)
+    bad[1] += 1                               # a gap in rank 1's buffer
+    with pytest.raises(ValueError):
+        P.validate_layouts(params, owner, 2, g, bad, lens)
+    bad = list(l)
+    bad[2], bad[3] = l[3], l[2]               # the tail out of parameter order
+    with pytest.raises(ValueError):
+        P.validate_layouts(params, owner, 2, g, bad, lens)
+    with pytest.raises(ValueError):
+        P.validate_layouts(params, owner, 2, g, l, [[13, 5], [0, 8]])
+    with pytest.raises(ValueError):
+        P.layouts(params, [0, 1, 0, 1, 1], 2)  # the block's tail split across ranks
+
+
+def test_layouts_with_empty_tensors():
+    # an empty tail tensor after a matrix in parameter order, but packed with the tail before it
+    params = [(0, 3, False), (0, 4, True), (0, 0, False), (0, 0, True)]
+    owner = [0, 0, 0, 0]
+    g, l, lens = P.layouts(params, owner, 1)
+    assert g == [0, 3, 7, 7] and l == [0, 3, 3, 7] and lens == [[7]]
+    P.validate_layouts(params, owner, 1, g, l, lens)
