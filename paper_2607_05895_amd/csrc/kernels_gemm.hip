@@ -188,7 +188,10 @@ struct TileCtx {
 // Product kinds of one NS step (one launch each); the epilogue is specialised per kind.
 constexpr int kProdGram = 0;    // A = X X^T: symmetric, mirror stores
 constexpr int kProdSquare = 1;  // B' = c A A + b A + a I: symmetric, addend E = A, diagonal term
-constexpr int kProdUpdate = 2;  // X' = B' X: stores X' and X'^T, or the fused parameter update
+constexpr int kProdUpdate = 2;  // X' = B' X: stores X' and X'^T
+constexpr int kProdApply = 3;   // the last X' = B' X, applying the parameter update (or writing the
+                                // standalone NS output) instead of storing X'; its own instantiation,
+                                // so that each update kernel carries only its own epilogue
 
 // (ca, cb, cc): this NS step's coefficients; the square product uses them as diagonal term, addend
 // factor and product factor (B' = cc A A + cb A + ca I).
@@ -347,8 +350,6 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     // stages, and every wave must be done reading LDS (its last fragments were consumed by MFMAs).
     MFSDP_WAIT_VMCNT(0);
     __builtin_amdgcn_s_barrier();
-    // the epilogue stages its output through LDS unless it applies the fused parameter update
-    const bool staged = !(PK == kProdUpdate && last && cur.d->fused);
     if (has_next) prologue(nxt);  // overlaps the epilogue below (it leaves stage NSTAGE-1 free)
 
     // Epilogue (global-address-space accesses: flat ones would also hold lgkmcnt, which the next
@@ -366,7 +367,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     const gu16* E = (const gu16*)dd.E[parity];
     gu16* C = (gu16*)dd.C[parity];
     gu16* CT = (gu16*)dd.CT[parity];
-    const ApplyDesc* fa = (PK == kProdUpdate && last) ? dd.fused : nullptr;
+    const ApplyDesc* fa = PK == kProdApply ? dd.fused : nullptr;  // set by the host for this kind
     if (last) {
       if (!dd.last_c || fa) C = nullptr;
       if (!dd.last_ct || fa) CT = nullptr;
@@ -394,65 +395,158 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
       }
     };
-    if (fa && fa->param_dtype == kDtBF16 && (fa->n & 3) == 0) {
-      // Fused update of a bf16 parameter with n % 4 == 0: per 32 x 32 block, the parameter values
-      // of its four groups are loaded first (one round trip), then updated and stored.
-      typedef __attribute__((address_space(1))) float gf32;
+    if (PK == kProdApply && fa->param_dtype == kDtBF16 && (fa->n & 7) == 0) {
+      // Fused update of a bf16 parameter with n % 8 == 0, staged through the LDS stage the next
+      // tile's prologue leaves free (32 KiB of fp32 per round), so that each wave reads and writes
+      // whole parameter row segments with 16-byte lanes: p <- p (1 - lr wd) - lr f O in fp32 from
+      // the unrounded O, one rounding to bf16; eight rounds per tile, each reading its parameter
+      // words before its LDS exchange. A wide parameter's rows are tile rows (rounds of 64 tile rows
+      // x 128 columns, 256-byte row segments); a tall parameter's rows are tile columns (rounds of
+      // one 32 x 32 block per wave, 64-byte row pieces), so that every wave's accumulators die
+      // round by round. 16-byte slots are XOR-swizzled per row so that the writes and the 16-lane
+      // reads hit 16 distinct bank groups (checked on the CPU with a bank model).
       typedef float f32x4 __attribute__((ext_vector_type(4)));
+      typedef __attribute__((address_space(1))) float gf32;
       typedef __attribute__((address_space(1))) f32x4 gf4;
+      typedef __attribute__((address_space(3))) f32x4 lf4;
+      lds_byte* slab = (lds_byte*)(smem + (NSTAGE - 1) * STAGE_BYTES);
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      const int frow = ln & 31, fhalf = ln >> 5, qd = ln & 3;
       const int64_t fm = fa->m, fn = fa->n;
       const float decay = fa->decay, stp = fa->step;
       const int mode = fa->mode;
       gu16* prm = (gu16*)fa->param;
       gf32* uo = (gf32*)fa->update_out;
-      static_for<MI>([&](auto mi_c) {
-        constexpr int mi = decltype(mi_c)::value;
-        const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
-        const int64_t iq = i - q;
-        // parameter elements (pr, pc .. pc + 3) this lane owns in group (ni, gg)
-        auto coords = [&](int ni, int gg, int64_t& pr, int64_t& pc) {
-          const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
-          if (fa_t) { pr = j + q; pc = iq; } else { pr = i; pc = j; }
-        };
-        static_for<NI>([&](auto ni_c) {
-          constexpr int ni = decltype(ni_c)::value;
-          u32x2 pw[4];
-          static_for<4>([&](auto gg_c) {
-            constexpr int gg = decltype(gg_c)::value;
-            int64_t pr, pc;
-            coords(ni, gg, pr, pc);
-            pw[gg] = u32x2{0u, 0u};
-            if (mode == 0 && pr < fm && pc < fn) pw[gg] = *(const gu2*)(prm + pr * fn + pc);
-          });
-          static_for<4>([&](auto gg_c) {
-            constexpr int gg = decltype(gg_c)::value;
-            float v0 = alpha * acc[mi][ni][4 * gg + 0];
-            float v1 = alpha * acc[mi][ni][4 * gg + 1];
-            float v2 = alpha * acc[mi][ni][4 * gg + 2];
-            float v3 = alpha * acc[mi][ni][4 * gg + 3];
-            if (fa_t) quad_transpose(v0, v1, v2, v3);
-            int64_t pr, pc;
-            coords(ni, gg, pr, pc);
-            if (pr < fm && pc < fn) {
-              float r0 = v0, r1 = v1, r2 = v2, r3 = v3;
-              if (mode == 0) {
-                const u32x2 w = pw[gg];
-                r0 = __uint_as_float(w.x << 16) * decay - stp * v0;
-                r1 = __uint_as_float(w.x & 0xffff0000u) * decay - stp * v1;
-                r2 = __uint_as_float(w.y << 16) * decay - stp * v2;
-                r3 = __uint_as_float(w.y & 0xffff0000u) * decay - stp * v3;
-                if (uo) *(gf4*)(uo + pr * fn + pc) = f32x4{v0, v1, v2, v3};
-              }
-              *(gu2*)(prm + pr * fn + pc) = u32x2{pack_bf16x2(r0, r1), pack_bf16x2(r2, r3)};
+      // Rounds R = 0 .. 7 (wide: block row mi = R / 2, column half h = R % 2; tall: block (mi, ni) =
+      // (R / NI, R % NI) of every wave).
+      // Lane coordinates of its two 8-element parameter pieces (it = 0, 1) in round R.
+      auto coords = [&](int R, int it, int64_t& pr, int64_t& pc) {
+        if (!fa_t) {
+          const int sr = w * 8 + it * 4 + (ln >> 4);
+          const int trow = (sr >> 5) * (MI * 32) + (R >> 1) * 32 + (sr & 31);
+          pr = int64_t(bi) * BT + trow;
+          pc = int64_t(bj) * BT + (R & 1) * 128 + (ln & 15) * 8;
+        } else {
+          // round (mi, ni) = (R / NI, R % NI); parameter row = tile column, columns = tile rows
+          const int jc = w * 16 + it * 8 + (ln >> 3), p = (ln >> 2) & 1, c4 = ln & 3;
+          pr = int64_t(bj) * BT + (jc >> 5) * (NI * 32) + (R % NI) * 32 + (jc & 31);
+          pc = int64_t(bi) * BT + p * (MI * 32) + (R / NI) * 32 + c4 * 8;
+        }
+      };
+      // the parameter words of round R, loaded before the round's LDS exchange so that it covers
+      // their latency (the read is the one dependent HBM access of this epilogue; the other
+      // epilogues only store)
+      auto load_round = [&](int R, u32x4* dst) {
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+          int64_t pr, pc;
+          coords(R, it, pr, pc);
+          dst[it] = u32x4{0u, 0u, 0u, 0u};
+          if (mode == 0 && pr < fm && pc < fn) dst[it] = *(const gu4*)(prm + pr * fn + pc);
+        }
+      };
+      // parameter elements (pr, pc .. pc + 7) from the fp32 values o0, o1 of O and the old words pw
+      auto update8 = [&](int64_t pr, int64_t pc, f32x4 o0, f32x4 o1, u32x4 pw) {
+        if (pr >= fm || pc >= fn) return;
+        const int64_t idx = pr * fn + pc;
+        float r[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+        if (mode == 0) {
+          const uint32_t wv[4] = {pw.x, pw.y, pw.z, pw.w};
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            r[2 * k] = __uint_as_float(wv[k] << 16) * decay - stp * r[2 * k];
+            r[2 * k + 1] = __uint_as_float(wv[k] & 0xffff0000u) * decay - stp * r[2 * k + 1];
+          }
+          if (uo) {
+            *(gf4*)(uo + idx) = o0;
+            *(gf4*)(uo + idx + 4) = o1;
+          }
+        }
+        *(gu4*)(prm + idx) = u32x4{pack_bf16x2(r[0], r[1]), pack_bf16x2(r[2], r[3]),
+                                   pack_bf16x2(r[4], r[5]), pack_bf16x2(r[6], r[7])};
+      };
+      // 16-byte slot swizzles of the two slab layouts (bijective within a row; conflict-free writes
+      // and 16-lane reads in a CPU bank model)
+      auto wsw = [](int row, int slot) { return (slot ^ (row & 31)) ^ ((slot >> 4) & 1); };
+      auto tsw = [](int jc, int slot) { return (slot ^ ((jc & 3) << 2) ^ ((jc & 1) * 3)) & 15; };
+      // second half of a round (the writes are done): exchange O through the slab, update
+      auto finish_round = [&](int R, const u32x4* pw, auto read_o) {
+        MFSDP_WAIT_LGKM0();
+        __builtin_amdgcn_s_barrier();
+#pragma unroll
+        for (int it = 0; it < 2; ++it) {
+          f32x4 o0, o1;
+          read_o(it, o0, o1);
+          int64_t pr, pc;
+          coords(R, it, pr, pc);
+          update8(pr, pc, o0, o1, pw[it]);
+        }
+        __builtin_amdgcn_s_barrier();  // slab reads done before the next round writes
+      };
+      if (!fa_t) {
+        // slab [64 rows][32 slots of 16 B]; round (mi, h): tile rows wm * 128 + mi * 32 + [0, 32)
+        // of both wave rows, tile columns h * 128 + [0, 128), written by the waves of that half
+        static_for<MI>([&](auto mi_c) {
+          constexpr int mi = decltype(mi_c)::value;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            u32x4 pw[2];
+            load_round(mi * 2 + h, pw);
+            if ((wn >> 1) == h) {
+              const int sr = wm * 32 + frow;
+              static_for<NI>([&](auto ni_c) {
+                constexpr int ni = decltype(ni_c)::value;
+                static_for<4>([&](auto gg_c) {
+                  constexpr int gg = decltype(gg_c)::value;
+                  const int slot = (wn & 1) * 16 + ni * 8 + gg * 2 + fhalf;
+                  *(lf4*)(slab + sr * 512 + wsw(sr, slot) * 16) =
+                      f32x4{alpha * acc[mi][ni][4 * gg], alpha * acc[mi][ni][4 * gg + 1],
+                            alpha * acc[mi][ni][4 * gg + 2], alpha * acc[mi][ni][4 * gg + 3]};
+                });
+              });
             }
+            finish_round(mi * 2 + h, pw, [&](int it, f32x4& o0, f32x4& o1) {
+              const int sr = w * 8 + it * 4 + (ln >> 4), c = ln & 15;
+              o0 = *(lf4*)(slab + sr * 512 + wsw(sr, 2 * c) * 16);
+              o1 = *(lf4*)(slab + sr * 512 + wsw(sr, 2 * c + 1) * 16);
+            });
+          }
+        });
+      } else {
+        // slab [128 tile columns][16 slots of 16 B, 4 tile rows each]; round (mi, ni): every
+        // wave's block (mi, ni), i.e. tile rows wm * 128 + mi * 32 + [0, 32) and tile columns
+        // wn * 64 + ni * 32 + [0, 32), written after a quad transpose; each of the 128 parameter
+        // rows (tile columns) then takes two 32-element pieces (one per wave row)
+        static_for<MI>([&](auto mi_c) {
+          constexpr int mi = decltype(mi_c)::value;
+          static_for<NI>([&](auto ni_c) {
+            constexpr int ni = decltype(ni_c)::value;
+            u32x4 pw[2];
+            load_round(mi * NI + ni, pw);
+            static_for<4>([&](auto gg_c) {
+              constexpr int gg = decltype(gg_c)::value;
+              float v0 = alpha * acc[mi][ni][4 * gg + 0];
+              float v1 = alpha * acc[mi][ni][4 * gg + 1];
+              float v2 = alpha * acc[mi][ni][4 * gg + 2];
+              float v3 = alpha * acc[mi][ni][4 * gg + 3];
+              quad_transpose(v0, v1, v2, v3);  // lane qd: column + qd at tile rows iq .. iq + 3
+              const int jc = wn * 32 + gg * 8 + fhalf * 4 + qd;
+              *(lf4*)(slab + jc * 256 + tsw(jc, wm * 8 + (frow >> 2)) * 16) = f32x4{v0, v1, v2, v3};
+            });
+            finish_round(mi * NI + ni, pw, [&](int it, f32x4& o0, f32x4& o1) {
+              const int jc = w * 16 + it * 8 + (ln >> 3), p = (ln >> 2) & 1, c4 = ln & 3;
+              o0 = *(lf4*)(slab + jc * 256 + tsw(jc, p * 8 + c4 * 2) * 16);
+              o1 = *(lf4*)(slab + jc * 256 + tsw(jc, p * 8 + c4 * 2 + 1) * 16);
+            });
           });
         });
-      });
+      }
       if (!has_next) break;
       cur = nxt;
       continue;
     }
-    if (staged) {
+    if constexpr (PK != kProdApply) {
       // Staged epilogue. The output tile leaves through the LDS stage the next tile's prologue does
       // not use, one 64-row slab (32 rows of each wave row) per round: the waves write their
       // values into the slab in the global panel-blocked layout, then each wave stores whole 1 KiB
@@ -580,46 +674,33 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       cur = nxt;
       continue;
     }
-    // (compile-time loops: every acc index must be a constant for acc to stay in registers)
-    static_for<MI>([&](auto mi_c) {
-      constexpr int mi = decltype(mi_c)::value;
-      const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
-      const int64_t iq = i - q;  // first row of this lane quad
-      static_for<NI>([&](auto ni_c) {
-        constexpr int ni = decltype(ni_c)::value;
-        static_for<4>([&](auto gg_c) {
-          constexpr int gg = decltype(gg_c)::value;
-          const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
-          float v0 = alpha * acc[mi][ni][4 * gg + 0];
-          float v1 = alpha * acc[mi][ni][4 * gg + 1];
-          float v2 = alpha * acc[mi][ni][4 * gg + 2];
-          float v3 = alpha * acc[mi][ni][4 * gg + 3];
-          if (E) {
-            const u32x2 ev = *(const gu2*)(E + blk_index(i, j, lde));
-            v0 += beta * __uint_as_float(ev.x << 16);
-            v1 += beta * __uint_as_float(ev.x & 0xffff0000u);
-            v2 += beta * __uint_as_float(ev.y << 16);
-            v3 += beta * __uint_as_float(ev.y & 0xffff0000u);
-          }
-          if (diag != 0.0f) {
-            if (i == j + 0) v0 += diag;
-            if (i == j + 1) v1 += diag;
-            if (i == j + 2) v2 += diag;
-            if (i == j + 3) v3 += diag;
-          }
-          if (C)
-            *(gu2*)(C + blk_index(i, j, ldc)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-          if (TD || fa_t) {
-            quad_transpose(v0, v1, v2, v3);
-            // lane q now holds column j + q at rows iq .. iq + 3
-            if (TD) *(gu2*)(TD + blk_index(j + q, iq, ldtd)) = u32x2{pack_bf16x2(v0, v1), pack_bf16x2(v2, v3)};
-            else apply4(*fa, j + q, iq, v0, v1, v2, v3);
-          } else if (fa) {
-            apply4(*fa, i, j, v0, v1, v2, v3);
-          }
+    if constexpr (PK == kProdApply) {
+      // Parameters the staged update does not take (fp32 parameters, or n % 8 != 0): straight from
+      // the accumulators, 4 elements per lane and group; a tall parameter takes the quad-transposed
+      // values. (Compile-time loops: every acc index must be a constant for acc to stay in registers.)
+      static_for<MI>([&](auto mi_c) {
+        constexpr int mi = decltype(mi_c)::value;
+        const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
+        const int64_t iq = i - q;  // first row of this lane quad
+        static_for<NI>([&](auto ni_c) {
+          constexpr int ni = decltype(ni_c)::value;
+          static_for<4>([&](auto gg_c) {
+            constexpr int gg = decltype(gg_c)::value;
+            const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+            float v0 = alpha * acc[mi][ni][4 * gg + 0];
+            float v1 = alpha * acc[mi][ni][4 * gg + 1];
+            float v2 = alpha * acc[mi][ni][4 * gg + 2];
+            float v3 = alpha * acc[mi][ni][4 * gg + 3];
+            if (fa_t) {
+              quad_transpose(v0, v1, v2, v3);
+              apply4(*fa, j + q, iq, v0, v1, v2, v3);  // lane q: column j + q at rows iq .. iq + 3
+            } else {
+              apply4(*fa, i, j, v0, v1, v2, v3);
+            }
+          });
         });
       });
-    });
+    }
     if (!has_next) break;
     cur = nxt;
   }
@@ -754,8 +835,11 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, cons
     else if (product == kProdSquare)
       hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdSquare>), grid, block, 0, st,
                          d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
-    else
+    else if (product == kProdUpdate)
       hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdUpdate>), grid, block, 0, st,
+                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
+    else
+      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdApply>), grid, block, 0, st,
                          d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
   } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,

@@ -463,9 +463,11 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const doub
   if ((rc = record(events, 1, st))) return rc;
   for (int k = 0; k < steps; ++k) {
     for (int ph = 0; ph < 3; ++ph) {
+      // the last update of the bf16 path applies the parameter update in its epilogue (kind 3)
+      const int kind = (ph == 2 && k == steps - 1 && apply_fused(ns_dtype, steps)) ? 3 : ph;
       e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, P.tiles[ph],
                       reinterpret_cast<const TileRef*>(ws + dl.off_sched[ph]), dl.ngroups[ph],
-                      ns_dtype, ph, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0,
+                      ns_dtype, kind, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0,
                       float(coeffs[3 * k]), float(coeffs[3 * k + 1]), float(coeffs[3 * k + 2]), st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
     }

@@ -145,7 +145,8 @@ constexpr int kAdamWBlockElems = 2048;
 hipError_t launch_prep(const PrepDesc* d_descs, int count, int total_tiles, int ns_dtype,
                        int reduce, float beta, float one_minus_beta, int nesterov, hipStream_t st);
 hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_t st);
-// product: 0 Gram, 1 square, 2 update (the order of the products in one NS step)
+// product: 0 Gram, 1 square, 2 update (the order of the products in one NS step); 3 the last update
+// of the bf16 path with the fused parameter update (its descriptors carry `fused`)
 // (ca, cb, cc): the NS step's coefficients (a_k, b_k, c_k), used by the square product.
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
                        int ngroups, int ns_dtype, int product, int parity, int first_step,
