@@ -596,19 +596,26 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         lde32 = int(dd.lde);
       }
       // values of round mi into the slab; DIAG: this is a diagonal tile of the square product
+      // The square product's addend E = A for round mi: each lane's 4-element pieces, loaded one
+      // round ahead of their use (double-buffered by round parity) so that their latency is covered
+      // by the previous round's exchange instead of stalling each round.
+      u32x2 ev[2][NI][4];
+      auto load_e = [&](auto mi_c) {
+        constexpr int mi = decltype(mi_c)::value;
+        const int il = wm * (MI * 32) + mi * 32 + frow;
+        static_for<NI>([&](auto ni) {
+          static_for<4>([&](auto gg) {
+            const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+            ev[mi & 1][ni][gg] = *(const gu2*)(Et + int(blk_index(il, lc, lde32)));
+          });
+        });
+      };
+      if constexpr (PK == kProdSquare) load_e(std::integral_constant<int, 0>{});
       auto write_round = [&](auto mi_c, auto diag_c) {
         constexpr int mi = decltype(mi_c)::value;
         constexpr bool DIAG = decltype(diag_c)::value;
         const int il = wm * (MI * 32) + mi * 32 + frow;  // tile row of this lane
-        u32x2 ev[NI][4];
-        if constexpr (PK == kProdSquare) {
-          static_for<NI>([&](auto ni) {
-            static_for<4>([&](auto gg) {
-              const int lc = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
-              ev[ni][gg] = *(const gu2*)(Et + int(blk_index(il, lc, lde32)));
-            });
-          });
-        }
+        if constexpr (PK == kProdSquare && mi + 1 < MI) load_e(std::integral_constant<int, mi + 1>{});
         static_for<NI>([&](auto ni_c) {
           constexpr int ni = decltype(ni_c)::value;
           static_for<4>([&](auto gg_c) {
@@ -618,7 +625,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
             float v2 = alpha * acc[mi][ni][4 * gg + 2];
             float v3 = alpha * acc[mi][ni][4 * gg + 3];
             if constexpr (PK == kProdSquare) {
-              const u32x2 e = ev[ni][gg];
+              const u32x2 e = ev[mi & 1][ni][gg];
               v0 += beta * __uint_as_float(e.x << 16);
               v1 += beta * __uint_as_float(e.x & 0xffff0000u);
               v2 += beta * __uint_as_float(e.y << 16);
