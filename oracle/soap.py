@@ -22,14 +22,18 @@ Readings (the paper fixes none of them):
 * bias correction as PyTorch AdamW: N' = (M'/(1 - beta1^t)) / (sqrt(V)/sqrt(1 - beta2^t) + eps), so
   that with Q_L = Q_R = I one SOAP step is exactly one AdamW step.
 * decoupled weight decay on the old parameter (as AdamW and the Muon/Shampoo steps here).
-* the statistics use the Shampoo update of ``shampoo.update_statistics`` (beta_s L + w_s G G^T;
-  the published SOAP uses the EMA w_s = 1 - beta_s) and start at zero; the bases start at the
+* the statistics are updated as Shampoo's (beta_s L + w_s G G^T and beta_s R + w_s G^T G, as in
+  ``shampoo.update_statistics``; the published SOAP uses the EMA w_s = 1 - beta_s) and start at zero; the bases start at the
   identity, so the first steps are AdamW and the first refresh begins the power iteration (the
   published code starts from a full eigendecomposition instead; ``refresh_iters`` > 1 repeats the
   power step + QR, i.e. runs orthogonal iteration towards the eigenvectors).
 * V is left unchanged when the basis is refreshed, as in the published algorithm.
 * the QR factor is the Householder one with LAPACK's sign convention (LAPACK's geqrf/orgqr through
   scipy.linalg.qr). Column signs of a basis do not change N (each column enters N twice).
+* one-sided preconditioning, as the published optimizer's maximum preconditioned dimension: a side
+  longer than ``max_precond_dim`` keeps the identity basis and no statistic (its Q and statistic
+  are returned as None), so on that side G', M' and N are untransformed; with both sides beyond
+  it the step is AdamW.
 """
 from __future__ import annotations
 
@@ -41,7 +45,6 @@ import numpy as np
 import scipy.linalg
 
 from .muon import _f64
-from .shampoo import update_statistics
 
 
 @dataclasses.dataclass
@@ -55,6 +58,7 @@ class SoapHParams:
     shampoo_weight: float = 0.05
     refresh: bool = False
     refresh_iters: int = 1
+    max_precond_dim: int = 4096
 
 
 def orthonormal_factor(A: np.ndarray) -> np.ndarray:
@@ -84,22 +88,29 @@ def adam_direction(Mp: np.ndarray, V: np.ndarray, beta1: float, beta2: float, ep
 
 
 def soap_step(param: np.ndarray, grad: np.ndarray, exp_avg: np.ndarray, exp_avg_sq: np.ndarray,
-              L: np.ndarray, R: np.ndarray, QL: np.ndarray, QR: np.ndarray, step: int,
-              hp: SoapHParams):
+              L, R, QL, QR, step: int, hp: SoapHParams):
     """One owner-local SOAP step on one whole m x n matrix at step number ``step`` (t >= 1).
-    Returns (param', M', V', L', R', Q_L', Q_R', N) in float64."""
+    Returns (param', M', V', L', R', Q_L', Q_R', N) in float64. A side longer than
+    hp.max_precond_dim is not preconditioned: its basis is the identity, its statistic is not kept,
+    and its L (or R) and Q_L (or Q_R) come back as None (the inputs are ignored)."""
     G = _f64(grad)
-    QL = np.asarray(QL, dtype=np.float64)
-    QR = np.asarray(QR, dtype=np.float64)
-    Gp = QL.T @ G @ QR
+    m, n = G.shape
+    left, right = m <= hp.max_precond_dim, n <= hp.max_precond_dim
+    QLm = np.asarray(QL, dtype=np.float64) if left else np.eye(m)
+    QRm = np.asarray(QR, dtype=np.float64) if right else np.eye(n)
+    Gp = QLm.T @ G @ QRm
     M = hp.beta1 * _f64(exp_avg) + (1.0 - hp.beta1) * G
-    Mp = QL.T @ M @ QR
+    Mp = QLm.T @ M @ QRm
     V = hp.beta2 * _f64(exp_avg_sq) + (1.0 - hp.beta2) * Gp * Gp
     Np = adam_direction(Mp, V, hp.beta1, hp.beta2, hp.eps, step)
-    N = QL @ Np @ QR.T
+    N = QLm @ Np @ QRm.T
     p_new = _f64(param) * (1.0 - hp.lr * hp.weight_decay) - hp.lr * N
-    L2, R2 = update_statistics(L, R, G, hp.shampoo_beta, hp.shampoo_weight)
+    L2 = hp.shampoo_beta * np.asarray(L, dtype=np.float64) + hp.shampoo_weight * (G @ G.T) if left else None
+    R2 = hp.shampoo_beta * np.asarray(R, dtype=np.float64) + hp.shampoo_weight * (G.T @ G) if right else None
+    QLo, QRo = (QLm if left else None), (QRm if right else None)
     if hp.refresh:
-        QL = refresh_basis(L2, QL, hp.refresh_iters)
-        QR = refresh_basis(R2, QR, hp.refresh_iters)
-    return p_new, M, V, L2, R2, QL, QR, N
+        if left:
+            QLo = refresh_basis(L2, QLm, hp.refresh_iters)
+        if right:
+            QRo = refresh_basis(R2, QRm, hp.refresh_iters)
+    return p_new, M, V, L2, R2, QLo, QRo, N

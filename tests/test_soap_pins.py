@@ -192,3 +192,68 @@ def test_bf16_gradient_widens_exactly():
     st["grad"] = synth.bf16_bits_to_f32(bits).astype(np.float64)
     ref = _run(st, 1, hp)
     np.testing.assert_array_equal(got[7], ref[7])
+
+
+# ------------------------------------------------------------------ one-sided preconditioning
+
+def test_both_sides_beyond_the_limit_is_adamw():
+    """Both sides longer than max_precond_dim: no basis on either side, the step is AdamW
+    (torch.optim.AdamW on the CPU in float64, three steps)."""
+    import torch
+    rng = np.random.default_rng(300)
+    m, n = 9, 7
+    hp = S.SoapHParams(lr=1e-2, weight_decay=0.1, beta1=0.9, beta2=0.99, eps=1e-8, max_precond_dim=6)
+    p = rng.standard_normal((m, n))
+    M = np.zeros((m, n))
+    V = np.zeros((m, n))
+    tp = torch.tensor(p.copy(), requires_grad=True)
+    opt = torch.optim.AdamW([tp], lr=hp.lr, betas=(hp.beta1, hp.beta2), eps=hp.eps, weight_decay=hp.weight_decay)
+    for t in range(1, 4):
+        g = rng.standard_normal((m, n))
+        p, M, V, L2, R2, QL, QR, N = S.soap_step(p, g, M, V, None, None, None, None, t, hp)
+        assert L2 is None and R2 is None and QL is None and QR is None
+        tp.grad = torch.tensor(g)
+        opt.step()
+        np.testing.assert_allclose(p, tp.detach().numpy(), rtol=0, atol=1e-14)
+        np.testing.assert_allclose(M, opt.state[tp]["exp_avg"].numpy(), rtol=0, atol=1e-15)
+        np.testing.assert_allclose(V, opt.state[tp]["exp_avg_sq"].numpy(), rtol=0, atol=1e-15)
+
+
+def test_one_sided_step_is_transpose_consistent():
+    """A left side beyond the limit on G (m x n) is the right side beyond it on G^T: every output
+    is the transpose, with the roles of the two bases and statistics swapped (three steps with a
+    refresh after each)."""
+    rng = np.random.default_rng(301)
+    m, n = 12, 5
+    hp = S.SoapHParams(lr=3e-3, weight_decay=0.01, refresh=True, max_precond_dim=8)
+    p = rng.standard_normal((m, n))
+    M, V, R, QR = np.zeros((m, n)), np.zeros((m, n)), np.zeros((n, n)), np.eye(n)
+    pt, Mt, Vt, Lt, QLt = p.T.copy(), np.zeros((n, m)), np.zeros((n, m)), np.zeros((n, n)), np.eye(n)
+    for t in range(1, 4):
+        g = rng.standard_normal((m, n))
+        p, M, V, L2, R, QL2, QR, N = S.soap_step(p, g, M, V, None, R, None, QR, t, hp)
+        pt, Mt, Vt, Lt, R2t, QLt, QR2t, Nt = S.soap_step(pt, g.T, Mt, Vt, Lt, None, QLt, None, t, hp)
+        assert L2 is None and QL2 is None and R2t is None and QR2t is None
+        for a, b in ((p, pt), (M, Mt), (V, Vt), (N, Nt)):
+            np.testing.assert_allclose(a, b.T, rtol=0, atol=1e-13)
+        np.testing.assert_allclose(R, Lt, rtol=0, atol=1e-13)
+        np.testing.assert_allclose(QR, QLt, rtol=0, atol=1e-12)
+
+
+def test_right_only_closed_form_on_an_aligned_gradient():
+    """Left side beyond the limit, right basis Q_R: a gradient G = A Q_R^T has G' = A, so at t = 1
+    from zero moments N = (A / (|A| + eps)) Q_R^T exactly (bias corrections cancel)."""
+    rng = np.random.default_rng(302)
+    m, n = 11, 4
+    q, r = np.linalg.qr(rng.standard_normal((n, n)))
+    QR = q * np.sign(np.diag(r))
+    A = rng.standard_normal((m, n))
+    G = A @ QR.T
+    hp = S.SoapHParams(lr=1e-2, eps=1e-8, max_precond_dim=n)
+    _, _, V, L2, R2, QL2, QR2, N = S.soap_step(np.zeros((m, n)), G, np.zeros((m, n)), np.zeros((m, n)),
+                                               None, np.zeros((n, n)), None, QR, 1, hp)
+    np.testing.assert_allclose(N, (A / (np.abs(A) + hp.eps)) @ QR.T, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(V, (1 - hp.beta2) * A * A, rtol=1e-13, atol=0)
+    assert L2 is None and QL2 is None
+    np.testing.assert_allclose(R2, hp.shampoo_weight * G.T @ G, rtol=1e-13, atol=1e-15)
+    np.testing.assert_array_equal(QR2, QR)   # no refresh: the basis is returned as it was
