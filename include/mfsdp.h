@@ -297,7 +297,9 @@ int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double 
 
 /* ---- SOAP owner step (Section 5.7: Adam in the eigenbasis of Shampoo's statistics) ---------- */
 
-/* One whole matrix the rank owns, for SOAP (Vyas et al. 2024, the matrix case).
+/* One whole matrix the rank owns, for SOAP (Vyas et al. 2024, the matrix case). A side longer than
+ * the call's max_precond_dim (hparams) has no basis: it is the identity, that side's statistic is
+ * not kept, and its L (or R) and QL (or QR) are not read or written (they may be NULL).
  *   param       m x n, param_dtype (F32 or BF16), updated in place (fp32 math, bf16 rounded to
  *               nearest even)
  *   grad        m x n, grad_dtype (F32 or BF16), read only
@@ -307,8 +309,8 @@ int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double 
  *   QL, QR      m x m and n x n fp32 orthogonal bases (row-major; columns are the basis vectors):
  *               read; overwritten by the refreshed bases when hp->refresh is 1. Start them at the
  *               identity (then the first steps are AdamW steps).
- *   m, n        1 .. 4096 (each side's basis is refreshed by a QR whose panels are held in
- *               registers, at most 4096 rows)
+ *   m, n        1 .. 65536; a side with a basis is at most max_precond_dim <= 4096 long (its basis
+ *               is refreshed by a QR whose panels are held in registers, at most 4096 rows)
  *   update_out  optional m x n fp32: receives the direction N. NULL = off.
  * All buffers are distinct device allocations (no aliasing), naturally aligned. */
 typedef struct {
@@ -335,8 +337,12 @@ typedef struct {
  *   L <- shampoo_beta L + shampoo_weight G G^T;  R <- shampoo_beta R + shampoo_weight G^T G
  *   refresh 1: refresh_iters times QL <- Q factor of the Householder QR of L QL (and R, QR alike),
  *   with LAPACK's sign convention; refresh 0: the bases are read only.
+ *   max_precond_dim: sides longer than it have no basis (QL or QR = I, no statistic; the published
+ *   optimizer's maximum preconditioned dimension); 0 means 4096, the longest side a refresh takes.
+ *   With both sides beyond it the step is AdamW.
  *   lr, weight_decay, shampoo_beta, shampoo_weight >= 0; beta1, beta2 in [0, 1); eps > 0;
- *   step t >= 1 (the bias-correction count); refresh 0/1; refresh_iters 1 .. 100. */
+ *   step t >= 1 (the bias-correction count); refresh 0/1; refresh_iters 1 .. 100;
+ *   max_precond_dim 0 .. 4096. */
 typedef struct {
   double lr;
   double weight_decay;
@@ -348,11 +354,14 @@ typedef struct {
   int32_t step;
   int32_t refresh;
   int32_t refresh_iters;
+  int32_t max_precond_dim;
 } mfsdp_soap_hparams;
 
 /* Bytes of device workspace mfsdp_soap_step needs for these entries and hyperparameters: per
  * matrix, zero-padded fp32 buffers of 8 mp np + 3 (mp^2 + np^2) floats (mp, np = m, n rounded up
- * to 128) and 16 (m + n) + 512 floats for the QR panels; plus launch descriptors. Data pointers are
+ * to 128) and 16 (m + n) + 512 floats for the QR panels when both sides have a basis (a side
+ * without one drops its 3 d^2 + 16 d + 256 floats and, on the left, 2 mp np more); plus launch
+ * descriptors. Data pointers are
  * not used. 0 on invalid arguments; count == 0 returns 0 with no error. */
 size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
                                  const mfsdp_soap_hparams* hp);

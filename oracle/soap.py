@@ -96,18 +96,27 @@ def soap_step(param: np.ndarray, grad: np.ndarray, exp_avg: np.ndarray, exp_avg_
     G = _f64(grad)
     m, n = G.shape
     left, right = m <= hp.max_precond_dim, n <= hp.max_precond_dim
-    QLm = np.asarray(QL, dtype=np.float64) if left else np.eye(m)
-    QRm = np.asarray(QR, dtype=np.float64) if right else np.eye(n)
-    Gp = QLm.T @ G @ QRm
+    QLm = np.asarray(QL, dtype=np.float64) if left else None
+    QRm = np.asarray(QR, dtype=np.float64) if right else None
+
+    def to_basis(X):      # Q_L^T X Q_R, a side without a basis being the identity
+        X = QLm.T @ X if left else X
+        return X @ QRm if right else X
+
+    def from_basis(X):    # Q_L X Q_R^T
+        X = QLm @ X if left else X
+        return X @ QRm.T if right else X
+
+    Gp = to_basis(G)
     M = hp.beta1 * _f64(exp_avg) + (1.0 - hp.beta1) * G
-    Mp = QLm.T @ M @ QRm
+    Mp = to_basis(M)
     V = hp.beta2 * _f64(exp_avg_sq) + (1.0 - hp.beta2) * Gp * Gp
     Np = adam_direction(Mp, V, hp.beta1, hp.beta2, hp.eps, step)
-    N = QLm @ Np @ QRm.T
+    N = from_basis(Np)
     p_new = _f64(param) * (1.0 - hp.lr * hp.weight_decay) - hp.lr * N
     L2 = hp.shampoo_beta * np.asarray(L, dtype=np.float64) + hp.shampoo_weight * (G @ G.T) if left else None
     R2 = hp.shampoo_beta * np.asarray(R, dtype=np.float64) + hp.shampoo_weight * (G.T @ G) if right else None
-    QLo, QRo = (QLm if left else None), (QRm if right else None)
+    QLo, QRo = QLm, QRm
     if hp.refresh:
         if left:
             QLo = refresh_basis(L2, QLm, hp.refresh_iters)

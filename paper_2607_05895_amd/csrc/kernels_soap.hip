@@ -106,6 +106,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
   const int64_t gc = int64_t(tj) * kTile + c;
   g_f32* Gp = (g_f32*)(d.Gp);
   g_f32* GMt = (g_f32*)(d.GMt);
+  g_f32* GM = (g_f32*)(d.GM);
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
     const int r = rr + 4 * i;
@@ -119,10 +120,15 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
       mo = beta1 * d.exp_avg[o] + (1.0f - beta1) * g;
       d.exp_avg[o] = mo;
     }
-    Gp[gr * d.np + gc] = g;
+    if (Gp) Gp[gr * d.np + gc] = g;
+    if (GM) {
+      GM[gr * 2 * d.np + gc] = g;
+      GM[gr * 2 * d.np + d.np + gc] = mo;
+    }
     tg[r][c] = g;
     tm[r][c] = mo;
   }
+  if (!GMt) return;  // (uniform over the workgroup: no barrier is skipped by part of it)
   __syncthreads();
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
@@ -158,7 +164,9 @@ __global__ __launch_bounds__(256) void soap_adam_kernel(const SoapAdamDesc* __re
       np_ = (mq * inv_bc1) / (sqrtf(v) * inv_sqrt_bc2 + eps);
     }
     tn[r][c] = np_;
+    if (d.Np) ((g_f32*)(d.Np))[gr * d.np + gc] = np_;
   }
+  if (!d.NpT) return;  // (uniform over the workgroup)
   __syncthreads();
   g_f32* NpT = (g_f32*)(d.NpT);
 #pragma unroll 4

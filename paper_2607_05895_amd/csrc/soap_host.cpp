@@ -126,11 +126,21 @@ void add_gemm(Build& b, std::vector<Prod> ps) {
   b.op(kOpGemm, gs, gt);
 }
 
+// Per matrix: left / right tell whether that side has a basis (its length is at most
+// max_precond_dim); a side without one is the identity, and its statistic, basis buffers and
+// product are skipped (kNone marks an unused buffer).
+constexpr size_t kNone = ~size_t(0);
 struct SoapPlan {
   int64_t m = 0, n = 0, mp = 0, np = 0;
-  size_t Gp = 0, GMt = 0, X1 = 0, GMr = 0, NpT = 0, QLp = 0, QLt = 0, QRp = 0, QRt = 0, Lp = 0, Rp = 0;
+  bool left = true, right = true;
+  size_t Gp = kNone, GMt = kNone, X1 = 0, GMr = 0, NpT = kNone, QLp = kNone, QLt = kNone, QRp = kNone,
+         QRt = kNone, Lp = kNone, Rp = kNone;
   QrSide L, R;
 };
+
+constexpr int64_t kSoapMaxDim = 65536;  // sides without a basis
+
+int64_t precond_limit(const mfsdp_soap_hparams* hp) { return hp->max_precond_dim == 0 ? kQrMaxDim : hp->max_precond_dim; }
 
 int check_soap_hp(const mfsdp_soap_hparams* hp) {
   if (!hp) return bad("hparams is NULL");
@@ -146,10 +156,12 @@ int check_soap_hp(const mfsdp_soap_hparams* hp) {
   if (hp->step < 1) return bad("step must be >= 1");
   if (hp->refresh != 0 && hp->refresh != 1) return bad("refresh must be 0 or 1");
   if (hp->refresh_iters < 1 || hp->refresh_iters > 100) return bad("refresh_iters must be in [1, 100]");
+  if (hp->max_precond_dim < 0 || hp->max_precond_dim > kQrMaxDim)
+    return bad("max_precond_dim must be in [0, 4096] (0: 4096, the longest side a basis refresh supports)");
   return MFSDP_OK;
 }
 
-int check_soap_entries(const mfsdp_soap_entry* en, int64_t count, bool data) {
+int check_soap_entries(const mfsdp_soap_entry* en, int64_t count, bool data, int64_t maxd) {
   if (count < 0) return bad("count must be >= 0");
   if (count > 0 && !en) return bad("entries is NULL");
   if (count > 4096) return bad("at most 4096 entries per call");
@@ -157,13 +169,14 @@ int check_soap_entries(const mfsdp_soap_entry* en, int64_t count, bool data) {
   for (int64_t i = 0; i < count; ++i) {
     const mfsdp_soap_entry& e = en[i];
     const std::string w = "entry " + std::to_string(i) + ": ";
-    if (e.m < 1 || e.n < 1 || e.m > kQrMaxDim || e.n > kQrMaxDim) return bad(w + "m and n must be in [1, 4096]");
+    if (e.m < 1 || e.n < 1 || e.m > kSoapMaxDim || e.n > kSoapMaxDim) return bad(w + "m and n must be in [1, 65536]");
     const int64_t s = rup(e.m, kShTile) + 2 * rup(e.n, kShTile);
     units += 3 * (s / kShCopyTile) * (s / kShCopyTile);
     if (units > (int64_t(1) << 30)) return bad("the entries of one call exceed 2^30 tiles per launch");
     if (!dtype_ok(e.param_dtype) || !dtype_ok(e.grad_dtype)) return bad(w + "dtype must be F32 or BF16");
     if (!data) continue;
-    if (!e.param || !e.grad || !e.exp_avg || !e.exp_avg_sq || !e.L || !e.R || !e.QL || !e.QR)
+    const bool left = e.m <= maxd, right = e.n <= maxd;
+    if (!e.param || !e.grad || !e.exp_avg || !e.exp_avg_sq || (left && (!e.L || !e.QL)) || (right && (!e.R || !e.QR)))
       return bad(w + "NULL pointer");
     const size_t pa = e.param_dtype == MFSDP_BF16 ? 2 : 4, ga = e.grad_dtype == MFSDP_BF16 ? 2 : 4;
     if (!aligned(e.param, pa) || !aligned(e.grad, ga) || !aligned(e.exp_avg, 4) || !aligned(e.exp_avg_sq, 4) ||
@@ -178,55 +191,69 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
                   Build& b, size_t& desc_at) {
   b.base = ws;
   Arena a;
+  const int64_t maxd = precond_limit(hp);
   std::vector<SoapPlan> P(static_cast<size_t>(count));
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
     e.m = en[i].m;
     e.n = en[i].n;
+    e.left = e.m <= maxd;
+    e.right = e.n <= maxd;
     e.mp = rup(e.m, kShTile);
     e.np = rup(e.n, kShTile);
     const size_t f = sizeof(float), mn = size_t(e.mp) * size_t(e.np) * f;
-    e.Gp = a.take(mn);
-    e.GMt = a.take(2 * mn);
-    e.X1 = a.take(2 * mn);   // later Z = Q_L N' (mp x np)
-    e.GMr = a.take(2 * mn);  // later N (mp x np)
-    e.NpT = a.take(mn);
-    const size_t mm = size_t(e.mp) * size_t(e.mp) * f, nn = size_t(e.np) * size_t(e.np) * f;
-    e.QLp = a.take(mm);  // later the refresh product S = L Q_L
-    e.QLt = a.take(mm);  // later the accumulated Q_L^T of the refresh
-    e.Lp = a.take(mm);
-    e.QRp = a.take(nn);
-    e.QRt = a.take(nn);
-    e.Rp = a.take(nn);
-    e.L.d = e.m;
-    e.L.dp = e.mp;
-    e.L.S = e.QLp;
-    e.L.Qt = e.QLt;
-    plan_qr_buffers(e.L, a);
-    e.R.d = e.n;
-    e.R.dp = e.np;
-    e.R.S = e.QRp;
-    e.R.Qt = e.QRt;
-    plan_qr_buffers(e.R, a);
+    if (e.left) e.Gp = a.take(mn);               // G for the left statistic
+    if (e.left || e.right) e.GMt = a.take(2 * mn);  // [G^T ; M^T]: left product, right statistic
+    e.X1 = a.take(2 * mn);   // Q_L^T [G | M] (or [G | M] itself); later Z = Q_L N' (or N')
+    e.GMr = a.take(2 * mn);  // [G' | M']; later N
+    if (e.left) e.NpT = a.take(mn);
+    if (e.left) {
+      const size_t mm = size_t(e.mp) * size_t(e.mp) * f;
+      e.QLp = a.take(mm);  // later the refresh product S = L Q_L
+      e.QLt = a.take(mm);  // later the accumulated Q_L^T of the refresh
+      e.Lp = a.take(mm);
+      e.L.d = e.m;
+      e.L.dp = e.mp;
+      e.L.S = e.QLp;
+      e.L.Qt = e.QLt;
+      plan_qr_buffers(e.L, a);
+    }
+    if (e.right) {
+      const size_t nn = size_t(e.np) * size_t(e.np) * f;
+      e.QRp = a.take(nn);
+      e.QRt = a.take(nn);
+      e.Rp = a.take(nn);
+      e.R.d = e.n;
+      e.R.dp = e.np;
+      e.R.S = e.QRp;
+      e.R.Qt = e.QRt;
+      plan_qr_buffers(e.R, a);
+    }
   }
   desc_at = a.off;
+  auto fp = [&](size_t off) { return off == kNone ? nullptr : b.ptr<float>(off); };
 
   std::vector<ShCopyDesc> cin;
   std::vector<SoapPrepDesc> prep;
   int ct = 0, pt = 0;
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
-    cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.Lp), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp, e.mp, ct));
-    cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.Rp), nullptr, e.n, e.n, e.n, e.np, 0, e.np, e.np, ct));
-    cin.push_back(copy_desc(en[i].QL, kDtF32, b.ptr<float>(e.QLp), b.ptr<float>(e.QLt), e.m, e.m, e.m, e.mp,
-                            e.mp, e.mp, e.mp, ct));
-    cin.push_back(copy_desc(en[i].QR, kDtF32, b.ptr<float>(e.QRp), b.ptr<float>(e.QRt), e.n, e.n, e.n, e.np,
-                            e.np, e.np, e.np, ct));
+    if (e.left) {
+      cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.Lp), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp, e.mp, ct));
+      cin.push_back(copy_desc(en[i].QL, kDtF32, b.ptr<float>(e.QLp), b.ptr<float>(e.QLt), e.m, e.m, e.m, e.mp,
+                              e.mp, e.mp, e.mp, ct));
+    }
+    if (e.right) {
+      cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.Rp), nullptr, e.n, e.n, e.n, e.np, 0, e.np, e.np, ct));
+      cin.push_back(copy_desc(en[i].QR, kDtF32, b.ptr<float>(e.QRp), b.ptr<float>(e.QRt), e.n, e.n, e.n, e.np,
+                              e.np, e.np, e.np, ct));
+    }
     SoapPrepDesc d{};
     d.grad = en[i].grad;
     d.exp_avg = en[i].exp_avg;
-    d.Gp = b.ptr<float>(e.Gp);
-    d.GMt = b.ptr<float>(e.GMt);
+    d.Gp = fp(e.Gp);
+    d.GMt = fp(e.GMt);
+    d.GM = e.left ? nullptr : b.ptr<float>(e.X1);
     d.m = e.m;
     d.n = e.n;
     d.mp = e.mp;
@@ -237,38 +264,50 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     pt += int((e.mp / kShCopyTile) * (e.np / kShCopyTile));
     prep.push_back(d);
   }
-  b.op(kOpCopyIn, cin, ct);
+  if (!cin.empty()) b.op(kOpCopyIn, cin, ct);
   b.op(kOpSoapPrep, prep, pt);
 
+  // Products (a side without a basis skips its own):
+  //   left:  X1 = Q_L^T [G | M];  Z = Q_L N' (from N'^T) into X1
+  //   right: [G' | M'] = X1 halves Q_R into GMr;  N = Z Q_R^T into GMr
+  // Adam reads [G' | M'] from GMr (right) or X1 (no right basis) and writes N'^T (left) or N'
+  // itself: into X1 as Z (right) or into GMr as N (neither); apply reads N from GMr, or from X1 when
+  // only the left side has a basis.
   const float ws_ = float(hp->shampoo_weight), bs_ = float(hp->shampoo_beta);
   std::vector<Prod> p1, p2, p3, p4;
   for (SoapPlan& e : P) {
     float* X1 = b.ptr<float>(e.X1);
     float* GMr = b.ptr<float>(e.GMr);
-    const float* GMt = b.ptr<float>(e.GMt);
-    const float* Gp = b.ptr<float>(e.Gp);
     const int64_t mp = e.mp, np = e.np;
-    p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, 2 * np, mp, 0, 1.0f, 0.0f});
-    // the statistics read only G and G^T: they join the first launch
-    p1.push_back(Prod{Gp, Gp, b.ptr<float>(e.Lp), b.ptr<float>(e.Lp), np, np, mp, mp, mp, mp, np, 1, ws_, bs_});
-    p1.push_back(Prod{GMt, GMt, b.ptr<float>(e.Rp), b.ptr<float>(e.Rp), mp, mp, np, np, np, np, mp, 1, ws_, bs_});
-    for (int h = 0; h < 2; ++h)
-      p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np, np,
-                        0, 1.0f, 0.0f});
-    p3.push_back(Prod{b.ptr<float>(e.QLp), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f,
-                      0.0f});
-    p4.push_back(Prod{X1, b.ptr<float>(e.QRp), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
+    if (e.left) {
+      const float* GMt = b.ptr<float>(e.GMt);
+      const float* Gp = b.ptr<float>(e.Gp);
+      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, 2 * np, mp, 0, 1.0f, 0.0f});
+      // the statistics read only G and G^T: they join the first launch
+      p1.push_back(Prod{Gp, Gp, b.ptr<float>(e.Lp), b.ptr<float>(e.Lp), np, np, mp, mp, mp, mp, np, 1, ws_, bs_});
+      p3.push_back(Prod{b.ptr<float>(e.QLp), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f,
+                        0.0f});
+    }
+    if (e.right) {
+      const float* GMt = b.ptr<float>(e.GMt);
+      p1.push_back(Prod{GMt, GMt, b.ptr<float>(e.Rp), b.ptr<float>(e.Rp), mp, mp, np, np, np, np, mp, 1, ws_, bs_});
+      for (int h = 0; h < 2; ++h)
+        p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np,
+                          np, 0, 1.0f, 0.0f});
+      p4.push_back(Prod{X1, b.ptr<float>(e.QRp), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
+    }
   }
-  add_gemm(b, p1);
-  add_gemm(b, p2);
+  if (!p1.empty()) add_gemm(b, p1);
+  if (!p2.empty()) add_gemm(b, p2);
 
   std::vector<SoapAdamDesc> ad;
   int at = 0;
   for (SoapPlan& e : P) {
     SoapAdamDesc d{};
-    d.GMr = b.ptr<float>(e.GMr);
+    d.GMr = b.ptr<float>(e.right ? e.GMr : e.X1);
     d.exp_avg_sq = en[&e - P.data()].exp_avg_sq;
-    d.NpT = b.ptr<float>(e.NpT);
+    d.NpT = fp(e.NpT);
+    d.Np = e.left ? nullptr : b.ptr<float>(e.right ? e.X1 : e.GMr);
     d.m = e.m;
     d.n = e.n;
     d.mp = e.mp;
@@ -279,15 +318,15 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     ad.push_back(d);
   }
   b.op(kOpSoapAdam, ad, at);
-  add_gemm(b, p3);
-  add_gemm(b, p4);
+  if (!p3.empty()) add_gemm(b, p3);
+  if (!p4.empty()) add_gemm(b, p4);
 
   std::vector<ShApplyDesc> ap;
   int apt = 0;
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
     ShApplyDesc d{};
-    d.U = b.ptr<float>(e.GMr);
+    d.U = b.ptr<float>((e.left && !e.right) ? e.X1 : e.GMr);
     d.ldu = e.np;
     d.param = en[i].param;
     d.update_out = en[i].update_out;
@@ -306,41 +345,51 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
   ct = 0;
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
-    cst.push_back(copy_desc(b.ptr<float>(e.Lp), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, ct));
-    cst.push_back(copy_desc(b.ptr<float>(e.Rp), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, ct));
+    if (e.left)
+      cst.push_back(copy_desc(b.ptr<float>(e.Lp), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, ct));
+    if (e.right)
+      cst.push_back(copy_desc(b.ptr<float>(e.Rp), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, ct));
   }
-  b.op(kOpCopyOut, cst, ct);
+  if (!cst.empty()) b.op(kOpCopyOut, cst, ct);
 
   if (hp->refresh) {
     std::vector<Prod> ps;
     std::vector<QrSide*> sides;
     for (SoapPlan& e : P) {
-      ps.push_back(Prod{b.ptr<float>(e.Lp), b.ptr<float>(e.QLt), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
-                        e.mp, e.mp, e.mp, 0, 1.0f, 0.0f});
-      ps.push_back(Prod{b.ptr<float>(e.Rp), b.ptr<float>(e.QRt), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
-                        e.np, e.np, e.np, 0, 1.0f, 0.0f});
-      sides.push_back(&e.L);
-      sides.push_back(&e.R);
-    }
-    // one refresh = the power step S = statistic * basis, then the QR of S; later repetitions reuse
-    // the first one's descriptors
-    const size_t first = b.ops.size();
-    add_gemm(b, ps);
-    add_qr_ops(b, sides);
-    const size_t last = b.ops.size();
-    for (int it = 1; it < hp->refresh_iters; ++it)
-      for (size_t k = first; k < last; ++k) {
-        const Op o = b.ops[k];
-        b.ops.push_back(o);
+      if (e.left) {
+        ps.push_back(Prod{b.ptr<float>(e.Lp), b.ptr<float>(e.QLt), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
+                          e.mp, e.mp, e.mp, 0, 1.0f, 0.0f});
+        sides.push_back(&e.L);
       }
-    std::vector<ShCopyDesc> co;
-    int cot = 0;
-    for (int64_t i = 0; i < count; ++i) {
-      SoapPlan& e = P[size_t(i)];
-      co.push_back(copy_desc(b.ptr<float>(e.QLt), kDtF32, en[i].QL, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, cot));
-      co.push_back(copy_desc(b.ptr<float>(e.QRt), kDtF32, en[i].QR, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, cot));
+      if (e.right) {
+        ps.push_back(Prod{b.ptr<float>(e.Rp), b.ptr<float>(e.QRt), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
+                          e.np, e.np, e.np, 0, 1.0f, 0.0f});
+        sides.push_back(&e.R);
+      }
     }
-    b.op(kOpCopyOutT, co, cot);
+    if (!ps.empty()) {
+      // one refresh = the power step S = statistic * basis, then the QR of S; later repetitions
+      // reuse the first one's descriptors
+      const size_t first = b.ops.size();
+      add_gemm(b, ps);
+      add_qr_ops(b, sides);
+      const size_t last = b.ops.size();
+      for (int it = 1; it < hp->refresh_iters; ++it)
+        for (size_t k = first; k < last; ++k) {
+          const Op o = b.ops[k];
+          b.ops.push_back(o);
+        }
+      std::vector<ShCopyDesc> co;
+      int cot = 0;
+      for (int64_t i = 0; i < count; ++i) {
+        SoapPlan& e = P[size_t(i)];
+        if (e.left)
+          co.push_back(copy_desc(b.ptr<float>(e.QLt), kDtF32, en[i].QL, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, cot));
+        if (e.right)
+          co.push_back(copy_desc(b.ptr<float>(e.QRt), kDtF32, en[i].QR, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, cot));
+      }
+      b.op(kOpCopyOutT, co, cot);
+    }
   }
   return desc_at + al(b.h.size());
 }
@@ -379,8 +428,8 @@ int workspace_error(size_t need, const char* query) {
 extern "C" {
 
 size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp) {
-  if (check_soap_entries(entries, count, false) != MFSDP_OK) return 0;
   if (check_soap_hp(hp) != MFSDP_OK) return 0;
+  if (check_soap_entries(entries, count, false, precond_limit(hp)) != MFSDP_OK) return 0;
   if (count == 0) return 0;
   Build b;
   size_t desc_at = 0;
@@ -389,9 +438,9 @@ size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
 
 int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
                     void* workspace, size_t workspace_bytes, void* stream) {
-  int rc = check_soap_entries(entries, count, true);
+  int rc = check_soap_hp(hp);
   if (rc != MFSDP_OK) return rc;
-  rc = check_soap_hp(hp);
+  rc = check_soap_entries(entries, count, true, precond_limit(hp));
   if (rc != MFSDP_OK) return rc;
   if (count == 0) return MFSDP_OK;
   Build b;

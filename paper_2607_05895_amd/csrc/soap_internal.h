@@ -19,14 +19,17 @@ constexpr int kQrRowsPerThread = 8;   // panel rows held in registers per thread
 constexpr int kQrMaxDim = kQrPanelThreads * kQrRowsPerThread;  // 4096
 constexpr int kQrApplyCols = 64;      // columns per block of the reflector application
 
-// M <- beta1 M + (1 - beta1) G over the real m x n block, and the padded layouts the products read:
-// Gp (mp x np, row stride np) = G, GMt rows [0, np) = G^T and rows [np, 2 np) = M^T (row stride mp).
-// 64 x 64 tiles over the padded mp x np domain; zeros outside the real block.
+// M <- beta1 M + (1 - beta1) G over the real m x n block, and the padded layouts the products read
+// (each written only if its pointer is set): Gp (mp x np, row stride np) = G; GMt rows [0, np) = G^T
+// and rows [np, 2 np) = M^T (row stride mp); GM (mp x 2 np, row stride 2 np) = [G | M] (a left side
+// without a basis: the right product reads G and M as they are). 64 x 64 tiles over the padded
+// mp x np domain; zeros outside the real block.
 struct SoapPrepDesc {
   const void* grad;
   float* exp_avg;
   float* Gp;
   float* GMt;
+  float* GM;
   int64_t m, n, mp, np;
   int32_t grad_dtype;
   int32_t tiles_n;
@@ -35,11 +38,14 @@ struct SoapPrepDesc {
 
 // Adam in the eigenbasis over the real block: GMr = [G' | M'] (mp x 2 np, row stride 2 np);
 // V <- beta2 V + (1 - beta2) G'^2 (caller m x n), N' = (M' inv_bc1) / (sqrt(V) inv_sqrt_bc2 + eps),
-// stored transposed into NpT (np x mp, row stride mp), zeros outside the real block.
+// stored transposed into NpT (np x mp, row stride mp) for the left back-product, or as it is into Np
+// (mp x np, row stride np) when the left side has no basis (each written only if its pointer is
+// set; Np must not overlap GMr); zeros outside the real block.
 struct SoapAdamDesc {
   const float* GMr;
   float* exp_avg_sq;
   float* NpT;
+  float* Np;
   int64_t m, n, mp, np;
   int32_t tiles_n;
   int32_t tile_begin;

@@ -28,7 +28,8 @@ EXPORTS = ("mfsdp_muon_workspace_size", "mfsdp_muon_step", "mfsdp_muon_step_time
 NOALLOC_SCRATCH_BYTES = 64 << 20
 MAX_GRAD_PARTS = 64
 ABI_VERSION = 6
-SOAP_MAX_DIM = 4096
+SOAP_MAX_DIM = 4096     # longest side with a basis (max_precond_dim at most this)
+SOAP_MAX_SIDE = 65536   # longest side of a SOAP matrix
 
 
 class MuonEntry(ctypes.Structure):
@@ -78,7 +79,7 @@ class SoapHParams(ctypes.Structure):
     _fields_ = [("lr", ctypes.c_double), ("weight_decay", ctypes.c_double), ("beta1", ctypes.c_double),
                 ("beta2", ctypes.c_double), ("eps", ctypes.c_double), ("shampoo_beta", ctypes.c_double),
                 ("shampoo_weight", ctypes.c_double), ("step", ctypes.c_int32), ("refresh", ctypes.c_int32),
-                ("refresh_iters", ctypes.c_int32)]
+                ("refresh_iters", ctypes.c_int32), ("max_precond_dim", ctypes.c_int32)]
 
 
 class PlanParam(ctypes.Structure):
@@ -512,19 +513,22 @@ def inverse_root_t(a, out, p=4, eps=1e-12, eps_rel=1e-6, iters=20, workspace=Non
 
 
 def soap_hparams(lr=3e-3, weight_decay=0.0, beta1=0.95, beta2=0.95, eps=1e-8, shampoo_beta=0.95,
-                 shampoo_weight=0.05, step=1, refresh=False, refresh_iters=1) -> SoapHParams:
+                 shampoo_weight=0.05, step=1, refresh=False, refresh_iters=1, max_precond_dim=0) -> SoapHParams:
+    """max_precond_dim: sides longer than it have no basis (0: 4096)."""
     return SoapHParams(lr, weight_decay, beta1, beta2, eps, shampoo_beta, shampoo_weight, int(step),
-                       int(bool(refresh)), int(refresh_iters))
+                       int(bool(refresh)), int(refresh_iters), int(max_precond_dim))
 
 
 def soap_entry_t(param, grad, exp_avg, exp_avg_sq, L, R, QL, QR, update_out=None) -> SoapEntry:
+    """L and QL (or R and QR) may be None for a side longer than the call's max_precond_dim."""
     if param.dim() != 2:
         raise ValueError(f"param: a SOAP entry is a 2D matrix, got shape {tuple(param.shape)}")
     m, n = param.shape
     f = ("float32",)
+    opt = lambda t, what, shape: _ptr(t, what, shape, f) if t is not None else None  # noqa: E731
     return SoapEntry(_ptr(param, "param"), _ptr(grad, "grad", (m, n)), _ptr(exp_avg, "exp_avg", (m, n), f),
-                     _ptr(exp_avg_sq, "exp_avg_sq", (m, n), f), _ptr(L, "L", (m, m), f), _ptr(R, "R", (n, n), f),
-                     _ptr(QL, "QL", (m, m), f), _ptr(QR, "QR", (n, n), f), m, n, _dt(param), _dt(grad),
+                     _ptr(exp_avg_sq, "exp_avg_sq", (m, n), f), opt(L, "L", (m, m)), opt(R, "R", (n, n)),
+                     opt(QL, "QL", (m, m)), opt(QR, "QR", (n, n)), m, n, _dt(param), _dt(grad),
                      _ptr(update_out, "update_out", (m, n), f) if update_out is not None else None)
 
 

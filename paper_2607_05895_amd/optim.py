@@ -26,8 +26,8 @@ _SHAMPOO_DEFAULTS = dict(lr=1e-3, weight_decay=0.0, beta=1.0, weight=1.0, eps=1e
                          adamw_betas=(0.9, 0.999), adamw_eps=1e-8, adamw_weight_decay=0.01)
 
 _SOAP_DEFAULTS = dict(lr=3e-3, weight_decay=0.01, beta1=0.95, beta2=0.95, eps=1e-8, shampoo_beta=0.95,
-                      precondition_frequency=10, refresh_iters=1, adamw_lr=1e-3, adamw_betas=(0.9, 0.999),
-                      adamw_eps=1e-8, adamw_weight_decay=0.01)
+                      precondition_frequency=10, refresh_iters=1, max_precond_dim=4096, adamw_lr=1e-3,
+                      adamw_betas=(0.9, 0.999), adamw_eps=1e-8, adamw_weight_decay=0.01)
 
 
 def _check_tensor(p: torch.Tensor, what: str) -> None:
@@ -218,12 +218,13 @@ class OwnerShampoo(_OwnerOptimizer):
 class OwnerSOAP(_OwnerOptimizer):
     """SOAP on the owned 2D matrices (Adam in the eigenbasis of the Shampoo statistics; the bases
     start at the identity and are refreshed by a power step + QR after the first step and then
-    every `precondition_frequency` steps) and AdamW on the other tensors. fp32 math on the GPU;
-    matrix sides up to 4096.
+    every `precondition_frequency` steps) and AdamW on the other tensors. fp32 math on the GPU. A
+    matrix side longer than `max_precond_dim` (at most 4096) has no basis and no statistic (the
+    identity on that side); sides up to 65536.
 
     Hyperparameters: lr, weight_decay, beta1, beta2, eps (Adam in the eigenbasis), shampoo_beta
     (statistics S <- shampoo_beta S + (1 - shampoo_beta) G G^T), precondition_frequency,
-    refresh_iters; adamw_lr, adamw_betas, adamw_eps, adamw_weight_decay.
+    refresh_iters, max_precond_dim; adamw_lr, adamw_betas, adamw_eps, adamw_weight_decay.
     """
 
     def __init__(self, params, **kw):
@@ -234,23 +235,29 @@ class OwnerSOAP(_OwnerOptimizer):
         d.update(kw)
         if int(d["precondition_frequency"]) < 1:
             raise ValueError("precondition_frequency must be >= 1")
+        if not 1 <= int(d["max_precond_dim"]) <= 4096:
+            raise ValueError("max_precond_dim must be in [1, 4096]")
         super().__init__(params, d)
 
     def _step_group(self, gi: int, group: dict, mats: List[torch.Tensor], tails: List[torch.Tensor]) -> None:
         # the library takes one step count and one refresh decision per call
         calls: Dict[Tuple[int, bool], list] = {}
+        maxd = int(group["max_precond_dim"])
         for p in mats:
-            if max(p.shape) > native.SOAP_MAX_DIM:
-                raise ValueError(f"SOAP supports matrix sides up to {native.SOAP_MAX_DIM}, got {tuple(p.shape)}")
+            if max(p.shape) > native.SOAP_MAX_SIDE:
+                raise ValueError(f"SOAP supports matrix sides up to {native.SOAP_MAX_SIDE}, got {tuple(p.shape)}")
             st = self.state[p]
-            if "QL" not in st:
+            if "exp_avg" not in st:
                 m, n = p.shape
                 st["exp_avg"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
                 st["exp_avg_sq"] = torch.zeros((m, n), dtype=torch.float32, device=p.device)
-                st["L"] = torch.zeros((m, m), dtype=torch.float32, device=p.device)
-                st["R"] = torch.zeros((n, n), dtype=torch.float32, device=p.device)
-                st["QL"] = torch.eye(m, dtype=torch.float32, device=p.device)
-                st["QR"] = torch.eye(n, dtype=torch.float32, device=p.device)
+                # a side beyond max_precond_dim keeps no statistic and no basis
+                if m <= maxd:
+                    st["L"] = torch.zeros((m, m), dtype=torch.float32, device=p.device)
+                    st["QL"] = torch.eye(m, dtype=torch.float32, device=p.device)
+                if n <= maxd:
+                    st["R"] = torch.zeros((n, n), dtype=torch.float32, device=p.device)
+                    st["QR"] = torch.eye(n, dtype=torch.float32, device=p.device)
                 st["step"] = 0
             st["step"] += 1
             t = st["step"]
@@ -258,14 +265,15 @@ class OwnerSOAP(_OwnerOptimizer):
             calls.setdefault((t, refresh), []).append(p)
         for (t, refresh), ps in calls.items():
             ents = [native.soap_entry_t(p, p.grad, self.state[p]["exp_avg"], self.state[p]["exp_avg_sq"],
-                                        self.state[p]["L"], self.state[p]["R"], self.state[p]["QL"],
-                                        self.state[p]["QR"]) for p in ps]
+                                        self.state[p].get("L"), self.state[p].get("R"), self.state[p].get("QL"),
+                                        self.state[p].get("QR")) for p in ps]
             beta_s = float(group["shampoo_beta"])
             hp = native.soap_hparams(lr=group["lr"], weight_decay=group["weight_decay"], beta1=group["beta1"],
                                      beta2=group["beta2"], eps=group["eps"], shampoo_beta=beta_s,
                                      shampoo_weight=1.0 - beta_s, step=t, refresh=refresh,
-                                     refresh_iters=group["refresh_iters"])
-            key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh, group["refresh_iters"])
+                                     refresh_iters=group["refresh_iters"], max_precond_dim=maxd)
+            key = (tuple((tuple(p.shape), p.dtype, p.grad.dtype) for p in ps), refresh, group["refresh_iters"],
+                   maxd)
             ws = self._workspace(gi, "soap" + ("+" if refresh else "-"), key,
                                  lambda: native.mfsdp_soap_workspace_size(ents, hp), ps[0].device)
             native.soap_step_t(ents, hp, ws)

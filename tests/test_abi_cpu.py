@@ -319,7 +319,7 @@ def _soap_entry(**kw):
 
 
 @pytest.mark.parametrize("bad", [
-    dict(m=0), dict(n=4097), dict(m=5000), dict(param=None), dict(grad=None), dict(exp_avg=None),
+    dict(m=0), dict(n=65537), dict(m=70000), dict(param=None), dict(grad=None), dict(exp_avg=None),
     dict(exp_avg_sq=None), dict(L=None), dict(R=None), dict(QL=None), dict(QR=None), dict(param_dtype=3),
     dict(grad_dtype=-1), dict(QL=FAKE * 7 + 2), dict(exp_avg_sq=FAKE * 4 + 1), dict(update_out=FAKE + 2),
 ])
@@ -333,7 +333,8 @@ def test_soap_rejects_bad_entries(bad):
 @pytest.mark.parametrize("bad", [
     dict(lr=-1.0), dict(weight_decay=-1.0), dict(beta1=1.0), dict(beta2=-0.1), dict(beta1=float("nan")),
     dict(eps=0.0), dict(shampoo_beta=-1.0), dict(shampoo_weight=float("inf")), dict(step=0),
-    dict(refresh_iters=0), dict(refresh_iters=101), dict(lr=float("inf")),
+    dict(refresh_iters=0), dict(refresh_iters=101), dict(lr=float("inf")), dict(max_precond_dim=-1),
+    dict(max_precond_dim=4097),
 ])
 def test_soap_rejects_bad_hparams(bad):
     hp = native.soap_hparams(**bad)
@@ -423,3 +424,19 @@ def test_noalloc_rejects_entries_beyond_the_scratch_before_any_gpu_work():
         native.mfsdp_muon_step_noalloc([_entry(m=0)], hp, 0)
     assert ei.value.status == native.E_INVALID
     native.mfsdp_muon_step_noalloc([], hp, 0)  # count == 0 is a no-op
+
+
+def test_soap_sides_beyond_the_preconditioned_limit():
+    """A side longer than max_precond_dim has no basis: its statistic and basis pointers are not
+    required, and its d x d buffers drop out of the workspace (size queries only: no GPU work)."""
+    two = native.mfsdp_soap_workspace_size([_soap_entry(m=3000, n=200)], native.soap_hparams())
+    one = native.mfsdp_soap_workspace_size([_soap_entry(m=3000, n=200)], native.soap_hparams(max_precond_dim=2048))
+    mp = 3072
+    assert two - one >= 3 * mp * mp * 4   # Q_L, Q_L^T / the power step, and L of the left side
+    assert native.mfsdp_soap_workspace_size([_soap_entry(m=20000, n=4096, L=None, QL=None)],
+                                            native.soap_hparams()) > 0
+    assert native.mfsdp_soap_workspace_size([_soap_entry(m=5000, n=6000, L=None, QL=None, R=None, QR=None)],
+                                            native.soap_hparams()) > 0
+    # a side within the limit still needs its pointers
+    with pytest.raises(native.MfsdpError, match="NULL"):
+        native.mfsdp_soap_step([_soap_entry(m=20000, n=200, R=None)], native.soap_hparams(), FAKE * 16, 1 << 40, 0)

@@ -159,6 +159,55 @@ def test_owner_soap_three_steps_match_oracle():
         assert check_bf16_param(from_dev(p.detach()), pout, 3e-3 * np.linalg.norm(N), 1e-4) <= 1.0, name
 
 
+def test_owner_soap_on_llama_layer_shapes():
+    """OwnerSOAP on Llama-3-8B layer shapes over two steps (refresh after the first): the FFN
+    matrices 14336 x 4096 and 4096 x 14336 keep a 4096 x 4096 basis on their short side only (the
+    long side is beyond max_precond_dim = 4096), a 4096 x 4096 matrix has both; against the oracle.
+    Gradients with a well-conditioned spectrum on the square matrix, so that its refreshed bases are
+    unique up to column signs."""
+    from paper_2607_05895_amd.optim import OwnerSOAP
+    import torch
+    rng = np.random.default_rng(15)
+    model = []
+    for name, (m, n) in (("gate", (14336, 4096)), ("down", (4096, 14336))):
+        p = synth.random_muon_tensors(rng, m, n, synth.BF16, synth.BF16).param
+        gs = [synth.random_muon_tensors(rng, m, n, synth.BF16, synth.BF16).grad for _ in range(2)]
+        model.append((name, p, gs, synth.BF16))
+    p = synth.random_muon_tensors(rng, 4096, 4096, synth.BF16, synth.BF16).param
+    model.append(("wq", p, [synth.f32_to_bf16_bits(g) for g in _well_conditioned_grads(rng, 4096, 2)], synth.BF16))
+    ps, grads = _torch_params(model)
+    opt = OwnerSOAP(ps, lr=3e-3, weight_decay=0.01, precondition_frequency=10)
+    for step in range(2):
+        for p_, g in zip(ps, grads):
+            p_.grad = g[step]
+        opt.step()
+    torch.cuda.synchronize()
+    for (name, p0, gs, dt), p_ in zip(model, ps):
+        m, n = p0.shape
+        st = opt.state[p_]
+        assert ("L" in st) == (m <= 4096) and ("R" in st) == (n <= 4096), name
+        M, V = np.zeros((m, n)), np.zeros((m, n))
+        L = np.zeros((m, m)) if m <= 4096 else None
+        R = np.zeros((n, n)) if n <= 4096 else None
+        QL = np.eye(m) if m <= 4096 else None
+        QR = np.eye(n) if n <= 4096 else None
+        pin = p0
+        for step in range(2):
+            hp = OSP.SoapHParams(lr=3e-3, weight_decay=0.01, refresh=step == 0)
+            pout, M, V, L, R, QL, QR, N = OSP.soap_step(pin, gs[step], M, V, L, R, QL, QR, step + 1, hp)
+            pin = synth.f32_to_bf16_bits(pout.astype(np.float32))
+        assert rel_fro(from_dev(st["exp_avg"]), M) <= 1e-5, name
+        assert rel_fro(from_dev(st["exp_avg_sq"]), V) <= 1e-5, name
+        for key, S_ref, Q_ref in (("L", L, QL), ("R", R, QR)):
+            if S_ref is None:
+                continue
+            assert rel_fro(from_dev(st[key]), S_ref) <= 1e-5, (name, key)
+            q = from_dev(st["Q" + key])
+            s_ = np.sign(np.sum(q * Q_ref, axis=0))
+            assert rel_fro(q * s_, Q_ref) <= 1e-4, (name, "Q" + key)
+        assert check_bf16_param(from_dev(p_.detach()), pout, 3e-3 * np.linalg.norm(N), 1e-4) <= 1.0, name
+
+
 @pytest.mark.parametrize("which", ["muon", "shampoo", "soap"])
 def test_state_dict_round_trip_continues_identically(which):
     """Three steps, the optimizer rebuilt from its state_dict after the first: the parameters end

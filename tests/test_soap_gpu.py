@@ -153,23 +153,28 @@ class _Mat:
     """One matrix with full-rank statistics and random orthogonal bases (host fp64 copies of the
     fp32 values the device holds)."""
 
-    def __init__(self, rng, m, n, pdt, gdt, g_std=1e-3, bases=True):
+    def __init__(self, rng, m, n, pdt, gdt, g_std=1e-3, bases=True, maxd=4096):
         t = synth.random_muon_tensors(rng, m, n, pdt, gdt, g_std=g_std, p_std=0.02)
         self.m, self.n, self.pdt, self.gdt = m, n, pdt, gdt
         self.p, self.g = t.param, t.grad
         self.M = _f32(rng.standard_normal((m, n)) * g_std)
         self.V = _f32(g_std ** 2 * (0.5 + rng.random((m, n))))
-        A = rng.standard_normal((m, 2 * m)) * g_std
-        B = rng.standard_normal((n, 2 * n)) * g_std
-        self.L, self.R = _f32(A @ A.T), _f32(B @ B.T)
-        self.QL = _f32(_orth(rng, m)) if bases else np.eye(m)
-        self.QR = _f32(_orth(rng, n)) if bases else np.eye(n)
+        # a side longer than maxd has no statistic and no basis
+        self.L = self.QL = self.R = self.QR = None
+        if m <= maxd:
+            A = rng.standard_normal((m, 2 * m)) * g_std
+            self.L = _f32(A @ A.T)
+            self.QL = _f32(_orth(rng, m)) if bases else np.eye(m)
+        if n <= maxd:
+            B = rng.standard_normal((n, 2 * n)) * g_std
+            self.R = _f32(B @ B.T)
+            self.QR = _f32(_orth(rng, n)) if bases else np.eye(n)
 
     def device(self):
         import torch
         self.dp = to_dev(self.p, self.pdt)
         self.dg = to_dev(self.g, self.gdt)
-        f = lambda x: to_dev(x.astype(np.float32), synth.F32)  # noqa: E731
+        f = lambda x: to_dev(x.astype(np.float32), synth.F32) if x is not None else None  # noqa: E731
         self.dM, self.dV, self.dL, self.dR = f(self.M), f(self.V), f(self.L), f(self.R)
         self.dQL, self.dQR = f(self.QL), f(self.QR)
         self.dN = torch.zeros((self.m, self.n), dtype=torch.float32, device="cuda")
@@ -195,11 +200,15 @@ def _check(mat, hp, full_rank=True):
     assert en <= N_TOL, ("N", en)
     assert rel_fro(from_dev(mat.dM), mat.M) <= 1e-6, ("M", rel_fro(from_dev(mat.dM), mat.M))
     assert rel_fro(from_dev(mat.dV), mat.V) <= 1e-5, ("V", rel_fro(from_dev(mat.dV), mat.V))
-    assert rel_fro(from_dev(mat.dL), mat.L) <= 1e-5
-    assert rel_fro(from_dev(mat.dR), mat.R) <= 1e-5
+    for dS, S_ref in ((mat.dL, mat.L), (mat.dR, mat.R)):
+        assert (dS is None) == (S_ref is None)
+        if dS is not None:
+            assert rel_fro(from_dev(dS), S_ref) <= 1e-5
     if hp.refresh:
         for dq, q_ref, S_stat, q_prev in ((mat.dQL, mat.QL, mat.L, mat.QL_prev),
                                           (mat.dQR, mat.QR, mat.R, mat.QR_prev)):
+            if dq is None:   # a side without a basis
+                continue
             qg = from_dev(dq)
             d = qg.shape[0]
             np.testing.assert_allclose(qg.T @ qg, np.eye(d), atol=2e-5)
@@ -379,3 +388,50 @@ def test_soap_benchmark_configuration_full_size(native):
     for x in mats:
         _oracle_step(x, step, hpo)
         _check(x, hpo)
+
+
+# ------------------------------------------------------------------ one-sided preconditioning
+
+ONE_SIDED = [(100, 50), (50, 100), (100, 200), (40, 50), (64, 64), (65, 30), (129, 64)]
+
+
+def test_soap_one_sided_grouped_three_steps(native):
+    """max_precond_dim = 64: sides longer than 64 have no basis. One call groups matrices with a
+    basis on the left only, the right only, both and neither (each side at the boundary 64 / 65
+    too), mixed dtypes, over three steps (no refresh, refresh, refresh with 3 repetitions), the
+    gradient redrawn every step."""
+    _say("soap one-sided grouped three steps")
+    rng = np.random.default_rng(9700)
+    mats = [_Mat(rng, m, n, synth.BF16 if i % 2 == 0 else synth.F32, synth.BF16 if i % 3 else synth.F32,
+                 maxd=64).device() for i, (m, n) in enumerate(ONE_SIDED)]
+    ents = [x.entry(native) for x in mats]
+    plan = [dict(refresh=False, step=1), dict(refresh=True, step=2), dict(refresh=True, refresh_iters=3, step=3)]
+    ws = native.soap_workspace_t(ents, _hp(native, refresh=True, refresh_iters=3, max_precond_dim=64)[0])
+    for k, kw in enumerate(plan):
+        if k > 0:
+            for x in mats:
+                x.g = synth.random_muon_tensors(rng, x.m, x.n, x.pdt, x.gdt).grad
+                x.dg.copy_(to_dev(x.g, x.gdt))
+        hpn, hpo, step = _hp(native, max_precond_dim=64, **kw)
+        native.soap_step_t(ents, hpn, ws)
+        _sync()
+        for x in mats:
+            _oracle_step(x, step, hpo)
+            _check(x, hpo)
+
+
+@pytest.mark.parametrize("shape", [(14336, 4096), (4096, 14336)])
+def test_soap_llama_ffn_shapes_one_sided(native, shape):
+    """The Llama-3-8B FFN shapes with the default limit (4096): the 14336 side has no basis, the
+    4096 side a 4096 x 4096 basis refreshed by the QR (a 4096 x 4096 full-rank statistic)."""
+    m, n = shape
+    _say(f"soap one-sided {m}x{n}")
+    rng = np.random.default_rng(9800 + m)
+    mat = _Mat(rng, m, n, synth.BF16, synth.BF16).device()
+    assert (mat.L is None) == (m > 4096) and (mat.R is None) == (n > 4096)
+    hpn, hpo, step = _hp(native)
+    ents = [mat.entry(native)]
+    native.soap_step_t(ents, hpn, native.soap_workspace_t(ents, hpn))
+    _sync()
+    _oracle_step(mat, step, hpo)
+    _check(mat, hpo)
