@@ -358,11 +358,11 @@ typedef struct {
 } mfsdp_soap_hparams;
 
 /* Bytes of device workspace mfsdp_soap_step needs for these entries and hyperparameters: per
- * matrix, zero-padded fp32 buffers of 8 mp np + 3 (mp^2 + np^2) floats (mp, np = m, n rounded up
- * to 128) and 16 (m + n) + 512 floats for the QR panels when both sides have a basis (a side
- * without one drops its 3 d^2 + 16 d + 256 floats and, on the left, 2 mp np more); plus launch
- * descriptors. Data pointers are
- * not used. 0 on invalid arguments; count == 0 returns 0 with no error. */
+ * matrix, zero-padded fp32 buffers of 8 mp np floats (mp, np = m, n rounded up to 128) and, per
+ * side with a basis (padded length dp), 3 dp^2 + 640 dp + 9 * 128^2 floats: statistic, basis and
+ * refresh product, and the QR's per-block reflectors and products (a side without a basis drops
+ * all of these and, on the left, 2 mp np more); plus launch descriptors. Data pointers are not
+ * used. 0 on invalid arguments; count == 0 returns 0 with no error. */
 size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
                                  const mfsdp_soap_hparams* hp);
 

@@ -183,12 +183,11 @@ __global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __rest
   const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
   const int t = threadIdx.x, c = t & 63, rr = t >> 6;
   const int64_t gc = int64_t(tj) * kTile + c;
-  if (gc >= d.d) return;
   g_f32* X = (g_f32*)(d.X);
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
     const int64_t gr = int64_t(ti) * kTile + rr + 4 * i;
-    if (gr < d.d) X[gr * d.ld + gc] = gr == gc ? 1.0f : 0.0f;
+    X[gr * d.ld + gc] = (gr == gc && gr < d.d) ? 1.0f : 0.0f;
   }
 }
 
@@ -197,10 +196,10 @@ __global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __rest
 // tau = 0 when nothing below the pivot is non-zero) and the compact-WY factor T of the panel
 // (T_kk = tau_k, T_{0:k,k} = -tau_k T_{0:k,0:k} V_{:,0:k}^T v_k), so that H_1 ... H_jb = I - V T V^T.
 // One 512-thread workgroup per panel; thread t holds rows t + 512 i (i < 8) of the panel in
-// registers. Per column: one block reduction for the norm below the pivot, one for the 15 dot
-// products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k, for T), whose 15
-// totals are formed once in LDS and then read by every thread. Every sum is
-// taken in a fixed order.
+// registers (the panel's columns are rows of the transposed matrix: each is read coalesced). Per
+// column: one block reduction for the norm below the pivot, one for the 15 dot products v_k . a_l
+// (l > k, to update the later columns) and v_i . v_k (i < k, for T), whose 15 totals are formed
+// once in LDS and then read by every thread. Every sum is taken in a fixed order.
 __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanelDesc* __restrict__ descs) {
   __shared__ float red1[kQrPanelThreads / 64];
   __shared__ float red2[kQrPanelThreads / 64][kQrPanel];
@@ -210,27 +209,22 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
   const QrPanelDesc& d = descs[blockIdx.x];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int jb = d.jb;
+  const int rows = jb > 0 ? d.d - d.c : 0;  // panel rows [c, d)
   float a[kQrRowsPerThread][kQrPanel];
+  {
+    const g_cf32* At = (const g_cf32*)(d.At) + int64_t(d.c) * d.ld + d.c;
 #pragma unroll
-  for (int i = 0; i < kQrRowsPerThread; ++i) {
-    const int lr = t + kQrPanelThreads * i;
-    if (lr < d.rows) {
-      const g_cf32x4* row = (const g_cf32x4*)(d.A + (int64_t(d.j0) + lr) * d.lda + d.j0);
+    for (int k = 0; k < kQrPanel; ++k)
 #pragma unroll
-      for (int q = 0; q < kQrPanel / 4; ++q) {
-        const f32x4 v = row[q];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) a[i][4 * q + j] = (4 * q + j < jb) ? v[j] : 0.0f;
+      for (int i = 0; i < kQrRowsPerThread; ++i) {
+        const int lr = t + kQrPanelThreads * i;
+        a[i][k] = (lr < rows && k < jb) ? At[int64_t(k) * d.ld + lr] : 0.0f;
       }
-    } else {
-#pragma unroll
-      for (int k = 0; k < kQrPanel; ++k) a[i][k] = 0.0f;
-    }
   }
   if (t < kQrPanel * kQrPanel) Ts[t / kQrPanel][t % kQrPanel] = 0.0f;
   // register rows that hold panel rows (uniform); the others are zero and are skipped. Columns
   // >= jb are zero as well: their dot products are exactly 0 and they stay 0.
-  const int used = (d.rows + kQrPanelThreads - 1) / kQrPanelThreads;
+  const int used = (rows + kQrPanelThreads - 1) / kQrPanelThreads;
 
   unrolled<kQrPanel>([&](auto kc) {
     constexpr int k = decltype(kc)::value;
@@ -314,147 +308,148 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
     }
   });
   __syncthreads();
+  // the panel's 16 columns of V and rows of Vt over every block row: rows [0, c - j0) above the
+  // panel are zero, rows [c - j0, vrows) are the registers (zero from d on; vrows - (c - j0) =
+  // dp - c <= kQrMaxDim)
+  const int top = d.c - d.j0, s16 = top;  // the panel's first column within the block = c - j0
+  {
+    g_f32* V = (g_f32*)(d.V) + s16;
+    g_f32* Vt = (g_f32*)(d.Vt) + int64_t(s16) * d.ldvt;
+    const int below = d.vrows - top;
 #pragma unroll
-  for (int i = 0; i < kQrRowsPerThread; ++i) {
-    const int lr = t + kQrPanelThreads * i;
-    if (lr < d.rows) {
-      g_f32x4* vrow = (g_f32x4*)(d.V + int64_t(lr) * kQrPanel);
+    for (int i = 0; i < kQrRowsPerThread; ++i) {
+      const int lr = t + kQrPanelThreads * i;
+      if (lr < below) {
+        g_f32x4* vrow = (g_f32x4*)(V + int64_t(top + lr) * kQrBlock);
 #pragma unroll
-      for (int q = 0; q < kQrPanel / 4; ++q)
-        vrow[q] = f32x4{a[i][4 * q], a[i][4 * q + 1], a[i][4 * q + 2], a[i][4 * q + 3]};
+        for (int q = 0; q < kQrPanel / 4; ++q)
+          vrow[q] = f32x4{a[i][4 * q], a[i][4 * q + 1], a[i][4 * q + 2], a[i][4 * q + 3]};
+#pragma unroll
+        for (int k = 0; k < kQrPanel; ++k) Vt[int64_t(k) * d.ldvt + top + lr] = a[i][k];
+      }
+    }
+    for (int r = t; r < top; r += kQrPanelThreads) {
+#pragma unroll
+      for (int q = 0; q < kQrPanel / 4; ++q) ((g_f32x4*)(V + int64_t(r) * kQrBlock))[q] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+      for (int k = 0; k < kQrPanel; ++k) Vt[int64_t(k) * d.ldvt + r] = 0.0f;
     }
   }
-  if (t < kQrPanel * kQrPanel) ((g_f32*)d.T)[t] = Ts[t / kQrPanel][t % kQrPanel];
+  if (t < kQrPanel * kQrPanel)
+    ((g_f32*)d.T)[int64_t(s16 + t / kQrPanel) * kQrBlock + s16 + t % kQrPanel] = Ts[t / kQrPanel][t % kQrPanel];
 }
 
-// X <- X - V (T^T (V^T X)) on one block of 64 columns, all `rows` rows. Thread (q, g) = (t % 16,
-// t / 16) owns the column quad 4q .. 4q + 3 and the rows g, g + 16, ... (16-byte loads and stores).
-// A first pass forms the 16 column sums W = V^T X: per thread, then over the four row groups of a
-// wave (lanes 16 and 32 apart), then over the four waves through LDS, in a fixed order; one wave
-// forms Y = T^T W; a second pass subtracts V Y.
-__global__ __launch_bounds__(256) void qr_apply_kernel(const QrApplyDesc* __restrict__ descs, int count) {
-  __shared__ float red[4][kQrPanel][kQrApplyCols];
-  __shared__ float ys[kQrPanel][kQrApplyCols];
+// x <- x - V_s (T_s^T (V_s^T x)) for one column x of A (a row of At, rows [c, d) of A): thread t
+// holds entries t + 256 i in registers, forms its part of the 16 sums V_s^T x (the panel's V rows are
+// 64 contiguous bytes), the workgroup reduces them in a fixed order (DPP reduce-scatter within each
+// row of 16 lanes, then over the wave's four rows, then over the four waves through LDS), 16
+// threads form y = T_s^T w (T_s upper triangular), and every thread subtracts V_s y from its
+// entries. The column is read once and written once.
+__global__ __launch_bounds__(kQrColThreads) void qr_col_kernel(const QrColDesc* __restrict__ descs, int count) {
+  __shared__ float red[kQrColThreads / 64][kQrPanel];
+  __shared__ float ws[kQrPanel];
+  __shared__ float ys[kQrPanel];
   const int e = find_desc(descs, count, blockIdx.x);
-  const QrApplyDesc& d = descs[e];
-  const int lt = blockIdx.x - d.tile_begin;
+  const QrColDesc& d = descs[e];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
-  const int q = t & 15, g = t >> 4;
-  const int lc = lt * kQrApplyCols + 4 * q;  // first column of this thread's quad, within [0, cols)
-  const bool live = lc < d.cols, full = lc + 4 <= d.cols;
-  g_f32* X = (g_f32*)(d.X) + int64_t(d.row0) * d.ldx + d.c0 + (live ? lc : 0);
-  const g_cf32x4* V = (const g_cf32x4*)(d.V);
-  auto load4 = [&](int64_t o) -> f32x4 {
-    if (full) return *(const g_cf32x4*)(X + o);
-    f32x4 x = {0.0f, 0.0f, 0.0f, 0.0f};
+  const int64_t col = int64_t(d.c) + kQrPanel + (blockIdx.x - d.tile_begin);
+  g_f32* x = (g_f32*)(d.At) + col * d.ld + d.c;
+  const g_cf32* V = (const g_cf32*)(d.V);
+  const int used = (d.rows + kQrColThreads - 1) / kQrColThreads;  // uniform
+  float xr[kQrColRows];
+  float part[kQrPanel];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (lc + j < d.cols) x[j] = X[o + j];
-    return x;
-  };
-  float wk[4][kQrPanel];
+  for (int k = 0; k < kQrPanel; ++k) part[k] = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int i = 0; i < kQrColRows; ++i) {
+    xr[i] = 0.0f;
+    if (i < used) {
+      const int r = t + kQrColThreads * i;
+      if (r < d.rows) {
+        xr[i] = x[r];
+        const g_cf32x4* vr = (const g_cf32x4*)(V + int64_t(r) * kQrBlock);
 #pragma unroll
-    for (int k = 0; k < kQrPanel; ++k) wk[j][k] = 0.0f;
-  if (live) {
-#pragma unroll 4
-    for (int r = g; r < d.rows; r += 16) {
-      const f32x4 x = load4(int64_t(r) * d.ldx);
+        for (int q = 0; q < kQrPanel / 4; ++q) {
+          const f32x4 v = vr[q];
 #pragma unroll
-      for (int qq = 0; qq < kQrPanel / 4; ++qq) {
-        const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + qq];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) wk[j][4 * qq + i] += v[i] * x[j];
+          for (int j = 0; j < 4; ++j) part[4 * q + j] += v[j] * xr[i];
+        }
       }
     }
   }
-  // lanes l, l ^ 16, l ^ 32, l ^ 48 hold the same columns (row groups 4w .. 4w + 3)
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int k = 0; k < kQrPanel; ++k) {
-      float v = wk[j][k];
-      v += __shfl_xor(v, 16);
-      v += __shfl_xor(v, 32);
-      wk[j][k] = v;
-    }
-  if (lane < 16) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int k = 0; k < kQrPanel; ++k) red[w][k][4 * q + j] = wk[j][k];
-  }
+  float rsum = row_reduce_scatter16(part, lane & 15);
+  rsum += __shfl_xor(rsum, 16);
+  rsum += __shfl_xor(rsum, 32);
+  if (lane < kQrPanel) red[w][lane] = rsum;
   __syncthreads();
-  if (t < kQrApplyCols) {
+  if (t < kQrPanel) ws[t] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
+  __syncthreads();
+  if (t < kQrPanel) {
     const g_cf32* T = (const g_cf32*)(d.T);
-    float W[kQrPanel];
-#pragma unroll
-    for (int k = 0; k < kQrPanel; ++k) W[k] = ((red[0][k][t] + red[1][k][t]) + red[2][k][t]) + red[3][k][t];
-#pragma unroll
-    for (int i = 0; i < kQrPanel; ++i) {
-      float y = 0.0f;
-#pragma unroll
-      for (int k = 0; k <= i; ++k) y += T[k * kQrPanel + i] * W[k];
-      ys[i][t] = y;
-    }
+    float y = 0.0f;
+    for (int k = 0; k <= t; ++k) y += T[k * kQrBlock + t] * ws[k];
+    ys[t] = y;
   }
   __syncthreads();
-  if (!live) return;
-  float y[4][kQrPanel];
+  float y[kQrPanel];
 #pragma unroll
-  for (int j = 0; j < 4; ++j)
+  for (int k = 0; k < kQrPanel; ++k) y[k] = ys[k];
 #pragma unroll
-    for (int k = 0; k < kQrPanel; ++k) y[j][k] = ys[k][4 * q + j];
-#pragma unroll 4
-  for (int r = g; r < d.rows; r += 16) {
-    const int64_t o = int64_t(r) * d.ldx;
-    f32x4 x = load4(o);
-    f32x4 s = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int i = 0; i < kQrColRows; ++i) {
+    if (i < used) {
+      const int r = t + kQrColThreads * i;
+      if (r < d.rows) {
+        const g_cf32x4* vr = (const g_cf32x4*)(V + int64_t(r) * kQrBlock);
+        float sub = 0.0f;
 #pragma unroll
-    for (int qq = 0; qq < kQrPanel / 4; ++qq) {
-      const f32x4 v = V[int64_t(r) * (kQrPanel / 4) + qq];
+        for (int q = 0; q < kQrPanel / 4; ++q) {
+          const f32x4 v = vr[q];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s[j] += v[i] * y[j][4 * qq + i];
-    }
-    if (full) {
-      *(g_f32x4*)(X + o) = x - s;
-    } else {
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (lc + j < d.cols) X[o + j] = x[j] - s[j];
+          for (int j = 0; j < 4; ++j) sub += v[j] * y[4 * q + j];
+        }
+        x[r] = xr[i] - sub;
+      }
     }
   }
 }
 
-// Transposed boundary copy: dst[c][r] = src[r][c] for r < rows, c < cols (64 x 64 tiles over the
-// real block, through a padded LDS tile).
-__global__ __launch_bounds__(256) void copy_out_t_kernel(const ShCopyDesc* __restrict__ descs, int count) {
-  __shared__ float tt[kTile][kTile + 1];
-  const int e = find_desc(descs, count, blockIdx.x);
-  const ShCopyDesc& d = descs[e];
-  const int lt = blockIdx.x - d.tile_begin;
-  const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
-  const int t = threadIdx.x, c = t & 63, rr = t >> 6;
-  const g_cf32* src = (const g_cf32*)(d.src);
-  g_f32* dst = (g_f32*)(d.dst);
-#pragma unroll 4
-  for (int i = 0; i < 16; ++i) {
-    const int r = rr + 4 * i;
-    const int64_t gr = int64_t(ti) * kTile + r, gc = int64_t(tj) * kTile + c;
-    tt[r][c] = (gr < d.rows && gc < d.cols) ? src[gr * d.ld_src + gc] : 0.0f;
+// The block's compact-WY factor: T held in LDS; for each panel s = 1 .. 7 (first column n0 = 16 s),
+// M = G[0:n0, n0:n0+16] T_s (G summed over its partials in order), then
+// T[0:n0, n0:n0+16] = -T[0:n0, 0:n0] M over the upper triangle of T[0:n0, 0:n0].
+__global__ __launch_bounds__(256) void qr_t_kernel(const QrTDesc* __restrict__ descs) {
+  __shared__ float Tl[kQrBlock][kQrBlock + 1];
+  __shared__ float M1[kQrBlock - kQrPanel][kQrPanel + 1];
+  const QrTDesc& d = descs[blockIdx.x];
+  const int t = threadIdx.x;
+  g_f32* T = (g_f32*)(d.T);
+  const g_cf32* G = (const g_cf32*)(d.G);
+  for (int idx = t; idx < kQrBlock * kQrBlock; idx += 256) {
+    const int i = idx / kQrBlock, j = idx % kQrBlock;
+    Tl[i][j] = (i / kQrPanel == j / kQrPanel) ? T[idx] : 0.0f;
   }
   __syncthreads();
-#pragma unroll 4
-  for (int i = 0; i < 16; ++i) {
-    const int r = rr + 4 * i;  // destination row = source column
-    const int64_t dr = int64_t(tj) * kTile + r, dc = int64_t(ti) * kTile + c;
-    if (dr < d.cols && dc < d.rows) dst[dr * d.ld_dst + dc] = tt[c][r];
+  for (int s = 1; s < kQrBlock / kQrPanel; ++s) {
+    const int n0 = kQrPanel * s;
+    for (int idx = t; idx < n0 * kQrPanel; idx += 256) {
+      const int i = idx / kQrPanel, j = idx % kQrPanel;
+      float acc = 0.0f;
+      for (int k = 0; k < kQrPanel; ++k) {
+        float g = 0.0f;
+        for (int q = 0; q < d.nG; ++q) g += G[int64_t(q) * kQrBlock * kQrBlock + i * kQrBlock + n0 + k];
+        acc += g * Tl[n0 + k][n0 + j];
+      }
+      M1[i][j] = acc;
+    }
+    __syncthreads();
+    for (int idx = t; idx < n0 * kQrPanel; idx += 256) {
+      const int i = idx / kQrPanel, j = idx % kQrPanel;
+      float acc = 0.0f;
+      for (int k = i; k < n0; ++k) acc += Tl[i][k] * M1[k][j];
+      Tl[i][n0 + j] = -acc;
+    }
+    __syncthreads();
   }
+  for (int idx = t; idx < kQrBlock * kQrBlock; idx += 256) T[idx] = Tl[idx / kQrBlock][idx % kQrBlock];
 }
 
 }  // namespace
@@ -485,15 +480,15 @@ hipError_t launch_qr_panel(const QrPanelDesc* d, int count, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_qr_apply(const QrApplyDesc* d, int count, int total_blocks, hipStream_t st) {
+hipError_t launch_qr_col(const QrColDesc* d, int count, int total_blocks, hipStream_t st) {
   if (total_blocks <= 0 || count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(qr_apply_kernel, dim3(total_blocks), dim3(256), 0, st, d, count);
+  hipLaunchKernelGGL(qr_col_kernel, dim3(total_blocks), dim3(kQrColThreads), 0, st, d, count);
   return hipGetLastError();
 }
 
-hipError_t launch_copy_out_transposed(const ShCopyDesc* d, int count, int total_tiles, hipStream_t st) {
-  if (total_tiles <= 0 || count <= 0) return hipSuccess;
-  hipLaunchKernelGGL(copy_out_t_kernel, dim3(total_tiles), dim3(256), 0, st, d, count);
+hipError_t launch_qr_t(const QrTDesc* d, int count, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(qr_t_kernel, dim3(count), dim3(256), 0, st, d);
   return hipGetLastError();
 }
 

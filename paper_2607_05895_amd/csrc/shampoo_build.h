@@ -44,8 +44,8 @@ struct Arena {
 };
 
 enum OpKind {
-  kOpCopyIn, kOpCopyOut, kOpCopyOutT, kOpGemm, kOpNorm, kOpScalars, kOpInit, kOpApply,
-  kOpSoapPrep, kOpSoapAdam, kOpEye, kOpQrPanel, kOpQrApply
+  kOpCopyIn, kOpCopyOut, kOpGemm, kOpNorm, kOpScalars, kOpInit, kOpApply,
+  kOpSoapPrep, kOpSoapAdam, kOpEye, kOpQrPanel, kOpQrCol, kOpQrT
 };
 struct Op {
   OpKind kind;
@@ -144,9 +144,6 @@ inline int run(Build& b, char* ws, size_t desc_at, hipStream_t st, const RunScal
     switch (o.kind) {
       case kOpCopyIn: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 0, st); break;
       case kOpCopyOut: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 1, st); break;
-      case kOpCopyOutT:
-        e = launch_copy_out_transposed(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, st);
-        break;
       case kOpGemm: e = launch_sh_gemm(reinterpret_cast<ShGemmDesc*>(dp), o.count, o.total, st); break;
       case kOpNorm: e = launch_sh_norm(reinterpret_cast<ShNormDesc*>(dp), o.count, o.total, st); break;
       case kOpScalars:
@@ -165,7 +162,8 @@ inline int run(Build& b, char* ws, size_t desc_at, hipStream_t st, const RunScal
         break;
       case kOpEye: e = launch_soap_eye(reinterpret_cast<SoapEyeDesc*>(dp), o.count, o.total, st); break;
       case kOpQrPanel: e = launch_qr_panel(reinterpret_cast<QrPanelDesc*>(dp), o.count, st); break;
-      case kOpQrApply: e = launch_qr_apply(reinterpret_cast<QrApplyDesc*>(dp), o.count, o.total, st); break;
+      case kOpQrCol: e = launch_qr_col(reinterpret_cast<QrColDesc*>(dp), o.count, o.total, st); break;
+      case kOpQrT: e = launch_qr_t(reinterpret_cast<QrTDesc*>(dp), o.count, st); break;
     }
     if (e != hipSuccess) return hip_err(e, "kernel launch");
   }

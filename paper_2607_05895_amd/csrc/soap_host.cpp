@@ -15,11 +15,15 @@
 //   Z       = Q_L N'             P = Q_L,    Q = N'^T               (mp x np, K = mp)
 //   N       = Z Q_R^T            P = Z,      Q = Q_R                (mp x np, K = np)
 //   L, R statistics              P = Q = G (sym, K = np), P = Q = G^T (sym, K = mp)
-//   refresh S = L Q_L            P = L,      Q = Q_L^T              (mp x mp, K = mp)
+//   refresh S^T = Q_L^T L        P = Q_L^T,  Q = L                  (mp x mp, K = mp)
 // The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
 // with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
-// block: per 16-column panel one panel launch (V, T) and one launch that applies the block
-// reflector to the trailing columns of S and to the accumulated Q^T (started at the identity).
+// block, with S held transposed (each column of S one contiguous row) and Q accumulated from the
+// identity as Q <- Q H_B per 128-column block B. Per block: eight 16-column panel launches (V, T
+// of the panel), each but the last followed by a launch that applies the panel's reflectors to the
+// block's later columns (one workgroup per column); then on the Shampoo GEMM G = V^T V (K-split),
+// the block's T (one workgroup), U = V T^T, W = X V and X <- X - W U^T for X = the trailing
+// columns of S (as rows of S^T) and X = Q's columns [j0, dp).
 // Zero padding is exact: padded rows and columns of G, M, the bases and the statistics are zero, so
 // every product's real block is unaffected and its padded part is zero.
 #include <hip/hip_runtime.h>
@@ -37,73 +41,25 @@ using namespace mfsdp::shb;
 
 namespace {
 
-// One basis refresh problem: S (d_pad x d_pad, real block d x d) is factored in place, Qt
-// accumulates Q^T.
+// One basis refresh problem: St (dp x dp) holds S^T (real block d x d) and is factored in place; Q
+// (dp x dp) accumulates the orthonormal factor (row-major, zero padding). V, Vt, T, G, U, Ws, Wq hold
+// the current block's reflectors, factor and products.
 struct QrSide {
   int64_t d = 0, dp = 0;
-  size_t S = 0, Qt = 0, V = 0, T = 0;
+  size_t St = 0, Q = 0, V = 0, Vt = 0, T = 0, G = 0, U = 0, Ws = 0, Wq = 0;
 };
 
-void plan_qr_buffers(QrSide& s, Arena& a) {
-  s.V = a.take(size_t(s.d) * kQrPanel * sizeof(float));
-  s.T = a.take(size_t(kQrPanel) * kQrPanel * sizeof(float));
-}
+constexpr int64_t kQrMaxGram = (kQrMaxDim + kQrGramChunk - 1) / kQrGramChunk;  // partials of V^T V
 
-// Qt = I, then per panel: factor it, apply its reflector to S's trailing columns and to Qt.
-// Sides are listed largest first in every grouped launch.
-void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
-  if (sides.empty()) return;
-  std::stable_sort(sides.begin(), sides.end(), [](const QrSide* x, const QrSide* y) { return x->d > y->d; });
-  std::vector<SoapEyeDesc> ey;
-  int et = 0;
-  for (QrSide* s : sides) {
-    SoapEyeDesc e{};
-    e.X = b.ptr<float>(s->Qt);
-    e.ld = s->dp;
-    e.d = s->d;
-    const int64_t tn = (s->d + kShCopyTile - 1) / kShCopyTile;
-    e.tiles_n = int32_t(tn);
-    e.tile_begin = et;
-    et += int(tn * tn);
-    ey.push_back(e);
-  }
-  b.op(kOpEye, ey, et);
-  for (int64_t j0 = 0; j0 < sides[0]->d; j0 += kQrPanel) {
-    std::vector<QrPanelDesc> pd;
-    std::vector<QrApplyDesc> ad;
-    int at = 0;
-    for (QrSide* s : sides) {
-      if (s->d <= j0) continue;
-      QrPanelDesc p{};
-      p.A = b.ptr<float>(s->S);
-      p.lda = s->dp;
-      p.V = b.ptr<float>(s->V);
-      p.T = b.ptr<float>(s->T);
-      p.j0 = int32_t(j0);
-      p.jb = int32_t(std::min<int64_t>(kQrPanel, s->d - j0));
-      p.rows = int32_t(s->d - j0);
-      pd.push_back(p);
-      auto apply = [&](size_t X, int64_t c0, int64_t cols) {
-        if (cols <= 0) return;
-        QrApplyDesc a{};
-        a.X = b.ptr<float>(X);
-        a.ldx = s->dp;
-        a.V = p.V;
-        a.T = p.T;
-        a.row0 = p.j0;
-        a.rows = p.rows;
-        a.c0 = int32_t(c0);
-        a.cols = int32_t(cols);
-        a.tile_begin = at;
-        at += int((cols + kQrApplyCols - 1) / kQrApplyCols);
-        ad.push_back(a);
-      };
-      apply(s->S, j0 + p.jb, s->d - j0 - p.jb);
-      apply(s->Qt, 0, s->d);
-    }
-    b.op(kOpQrPanel, pd, int(pd.size()));
-    b.op(kOpQrApply, ad, at);
-  }
+void plan_qr_buffers(QrSide& s, Arena& a) {
+  const size_t f = sizeof(float), col = size_t(s.dp) * kQrBlock * f, sq = size_t(kQrBlock) * kQrBlock * f;
+  s.V = a.take(col);
+  s.Vt = a.take(col);
+  s.U = a.take(col);
+  s.Ws = a.take(col);
+  s.Wq = a.take(col);
+  s.T = a.take(sq);
+  s.G = a.take(size_t(kQrMaxGram) * sq);
 }
 
 // A grouped product before its tile offset is known (so that a launch can be ordered by cost).
@@ -124,6 +80,116 @@ void add_gemm(Build& b, std::vector<Prod> ps) {
     gs.push_back(gemm_desc(p.P, p.Q, p.E, p.C, p.ldp, p.ldq, p.lde, p.ldc, p.M, p.N, p.K, p.sym, p.alpha,
                            p.beta, 0.0f, gt));
   b.op(kOpGemm, gs, gt);
+}
+
+// The Householder QR of each side's S (given as St): Q = H_1 H_2 ... H_d into each side's Q buffer
+// (set to the identity first). Sides are listed largest first in every grouped launch.
+void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
+  if (sides.empty()) return;
+  std::stable_sort(sides.begin(), sides.end(), [](const QrSide* x, const QrSide* y) { return x->d > y->d; });
+  {
+    std::vector<SoapEyeDesc> ey;
+    int et = 0;
+    for (QrSide* s : sides) {
+      SoapEyeDesc e{};
+      e.X = b.ptr<float>(s->Q);
+      e.ld = s->dp;
+      e.d = s->d;
+      e.dp = s->dp;
+      const int64_t tn = s->dp / kShCopyTile;
+      e.tiles_n = int32_t(tn);
+      e.tile_begin = et;
+      et += int(tn * tn);
+      ey.push_back(e);
+    }
+    b.op(kOpEye, ey, et);
+  }
+  for (int64_t j0 = 0; j0 < sides[0]->d; j0 += kQrBlock) {
+    std::vector<QrSide*> act;
+    for (QrSide* s : sides)
+      if (s->d > j0) act.push_back(s);
+    // panels and their application to the rest of the block
+    for (int64_t c = j0; c < j0 + kQrBlock; c += kQrPanel) {
+      std::vector<QrPanelDesc> pd;
+      std::vector<QrColDesc> cd;
+      int ct = 0;
+      for (QrSide* s : act) {
+        QrPanelDesc p{};
+        p.At = b.ptr<float>(s->St);
+        p.ld = s->dp;
+        p.V = b.ptr<float>(s->V);
+        p.Vt = b.ptr<float>(s->Vt);
+        p.T = b.ptr<float>(s->T);
+        p.ldvt = s->dp;
+        p.j0 = int32_t(j0);
+        p.c = int32_t(c);
+        p.jb = int32_t(std::clamp<int64_t>(s->d - c, 0, kQrPanel));
+        p.d = int32_t(s->d);
+        p.vrows = int32_t(s->dp - j0);
+        pd.push_back(p);
+        const int64_t ncols = std::min(j0 + kQrBlock, s->d) - (c + kQrPanel);
+        if (ncols > 0) {
+          QrColDesc q{};
+          q.At = b.ptr<float>(s->St);
+          q.ld = s->dp;
+          q.V = b.ptr<float>(s->V) + (c - j0) * kQrBlock + (c - j0);
+          q.T = b.ptr<float>(s->T) + (c - j0) * kQrBlock + (c - j0);
+          q.c = int32_t(c);
+          q.rows = int32_t(s->d - c);
+          q.ncols = int32_t(ncols);
+          q.tile_begin = ct;
+          ct += int(ncols);
+          cd.push_back(q);
+        }
+      }
+      b.op(kOpQrPanel, pd, int(pd.size()));
+      if (!cd.empty()) b.op(kOpQrCol, cd, ct);
+    }
+    // G = V^T V in K chunks, then the block's T
+    {
+      std::vector<Prod> gp;
+      std::vector<QrTDesc> td;
+      for (QrSide* s : act) {
+        const int64_t vrows = s->dp - j0;
+        int32_t ng = 0;
+        for (int64_t k0 = 0; k0 < vrows; k0 += kQrGramChunk, ++ng) {
+          const float* vt = b.ptr<float>(s->Vt) + k0;
+          float* g = b.ptr<float>(s->G) + size_t(ng) * kQrBlock * kQrBlock;
+          gp.push_back(Prod{vt, vt, nullptr, g, s->dp, s->dp, 0, kQrBlock, kQrBlock, kQrBlock,
+                            std::min<int64_t>(kQrGramChunk, vrows - k0), 1, 1.0f, 0.0f});
+        }
+        td.push_back(QrTDesc{b.ptr<float>(s->T), b.ptr<float>(s->G), ng});
+      }
+      add_gemm(b, gp);
+      b.op(kOpQrT, td, int(td.size()));
+    }
+    // U = V T^T; W = X V; X <- X - W U^T for the trailing columns of S and for Q's columns [j0, dp)
+    {
+      std::vector<Prod> up, wp, xp;
+      for (QrSide* s : act) {
+        const int64_t vrows = s->dp - j0;
+        float* V = b.ptr<float>(s->V);
+        float* Vt = b.ptr<float>(s->Vt);
+        float* U = b.ptr<float>(s->U);
+        up.push_back(Prod{V, b.ptr<float>(s->T), nullptr, U, kQrBlock, kQrBlock, 0, kQrBlock, vrows, kQrBlock,
+                          kQrBlock, 0, 1.0f, 0.0f});
+        const int64_t trail = s->dp - j0 - kQrBlock;  // St rows [j0 + 128, dp)
+        if (trail > 0 && j0 + kQrBlock < s->d) {
+          float* X = b.ptr<float>(s->St) + (j0 + kQrBlock) * s->dp + j0;
+          float* W = b.ptr<float>(s->Ws);
+          wp.push_back(Prod{X, Vt, nullptr, W, s->dp, s->dp, 0, kQrBlock, trail, kQrBlock, vrows, 0, 1.0f, 0.0f});
+          xp.push_back(Prod{W, U, X, X, kQrBlock, kQrBlock, s->dp, s->dp, trail, vrows, kQrBlock, 0, -1.0f, 1.0f});
+        }
+        float* X = b.ptr<float>(s->Q) + j0;
+        float* W = b.ptr<float>(s->Wq);
+        wp.push_back(Prod{X, Vt, nullptr, W, s->dp, s->dp, 0, kQrBlock, s->dp, kQrBlock, vrows, 0, 1.0f, 0.0f});
+        xp.push_back(Prod{W, U, X, X, kQrBlock, kQrBlock, s->dp, s->dp, s->dp, vrows, kQrBlock, 0, -1.0f, 1.0f});
+      }
+      add_gemm(b, up);
+      add_gemm(b, wp);
+      add_gemm(b, xp);
+    }
+  }
 }
 
 // Per matrix: left / right tell whether that side has a basis (its length is at most
@@ -209,13 +275,13 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     if (e.left) e.NpT = a.take(mn);
     if (e.left) {
       const size_t mm = size_t(e.mp) * size_t(e.mp) * f;
-      e.QLp = a.take(mm);  // later the refresh product S = L Q_L
-      e.QLt = a.take(mm);  // later the accumulated Q_L^T of the refresh
+      e.QLp = a.take(mm);  // later the refresh product S^T = Q_L^T L
+      e.QLt = a.take(mm);  // later the accumulated Q_L of the refresh
       e.Lp = a.take(mm);
       e.L.d = e.m;
       e.L.dp = e.mp;
-      e.L.S = e.QLp;
-      e.L.Qt = e.QLt;
+      e.L.St = e.QLp;
+      e.L.Q = e.QLt;
       plan_qr_buffers(e.L, a);
     }
     if (e.right) {
@@ -225,8 +291,8 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
       e.Rp = a.take(nn);
       e.R.d = e.n;
       e.R.dp = e.np;
-      e.R.S = e.QRp;
-      e.R.Qt = e.QRt;
+      e.R.St = e.QRp;
+      e.R.Q = e.QRt;
       plan_qr_buffers(e.R, a);
     }
   }
@@ -357,28 +423,42 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     std::vector<QrSide*> sides;
     for (SoapPlan& e : P) {
       if (e.left) {
-        ps.push_back(Prod{b.ptr<float>(e.Lp), b.ptr<float>(e.QLt), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
+        ps.push_back(Prod{b.ptr<float>(e.QLt), b.ptr<float>(e.Lp), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
                           e.mp, e.mp, e.mp, 0, 1.0f, 0.0f});
         sides.push_back(&e.L);
       }
       if (e.right) {
-        ps.push_back(Prod{b.ptr<float>(e.Rp), b.ptr<float>(e.QRt), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
+        ps.push_back(Prod{b.ptr<float>(e.QRt), b.ptr<float>(e.Rp), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
                           e.np, e.np, e.np, 0, 1.0f, 0.0f});
         sides.push_back(&e.R);
       }
     }
     if (!ps.empty()) {
-      // one refresh = the power step S = statistic * basis, then the QR of S; later repetitions
-      // reuse the first one's descriptors
+      // one refresh = the power step S^T = basis^T statistic (S = statistic * basis), then the QR
+      // of S, which leaves the new basis Q in the buffer that held the old basis transposed; a
+      // further power step first transposes it back (a copy into the S^T buffer, then that buffer
+      // copied onto itself with its transpose into the basis buffer). Repetitions reuse the first
+      // one's descriptors.
+      std::vector<ShCopyDesc> t1, t2;
+      int n1 = 0, n2 = 0;
+      for (QrSide* q : sides) {
+        t1.push_back(copy_desc(b.ptr<float>(q->Q), kDtF32, b.ptr<float>(q->St), nullptr, q->d, q->d, q->dp, q->dp, 0,
+                               q->dp, q->dp, n1));
+        t2.push_back(copy_desc(b.ptr<float>(q->St), kDtF32, b.ptr<float>(q->St), b.ptr<float>(q->Q), q->d, q->d,
+                               q->dp, q->dp, q->dp, q->dp, q->dp, n2));
+      }
       const size_t first = b.ops.size();
       add_gemm(b, ps);
       add_qr_ops(b, sides);
       const size_t last = b.ops.size();
-      for (int it = 1; it < hp->refresh_iters; ++it)
+      for (int it = 1; it < hp->refresh_iters; ++it) {
+        b.op(kOpCopyIn, t1, n1);
+        b.op(kOpCopyIn, t2, n2);
         for (size_t k = first; k < last; ++k) {
           const Op o = b.ops[k];
           b.ops.push_back(o);
         }
+      }
       std::vector<ShCopyDesc> co;
       int cot = 0;
       for (int64_t i = 0; i < count; ++i) {
@@ -388,7 +468,7 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
         if (e.right)
           co.push_back(copy_desc(b.ptr<float>(e.QRt), kDtF32, en[i].QR, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, cot));
       }
-      b.op(kOpCopyOutT, co, cot);
+      b.op(kOpCopyOut, co, cot);
     }
   }
   return desc_at + al(b.h.size());
@@ -401,20 +481,21 @@ size_t build_factor(int64_t d, const float* a, float* q, char* ws, Build& b, siz
   s.d = d;
   s.dp = rup(d, kShTile);
   const size_t mat = size_t(s.dp) * size_t(s.dp) * sizeof(float);
-  s.S = ar.take(mat);
-  s.Qt = ar.take(mat);
+  s.St = ar.take(mat);
+  s.Q = ar.take(mat);
   plan_qr_buffers(s, ar);
   desc_at = ar.off;
   std::vector<ShCopyDesc> cin;
   int ct = 0;
-  cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.S), nullptr, d, d, d, s.dp, 0, s.dp, s.dp, ct));
+  // St = a^T (the Q buffer takes a itself, then the identity)
+  cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.Q), b.ptr<float>(s.St), d, d, d, s.dp, s.dp, s.dp, s.dp, ct));
   b.op(kOpCopyIn, cin, ct);
   std::vector<QrSide*> sides{&s};
   add_qr_ops(b, sides);
   std::vector<ShCopyDesc> co;
   int cot = 0;
-  co.push_back(copy_desc(b.ptr<float>(s.Qt), kDtF32, q, nullptr, d, d, s.dp, d, 0, d, d, cot));
-  b.op(kOpCopyOutT, co, cot);
+  co.push_back(copy_desc(b.ptr<float>(s.Q), kDtF32, q, nullptr, d, d, s.dp, d, 0, d, d, cot));
+  b.op(kOpCopyOut, co, cot);
   return desc_at + al(b.h.size());
 }
 

@@ -2,8 +2,10 @@
 //
 // The products of the step run on the Shampoo GEMM (sh_gemm_kernel) over zero-padded row-major
 // buffers (multiples of kShTile). The kernels declared here are the ones specific to SOAP: the
-// first-moment pass, the Adam pass in the eigenbasis, and the blocked Householder QR that refreshes
-// a basis (panel factorization + block-reflector application).
+// first-moment pass, the Adam pass in the eigenbasis, and the pieces of the blocked Householder QR
+// that refreshes a basis (16-column panel factorization, the panel's reflector applied to the rest
+// of its 128-column block, and the block's compact-WY factor; the block's update of the trailing
+// matrix and of the accumulated Q runs on the Shampoo GEMM).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -14,10 +16,14 @@
 namespace mfsdp {
 
 constexpr int kQrPanel = 16;          // columns per Householder panel
+constexpr int kQrBlock = 128;         // columns per block reflector (8 panels; the GEMM's tile)
 constexpr int kQrPanelThreads = 512;  // one workgroup per panel (2 waves per SIMD: 256 registers each)
 constexpr int kQrRowsPerThread = 8;   // panel rows held in registers per thread
 constexpr int kQrMaxDim = kQrPanelThreads * kQrRowsPerThread;  // 4096
-constexpr int kQrApplyCols = 64;      // columns per block of the reflector application
+constexpr int kQrColThreads = 256;    // in-block application: one workgroup per column
+constexpr int kQrColRows = kQrMaxDim / kQrColThreads;          // column entries per thread
+constexpr int kQrGramChunk = 512;     // K chunk of the split V^T V product
+static_assert(kQrBlock == kShTile, "the block update runs on the Shampoo GEMM's tiles");
 
 // M <- beta1 M + (1 - beta1) G over the real m x n block, and the padded layouts the products read
 // (each written only if its pointer is set): Gp (mp x np, row stride np) = G; GMt rows [0, np) = G^T
@@ -51,38 +57,58 @@ struct SoapAdamDesc {
   int32_t tile_begin;
 };
 
-// X = I over the real d x d block of a padded buffer (row stride ld).
+// X = I over the real d x d block of a padded dp x dp buffer (row stride ld), zero elsewhere.
 struct SoapEyeDesc {
   float* X;
   int64_t ld;
-  int64_t d;
+  int64_t d, dp;
   int32_t tiles_n;
   int32_t tile_begin;
 };
 
-// Householder factorization of one panel: columns [j0, j0 + jb) of A, rows [j0, j0 + rows)
-// (rows = d - j0 <= kQrMaxDim). Writes V (rows x 16, row-major: column k is v_k, zero above its
-// pivot, 1 on it, zero for k >= jb) and T (16 x 16 upper triangular, H_1 ... H_jb = I - V T V^T).
-// A is only read (R is not needed). The panel's 16 columns must lie inside A's row stride.
+// The refresh factors A (d x d, real block of a padded dp x dp matrix) stored transposed: At is
+// row-major with row stride ld and holds A^T, so column j of A is row j of At (contiguous). Each
+// 128-column block [j0, j0 + 128) of A has its reflectors in V ((dp - j0) x 128, row-major, row 0 =
+// A's row j0), the same transposed in Vt (128 x (dp - j0), row stride ldvt), and its compact-WY
+// factor T (128 x 128 upper triangular, row-major), so that the block's reflectors multiply to
+// H_1 ... H_128 = I - V T V^T (reflectors past the real dimension are the identity: zero columns of
+// V, zero rows and columns of T).
+
+// Householder factorization of panel s of a block: A's columns [c, c + jb) (c = j0 + 16 s), rows
+// [c, d) (d - c <= kQrMaxDim; jb = min(16, d - c), 0 when c >= d). Writes the panel's 16 columns of V
+// and rows of Vt over all dp - j0 block rows (zero above the pivot rows, 1 on them, zero below d and
+// for columns >= jb) and its 16 x 16 factor into T's diagonal block s. A is only read (R is not
+// needed).
 struct QrPanelDesc {
-  const float* A;
-  int64_t lda;
+  const float* At;
+  int64_t ld;
   float* V;
+  float* Vt;
   float* T;
-  int32_t j0, jb, rows;
+  int64_t ldvt;
+  int32_t j0, c, jb, d, vrows;  // vrows = dp - j0
 };
 
-// X <- (I - V T^T V^T) X on rows [row0, row0 + rows) and columns [c0, c0 + cols) of X: the panel's
-// block reflector applied from the left, both to the trailing columns of the matrix being
-// factored and to the accumulated Q^T.
-struct QrApplyDesc {
-  float* X;
-  int64_t ldx;
-  const float* V;
-  const float* T;
-  int32_t row0, rows;
-  int32_t c0, cols;
-  int32_t tile_begin;  // blocks of kQrApplyCols columns, prefix over the launch
+// The reflectors of panel s applied to the block's later columns: x <- (I - V_s T_s^T V_s^T) x for
+// every column x of A in [c + 16, c + 16 + ncols), over rows [c, d), with V_s the panel's 16
+// columns of V and T_s its diagonal block of T. One workgroup per column.
+struct QrColDesc {
+  float* At;
+  int64_t ld;
+  const float* V;  // the panel's first column of V, at row c - j0 (row stride kQrBlock)
+  const float* T;  // the panel's diagonal block of T (row stride kQrBlock)
+  int32_t c, rows, ncols;
+  int32_t tile_begin;  // first workgroup of this problem in the launch
+};
+
+// The block's factor T from its panels' diagonal blocks (already in T) and G = V^T V, given as nG
+// partial sums (consecutive 128 x 128 row-major): for s = 1 .. 7,
+// T[0:16s, 16s:16s+16] = -T[0:16s, 0:16s] G[0:16s, 16s:16s+16] T_s; zero below the diagonal blocks.
+// One workgroup per block.
+struct QrTDesc {
+  float* T;
+  const float* G;
+  int32_t nG;
 };
 
 hipError_t launch_soap_prep(const SoapPrepDesc* d, int count, int total_tiles, float beta1,
@@ -91,8 +117,7 @@ hipError_t launch_soap_adam(const SoapAdamDesc* d, int count, int total_tiles, f
                             float inv_bc1, float inv_sqrt_bc2, hipStream_t st);
 hipError_t launch_soap_eye(const SoapEyeDesc* d, int count, int total_tiles, hipStream_t st);
 hipError_t launch_qr_panel(const QrPanelDesc* d, int count, hipStream_t st);
-hipError_t launch_qr_apply(const QrApplyDesc* d, int count, int total_blocks, hipStream_t st);
-// dst (caller, cols x rows, row stride ld_dst) = transpose of src (padded, rows x cols inside).
-hipError_t launch_copy_out_transposed(const ShCopyDesc* d, int count, int total_tiles, hipStream_t st);
+hipError_t launch_qr_col(const QrColDesc* d, int count, int total_blocks, hipStream_t st);
+hipError_t launch_qr_t(const QrTDesc* d, int count, hipStream_t st);
 
 }  // namespace mfsdp
