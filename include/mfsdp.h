@@ -359,7 +359,7 @@ typedef struct {
 
 /* Bytes of device workspace mfsdp_soap_step needs for these entries and hyperparameters: per
  * matrix, zero-padded fp32 buffers of 8 mp np floats (mp, np = m, n rounded up to 128) and, per
- * side with a basis (padded length dp), 3 dp^2 + 640 dp + 9 * 128^2 floats: statistic, basis and
+ * side with a basis (padded length dp), 3 dp^2 + 640 dp + 17 * 128^2 floats: statistic, basis and
  * refresh product, and the QR's per-block reflectors and products (a side without a basis drops
  * all of these and, on the left, 2 mp np more); plus launch descriptors. Data pointers are not
  * used. 0 on invalid arguments; count == 0 returns 0 with no error. */

@@ -193,19 +193,19 @@ __global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __rest
 
 // Householder factorization of one 16-column panel (LAPACK's convention: for the column x below and
 // on the pivot, beta = -sign(x_0) ||x||, tau = (beta - x_0) / beta, v = x / (x_0 - beta) with v_0 = 1;
-// tau = 0 when nothing below the pivot is non-zero) and the compact-WY factor T of the panel
-// (T_kk = tau_k, T_{0:k,k} = -tau_k T_{0:k,0:k} V_{:,0:k}^T v_k), so that H_1 ... H_jb = I - V T V^T.
-// One 512-thread workgroup per panel; thread t holds rows t + 512 i (i < 8) of the panel in
-// registers (the panel's columns are rows of the transposed matrix: each is read coalesced). Per
-// column: one block reduction for the norm below the pivot, one for the 15 dot products v_k . a_l
-// (l > k, to update the later columns) and v_i . v_k (i < k, for T), whose 15 totals are formed
-// once in LDS and then read by every thread. Every sum is taken in a fixed order.
+// tau = 0 when nothing below the pivot is non-zero). Its 16 x 16 block of T receives tau_k on the
+// diagonal and the dot products v_j . v_k (j < k) above it, from which the applications and the
+// block's factor form what they need. One 512-thread workgroup per panel; thread t holds rows
+// t + 512 i (i < 8) of the panel in registers (the panel's columns are rows of the transposed matrix:
+// each is read coalesced). Per column two block reductions: the norm below the pivot, then the 15
+// dot products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k), whose partials
+// every wave sums itself (lane l: slot l, in wave order) and reads back from its lanes, so that no
+// third barrier is needed. Every sum is taken in a fixed order.
 __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanelDesc* __restrict__ descs) {
   __shared__ float red1[kQrPanelThreads / 64];
   __shared__ float red2[kQrPanelThreads / 64][kQrPanel];
-  __shared__ float tot[kQrPanel];
   __shared__ float alpha_s;
-  __shared__ float Ts[kQrPanel][kQrPanel];
+  __shared__ float Ds[kQrPanel][kQrPanel];
   const QrPanelDesc& d = descs[blockIdx.x];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int jb = d.jb;
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
         a[i][k] = (lr < rows && k < jb) ? At[int64_t(k) * d.ld + lr] : 0.0f;
       }
   }
-  if (t < kQrPanel * kQrPanel) Ts[t / kQrPanel][t % kQrPanel] = 0.0f;
+  if (t < kQrPanel * kQrPanel) Ds[t / kQrPanel][t % kQrPanel] = 0.0f;
   // register rows that hold panel rows (uniform); the others are zero and are skipped. Columns
   // >= jb are zero as well: their dot products are exactly 0 and they stay 0.
   const int used = (rows + kQrPanelThreads - 1) / kQrPanelThreads;
@@ -278,34 +278,27 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
       if (lane < kQrPanel - 1) red2[w][lane] = r;
     }
     __syncthreads();
-    // the 15 block totals, each summed once over the waves in wave order
-    if (t < kQrPanel - 1) {
-      float acc = 0.0f;
+    // the 15 block totals: lane l of every wave sums slot l over the waves in wave order, and the
+    // wave reads the totals from its lanes (red2 and red1 are written again only after the next
+    // step's first barrier)
+    float mine = 0.0f;
 #pragma unroll
-      for (int j = 0; j < kQrPanelThreads / 64; ++j) acc += red2[j][t];
-      tot[t] = acc;
-    }
-    __syncthreads();
-    auto total = [&](int sl) { return tot[sl]; };
-    float f[kQrPanel];
+    for (int j = 0; j < kQrPanelThreads / 64; ++j) mine += red2[j][lane & (kQrPanel - 1)];
+    float tot[kQrPanel - 1];
 #pragma unroll
-    for (int l = k + 1; l < kQrPanel; ++l) f[l] = tau * total(l - 1);
+    for (int sl = 0; sl < kQrPanel - 1; ++sl)
+      tot[sl] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine), sl));
 #pragma unroll
     for (int i = 0; i < kQrRowsPerThread; ++i) {
       if (i < used) {
 #pragma unroll
-        for (int l = k + 1; l < kQrPanel; ++l) a[i][l] -= f[l] * a[i][k];
+        for (int l = k + 1; l < kQrPanel; ++l) a[i][l] -= (tau * tot[l - 1]) * a[i][k];
       }
     }
-    if (t < k) {
-      float acc = 0.0f;
 #pragma unroll
-      for (int j = 0; j < k; ++j)
-        if (j >= t) acc += Ts[t][j] * total(j);
-      Ts[t][k] = -tau * acc;
-    } else if (t == k) {
-      Ts[k][k] = tau;
-    }
+    for (int j = 0; j < k; ++j)
+      if (t == j) Ds[j][k] = tot[j];
+    if (t == k) Ds[k][k] = tau;
   });
   __syncthreads();
   // the panel's 16 columns of V and rows of Vt over every block row: rows [0, c - j0) above the
@@ -336,22 +329,26 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
     }
   }
   if (t < kQrPanel * kQrPanel)
-    ((g_f32*)d.T)[int64_t(s16 + t / kQrPanel) * kQrBlock + s16 + t % kQrPanel] = Ts[t / kQrPanel][t % kQrPanel];
+    ((g_f32*)d.T)[int64_t(s16 + t / kQrPanel) * kQrBlock + s16 + t % kQrPanel] = Ds[t / kQrPanel][t % kQrPanel];
 }
 
-// x <- x - V_s (T_s^T (V_s^T x)) for one column x of A (a row of At, rows [c, d) of A): thread t
-// holds entries t + 256 i in registers, forms its part of the 16 sums V_s^T x (the panel's V rows are
-// 64 contiguous bytes), the workgroup reduces them in a fixed order (DPP reduce-scatter within each
-// row of 16 lanes, then over the wave's four rows, then over the four waves through LDS), 16
-// threads form y = T_s^T w (T_s upper triangular), and every thread subtracts V_s y from its
-// entries. The column is read once and written once.
+// x <- H_16 ... H_1 x = x - V_s y for one column x of A (a row of At, rows [c, d) of A), with
+// y_k = tau_k (w_k - sum_{j<k} (v_j . v_k) y_j) and w = V_s^T x (the reflectors applied one after the
+// other, in the reduced coordinates). Thread t holds entries t + 256 i in registers and forms its
+// part of the 16 sums w (the panel's V rows are 64 contiguous bytes); the workgroup reduces them in
+// a fixed order (DPP reduce-scatter within each row of 16 lanes, then over the wave's four rows, then
+// over the four waves through LDS), one thread runs the 16-step recurrence for y, and every thread
+// subtracts V_s y from its entries. The column is read once and written once.
 __global__ __launch_bounds__(kQrColThreads) void qr_col_kernel(const QrColDesc* __restrict__ descs, int count) {
   __shared__ float red[kQrColThreads / 64][kQrPanel];
   __shared__ float ws[kQrPanel];
   __shared__ float ys[kQrPanel];
+  __shared__ float Ts[kQrPanel][kQrPanel];
   const int e = find_desc(descs, count, blockIdx.x);
   const QrColDesc& d = descs[e];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  static_assert(kQrColThreads == kQrPanel * kQrPanel, "one thread per entry of the panel's block of T");
+  Ts[t / kQrPanel][t % kQrPanel] = ((const g_cf32*)(d.T))[(t / kQrPanel) * kQrBlock + t % kQrPanel];
   const int64_t col = int64_t(d.c) + kQrPanel + (blockIdx.x - d.tile_begin);
   g_f32* x = (g_f32*)(d.At) + col * d.ld + d.c;
   const g_cf32* V = (const g_cf32*)(d.V);
@@ -384,11 +381,16 @@ __global__ __launch_bounds__(kQrColThreads) void qr_col_kernel(const QrColDesc* 
   __syncthreads();
   if (t < kQrPanel) ws[t] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
   __syncthreads();
-  if (t < kQrPanel) {
-    const g_cf32* T = (const g_cf32*)(d.T);
-    float y = 0.0f;
-    for (int k = 0; k <= t; ++k) y += T[k * kQrBlock + t] * ws[k];
-    ys[t] = y;
+  if (t == 0) {
+    float yk[kQrPanel];
+#pragma unroll
+    for (int k = 0; k < kQrPanel; ++k) {
+      float acc = ws[k];
+#pragma unroll
+      for (int j = 0; j < k; ++j) acc -= Ts[j][k] * yk[j];
+      yk[k] = Ts[k][k] * acc;
+      ys[k] = yk[k];
+    }
   }
   __syncthreads();
   float y[kQrPanel];
@@ -413,19 +415,62 @@ __global__ __launch_bounds__(kQrColThreads) void qr_col_kernel(const QrColDesc* 
   }
 }
 
-// The block's compact-WY factor: T held in LDS; for each panel s = 1 .. 7 (first column n0 = 16 s),
-// M = G[0:n0, n0:n0+16] T_s (G summed over its partials in order), then
-// T[0:n0, n0:n0+16] = -T[0:n0, 0:n0] M over the upper triangle of T[0:n0, 0:n0].
+// The block's compact-WY factor, held in LDS. Each panel's diagonal block first, row by row (one
+// thread per row i; T_kk = tau_k, T_ik = -tau_k sum_{j=i}^{k-1} T_ij (v_j . v_k), from the tau and dot
+// products the panel left in its block); then, with the blocks of G above the diagonal blocks (G
+// summed over its partials in order), for each panel s = 1 .. 7 (first column n0 = 16 s),
+// M = G[0:n0, n0:n0+16] T_s and T[0:n0, n0:n0+16] = -T[0:n0, 0:n0] M over the upper triangle of
+// T[0:n0, 0:n0].
 __global__ __launch_bounds__(256) void qr_t_kernel(const QrTDesc* __restrict__ descs) {
   __shared__ float Tl[kQrBlock][kQrBlock + 1];
+  __shared__ float Gl[kQrBlock][kQrBlock + 1];
   __shared__ float M1[kQrBlock - kQrPanel][kQrPanel + 1];
+  __shared__ float Dl[kQrBlock][kQrPanel];  // row i: the panel's tau / dot-product row i
   const QrTDesc& d = descs[blockIdx.x];
   const int t = threadIdx.x;
   g_f32* T = (g_f32*)(d.T);
   const g_cf32* G = (const g_cf32*)(d.G);
-  for (int idx = t; idx < kQrBlock * kQrBlock; idx += 256) {
-    const int i = idx / kQrBlock, j = idx % kQrBlock;
-    Tl[i][j] = (i / kQrPanel == j / kQrPanel) ? T[idx] : 0.0f;
+  // thread t owns column j = t % 128 and rows i = t / 128 + 2 m (m < 64) of both matrices; the
+  // partials of G are summed with every load of one partial in flight together
+  constexpr int kM = kQrBlock * kQrBlock / 256;
+  const int tj = t % kQrBlock, ti = t / kQrBlock;
+  float g[kM];
+#pragma unroll
+  for (int m = 0; m < kM; ++m) g[m] = 0.0f;
+  for (int q = 0; q < d.nG; ++q) {
+    const g_cf32* Gq = G + int64_t(q) * kQrBlock * kQrBlock;
+#pragma unroll
+    for (int m = 0; m < kM; ++m) g[m] += Gq[(ti + 2 * m) * kQrBlock + tj];  // (every partial is whole)
+  }
+#pragma unroll
+  for (int m = 0; m < kM; ++m) {
+    const int i = ti + 2 * m;
+    Tl[i][tj] = 0.0f;
+    Gl[i][tj] = g[m];
+  }
+  for (int idx = t; idx < kQrBlock * kQrPanel; idx += 256) {
+    const int i = idx / kQrPanel, jj = idx % kQrPanel;
+    Dl[i][jj] = T[i * kQrBlock + (i / kQrPanel) * kQrPanel + jj];
+  }
+  __syncthreads();
+  if (t < kQrBlock) {
+    const int i = t, b0 = (i / kQrPanel) * kQrPanel, ii = i % kQrPanel;
+    float row[kQrPanel];
+#pragma unroll
+    for (int k = 0; k < kQrPanel; ++k) {
+      float v = 0.0f;
+      if (k == ii) {
+        v = Dl[i][ii];
+      } else if (k > ii) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < k; ++j)
+          if (j >= ii) acc += row[j] * Dl[b0 + j][k];
+        v = -Dl[b0 + k][k] * acc;
+      }
+      row[k] = v;
+      Tl[i][b0 + k] = v;
+    }
   }
   __syncthreads();
   for (int s = 1; s < kQrBlock / kQrPanel; ++s) {
@@ -433,18 +478,22 @@ __global__ __launch_bounds__(256) void qr_t_kernel(const QrTDesc* __restrict__ d
     for (int idx = t; idx < n0 * kQrPanel; idx += 256) {
       const int i = idx / kQrPanel, j = idx % kQrPanel;
       float acc = 0.0f;
-      for (int k = 0; k < kQrPanel; ++k) {
-        float g = 0.0f;
-        for (int q = 0; q < d.nG; ++q) g += G[int64_t(q) * kQrBlock * kQrBlock + i * kQrBlock + n0 + k];
-        acc += g * Tl[n0 + k][n0 + j];
-      }
+#pragma unroll
+      for (int k = 0; k < kQrPanel; ++k) acc += Gl[i][n0 + k] * Tl[n0 + k][n0 + j];
       M1[i][j] = acc;
     }
     __syncthreads();
+    // T[0:n0, 0:n0] is upper triangular with zeros below (whole 16-row groups summed; four
+    // accumulators per group, added in a fixed order)
     for (int idx = t; idx < n0 * kQrPanel; idx += 256) {
       const int i = idx / kQrPanel, j = idx % kQrPanel;
       float acc = 0.0f;
-      for (int k = i; k < n0; ++k) acc += Tl[i][k] * M1[k][j];
+      for (int k0 = (i / kQrPanel) * kQrPanel; k0 < n0; k0 += kQrPanel) {
+        float p[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int k = 0; k < kQrPanel; ++k) p[k & 3] += Tl[i][k0 + k] * M1[k0 + k][j];
+        acc += (p[0] + p[1]) + (p[2] + p[3]);
+      }
       Tl[i][n0 + j] = -acc;
     }
     __syncthreads();

@@ -82,6 +82,35 @@ void add_gemm(Build& b, std::vector<Prod> ps) {
   b.op(kOpGemm, gs, gt);
 }
 
+// The block update's two products for each side (X = the trailing columns of S as rows of St, and
+// X = Q's columns [j0, dp)): with wp, W = X V is appended to wp and wp is launched; with xp,
+// X <- X - W U^T is appended to xp and xp is launched.
+void add_wx(Build& b, const std::vector<QrSide*>& act, int64_t j0, std::vector<Prod>* wp, std::vector<Prod>* xp) {
+  for (QrSide* s : act) {
+    const int64_t vrows = s->dp - j0;
+    const float* Vt = b.ptr<float>(s->Vt);
+    const float* U = b.ptr<float>(s->U);
+    const int64_t trail = s->dp - j0 - kQrBlock;  // St rows [j0 + 128, dp)
+    struct Part {
+      float* X;
+      float* W;
+      int64_t rows;
+    };
+    std::vector<Part> parts;
+    if (trail > 0 && j0 + kQrBlock < s->d)
+      parts.push_back(Part{b.ptr<float>(s->St) + (j0 + kQrBlock) * s->dp + j0, b.ptr<float>(s->Ws), trail});
+    parts.push_back(Part{b.ptr<float>(s->Q) + j0, b.ptr<float>(s->Wq), s->dp});
+    for (const Part& p : parts) {
+      if (wp)
+        wp->push_back(Prod{p.X, Vt, nullptr, p.W, s->dp, s->dp, 0, kQrBlock, p.rows, kQrBlock, vrows, 0, 1.0f, 0.0f});
+      if (xp)
+        xp->push_back(Prod{p.W, U, p.X, p.X, kQrBlock, kQrBlock, s->dp, s->dp, p.rows, vrows, kQrBlock, 0, -1.0f, 1.0f});
+    }
+  }
+  if (wp) add_gemm(b, *wp);
+  if (xp) add_gemm(b, *xp);
+}
+
 // The Householder QR of each side's S (given as St): Q = H_1 H_2 ... H_d into each side's Q buffer
 // (set to the identity first). Sides are listed largest first in every grouped launch.
 void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
@@ -145,7 +174,7 @@ void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
       b.op(kOpQrPanel, pd, int(pd.size()));
       if (!cd.empty()) b.op(kOpQrCol, cd, ct);
     }
-    // G = V^T V in K chunks, then the block's T
+    // G = V^T V in K chunks together with W = X V (both read only V), then the block's T
     {
       std::vector<Prod> gp;
       std::vector<QrTDesc> td;
@@ -160,34 +189,18 @@ void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
         }
         td.push_back(QrTDesc{b.ptr<float>(s->T), b.ptr<float>(s->G), ng});
       }
-      add_gemm(b, gp);
+      add_wx(b, act, j0, &gp, nullptr);
       b.op(kOpQrT, td, int(td.size()));
     }
-    // U = V T^T; W = X V; X <- X - W U^T for the trailing columns of S and for Q's columns [j0, dp)
+    // U = V T^T, then X <- X - W U^T
     {
-      std::vector<Prod> up, wp, xp;
-      for (QrSide* s : act) {
-        const int64_t vrows = s->dp - j0;
-        float* V = b.ptr<float>(s->V);
-        float* Vt = b.ptr<float>(s->Vt);
-        float* U = b.ptr<float>(s->U);
-        up.push_back(Prod{V, b.ptr<float>(s->T), nullptr, U, kQrBlock, kQrBlock, 0, kQrBlock, vrows, kQrBlock,
-                          kQrBlock, 0, 1.0f, 0.0f});
-        const int64_t trail = s->dp - j0 - kQrBlock;  // St rows [j0 + 128, dp)
-        if (trail > 0 && j0 + kQrBlock < s->d) {
-          float* X = b.ptr<float>(s->St) + (j0 + kQrBlock) * s->dp + j0;
-          float* W = b.ptr<float>(s->Ws);
-          wp.push_back(Prod{X, Vt, nullptr, W, s->dp, s->dp, 0, kQrBlock, trail, kQrBlock, vrows, 0, 1.0f, 0.0f});
-          xp.push_back(Prod{W, U, X, X, kQrBlock, kQrBlock, s->dp, s->dp, trail, vrows, kQrBlock, 0, -1.0f, 1.0f});
-        }
-        float* X = b.ptr<float>(s->Q) + j0;
-        float* W = b.ptr<float>(s->Wq);
-        wp.push_back(Prod{X, Vt, nullptr, W, s->dp, s->dp, 0, kQrBlock, s->dp, kQrBlock, vrows, 0, 1.0f, 0.0f});
-        xp.push_back(Prod{W, U, X, X, kQrBlock, kQrBlock, s->dp, s->dp, s->dp, vrows, kQrBlock, 0, -1.0f, 1.0f});
-      }
+      std::vector<Prod> up;
+      for (QrSide* s : act)
+        up.push_back(Prod{b.ptr<float>(s->V), b.ptr<float>(s->T), nullptr, b.ptr<float>(s->U), kQrBlock, kQrBlock, 0,
+                          kQrBlock, s->dp - j0, kQrBlock, kQrBlock, 0, 1.0f, 0.0f});
       add_gemm(b, up);
-      add_gemm(b, wp);
-      add_gemm(b, xp);
+      std::vector<Prod> xp;
+      add_wx(b, act, j0, nullptr, &xp);
     }
   }
 }

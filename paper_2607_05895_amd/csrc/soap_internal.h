@@ -22,7 +22,7 @@ constexpr int kQrRowsPerThread = 8;   // panel rows held in registers per thread
 constexpr int kQrMaxDim = kQrPanelThreads * kQrRowsPerThread;  // 4096
 constexpr int kQrColThreads = 256;    // in-block application: one workgroup per column
 constexpr int kQrColRows = kQrMaxDim / kQrColThreads;          // column entries per thread
-constexpr int kQrGramChunk = 512;     // K chunk of the split V^T V product
+constexpr int kQrGramChunk = 256;     // K chunk of the split V^T V product
 static_assert(kQrBlock == kShTile, "the block update runs on the Shampoo GEMM's tiles");
 
 // M <- beta1 M + (1 - beta1) G over the real m x n block, and the padded layouts the products read
