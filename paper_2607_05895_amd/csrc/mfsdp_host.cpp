@@ -879,4 +879,41 @@ int staging_acquire(size_t bytes, void** host) { return ring().acquire(bytes, ho
 int staging_upload(int slot, void* dst, size_t bytes, hipStream_t st) {
   return ring().upload(slot, dst, bytes, st);
 }
+
+// One auxiliary stream per device (default priority, non-blocking) and a ring of events for the
+// fork / join dependencies between it and the caller's stream, created on first use and kept until
+// the process ends. An event may be recorded again while an earlier wait on it is still pending: a
+// wait takes the record that precedes it on the host.
+namespace {
+struct AuxState {
+  hipStream_t stream = nullptr;
+  hipEvent_t events[8] = {};
+  unsigned next = 0;
+};
+std::mutex g_aux_mu;
+std::vector<AuxState> g_aux;
+}  // namespace
+
+int aux_stream(hipStream_t* out, hipEvent_t* ev) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_aux_mu);
+  if (dev >= int(g_aux.size())) g_aux.resize(size_t(dev) + 1);
+  AuxState& a = g_aux[size_t(dev)];
+  if (!a.stream) {
+    e = hipStreamCreateWithFlags(&a.stream, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      a.stream = nullptr;
+      return hip_fail(e, "hipStreamCreateWithFlags");
+    }
+    for (hipEvent_t& x : a.events) {
+      e = hipEventCreateWithFlags(&x, hipEventDisableTiming);
+      if (e != hipSuccess) return hip_fail(e, "hipEventCreateWithFlags");
+    }
+  }
+  *out = a.stream;
+  if (ev) *ev = a.events[a.next++ % 8];
+  return MFSDP_OK;
+}
 }  // namespace mfsdp

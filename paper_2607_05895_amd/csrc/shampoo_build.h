@@ -20,6 +20,8 @@ namespace mfsdp {
 int set_last_error(int status, const std::string& msg);
 int staging_acquire(size_t bytes, void** host);
 int staging_upload(int slot, void* dst, size_t bytes, hipStream_t st);
+// The device's auxiliary stream and (if ev is set) the next event of its ring.
+int aux_stream(hipStream_t* out, hipEvent_t* ev);
 
 namespace shb {
 
@@ -45,13 +47,16 @@ struct Arena {
 
 enum OpKind {
   kOpCopyIn, kOpCopyOut, kOpGemm, kOpNorm, kOpScalars, kOpInit, kOpApply,
-  kOpSoapPrep, kOpSoapAdam, kOpEye, kOpQrPanel, kOpQrCol, kOpQrT
+  kOpSoapPrep, kOpSoapAdam, kOpEye, kOpQrPanel, kOpQrCol, kOpQrT,
+  kOpFork,  // the auxiliary stream waits for everything enqueued so far on the caller's stream
+  kOpJoin   // the caller's stream waits for everything enqueued so far on the auxiliary stream
 };
 struct Op {
   OpKind kind;
   size_t desc_off;
   int count;
   int total;  // grid blocks
+  int aux;    // 1: launched on the auxiliary stream
 };
 
 // Per-call scalars the kernels take by value.
@@ -77,11 +82,14 @@ struct Build {
     std::memcpy(h.data() + o, v.data(), v.size() * sizeof(T));
     return o;
   }
+  int aux = 0;  // stream of the ops added next
   template <class T>
   void op(OpKind k, const std::vector<T>& v, int total) {
     if (v.empty() || total <= 0) return;
-    ops.push_back(Op{k, put(v), int(v.size()), total});
+    ops.push_back(Op{k, put(v), int(v.size()), total, aux});
   }
+  void fork() { ops.push_back(Op{kOpFork, 0, 0, 0, 0}); }
+  void join() { ops.push_back(Op{kOpJoin, 0, 0, 0, 0}); }
 };
 
 inline ShCopyDesc copy_desc(const void* src, int dt, void* dst, float* dstT, int64_t rows, int64_t cols,
@@ -129,7 +137,8 @@ inline ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, floa
   return g;
 }
 
-inline int run(Build& b, char* ws, size_t desc_at, hipStream_t st, const RunScalars& s) {
+inline int run(Build& b, char* ws, size_t desc_at, hipStream_t main_st, const RunScalars& s) {
+  hipStream_t st = main_st;
   if (!b.h.empty()) {
     void* host = nullptr;
     const int slot = staging_acquire(b.h.size(), &host);
@@ -138,9 +147,23 @@ inline int run(Build& b, char* ws, size_t desc_at, hipStream_t st, const RunScal
     const int rc = staging_upload(slot, ws + desc_at, b.h.size(), st);
     if (rc != MFSDP_OK) return rc;
   }
+  hipStream_t aux = nullptr;
+  bool forked = false;
   for (const Op& o : b.ops) {
+    if (o.kind == kOpFork || o.kind == kOpJoin) {
+      hipEvent_t ev = nullptr;
+      const int rc = aux_stream(&aux, &ev);
+      if (rc != MFSDP_OK) return rc;
+      hipError_t e = hipEventRecord(ev, o.kind == kOpFork ? main_st : aux);
+      if (e == hipSuccess) e = hipStreamWaitEvent(o.kind == kOpFork ? aux : main_st, ev, 0);
+      if (e != hipSuccess) return hip_err(e, "stream fork / join");
+      forked = o.kind == kOpFork;
+      continue;
+    }
     char* dp = ws + desc_at + o.desc_off;
     hipError_t e = hipSuccess;
+    if (o.aux && !forked) return set_last_error(MFSDP_E_INVALID, "internal: auxiliary-stream op outside a fork");
+    st = o.aux ? aux : main_st;
     switch (o.kind) {
       case kOpCopyIn: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 0, st); break;
       case kOpCopyOut: e = launch_sh_copy(reinterpret_cast<ShCopyDesc*>(dp), o.count, o.total, 1, st); break;
@@ -164,9 +187,13 @@ inline int run(Build& b, char* ws, size_t desc_at, hipStream_t st, const RunScal
       case kOpQrPanel: e = launch_qr_panel(reinterpret_cast<QrPanelDesc*>(dp), o.count, st); break;
       case kOpQrCol: e = launch_qr_col(reinterpret_cast<QrColDesc*>(dp), o.count, o.total, st); break;
       case kOpQrT: e = launch_qr_t(reinterpret_cast<QrTDesc*>(dp), o.count, st); break;
+      case kOpFork:
+      case kOpJoin:
+        break;
     }
     if (e != hipSuccess) return hip_err(e, "kernel launch");
   }
+  if (forked) return set_last_error(MFSDP_E_INVALID, "internal: auxiliary stream not joined");
   return MFSDP_OK;
 }
 

@@ -19,11 +19,12 @@
 // The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
 // with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
 // block, with S held transposed (each column of S one contiguous row) and Q accumulated from the
-// identity as Q <- Q H_B per 128-column block B. Per block: eight 16-column panel launches (V, T
-// of the panel), each but the last followed by a launch that applies the panel's reflectors to the
-// block's later columns (one workgroup per column); then on the Shampoo GEMM G = V^T V (K-split),
-// the block's T (one workgroup), U = V T^T, W = X V and X <- X - W U^T for X = the trailing
-// columns of S (as rows of S^T) and X = Q's columns [j0, dp).
+// identity as Q <- Q H_B per 128-column block B. Per block: eight 16-column panel launches (the
+// panel's reflectors), each but the last followed by a launch that applies them to the block's
+// later columns (one workgroup per column); then on the Shampoo GEMM G = V^T V (K-split) with
+// W = X V, the block's T (one workgroup), U = V T^T and X <- X - W U^T for X = the trailing columns
+// of S (as rows of S^T) and X = Q's columns [j0, dp). The part of that update beyond the next
+// block's columns runs on an auxiliary stream, overlapping the next block's panels (look-ahead).
 // Zero padding is exact: padded rows and columns of G, M, the bases and the statistics are zero, so
 // every product's real block is unaffected and its padded part is zero.
 #include <hip/hip_runtime.h>
@@ -82,33 +83,39 @@ void add_gemm(Build& b, std::vector<Prod> ps) {
   b.op(kOpGemm, gs, gt);
 }
 
-// The block update's two products for each side (X = the trailing columns of S as rows of St, and
-// X = Q's columns [j0, dp)): with wp, W = X V is appended to wp and wp is launched; with xp,
-// X <- X - W U^T is appended to xp and xp is launched.
-void add_wx(Build& b, const std::vector<QrSide*>& act, int64_t j0, std::vector<Prod>* wp, std::vector<Prod>* xp) {
+// The block update's products for each side, over X = the trailing columns of S (rows [j0 + 128,
+// dp) of St) and X = Q's columns [j0, dp): kW appends W = X V (whole X) to ps; kXNext appends
+// X <- X - W U^T for St's next 128 rows (the next block's columns); kXRest appends it for the
+// remaining St rows and for Q.
+enum WxPart { kW, kXNext, kXRest };
+void add_wx(Build& b, const std::vector<QrSide*>& act, int64_t j0, WxPart part, std::vector<Prod>& ps) {
   for (QrSide* s : act) {
     const int64_t vrows = s->dp - j0;
     const float* Vt = b.ptr<float>(s->Vt);
     const float* U = b.ptr<float>(s->U);
     const int64_t trail = s->dp - j0 - kQrBlock;  // St rows [j0 + 128, dp)
-    struct Part {
-      float* X;
-      float* W;
-      int64_t rows;
+    const bool has_trail = trail > 0 && j0 + kQrBlock < s->d;
+    float* XS = b.ptr<float>(s->St) + (j0 + kQrBlock) * s->dp + j0;
+    float* WS = b.ptr<float>(s->Ws);
+    float* XQ = b.ptr<float>(s->Q) + j0;
+    float* WQ = b.ptr<float>(s->Wq);
+    auto w = [&](float* X, float* W, int64_t rows) {
+      ps.push_back(Prod{X, Vt, nullptr, W, s->dp, s->dp, 0, kQrBlock, rows, kQrBlock, vrows, 0, 1.0f, 0.0f});
     };
-    std::vector<Part> parts;
-    if (trail > 0 && j0 + kQrBlock < s->d)
-      parts.push_back(Part{b.ptr<float>(s->St) + (j0 + kQrBlock) * s->dp + j0, b.ptr<float>(s->Ws), trail});
-    parts.push_back(Part{b.ptr<float>(s->Q) + j0, b.ptr<float>(s->Wq), s->dp});
-    for (const Part& p : parts) {
-      if (wp)
-        wp->push_back(Prod{p.X, Vt, nullptr, p.W, s->dp, s->dp, 0, kQrBlock, p.rows, kQrBlock, vrows, 0, 1.0f, 0.0f});
-      if (xp)
-        xp->push_back(Prod{p.W, U, p.X, p.X, kQrBlock, kQrBlock, s->dp, s->dp, p.rows, vrows, kQrBlock, 0, -1.0f, 1.0f});
+    auto x = [&](float* X, const float* W, int64_t rows) {
+      ps.push_back(Prod{W, U, X, X, kQrBlock, kQrBlock, s->dp, s->dp, rows, vrows, kQrBlock, 0, -1.0f, 1.0f});
+    };
+    if (part == kW) {
+      if (has_trail) w(XS, WS, trail);
+      w(XQ, WQ, s->dp);
+    } else if (part == kXNext) {
+      if (has_trail) x(XS, WS, kQrBlock);
+    } else {
+      if (has_trail && trail > kQrBlock)
+        x(XS + kQrBlock * s->dp, WS + kQrBlock * kQrBlock, trail - kQrBlock);
+      x(XQ, WQ, s->dp);
     }
   }
-  if (wp) add_gemm(b, *wp);
-  if (xp) add_gemm(b, *xp);
 }
 
 // The Householder QR of each side's S (given as St): Q = H_1 H_2 ... H_d into each side's Q buffer
@@ -174,6 +181,9 @@ void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
       b.op(kOpQrPanel, pd, int(pd.size()));
       if (!cd.empty()) b.op(kOpQrCol, cd, ct);
     }
+    // (the previous block's update of the trailing columns beyond this block and of Q, on the
+    // auxiliary stream, overlapped the panels above; it must end before W reads them)
+    if (j0 > 0) b.join();
     // G = V^T V in K chunks together with W = X V (both read only V), then the block's T
     {
       std::vector<Prod> gp;
@@ -189,20 +199,29 @@ void add_qr_ops(Build& b, std::vector<QrSide*> sides) {
         }
         td.push_back(QrTDesc{b.ptr<float>(s->T), b.ptr<float>(s->G), ng});
       }
-      add_wx(b, act, j0, &gp, nullptr);
+      add_wx(b, act, j0, kW, gp);
+      add_gemm(b, gp);
       b.op(kOpQrT, td, int(td.size()));
     }
-    // U = V T^T, then X <- X - W U^T
+    // U = V T^T; X <- X - W U^T for the next block's columns first, then (on the auxiliary stream,
+    // while the next block's panels run) for the rest of the trailing columns and for Q
     {
       std::vector<Prod> up;
       for (QrSide* s : act)
         up.push_back(Prod{b.ptr<float>(s->V), b.ptr<float>(s->T), nullptr, b.ptr<float>(s->U), kQrBlock, kQrBlock, 0,
                           kQrBlock, s->dp - j0, kQrBlock, kQrBlock, 0, 1.0f, 0.0f});
       add_gemm(b, up);
-      std::vector<Prod> xp;
-      add_wx(b, act, j0, nullptr, &xp);
+      std::vector<Prod> xn, xr;
+      add_wx(b, act, j0, kXNext, xn);
+      add_gemm(b, xn);
+      add_wx(b, act, j0, kXRest, xr);
+      b.fork();
+      b.aux = 1;
+      add_gemm(b, xr);
+      b.aux = 0;
     }
   }
+  b.join();
 }
 
 // Per matrix: left / right tell whether that side has a basis (its length is at most
