@@ -10,13 +10,16 @@
 
 namespace mfsdp {
 
-// One output tile of a grouped NS product: problem (matrix) index and 256 x 256 block coordinates;
-// e < 0 marks an idle slot. The bf16 NS kernels run a persistent grid of kGemmXcds x
-// kGemmSlots workgroups; workgroup b serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes
-// tile sched[g * kGemmSlots + slot] of every group g = xcd, xcd + kGemmXcds, ...
+// One output tile of a grouped NS product: problem (matrix) index, 256 x 256 block coordinates and,
+// for a problem whose contraction is split, the K range ks of the tile; e < 0 marks an idle slot.
+// The bf16 NS kernels run a persistent grid of kGemmXcds x kGemmSlots workgroups; workgroup b
+// serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes tile sched[g * kGemmSlots + slot] of
+// every group g = xcd, xcd + kGemmXcds, ...
 struct TileRef {
   int32_t e;
   int16_t bi, bj;
+  int16_t ks;
+  int16_t unused;
 };
 constexpr int kGemmXcds = 8;    // MI355X: 8 XCDs (workgroups are dealt to them round robin)
 constexpr int kGemmSlots = 32;  // CUs per XCD = tiles per group
@@ -35,8 +38,12 @@ struct TileGrid {
 // the XCDs longest first, each to the XCD with the least work so far (a group's cost is the
 // largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
 // g % kGemmXcds; XCDs with fewer groups get empty ones (every slot e = -1).
+// splits (optional, per problem): the number of K ranges each tile of the problem is cut into; the
+// ranges of one tile are listed together and each costs cost / splits.
 inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
-                                           const std::vector<int64_t>& cost) {
+                                           const std::vector<int64_t>& cost,
+                                           const std::vector<int>* splits = nullptr) {
+  auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
   std::vector<TileRef> flat;
   for (int e : order) {
     const TileGrid& g = grids[e];
@@ -44,16 +51,17 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
       const int r1 = std::min(g.tm, r0 + kGroupRows);
       for (int c = g.sym ? r0 : 0; c < g.tn; ++c)
         for (int r = r0; r < r1; ++r)
-          if (!g.sym || r <= c) flat.push_back(TileRef{e, int16_t(r), int16_t(c)});
+          if (!g.sym || r <= c)
+            for (int ks = 0; ks < nks(e); ++ks) flat.push_back(TileRef{e, int16_t(r), int16_t(c), int16_t(ks), 0});
     }
   }
-  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0});
+  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0, 0, 0});
   const size_t ng = flat.size() / kGemmSlots;
   std::vector<int64_t> gcost(ng, 0);
   for (size_t g = 0; g < ng; ++g)
     for (int s = 0; s < kGemmSlots; ++s) {
       const TileRef& t = flat[g * kGemmSlots + s];
-      if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e]);
+      if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e] / nks(t.e));
     }
   std::vector<size_t> by(ng);
   for (size_t g = 0; g < ng; ++g) by[g] = g;
@@ -69,12 +77,44 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
   }
   size_t rounds = 0;
   for (const auto& l : lists) rounds = std::max(rounds, l.size());
-  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0});
+  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0, 0, 0});
   for (int x = 0; x < kGemmXcds; ++x)
     for (size_t i = 0; i < lists[x].size(); ++i)
       std::memcpy(&s[(i * kGemmXcds + x) * kGemmSlots], &flat[lists[x][i] * kGemmSlots],
                   kGemmSlots * sizeof(TileRef));
   return s;
+}
+
+// K splits of a Gram product launch (upper tiles tiles[e] of contraction length K[e] per problem)
+// with fewer tiles than the persistent grid has workgroups. A tile's time is set by its K, so a
+// few long-K tiles (say those of a 768 x 3072 matrix among 768 x 768 ones) would alone set the
+// launch's length while most of the chip waits. Each problem gets the largest f <= kSplitMax that
+// divides K / 32 and keeps K / f at least at a target: first the larger of kSplitMinK and the
+// launch's work per workgroup, then the longest K range any problem is left with (so that no tile
+// is cut shorter than the launch needs). f = 1 everywhere when the launch fills the grid.
+constexpr int64_t kSplitMinK = 512;
+constexpr int kSplitMax = 8;
+inline std::vector<int> gram_splits(const std::vector<int64_t>& tiles, const std::vector<int64_t>& K) {
+  const size_t n = tiles.size();
+  std::vector<int> f(n, 1);
+  const int64_t slots = int64_t(kGemmXcds) * kGemmSlots;
+  int64_t T = 0, W = 0;
+  for (size_t e = 0; e < n; ++e) {
+    T += tiles[e];
+    W += tiles[e] * K[e];
+  }
+  if (n == 0 || T >= slots) return f;
+  auto fit = [](int64_t k, int64_t target) {
+    int best = 1;
+    for (int c = 2; c <= kSplitMax; ++c)
+      if ((k / 32) % c == 0 && k / c >= target) best = c;
+    return best;
+  };
+  const int64_t kt = std::max(kSplitMinK, W / slots);
+  int64_t kcrit = 0;
+  for (size_t e = 0; e < n; ++e) kcrit = std::max(kcrit, K[e] / fit(K[e], kt));
+  for (size_t e = 0; e < n; ++e) f[e] = fit(K[e], kcrit);
+  return f;
 }
 
 }  // namespace mfsdp

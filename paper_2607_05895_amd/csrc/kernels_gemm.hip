@@ -179,7 +179,7 @@ struct WaveGrid {
 // Per-tile state of the persistent kernel: operand sources of the DMA and the tile coordinates.
 struct TileCtx {
   const GemmDesc* d;
-  int bi, bj, nk;
+  int bi, bj, nk, ks;
   const uint16_t* psrc;
   const uint16_t* qsrc;
   int64_t pstep, qstep;
@@ -226,11 +226,16 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       c.d = &dd;
       c.bi = r.bi;
       c.bj = r.bj;
-      c.nk = dd.K / BKE;
+      c.ks = r.ks;
+      // a split Gram tile covers K range ks of nks (each range a whole number of 16 x 32 blocks:
+      // it starts nk * ks blocks further along every panel)
+      const int nks = (PK == kProdGram && dd.nks > 1) ? dd.nks : 1;
+      c.nk = dd.K / BKE / nks;
+      const int64_t k0 = int64_t(c.nk) * (nks > 1 ? r.ks : 0) * (kBlkRows * BKE);
       const uint16_t* P = static_cast<const uint16_t*>(dd.P[parity]);
       const uint16_t* Q = static_cast<const uint16_t*>(dd.Q[parity]);
-      c.psrc = P + blk_index(int64_t(c.bi) * BT + drow, dchunk * 8, dd.ldp);
-      c.qsrc = Q + blk_index(int64_t(c.bj) * BT + drow, dchunk * 8, dd.ldq);
+      c.psrc = P + blk_index(int64_t(c.bi) * BT + drow, dchunk * 8, dd.ldp) + k0;
+      c.qsrc = Q + blk_index(int64_t(c.bj) * BT + drow, dchunk * 8, dd.ldq) + k0;
       c.pstep = int64_t(NW * kBlkRows) * dd.ldp;  // NW row panels further down
       c.qstep = int64_t(NW * kBlkRows) * dd.ldq;
       return true;
@@ -361,6 +366,32 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
     // store).
     const GemmDesc& dd = *cur.d;
     const int bi = cur.bi, bj = cur.bj;
+    if constexpr (PK == kProdGram) {
+      if (dd.nks > 1) {
+        // split contraction: this K range's fp32 partial tile, row-major, 16-byte stores straight
+        // from the accumulators (each lane: 4 consecutive columns of one row per group); the
+        // second pass forms A
+        typedef float f32x4s __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(1))) f32x4s gf4s;
+        float* part = dd.part + (int64_t(upper_index(bi, bj, dd.tiles_m)) * dd.nks + cur.ks) * (BT * BT);
+        static_for<MI>([&](auto mi_c) {
+          constexpr int mi = decltype(mi_c)::value;
+          const int il = wm * (MI * 32) + mi * 32 + frow;
+          static_for<NI>([&](auto ni_c) {
+            constexpr int ni = decltype(ni_c)::value;
+            static_for<4>([&](auto gg_c) {
+              constexpr int gg = decltype(gg_c)::value;
+              const int jl = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+              *(gf4s*)(part + il * BT + jl) = f32x4s{acc[mi][ni][4 * gg], acc[mi][ni][4 * gg + 1],
+                                                     acc[mi][ni][4 * gg + 2], acc[mi][ni][4 * gg + 3]};
+            });
+          });
+        });
+        if (!has_next) break;
+        cur = nxt;
+        continue;
+      }
+    }
     const float alpha = PK == kProdSquare ? cc : dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
     const float beta = PK == kProdSquare ? cb : dd.beta * (first ? scale_pow(dd.scale, dd.beta_scale_pow) : 1.0f);
     const float diag = (PK == kProdSquare && bi == bj) ? ca : 0.0f;
@@ -717,6 +748,50 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
 #undef MFSDP_WAIT_VMCNT
 #undef MFSDP_WAIT_LGKM0
 
+// Second pass of a split Gram product: one 256-thread workgroup per (job, 32-row slab of the tile).
+// Thread t adds the nks partials of 4 consecutive columns 4 (t % 64) of rows t / 64 + 4 i in range
+// order, scales as the Gram epilogue does and stores 8 bytes of bf16 into the tile; an off-diagonal
+// tile's slab also goes through LDS to its mirror, where it is one 64-byte row piece per tile column.
+constexpr int kSumSlab = 32;
+__global__ __launch_bounds__(256) void gram_sum_kernel(const GemmDesc* __restrict__ descs,
+                                                       const TileRef* __restrict__ jobs, int parity,
+                                                       int first) {
+  typedef float f32x4s __attribute__((ext_vector_type(4)));
+  typedef __attribute__((address_space(1))) const f32x4s gcf4s;
+  __shared__ float tt[kSumSlab][BT + 1];
+  const TileRef job = jobs[blockIdx.x / (BT / kSumSlab)];
+  const int slab = blockIdx.x % (BT / kSumSlab);
+  const GemmDesc& dd = descs[job.e];
+  const int bi = job.bi, bj = job.bj, nks = dd.nks;
+  const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
+  const float* part = dd.part + int64_t(upper_index(bi, bj, dd.tiles_m)) * nks * (BT * BT);
+  gu16* C = (gu16*)dd.C[parity];
+  const int64_t ldc = dd.ldc;
+  const int t = threadIdx.x, c4 = (t & 63) * 4;
+#pragma unroll
+  for (int i = 0; i < kSumSlab / 4; ++i) {
+    const int rl = (t >> 6) + 4 * i, r = slab * kSumSlab + rl;
+    f32x4s a = *(gcf4s*)(part + r * BT + c4);
+    for (int ks = 1; ks < nks; ++ks) a += *(gcf4s*)(part + int64_t(ks) * (BT * BT) + r * BT + c4);
+    a *= alpha;
+    *(gu2*)(C + blk_index(int64_t(bi) * BT + r, int64_t(bj) * BT + c4, ldc)) =
+        u32x2{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3])};
+    tt[rl][c4] = a[0];
+    tt[rl][c4 + 1] = a[1];
+    tt[rl][c4 + 2] = a[2];
+    tt[rl][c4 + 3] = a[3];
+  }
+  if (bi == bj) return;  // (uniform) the diagonal tile is whole
+  __syncthreads();
+  // mirror row bj * 256 + t, columns bi * 256 + 32 slab .. + 31: one 16 x 32 block row piece
+  uint32_t w[kSumSlab / 2];
+#pragma unroll
+  for (int k = 0; k < kSumSlab / 2; ++k) w[k] = pack_bf16x2(tt[2 * k][t], tt[2 * k + 1][t]);
+  gu4* dst = (gu4*)(C + blk_index(int64_t(bj) * BT + t, int64_t(bi) * BT + slab * kSumSlab, ldc));
+#pragma unroll
+  for (int k = 0; k < kSumSlab / 8; ++k) dst[k] = u32x4{w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]};
+}
+
 // fp32 NS products on fp32 MFMA. One 64 x 64 output tile per 256-thread workgroup: 4 waves of
 // 32 x 32 (v_mfma_f32_32x32x2f32), K steps of 32 double-buffered in LDS with the next step's 16-byte
 // global loads held in registers. The K index inside a step is permuted identically on both
@@ -851,6 +926,14 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, cons
   } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
                        parity, first_step, last_step, ca, cb, cc);
+  return hipGetLastError();
+}
+
+hipError_t launch_gram_sum(const GemmDesc* d_descs, const TileRef* d_jobs, int njobs, int parity,
+                           int first, hipStream_t st) {
+  if (njobs <= 0) return hipSuccess;
+  hipLaunchKernelGGL(gram_sum_kernel, dim3(njobs * (BT / kSumSlab)), dim3(256), 0, st, d_descs, d_jobs,
+                     parity, first);
   return hipGetLastError();
 }
 

@@ -100,12 +100,13 @@ NsPlan plan_ns(int64_t m, int64_t n, int ns_dtype, size_t base) {
 
 // Descriptor region at the start of the workspace.
 struct DescLayout {
-  size_t off_prep, off_norm, off_gemm[3], off_apply, off_sched[3], bytes;
+  size_t off_prep, off_norm, off_gemm[3], off_apply, off_sched[3], off_jobs, bytes;
   int ngroups[3];
+  int njobs;  // tiles of the split Gram problems (second pass)
 };
 
 
-DescLayout plan_descs(int64_t count, const size_t sched_bytes[3]) {
+DescLayout plan_descs(int64_t count, const size_t sched_bytes[3], int njobs) {
   DescLayout d{};
   size_t o = 0;
   d.off_prep = o; o += align_up(sizeof(PrepDesc) * count);
@@ -113,6 +114,8 @@ DescLayout plan_descs(int64_t count, const size_t sched_bytes[3]) {
   for (int k = 0; k < 3; ++k) { d.off_gemm[k] = o; o += align_up(sizeof(GemmDesc) * count); }
   d.off_apply = o; o += align_up(sizeof(ApplyDesc) * count);
   for (int k = 0; k < 3; ++k) { d.off_sched[k] = o; o += align_up(sched_bytes[k]); }
+  d.off_jobs = o; o += align_up(sizeof(TileRef) * size_t(njobs));
+  d.njobs = njobs;
   d.bytes = o;
   return d;
 }
@@ -264,10 +267,15 @@ struct Plan {
   std::vector<int> order[3];
   std::vector<TileRef> sched[3];
   int tiles[3] = {0, 0, 0};
+  std::vector<int> split;      // per Gram problem (launch order): K ranges per tile
+  std::vector<size_t> part;    // per Gram problem: offset of its partial tiles (split ones)
+  std::vector<TileRef> jobs;   // the split problems' upper tiles (second pass)
   DescLayout dl{};
   size_t bytes = 0;
 };
 
+// On the bf16 path a Gram launch with fewer tiles than the persistent grid has workgroups may split
+// long contractions (gram_splits); the split problems' partial tiles follow the per-matrix buffers.
 template <typename ShapeAt>
 Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   Plan P;
@@ -293,15 +301,37 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
       cost.push_back(ph == 0 ? p.s_pad : p.r_pad);
       P.tiles[ph] += g.sym ? g.tm * (g.tm + 1) / 2 : g.tm * g.tn;
     }
-    if (ns_dtype == MFSDP_BF16) P.sched[ph] = build_schedule(pos, grids, cost);
+    if (ph == 0) {
+      P.split.assign(size_t(count), 1);
+      if (ns_dtype == MFSDP_BF16) {
+        std::vector<int64_t> tl, kl;
+        for (const TileGrid& g : grids) tl.push_back(int64_t(g.tm) * (g.tm + 1) / 2);
+        for (int64_t c : cost) kl.push_back(c);
+        P.split = gram_splits(tl, kl);
+      }
+      for (int k = 0; k < int(count); ++k)
+        if (P.split[size_t(k)] > 1)
+          for (int bi = 0; bi < grids[size_t(k)].tm; ++bi)
+            for (int bj = bi; bj < grids[size_t(k)].tm; ++bj)
+              P.jobs.push_back(TileRef{k, int16_t(bi), int16_t(bj), 0, 0});
+    }
+    if (ns_dtype == MFSDP_BF16) P.sched[ph] = build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr);
     sched_bytes[ph] = P.sched[ph].size() * sizeof(TileRef);
   }
-  P.dl = plan_descs(count, sched_bytes);
+  P.dl = plan_descs(count, sched_bytes, int(P.jobs.size()));
   for (int ph = 0; ph < 3; ++ph) P.dl.ngroups[ph] = int(P.sched[ph].size() / kGemmSlots);
   size_t o = P.dl.bytes;
   for (int64_t i = 0; i < count; ++i) {
     P.ns.push_back(plan_ns(shapes[i].m, shapes[i].n, ns_dtype, o));
     o += P.ns.back().bytes;
+  }
+  P.part.assign(size_t(count), 0);
+  for (int k = 0; k < int(count); ++k) {
+    const int f = P.split[size_t(k)];
+    if (f <= 1) continue;
+    const int64_t tr = shapes[size_t(P.order[0][size_t(k)])].r_pad / kTileBF16;
+    P.part[size_t(k)] = o;
+    o += align_up(size_t(tr * (tr + 1) / 2) * size_t(f) * kTileBF16 * kTileBF16 * sizeof(float));
   }
   P.bytes = o;
   return P;
@@ -358,6 +388,8 @@ void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, u
         d.sym = 1; d.tiles_m = d.tiles_n = tr;
         d.tile_count = tr * (tr + 1) / 2;
         d.last_c = 1; d.last_ct = 0;
+        d.nks = P.split[size_t(k)];
+        d.part = d.nks > 1 ? reinterpret_cast<float*>(ws + P.part[size_t(k)]) : nullptr;
       } else if (phase == 1) {
         d.ldp = d.ldq = d.lde = d.ldc = p.r_pad; d.ldct = 0;
         d.M = d.N = d.K = int(p.r_pad);
@@ -386,6 +418,7 @@ void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, u
       std::memcpy(h + P.dl.off_sched[phase], P.sched[phase].data(),
                   P.sched[phase].size() * sizeof(TileRef));
   }
+  if (!P.jobs.empty()) std::memcpy(h + P.dl.off_jobs, P.jobs.data(), P.jobs.size() * sizeof(TileRef));
 }
 
 PrepDesc make_prep(const NsPlan& p, uint8_t* ws, const void* grad, int grad_dtype, float* momentum,
@@ -470,6 +503,12 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const doub
                       ns_dtype, kind, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0,
                       float(coeffs[3 * k]), float(coeffs[3 * k + 1]), float(coeffs[3 * k + 2]), st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
+      if (ph == 0 && dl.njobs > 0) {
+        e = launch_gram_sum(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[0]),
+                            reinterpret_cast<const TileRef*>(ws + dl.off_jobs), dl.njobs, k & 1,
+                            k == 0 ? 1 : 0, st);
+        if (e != hipSuccess) return hip_fail(e, "split Gram sum launch");
+      }
     }
   }
   if ((rc = record(events, 2, st))) return rc;

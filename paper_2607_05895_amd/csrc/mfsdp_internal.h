@@ -116,7 +116,16 @@ struct GemmDesc {
   // bf16 update product only: on the last step, apply the parameter update (or write the
   // standalone NS output) from the fp32 accumulators instead of storing the final iterate
   const ApplyDesc* fused;
+  // bf16 Gram product with a split contraction (nks > 1): tile (bi, bj, range ks) stores its fp32
+  // partial product in part (one 256 x 256 row-major tile per upper tile and range, at
+  // ((upper index of (bi, bj)) * nks + ks) * 65536 floats) and a second pass adds the ranges in
+  // order and stores A; 0 or 1: not split
+  float* part;
+  int32_t nks;
 };
+// Upper index of tile (bi, bj), bi <= bj, of a symmetric problem with tm tiles per side (row-major
+// over the upper triangle).
+__host__ __device__ constexpr int upper_index(int bi, int bj, int tm) { return bi * tm - bi * (bi - 1) / 2 + (bj - bi); }
 
 constexpr int kAdamWMaxPerLaunch = 32;
 struct AdamWDesc {
@@ -153,6 +162,11 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, cons
                        int last_step, float ca, float cb, float cc, hipStream_t st);
 hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
                         hipStream_t st);
+// The second pass of a split Gram product: for each job (problem e in the Gram launch's order,
+// upper tile bi <= bj) the problem's nks partial tiles added in range order, scaled as the Gram
+// epilogue scales, stored as A (bf16) at (bi, bj) and mirrored at (bj, bi).
+hipError_t launch_gram_sum(const GemmDesc* d_descs, const TileRef* d_jobs, int njobs, int parity,
+                           int first, hipStream_t st);
 hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);
 
 // NS tile sizes (padding granularity of the workspace buffers).

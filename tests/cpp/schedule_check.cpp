@@ -1,8 +1,9 @@
 // CPU check of the NS GEMM tile schedules (gemm_schedule.h): every tile of every problem exactly
-// once (upper triangle only for symmetric products), whole rounds of XCD groups, every group's
-// tiles on one XCD, the deal's balance (the busiest XCD within one group of the mean), and
-// determinism; random launches plus the owner shares' own launches. Exit code 0 on success; every
-// failure prints what it found.
+// once (upper triangle only for symmetric products; every K range of a split problem's tile once),
+// whole rounds of XCD groups, every group's tiles on one XCD, the deal's balance (the busiest XCD
+// within one group of the mean), and determinism; random launches plus the owner shares' own
+// launches; the Gram launches' K splits (gram_splits) on hand-worked cases. Exit code 0 on
+// success; every failure prints what it found.
 #include <cstdio>
 #include <map>
 #include <random>
@@ -23,19 +24,24 @@ static int g_fail = 0;
     }                                                  \
   } while (0)
 
-static void check_launch(const std::vector<TileGrid>& grids, const std::vector<int64_t>& cost) {
+static void check_launch(const std::vector<TileGrid>& grids, const std::vector<int64_t>& cost,
+                         const std::vector<int>* splits = nullptr) {
   std::vector<int> pos(grids.size());
   for (size_t k = 0; k < pos.size(); ++k) pos[k] = int(k);
-  const std::vector<TileRef> s = build_schedule(pos, grids, cost);
-  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost);
+  auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
+  const std::vector<TileRef> s = build_schedule(pos, grids, cost, splits);
+  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost, splits);
   CHECK(s.size() == s2.size() && std::memcmp(s.data(), s2.data(), s.size() * sizeof(TileRef)) == 0,
         "not deterministic");
   const size_t round = size_t(kGemmXcds) * kGemmSlots;
   CHECK(s.size() % round == 0, "%zu slots: not whole rounds", s.size());
-  std::map<std::tuple<int, int, int>, int> seen;
+  std::map<std::tuple<int, int, int, int>, int> seen;
   int64_t load[kGemmXcds] = {};
   int64_t ntiles = 0, total = 0, gmax = 0;
-  for (const TileGrid& g : grids) ntiles += g.sym ? int64_t(g.tm) * (g.tm + 1) / 2 : int64_t(g.tm) * g.tn;
+  for (size_t e = 0; e < grids.size(); ++e) {
+    const TileGrid& g = grids[e];
+    ntiles += (g.sym ? int64_t(g.tm) * (g.tm + 1) / 2 : int64_t(g.tm) * g.tn) * nks(int(e));
+  }
   for (size_t g = 0; g < s.size() / kGemmSlots; ++g) {
     int64_t gc = 0;
     for (int sl = 0; sl < kGemmSlots; ++sl) {
@@ -45,8 +51,9 @@ static void check_launch(const std::vector<TileGrid>& grids, const std::vector<i
       const TileGrid& gr = grids[t.e];
       CHECK(t.bi >= 0 && t.bi < gr.tm && t.bj >= 0 && t.bj < gr.tn && (!gr.sym || t.bi <= t.bj),
             "tile (%d, %d) outside problem %d", t.bi, t.bj, t.e);
-      seen[std::make_tuple(int(t.e), int(t.bi), int(t.bj))] += 1;
-      gc = std::max(gc, cost[t.e]);
+      CHECK(t.ks >= 0 && t.ks < nks(t.e), "K range %d of problem %d (%d ranges)", t.ks, t.e, nks(t.e));
+      seen[std::make_tuple(int(t.e), int(t.bi), int(t.bj), int(t.ks))] += 1;
+      gc = std::max(gc, cost[t.e] / nks(t.e));
     }
     load[g % kGemmXcds] += gc;   // group g runs on XCD g % kGemmXcds
     total += gc;
@@ -109,6 +116,27 @@ int main() {
                   std::make_pair(8192, 28672), std::make_pair(8192, 28672), std::make_pair(8192, 28672)})
     l70.push_back(sh);
   share("llama3_70b_share", l70);
+  // K splits of the Gram launch (upper tiles, K): the GPT-2-small share's 768 x 3072 matrices cut in
+  // 4 ranges of 768, the K of its 768 x 768 ones; one 768 x 3072 matrix alone in 6 ranges of 512
+  // (96 K blocks of 32 = 6 x 16); a launch that fills the grid, and a uniform one whose work per
+  // workgroup exceeds half its K, not split
+  {
+    std::vector<int64_t> tl, kl;
+    for (int i = 0; i < 4; ++i) { tl.push_back(6); kl.push_back(3072); }
+    for (int i = 0; i < 8; ++i) { tl.push_back(6); kl.push_back(768); }
+    const std::vector<int> f = gram_splits(tl, kl);
+    for (int i = 0; i < 12; ++i) CHECK(f[i] == (i < 4 ? 4 : 1), "gpt2 share: problem %d split %d", i, f[i]);
+    std::vector<TileGrid> grids(12, TileGrid{3, 3, true});
+    check_launch(grids, kl, &f);
+    CHECK(gram_splits({6}, {3072})[0] == 6, "one 768 x 3072 matrix: %d", gram_splits({6}, {3072})[0]);
+    CHECK(gram_splits({300}, {4096})[0] == 1, "a full launch was split");
+    CHECK(gram_splits({200, 20}, {3072, 3072})[0] == 1, "a uniform launch was split");
+    const std::vector<int> g2 = gram_splits({10, 10}, {8192, 256});
+    CHECK(g2[0] == 8 && g2[1] == 1, "8192 / 256: %d %d", g2[0], g2[1]);
+    std::vector<TileGrid> gg{TileGrid{4, 4, true}, TileGrid{4, 4, true}};
+    check_launch(gg, {8192, 256}, &g2);
+  }
+  std::printf("gram splits: ok\n");
   if (g_fail) {
     std::printf("%d failures\n", g_fail);
     return 1;
