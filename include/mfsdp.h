@@ -120,7 +120,10 @@ typedef struct {
 
 /* Bytes of device workspace mfsdp_muon_step (and mfsdp_muon_step_reduce) needs for these entries
  * and hyperparameters (Newton-Schulz iterates in both layouts, the r x r Gram and polynomial
- * matrices, norm partials and launch descriptors); the entries' data pointers are not used.
+ * matrices, norm partials, launch descriptors and, when the Gram product of a call has fewer tiles
+ * than the GPU has compute units and some of its contractions are long, fp32 partial tiles of
+ * those contractions split into ranges: at most a quarter of the rest); the entries' data
+ * pointers are not used.
  * Returns 0 if the arguments are invalid (see mfsdp_last_error). count == 0 returns 0 with no
  * error. */
 size_t mfsdp_muon_workspace_size(const mfsdp_muon_entry* entries, int64_t count,

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cstdint>
 #include <cstring>
 #include <vector>
 
@@ -91,10 +92,13 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
 // launch's length while most of the chip waits. Each problem gets the largest f <= kSplitMax that
 // divides K / 32 and keeps K / f at least at a target: first the larger of kSplitMinK and the
 // launch's work per workgroup, then the longest K range any problem is left with (so that no tile
-// is cut shorter than the launch needs). f = 1 everywhere when the launch fills the grid.
+// is cut shorter than the launch needs). f = 1 everywhere when the launch fills the grid. The split
+// problems' partial tiles (tiles x f each) are held to max_parts: while over, the problem with the
+// most ranges (the most tiles among equals, then the first) drops to its next smaller count.
 constexpr int64_t kSplitMinK = 512;
 constexpr int kSplitMax = 8;
-inline std::vector<int> gram_splits(const std::vector<int64_t>& tiles, const std::vector<int64_t>& K) {
+inline std::vector<int> gram_splits(const std::vector<int64_t>& tiles, const std::vector<int64_t>& K,
+                                    int64_t max_parts = INT64_MAX) {
   const size_t n = tiles.size();
   std::vector<int> f(n, 1);
   const int64_t slots = int64_t(kGemmXcds) * kGemmSlots;
@@ -114,6 +118,20 @@ inline std::vector<int> gram_splits(const std::vector<int64_t>& tiles, const std
   int64_t kcrit = 0;
   for (size_t e = 0; e < n; ++e) kcrit = std::max(kcrit, K[e] / fit(K[e], kt));
   for (size_t e = 0; e < n; ++e) f[e] = fit(K[e], kcrit);
+  auto parts = [&] {
+    int64_t p = 0;
+    for (size_t e = 0; e < n; ++e)
+      if (f[e] > 1) p += tiles[e] * f[e];
+    return p;
+  };
+  while (parts() > max_parts) {
+    size_t w = 0;
+    for (size_t e = 1; e < n; ++e)
+      if (f[e] > f[w] || (f[e] == f[w] && tiles[e] > tiles[w])) w = e;
+    int c = f[w] - 1;
+    while (c > 1 && (K[w] / 32) % c != 0) --c;
+    f[w] = c;
+  }
   return f;
 }
 

@@ -275,7 +275,8 @@ struct Plan {
 };
 
 // On the bf16 path a Gram launch with fewer tiles than the persistent grid has workgroups may split
-// long contractions (gram_splits); the split problems' partial tiles follow the per-matrix buffers.
+// long contractions (gram_splits); the split problems' partial tiles follow the per-matrix buffers
+// and take at most a quarter of their bytes.
 template <typename ShapeAt>
 Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   Plan P;
@@ -307,7 +308,10 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
         std::vector<int64_t> tl, kl;
         for (const TileGrid& g : grids) tl.push_back(int64_t(g.tm) * (g.tm + 1) / 2);
         for (int64_t c : cost) kl.push_back(c);
-        P.split = gram_splits(tl, kl);
+        size_t base = 0;
+        for (const NsPlan& q : shapes) base += q.bytes;
+        const size_t part_bytes = size_t(kTileBF16) * kTileBF16 * sizeof(float);
+        P.split = gram_splits(tl, kl, int64_t(base / 4 / part_bytes));
       }
       for (int k = 0; k < int(count); ++k)
         if (P.split[size_t(k)] > 1)

@@ -135,6 +135,16 @@ int main() {
     CHECK(g2[0] == 8 && g2[1] == 1, "8192 / 256: %d %d", g2[0], g2[1]);
     std::vector<TileGrid> gg{TileGrid{4, 4, true}, TileGrid{4, 4, true}};
     check_launch(gg, {8192, 256}, &g2);
+    // the partial-tile budget: one 2048 x 2048 matrix (36 tiles, 4 ranges uncapped) drops to 2
+    // ranges under 100 partial tiles and to none under 48; the GPT-2 share's 96 fit 140
+    CHECK(gram_splits({36}, {2048})[0] == 4, "2048 x 2048 uncapped: %d", gram_splits({36}, {2048})[0]);
+    CHECK(gram_splits({36}, {2048}, 100)[0] == 2, "2048 x 2048 capped at 100: %d", gram_splits({36}, {2048}, 100)[0]);
+    CHECK(gram_splits({36}, {2048}, 48)[0] == 1, "2048 x 2048 capped at 48: %d", gram_splits({36}, {2048}, 48)[0]);
+    CHECK(gram_splits(tl, kl, 140) == f, "GPT-2 share under a 140-tile budget");
+    const std::vector<int> g3 = gram_splits(tl, kl, 60);
+    int64_t p3 = 0;
+    for (int i = 0; i < 12; ++i) p3 += g3[i] > 1 ? tl[i] * g3[i] : 0;
+    CHECK(p3 <= 60, "GPT-2 share under a 60-tile budget: %lld partial tiles", (long long)p3);
   }
   std::printf("gram splits: ok\n");
   if (g_fail) {
