@@ -17,7 +17,9 @@ also runs every rank's planned share on the GPU and reports the step-time imbala
 `shampoo` times the Shampoo owner step (fp32 accuracy; products on the bf16 MFMA with split
 operands, rates given against the fp32 MFMA peak and the split-product ceiling) on the GPT-2-small share, with and without
 preconditioner refresh; `soap` times the SOAP owner step (Adam in the eigenbasis of the Shampoo
-statistics) on the same share, with and without the basis refresh (power step + Householder QR).
+statistics) on the same share, with and without the basis refresh (power step + Householder QR), and
+`soap_llama_layer` on one Llama-3-8B layer's seven matrices (sides up to 4096 preconditioned: the
+14336-long FFN sides keep the identity basis).
 """
 from __future__ import annotations
 
@@ -492,25 +494,32 @@ def time_shampoo(native, torch, dev, hev, stream, steps, warmup, iters=20) -> di
     return out
 
 
-def soap_nominal_flop(shapes, refresh_iters: int, refresh: bool) -> float:
-    """Nominal flop of one SOAP step: Q_L^T [G | M] (4 m^2 n), its two halves times Q_R (4 m n^2),
-    Q_L N' (2 m^2 n), (Q_L N') Q_R^T (2 m n^2) and the statistics (2 m^2 n + 2 m n^2); per refresh
-    iteration the power step S Q (2 d^3 per side) and a Householder QR with the explicit Q
-    (LAPACK's count, 4/3 d^3 for the factorization and 4/3 d^3 for forming Q)."""
+def soap_nominal_flop(shapes, refresh_iters: int, refresh: bool, max_precond_dim: int = 4096) -> float:
+    """Nominal flop of one SOAP step: per side with a basis (length <= max_precond_dim), on the left
+    Q_L^T [G | M] (4 m^2 n), Q_L N' (2 m^2 n) and the statistic G G^T (2 m^2 n), on the right [G' | M']
+    Q_R (4 m n^2), (Q_L N') Q_R^T (2 m n^2) and G^T G (2 m n^2); per refresh iteration and side the
+    power step S Q (2 d^3) and a Householder QR with the explicit Q (LAPACK's count, 4/3 d^3 for the
+    factorization and 4/3 d^3 for forming Q)."""
     tot = 0.0
     for m, n in shapes:
-        tot += 8.0 * m * n * (m + n)
-        if refresh:
-            tot += refresh_iters * (2.0 + 8.0 / 3.0) * (m ** 3 + n ** 3)
+        for d, other in ((m, n), (n, m)):
+            if d <= max_precond_dim:
+                tot += 8.0 * d * d * other
+                if refresh:
+                    tot += refresh_iters * (2.0 + 8.0 / 3.0) * d ** 3
     return tot
 
 
-def time_soap(native, torch, dev, hev, stream, steps, warmup) -> dict:
-    """The SOAP owner step (Section 5.7) on the GPT-2-small share's 12 matrices, fp32 math, bases
-    starting at the identity and statistics at zero (the cost does not depend on the values)."""
+def time_soap(native, torch, dev, hev, stream, steps, warmup, shapes=None, label=None,
+              max_precond_dim=4096, tag="soap") -> dict:
+    """The SOAP owner step (Section 5.7), fp32 math, bases starting at the identity and statistics at
+    zero (the cost does not depend on the values): by default on the GPT-2-small share's 12
+    matrices; sides longer than max_precond_dim keep the identity basis."""
     import synth
-    wl = synth.workload(2)
-    shapes = [(e.m, e.n) for e in wl.muon]
+    if shapes is None:
+        wl = synth.workload(2)
+        shapes = [(e.m, e.n) for e in wl.muon]
+        label = wl.name + " (12 matrices: 8 x 768x768, 2 x 3072x768, 2 x 768x3072)"
     gen = torch.Generator(device=dev)
     gen.manual_seed(3)
     keep, ents = [], []
@@ -518,15 +527,18 @@ def time_soap(native, torch, dev, hev, stream, steps, warmup) -> dict:
         t = ((torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
              (torch.randn(m, n, device=dev, generator=gen) * 0.02).to(torch.bfloat16),
              torch.zeros(m, n, device=dev), torch.zeros(m, n, device=dev),
-             torch.zeros(m, m, device=dev), torch.zeros(n, n, device=dev),
-             torch.eye(m, device=dev), torch.eye(n, device=dev))
+             torch.zeros(m, m, device=dev) if m <= max_precond_dim else None,
+             torch.zeros(n, n, device=dev) if n <= max_precond_dim else None,
+             torch.eye(m, device=dev) if m <= max_precond_dim else None,
+             torch.eye(n, device=dev) if n <= max_precond_dim else None)
         keep.append(t)
         ents.append(native.soap_entry_t(*t))
-    out = {"workload": wl.name + " (12 matrices: 8 x 768x768, 2 x 3072x768, 2 x 768x3072)",
-           "dtype": "f32", "betas": [0.95, 0.95], "shampoo_beta": 0.95}
+    out = {"workload": label, "dtype": "f32", "betas": [0.95, 0.95], "shampoo_beta": 0.95,
+           "max_precond_dim": max_precond_dim}
     step_no = 1
     for refresh in (True, False):
-        hp = native.soap_hparams(lr=3e-3, weight_decay=0.01, refresh=refresh, refresh_iters=1)
+        hp = native.soap_hparams(lr=3e-3, weight_decay=0.01, refresh=refresh, refresh_iters=1,
+                                 max_precond_dim=max_precond_dim)
         ws = native.soap_workspace_t(ents, hp, device=dev)
 
         def one():
@@ -544,15 +556,17 @@ def time_soap(native, torch, dev, hev, stream, steps, warmup) -> dict:
         hev.record(b, stream)
         torch.cuda.synchronize()
         ms = hev.elapsed_ms(a, b) / steps
-        fl = soap_nominal_flop(shapes, 1, refresh)
+        fl = soap_nominal_flop(shapes, 1, refresh, max_precond_dim)
         key = "refresh" if refresh else "no_refresh"
         out[key] = {"ms_per_step": round(ms, 4), "nominal_flop_per_step": fl,
                     "nominal_tflops": round(fl / (ms * 1e-3) / 1e12, 2),
                     "x_fp32_mfma_peak": round(fl / (ms * 1e-3) / 1e12 / PEAK_F32_MFMA_TFLOPS, 4),
                     "frac_split_bf16_peak": round(fl / (ms * 1e-3) / 1e12 / PEAK_SPLIT_TFLOPS, 4),
                     "workspace_gib": round(ws.numel() / 2 ** 30, 3)}
-        log(f"soap ({key}): {ms:.3f} ms per step, {fl / (ms * 1e-3) / 1e12:.1f} nominal TFLOP/s")
+        log(f"{tag} ({key}): {ms:.3f} ms per step, {fl / (ms * 1e-3) / 1e12:.1f} nominal TFLOP/s")
         del ws
+    del keep, ents
+    torch.cuda.empty_cache()
     return out
 
 
@@ -768,6 +782,13 @@ def main() -> int:
         out["shampoo"] = time_shampoo(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
     if not args.no_soap:
         out["soap"] = time_soap(native, torch, dev, hev, stream, max(3, args.steps // 4), 1)
+        # one Llama-3-8B layer: q, k, v, o, gate, up, down
+        layer = [(4096, 4096), (1024, 4096), (1024, 4096), (4096, 4096), (14336, 4096), (14336, 4096),
+                 (4096, 14336)]
+        out["soap_llama_layer"] = time_soap(
+            native, torch, dev, hev, stream, 3, 1, layer,
+            "llama3_8b_layer (q, k, v, o 4096x4096 / 1024x4096, gate, up 14336x4096, down 4096x14336)",
+            tag="soap_llama_layer")
     if not args.no_cpu_baseline:
         # about 10-30 s of fp64 work on the host: one matrix of each Llama-3-8B shape
         sample = {3: [0, 1, 4, 6], 2: list(range(12)), 1: [0], 4: [0, 1], 5: [1]}.get(args.workload, [0])
