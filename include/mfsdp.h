@@ -372,8 +372,12 @@ size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
 /* One SOAP step on every entry (host array of count entries), enqueued on `stream` (hipStream_t,
  * NULL = default stream); no host synchronisation. Every product runs at fp32 accuracy on the
  * bf16 MFMA as in mfsdp_shampoo_step (grouped over the entries); the refresh QR is a blocked
- * Householder factorization (panels of 16 columns). The workspace (device, 256-byte aligned,
- * >= the size query) must not be in use by another call still running. Returns MFSDP_OK,
+ * Householder factorization (16-column panels in 128-column blocks whose updates run on the same
+ * GEMM). Part of each block update runs on a library-owned auxiliary stream of the current device
+ * (default priority, created on first use, kept until the process ends), forked from `stream` and
+ * joined back into it through events before the call returns, so `stream` orders everything the
+ * call enqueues (and a graph captured from `stream` contains it). The workspace (device, 256-byte
+ * aligned, >= the size query) must not be in use by another call still running. Returns MFSDP_OK,
  * MFSDP_E_INVALID, MFSDP_E_WORKSPACE or MFSDP_E_HIP; on an argument error nothing is enqueued.
  * At most 4096 entries per call. */
 int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
