@@ -197,14 +197,14 @@ __global__ __launch_bounds__(256) void soap_eye_kernel(const SoapEyeDesc* __rest
 // diagonal and the dot products v_j . v_k (j < k) above it, from which the applications and the
 // block's factor form what they need. One 512-thread workgroup per panel; thread t holds rows
 // t + 512 i (i < 8) of the panel in registers (the panel's columns are rows of the transposed matrix:
-// each is read coalesced). Per column two block reductions: the norm below the pivot, then the 15
-// dot products v_k . a_l (l > k, to update the later columns) and v_i . v_k (i < k), whose partials
-// every wave sums itself (lane l: slot l, in wave order) and reads back from its lanes, so that no
-// third barrier is needed. Every sum is taken in a fixed order.
+// each is read coalesced). One block reduction per column, of 16 sums at once (column k's squared
+// norm below the pivot and its products with the other 15 columns there), formed in the same pass
+// over the rows that applies the previous reflector; every wave sums the waves' partials itself
+// (lane l: slot l, in wave order) and reads them back from its lanes. Every sum is taken in a fixed
+// order.
 __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanelDesc* __restrict__ descs) {
-  __shared__ float red1[kQrPanelThreads / 64];
-  __shared__ float red2[kQrPanelThreads / 64][kQrPanel];
-  __shared__ float alpha_s;
+  __shared__ float red[2][kQrPanelThreads / 64][kQrPanel];  // by column parity: the waves' sums
+  __shared__ float piv[2][kQrPanel];                         // by column parity: the pivot row
   __shared__ float Ds[kQrPanel][kQrPanel];
   const QrPanelDesc& d = descs[blockIdx.x];
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
@@ -225,80 +225,85 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
   // register rows that hold panel rows (uniform); the others are zero and are skipped. Columns
   // >= jb are zero as well: their dot products are exactly 0 and they stay 0.
   const int used = (rows + kQrPanelThreads - 1) / kQrPanelThreads;
+  // Column k's sums over the rows below its pivot: slot l = a_k . a_l (slot k: the squared norm),
+  // reduced within each wave (lane l: slot l) into red[k & 1]; the pivot row into piv[k & 1].
+  auto reduce_col = [&](auto kc) {
+    constexpr int k = decltype(kc)::value;
+    float part[kQrPanel];
+#pragma unroll
+    for (int l = 0; l < kQrPanel; ++l) part[l] = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kQrRowsPerThread; ++i) {
+      if (i < used && t + kQrPanelThreads * i > k) {
+        const float ak = a[i][k];
+#pragma unroll
+        for (int l = 0; l < kQrPanel; ++l) part[l] += ak * a[i][l];
+      }
+    }
+    // lane l of every row: the row's sum of slot l; then over the four rows of the wave (the
+    // adds are commutative pairs, so every lane of a column l agrees bit for bit)
+    float r = row_reduce_scatter16(part, lane & 15);
+    r += __shfl_xor(r, 16);
+    r += __shfl_xor(r, 32);
+    if (lane < kQrPanel) red[k & 1][w][lane] = r;
+    if (t == k) {
+#pragma unroll
+      for (int l = 0; l < kQrPanel; ++l) piv[k & 1][l] = a[0][l];
+    }
+  };
+  if (jb > 0) {  // (uniform)
+    reduce_col(std::integral_constant<int, 0>{});
+    __syncthreads();
+  }
 
+  // One barrier per column: the sums of column k were formed (and reduced) in the pass that applied
+  // reflector k - 1. With them, v_k = e_k + scale a_k (below the pivot), and every product with v_k
+  // follows without another reduction: v_k . a_l = a_l[k] + scale (a_k . a_l), v_j . v_k = v_j[k] +
+  // scale (a_k . v_j).
   unrolled<kQrPanel>([&](auto kc) {
     constexpr int k = decltype(kc)::value;
     if (k >= jb) return;  // (uniform: jb is the panel's width)
-    // norm of the column below the pivot (local row k), and the pivot itself
-    float s = 0.0f;
+    // the block totals: lane l of every wave sums slot l over the waves in wave order, and the wave
+    // reads them from its lanes (red[k & 1] and piv[k & 1] are written again only after the next
+    // column's barrier)
+    float mine = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kQrRowsPerThread; ++i) {
-      const int lr = t + kQrPanelThreads * i;
-      if (i < used && lr > k) s += a[i][k] * a[i][k];
+    for (int j = 0; j < kQrPanelThreads / 64; ++j) mine += red[k & 1][j][lane & (kQrPanel - 1)];
+    float tot[kQrPanel], pv[kQrPanel];
+#pragma unroll
+    for (int l = 0; l < kQrPanel; ++l) {
+      tot[l] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine), l));
+      pv[l] = piv[k & 1][l];
     }
-    s = wave_sum(s);
-    if (lane == 0) red1[w] = s;
-    if (t == k) alpha_s = a[0][k];
-    __syncthreads();
-    float sigma = 0.0f;
-#pragma unroll
-    for (int j = 0; j < kQrPanelThreads / 64; ++j) sigma += red1[j];
-    const float alpha = alpha_s;
+    const float alpha = pv[k], sigma = tot[k];
     float tau = 0.0f, scale = 0.0f;
     if (sigma != 0.0f) {
       const float beta = -copysignf(sqrtf(alpha * alpha + sigma), alpha);
       tau = (beta - alpha) / beta;
       scale = 1.0f / (alpha - beta);
     }
+    float f[kQrPanel];
+#pragma unroll
+    for (int l = k + 1; l < kQrPanel; ++l) f[l] = tau * (pv[l] + scale * tot[l]);
 #pragma unroll
     for (int i = 0; i < kQrRowsPerThread; ++i) {
       if (i < used) {
         const int lr = t + kQrPanelThreads * i;
         a[i][k] = lr > k ? a[i][k] * scale : (lr == k ? 1.0f : 0.0f);
-      }
-    }
-    // slot s < k: v_s . v_k (for T); slot s >= k: v_k . a_{s+1} (to update column s + 1)
-    {
-      float part[kQrPanel];
 #pragma unroll
-      for (int sl = 0; sl < kQrPanel; ++sl) part[sl] = 0.0f;
-#pragma unroll
-      for (int i = 0; i < kQrRowsPerThread; ++i) {
-        if (i < used) {
-          const float vk = a[i][k];
-#pragma unroll
-          for (int sl = 0; sl < kQrPanel - 1; ++sl) part[sl] += vk * a[i][sl < k ? sl : sl + 1];
-        }
-      }
-      // lane l of every row: the row's sum of slot l; then over the four rows of the wave (the
-      // adds are commutative pairs, so every lane of a column l agrees bit for bit)
-      float r = row_reduce_scatter16(part, lane & 15);
-      r += __shfl_xor(r, 16);
-      r += __shfl_xor(r, 32);
-      if (lane < kQrPanel - 1) red2[w][lane] = r;
-    }
-    __syncthreads();
-    // the 15 block totals: lane l of every wave sums slot l over the waves in wave order, and the
-    // wave reads the totals from its lanes (red2 and red1 are written again only after the next
-    // step's first barrier)
-    float mine = 0.0f;
-#pragma unroll
-    for (int j = 0; j < kQrPanelThreads / 64; ++j) mine += red2[j][lane & (kQrPanel - 1)];
-    float tot[kQrPanel - 1];
-#pragma unroll
-    for (int sl = 0; sl < kQrPanel - 1; ++sl)
-      tot[sl] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mine), sl));
-#pragma unroll
-    for (int i = 0; i < kQrRowsPerThread; ++i) {
-      if (i < used) {
-#pragma unroll
-        for (int l = k + 1; l < kQrPanel; ++l) a[i][l] -= (tau * tot[l - 1]) * a[i][k];
+        for (int l = k + 1; l < kQrPanel; ++l) a[i][l] -= f[l] * a[i][k];
       }
     }
 #pragma unroll
     for (int j = 0; j < k; ++j)
-      if (t == j) Ds[j][k] = tot[j];
+      if (t == j) Ds[j][k] = pv[j] + scale * tot[j];
     if (t == k) Ds[k][k] = tau;
+    if constexpr (k + 1 < kQrPanel) {
+      if (k + 1 < jb) {  // (uniform)
+        reduce_col(std::integral_constant<int, k + 1>{});
+        __syncthreads();
+      }
+    }
   });
   __syncthreads();
   // the panel's 16 columns of V and rows of Vt over every block row: rows [0, c - j0) above the
