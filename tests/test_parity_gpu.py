@@ -205,6 +205,24 @@ def test_muon_single_matrix_few_tiles(native, shape):
         assert torch.equal(a, b)
 
 
+def test_muon_split_gram_contraction(native):
+    """Two 1024 x 8192 matrices (wide and tall) alone in a call: their Gram launch has 20 tiles with
+    K = 8192, so the contraction is split into K ranges (as many as the partial-tile budget, a
+    quarter of the per-matrix buffers, allows); each range's fp32 partial tile is added in order by
+    the second pass. Matches the oracle and is bitwise reproducible."""
+    import torch
+    _say("muon split Gram contraction: 1024x8192, 8192x1024")
+    rng = np.random.default_rng(5100)
+    specs = [synth.MuonSpec(1024, 8192, "wide"), synth.MuonSpec(8192, 1024, "tall")]
+    tensors = [synth.random_muon_tensors(rng, e.m, e.n) for e in specs]
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
+    dev = _run_muon(native, tensors, specs, hp)
+    _check_muon(tensors, specs, dev, hp, 2e-2)
+    dev2 = _run_muon(native, tensors, specs, hp)
+    for a, b in zip(dev[0], dev2[0]):
+        assert torch.equal(a, b)
+
+
 MIXED = [(256, 512), (512, 256), (384, 384), (100, 700), (700, 100), (130, 1000), (1, 50),
          (50, 1), (768, 3072), (3072, 768)]
 

@@ -102,6 +102,17 @@ def test_noalloc_fp32_path_after_bf16():
     assert rel_fro(from_dev(c[1][2]), buf_or) <= 1e-6
 
 
+def test_noalloc_split_gram_contraction_matches_workspace_step():
+    """One 768 x 3072 matrix alone: its Gram launch has 6 tiles with K = 3072, so both entry points
+    split that contraction into K ranges (within the partial-tile budget of the plan they share);
+    the outputs equal bitwise and match the oracle."""
+    from paper_2607_05895_amd import native
+    rng = np.random.default_rng(79)
+    _say("noalloc call: 768x3072 (bf16, split Gram contraction)")
+    items = _make(rng, [(768, 3072)], synth.BF16, synth.BF16)
+    _compare(native, items, dict(lr=0.02, weight_decay=0.01), 2e-2)
+
+
 def test_noalloc_rejects_entries_beyond_the_scratch():
     import torch
     from paper_2607_05895_amd import native
