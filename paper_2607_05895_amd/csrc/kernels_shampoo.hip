@@ -121,8 +121,10 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
   {
     // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
     const int lrow = t >> 2, lch = t & 3;
-    f32x4 ra[2], rb[2];
-    auto gload = [&](int k0) {
+    // two register sets, so that the loads of step k + 2 are issued while step k multiplies and
+    // step k + 1's loads (issued a step earlier) are split into LDS
+    f32x4 ra0[2], rb0[2], ra1[2], rb1[2];
+    auto gload = [&](f32x4 (&ra)[2], f32x4 (&rb)[2], int k0) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int r = lrow + 64 * j;
@@ -131,7 +133,7 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
       }
     };
     // plane (operand o, part p) of stage s; the 8-byte piece of row r holding k 4 lch .. + 3
-    auto lstore = [&](int s) {
+    auto lstore = [&](int s, const f32x4 (&ra)[2], const f32x4 (&rb)[2]) {
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int r = lrow + 64 * j;
@@ -151,16 +153,9 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
     auto frag = [&](int s, int plane, int r) {
       return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kStage + plane * kPlane + split_slot(r, fh) * 16);
     };
-    const int nk = d.K / 16;
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int s = kt & 1;
-      if (kt + 1 < nk) gload((kt + 1) * 16);
-      // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid,
-      // hi.hi) term by term over the four blocks, so that consecutive MFMAs use different
-      // accumulators
+    // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi)
+    // term by term over the four blocks, so that consecutive MFMAs use different accumulators
+    auto mfma_stage = [&](int s) {
       bf16x8_t af[2][3], bf[2][3];
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -178,7 +173,22 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
           for (int j = 0; j < 2; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]], acc[i][j],
                                                                 0, 0, 0);
-      if (kt + 1 < nk) lstore(s ^ 1);
+    };
+    const int nk = d.K / 16;
+    // even steps live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
+    gload(ra0, rb0, 0);
+    if (nk > 1) gload(ra1, rb1, 16);
+    lstore(0, ra0, rb0);
+    __syncthreads();
+    for (int kt = 0; kt < nk; kt += 2) {
+      if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * 16);
+      mfma_stage(0);
+      if (kt + 1 < nk) lstore(1, ra1, rb1);
+      __syncthreads();
+      if (kt + 1 >= nk) break;
+      if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * 16);
+      mfma_stage(1);
+      if (kt + 2 < nk) lstore(0, ra0, rb0);
       __syncthreads();
     }
   }
