@@ -1,6 +1,8 @@
 """The NS GEMM tile schedules (csrc/gemm_schedule.h, plain host C++) built with g++ and checked on the
-CPU: every tile of every problem exactly once, whole rounds of XCD groups, the deal's balance and
-determinism, on random launches and on the owner shares' own launches."""
+CPU: every tile of every problem exactly once (every K range of a split Gram tile once), whole rounds
+of XCD groups, the deal's balance and determinism, on random launches and on the owner shares' own
+launches; and the Gram launches' K splits on hand-worked cases, with and without the partial-tile
+budget."""
 import os
 import subprocess
 import tempfile
