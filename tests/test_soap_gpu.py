@@ -70,8 +70,10 @@ def _sign_aligned_err(q, q_ref):
 
 # ------------------------------------------------------------------ orthonormal factor
 
-@pytest.mark.parametrize("d", [1, 2, 15, 16, 17, 100, 129, 300, 640])
+@pytest.mark.parametrize("d", [1, 2, 15, 16, 17, 100, 127, 128, 129, 255, 256, 257, 300, 640])
 def test_orthonormal_factor_matches_numpy_qr(native, d):
+    """Against LAPACK's QR: one-panel and ragged sizes, and sizes at and around the 128-column blocks
+    whose updates run on the GEMM (127 .. 129, 255 .. 257)."""
     import torch
     _say(f"orthonormal factor d={d}")
     rng = np.random.default_rng(100 + d)
