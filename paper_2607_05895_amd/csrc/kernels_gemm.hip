@@ -748,11 +748,11 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
 #undef MFSDP_WAIT_VMCNT
 #undef MFSDP_WAIT_LGKM0
 
-// Second pass of a split Gram product: one 256-thread workgroup per (job, 32-row slab of the tile).
+// Second pass of a split Gram product: one 256-thread workgroup per (job, 16-row slab of the tile).
 // Thread t adds the nks partials of 4 consecutive columns 4 (t % 64) of rows t / 64 + 4 i in range
 // order, scales as the Gram epilogue does and stores 8 bytes of bf16 into the tile; an off-diagonal
-// tile's slab also goes through LDS to its mirror, where it is one 64-byte row piece per tile column.
-constexpr int kSumSlab = 32;
+// tile's slab also goes through LDS to its mirror, where it is one 32-byte row piece per tile column.
+constexpr int kSumSlab = 16;
 __global__ __launch_bounds__(256) void gram_sum_kernel(const GemmDesc* __restrict__ descs,
                                                        const TileRef* __restrict__ jobs, int parity,
                                                        int first) {
@@ -783,7 +783,8 @@ __global__ __launch_bounds__(256) void gram_sum_kernel(const GemmDesc* __restric
   }
   if (bi == bj) return;  // (uniform) the diagonal tile is whole
   __syncthreads();
-  // mirror row bj * 256 + t, columns bi * 256 + 32 slab .. + 31: one 16 x 32 block row piece
+  // mirror row bj * 256 + t, columns bi * 256 + kSumSlab slab .. + kSumSlab - 1: part of one row of a
+  // 16 x 32 block
   uint32_t w[kSumSlab / 2];
 #pragma unroll
   for (int k = 0; k < kSumSlab / 2; ++k) w[k] = pack_bf16x2(tt[2 * k][t], tt[2 * k + 1][t]);
