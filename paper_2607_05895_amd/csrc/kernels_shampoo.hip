@@ -59,21 +59,127 @@ __device__ __forceinline__ void split3x4(const f32x4& x, u32x2& hi, u32x2& mid, 
 // reads) fall in 16 distinct 16-byte bank groups, and a wave's 8-byte stores (4 lanes per row) in 32.
 __device__ __forceinline__ int split_slot(int r, int c) { return r * 2 + (c ^ ((r >> 3) & 1)); }
 
-// C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup.
+// Exact split of four fp32 values whose values are bf16 numbers (an operand with one part): the
+// packed bf16 values themselves.
+__device__ __forceinline__ u32x2 split1x4(const f32x4& x) {
+  return u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
+}
+
+constexpr int kShPlane = kShTile * 32;  // bytes of one split plane (128 x 16 bf16)
+constexpr int kShStage = 6 * kShPlane;  // both operands of one K step, three planes each
+
+// The products of one 128 x 128 output tile, P rows from bi, Q rows from bj, into acc, with PA
+// parts of P and PB parts of Q (3: fp32 split into hi + mid + lo; 1: an operand whose values are
+// bf16 numbers, so that its mid and lo parts are zero and the products with them are dropped,
+// which leaves the accumulated sums unchanged).
 // 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The next K step's
 // global loads are held in registers during the current step's products (LDS double buffer).
-// The products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32 accuracy. K steps of 16; when a step is staged into LDS every element is
-// split once into hi + mid + lo bf16 parts (three planes per operand, 24 KiB per stage); a lane's
-// fragment is 8 consecutive k of one row from each plane, and the six partial products above 2^-24
-// relative are accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo,
-// lo.mid, lo.lo are below 2^-32). Six bf16 MFMAs per 16 k take 192 cycles against 512 for the fp32
-// MFMA. 48 KiB of LDS lets three workgroups share a CU.
+// The products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32
+// accuracy. K steps of 16; when a step is staged into LDS every element is split once into
+// hi + mid + lo bf16 parts (three planes per operand, 24 KiB per stage); a lane's fragment is 8
+// consecutive k of one row from each plane, and the six partial products above 2^-24 relative are
+// accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo, lo.mid, lo.lo are
+// below 2^-32). Six bf16 MFMAs per 16 k take 192 cycles against 512 for the fp32 MFMA.
+template <int PA, int PB>
+__device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, int bj, uint8_t* lds_raw,
+                                                 f32x16 (&acc)[2][2]) {
+  const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
+  const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wr = w >> 1, wc = w & 1;
+  const int fr = lane & 31, fh = lane >> 5;
+  // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
+  const int lrow = t >> 2, lch = t & 3;
+  // two register sets, so that the loads of step k + 2 are issued while step k multiplies and
+  // step k + 1's loads (issued a step earlier) are split into LDS
+  f32x4 ra0[2], rb0[2], ra1[2], rb1[2];
+  auto gload = [&](f32x4 (&ra)[2], f32x4 (&rb)[2], int k0) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r = lrow + 64 * j;
+      ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
+      rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
+    }
+  };
+  // plane (operand o, part p) of stage s is plane 3 o + p; the 8-byte piece of row r holding
+  // k 4 lch .. + 3
+  auto lstore = [&](int s, const f32x4 (&ra)[2], const f32x4 (&rb)[2]) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int r = lrow + 64 * j;
+      const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
+      uint8_t* base = lds_raw + s * kShStage;
+      u32x2 h, m, l;
+      if (PA == 3) {
+        split3x4(ra[j], h, m, l);
+        *reinterpret_cast<u32x2*>(base + 0 * kShPlane + off) = h;
+        *reinterpret_cast<u32x2*>(base + 1 * kShPlane + off) = m;
+        *reinterpret_cast<u32x2*>(base + 2 * kShPlane + off) = l;
+      } else {
+        *reinterpret_cast<u32x2*>(base + 0 * kShPlane + off) = split1x4(ra[j]);
+      }
+      if (PB == 3) {
+        split3x4(rb[j], h, m, l);
+        *reinterpret_cast<u32x2*>(base + 3 * kShPlane + off) = h;
+        *reinterpret_cast<u32x2*>(base + 4 * kShPlane + off) = m;
+        *reinterpret_cast<u32x2*>(base + 5 * kShPlane + off) = l;
+      } else {
+        *reinterpret_cast<u32x2*>(base + 3 * kShPlane + off) = split1x4(rb[j]);
+      }
+    }
+  };
+  auto frag = [&](int s, int plane, int r) {
+    return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kShStage + plane * kShPlane + split_slot(r, fh) * 16);
+  };
+  // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi)
+  // term by term over the four blocks, so that consecutive MFMAs use different accumulators
+  auto mfma_stage = [&](int s) {
+    bf16x8_t af[2][PA], bf[2][PB];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int pt = 0; pt < PA; ++pt) af[i][pt] = frag(s, pt, wr * 64 + i * 32 + fr);
+#pragma unroll
+      for (int pt = 0; pt < PB; ++pt) bf[i][pt] = frag(s, 3 + pt, wc * 64 + i * 32 + fr);
+    }
+    constexpr int kTerm[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
+#pragma unroll
+    for (int tm = 0; tm < 6; ++tm) {
+      if (kTerm[tm][0] >= PA || kTerm[tm][1] >= PB) continue;
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]],
+                                                              acc[i][j], 0, 0, 0);
+    }
+  };
+  const int nk = d.K / 16;
+  // even steps live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
+  gload(ra0, rb0, 0);
+  if (nk > 1) gload(ra1, rb1, 16);
+  lstore(0, ra0, rb0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * 16);
+    mfma_stage(0);
+    if (kt + 1 < nk) lstore(1, ra1, rb1);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * 16);
+    mfma_stage(1);
+    if (kt + 2 < nk) lstore(0, ra0, rb0);
+    __syncthreads();
+  }
+}
+
+// C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup (products as in
+// sh_tile_products, with the descriptor's part counts: both one part, Q one part, else three and
+// three). 48 KiB of LDS lets three workgroups share a CU.
 // Symmetric problems compute the upper tiles only and store each tile transposed as well, through
 // LDS, with coalesced row stores.
 __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs, int count) {
-  constexpr int kPlane = kShTile * 32;                        // bytes of one split plane (128 x 16 bf16)
-  constexpr int kStage = 6 * kPlane;  // both operands of one K step, three planes each
-  __shared__ __attribute__((aligned(16))) uint8_t lds_raw[2 * kStage];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_raw[2 * kShStage];
   const int e = find_desc(descs, count, blockIdx.x);
   const ShGemmDesc& d = descs[e];
   int lt = blockIdx.x - d.tile_begin;
@@ -94,6 +200,7 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
   }
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wr = w >> 1, wc = w & 1;
+  const int fr = lane & 31, fh = lane >> 5;
   if (d.conv_in && *d.conv_in < kShConvTol) {  // converged side: the iterate no longer changes
     if (d.copy_on_skip) {
       const g_cf32* src = (const g_cf32*)(d.E);
@@ -110,88 +217,17 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
     }
     return;
   }
-  const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
-  const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
   f32x16 acc[2][2];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  const int fr = lane & 31, fh = lane >> 5;
-  {
-    // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
-    const int lrow = t >> 2, lch = t & 3;
-    // two register sets, so that the loads of step k + 2 are issued while step k multiplies and
-    // step k + 1's loads (issued a step earlier) are split into LDS
-    f32x4 ra0[2], rb0[2], ra1[2], rb1[2];
-    auto gload = [&](f32x4 (&ra)[2], f32x4 (&rb)[2], int k0) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int r = lrow + 64 * j;
-        ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
-        rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
-      }
-    };
-    // plane (operand o, part p) of stage s; the 8-byte piece of row r holding k 4 lch .. + 3
-    auto lstore = [&](int s, const f32x4 (&ra)[2], const f32x4 (&rb)[2]) {
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int r = lrow + 64 * j;
-        const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
-        u32x2 h, m, l;
-        split3x4(ra[j], h, m, l);
-        uint8_t* base = lds_raw + s * kStage;
-        *reinterpret_cast<u32x2*>(base + 0 * kPlane + off) = h;
-        *reinterpret_cast<u32x2*>(base + 1 * kPlane + off) = m;
-        *reinterpret_cast<u32x2*>(base + 2 * kPlane + off) = l;
-        split3x4(rb[j], h, m, l);
-        *reinterpret_cast<u32x2*>(base + 3 * kPlane + off) = h;
-        *reinterpret_cast<u32x2*>(base + 4 * kPlane + off) = m;
-        *reinterpret_cast<u32x2*>(base + 5 * kPlane + off) = l;
-      }
-    };
-    auto frag = [&](int s, int plane, int r) {
-      return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kStage + plane * kPlane + split_slot(r, fh) * 16);
-    };
-    // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi)
-    // term by term over the four blocks, so that consecutive MFMAs use different accumulators
-    auto mfma_stage = [&](int s) {
-      bf16x8_t af[2][3], bf[2][3];
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int pt = 0; pt < 3; ++pt) {
-          af[i][pt] = frag(s, pt, wr * 64 + i * 32 + fr);
-          bf[i][pt] = frag(s, 3 + pt, wc * 64 + i * 32 + fr);
-        }
-      constexpr int kTerm[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
-#pragma unroll
-      for (int tm = 0; tm < 6; ++tm)
-#pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-          for (int j = 0; j < 2; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]], acc[i][j],
-                                                                0, 0, 0);
-    };
-    const int nk = d.K / 16;
-    // even steps live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
-    gload(ra0, rb0, 0);
-    if (nk > 1) gload(ra1, rb1, 16);
-    lstore(0, ra0, rb0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; kt += 2) {
-      if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * 16);
-      mfma_stage(0);
-      if (kt + 1 < nk) lstore(1, ra1, rb1);
-      __syncthreads();
-      if (kt + 1 >= nk) break;
-      if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * 16);
-      mfma_stage(1);
-      if (kt + 2 < nk) lstore(0, ra0, rb0);
-      __syncthreads();
-    }
-  }
+  if (d.p_parts == 1 && d.q_parts == 1)
+    sh_tile_products<1, 1>(d, bi, bj, lds_raw, acc);
+  else if (d.q_parts == 1)
+    sh_tile_products<3, 1>(d, bi, bj, lds_raw, acc);
+  else
+    sh_tile_products<3, 3>(d, bi, bj, lds_raw, acc);
 
   // Epilogue. Accumulator element v of block (i, j) is C row 8 (v / 4) + 4 h + v % 4, column
   // lane % 32 of that 32 x 32 block (h = lane / 32). E may alias C: each element is read and then
@@ -278,7 +314,7 @@ __global__ __launch_bounds__(256) void sh_copy_in_kernel(const ShCopyDesc* __res
     const int r = rr + 4 * i;
     const int64_t gr = int64_t(ti) * kShCopyTile + r;
     const float v = (gr < d.rows && gc < d.cols) ? ld_any(d.src, gr * d.ld_src + gc, d.src_dtype) : 0.0f;
-    dst[gr * d.ld_dst + gc] = v;
+    if (dst) dst[gr * d.ld_dst + gc] = v;
     tt[r][c] = v;
   }
   if (d.dstT) {

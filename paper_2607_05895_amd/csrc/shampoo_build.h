@@ -132,6 +132,7 @@ inline ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, floa
   g.beta = beta;
   g.diag = diag;
   g.tile_begin = tiles;
+  g.p_parts = g.q_parts = 3;
   const int64_t tm = M / kShTile, tn = N / kShTile;
   tiles += int(sym ? tn * (tn + 1) / 2 : tm * tn);
   return g;

@@ -39,10 +39,12 @@ namespace {
 constexpr int kNormChunkRows = 16;
 constexpr int64_t kMaxDim = 1 << 16;
 
-// One inverse-root problem on a padded d_pad x d_pad statistic held in M.
+// One inverse-root problem on a padded d_pad x d_pad statistic, held in M or, when S is set, at S
+// (a caller buffer, row stride d_pad; M then only receives the iteration's first M).
 struct Side {
   int64_t d = 0, dp = 0;
   size_t M = 0, T2 = 0, T4 = 0, X[2] = {0, 0}, partials = 0, sc = 0, resid = 0;
+  const float* S = nullptr;
   float* out = nullptr;  // caller destination of the root (d x d, row stride d)
   bool has_out = false;  // copy the root out (decided by the call, not by the pointer value,
                          // so that the size query, which sees no pointers, builds the same ops)
@@ -64,6 +66,7 @@ void plan_side(Side& s, int64_t d, Arena& a) {
 
 struct EntryPlan {
   int64_t m, n, mp, np;
+  bool grad_bf16;
   size_t Gp, GpT, Y;
   Side L, R;
 };
@@ -79,7 +82,7 @@ void add_root_ops(Build& b, std::vector<Side*> sides, int p, int iters) {
   int nblocks = 0, itiles = 0;
   for (Side* s : sides) {
     ShNormDesc n{};
-    n.S = b.ptr<float>(s->M);
+    n.S = s->S ? s->S : b.ptr<float>(s->M);
     n.ld = s->dp;
     n.rows_pad = int32_t(s->dp);
     n.chunk_rows = kNormChunkRows;
@@ -95,7 +98,7 @@ void add_root_ops(Build& b, std::vector<Side*> sides, int p, int iters) {
     c.out = b.ptr<float>(s->sc);
     sd.push_back(c);
     ShInitDesc in{};
-    in.S = b.ptr<float>(s->M);
+    in.S = n.S;
     in.M = b.ptr<float>(s->M);
     in.X = b.ptr<float>(s->X[0]);
     in.resid = b.ptr<float>(s->resid);
@@ -229,6 +232,7 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     e.n = en[i].n;
     e.mp = rup(e.m, kShTile);
     e.np = rup(e.n, kShTile);
+    e.grad_bf16 = en[i].grad_dtype == MFSDP_BF16;
     const size_t gbytes = size_t(e.mp) * size_t(e.np) * sizeof(float);
     e.Gp = a.take(gbytes);
     e.GpT = a.take(gbytes);
@@ -238,6 +242,11 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     e.L.out = en[i].PL;
     e.R.out = en[i].PR;
     e.L.has_out = e.R.has_out = true;
+    // a side whose dimension is a multiple of the tile works on the caller's buffers where they
+    // lie (their layout is the padded one): the statistic is updated in place and the root is
+    // taken of it there, a stored preconditioner is read there; neither is copied in or out
+    if (e.m == e.mp) e.L.S = en[i].L;
+    if (e.n == e.np) e.R.S = en[i].R;
   }
   desc_at = a.off;
   const bool refresh = hp->refresh != 0;
@@ -250,16 +259,18 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     EntryPlan& e = P[size_t(i)];
     cin.push_back(copy_desc(en[i].grad, en[i].grad_dtype, b.ptr<float>(e.Gp), b.ptr<float>(e.GpT), e.m,
                             e.n, e.n, e.np, e.mp, e.mp, e.np, ct));
-    cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.L.M), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp,
-                            e.mp, ct));
-    cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.R.M), nullptr, e.n, e.n, e.n, e.np, 0, e.np,
-                            e.np, ct));
-    if (!refresh) {
+    if (!e.L.S)
+      cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.L.M), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp,
+                              e.mp, ct));
+    if (!e.R.S)
+      cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.R.M), nullptr, e.n, e.n, e.n, e.np, 0, e.np,
+                              e.np, ct));
+    if (!refresh && !e.L.S)
       cin.push_back(copy_desc(en[i].PL, kDtF32, b.ptr<float>(e.L.X[0]), nullptr, e.m, e.m, e.m, e.mp, 0,
                               e.mp, e.mp, ct));
+    if (!refresh && !e.R.S)
       cin.push_back(copy_desc(en[i].PR, kDtF32, b.ptr<float>(e.R.X[0]), nullptr, e.n, e.n, e.n, e.np, 0,
                               e.np, e.np, ct));
-    }
   }
   b.op(kOpCopyIn, cin, ct);
 
@@ -269,16 +280,22 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   std::stable_sort(order.begin(), order.end(), [](const EntryPlan* x, const EntryPlan* y) {
     return std::max(x->mp, x->np) > std::max(y->mp, y->np);
   });
+  // a bf16 gradient is exact in one bf16 part: the statistics take one product, P_L G three
+  auto stat = [&](const Side& s, float* caller) { return s.S ? caller : b.ptr<float>(s.M); };
   std::vector<ShGemmDesc> gs;
   int gt = 0;
   for (EntryPlan* ep : order) {
     EntryPlan& e = *ep;
-    gs.push_back(gemm_desc(b.ptr<float>(e.Gp), b.ptr<float>(e.Gp), b.ptr<float>(e.L.M), b.ptr<float>(e.L.M),
-                           e.np, e.np, e.mp, e.mp, e.mp, e.mp, e.np, 1, float(hp->weight),
-                           float(hp->beta), 0.0f, gt));
-    gs.push_back(gemm_desc(b.ptr<float>(e.GpT), b.ptr<float>(e.GpT), b.ptr<float>(e.R.M),
-                           b.ptr<float>(e.R.M), e.mp, e.mp, e.np, e.np, e.np, e.np, e.mp, 1,
-                           float(hp->weight), float(hp->beta), 0.0f, gt));
+    const mfsdp_shampoo_entry& c = en[ep - P.data()];
+    const int gparts = e.grad_bf16 ? 1 : 3;
+    float* Ls = stat(e.L, c.L);
+    float* Rs = stat(e.R, c.R);
+    gs.push_back(gemm_desc(b.ptr<float>(e.Gp), b.ptr<float>(e.Gp), Ls, Ls, e.np, e.np, e.mp, e.mp, e.mp, e.mp,
+                           e.np, 1, float(hp->weight), float(hp->beta), 0.0f, gt));
+    gs.back().p_parts = gs.back().q_parts = gparts;
+    gs.push_back(gemm_desc(b.ptr<float>(e.GpT), b.ptr<float>(e.GpT), Rs, Rs, e.mp, e.mp, e.np, e.np, e.np, e.np,
+                           e.mp, 1, float(hp->weight), float(hp->beta), 0.0f, gt));
+    gs.back().p_parts = gs.back().q_parts = gparts;
   }
   b.op(kOpGemm, gs, gt);
 
@@ -286,10 +303,12 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   ct = 0;
   for (int64_t i = 0; i < count; ++i) {
     EntryPlan& e = P[size_t(i)];
-    cst.push_back(copy_desc(b.ptr<float>(e.L.M), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m,
-                            e.m, ct));
-    cst.push_back(copy_desc(b.ptr<float>(e.R.M), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n,
-                            e.n, ct));
+    if (!e.L.S)
+      cst.push_back(copy_desc(b.ptr<float>(e.L.M), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m,
+                              e.m, ct));
+    if (!e.R.S)
+      cst.push_back(copy_desc(b.ptr<float>(e.R.M), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n,
+                              e.n, ct));
   }
   b.op(kOpCopyOut, cst, ct);
 
@@ -306,10 +325,15 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   int ty = 0, tu = 0;
   for (EntryPlan* ep : order) {
     EntryPlan& e = *ep;
-    gy.push_back(gemm_desc(b.ptr<float>(e.L.X[fin]), b.ptr<float>(e.GpT), nullptr, b.ptr<float>(e.Y),
-                           e.mp, e.mp, 0, e.np, e.mp, e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
-    gu.push_back(gemm_desc(b.ptr<float>(e.Y), b.ptr<float>(e.R.X[fin]), nullptr, b.ptr<float>(e.Gp),
-                           e.np, e.np, 0, e.np, e.mp, e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
+    const size_t i = size_t(ep - P.data());
+    // the preconditioners: this step's roots, or the stored ones (read where they lie, or copied)
+    const float* pl = (!refresh && e.L.S) ? en[i].PL : b.ptr<float>(e.L.X[fin]);
+    const float* pr = (!refresh && e.R.S) ? en[i].PR : b.ptr<float>(e.R.X[fin]);
+    gy.push_back(gemm_desc(pl, b.ptr<float>(e.GpT), nullptr, b.ptr<float>(e.Y), e.mp, e.mp, 0, e.np, e.mp,
+                           e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
+    if (e.grad_bf16) gy.back().q_parts = 1;
+    gu.push_back(gemm_desc(b.ptr<float>(e.Y), pr, nullptr, b.ptr<float>(e.Gp), e.np, e.np, 0, e.np, e.mp,
+                           e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
   }
   b.op(kOpGemm, gy, ty);
   b.op(kOpGemm, gu, tu);
@@ -345,10 +369,14 @@ size_t build_root(int64_t d, int p, int iters, const float* a, float* out, char*
   s.out = out;
   s.has_out = true;
   desc_at = ar.off;
-  std::vector<ShCopyDesc> cin;
-  int ct = 0;
-  cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.M), nullptr, d, d, d, s.dp, 0, s.dp, s.dp, ct));
-  b.op(kOpCopyIn, cin, ct);
+  if (d == s.dp) {
+    s.S = a;  // read where it lies
+  } else {
+    std::vector<ShCopyDesc> cin;
+    int ct = 0;
+    cin.push_back(copy_desc(a, kDtF32, b.ptr<float>(s.M), nullptr, d, d, d, s.dp, 0, s.dp, s.dp, ct));
+    b.op(kOpCopyIn, cin, ct);
+  }
   std::vector<Side*> sides{&s};
   add_root_ops(b, sides, p, iters);
   return desc_at + al(b.h.size());

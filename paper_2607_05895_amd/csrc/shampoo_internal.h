@@ -45,10 +45,15 @@ struct ShGemmDesc {
   float* resid_out;      // max |C - I| over the real block (rows, cols < valid), atomic max
   int32_t copy_on_skip;
   int32_t valid;
+  // parts of the bf16 split per operand: 1 when every value of the operand is a bf16 number (a
+  // bf16 gradient widened to fp32, with zero padding), so that the products with its zero mid and
+  // lo parts are dropped; anything else is 3. Honoured for (1, 1) and (any, 1).
+  int32_t p_parts, q_parts;
 };
 
 // Boundary copies over 64 x 64 tiles of a padded rows_pad x cols_pad domain.
-// in  (dir 0): dst[r][c] = src[r][c] inside rows x cols, 0 elsewhere; optional dstT[c][r] too.
+// in  (dir 0): dst[r][c] = src[r][c] inside rows x cols, 0 elsewhere; optional dstT[c][r] too
+//              (dst may be null when dstT is set).
 // out (dir 1): dst (caller, rows x cols fp32, row stride ld_dst) = src (padded fp32) inside.
 struct ShCopyDesc {
   const void* src;

@@ -10,12 +10,14 @@
 //
 // Every product is an NT product C = alpha P Q^T (+ beta E) on the Shampoo GEMM, over padded
 // row-major buffers (mp, np = m, n rounded up to 128), grouped over the entries:
-//   X1      = Q_L^T [G | M]      P = Q_L^T,  Q = [G^T ; M^T]        (mp x 2np, K = mp)
+//   X1      = Q_L^T [G | M]      P = Q_L^T,  Q = [G^T ; M^T]        (two mp x np, K = mp)
 //   [G'|M'] = X1 halves . Q_R    P = X1 half, Q = Q_R^T              (two mp x np, K = np)
 //   Z       = Q_L N'             P = Q_L,    Q = N'^T               (mp x np, K = mp)
 //   N       = Z Q_R^T            P = Z,      Q = Q_R                (mp x np, K = np)
 //   L, R statistics              P = Q = G (sym, K = np), P = Q = G^T (sym, K = mp)
 //   refresh S^T = Q_L^T L        P = Q_L^T,  Q = L                  (mp x mp, K = mp)
+// A bf16 gradient widened to fp32 is a one-part operand of the split-bf16 GEMM (its mid and lo
+// parts are zero): the statistics then take one bf16 product per step, Q_L^T G three.
 // The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
 // with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
 // block, with S held transposed (each column of S one contiguous row) and Q accumulated from the
@@ -70,16 +72,22 @@ struct Prod {
   int64_t ldp, ldq, lde, ldc, M, N, K;
   int sym;
   float alpha, beta;
+  int pparts = 3, qparts = 3;  // bf16 parts of P and Q (1: the operand's values are bf16 numbers)
 };
 
 void add_gemm(Build& b, std::vector<Prod> ps) {
-  // longest tiles (largest K) first: the hardware dispatches blocks in order
-  std::stable_sort(ps.begin(), ps.end(), [](const Prod& x, const Prod& y) { return x.K > y.K; });
+  // longest tiles first (K times the bf16 products per step; a one-part product is load-bound at
+  // about a third of the six-product time): the hardware dispatches blocks in order
+  auto cost = [](const Prod& x) { return x.K * (x.pparts == 1 && x.qparts == 1 ? 2 : x.qparts == 1 ? 3 : 6); };
+  std::stable_sort(ps.begin(), ps.end(), [&](const Prod& x, const Prod& y) { return cost(x) > cost(y); });
   std::vector<ShGemmDesc> gs;
   int gt = 0;
-  for (const Prod& p : ps)
+  for (const Prod& p : ps) {
     gs.push_back(gemm_desc(p.P, p.Q, p.E, p.C, p.ldp, p.ldq, p.lde, p.ldc, p.M, p.N, p.K, p.sym, p.alpha,
                            p.beta, 0.0f, gt));
+    gs.back().p_parts = p.pparts;
+    gs.back().q_parts = p.qparts;
+  }
   b.op(kOpGemm, gs, gt);
 }
 
@@ -231,6 +239,10 @@ constexpr size_t kNone = ~size_t(0);
 struct SoapPlan {
   int64_t m = 0, n = 0, mp = 0, np = 0;
   bool left = true, right = true;
+  // a side with a basis whose length is a multiple of the tile reads and updates the caller's
+  // statistic where it lies and reads the caller's basis there (no copy in or out; the basis is
+  // still copied transposed)
+  bool lin = false, rin = false;
   size_t Gp = kNone, GMt = kNone, X1 = 0, GMr = 0, NpT = kNone, QLp = kNone, QLt = kNone, QRp = kNone,
          QRt = kNone, Lp = kNone, Rp = kNone;
   QrSide L, R;
@@ -299,6 +311,8 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     e.right = e.n <= maxd;
     e.mp = rup(e.m, kShTile);
     e.np = rup(e.n, kShTile);
+    e.lin = e.left && e.m == e.mp;
+    e.rin = e.right && e.n == e.np;
     const size_t f = sizeof(float), mn = size_t(e.mp) * size_t(e.np) * f;
     if (e.left) e.Gp = a.take(mn);               // G for the left statistic
     if (e.left || e.right) e.GMt = a.take(2 * mn);  // [G^T ; M^T]: left product, right statistic
@@ -330,6 +344,11 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
   }
   desc_at = a.off;
   auto fp = [&](size_t off) { return off == kNone ? nullptr : b.ptr<float>(off); };
+  // statistic and basis (row-major) of each side: the caller's buffers or their padded copies
+  auto Lb = [&](const SoapPlan& e) { return e.lin ? en[&e - P.data()].L : b.ptr<float>(e.Lp); };
+  auto Rb = [&](const SoapPlan& e) { return e.rin ? en[&e - P.data()].R : b.ptr<float>(e.Rp); };
+  auto QLb = [&](const SoapPlan& e) { return e.lin ? en[&e - P.data()].QL : b.ptr<float>(e.QLp); };
+  auto QRb = [&](const SoapPlan& e) { return e.rin ? en[&e - P.data()].QR : b.ptr<float>(e.QRp); };
 
   std::vector<ShCopyDesc> cin;
   std::vector<SoapPrepDesc> prep;
@@ -337,14 +356,16 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
     if (e.left) {
-      cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.Lp), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp, e.mp, ct));
-      cin.push_back(copy_desc(en[i].QL, kDtF32, b.ptr<float>(e.QLp), b.ptr<float>(e.QLt), e.m, e.m, e.m, e.mp,
-                              e.mp, e.mp, e.mp, ct));
+      if (!e.lin)
+        cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.Lp), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp, e.mp, ct));
+      cin.push_back(copy_desc(en[i].QL, kDtF32, e.lin ? nullptr : b.ptr<float>(e.QLp), b.ptr<float>(e.QLt), e.m, e.m,
+                              e.m, e.mp, e.mp, e.mp, e.mp, ct));
     }
     if (e.right) {
-      cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.Rp), nullptr, e.n, e.n, e.n, e.np, 0, e.np, e.np, ct));
-      cin.push_back(copy_desc(en[i].QR, kDtF32, b.ptr<float>(e.QRp), b.ptr<float>(e.QRt), e.n, e.n, e.n, e.np,
-                              e.np, e.np, e.np, ct));
+      if (!e.rin)
+        cin.push_back(copy_desc(en[i].R, kDtF32, b.ptr<float>(e.Rp), nullptr, e.n, e.n, e.n, e.np, 0, e.np, e.np, ct));
+      cin.push_back(copy_desc(en[i].QR, kDtF32, e.rin ? nullptr : b.ptr<float>(e.QRp), b.ptr<float>(e.QRt), e.n, e.n,
+                              e.n, e.np, e.np, e.np, e.np, ct));
     }
     SoapPrepDesc d{};
     d.grad = en[i].grad;
@@ -377,22 +398,27 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     float* X1 = b.ptr<float>(e.X1);
     float* GMr = b.ptr<float>(e.GMr);
     const int64_t mp = e.mp, np = e.np;
+    // a bf16 gradient (widened exactly, zero padded) is one bf16 part: one product per statistic
+    const int gparts = en[&e - P.data()].grad_dtype == MFSDP_BF16 ? 1 : 3;
     if (e.left) {
       const float* GMt = b.ptr<float>(e.GMt);
       const float* Gp = b.ptr<float>(e.Gp);
-      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, 2 * np, mp, 0, 1.0f, 0.0f});
+      // the G half of Q_L^T [G | M] has a one-part Q when the gradient is bf16
+      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, np, mp, 0, 1.0f, 0.0f, 3,
+                        gparts});
+      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt + np * mp, nullptr, X1 + np, mp, mp, 0, 2 * np, mp, np, mp, 0,
+                        1.0f, 0.0f});
       // the statistics read only G and G^T: they join the first launch
-      p1.push_back(Prod{Gp, Gp, b.ptr<float>(e.Lp), b.ptr<float>(e.Lp), np, np, mp, mp, mp, mp, np, 1, ws_, bs_});
-      p3.push_back(Prod{b.ptr<float>(e.QLp), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f,
-                        0.0f});
+      p1.push_back(Prod{Gp, Gp, Lb(e), Lb(e), np, np, mp, mp, mp, mp, np, 1, ws_, bs_, gparts, gparts});
+      p3.push_back(Prod{QLb(e), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f, 0.0f});
     }
     if (e.right) {
       const float* GMt = b.ptr<float>(e.GMt);
-      p1.push_back(Prod{GMt, GMt, b.ptr<float>(e.Rp), b.ptr<float>(e.Rp), mp, mp, np, np, np, np, mp, 1, ws_, bs_});
+      p1.push_back(Prod{GMt, GMt, Rb(e), Rb(e), mp, mp, np, np, np, np, mp, 1, ws_, bs_, gparts, gparts});
       for (int h = 0; h < 2; ++h)
         p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np,
                           np, 0, 1.0f, 0.0f});
-      p4.push_back(Prod{X1, b.ptr<float>(e.QRp), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
+      p4.push_back(Prod{X1, QRb(e), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
     }
   }
   if (!p1.empty()) add_gemm(b, p1);
@@ -443,9 +469,9 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
   ct = 0;
   for (int64_t i = 0; i < count; ++i) {
     SoapPlan& e = P[size_t(i)];
-    if (e.left)
+    if (e.left && !e.lin)
       cst.push_back(copy_desc(b.ptr<float>(e.Lp), kDtF32, en[i].L, nullptr, e.m, e.m, e.mp, e.m, 0, e.m, e.m, ct));
-    if (e.right)
+    if (e.right && !e.rin)
       cst.push_back(copy_desc(b.ptr<float>(e.Rp), kDtF32, en[i].R, nullptr, e.n, e.n, e.np, e.n, 0, e.n, e.n, ct));
   }
   if (!cst.empty()) b.op(kOpCopyOut, cst, ct);
@@ -455,12 +481,12 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     std::vector<QrSide*> sides;
     for (SoapPlan& e : P) {
       if (e.left) {
-        ps.push_back(Prod{b.ptr<float>(e.QLt), b.ptr<float>(e.Lp), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
+        ps.push_back(Prod{b.ptr<float>(e.QLt), Lb(e), nullptr, b.ptr<float>(e.QLp), e.mp, e.mp, 0, e.mp,
                           e.mp, e.mp, e.mp, 0, 1.0f, 0.0f});
         sides.push_back(&e.L);
       }
       if (e.right) {
-        ps.push_back(Prod{b.ptr<float>(e.QRt), b.ptr<float>(e.Rp), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
+        ps.push_back(Prod{b.ptr<float>(e.QRt), Rb(e), nullptr, b.ptr<float>(e.QRp), e.np, e.np, 0, e.np,
                           e.np, e.np, e.np, 0, 1.0f, 0.0f});
         sides.push_back(&e.R);
       }

@@ -93,6 +93,8 @@ def test_inverse_root_matches_oracle(native, d, p):
     ref = OS.inverse_root(a.astype(np.float64), p, 1e-9, 1e-6)
     err = rel_fro(from_dev(out), ref)
     assert err <= 1e-4, err
+    # a tile-multiple d is read where it lies: still read only
+    np.testing.assert_array_equal(from_dev(ad), a)
 
 
 def test_inverse_root_of_diagonal_and_scaled_identity(native):
@@ -227,12 +229,13 @@ def test_shampoo_grouped_mixed_shapes_two_steps_ema(native):
 
 def test_shampoo_stale_preconditioners(native):
     """refresh = 0: the stored P_L, P_R (seeded SPD inputs, not computed by the library) are used
-    as given and left unchanged, while the statistics still accumulate."""
+    as given and left unchanged, while the statistics still accumulate. Sides whose dimension is a
+    multiple of 128 (read in place) and others (copied) in one call, bf16 and fp32 gradients."""
     _say("shampoo stale preconditioners")
     rng = np.random.default_rng(4000)
     mats = []
-    for (m, n) in [(65, 129), (256, 512), (300, 300)]:
-        x = _Mat(rng, m, n, synth.BF16, synth.BF16).device()
+    for i, (m, n) in enumerate([(65, 129), (256, 512), (300, 300), (384, 200), (130, 256)]):
+        x = _Mat(rng, m, n, synth.BF16, synth.F32 if i >= 3 else synth.BF16).device()
         x.PL = _spd(rng, m, 10.0)
         x.PR = _spd(rng, n, 10.0)
         x.dPL.copy_(to_dev(x.PL.astype(np.float32), synth.F32))
@@ -347,8 +350,9 @@ def test_inverse_root_iteration_cap_beyond_convergence(native, p):
 def test_shampoo_benchmark_configuration_full_size(native):
     """The configuration bench.py --shampoo times: the GPT-2-small share's 12 matrices in one call,
     EMA statistics (beta 0.95, weight 0.05), ridge 1e-12 + 1e-6 ||S||_F, 20 root iterations, bf16
-    parameters and gradients; every matrix against the oracle (two steps, so the second sees EMA
-    statistics)."""
+    parameters and gradients; every matrix against the oracle (two refresh steps, so the second sees
+    EMA statistics, then a stale step on a third gradient, as timed too)."""
+    import torch
     _say("shampoo benchmark configuration")
     wl = synth.workload(2)
     rng = np.random.default_rng(8000)
@@ -367,3 +371,19 @@ def test_shampoo_benchmark_configuration_full_size(native):
             _oracle_step(x, hpo)
     for x in mats:
         _check(x, hpo)
+    # the stale step: the preconditioners are the oracle's fp32-rounded ones as stored on the device
+    hpn2, hpo2 = _hp(native, lr=1e-3, weight_decay=0.01, beta=0.95, weight=0.05, refresh=False)
+    keep = []
+    for x in mats:
+        x.g = synth.random_muon_tensors(rng, x.m, x.n, x.pdt, x.gdt, g_std=0.02).grad
+        x.dg.copy_(to_dev(x.g, x.gdt))
+        x.PL = from_dev(x.dPL).astype(np.float64)
+        x.PR = from_dev(x.dPR).astype(np.float64)
+        keep.append((x.dPL.clone(), x.dPR.clone()))
+    native.shampoo_step_t(ents, hpn2, ws)
+    _sync()
+    for x, (kl, kr) in zip(mats, keep):
+        _oracle_step(x, hpo2)
+        assert rel_fro(from_dev(x.dU), x.U_or) <= 1e-5
+        assert torch.equal(kl, x.dPL) and torch.equal(kr, x.dPR)
+        _check(x, hpo2)

@@ -377,7 +377,9 @@ def test_soap_step_with_a_4096_side(native):
 def test_soap_benchmark_configuration_full_size(native):
     """The configuration bench.py times: the GPT-2-small share's 12 matrices in one call, bf16
     parameters and gradients, full-rank statistics and random orthogonal bases, refresh on; every
-    matrix against the oracle."""
+    matrix against the oracle. Then a step without refresh on a new gradient (also timed): the
+    bases, read where they lie, stay unchanged."""
+    import torch
     _say("soap benchmark configuration")
     wl = synth.workload(2)
     rng = np.random.default_rng(9500)
@@ -390,6 +392,20 @@ def test_soap_benchmark_configuration_full_size(native):
     for x in mats:
         _oracle_step(x, step, hpo)
         _check(x, hpo)
+    hpn2, hpo2, step2 = _hp(native, lr=3e-3, weight_decay=0.01, step=6, refresh=False)
+    keep = []
+    for x in mats:
+        x.g = synth.random_muon_tensors(rng, x.m, x.n, x.pdt, x.gdt, g_std=0.02).grad
+        x.dg.copy_(to_dev(x.g, x.gdt))
+        x.QL = from_dev(x.dQL).astype(np.float64)   # the refreshed bases as the device stores them
+        x.QR = from_dev(x.dQR).astype(np.float64)
+        keep.append((x.dQL.clone(), x.dQR.clone()))
+    native.soap_step_t(ents, hpn2, ws)
+    _sync()
+    for x, (kl, kr) in zip(mats, keep):
+        _oracle_step(x, step2, hpo2)
+        _check(x, hpo2)
+        assert torch.equal(kl, x.dQL) and torch.equal(kr, x.dQR)
 
 
 # ------------------------------------------------------------------ one-sided preconditioning
