@@ -72,101 +72,114 @@ constexpr int kShStage = 6 * kShPlane;  // both operands of one K step, three pl
 // parts of P and PB parts of Q (3: fp32 split into hi + mid + lo; 1: an operand whose values are
 // bf16 numbers, so that its mid and lo parts are zero and the products with them are dropped,
 // which leaves the accumulated sums unchanged).
-// 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The next K step's
-// global loads are held in registers during the current step's products (LDS double buffer).
-// The products run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32
-// accuracy. K steps of 16; when a step is staged into LDS every element is split once into
-// hi + mid + lo bf16 parts (three planes per operand, 24 KiB per stage); a lane's fragment is 8
-// consecutive k of one row from each plane, and the six partial products above 2^-24 relative are
-// accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi; the dropped mid.lo, lo.mid, lo.lo are
-// below 2^-32). Six bf16 MFMAs per 16 k take 192 cycles against 512 for the fp32 MFMA.
-template <int PA, int PB>
+// 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The products
+// run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32 accuracy: when a
+// K step of 16 is staged into LDS every element is split once into hi + mid + lo bf16 parts (three
+// planes per operand); a lane's fragment is 8 consecutive k of one row from each plane, and the
+// six partial products above 2^-24 relative are accumulated (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid,
+// hi.hi; the dropped mid.lo, lo.mid, lo.lo are below 2^-32). Six bf16 MFMAs per 16 k take 192
+// cycles against 512 for the fp32 MFMA.
+// A stage holds KS K steps (KS (PA + PB) planes, at most six: 24 KiB); the LDS is double
+// buffered, and two register sets hold the global loads of the next two stages, so that the loads
+// of stage k + 2 are issued while stage k multiplies and stage k + 1's loads (issued a stage
+// earlier) are split into LDS. Few products per step (one-part operands) take several steps per
+// stage, so that a barrier and the load latency are spread over more MFMAs.
+template <int PA, int PB, int KS>
 __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, int bj, uint8_t* lds_raw,
                                                  f32x16 (&acc)[2][2]) {
+  static_assert(KS * (PA + PB) <= 6, "a stage holds at most six planes");
   const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
   const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wr = w >> 1, wc = w & 1;
   const int fr = lane & 31, fh = lane >> 5;
-  // staging: thread t loads k 4 (t & 3) .. + 3 of rows t / 4 and t / 4 + 64 of both operands
+  // staging: thread t loads k 4 (t & 3) .. + 3 of each step of rows t / 4 and t / 4 + 64 of both
+  // operands
   const int lrow = t >> 2, lch = t & 3;
-  // two register sets, so that the loads of step k + 2 are issued while step k multiplies and
-  // step k + 1's loads (issued a step earlier) are split into LDS
-  f32x4 ra0[2], rb0[2], ra1[2], rb1[2];
-  auto gload = [&](f32x4 (&ra)[2], f32x4 (&rb)[2], int k0) {
+  f32x4 ra0[KS][2], rb0[KS][2], ra1[KS][2], rb1[KS][2];
+  auto gload = [&](f32x4 (&ra)[KS][2], f32x4 (&rb)[KS][2], int k0) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = lrow + 64 * j;
-      ra[j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + lch * 4);
-      rb[j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + lch * 4);
-    }
-  };
-  // plane (operand o, part p) of stage s is plane 3 o + p; the 8-byte piece of row r holding
-  // k 4 lch .. + 3
-  auto lstore = [&](int s, const f32x4 (&ra)[2], const f32x4 (&rb)[2]) {
+    for (int u = 0; u < KS; ++u)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int r = lrow + 64 * j;
-      const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
-      uint8_t* base = lds_raw + s * kShStage;
-      u32x2 h, m, l;
-      if (PA == 3) {
-        split3x4(ra[j], h, m, l);
-        *reinterpret_cast<u32x2*>(base + 0 * kShPlane + off) = h;
-        *reinterpret_cast<u32x2*>(base + 1 * kShPlane + off) = m;
-        *reinterpret_cast<u32x2*>(base + 2 * kShPlane + off) = l;
-      } else {
-        *reinterpret_cast<u32x2*>(base + 0 * kShPlane + off) = split1x4(ra[j]);
+      for (int j = 0; j < 2; ++j) {
+        const int r = lrow + 64 * j;
+        ra[u][j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + 16 * u + lch * 4);
+        rb[u][j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + 16 * u + lch * 4);
       }
-      if (PB == 3) {
-        split3x4(rb[j], h, m, l);
-        *reinterpret_cast<u32x2*>(base + 3 * kShPlane + off) = h;
-        *reinterpret_cast<u32x2*>(base + 4 * kShPlane + off) = m;
-        *reinterpret_cast<u32x2*>(base + 5 * kShPlane + off) = l;
-      } else {
-        *reinterpret_cast<u32x2*>(base + 3 * kShPlane + off) = split1x4(rb[j]);
-      }
-    }
   };
-  auto frag = [&](int s, int plane, int r) {
-    return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kShStage + plane * kShPlane + split_slot(r, fh) * 16);
+  // plane (step u, operand o, part p) of a stage is u (PA + PB) + o PA + p; the 8-byte piece of
+  // row r holding k 4 lch .. + 3
+  auto plane = [](int u, int o, int p) { return u * (PA + PB) + o * PA + p; };
+  auto lstore = [&](int s, const f32x4 (&ra)[KS][2], const f32x4 (&rb)[KS][2]) {
+#pragma unroll
+    for (int u = 0; u < KS; ++u)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int r = lrow + 64 * j;
+        const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
+        uint8_t* base = lds_raw + s * kShStage + off;
+        u32x2 h, m, l;
+        if (PA == 3) {
+          split3x4(ra[u][j], h, m, l);
+          *reinterpret_cast<u32x2*>(base + plane(u, 0, 0) * kShPlane) = h;
+          *reinterpret_cast<u32x2*>(base + plane(u, 0, 1) * kShPlane) = m;
+          *reinterpret_cast<u32x2*>(base + plane(u, 0, 2) * kShPlane) = l;
+        } else {
+          *reinterpret_cast<u32x2*>(base + plane(u, 0, 0) * kShPlane) = split1x4(ra[u][j]);
+        }
+        if (PB == 3) {
+          split3x4(rb[u][j], h, m, l);
+          *reinterpret_cast<u32x2*>(base + plane(u, 1, 0) * kShPlane) = h;
+          *reinterpret_cast<u32x2*>(base + plane(u, 1, 1) * kShPlane) = m;
+          *reinterpret_cast<u32x2*>(base + plane(u, 1, 2) * kShPlane) = l;
+        } else {
+          *reinterpret_cast<u32x2*>(base + plane(u, 1, 0) * kShPlane) = split1x4(rb[u][j]);
+        }
+      }
+  };
+  auto frag = [&](int s, int pl, int r) {
+    return *reinterpret_cast<const bf16x8_t*>(lds_raw + s * kShStage + pl * kShPlane + split_slot(r, fh) * 16);
   };
   // parts 0, 1, 2 = hi, mid, lo; the six products (lo.hi, hi.lo, mid.mid, mid.hi, hi.mid, hi.hi)
   // term by term over the four blocks, so that consecutive MFMAs use different accumulators
   auto mfma_stage = [&](int s) {
-    bf16x8_t af[2][PA], bf[2][PB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int u = 0; u < KS; ++u) {
+      bf16x8_t af[2][PA], bf[2][PB];
 #pragma unroll
-      for (int pt = 0; pt < PA; ++pt) af[i][pt] = frag(s, pt, wr * 64 + i * 32 + fr);
+      for (int i = 0; i < 2; ++i) {
 #pragma unroll
-      for (int pt = 0; pt < PB; ++pt) bf[i][pt] = frag(s, 3 + pt, wc * 64 + i * 32 + fr);
-    }
-    constexpr int kTerm[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
+        for (int pt = 0; pt < PA; ++pt) af[i][pt] = frag(s, plane(u, 0, pt), wr * 64 + i * 32 + fr);
 #pragma unroll
-    for (int tm = 0; tm < 6; ++tm) {
-      if (kTerm[tm][0] >= PA || kTerm[tm][1] >= PB) continue;
+        for (int pt = 0; pt < PB; ++pt) bf[i][pt] = frag(s, plane(u, 1, pt), wc * 64 + i * 32 + fr);
+      }
+      constexpr int kTerm[6][2] = {{2, 0}, {0, 2}, {1, 1}, {1, 0}, {0, 1}, {0, 0}};
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int tm = 0; tm < 6; ++tm) {
+        if (kTerm[tm][0] >= PA || kTerm[tm][1] >= PB) continue;
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]],
-                                                              acc[i][j], 0, 0, 0);
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 2; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i][kTerm[tm][0]], bf[j][kTerm[tm][1]],
+                                                                acc[i][j], 0, 0, 0);
+      }
     }
   };
-  const int nk = d.K / 16;
-  // even steps live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
+  constexpr int kStep = 16 * KS;  // k per stage (K is a multiple of 128)
+  const int nk = d.K / kStep;
+  // even stages live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
   gload(ra0, rb0, 0);
-  if (nk > 1) gload(ra1, rb1, 16);
+  if (nk > 1) gload(ra1, rb1, kStep);
   lstore(0, ra0, rb0);
   __syncthreads();
   for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * 16);
+    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * kStep);
     mfma_stage(0);
     if (kt + 1 < nk) lstore(1, ra1, rb1);
     __syncthreads();
     if (kt + 1 >= nk) break;
-    if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * 16);
+    if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * kStep);
     mfma_stage(1);
     if (kt + 2 < nk) lstore(0, ra0, rb0);
     __syncthreads();
@@ -223,11 +236,11 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
   if (d.p_parts == 1 && d.q_parts == 1)
-    sh_tile_products<1, 1>(d, bi, bj, lds_raw, acc);
+    sh_tile_products<1, 1, 2>(d, bi, bj, lds_raw, acc);
   else if (d.q_parts == 1)
-    sh_tile_products<3, 1>(d, bi, bj, lds_raw, acc);
+    sh_tile_products<3, 1, 1>(d, bi, bj, lds_raw, acc);
   else
-    sh_tile_products<3, 3>(d, bi, bj, lds_raw, acc);
+    sh_tile_products<3, 3, 1>(d, bi, bj, lds_raw, acc);
 
   // Epilogue. Accumulator element v of block (i, j) is C row 8 (v / 4) + 4 h + v % 4, column
   // lane % 32 of that 32 x 32 block (h = lane / 32). E may alias C: each element is read and then
