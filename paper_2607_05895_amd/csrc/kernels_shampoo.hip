@@ -88,23 +88,31 @@ template <int PA, int PB, int KS>
 __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, int bj, uint8_t* lds_raw,
                                                  f32x16 (&acc)[2][2]) {
   static_assert(KS * (PA + PB) <= 6, "a stage holds at most six planes");
-  const g_cf32* __restrict__ P = (const g_cf32*)(d.P) + int64_t(bi) * kShTile * d.ldp;
-  const g_cf32* __restrict__ Q = (const g_cf32*)(d.Q) + int64_t(bj) * kShTile * d.ldq;
+  typedef __attribute__((address_space(1))) const uint8_t g_cu8;
+  // tile rows of both operands (uniform) and this thread's byte offsets into them (32-bit: a tile
+  // spans at most 128 rows of 65536 floats)
+  g_cu8* P = (g_cu8*)(d.P) + int64_t(bi) * kShTile * d.ldp * 4;
+  g_cu8* Q = (g_cu8*)(d.Q) + int64_t(bj) * kShTile * d.ldq * 4;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wr = w >> 1, wc = w & 1;
   const int fr = lane & 31, fh = lane >> 5;
   // staging: thread t loads k 4 (t & 3) .. + 3 of each step of rows t / 4 and t / 4 + 64 of both
   // operands
   const int lrow = t >> 2, lch = t & 3;
+  uint32_t po[2], qo[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    po[j] = uint32_t((lrow + 64 * j) * d.ldp + lch * 4) * 4u;
+    qo[j] = uint32_t((lrow + 64 * j) * d.ldq + lch * 4) * 4u;
+  }
   f32x4 ra0[KS][2], rb0[KS][2], ra1[KS][2], rb1[KS][2];
   auto gload = [&](f32x4 (&ra)[KS][2], f32x4 (&rb)[KS][2], int k0) {
 #pragma unroll
     for (int u = 0; u < KS; ++u)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        const int r = lrow + 64 * j;
-        ra[u][j] = *(const g_cf32x4*)(P + int64_t(r) * d.ldp + k0 + 16 * u + lch * 4);
-        rb[u][j] = *(const g_cf32x4*)(Q + int64_t(r) * d.ldq + k0 + 16 * u + lch * 4);
+        ra[u][j] = *(const g_cf32x4*)(P + (k0 + 16 * u) * 4 + po[j]);
+        rb[u][j] = *(const g_cf32x4*)(Q + (k0 + 16 * u) * 4 + qo[j]);
       }
   };
   // plane (step u, operand o, part p) of a stage is u (PA + PB) + o PA + p; the 8-byte piece of
@@ -166,24 +174,47 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
       }
     }
   };
-  constexpr int kStep = 16 * KS;  // k per stage (K is a multiple of 128)
+  constexpr int kStep = 16 * KS;  // k per stage
+  constexpr int kTerms = PA == 3 && PB == 3 ? 6 : PA == 3 || PB == 3 ? 3 : 1;
+  constexpr int kMfma = KS * 4 * kTerms;  // MFMAs per stage and wave
+  constexpr int kSplitValu = KS * 2 * ((PA == 3 ? 22 : 2) + (PB == 3 ? 22 : 2));  // split VALU per stage, about
+  // one stage's products on LDS buffer mb while the next stage's loads (set) are split into buffer
+  // sb: with split operands the split's vector instructions and LDS stores are interleaved with the
+  // MFMAs (they are independent), so that a wave's MFMA pipe and vector ALU work at the same time
+  // (one-part products have little to interleave and run faster in program order)
+  auto stage = [&](int mb, int sb, const f32x4 (&ra)[KS][2], const f32x4 (&rb)[KS][2]) {
+    mfma_stage(mb);
+    lstore(sb, ra, rb);
+    if constexpr (kTerms > 1) {
+      constexpr int kV = (kSplitValu + kMfma - 1) / kMfma;
+#pragma unroll
+      for (int i = 0; i < kMfma; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, kV, 0);  // vector ALU
+        __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);   // LDS store
+      }
+    }
+  };
+  // K is a multiple of 128, so nk is even and at least 4: even stages live in LDS buffer 0 and
+  // register set 0, odd ones in buffer 1 and set 1, and the loads run two stages ahead
   const int nk = d.K / kStep;
-  // even stages live in LDS stage 0 and register set 0, odd ones in stage 1 and set 1
   gload(ra0, rb0, 0);
-  if (nk > 1) gload(ra1, rb1, kStep);
+  gload(ra1, rb1, kStep);
   lstore(0, ra0, rb0);
   __syncthreads();
-  for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) gload(ra0, rb0, (kt + 2) * kStep);
-    mfma_stage(0);
-    if (kt + 1 < nk) lstore(1, ra1, rb1);
+  int kt = 0;
+  for (; kt + 2 < nk; kt += 2) {
+    gload(ra0, rb0, (kt + 2) * kStep);
+    stage(0, 1, ra1, rb1);
     __syncthreads();
-    if (kt + 1 >= nk) break;
-    if (kt + 3 < nk) gload(ra1, rb1, (kt + 3) * kStep);
-    mfma_stage(1);
-    if (kt + 2 < nk) lstore(0, ra0, rb0);
+    gload(ra1, rb1, (kt + 3) * kStep);
+    stage(1, 0, ra0, rb0);
     __syncthreads();
   }
+  stage(0, 1, ra1, rb1);
+  __syncthreads();
+  mfma_stage(1);
+  __syncthreads();
 }
 
 // C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup (products as in

@@ -23,7 +23,7 @@ constexpr int kShCopyTile = 64;  // copy / init / apply tile
 constexpr float kShConvTol = 1e-5f;
 
 // C = alpha * P Q^T + beta * E + diag * I over one padded problem (P: M x K, Q: N x K, all
-// row-major with the given row strides). sym: only tiles bi <= bj are computed; each is stored at
+// row-major with the given row strides; M, N and K multiples of kShTile). sym: only tiles bi <= bj are computed; each is stored at
 // (bi, bj) and transposed at (bj, bi). E may alias C (each element is read before it is written,
 // by the same thread).
 struct ShGemmDesc {
