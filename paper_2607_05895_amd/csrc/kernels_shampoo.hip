@@ -273,52 +273,65 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
   else
     sh_tile_products<3, 3, 1>(d, bi, bj, lds_raw, acc);
 
-  // Epilogue. Accumulator element v of block (i, j) is C row 8 (v / 4) + 4 h + v % 4, column
-  // lane % 32 of that 32 x 32 block (h = lane / 32). E may alias C: each element is read and then
-  // written by the same thread; the final values stay in acc for the transposed stores.
-  // Symmetric problems are stored exactly symmetric: an upper tile is also stored transposed, and a
-  // diagonal tile keeps its upper triangle and mirrors it into the lower one (in floating point the
-  // two triangles of a product of two different symmetric matrices differ; kept, that
-  // antisymmetric part is amplified by the NT form of the iteration).
+  // Epilogue, in two passes over the tile's row halves (the waves with wr = h hold rows
+  // 64 h .. 64 h + 63). Accumulator element v of block (i, j) is row 32 i + 8 (v / 4) + 4 (lane / 32)
+  // + v % 4 of the half, column 64 wc + 32 j + lane % 32. E's half (which may alias C) is first
+  // copied into LDS by direct global->LDS loads (64 x 128 fp32 = 32 KiB, rows of 512 B), so that no
+  // store of C waits for an E load behind it; every element of E used is read before the element is
+  // written, by the same thread. The final values stay in acc for the transposed stores.
+  // Symmetric problems are stored exactly symmetric: an upper tile is also stored transposed,
+  // through a 64 x 128 LDS tile per half (element (rl, c) at rl * 128 + (c ^ rl)), and a diagonal
+  // tile keeps its upper triangle and mirrors it into the lower one (in floating point the two
+  // triangles of a product of two different symmetric matrices differ; kept, that antisymmetric
+  // part is amplified by the NT form of the iteration). The lower triangle of a diagonal tile's E
+  // may be overwritten by the first half's mirror before the second half is copied; it is not used.
+  typedef __attribute__((address_space(3))) uint8_t lds_u8;
   g_f32* C = (g_f32*)(d.C);
   const g_cf32* E = (const g_cf32*)(d.E);
   const bool diag_tile = d.sym && bi == bj;
   const int64_t r0 = int64_t(bi) * kShTile, c0 = int64_t(bj) * kShTile;
+  float* tl = reinterpret_cast<float*>(lds_raw);
   float res = 0.0f;  // max |C - I| over this thread's elements of the real block
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int h = 0; h < 2; ++h) {
+    if (h == 1 && (E || d.sym)) __syncthreads();  // the first half's LDS reads are done
+    if (E) {
+      // wave w copies rows 16 w .. 16 w + 15 of the half, two rows (1 KiB) per instruction (a
+      // uniform row base and 32-bit lane offsets)
+      typedef __attribute__((address_space(1))) const uint8_t g_cu8e;
+      g_cu8e* eb = (g_cu8e*)(E + (r0 + 64 * h + 16 * w) * d.lde + c0);
+      const uint32_t eo = uint32_t(((lane >> 5) * d.lde + 4 * (lane & 31)) * 4);
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int i = 0; i < 8; ++i)
+        __builtin_amdgcn_global_load_lds((const void*)(eb + 2 * i * d.lde * 4 + eo),
+                                         (lds_u8*)(lds_raw + (16 * w + 2 * i) * 512), 16, 0, 0);
+      __builtin_amdgcn_s_waitcnt((7 << 4) | (0xF << 8));  // vmcnt(0): this wave's copies landed
+      __syncthreads();
+    }
+    if (wr == h) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = wr * 64 + i * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
-        const int c = wc * 64 + j * 32 + fr;
-        if (diag_tile && r > c) continue;  // filled from the upper triangle below
-        const int64_t gr = r0 + r, gc = c0 + c;
-        float x = d.alpha * acc[i][j][v];
-        if (E) x += d.beta * E[gr * d.lde + gc];
-        if (gr == gc) x += d.diag;
-        C[gr * d.ldc + gc] = x;
-        acc[i][j][v] = x;
-        if (gr < d.valid && gc < d.valid) {
-          const float dv = fabsf(x - (gr == gc ? 1.0f : 0.0f));
-          res = (dv > res || dv != dv) ? dv : res;  // keeps a NaN
-        }
-      }
-  if (d.resid_out) {
-    // NaN propagates as the largest bit pattern, so a diverged side never counts as converged
-    uint32_t rb = __float_as_uint(res);
-    if (res != res) rb = 0x7fc00000u;
-    for (int o = 32; o > 0; o >>= 1) rb = max(rb, uint32_t(__shfl_xor(int(rb), o)));
-    if (lane == 0) atomicMax(reinterpret_cast<unsigned int*>(d.resid_out), rb);
-  }
-  if (d.sym) {
-    // two passes over the tile's row halves (the waves with wr = h own rows 64 h .. 64 h + 63),
-    // each through a 64 x 128 LDS tile (32 KiB): element (rl, c) at rl * 128 + (c ^ rl)
-    float* tl = reinterpret_cast<float*>(lds_raw);
+      for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      if (h == 1) __syncthreads();  // the first half's transposed reads are done
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int rl = i * 32 + 8 * (v >> 2) + 4 * fh + (v & 3);
+            const int r = 64 * h + rl, c = wc * 64 + j * 32 + fr;
+            if (diag_tile && r > c) continue;  // filled from the upper triangle below
+            const int64_t gr = r0 + r, gc = c0 + c;
+            float x = d.alpha * acc[i][j][v];
+            if (E) x += d.beta * tl[rl * kShTile + c];
+            if (gr == gc) x += d.diag;
+            C[gr * d.ldc + gc] = x;
+            acc[i][j][v] = x;
+            if (gr < d.valid && gc < d.valid) {
+              const float dv = fabsf(x - (gr == gc ? 1.0f : 0.0f));
+              res = (dv > res || dv != dv) ? dv : res;  // keeps a NaN
+            }
+          }
+    }
+    if (d.sym) {
+      if (E) __syncthreads();  // E's LDS reads are done
       if (wr == h) {
 #pragma unroll
         for (int i = 0; i < 2; ++i)
@@ -340,6 +353,13 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
         if (!diag_tile || c > r) C[(c0 + c) * d.ldc + r0 + r] = tl[lane * kShTile + (c ^ lane)];
       }
     }
+  }
+  if (d.resid_out) {
+    // NaN propagates as the largest bit pattern, so a diverged side never counts as converged
+    uint32_t rb = __float_as_uint(res);
+    if (res != res) rb = 0x7fc00000u;
+    for (int o = 32; o > 0; o >>= 1) rb = max(rb, uint32_t(__shfl_xor(int(rb), o)));
+    if (lane == 0) atomicMax(reinterpret_cast<unsigned int*>(d.resid_out), rb);
   }
 }
 
