@@ -220,9 +220,10 @@ int check_shampoo_entries(const mfsdp_shampoo_entry* en, int64_t count, bool dat
 }
 
 // Builds the whole Shampoo step for `count` entries. Returns the workspace bytes (buffers, then
-// the descriptor region at desc_at).
+// the descriptor region at desc_at). `sizing`: for the size query, which sees no pointers (every
+// side is then taken as copied: the most descriptors a step can need).
 size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_shampoo_hparams* hp,
-                     char* ws, Build& b, size_t& desc_at) {
+                     char* ws, Build& b, size_t& desc_at, bool sizing) {
   b.base = ws;
   Arena a;
   std::vector<EntryPlan> P(static_cast<size_t>(count));
@@ -243,10 +244,11 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     e.R.out = en[i].PR;
     e.L.has_out = e.R.has_out = true;
     // a side whose dimension is a multiple of the tile works on the caller's buffers where they
-    // lie (their layout is the padded one): the statistic is updated in place and the root is
-    // taken of it there, a stored preconditioner is read there; neither is copied in or out
-    if (e.m == e.mp) e.L.S = en[i].L;
-    if (e.n == e.np) e.R.S = en[i].R;
+    // lie (their layout is the padded one; 16-byte aligned, as the GEMM's vector accesses need):
+    // the statistic is updated in place and the root is taken of it there, a stored
+    // preconditioner is read there; neither is copied in or out
+    if (!sizing && e.m == e.mp && aligned(en[i].L, 16) && aligned(en[i].PL, 16)) e.L.S = en[i].L;
+    if (!sizing && e.n == e.np && aligned(en[i].R, 16) && aligned(en[i].PR, 16)) e.R.S = en[i].R;
   }
   desc_at = a.off;
   const bool refresh = hp->refresh != 0;
@@ -361,7 +363,7 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
 }
 
 size_t build_root(int64_t d, int p, int iters, const float* a, float* out, char* ws, Build& b,
-                  size_t& desc_at) {
+                  size_t& desc_at, bool sizing) {
   b.base = ws;
   Arena ar;
   Side s;
@@ -369,7 +371,7 @@ size_t build_root(int64_t d, int p, int iters, const float* a, float* out, char*
   s.out = out;
   s.has_out = true;
   desc_at = ar.off;
-  if (d == s.dp) {
+  if (!sizing && d == s.dp && aligned(a, 16)) {
     s.S = a;  // read where it lies
   } else {
     std::vector<ShCopyDesc> cin;
@@ -393,7 +395,7 @@ size_t mfsdp_shampoo_workspace_size(const mfsdp_shampoo_entry* entries, int64_t 
   if (count == 0) return 0;
   Build b;
   size_t desc_at = 0;
-  return build_shampoo(entries, count, hp, nullptr, b, desc_at);
+  return build_shampoo(entries, count, hp, nullptr, b, desc_at, true);
 }
 
 int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count, const mfsdp_shampoo_hparams* hp,
@@ -405,7 +407,7 @@ int mfsdp_shampoo_step(const mfsdp_shampoo_entry* entries, int64_t count, const 
   if (count == 0) return MFSDP_OK;
   Build b;
   size_t desc_at = 0;
-  const size_t need = build_shampoo(entries, count, hp, static_cast<char*>(workspace), b, desc_at);
+  const size_t need = build_shampoo(entries, count, hp, static_cast<char*>(workspace), b, desc_at, false);
   if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
     return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
                                              "mfsdp_shampoo_workspace_size (" + std::to_string(need) + " bytes)");
@@ -422,7 +424,7 @@ size_t mfsdp_inverse_root_workspace_size(int64_t d, int32_t p, int32_t iters) {
   if (d < 1 || d > kMaxDim || (p != 1 && p != 2 && p != 4) || iters < 1 || iters > 100) return 0;
   Build b;
   size_t desc_at = 0;
-  return build_root(d, p, iters, nullptr, nullptr, nullptr, b, desc_at);
+  return build_root(d, p, iters, nullptr, nullptr, nullptr, b, desc_at, true);
 }
 
 int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double eps, double eps_rel,
@@ -436,7 +438,7 @@ int mfsdp_inverse_root(const float* a, float* out, int64_t d, int32_t p, double 
   if (iters < 1 || iters > 100) return bad("iters must be in [1, 100]");
   Build b;
   size_t desc_at = 0;
-  const size_t need = build_root(d, p, iters, a, out, static_cast<char*>(workspace), b, desc_at);
+  const size_t need = build_root(d, p, iters, a, out, static_cast<char*>(workspace), b, desc_at, false);
   if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
     return set_last_error(MFSDP_E_WORKSPACE, "workspace NULL, not 256-byte aligned or smaller than "
                                              "mfsdp_inverse_root_workspace_size (" + std::to_string(need) + " bytes)");

@@ -239,9 +239,10 @@ constexpr size_t kNone = ~size_t(0);
 struct SoapPlan {
   int64_t m = 0, n = 0, mp = 0, np = 0;
   bool left = true, right = true;
-  // a side with a basis whose length is a multiple of the tile reads and updates the caller's
-  // statistic where it lies and reads the caller's basis there (no copy in or out; the basis is
-  // still copied transposed)
+  // a side with a basis whose length is a multiple of the tile (and whose caller buffers are
+  // 16-byte aligned, as the GEMM's vector accesses need) reads and updates the caller's statistic
+  // where it lies and reads the caller's basis there (no copy in or out; the basis is still copied
+  // transposed)
   bool lin = false, rin = false;
   size_t Gp = kNone, GMt = kNone, X1 = 0, GMr = 0, NpT = kNone, QLp = kNone, QLt = kNone, QRp = kNone,
          QRt = kNone, Lp = kNone, Rp = kNone;
@@ -297,8 +298,10 @@ int check_soap_entries(const mfsdp_soap_entry* en, int64_t count, bool data, int
   return MFSDP_OK;
 }
 
+// `sizing`: for the size query, which sees no pointers (no side is then taken as in place: the
+// most descriptors a step can need).
 size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hparams* hp, char* ws,
-                  Build& b, size_t& desc_at) {
+                  Build& b, size_t& desc_at, bool sizing) {
   b.base = ws;
   Arena a;
   const int64_t maxd = precond_limit(hp);
@@ -311,8 +314,8 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     e.right = e.n <= maxd;
     e.mp = rup(e.m, kShTile);
     e.np = rup(e.n, kShTile);
-    e.lin = e.left && e.m == e.mp;
-    e.rin = e.right && e.n == e.np;
+    e.lin = !sizing && e.left && e.m == e.mp && aligned(en[i].L, 16) && aligned(en[i].QL, 16);
+    e.rin = !sizing && e.right && e.n == e.np && aligned(en[i].R, 16) && aligned(en[i].QR, 16);
     const size_t f = sizeof(float), mn = size_t(e.mp) * size_t(e.np) * f;
     if (e.left) e.Gp = a.take(mn);               // G for the left statistic
     if (e.left || e.right) e.GMt = a.take(2 * mn);  // [G^T ; M^T]: left product, right statistic
@@ -572,7 +575,7 @@ size_t mfsdp_soap_workspace_size(const mfsdp_soap_entry* entries, int64_t count,
   if (count == 0) return 0;
   Build b;
   size_t desc_at = 0;
-  return build_soap(entries, count, hp, nullptr, b, desc_at);
+  return build_soap(entries, count, hp, nullptr, b, desc_at, true);
 }
 
 int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_soap_hparams* hp,
@@ -584,7 +587,7 @@ int mfsdp_soap_step(const mfsdp_soap_entry* entries, int64_t count, const mfsdp_
   if (count == 0) return MFSDP_OK;
   Build b;
   size_t desc_at = 0;
-  const size_t need = build_soap(entries, count, hp, static_cast<char*>(workspace), b, desc_at);
+  const size_t need = build_soap(entries, count, hp, static_cast<char*>(workspace), b, desc_at, false);
   if (!workspace || !aligned(workspace, kAl) || workspace_bytes < need)
     return workspace_error(need, "mfsdp_soap_workspace_size");
   RunScalars rs;

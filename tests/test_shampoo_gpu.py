@@ -256,6 +256,45 @@ def test_shampoo_stale_preconditioners(native):
         _check(x, hpo)
 
 
+def _offset_view(t):
+    """The same values in a buffer that starts 4 bytes past a 16-byte boundary (a view into a larger
+    allocation)."""
+    import torch
+    big = torch.zeros(t.numel() + 1, dtype=t.dtype, device=t.device)
+    v = big[1:].view(t.shape)
+    v.copy_(t)
+    assert v.data_ptr() % 16 == 4
+    return v
+
+
+@pytest.mark.parametrize("refresh", [True, False])
+def test_shampoo_unaligned_caller_buffers_take_the_copy_path(native, refresh):
+    """Tile-multiple sides use 16-byte aligned caller statistics and preconditioners where they lie
+    and copy the others: the same step on the same values through both paths gives the same bits
+    (the copies are exact and the arithmetic is the same)."""
+    import torch
+    _say(f"shampoo in place vs copied buffers, refresh {refresh}")
+    m, n = 256, 384
+    runs = []
+    for offset in (False, True):
+        x = _Mat(np.random.default_rng(4200 + refresh), m, n, synth.BF16, synth.BF16).device()
+        S = _spd(np.random.default_rng(77), m, 10.0).astype(np.float32)
+        T = _spd(np.random.default_rng(78), n, 10.0).astype(np.float32)
+        x.dL.copy_(to_dev(S * 1e-3, synth.F32))
+        x.dR.copy_(to_dev(T * 1e-3, synth.F32))
+        x.dPL.copy_(to_dev(S, synth.F32))
+        x.dPR.copy_(to_dev(T, synth.F32))
+        if offset:
+            x.dL, x.dR, x.dPL, x.dPR = (_offset_view(t) for t in (x.dL, x.dR, x.dPL, x.dPR))
+        hpn, _ = _hp(native, refresh=refresh, beta=0.9, weight=0.1)
+        ents = [x.entry(native)]
+        native.shampoo_step_t(ents, hpn, native.shampoo_workspace_t(ents, hpn))
+        _sync()
+        runs.append([t.clone() for t in (x.dU, x.dL, x.dR, x.dPL, x.dPR, x.dp)])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+
+
 @pytest.mark.parametrize("eps_rel", [1e-6, 1e-4])
 @pytest.mark.parametrize("dts", [(synth.BF16, synth.BF16), (synth.F32, synth.F32)])
 def test_shampoo_stale_step_on_new_gradient_after_rank_deficient_refresh(native, eps_rel, dts):

@@ -374,6 +374,37 @@ def test_soap_step_with_a_4096_side(native):
     _check(mat, hpo)
 
 
+def _offset_view(t):
+    """The same values in a buffer that starts 4 bytes past a 16-byte boundary (a view into a larger
+    allocation)."""
+    import torch
+    big = torch.zeros(t.numel() + 1, dtype=t.dtype, device=t.device)
+    v = big[1:].view(t.shape)
+    v.copy_(t)
+    assert v.data_ptr() % 16 == 4
+    return v
+
+
+@pytest.mark.parametrize("refresh", [True, False])
+def test_soap_unaligned_caller_buffers_take_the_copy_path(native, refresh):
+    """Tile-multiple sides use 16-byte aligned caller statistics and bases where they lie and copy
+    the others: the same step on the same values through both paths gives the same bits."""
+    import torch
+    _say(f"soap in place vs copied buffers, refresh {refresh}")
+    runs = []
+    for offset in (False, True):
+        x = _Mat(np.random.default_rng(9900 + refresh), 256, 384, synth.BF16, synth.BF16).device()
+        if offset:
+            x.dL, x.dR, x.dQL, x.dQR = (_offset_view(t) for t in (x.dL, x.dR, x.dQL, x.dQR))
+        hpn, _, _ = _hp(native, refresh=refresh)
+        ents = [x.entry(native)]
+        native.soap_step_t(ents, hpn, native.soap_workspace_t(ents, hpn))
+        _sync()
+        runs.append([t.clone() for t in (x.dN, x.dp, x.dM, x.dV, x.dL, x.dR, x.dQL, x.dQR)])
+    for a, b in zip(*runs):
+        assert torch.equal(a, b)
+
+
 def test_soap_benchmark_configuration_full_size(native):
     """The configuration bench.py times: the GPT-2-small share's 12 matrices in one call, bf16
     parameters and gradients, full-rank statistics and random orthogonal bases, refresh on; every
