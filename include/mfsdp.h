@@ -265,7 +265,8 @@ typedef struct {
 } mfsdp_shampoo_hparams;
 
 /* Bytes of device workspace mfsdp_shampoo_step needs for these entries and hyperparameters:
- * per matrix, zero-padded fp32 copies of G and G^T and of P_L G (3 mp np floats) and five
+ * per matrix, zero-padded copies of G and G^T (fp32, or bf16 for a bf16 gradient), P_L G and U
+ * (3 mp np floats in all) and five
  * padded matrices per side for the root iteration (5 (mp^2 + np^2) floats), mp, np = m, n rounded
  * up to 128; plus launch descriptors. Data pointers are not used. 0 on invalid arguments;
  * count == 0 returns 0 with no error. */

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "mfsdp_internal.h"
 #include "shampoo_internal.h"
 
@@ -59,19 +61,14 @@ __device__ __forceinline__ void split3x4(const f32x4& x, u32x2& hi, u32x2& mid, 
 // reads) fall in 16 distinct 16-byte bank groups, and a wave's 8-byte stores (4 lanes per row) in 32.
 __device__ __forceinline__ int split_slot(int r, int c) { return r * 2 + (c ^ ((r >> 3) & 1)); }
 
-// Exact split of four fp32 values whose values are bf16 numbers (an operand with one part): the
-// packed bf16 values themselves.
-__device__ __forceinline__ u32x2 split1x4(const f32x4& x) {
-  return u32x2{pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3])};
-}
-
 constexpr int kShPlane = kShTile * 32;  // bytes of one split plane (128 x 16 bf16)
 constexpr int kShStage = 6 * kShPlane;  // both operands of one K step, three planes each
 
-// The products of one 128 x 128 output tile, P rows from bi, Q rows from bj, into acc, with PA
-// parts of P and PB parts of Q (3: fp32 split into hi + mid + lo; 1: an operand whose values are
-// bf16 numbers, so that its mid and lo parts are zero and the products with them are dropped,
-// which leaves the accumulated sums unchanged).
+// The products of one 128 x 128 output tile, P rows from bi, Q rows from bj, into acc. An fp32
+// operand is split into three bf16 parts (hi + mid + lo); an operand stored as bf16 (ABF, BBF: a
+// bf16 gradient) is its own single part, as if its mid and lo parts were zero: the products with
+// them are dropped, which leaves the accumulated sums unchanged. It is loaded as it is, 8 bytes per
+// 4 elements, and stored into its plane without a split.
 // 4 waves in a 2 x 2 arrangement, each 64 x 64 as 2 x 2 blocks of 32 x 32 outputs. The products
 // run on the bf16 MFMA (v_mfma_f32_32x32x16_bf16, fp32 accumulation) at fp32 accuracy: when a
 // K step of 16 is staged into LDS every element is split once into hi + mid + lo bf16 parts (three
@@ -84,15 +81,21 @@ constexpr int kShStage = 6 * kShPlane;  // both operands of one K step, three pl
 // of stage k + 2 are issued while stage k multiplies and stage k + 1's loads (issued a stage
 // earlier) are split into LDS. Few products per step (one-part operands) take several steps per
 // stage, so that a barrier and the load latency are spread over more MFMAs.
-template <int PA, int PB, int KS>
+template <bool ABF, bool BBF>
 __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, int bj, uint8_t* lds_raw,
                                                  f32x16 (&acc)[2][2]) {
+  constexpr int PA = ABF ? 1 : 3, PB = BBF ? 1 : 3;  // parts per operand
+  constexpr int KS = ABF && BBF ? 2 : 1;             // K steps per stage
   static_assert(KS * (PA + PB) <= 6, "a stage holds at most six planes");
   typedef __attribute__((address_space(1))) const uint8_t g_cu8;
+  typedef __attribute__((address_space(1))) const u32x2 g_cu32x2;
+  constexpr int ea = ABF ? 2 : 4, eb = BBF ? 2 : 4;  // bytes per element
+  using TA = typename std::conditional<ABF, u32x2, f32x4>::type;
+  using TB = typename std::conditional<BBF, u32x2, f32x4>::type;
   // tile rows of both operands (uniform) and this thread's byte offsets into them (32-bit: a tile
   // spans at most 128 rows of 65536 floats)
-  g_cu8* P = (g_cu8*)(d.P) + int64_t(bi) * kShTile * d.ldp * 4;
-  g_cu8* Q = (g_cu8*)(d.Q) + int64_t(bj) * kShTile * d.ldq * 4;
+  g_cu8* P = (g_cu8*)(d.P) + int64_t(bi) * kShTile * d.ldp * ea;
+  g_cu8* Q = (g_cu8*)(d.Q) + int64_t(bj) * kShTile * d.ldq * eb;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
   const int wr = w >> 1, wc = w & 1;
   const int fr = lane & 31, fh = lane >> 5;
@@ -102,23 +105,26 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
   uint32_t po[2], qo[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    po[j] = uint32_t((lrow + 64 * j) * d.ldp + lch * 4) * 4u;
-    qo[j] = uint32_t((lrow + 64 * j) * d.ldq + lch * 4) * 4u;
+    po[j] = uint32_t((lrow + 64 * j) * d.ldp + lch * 4) * uint32_t(ea);
+    qo[j] = uint32_t((lrow + 64 * j) * d.ldq + lch * 4) * uint32_t(eb);
   }
-  f32x4 ra0[KS][2], rb0[KS][2], ra1[KS][2], rb1[KS][2];
-  auto gload = [&](f32x4 (&ra)[KS][2], f32x4 (&rb)[KS][2], int k0) {
+  TA ra0[KS][2], ra1[KS][2];
+  TB rb0[KS][2], rb1[KS][2];
+  auto gload = [&](TA (&ra)[KS][2], TB (&rb)[KS][2], int k0) {
 #pragma unroll
     for (int u = 0; u < KS; ++u)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
-        ra[u][j] = *(const g_cf32x4*)(P + (k0 + 16 * u) * 4 + po[j]);
-        rb[u][j] = *(const g_cf32x4*)(Q + (k0 + 16 * u) * 4 + qo[j]);
+        if constexpr (ABF) ra[u][j] = *(g_cu32x2*)(P + (k0 + 16 * u) * ea + po[j]);
+        else ra[u][j] = *(const g_cf32x4*)(P + (k0 + 16 * u) * ea + po[j]);
+        if constexpr (BBF) rb[u][j] = *(g_cu32x2*)(Q + (k0 + 16 * u) * eb + qo[j]);
+        else rb[u][j] = *(const g_cf32x4*)(Q + (k0 + 16 * u) * eb + qo[j]);
       }
   };
   // plane (step u, operand o, part p) of a stage is u (PA + PB) + o PA + p; the 8-byte piece of
   // row r holding k 4 lch .. + 3
   auto plane = [](int u, int o, int p) { return u * (PA + PB) + o * PA + p; };
-  auto lstore = [&](int s, const f32x4 (&ra)[KS][2], const f32x4 (&rb)[KS][2]) {
+  auto lstore = [&](int s, const TA (&ra)[KS][2], const TB (&rb)[KS][2]) {
 #pragma unroll
     for (int u = 0; u < KS; ++u)
 #pragma unroll
@@ -127,21 +133,21 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
         const int off = split_slot(r, lch >> 1) * 16 + (lch & 1) * 8;
         uint8_t* base = lds_raw + s * kShStage + off;
         u32x2 h, m, l;
-        if (PA == 3) {
+        if constexpr (ABF) {
+          *reinterpret_cast<u32x2*>(base + plane(u, 0, 0) * kShPlane) = ra[u][j];
+        } else {
           split3x4(ra[u][j], h, m, l);
           *reinterpret_cast<u32x2*>(base + plane(u, 0, 0) * kShPlane) = h;
           *reinterpret_cast<u32x2*>(base + plane(u, 0, 1) * kShPlane) = m;
           *reinterpret_cast<u32x2*>(base + plane(u, 0, 2) * kShPlane) = l;
-        } else {
-          *reinterpret_cast<u32x2*>(base + plane(u, 0, 0) * kShPlane) = split1x4(ra[u][j]);
         }
-        if (PB == 3) {
+        if constexpr (BBF) {
+          *reinterpret_cast<u32x2*>(base + plane(u, 1, 0) * kShPlane) = rb[u][j];
+        } else {
           split3x4(rb[u][j], h, m, l);
           *reinterpret_cast<u32x2*>(base + plane(u, 1, 0) * kShPlane) = h;
           *reinterpret_cast<u32x2*>(base + plane(u, 1, 1) * kShPlane) = m;
           *reinterpret_cast<u32x2*>(base + plane(u, 1, 2) * kShPlane) = l;
-        } else {
-          *reinterpret_cast<u32x2*>(base + plane(u, 1, 0) * kShPlane) = split1x4(rb[u][j]);
         }
       }
   };
@@ -177,12 +183,12 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
   constexpr int kStep = 16 * KS;  // k per stage
   constexpr int kTerms = PA == 3 && PB == 3 ? 6 : PA == 3 || PB == 3 ? 3 : 1;
   constexpr int kMfma = KS * 4 * kTerms;  // MFMAs per stage and wave
-  constexpr int kSplitValu = KS * 2 * ((PA == 3 ? 22 : 2) + (PB == 3 ? 22 : 2));  // split VALU per stage, about
+  constexpr int kSplitValu = KS * 2 * ((ABF ? 0 : 22) + (BBF ? 0 : 22));  // split VALU per stage, about
   // one stage's products on LDS buffer mb while the next stage's loads (set) are split into buffer
   // sb: with split operands the split's vector instructions and LDS stores are interleaved with the
   // MFMAs (they are independent), so that a wave's MFMA pipe and vector ALU work at the same time
   // (one-part products have little to interleave and run faster in program order)
-  auto stage = [&](int mb, int sb, const f32x4 (&ra)[KS][2], const f32x4 (&rb)[KS][2]) {
+  auto stage = [&](int mb, int sb, const TA (&ra)[KS][2], const TB (&rb)[KS][2]) {
     mfma_stage(mb);
     lstore(sb, ra, rb);
     if constexpr (kTerms > 1) {
@@ -218,8 +224,7 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
 }
 
 // C = alpha P Q^T + beta E + diag I on one 128 x 128 output tile per workgroup (products as in
-// sh_tile_products, with the descriptor's part counts: both one part, Q one part, else three and
-// three). 48 KiB of LDS lets three workgroups share a CU.
+// sh_tile_products, with the descriptor's operand types: both bf16, Q bf16, or both fp32). 48 KiB of LDS lets three workgroups share a CU.
 // Symmetric problems compute the upper tiles only and store each tile transposed as well, through
 // LDS, with coalesced row stores.
 __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __restrict__ descs, int count) {
@@ -266,12 +271,12 @@ __global__ __launch_bounds__(256, 3) void sh_gemm_kernel(const ShGemmDesc* __res
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
-  if (d.p_parts == 1 && d.q_parts == 1)
-    sh_tile_products<1, 1, 2>(d, bi, bj, lds_raw, acc);
-  else if (d.q_parts == 1)
-    sh_tile_products<3, 1, 1>(d, bi, bj, lds_raw, acc);
+  if (d.q_bf16 && d.p_bf16)
+    sh_tile_products<true, true>(d, bi, bj, lds_raw, acc);
+  else if (d.q_bf16)
+    sh_tile_products<false, true>(d, bi, bj, lds_raw, acc);
   else
-    sh_tile_products<3, 3, 1>(d, bi, bj, lds_raw, acc);
+    sh_tile_products<false, false>(d, bi, bj, lds_raw, acc);
 
   // Epilogue, in two passes over the tile's row halves (the waves with wr = h hold rows
   // 64 h .. 64 h + 63). Accumulator element v of block (i, j) is row 32 i + 8 (v / 4) + 4 (lane / 32)
@@ -371,14 +376,19 @@ __global__ __launch_bounds__(256) void sh_copy_in_kernel(const ShCopyDesc* __res
   const int lt = blockIdx.x - d.tile_begin;
   const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
   const int t = threadIdx.x, c = t & 63, rr = t >> 6;
-  g_f32* dst = (g_f32*)(d.dst);
+  typedef __attribute__((address_space(1))) uint16_t g_u16;
   const int64_t gc = int64_t(tj) * kShCopyTile + c;
+  // a bf16 destination takes the value's upper 16 bits: exact, the values being bf16 numbers
+  auto put = [&](void* base, int64_t i, float v) {
+    if (d.dst_bf16) ((g_u16*)base)[i] = uint16_t(__float_as_uint(v) >> 16);
+    else ((g_f32*)base)[i] = v;
+  };
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
     const int r = rr + 4 * i;
     const int64_t gr = int64_t(ti) * kShCopyTile + r;
     const float v = (gr < d.rows && gc < d.cols) ? ld_any(d.src, gr * d.ld_src + gc, d.src_dtype) : 0.0f;
-    if (dst) dst[gr * d.ld_dst + gc] = v;
+    if (d.dst) put(d.dst, gr * d.ld_dst + gc, v);
     tt[r][c] = v;
   }
   if (d.dstT) {
@@ -386,7 +396,7 @@ __global__ __launch_bounds__(256) void sh_copy_in_kernel(const ShCopyDesc* __res
 #pragma unroll 4
     for (int i = 0; i < 16; ++i) {
       const int r = rr + 4 * i;  // row of the transposed tile = column of the source tile
-      ((g_f32*)d.dstT)[(int64_t(tj) * kShCopyTile + r) * d.ld_dstT + int64_t(ti) * kShCopyTile + c] = tt[c][r];
+      put(d.dstT, (int64_t(tj) * kShCopyTile + r) * d.ld_dstT + int64_t(ti) * kShCopyTile + c, tt[c][r]);
     }
   }
 }

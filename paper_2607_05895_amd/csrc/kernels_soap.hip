@@ -104,9 +104,15 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
   const int ti = lt / d.tiles_n, tj = lt - ti * d.tiles_n;
   const int t = threadIdx.x, c = t & 63, rr = t >> 6;
   const int64_t gc = int64_t(tj) * kTile + c;
+  typedef __attribute__((address_space(1))) uint16_t g_u16;
   g_f32* Gp = (g_f32*)(d.Gp);
   g_f32* GMt = (g_f32*)(d.GMt);
   g_f32* GM = (g_f32*)(d.GM);
+  // G (and G^T) as bf16: the value's upper 16 bits, exact for a bf16 gradient
+  auto put_g = [&](g_f32* base, int64_t i, float v) {
+    if (d.g_bf16) ((g_u16*)base)[i] = uint16_t(__float_as_uint(v) >> 16);
+    else base[i] = v;
+  };
 #pragma unroll 4
   for (int i = 0; i < 16; ++i) {
     const int r = rr + 4 * i;
@@ -120,7 +126,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
       mo = beta1 * d.exp_avg[o] + (1.0f - beta1) * g;
       d.exp_avg[o] = mo;
     }
-    if (Gp) Gp[gr * d.np + gc] = g;
+    if (Gp) put_g(Gp, gr * d.np + gc, g);
     if (GM) {
       GM[gr * 2 * d.np + gc] = g;
       GM[gr * 2 * d.np + d.np + gc] = mo;
@@ -134,7 +140,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
   for (int i = 0; i < 16; ++i) {
     const int r = rr + 4 * i;  // row of the transposed tile = column of the source tile
     const int64_t o = (int64_t(tj) * kTile + r) * d.mp + int64_t(ti) * kTile + c;
-    GMt[o] = tg[c][r];
+    put_g(GMt, o, tg[c][r]);
     GMt[o + d.np * d.mp] = tm[c][r];
   }
 }

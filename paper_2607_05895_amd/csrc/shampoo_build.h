@@ -92,7 +92,7 @@ struct Build {
   void join() { ops.push_back(Op{kOpJoin, 0, 0, 0, 0}); }
 };
 
-inline ShCopyDesc copy_desc(const void* src, int dt, void* dst, float* dstT, int64_t rows, int64_t cols,
+inline ShCopyDesc copy_desc(const void* src, int dt, void* dst, void* dstT, int64_t rows, int64_t cols,
                             int64_t ld_src, int64_t ld_dst, int64_t ld_dstT, int64_t dom_rows,
                             int64_t dom_cols, int& tiles) {
   ShCopyDesc c{};
@@ -132,7 +132,6 @@ inline ShGemmDesc gemm_desc(const float* P, const float* Q, const float* E, floa
   g.beta = beta;
   g.diag = diag;
   g.tile_begin = tiles;
-  g.p_parts = g.q_parts = 3;
   const int64_t tm = M / kShTile, tn = N / kShTile;
   tiles += int(sym ? tn * (tn + 1) / 2 : tm * tn);
   return g;

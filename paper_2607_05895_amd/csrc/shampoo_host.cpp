@@ -64,11 +64,18 @@ void plan_side(Side& s, int64_t d, Arena& a) {
   s.resid = a.take(2 * sizeof(float));
 }
 
+// Gp, GpT: G and G^T zero-padded (fp32, or for a bf16 gradient bf16 G and G^T both in Gp, which
+// leaves GpT free); Y = P_L G; U = Y P_R goes to Gp for an fp32 gradient, GpT for a bf16 one.
 struct EntryPlan {
   int64_t m, n, mp, np;
   bool grad_bf16;
   size_t Gp, GpT, Y;
   Side L, R;
+  size_t g() const { return Gp; }  // G (row stride np)
+  size_t gt() const {              // G^T (row stride mp)
+    return grad_bf16 ? Gp + size_t(mp) * size_t(np) * 2 : GpT;
+  }
+  size_t u() const { return grad_bf16 ? GpT : Gp; }
 };
 
 // Root ops for every side: norms, scalars, init, the iterations and the copy of X to side.out.
@@ -259,8 +266,10 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   int ct = 0;
   for (int64_t i = 0; i < count; ++i) {
     EntryPlan& e = P[size_t(i)];
-    cin.push_back(copy_desc(en[i].grad, en[i].grad_dtype, b.ptr<float>(e.Gp), b.ptr<float>(e.GpT), e.m,
-                            e.n, e.n, e.np, e.mp, e.mp, e.np, ct));
+    // a bf16 gradient is copied as bf16 (exact): the GEMM reads it as a one-part operand
+    cin.push_back(copy_desc(en[i].grad, en[i].grad_dtype, b.ptr<float>(e.g()), b.ptr<float>(e.gt()), e.m, e.n,
+                            e.n, e.np, e.mp, e.mp, e.np, ct));
+    cin.back().dst_bf16 = e.grad_bf16 ? 1 : 0;
     if (!e.L.S)
       cin.push_back(copy_desc(en[i].L, kDtF32, b.ptr<float>(e.L.M), nullptr, e.m, e.m, e.m, e.mp, 0, e.mp,
                               e.mp, ct));
@@ -282,22 +291,22 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   std::stable_sort(order.begin(), order.end(), [](const EntryPlan* x, const EntryPlan* y) {
     return std::max(x->mp, x->np) > std::max(y->mp, y->np);
   });
-  // a bf16 gradient is exact in one bf16 part: the statistics take one product, P_L G three
+  // a bf16 gradient is one bf16 part: the statistics take one product, P_L G three
   auto stat = [&](const Side& s, float* caller) { return s.S ? caller : b.ptr<float>(s.M); };
   std::vector<ShGemmDesc> gs;
   int gt = 0;
   for (EntryPlan* ep : order) {
     EntryPlan& e = *ep;
     const mfsdp_shampoo_entry& c = en[ep - P.data()];
-    const int gparts = e.grad_bf16 ? 1 : 3;
+    const int bf = e.grad_bf16 ? 1 : 0;
     float* Ls = stat(e.L, c.L);
     float* Rs = stat(e.R, c.R);
-    gs.push_back(gemm_desc(b.ptr<float>(e.Gp), b.ptr<float>(e.Gp), Ls, Ls, e.np, e.np, e.mp, e.mp, e.mp, e.mp,
+    gs.push_back(gemm_desc(b.ptr<float>(e.g()), b.ptr<float>(e.g()), Ls, Ls, e.np, e.np, e.mp, e.mp, e.mp, e.mp,
                            e.np, 1, float(hp->weight), float(hp->beta), 0.0f, gt));
-    gs.back().p_parts = gs.back().q_parts = gparts;
-    gs.push_back(gemm_desc(b.ptr<float>(e.GpT), b.ptr<float>(e.GpT), Rs, Rs, e.mp, e.mp, e.np, e.np, e.np, e.np,
+    gs.back().p_bf16 = gs.back().q_bf16 = bf;
+    gs.push_back(gemm_desc(b.ptr<float>(e.gt()), b.ptr<float>(e.gt()), Rs, Rs, e.mp, e.mp, e.np, e.np, e.np, e.np,
                            e.mp, 1, float(hp->weight), float(hp->beta), 0.0f, gt));
-    gs.back().p_parts = gs.back().q_parts = gparts;
+    gs.back().p_bf16 = gs.back().q_bf16 = bf;
   }
   b.op(kOpGemm, gs, gt);
 
@@ -331,10 +340,10 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     // the preconditioners: this step's roots, or the stored ones (read where they lie, or copied)
     const float* pl = (!refresh && e.L.S) ? en[i].PL : b.ptr<float>(e.L.X[fin]);
     const float* pr = (!refresh && e.R.S) ? en[i].PR : b.ptr<float>(e.R.X[fin]);
-    gy.push_back(gemm_desc(pl, b.ptr<float>(e.GpT), nullptr, b.ptr<float>(e.Y), e.mp, e.mp, 0, e.np, e.mp,
+    gy.push_back(gemm_desc(pl, b.ptr<float>(e.gt()), nullptr, b.ptr<float>(e.Y), e.mp, e.mp, 0, e.np, e.mp,
                            e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
-    if (e.grad_bf16) gy.back().q_parts = 1;
-    gu.push_back(gemm_desc(b.ptr<float>(e.Y), pr, nullptr, b.ptr<float>(e.Gp), e.np, e.np, 0, e.np, e.mp,
+    gy.back().q_bf16 = e.grad_bf16 ? 1 : 0;
+    gu.push_back(gemm_desc(b.ptr<float>(e.Y), pr, nullptr, b.ptr<float>(e.u()), e.np, e.np, 0, e.np, e.mp,
                            e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
   }
   b.op(kOpGemm, gy, ty);
@@ -345,7 +354,7 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
   for (int64_t i = 0; i < count; ++i) {
     EntryPlan& e = P[size_t(i)];
     ShApplyDesc d{};
-    d.U = b.ptr<float>(e.Gp);
+    d.U = b.ptr<float>(e.u());
     d.ldu = e.np;
     d.param = en[i].param;
     d.update_out = en[i].update_out;

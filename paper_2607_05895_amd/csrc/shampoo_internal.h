@@ -45,25 +45,27 @@ struct ShGemmDesc {
   float* resid_out;      // max |C - I| over the real block (rows, cols < valid), atomic max
   int32_t copy_on_skip;
   int32_t valid;
-  // parts of the bf16 split per operand: 1 when every value of the operand is a bf16 number (a
-  // bf16 gradient widened to fp32, with zero padding), so that the products with its zero mid and
-  // lo parts are dropped; anything else is 3. Honoured for (1, 1) and (any, 1).
-  int32_t p_parts, q_parts;
+  // operand stored as bf16 (a bf16 gradient; row stride in elements): it is one part of the bf16
+  // split, so the products with the zero mid and lo parts of an fp32 split are dropped. Both P and
+  // Q, or Q alone (P alone is not supported). fp32 operands are split into three parts.
+  int32_t p_bf16, q_bf16;
 };
 
 // Boundary copies over 64 x 64 tiles of a padded rows_pad x cols_pad domain.
 // in  (dir 0): dst[r][c] = src[r][c] inside rows x cols, 0 elsewhere; optional dstT[c][r] too
-//              (dst may be null when dstT is set).
+//              (dst may be null when dstT is set); both fp32, or both bf16 when dst_bf16 (for a
+//              bf16 source: the copy is exact).
 // out (dir 1): dst (caller, rows x cols fp32, row stride ld_dst) = src (padded fp32) inside.
 struct ShCopyDesc {
   const void* src;
   void* dst;
-  float* dstT;
+  void* dstT;
   int64_t rows, cols;
   int64_t ld_src, ld_dst, ld_dstT;
   int32_t src_dtype;   // kDtF32 / kDtBF16 (dir 0)
   int32_t tiles_n;     // column tiles of the domain
   int32_t tile_begin;
+  int32_t dst_bf16;    // dir 0: dst and dstT hold bf16
 };
 
 // Sum of squares and trace of a padded d_pad x d_pad statistic, in row chunks (fp64 partials).

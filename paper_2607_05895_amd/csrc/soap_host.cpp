@@ -16,8 +16,8 @@
 //   N       = Z Q_R^T            P = Z,      Q = Q_R                (mp x np, K = np)
 //   L, R statistics              P = Q = G (sym, K = np), P = Q = G^T (sym, K = mp)
 //   refresh S^T = Q_L^T L        P = Q_L^T,  Q = L                  (mp x mp, K = mp)
-// A bf16 gradient widened to fp32 is a one-part operand of the split-bf16 GEMM (its mid and lo
-// parts are zero): the statistics then take one bf16 product per step, Q_L^T G three.
+// A bf16 gradient is kept as bf16 (G, and the G^T half of [G^T ; M^T]) and is a one-part operand
+// of the split-bf16 GEMM: the statistics then take one bf16 product per step, Q_L^T G three.
 // The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
 // with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
 // block, with S held transposed (each column of S one contiguous row) and Q accumulated from the
@@ -72,21 +72,21 @@ struct Prod {
   int64_t ldp, ldq, lde, ldc, M, N, K;
   int sym;
   float alpha, beta;
-  int pparts = 3, qparts = 3;  // bf16 parts of P and Q (1: the operand's values are bf16 numbers)
+  bool pbf = false, qbf = false;  // P, Q stored as bf16 (one-part operands; both, or Q alone)
 };
 
 void add_gemm(Build& b, std::vector<Prod> ps) {
   // longest tiles first (K times the bf16 products per step; a one-part product is load-bound at
   // about a third of the six-product time): the hardware dispatches blocks in order
-  auto cost = [](const Prod& x) { return x.K * (x.pparts == 1 && x.qparts == 1 ? 2 : x.qparts == 1 ? 3 : 6); };
+  auto cost = [](const Prod& x) { return x.K * (x.pbf && x.qbf ? 2 : x.qbf ? 3 : 6); };
   std::stable_sort(ps.begin(), ps.end(), [&](const Prod& x, const Prod& y) { return cost(x) > cost(y); });
   std::vector<ShGemmDesc> gs;
   int gt = 0;
   for (const Prod& p : ps) {
     gs.push_back(gemm_desc(p.P, p.Q, p.E, p.C, p.ldp, p.ldq, p.lde, p.ldc, p.M, p.N, p.K, p.sym, p.alpha,
                            p.beta, 0.0f, gt));
-    gs.back().p_parts = p.pparts;
-    gs.back().q_parts = p.qparts;
+    gs.back().p_bf16 = p.pbf ? 1 : 0;
+    gs.back().q_bf16 = p.qbf ? 1 : 0;
   }
   b.op(kOpGemm, gs, gt);
 }
@@ -381,6 +381,7 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     d.mp = e.mp;
     d.np = e.np;
     d.grad_dtype = en[i].grad_dtype == MFSDP_BF16 ? kDtBF16 : kDtF32;
+    d.g_bf16 = d.grad_dtype == kDtBF16 ? 1 : 0;
     d.tiles_n = int32_t(e.np / kShCopyTile);
     d.tile_begin = pt;
     pt += int((e.mp / kShCopyTile) * (e.np / kShCopyTile));
@@ -401,23 +402,24 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     float* X1 = b.ptr<float>(e.X1);
     float* GMr = b.ptr<float>(e.GMr);
     const int64_t mp = e.mp, np = e.np;
-    // a bf16 gradient (widened exactly, zero padded) is one bf16 part: one product per statistic
-    const int gparts = en[&e - P.data()].grad_dtype == MFSDP_BF16 ? 1 : 3;
+    // a bf16 gradient (stored as bf16 by the first-moment pass) is one bf16 part: one product per
+    // statistic, three for Q_L^T G
+    const bool gbf = en[&e - P.data()].grad_dtype == MFSDP_BF16;
     if (e.left) {
       const float* GMt = b.ptr<float>(e.GMt);
       const float* Gp = b.ptr<float>(e.Gp);
       // the G half of Q_L^T [G | M] has a one-part Q when the gradient is bf16
-      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, np, mp, 0, 1.0f, 0.0f, 3,
-                        gparts});
+      p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, np, mp, 0, 1.0f, 0.0f, false,
+                        gbf});
       p1.push_back(Prod{b.ptr<float>(e.QLt), GMt + np * mp, nullptr, X1 + np, mp, mp, 0, 2 * np, mp, np, mp, 0,
                         1.0f, 0.0f});
       // the statistics read only G and G^T: they join the first launch
-      p1.push_back(Prod{Gp, Gp, Lb(e), Lb(e), np, np, mp, mp, mp, mp, np, 1, ws_, bs_, gparts, gparts});
+      p1.push_back(Prod{Gp, Gp, Lb(e), Lb(e), np, np, mp, mp, mp, mp, np, 1, ws_, bs_, gbf, gbf});
       p3.push_back(Prod{QLb(e), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f, 0.0f});
     }
     if (e.right) {
       const float* GMt = b.ptr<float>(e.GMt);
-      p1.push_back(Prod{GMt, GMt, Rb(e), Rb(e), mp, mp, np, np, np, np, mp, 1, ws_, bs_, gparts, gparts});
+      p1.push_back(Prod{GMt, GMt, Rb(e), Rb(e), mp, mp, np, np, np, np, mp, 1, ws_, bs_, gbf, gbf});
       for (int h = 0; h < 2; ++h)
         p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np,
                           np, 0, 1.0f, 0.0f});

@@ -28,8 +28,10 @@ static_assert(kQrBlock == kShTile, "the block update runs on the Shampoo GEMM's 
 // M <- beta1 M + (1 - beta1) G over the real m x n block, and the padded layouts the products read
 // (each written only if its pointer is set): Gp (mp x np, row stride np) = G; GMt rows [0, np) = G^T
 // and rows [np, 2 np) = M^T (row stride mp); GM (mp x 2 np, row stride 2 np) = [G | M] (a left side
-// without a basis: the right product reads G and M as they are). 64 x 64 tiles over the padded
-// mp x np domain; zeros outside the real block.
+// without a basis: the right product reads G and M as they are). With g_bf16 (a bf16 gradient) Gp
+// and GMt's G^T rows hold bf16 (same row strides in elements; exact), for the GEMM's one-part
+// operands; M^T stays fp32 at GMt + np mp. 64 x 64 tiles over the padded mp x np domain; zeros
+// outside the real block.
 struct SoapPrepDesc {
   const void* grad;
   float* exp_avg;
@@ -40,6 +42,7 @@ struct SoapPrepDesc {
   int32_t grad_dtype;
   int32_t tiles_n;
   int32_t tile_begin;
+  int32_t g_bf16;
 };
 
 // Adam in the eigenbasis over the real block: GMr = [G' | M'] (mp x 2 np, row stride 2 np);
