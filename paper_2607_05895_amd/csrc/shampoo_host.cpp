@@ -65,7 +65,8 @@ void plan_side(Side& s, int64_t d, Arena& a) {
 }
 
 // Gp, GpT: G and G^T zero-padded (fp32, or for a bf16 gradient bf16 G and G^T both in Gp, which
-// leaves GpT free); Y = P_L G; U = Y P_R goes to Gp for an fp32 gradient, GpT for a bf16 one.
+// leaves GpT free); Y = P_L G (or Y^T = P_R G^T for a wide bf16 G); U goes to Gp for an fp32
+// gradient, GpT for a bf16 one.
 struct EntryPlan {
   int64_t m, n, mp, np;
   bool grad_bf16;
@@ -340,11 +341,23 @@ size_t build_shampoo(const mfsdp_shampoo_entry* en, int64_t count, const mfsdp_s
     // the preconditioners: this step's roots, or the stored ones (read where they lie, or copied)
     const float* pl = (!refresh && e.L.S) ? en[i].PL : b.ptr<float>(e.L.X[fin]);
     const float* pr = (!refresh && e.R.S) ? en[i].PR : b.ptr<float>(e.R.X[fin]);
-    gy.push_back(gemm_desc(pl, b.ptr<float>(e.gt()), nullptr, b.ptr<float>(e.Y), e.mp, e.mp, 0, e.np, e.mp,
-                           e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
-    gy.back().q_bf16 = e.grad_bf16 ? 1 : 0;
-    gu.push_back(gemm_desc(b.ptr<float>(e.Y), pr, nullptr, b.ptr<float>(e.u()), e.np, e.np, 0, e.np, e.mp,
-                           e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
+    // U = P_L G P_R^T. Both association orders take the same fp32 flop, but with a bf16 G the product
+    // that reads G takes three bf16 MFMAs per step and the other six, so the larger of the two
+    // products should be the one with G: a wide G (n > m) forms Y^T = P_R G^T (n x m) first and then
+    // U = P_L Y; otherwise Y = P_L G, then U = Y P_R^T.
+    if (e.grad_bf16 && e.n > e.m) {
+      gy.push_back(gemm_desc(pr, b.ptr<float>(e.g()), nullptr, b.ptr<float>(e.Y), e.np, e.np, 0, e.mp, e.np,
+                             e.mp, e.np, 0, 1.0f, 0.0f, 0.0f, ty));
+      gy.back().q_bf16 = 1;
+      gu.push_back(gemm_desc(pl, b.ptr<float>(e.Y), nullptr, b.ptr<float>(e.u()), e.mp, e.mp, 0, e.np, e.mp,
+                             e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, tu));
+    } else {
+      gy.push_back(gemm_desc(pl, b.ptr<float>(e.gt()), nullptr, b.ptr<float>(e.Y), e.mp, e.mp, 0, e.np, e.mp,
+                             e.np, e.mp, 0, 1.0f, 0.0f, 0.0f, ty));
+      gy.back().q_bf16 = e.grad_bf16 ? 1 : 0;
+      gu.push_back(gemm_desc(b.ptr<float>(e.Y), pr, nullptr, b.ptr<float>(e.u()), e.np, e.np, 0, e.np, e.mp,
+                             e.np, e.np, 0, 1.0f, 0.0f, 0.0f, tu));
+    }
   }
   b.op(kOpGemm, gy, ty);
   b.op(kOpGemm, gu, tu);
