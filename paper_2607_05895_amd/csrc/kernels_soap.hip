@@ -108,6 +108,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
   g_f32* Gp = (g_f32*)(d.Gp);
   g_f32* GMt = (g_f32*)(d.GMt);
   g_f32* GM = (g_f32*)(d.GM);
+  g_f32* Mr = (g_f32*)(d.Mr);
   // G (and G^T) as bf16: the value's upper 16 bits, exact for a bf16 gradient
   auto put_g = [&](g_f32* base, int64_t i, float v) {
     if (d.g_bf16) ((g_u16*)base)[i] = uint16_t(__float_as_uint(v) >> 16);
@@ -127,6 +128,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
       d.exp_avg[o] = mo;
     }
     if (Gp) put_g(Gp, gr * d.np + gc, g);
+    if (Mr) Mr[gr * d.np + gc] = mo;
     if (GM) {
       GM[gr * 2 * d.np + gc] = g;
       GM[gr * 2 * d.np + d.np + gc] = mo;
@@ -141,7 +143,7 @@ __global__ __launch_bounds__(256) void soap_prep_kernel(const SoapPrepDesc* __re
     const int r = rr + 4 * i;  // row of the transposed tile = column of the source tile
     const int64_t o = (int64_t(tj) * kTile + r) * d.mp + int64_t(ti) * kTile + c;
     put_g(GMt, o, tg[c][r]);
-    GMt[o + d.np * d.mp] = tm[c][r];
+    if (!Mr) GMt[o + d.np * d.mp] = tm[c][r];
   }
 }
 

@@ -17,7 +17,10 @@
 //   L, R statistics              P = Q = G (sym, K = np), P = Q = G^T (sym, K = mp)
 //   refresh S^T = Q_L^T L        P = Q_L^T,  Q = L                  (mp x mp, K = mp)
 // A bf16 gradient is kept as bf16 (G, and the G^T half of [G^T ; M^T]) and is a one-part operand
-// of the split-bf16 GEMM: the statistics then take one bf16 product per step, Q_L^T G three.
+// of the split-bf16 GEMM: the statistics then take one bf16 product per step, Q_L^T G three. For a
+// wide matrix (n > m) with both bases the right product runs first (X1 = Q_R^T [G^T | M^T] with G
+// and M read row-major, then [G' | M'] = Q_L^T X1^T), so that the larger product is the one with
+// the one-part G.
 // The first-moment pass writes G, G^T and M^T; the Adam pass writes N'^T; both bases are copied in
 // with their transposes. The refresh QR is a blocked Householder factorization of S's real d x d
 // block, with S held transposed (each column of S one contiguous row) and Q accumulated from the
@@ -239,6 +242,11 @@ constexpr size_t kNone = ~size_t(0);
 struct SoapPlan {
   int64_t m = 0, n = 0, mp = 0, np = 0;
   bool left = true, right = true;
+  // the right product first: [G Q_R | M Q_R], then Q_L^T of it. Both orders take the same fp32
+  // flop, but the product that reads a bf16 G takes three bf16 MFMAs per step instead of six, so
+  // for a wide matrix (n > m) with a bf16 gradient and both bases the larger product is then the
+  // cheaper one
+  bool rfirst = false;
   // a side with a basis whose length is a multiple of the tile (and whose caller buffers are
   // 16-byte aligned, as the GEMM's vector accesses need) reads and updates the caller's statistic
   // where it lies and reads the caller's basis there (no copy in or out; the basis is still copied
@@ -314,6 +322,7 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     e.right = e.n <= maxd;
     e.mp = rup(e.m, kShTile);
     e.np = rup(e.n, kShTile);
+    e.rfirst = e.left && e.right && e.n > e.m && en[i].grad_dtype == MFSDP_BF16;
     e.lin = !sizing && e.left && e.m == e.mp && aligned(en[i].L, 16) && aligned(en[i].QL, 16);
     e.rin = !sizing && e.right && e.n == e.np && aligned(en[i].R, 16) && aligned(en[i].QR, 16);
     const size_t f = sizeof(float), mn = size_t(e.mp) * size_t(e.np) * f;
@@ -376,6 +385,7 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     d.Gp = fp(e.Gp);
     d.GMt = fp(e.GMt);
     d.GM = e.left ? nullptr : b.ptr<float>(e.X1);
+    d.Mr = e.rfirst ? b.ptr<float>(e.GMt) + e.np * e.mp : nullptr;
     d.m = e.m;
     d.n = e.n;
     d.mp = e.mp;
@@ -393,6 +403,7 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
   // Products (a side without a basis skips its own):
   //   left:  X1 = Q_L^T [G | M];  Z = Q_L N' (from N'^T) into X1
   //   right: [G' | M'] = X1 halves Q_R into GMr;  N = Z Q_R^T into GMr
+  //   (rfirst: X1 = Q_R^T [G^T | M^T], then [G' | M'] = Q_L^T X1^T into GMr; the rest as above)
   // Adam reads [G' | M'] from GMr (right) or X1 (no right basis) and writes N'^T (left) or N'
   // itself: into X1 as Z (right) or into GMr as N (neither); apply reads N from GMr, or from X1 when
   // only the left side has a basis.
@@ -405,14 +416,24 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     // a bf16 gradient (stored as bf16 by the first-moment pass) is one bf16 part: one product per
     // statistic, three for Q_L^T G
     const bool gbf = en[&e - P.data()].grad_dtype == MFSDP_BF16;
-    if (e.left) {
+    if (e.rfirst) {
+      // X1 (as 2 np x mp, row stride mp) = [(G Q_R)^T ; (M Q_R)^T] = Q_R^T [G^T | M^T]; then
+      // [G' | M'] = Q_L^T [G Q_R | M Q_R] into GMr; G is bf16 in Gp, M row-major after GMt's G^T rows
+      const float* QRt = b.ptr<float>(e.QRt);
+      const float* Mr = b.ptr<float>(e.GMt) + np * mp;
+      p1.push_back(Prod{QRt, b.ptr<float>(e.Gp), nullptr, X1, np, np, 0, mp, np, mp, np, 0, 1.0f, 0.0f, false, true});
+      p1.push_back(Prod{QRt, Mr, nullptr, X1 + np * mp, np, np, 0, mp, np, mp, np, 0, 1.0f, 0.0f});
+      p2.push_back(Prod{b.ptr<float>(e.QLt), X1, nullptr, GMr, mp, mp, 0, 2 * np, mp, 2 * np, mp, 0, 1.0f, 0.0f});
+    } else if (e.left) {
       const float* GMt = b.ptr<float>(e.GMt);
-      const float* Gp = b.ptr<float>(e.Gp);
       // the G half of Q_L^T [G | M] has a one-part Q when the gradient is bf16
       p1.push_back(Prod{b.ptr<float>(e.QLt), GMt, nullptr, X1, mp, mp, 0, 2 * np, mp, np, mp, 0, 1.0f, 0.0f, false,
                         gbf});
       p1.push_back(Prod{b.ptr<float>(e.QLt), GMt + np * mp, nullptr, X1 + np, mp, mp, 0, 2 * np, mp, np, mp, 0,
                         1.0f, 0.0f});
+    }
+    if (e.left) {
+      const float* Gp = b.ptr<float>(e.Gp);
       // the statistics read only G and G^T: they join the first launch
       p1.push_back(Prod{Gp, Gp, Lb(e), Lb(e), np, np, mp, mp, mp, mp, np, 1, ws_, bs_, gbf, gbf});
       p3.push_back(Prod{QLb(e), b.ptr<float>(e.NpT), nullptr, X1, mp, mp, 0, np, mp, np, mp, 0, 1.0f, 0.0f});
@@ -420,9 +441,10 @@ size_t build_soap(const mfsdp_soap_entry* en, int64_t count, const mfsdp_soap_hp
     if (e.right) {
       const float* GMt = b.ptr<float>(e.GMt);
       p1.push_back(Prod{GMt, GMt, Rb(e), Rb(e), mp, mp, np, np, np, np, mp, 1, ws_, bs_, gbf, gbf});
-      for (int h = 0; h < 2; ++h)
-        p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np,
-                          np, 0, 1.0f, 0.0f});
+      if (!e.rfirst)
+        for (int h = 0; h < 2; ++h)
+          p2.push_back(Prod{X1 + h * np, b.ptr<float>(e.QRt), nullptr, GMr + h * np, 2 * np, np, 0, 2 * np, mp, np,
+                            np, 0, 1.0f, 0.0f});
       p4.push_back(Prod{X1, QRb(e), nullptr, GMr, np, np, 0, np, mp, np, np, 0, 1.0f, 0.0f});
     }
   }

@@ -30,14 +30,16 @@ static_assert(kQrBlock == kShTile, "the block update runs on the Shampoo GEMM's 
 // and rows [np, 2 np) = M^T (row stride mp); GM (mp x 2 np, row stride 2 np) = [G | M] (a left side
 // without a basis: the right product reads G and M as they are). With g_bf16 (a bf16 gradient) Gp
 // and GMt's G^T rows hold bf16 (same row strides in elements; exact), for the GEMM's one-part
-// operands; M^T stays fp32 at GMt + np mp. 64 x 64 tiles over the padded mp x np domain; zeros
-// outside the real block.
+// operands; M^T stays fp32 at GMt + np mp, unless Mr is set: then M itself (row stride np) goes
+// there instead (the right product first, for a wide matrix). 64 x 64 tiles over the padded
+// mp x np domain; zeros outside the real block.
 struct SoapPrepDesc {
   const void* grad;
   float* exp_avg;
   float* Gp;
   float* GMt;
   float* GM;
+  float* Mr;
   int64_t m, n, mp, np;
   int32_t grad_dtype;
   int32_t tiles_n;
