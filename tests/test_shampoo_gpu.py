@@ -97,6 +97,29 @@ def test_inverse_root_matches_oracle(native, d, p):
     np.testing.assert_array_equal(from_dev(ad), a)
 
 
+def test_inverse_root_input_read_in_place_or_copied(native):
+    """A tile-multiple d whose input is 16-byte aligned is read where it lies; the same values at a
+    4-byte offset take the copy path. Same bits either way."""
+    import torch
+    _say("inverse root: aligned vs offset input")
+    d = 256
+    a = _spd(np.random.default_rng(1300), d, 1e3).astype(np.float32)
+    outs = []
+    for offset in (False, True):
+        ad = to_dev(a, synth.F32)
+        if offset:
+            big = torch.zeros(d * d + 1, dtype=torch.float32, device="cuda")
+            ad = big[1:].view(d, d)
+            ad.copy_(to_dev(a, synth.F32))
+            assert ad.data_ptr() % 16 == 4
+        out = torch.empty((d, d), dtype=torch.float32, device="cuda")
+        native.inverse_root_t(ad, out, p=4, eps=1e-9, eps_rel=1e-6, iters=30)
+        _sync()
+        outs.append(out.clone())
+        np.testing.assert_array_equal(from_dev(ad), a)
+    assert torch.equal(outs[0], outs[1])
+
+
 def test_inverse_root_of_diagonal_and_scaled_identity(native):
     import torch
     _say("inverse root diagonal")
