@@ -93,7 +93,7 @@ __device__ __forceinline__ void sh_tile_products(const ShGemmDesc& d, int bi, in
   using TA = typename std::conditional<ABF, u32x2, f32x4>::type;
   using TB = typename std::conditional<BBF, u32x2, f32x4>::type;
   // tile rows of both operands (uniform) and this thread's byte offsets into them (32-bit: a tile
-  // spans at most 128 rows of 65536 floats)
+  // spans at most 128 rows with a row stride of at most 2 x 65536 elements, under 2^27 bytes)
   g_cu8* P = (g_cu8*)(d.P) + int64_t(bi) * kShTile * d.ldp * ea;
   g_cu8* Q = (g_cu8*)(d.Q) + int64_t(bj) * kShTile * d.ldq * eb;
   const int t = threadIdx.x, lane = t & 63, w = t >> 6;
