@@ -11,11 +11,12 @@
 
 namespace mfsdp {
 
-// One output tile of a grouped NS product: problem (matrix) index, 256 x 256 block coordinates and,
-// for a problem whose contraction is split, the K range ks of the tile; e < 0 marks an idle slot.
-// The bf16 NS kernels run a persistent grid of kGemmXcds x kGemmSlots workgroups; workgroup b
-// serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes tile sched[g * kGemmSlots + slot] of
-// every group g = xcd, xcd + kGemmXcds, ...
+// One output tile of a grouped NS product: problem (matrix) index, block coordinates (in tiles of
+// the launch: 256 x 256, or 128 x 128) and, for a problem whose contraction is split, the K range ks
+// of the tile; e < 0 marks an idle slot. The bf16 NS kernels run a persistent grid of kGemmXcds x S
+// workgroups (S = kGemmSlots on 256 x 256 tiles, one workgroup per CU; twice that on 128 x 128
+// tiles); workgroup b serves XCD b % kGemmXcds, slot b / kGemmXcds, and takes tile
+// sched[g * S + slot] of every group g = xcd, xcd + kGemmXcds, ...
 struct TileRef {
   int32_t e;
   int16_t bi, bj;
@@ -33,8 +34,8 @@ struct TileGrid {
 };
 
 // Tile schedule of one product for the persistent bf16 kernel. Tiles are put in locality order
-// (bands of kGroupRows block rows, within a band column by column, upper triangle only for
-// symmetric products) and cut into groups of kGemmSlots tiles, so that the workgroups of one XCD
+// (bands of group_rows block rows, within a band column by column, upper triangle only for
+// symmetric products) and cut into groups of `slots` tiles, so that the workgroups of one XCD
 // run the tiles of a group together and share its operand blocks in L2. Groups are then dealt to
 // the XCDs longest first, each to the XCD with the least work so far (a group's cost is the
 // largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
@@ -43,25 +44,26 @@ struct TileGrid {
 // ranges of one tile are listed together and each costs cost / splits.
 inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
                                            const std::vector<int64_t>& cost,
-                                           const std::vector<int>* splits = nullptr) {
+                                           const std::vector<int>* splits = nullptr,
+                                           int slots = kGemmSlots, int group_rows = kGroupRows) {
   auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
   std::vector<TileRef> flat;
   for (int e : order) {
     const TileGrid& g = grids[e];
-    for (int r0 = 0; r0 < g.tm; r0 += kGroupRows) {
-      const int r1 = std::min(g.tm, r0 + kGroupRows);
+    for (int r0 = 0; r0 < g.tm; r0 += group_rows) {
+      const int r1 = std::min(g.tm, r0 + group_rows);
       for (int c = g.sym ? r0 : 0; c < g.tn; ++c)
         for (int r = r0; r < r1; ++r)
           if (!g.sym || r <= c)
             for (int ks = 0; ks < nks(e); ++ks) flat.push_back(TileRef{e, int16_t(r), int16_t(c), int16_t(ks), 0});
     }
   }
-  while (flat.size() % kGemmSlots) flat.push_back(TileRef{-1, 0, 0, 0, 0});
-  const size_t ng = flat.size() / kGemmSlots;
+  while (flat.size() % size_t(slots)) flat.push_back(TileRef{-1, 0, 0, 0, 0});
+  const size_t ng = flat.size() / size_t(slots);
   std::vector<int64_t> gcost(ng, 0);
   for (size_t g = 0; g < ng; ++g)
-    for (int s = 0; s < kGemmSlots; ++s) {
-      const TileRef& t = flat[g * kGemmSlots + s];
+    for (int s = 0; s < slots; ++s) {
+      const TileRef& t = flat[g * size_t(slots) + size_t(s)];
       if (t.e >= 0) gcost[g] = std::max(gcost[g], cost[t.e] / nks(t.e));
     }
   std::vector<size_t> by(ng);
@@ -78,16 +80,16 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
   }
   size_t rounds = 0;
   for (const auto& l : lists) rounds = std::max(rounds, l.size());
-  std::vector<TileRef> s(rounds * kGemmXcds * kGemmSlots, TileRef{-1, 0, 0, 0, 0});
+  std::vector<TileRef> s(rounds * kGemmXcds * size_t(slots), TileRef{-1, 0, 0, 0, 0});
   for (int x = 0; x < kGemmXcds; ++x)
     for (size_t i = 0; i < lists[x].size(); ++i)
-      std::memcpy(&s[(i * kGemmXcds + x) * kGemmSlots], &flat[lists[x][i] * kGemmSlots],
-                  kGemmSlots * sizeof(TileRef));
+      std::memcpy(&s[(i * kGemmXcds + size_t(x)) * size_t(slots)], &flat[lists[x][i] * size_t(slots)],
+                  size_t(slots) * sizeof(TileRef));
   return s;
 }
 
 // K splits of a Gram product launch (upper tiles tiles[e] of contraction length K[e] per problem)
-// with fewer tiles than the persistent grid has workgroups. A tile's time is set by its K, so a
+// with fewer tiles than the persistent grid has workgroups (slots: the grid's workgroups). A tile's time is set by its K, so a
 // few long-K tiles (say those of a 768 x 3072 matrix among 768 x 768 ones) would alone set the
 // launch's length while most of the chip waits. Each problem gets the largest f <= kSplitMax that
 // divides K / 32 and keeps K / f at least at a target: first the larger of kSplitMinK and the
@@ -98,10 +100,10 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
 constexpr int64_t kSplitMinK = 512;
 constexpr int kSplitMax = 8;
 inline std::vector<int> gram_splits(const std::vector<int64_t>& tiles, const std::vector<int64_t>& K,
-                                    int64_t max_parts = INT64_MAX) {
+                                    int64_t max_parts = INT64_MAX,
+                                    int64_t slots = int64_t(kGemmXcds) * kGemmSlots) {
   const size_t n = tiles.size();
   std::vector<int> f(n, 1);
-  const int64_t slots = int64_t(kGemmXcds) * kGemmSlots;
   int64_t T = 0, W = 0;
   for (size_t e = 0; e < n; ++e) {
     T += tiles[e];

@@ -10,7 +10,8 @@
 // (TileRef); each 256 x 256 output tile is 2 x 4 waves of 128 x 64, as 4 x 2 blocks of
 // v_mfma_f32_32x32x16_bf16 with fp32 accumulation. K advances 32 elements per step through a
 // five-stage LDS ring filled by direct global->LDS loads; the next tile's first loads overlap the
-// current tile's epilogue.
+// current tile's epilogue. The Gram and square products of a small share run the same kernel on
+// 128 x 128 tiles (2 x 2 waves of 64 x 64, two workgroups per CU), four times the tiles.
 // fp32 path: 64 x 64 tiles on the fp32 MFMA (v_mfma_f32_32x32x2f32).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -134,8 +135,8 @@ __device__ __forceinline__ void apply4(const ApplyDesc& a, int64_t pr, int64_t p
 // ---------------------------------------------------------------------------------------------
 // bf16 MFMA kernel
 //
-// Main loop: K in steps of 32 elements. A stage holds the P rows (256 x 32 bf16 = 16 KiB) followed
-// by the Q rows (16 KiB) of one K step. Stages are filled by direct global->LDS loads
+// Main loop: K in steps of 32 elements. A stage holds the P rows (TB x 32 bf16: 16 KiB on 256 x 256
+// tiles) followed by the Q rows of one K step. Stages are filled by direct global->LDS loads
 // (global_load_lds_dwordx4: each wave instruction writes 64 x 16 B = 1 KiB of LDS contiguously),
 // so no registers or ds_write instructions carry the tiles. One workgroup barrier per K step kt,
 // placed between its two 16-wide K slices: before it every wave waits (explicit vmcnt) for its own
@@ -147,11 +148,10 @@ __device__ __forceinline__ void apply4(const ApplyDesc& a, int64_t pr, int64_t p
 // LDS row layout: 64 B per row = four 16-B chunks; chunk c of row r is stored in slot c ^ g(r)
 // with g(r) = (r1 ^ r3) | r2 << 1 (bits of r). Groups of 8 (or 16) consecutive rows read by one
 // ds_read_b128 cycle then hit distinct banks for 32 (or 64) banks of 4 B.
-constexpr int BT = 256;                      // output tile (both sides)
+constexpr int BT = 256;                      // output tile (both sides) of the full-size kernel
 constexpr int BKE = 32;                      // K elements per stage
 constexpr int ROWB = BKE * 2;                // bytes per staged row (64)
-constexpr int STAGE_BYTES = 2 * BT * ROWB;   // 32 KiB
-constexpr int NSTAGE = 5;                    // 160 KiB of LDS
+constexpr int NSTAGE = 5;                    // 160 KiB of LDS (80 KiB on 128 x 128 tiles)
 
 typedef __attribute__((address_space(3))) uint8_t lds_byte;
 
@@ -163,17 +163,20 @@ __device__ __forceinline__ int swz(int r) { return ((r >> 1 ^ r >> 3) & 1) | (((
 // are not waited for)
 #define MFSDP_WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xF | (7 << 4) | (0 << 8) | (3 << 14))
 
-constexpr int kGemmWaves = 8;  // waves per workgroup of the bf16 kernel
-// NW waves per workgroup arranged WM x WN over the 256 x 256 tile; each wave owns
-// (256 / WM) x (256 / WN) outputs as MI x NI blocks of 32 x 32. With 8 waves two share each SIMD,
-// so one can issue while the other waits.
-template <int NW>
+constexpr int kGemmWaves = 8;  // waves per workgroup of the bf16 kernel on 256 x 256 tiles
+constexpr int kGemmWavesSmall = 4;  // and on 128 x 128 tiles (two workgroups per CU)
+// NW waves per workgroup arranged WM x WN over the TB x TB tile; each wave owns
+// (TB / WM) x (TB / WN) outputs as MI x NI blocks of 32 x 32. Two waves share each SIMD (8 waves
+// of one workgroup, or 4 of each of two), so one can issue while the other waits.
+template <int NW, int TB>
 struct WaveGrid {
   static constexpr int WM = 2;
   static constexpr int WN = NW / 2;
-  static constexpr int MI = BT / (WM * 32);
-  static constexpr int NI = BT / (WN * 32);
-  static constexpr int LOADS = 32 / NW;  // DMA instructions per thread per stage
+  static constexpr int MI = TB / (WM * 32);
+  static constexpr int NI = TB / (WN * 32);
+  static constexpr int LOADS = 2 * TB / kBlkRows / NW;  // DMA instructions per thread per stage
+  static constexpr int STAGE = 2 * TB * ROWB;           // bytes per stage: P rows, then Q rows
+  static constexpr int SLOTS = TB == BT ? kGemmSlots : 2 * kGemmSlots;  // workgroups per XCD
 };
 
 // Per-tile state of the persistent kernel: operand sources of the DMA and the tile coordinates.
@@ -195,14 +198,14 @@ constexpr int kProdApply = 3;   // the last X' = B' X, applying the parameter up
 
 // (ca, cb, cc): this NS step's coefficients; the square product uses them as diagonal term, addend
 // factor and product factor (B' = cc A A + cb A + ca I).
-template <int NW, int PK>
-__global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
+template <int NW, int TB, int PK>
+__global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
                                                                const TileRef* __restrict__ sched,
                                                                int ngroups, int parity, int first,
                                                                int last, float ca, float cb,
                                                                float cc) {
-  using WG = WaveGrid<NW>;
-  constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS;
+  using WG = WaveGrid<NW, TB>;
+  constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS, STAGE_BYTES = WG::STAGE;
   constexpr int PL = LOADS / 2;        // DMA instructions for P (and for Q) per thread per stage
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NSTAGE * STAGE_BYTES];
 
@@ -211,7 +214,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   const int lane = t & 63, w = t >> 6;
   const int wm = w / WG::WN, wn = w % WG::WN;
   // DMA mapping: instruction c of wave w covers staged rows j * 16 + lane / 4 with j = c * NW + w;
-  // j < 16 are P rows, j >= 16 the rows j - 16 of Q. Lane slot = lane % 4 holds global chunk
+  // j < TB / 16 are P rows, the others the rows j - TB / 16 of Q. Lane slot = lane % 4 holds global chunk
   // slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
   const int drow = w * 16 + (lane >> 2);
   const int dchunk = (lane & 3) ^ swz(lane >> 2);
@@ -220,7 +223,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   // next non-idle tile of this workgroup at or after group g (g advances by kGemmXcds)
   auto next_tile = [&](int& g, TileCtx& c) -> bool {
     for (; g < ngroups; g += kGemmXcds) {
-      const TileRef r = sched[g * kGemmSlots + slot];
+      const TileRef r = sched[g * WG::SLOTS + slot];
       if (r.e < 0) continue;
       const GemmDesc& dd = descs[r.e];
       c.d = &dd;
@@ -234,8 +237,8 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       const int64_t k0 = int64_t(c.nk) * (nks > 1 ? r.ks : 0) * (kBlkRows * BKE);
       const uint16_t* P = static_cast<const uint16_t*>(dd.P[parity]);
       const uint16_t* Q = static_cast<const uint16_t*>(dd.Q[parity]);
-      c.psrc = P + blk_index(int64_t(c.bi) * BT + drow, dchunk * 8, dd.ldp) + k0;
-      c.qsrc = Q + blk_index(int64_t(c.bj) * BT + drow, dchunk * 8, dd.ldq) + k0;
+      c.psrc = P + blk_index(int64_t(c.bi) * TB + drow, dchunk * 8, dd.ldp) + k0;
+      c.qsrc = Q + blk_index(int64_t(c.bj) * TB + drow, dchunk * 8, dd.ldq) + k0;
       c.pstep = int64_t(NW * kBlkRows) * dd.ldp;  // NW row panels further down
       c.qstep = int64_t(NW * kBlkRows) * dd.ldq;
       return true;
@@ -250,7 +253,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       __builtin_amdgcn_global_load_lds(c.psrc + i * c.pstep + koff, sb + i * NW * 1024, 16, 0, 0);
 #pragma unroll
     for (int i = 0; i < PL; ++i)
-      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + 16384 + i * NW * 1024, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + TB * ROWB + i * NW * 1024, 16, 0, 0);
   };
   // steps 0 .. NSTAGE-2 of a tile into stages 0 .. NSTAGE-2 (steps past the end are clamped to the
   // last one: in-bounds reloads into stages nobody reads)
@@ -262,7 +265,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
   // fragment reads: row (base + lane % 32), chunk q = 2 kk + lane / 32 at slot q ^ swz(lane % 32)
   const int frow = lane & 31, fhalf = lane >> 5;
   const int pbase = (wm * (MI * 32) + frow) * ROWB;
-  const int qbase = (BT + wn * (NI * 32) + frow) * ROWB;
+  const int qbase = (TB + wn * (NI * 32) + frow) * ROWB;
   const int slot0 = ((0 + fhalf) ^ swz(frow)) * 16;
   const int slot1 = ((2 + fhalf) ^ swz(frow)) * 16;
   constexpr int NMF = MI * NI;      // MFMAs per 16-wide K slice
@@ -373,7 +376,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         // second pass forms A
         typedef float f32x4s __attribute__((ext_vector_type(4)));
         typedef __attribute__((address_space(1))) f32x4s gf4s;
-        float* part = dd.part + (int64_t(upper_index(bi, bj, dd.tiles_m)) * dd.nks + cur.ks) * (BT * BT);
+        float* part = dd.part + (int64_t(upper_index(bi, bj, dd.tiles_m)) * dd.nks + cur.ks) * (TB * TB);
         static_for<MI>([&](auto mi_c) {
           constexpr int mi = decltype(mi_c)::value;
           const int il = wm * (MI * 32) + mi * 32 + frow;
@@ -382,7 +385,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
             static_for<4>([&](auto gg_c) {
               constexpr int gg = decltype(gg_c)::value;
               const int jl = wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
-              *(gf4s*)(part + il * BT + jl) = f32x4s{acc[mi][ni][4 * gg], acc[mi][ni][4 * gg + 1],
+              *(gf4s*)(part + il * TB + jl) = f32x4s{acc[mi][ni][4 * gg], acc[mi][ni][4 * gg + 1],
                                                      acc[mi][ni][4 * gg + 2], acc[mi][ni][4 * gg + 3]};
             });
           });
@@ -426,7 +429,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         if (q_hi) { v0 = y0; v1 = y1; } else { v2 = y0; v3 = y1; }
       }
     };
-    if (PK == kProdApply && fa->param_dtype == kDtBF16 && (fa->n & 7) == 0) {
+    if (PK == kProdApply && TB == BT && fa->param_dtype == kDtBF16 && (fa->n & 7) == 0) {
       // Fused update of a bf16 parameter with n % 8 == 0, staged through the LDS stage the next
       // tile's prologue leaves free (32 KiB of fp32 per round), so that each wave reads and writes
       // whole parameter row segments with 16-byte lanes: p <- p (1 - lr wd) - lr f O in fp32 from
@@ -599,7 +602,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       // 1 KiB * (8 (sr / 16) + c / 32)), 64-byte block rows whose 16-byte chunks are swizzled by
       // swz(row % 16)
       auto slab_off = [](int sr, int c) -> int {
-        return ((((sr >> 4) << 3) + (c >> 5)) << 10) + ((sr & 15) << 6) +
+        return (((sr >> 4) * (TB / 32) + (c >> 5)) << 10) + ((sr & 15) << 6) +
                ((((c & 31) >> 3) ^ swz(sr & 15)) << 4) + ((c & 7) << 1);
       };
       // this lane's slab writes: row wm * 32 + frow, columns wn * 64 + ni * 32 + gg * 8 + fhalf * 4
@@ -614,16 +617,16 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       // ds_read_b64_tr_b16 of slab rows 8 g + r (+ 4), r = 0..3, columns 4 c .. 4 c + 3 (lane of
       // the 16-lane group = 4 r + c)
       const int tg = ln >> 4, til = ln & 15, tr_r = (ln >> 2) & 3, tr_c = ln & 3;
-      constexpr int BPW = 32 / NW;  // blocks of a slab stored per wave
+      constexpr int BPW = 4 * (TB / 32) / NW;  // blocks of a slab (64 rows) stored per wave
       const float* dscale = dd.scale;
       (void)dscale;
       const int ldc32 = int(ldc), ldtd32 = int(ldtd);
-      gu16* Ct = C ? C + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, ldc) : nullptr;
-      gu16* Tt = TD ? TD + blk_index(int64_t(bj) * BT, int64_t(bi) * BT, ldtd) : nullptr;
+      gu16* Ct = C ? C + blk_index(int64_t(bi) * TB, int64_t(bj) * TB, ldc) : nullptr;
+      gu16* Tt = TD ? TD + blk_index(int64_t(bj) * TB, int64_t(bi) * TB, ldtd) : nullptr;
       const gu16* Et = nullptr;
       int lde32 = 0;
       if constexpr (PK == kProdSquare) {
-        Et = E + blk_index(int64_t(bi) * BT, int64_t(bj) * BT, dd.lde);
+        Et = E + blk_index(int64_t(bi) * TB, int64_t(bj) * TB, dd.lde);
         lde32 = int(dd.lde);
       }
       // values of round mi into the slab; DIAG: this is a diagonal tile of the square product
@@ -686,7 +689,7 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
         if (Ct) {
 #pragma unroll
           for (int bb = 0; bb < BPW; ++bb) {
-            const int blk = w * BPW + bb, sp = blk >> 3, cb = blk & 7;
+            const int blk = w * BPW + bb, sp = blk / (TB / 32), cb = blk % (TB / 32);
             const u32x4 val = *(l4x*)(slab + (blk << 10) + rd_off);
             const int dr = (sp >> 1) * (MI * 32) + mi * 32 + (sp & 1) * 16 + row_in;
             *(gu4*)(Ct + int(blk_index(dr, cb * 32 + ch * 8, ldc32))) = val;
@@ -718,13 +721,13 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
       // values. (Compile-time loops: every acc index must be a constant for acc to stay in registers.)
       static_for<MI>([&](auto mi_c) {
         constexpr int mi = decltype(mi_c)::value;
-        const int64_t i = int64_t(bi) * BT + wm * (MI * 32) + mi * 32 + frow;
+        const int64_t i = int64_t(bi) * TB + wm * (MI * 32) + mi * 32 + frow;
         const int64_t iq = i - q;  // first row of this lane quad
         static_for<NI>([&](auto ni_c) {
           constexpr int ni = decltype(ni_c)::value;
           static_for<4>([&](auto gg_c) {
             constexpr int gg = decltype(gg_c)::value;
-            const int64_t j = int64_t(bj) * BT + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
+            const int64_t j = int64_t(bj) * TB + wn * (NI * 32) + ni * 32 + gg * 8 + fhalf * 4;
             float v0 = alpha * acc[mi][ni][4 * gg + 0];
             float v1 = alpha * acc[mi][ni][4 * gg + 1];
             float v2 = alpha * acc[mi][ni][4 * gg + 2];
@@ -748,33 +751,37 @@ __global__ __launch_bounds__(NW * 64, 1) void gemm_bf16_kernel(const GemmDesc* _
 #undef MFSDP_WAIT_VMCNT
 #undef MFSDP_WAIT_LGKM0
 
-// Second pass of a split Gram product: one 256-thread workgroup per (job, 16-row slab of the tile).
-// Thread t adds the nks partials of 4 consecutive columns 4 (t % 64) of rows t / 64 + 4 i in range
-// order, scales as the Gram epilogue does and stores 8 bytes of bf16 into the tile; an off-diagonal
-// tile's slab also goes through LDS to its mirror, where it is one 32-byte row piece per tile column.
+// Second pass of a split Gram product (TB x TB tiles): one 256-thread workgroup per (job, 16-row
+// slab of the tile). Thread t adds the nks partials of 4 consecutive columns 4 (t % (TB / 4)) of rows
+// t / (TB / 4) + (1024 / TB) i in range order, scales as the Gram epilogue does and stores 8 bytes of
+// bf16 into the tile; an off-diagonal tile's slab also goes through LDS to its mirror, where it is one
+// 32-byte row piece per tile column (threads t < TB).
 constexpr int kSumSlab = 16;
+template <int TB>
 __global__ __launch_bounds__(256) void gram_sum_kernel(const GemmDesc* __restrict__ descs,
                                                        const TileRef* __restrict__ jobs, int parity,
                                                        int first) {
   typedef float f32x4s __attribute__((ext_vector_type(4)));
   typedef __attribute__((address_space(1))) const f32x4s gcf4s;
-  __shared__ float tt[kSumSlab][BT + 1];
-  const TileRef job = jobs[blockIdx.x / (BT / kSumSlab)];
-  const int slab = blockIdx.x % (BT / kSumSlab);
+  constexpr int TPR = TB / 4;          // threads per row
+  constexpr int RPP = 256 / TPR;       // rows per pass
+  __shared__ float tt[kSumSlab][TB + 1];
+  const TileRef job = jobs[blockIdx.x / (TB / kSumSlab)];
+  const int slab = blockIdx.x % (TB / kSumSlab);
   const GemmDesc& dd = descs[job.e];
   const int bi = job.bi, bj = job.bj, nks = dd.nks;
   const float alpha = dd.alpha * (first ? scale_pow(dd.scale, dd.alpha_scale_pow) : 1.0f);
-  const float* part = dd.part + int64_t(upper_index(bi, bj, dd.tiles_m)) * nks * (BT * BT);
+  const float* part = dd.part + int64_t(upper_index(bi, bj, dd.tiles_m)) * nks * (TB * TB);
   gu16* C = (gu16*)dd.C[parity];
   const int64_t ldc = dd.ldc;
-  const int t = threadIdx.x, c4 = (t & 63) * 4;
+  const int t = threadIdx.x, c4 = (t % TPR) * 4;
 #pragma unroll
-  for (int i = 0; i < kSumSlab / 4; ++i) {
-    const int rl = (t >> 6) + 4 * i, r = slab * kSumSlab + rl;
-    f32x4s a = *(gcf4s*)(part + r * BT + c4);
-    for (int ks = 1; ks < nks; ++ks) a += *(gcf4s*)(part + int64_t(ks) * (BT * BT) + r * BT + c4);
+  for (int i = 0; i < kSumSlab / RPP; ++i) {
+    const int rl = t / TPR + RPP * i, r = slab * kSumSlab + rl;
+    f32x4s a = *(gcf4s*)(part + r * TB + c4);
+    for (int ks = 1; ks < nks; ++ks) a += *(gcf4s*)(part + int64_t(ks) * (TB * TB) + r * TB + c4);
     a *= alpha;
-    *(gu2*)(C + blk_index(int64_t(bi) * BT + r, int64_t(bj) * BT + c4, ldc)) =
+    *(gu2*)(C + blk_index(int64_t(bi) * TB + r, int64_t(bj) * TB + c4, ldc)) =
         u32x2{pack_bf16x2(a[0], a[1]), pack_bf16x2(a[2], a[3])};
     tt[rl][c4] = a[0];
     tt[rl][c4 + 1] = a[1];
@@ -783,12 +790,13 @@ __global__ __launch_bounds__(256) void gram_sum_kernel(const GemmDesc* __restric
   }
   if (bi == bj) return;  // (uniform) the diagonal tile is whole
   __syncthreads();
-  // mirror row bj * 256 + t, columns bi * 256 + kSumSlab slab .. + kSumSlab - 1: part of one row of a
+  if (t >= TB) return;
+  // mirror row bj * TB + t, columns bi * TB + kSumSlab slab .. + kSumSlab - 1: part of one row of a
   // 16 x 32 block
   uint32_t w[kSumSlab / 2];
 #pragma unroll
   for (int k = 0; k < kSumSlab / 2; ++k) w[k] = pack_bf16x2(tt[2 * k][t], tt[2 * k + 1][t]);
-  gu4* dst = (gu4*)(C + blk_index(int64_t(bj) * BT + t, int64_t(bi) * BT + slab * kSumSlab, ldc));
+  gu4* dst = (gu4*)(C + blk_index(int64_t(bj) * TB + t, int64_t(bi) * TB + slab * kSumSlab, ldc));
 #pragma unroll
   for (int k = 0; k < kSumSlab / 8; ++k) dst[k] = u32x4{w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]};
 }
@@ -906,24 +914,36 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const GemmDesc* __restric
 
 }  // namespace
 
+template <int NW, int TB, int PK>
+void launch_bf16(const GemmDesc* d_descs, const TileRef* d_sched, int ngroups, int parity, int first_step,
+                 int last_step, float ca, float cb, float cc, hipStream_t st) {
+  hipLaunchKernelGGL((gemm_bf16_kernel<NW, TB, PK>), dim3(kGemmXcds * WaveGrid<NW, TB>::SLOTS),
+                     dim3(NW * 64), 0, st, d_descs, d_sched, ngroups, parity, first_step, last_step, ca,
+                     cb, cc);
+}
+
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
                        int ngroups, int ns_dtype, int product, int parity, int first_step,
-                       int last_step, float ca, float cb, float cc, hipStream_t st) {
+                       int last_step, float ca, float cb, float cc, int tile, hipStream_t st) {
   if (total_tiles <= 0) return hipSuccess;
   if (ns_dtype == kDtBF16) {
-    const dim3 grid(kGemmXcds * kGemmSlots), block(kGemmWaves * 64);
-    if (product == kProdGram)
-      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdGram>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
+    constexpr int W = kGemmWaves;
+    constexpr int WS = kGemmWavesSmall, TS = kTileBF16Small;
+    if (tile == TS) {
+      if (product == kProdGram)
+        launch_bf16<WS, TS, kProdGram>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
+      else if (product == kProdSquare)
+        launch_bf16<WS, TS, kProdSquare>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
+      else
+        return hipErrorInvalidValue;
+    } else if (product == kProdGram)
+      launch_bf16<W, BT, kProdGram>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
     else if (product == kProdSquare)
-      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdSquare>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
+      launch_bf16<W, BT, kProdSquare>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
     else if (product == kProdUpdate)
-      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdUpdate>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
+      launch_bf16<W, BT, kProdUpdate>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
     else
-      hipLaunchKernelGGL((gemm_bf16_kernel<kGemmWaves, kProdApply>), grid, block, 0, st,
-                         d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc);
+      launch_bf16<W, BT, kProdApply>(d_descs, d_sched, ngroups, parity, first_step, last_step, ca, cb, cc, st);
   } else
     hipLaunchKernelGGL(gemm_f32_kernel, dim3(total_tiles), dim3(256), 0, st, d_descs, count,
                        parity, first_step, last_step, ca, cb, cc);
@@ -931,10 +951,14 @@ hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, cons
 }
 
 hipError_t launch_gram_sum(const GemmDesc* d_descs, const TileRef* d_jobs, int njobs, int parity,
-                           int first, hipStream_t st) {
+                           int first, int tile, hipStream_t st) {
   if (njobs <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gram_sum_kernel, dim3(njobs * (BT / kSumSlab)), dim3(256), 0, st, d_descs, d_jobs,
-                     parity, first);
+  if (tile == kTileBF16Small)
+    hipLaunchKernelGGL(gram_sum_kernel<kTileBF16Small>, dim3(njobs * (kTileBF16Small / kSumSlab)), dim3(256),
+                       0, st, d_descs, d_jobs, parity, first);
+  else
+    hipLaunchKernelGGL(gram_sum_kernel<BT>, dim3(njobs * (BT / kSumSlab)), dim3(256), 0, st, d_descs,
+                       d_jobs, parity, first);
   return hipGetLastError();
 }
 

@@ -267,6 +267,7 @@ struct Plan {
   std::vector<int> order[3];
   std::vector<TileRef> sched[3];
   int tiles[3] = {0, 0, 0};
+  int tile[3] = {0, 0, 0};     // output tile of each product's launch
   std::vector<int> split;      // per Gram problem (launch order): K ranges per tile
   std::vector<size_t> part;    // per Gram problem: offset of its partial tiles (split ones)
   std::vector<TileRef> jobs;   // the split problems' upper tiles (second pass)
@@ -276,7 +277,9 @@ struct Plan {
 
 // On the bf16 path a Gram launch with fewer tiles than the persistent grid has workgroups may split
 // long contractions (gram_splits); the split problems' partial tiles follow the per-matrix buffers
-// and take at most a quarter of their bytes.
+// and take at most a quarter of their bytes. When the r x r products' 128 x 128 tiles fit one round
+// of the two-workgroups-per-CU grid, the Gram and square launches run on those (small shares: four
+// times the tiles of launches that would leave most CUs idle, each with a quarter of the epilogue).
 template <typename ShapeAt>
 Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   Plan P;
@@ -286,9 +289,18 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
     shape_at(i, m, n);
     shapes.push_back(plan_ns(m, n, ns_dtype, 0));
   }
-  const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
+  const bool bf = ns_dtype == MFSDP_BF16;
+  int64_t small_tiles = 0;  // upper 128 x 128 tiles of the r x r products
+  for (const NsPlan& p : shapes) {
+    const int64_t t = p.r_pad / kTileBF16Small;
+    small_tiles += t * (t + 1) / 2;
+  }
+  const int64_t small_slots = int64_t(kGemmXcds) * 2 * kGemmSlots;
   size_t sched_bytes[3] = {0, 0, 0};
   for (int ph = 0; ph < 3; ++ph) {
+    const bool small = bf && ph < 2 && small_tiles <= small_slots;
+    const int tile = !bf ? kTileF32 : small ? kTileBF16Small : kTileBF16;
+    P.tile[ph] = tile;
     P.order[ph] = phase_order(shapes, ph);
     std::vector<TileGrid> grids;
     std::vector<int> pos;
@@ -310,8 +322,9 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
         for (int64_t c : cost) kl.push_back(c);
         size_t base = 0;
         for (const NsPlan& q : shapes) base += q.bytes;
-        const size_t part_bytes = size_t(kTileBF16) * kTileBF16 * sizeof(float);
-        P.split = gram_splits(tl, kl, int64_t(base / 4 / part_bytes));
+        const size_t part_bytes = size_t(tile) * tile * sizeof(float);
+        P.split = gram_splits(tl, kl, int64_t(base / 4 / part_bytes),
+                              small ? small_slots : int64_t(kGemmXcds) * kGemmSlots);
       }
       for (int k = 0; k < int(count); ++k)
         if (P.split[size_t(k)] > 1)
@@ -319,11 +332,15 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
             for (int bj = bi; bj < grids[size_t(k)].tm; ++bj)
               P.jobs.push_back(TileRef{k, int16_t(bi), int16_t(bj), 0, 0});
     }
-    if (ns_dtype == MFSDP_BF16) P.sched[ph] = build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr);
+    if (bf)
+      P.sched[ph] = small ? build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr, 2 * kGemmSlots,
+                                           2 * kGroupRows)
+                          : build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr);
     sched_bytes[ph] = P.sched[ph].size() * sizeof(TileRef);
   }
   P.dl = plan_descs(count, sched_bytes, int(P.jobs.size()));
-  for (int ph = 0; ph < 3; ++ph) P.dl.ngroups[ph] = int(P.sched[ph].size() / kGemmSlots);
+  for (int ph = 0; ph < 3; ++ph)
+    P.dl.ngroups[ph] = int(P.sched[ph].size() / (P.tile[ph] == kTileBF16Small ? 2 * kGemmSlots : kGemmSlots));
   size_t o = P.dl.bytes;
   for (int64_t i = 0; i < count; ++i) {
     P.ns.push_back(plan_ns(shapes[i].m, shapes[i].n, ns_dtype, o));
@@ -333,9 +350,9 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
   for (int k = 0; k < int(count); ++k) {
     const int f = P.split[size_t(k)];
     if (f <= 1) continue;
-    const int64_t tr = shapes[size_t(P.order[0][size_t(k)])].r_pad / kTileBF16;
+    const int64_t tr = shapes[size_t(P.order[0][size_t(k)])].r_pad / P.tile[0];
     P.part[size_t(k)] = o;
-    o += align_up(size_t(tr * (tr + 1) / 2) * size_t(f) * kTileBF16 * kTileBF16 * sizeof(float));
+    o += align_up(size_t(tr * (tr + 1) / 2) * size_t(f) * P.tile[0] * P.tile[0] * sizeof(float));
   }
   P.bytes = o;
   return P;
@@ -358,9 +375,10 @@ bool apply_fused(int ns_dtype, int steps) { return ns_dtype == MFSDP_BF16 && ste
 
 // Descriptors of the three products, stored in the phase's problem order; the schedules refer
 // to problems by that position.
-void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, uint8_t* h, int tile) {
+void fill_gemm_descs(const Plan& P, uint8_t* ws, const mfsdp_muon_hparams& hp, uint8_t* h) {
   const int n = int(P.ns.size());
   for (int phase = 0; phase < 3; ++phase) {
+    const int tile = P.tile[phase];
     GemmDesc* out = reinterpret_cast<GemmDesc*>(h + P.dl.off_gemm[phase]);
     const std::vector<int>& ord = P.order[phase];
     int begin = 0;
@@ -505,12 +523,13 @@ int enqueue_pipeline(const Plan& P, uint8_t* ws, int slot, int steps, const doub
       e = launch_gemm(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[ph]), count, P.tiles[ph],
                       reinterpret_cast<const TileRef*>(ws + dl.off_sched[ph]), dl.ngroups[ph],
                       ns_dtype, kind, k & 1, k == 0 ? 1 : 0, k == steps - 1 ? 1 : 0,
-                      float(coeffs[3 * k]), float(coeffs[3 * k + 1]), float(coeffs[3 * k + 2]), st);
+                      float(coeffs[3 * k]), float(coeffs[3 * k + 1]), float(coeffs[3 * k + 2]), P.tile[ph],
+                      st);
       if (e != hipSuccess) return hip_fail(e, "NS GEMM launch");
       if (ph == 0 && dl.njobs > 0) {
         e = launch_gram_sum(reinterpret_cast<const GemmDesc*>(ws + dl.off_gemm[0]),
                             reinterpret_cast<const TileRef*>(ws + dl.off_jobs), dl.njobs, k & 1,
-                            k == 0 ? 1 : 0, st);
+                            k == 0 ? 1 : 0, P.tile[0], st);
         if (e != hipSuccess) return hip_fail(e, "split Gram sum launch");
       }
     }
@@ -684,8 +703,7 @@ int muon_impl(const mfsdp_muon_entry* entries, int64_t count, const mfsdp_muon_h
                           float(1.0 - hp->lr * hp->weight_decay), float(hp->lr * f), apply_tiles);
     apply_tiles += apply[i].tiles_m * apply[i].tiles_n;
   }
-  const int tile = hp->ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
-  fill_gemm_descs(P, ws, *hp, h, tile);
+  fill_gemm_descs(P, ws, *hp, h);
   const std::vector<double> coeffs = step_coeffs(hp->a, hp->b, hp->c, hp->ns_steps, hp->ns_schedule);
   return enqueue_pipeline(P, ws, slot, hp->ns_steps, coeffs.data(), hp->ns_dtype, hp->momentum,
                           hp->nesterov, hp->eps, prep_tiles, apply_tiles, st, events, ra != nullptr,
@@ -773,8 +791,7 @@ int ns_impl(const void* x, int32_t x_dtype, void* out, int32_t out_dtype, int64_
   mfsdp_muon_hparams hp{};
   hp.ns_steps = steps;
   hp.ns_dtype = ns_dtype;
-  const int tile = ns_dtype == MFSDP_BF16 ? kTileBF16 : kTileF32;
-  fill_gemm_descs(P, ws, hp, h, tile);
+  fill_gemm_descs(P, ws, hp, h);
   return enqueue_pipeline(P, ws, slot, steps, coeffs, ns_dtype, 0.0, 0, eps,
                           p.prep_tiles_m * p.prep_tiles_n, apply[0].tiles_m * apply[0].tiles_n, st,
                           nullptr);

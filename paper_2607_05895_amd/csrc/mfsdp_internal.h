@@ -157,20 +157,25 @@ hipError_t launch_norm(const NormDesc* d_descs, int count, float eps, hipStream_
 // product: 0 Gram, 1 square, 2 update (the order of the products in one NS step); 3 the last update
 // of the bf16 path with the fused parameter update (its descriptors carry `fused`)
 // (ca, cb, cc): the NS step's coefficients (a_k, b_k, c_k), used by the square product.
+// tile: the bf16 path's output tile, kTileBF16 or (Gram and square products only) kTileBF16Small;
+// the descriptors' tile grids and the schedule are in that tile.
 hipError_t launch_gemm(const GemmDesc* d_descs, int count, int total_tiles, const TileRef* d_sched,
                        int ngroups, int ns_dtype, int product, int parity, int first_step,
-                       int last_step, float ca, float cb, float cc, hipStream_t st);
+                       int last_step, float ca, float cb, float cc, int tile, hipStream_t st);
 hipError_t launch_apply(const ApplyDesc* d_descs, int count, int total_tiles, int ns_dtype,
                         hipStream_t st);
 // The second pass of a split Gram product: for each job (problem e in the Gram launch's order,
 // upper tile bi <= bj) the problem's nks partial tiles added in range order, scaled as the Gram
 // epilogue scales, stored as A (bf16) at (bi, bj) and mirrored at (bj, bi).
 hipError_t launch_gram_sum(const GemmDesc* d_descs, const TileRef* d_jobs, int njobs, int parity,
-                           int first, hipStream_t st);
+                           int first, int tile, hipStream_t st);
 hipError_t launch_adamw(const AdamWBatch& batch, int total_blocks, hipStream_t st);
 
 // NS tile sizes (padding granularity of the workspace buffers).
 constexpr int kTileBF16 = 256;
+// The bf16 Gram and square products of a launch with few 256 x 256 tiles run on 128 x 128 tiles,
+// two workgroups per CU (the padding stays 256).
+constexpr int kTileBF16Small = 128;
 constexpr int kTileF32 = 64;
 constexpr int kPrepRows = 64;                    // prep tile rows
 constexpr int kPrepColsBF16 = 256;              // prep tile columns on the bf16 path (divides 256)

@@ -2,7 +2,8 @@
 // once (upper triangle only for symmetric products; every K range of a split problem's tile once),
 // whole rounds of XCD groups, every group's tiles on one XCD, the deal's balance (the busiest XCD
 // within one group of the mean), and determinism; random launches plus the owner shares' own
-// launches; the Gram launches' K splits (gram_splits) on hand-worked cases. Exit code 0 on
+// launches, on the 256 x 256 grid (one workgroup per CU) and the 128 x 128 one (two); the Gram
+// launches' K splits (gram_splits) on hand-worked cases. Exit code 0 on
 // success; every failure prints what it found.
 #include <cstdio>
 #include <map>
@@ -25,15 +26,16 @@ static int g_fail = 0;
   } while (0)
 
 static void check_launch(const std::vector<TileGrid>& grids, const std::vector<int64_t>& cost,
-                         const std::vector<int>* splits = nullptr) {
+                         const std::vector<int>* splits = nullptr, int slots = kGemmSlots,
+                         int group_rows = kGroupRows) {
   std::vector<int> pos(grids.size());
   for (size_t k = 0; k < pos.size(); ++k) pos[k] = int(k);
   auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
-  const std::vector<TileRef> s = build_schedule(pos, grids, cost, splits);
-  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost, splits);
+  const std::vector<TileRef> s = build_schedule(pos, grids, cost, splits, slots, group_rows);
+  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost, splits, slots, group_rows);
   CHECK(s.size() == s2.size() && std::memcmp(s.data(), s2.data(), s.size() * sizeof(TileRef)) == 0,
         "not deterministic");
-  const size_t round = size_t(kGemmXcds) * kGemmSlots;
+  const size_t round = size_t(kGemmXcds) * size_t(slots);
   CHECK(s.size() % round == 0, "%zu slots: not whole rounds", s.size());
   std::map<std::tuple<int, int, int, int>, int> seen;
   int64_t load[kGemmXcds] = {};
@@ -42,10 +44,10 @@ static void check_launch(const std::vector<TileGrid>& grids, const std::vector<i
     const TileGrid& g = grids[e];
     ntiles += (g.sym ? int64_t(g.tm) * (g.tm + 1) / 2 : int64_t(g.tm) * g.tn) * nks(int(e));
   }
-  for (size_t g = 0; g < s.size() / kGemmSlots; ++g) {
+  for (size_t g = 0; g < s.size() / size_t(slots); ++g) {
     int64_t gc = 0;
-    for (int sl = 0; sl < kGemmSlots; ++sl) {
-      const TileRef& t = s[g * kGemmSlots + sl];
+    for (int sl = 0; sl < slots; ++sl) {
+      const TileRef& t = s[g * size_t(slots) + size_t(sl)];
       if (t.e < 0) continue;
       CHECK(t.e < int(grids.size()), "problem %d", t.e);
       const TileGrid& gr = grids[t.e];
@@ -100,6 +102,7 @@ int main() {
     }
     std::stable_sort(cost.begin(), cost.end(), std::greater<int64_t>());
     check_launch(grids, cost);
+    check_launch(grids, cost, nullptr, 2 * kGemmSlots, 2 * kGroupRows);
   }
   std::printf("random launches: ok\n");
   share("gpt2_small_share", {{768, 768}, {768, 768}, {768, 768}, {768, 768}, {768, 768}, {768, 768},
@@ -145,6 +148,15 @@ int main() {
     int64_t p3 = 0;
     for (int i = 0; i < 12; ++i) p3 += g3[i] > 1 ? tl[i] * g3[i] : 0;
     CHECK(p3 <= 60, "GPT-2 share under a 60-tile budget: %lld partial tiles", (long long)p3);
+    // the same share's Gram launch on 128 x 128 tiles (21 upper tiles per matrix) and the grid of
+    // two workgroups per CU: the 768 x 3072 matrices again in 4 ranges (504 tiles for 512 slots)
+    const int64_t small = int64_t(kGemmXcds) * 2 * kGemmSlots;
+    std::vector<int64_t> t128(12, 21);
+    const std::vector<int> f128 = gram_splits(t128, kl, INT64_MAX, small);
+    for (int i = 0; i < 12; ++i) CHECK(f128[i] == (i < 4 ? 4 : 1), "gpt2 share, 128: problem %d split %d", i, f128[i]);
+    std::vector<TileGrid> g128(12, TileGrid{6, 6, true});
+    check_launch(g128, kl, &f128, 2 * kGemmSlots, 2 * kGroupRows);
+    CHECK(gram_splits({528}, {4096}, INT64_MAX, small)[0] == 1, "a full 128 x 128 launch was split");
   }
   std::printf("gram splits: ok\n");
   if (g_fail) {

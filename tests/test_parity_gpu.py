@@ -188,9 +188,10 @@ def test_muon_gpt2_small_share(native):
 
 @pytest.mark.parametrize("shape", [(2048, 4096), (4096, 2048), (1024, 4096), (2048, 2048)])
 def test_muon_single_matrix_few_tiles(native, shape):
-    """One matrix alone in a call, so that each launch has fewer tiles than the GPU has CUs
-    (2048 x 4096: 36 / 36 / 128 tiles, wide and tall, the last update with the fused parameter
-    update). Matches the oracle and is bitwise reproducible."""
+    """One matrix alone in a call, so that each launch has fewer 256 x 256 tiles than the GPU has
+    CUs (2048 x 4096: 36 / 36 / 128, wide and tall, the last update with the fused parameter update);
+    the Gram and square launches run on 128 x 128 tiles (136 upper ones; the Gram's K = 4096 in 2
+    ranges). Matches the oracle and is bitwise reproducible."""
     import torch
     m, n = shape
     _say(f"muon single matrix {m}x{n}")
@@ -206,14 +207,32 @@ def test_muon_single_matrix_few_tiles(native, shape):
 
 
 def test_muon_split_gram_contraction(native):
-    """Two 1024 x 8192 matrices (wide and tall) alone in a call: their Gram launch has 20 tiles with
-    K = 8192, so the contraction is split into K ranges (as many as the partial-tile budget, a
-    quarter of the per-matrix buffers, allows); each range's fp32 partial tile is added in order by
-    the second pass. Matches the oracle and is bitwise reproducible."""
+    """Two 1024 x 8192 matrices (wide and tall) alone in a call: their Gram launch runs on 128 x 128
+    tiles (72 upper ones, K = 8192), so the contraction is split into K ranges (4 of 2048, within the
+    partial-tile budget of a quarter of the per-matrix buffers); each range's fp32 partial tile is
+    added in order by the second pass. Matches the oracle and is bitwise reproducible."""
     import torch
     _say("muon split Gram contraction: 1024x8192, 8192x1024")
     rng = np.random.default_rng(5100)
     specs = [synth.MuonSpec(1024, 8192, "wide"), synth.MuonSpec(8192, 1024, "tall")]
+    tensors = [synth.random_muon_tensors(rng, e.m, e.n) for e in specs]
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
+    dev = _run_muon(native, tensors, specs, hp)
+    _check_muon(tensors, specs, dev, hp, 2e-2)
+    dev2 = _run_muon(native, tensors, specs, hp)
+    for a, b in zip(dev[0], dev2[0]):
+        assert torch.equal(a, b)
+
+
+def test_muon_split_gram_contraction_full_size_tiles(native):
+    """A 4096 x 4096 and a 1024 x 8192 matrix in one call: too many 128 x 128 tiles for one round
+    (528 + 36), so every launch runs on 256 x 256 tiles, and the Gram launch (146 tiles) splits the
+    1024 x 8192 matrix's K = 8192 into 2 ranges, summed by the 256 x 256 second pass. Matches the
+    oracle and is bitwise reproducible."""
+    import torch
+    _say("muon split Gram contraction on 256 x 256 tiles: 4096x4096, 1024x8192")
+    rng = np.random.default_rng(5200)
+    specs = [synth.MuonSpec(4096, 4096, "square"), synth.MuonSpec(1024, 8192, "wide")]
     tensors = [synth.random_muon_tensors(rng, e.m, e.n) for e in specs]
     hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
     dev = _run_muon(native, tensors, specs, hp)
