@@ -41,11 +41,15 @@ struct TileGrid {
 // largest K among its tiles: its tiles run side by side). Group g of the result runs on XCD
 // g % kGemmXcds; XCDs with fewer groups get empty ones (every slot e = -1).
 // splits (optional, per problem): the number of K ranges each tile of the problem is cut into; the
-// ranges of one tile are listed together and each costs cost / splits.
+// ranges of one tile are listed together and each costs cost / splits. fill (<= slots, default
+// slots): tiles per group; a group's remaining slots stay idle, which spreads a launch with few
+// tiles over more XCDs.
 inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const std::vector<TileGrid>& grids,
                                            const std::vector<int64_t>& cost,
                                            const std::vector<int>* splits = nullptr,
-                                           int slots = kGemmSlots, int group_rows = kGroupRows) {
+                                           int slots = kGemmSlots, int group_rows = kGroupRows,
+                                           int fill = 0) {
+  if (fill <= 0 || fill > slots) fill = slots;
   auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
   std::vector<TileRef> flat;
   for (int e : order) {
@@ -57,6 +61,15 @@ inline std::vector<TileRef> build_schedule(const std::vector<int>& order, const 
           if (!g.sym || r <= c)
             for (int ks = 0; ks < nks(e); ++ks) flat.push_back(TileRef{e, int16_t(r), int16_t(c), int16_t(ks), 0});
     }
+  }
+  if (fill < slots) {  // spread: fill tiles, then slots - fill idle ones, per group
+    std::vector<TileRef> spread;
+    for (size_t i = 0; i < flat.size(); ++i) {
+      spread.push_back(flat[i]);
+      if ((i + 1) % size_t(fill) == 0 || i + 1 == flat.size())
+        while (spread.size() % size_t(slots)) spread.push_back(TileRef{-1, 0, 0, 0, 0});
+    }
+    flat.swap(spread);
   }
   while (flat.size() % size_t(slots)) flat.push_back(TileRef{-1, 0, 0, 0, 0});
   const size_t ng = flat.size() / size_t(slots);

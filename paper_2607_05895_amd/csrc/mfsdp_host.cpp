@@ -332,10 +332,16 @@ Plan make_plan(int64_t count, int ns_dtype, ShapeAt shape_at) {
             for (int bj = bi; bj < grids[size_t(k)].tm; ++bj)
               P.jobs.push_back(TileRef{k, int16_t(bi), int16_t(bj), 0, 0});
     }
-    if (bf)
-      P.sched[ph] = small ? build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr, 2 * kGemmSlots,
-                                           2 * kGroupRows)
-                          : build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr);
+    if (bf && small) {
+      // at most one tile per CU when they fit: groups of kGemmSlots tiles on the 2 x kGemmSlots slots
+      int64_t n = 0;
+      for (size_t k = 0; k < grids.size(); ++k)
+        n += int64_t(grids[k].tm) * (grids[k].tm + 1) / 2 * (ph == 0 ? P.split[k] : 1);
+      const int fill = n <= int64_t(kGemmXcds) * kGemmSlots ? kGemmSlots : 2 * kGemmSlots;
+      P.sched[ph] = build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr, 2 * kGemmSlots,
+                                   2 * kGroupRows, fill);
+    } else if (bf)
+      P.sched[ph] = build_schedule(pos, grids, cost, ph == 0 ? &P.split : nullptr);
     sched_bytes[ph] = P.sched[ph].size() * sizeof(TileRef);
   }
   P.dl = plan_descs(count, sched_bytes, int(P.jobs.size()));

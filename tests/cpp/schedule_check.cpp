@@ -27,12 +27,12 @@ static int g_fail = 0;
 
 static void check_launch(const std::vector<TileGrid>& grids, const std::vector<int64_t>& cost,
                          const std::vector<int>* splits = nullptr, int slots = kGemmSlots,
-                         int group_rows = kGroupRows) {
+                         int group_rows = kGroupRows, int fill = 0) {
   std::vector<int> pos(grids.size());
   for (size_t k = 0; k < pos.size(); ++k) pos[k] = int(k);
   auto nks = [&](int e) { return splits ? (*splits)[e] : 1; };
-  const std::vector<TileRef> s = build_schedule(pos, grids, cost, splits, slots, group_rows);
-  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost, splits, slots, group_rows);
+  const std::vector<TileRef> s = build_schedule(pos, grids, cost, splits, slots, group_rows, fill);
+  const std::vector<TileRef> s2 = build_schedule(pos, grids, cost, splits, slots, group_rows, fill);
   CHECK(s.size() == s2.size() && std::memcmp(s.data(), s2.data(), s.size() * sizeof(TileRef)) == 0,
         "not deterministic");
   const size_t round = size_t(kGemmXcds) * size_t(slots);
@@ -49,6 +49,7 @@ static void check_launch(const std::vector<TileGrid>& grids, const std::vector<i
     for (int sl = 0; sl < slots; ++sl) {
       const TileRef& t = s[g * size_t(slots) + size_t(sl)];
       if (t.e < 0) continue;
+      CHECK(fill <= 0 || sl < fill, "tile in slot %d of a group filled to %d", sl, fill);
       CHECK(t.e < int(grids.size()), "problem %d", t.e);
       const TileGrid& gr = grids[t.e];
       CHECK(t.bi >= 0 && t.bi < gr.tm && t.bj >= 0 && t.bj < gr.tn && (!gr.sym || t.bi <= t.bj),
@@ -103,6 +104,7 @@ int main() {
     std::stable_sort(cost.begin(), cost.end(), std::greater<int64_t>());
     check_launch(grids, cost);
     check_launch(grids, cost, nullptr, 2 * kGemmSlots, 2 * kGroupRows);
+    check_launch(grids, cost, nullptr, 2 * kGemmSlots, 2 * kGroupRows, kGemmSlots);
   }
   std::printf("random launches: ok\n");
   share("gpt2_small_share", {{768, 768}, {768, 768}, {768, 768}, {768, 768}, {768, 768}, {768, 768},
@@ -156,6 +158,15 @@ int main() {
     for (int i = 0; i < 12; ++i) CHECK(f128[i] == (i < 4 ? 4 : 1), "gpt2 share, 128: problem %d split %d", i, f128[i]);
     std::vector<TileGrid> g128(12, TileGrid{6, 6, true});
     check_launch(g128, kl, &f128, 2 * kGemmSlots, 2 * kGroupRows);
+    // its square launch (252 tiles) spread to one tile per CU: 8 groups of at most 32, one per XCD
+    {
+      std::vector<int> pos(12);
+      for (int i = 0; i < 12; ++i) pos[i] = i;
+      const std::vector<int64_t> k768(12, 768);
+      const std::vector<TileRef> sq = build_schedule(pos, g128, k768, nullptr, 2 * kGemmSlots, 2 * kGroupRows, kGemmSlots);
+      CHECK(sq.size() == size_t(kGemmXcds) * 2 * kGemmSlots, "square spread: %zu slots", sq.size());
+      check_launch(g128, k768, nullptr, 2 * kGemmSlots, 2 * kGroupRows, kGemmSlots);
+    }
     CHECK(gram_splits({528}, {4096}, INT64_MAX, small)[0] == 1, "a full 128 x 128 launch was split");
   }
   std::printf("gram splits: ok\n");
