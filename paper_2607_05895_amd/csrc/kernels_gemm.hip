@@ -199,11 +199,9 @@ constexpr int kProdApply = 3;   // the last X' = B' X, applying the parameter up
 // (ca, cb, cc): this NS step's coefficients; the square product uses them as diagonal term, addend
 // factor and product factor (B' = cc A A + cb A + ca I).
 template <int NW, int TB, int PK>
-__global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(const GemmDesc* __restrict__ descs,
-                                                               const TileRef* __restrict__ sched,
-                                                               int ngroups, int parity, int first,
-                                                               int last, float ca, float cb,
-                                                               float cc) {
+__global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
+    const GemmDesc* __restrict__ descs, const TileRef* __restrict__ sched, int ngroups, int parity,
+    int first, int last, float ca, float cb, float cc) {
   using WG = WaveGrid<NW, TB>;
   constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS, STAGE_BYTES = WG::STAGE;
   constexpr int PL = LOADS / 2;        // DMA instructions for P (and for Q) per thread per stage
@@ -214,8 +212,8 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(co
   const int lane = t & 63, w = t >> 6;
   const int wm = w / WG::WN, wn = w % WG::WN;
   // DMA mapping: instruction c of wave w covers staged rows j * 16 + lane / 4 with j = c * NW + w;
-  // j < TB / 16 are P rows, the others the rows j - TB / 16 of Q. Lane slot = lane % 4 holds global chunk
-  // slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
+  // j < TB / 16 are P rows, the others the rows j - TB / 16 of Q. Lane slot = lane % 4 holds global
+  // chunk slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
   const int drow = w * 16 + (lane >> 2);
   const int dchunk = (lane & 3) ^ swz(lane >> 2);
   const int dma_wave_off = w * 1024;  // + c * NW * 1024 within a stage
@@ -253,7 +251,8 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(co
       __builtin_amdgcn_global_load_lds(c.psrc + i * c.pstep + koff, sb + i * NW * 1024, 16, 0, 0);
 #pragma unroll
     for (int i = 0; i < PL; ++i)
-      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + TB * ROWB + i * NW * 1024, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + TB * ROWB + i * NW * 1024, 16, 0,
+                                       0);
   };
   // steps 0 .. NSTAGE-2 of a tile into stages 0 .. NSTAGE-2 (steps past the end are clamped to the
   // last one: in-bounds reloads into stages nobody reads)
