@@ -242,6 +242,26 @@ def test_muon_split_gram_contraction_full_size_tiles(native):
         assert torch.equal(a, b)
 
 
+def test_muon_small_and_full_size_tiles_give_the_same_bits(native):
+    """Two 768 x 768 matrices stepped alone (their Gram and square launches run on 128 x 128 tiles)
+    and again next to a 4096 x 4096 matrix (too many 128 x 128 tiles: every launch on 256 x 256
+    tiles). Neither call splits a contraction, and each output element is accumulated over K in the
+    same order on either tile, so the 768 x 768 matrices' parameters, momenta and updates agree
+    bit for bit."""
+    import torch
+    _say("muon 128 x 128 vs 256 x 256 tiles: 2 x 768x768 alone and next to 4096x4096")
+    rng = np.random.default_rng(5300)
+    small = [synth.MuonSpec(768, 768, "a"), synth.MuonSpec(768, 768, "b")]
+    tensors = [synth.random_muon_tensors(rng, e.m, e.n) for e in small]
+    big = synth.MuonSpec(4096, 4096, "big")
+    hp = synth.MuonHParams(lr=0.02, weight_decay=0.01)
+    alone = _run_muon(native, tensors, small, hp)
+    mixed = _run_muon(native, tensors + [synth.random_muon_tensors(rng, big.m, big.n)], small + [big], hp)
+    for a, b in zip(alone, mixed[:2]):
+        for x, y in zip(a[:1] + a[2:], b[:1] + b[2:]):  # param, momentum, update
+            assert torch.equal(x, y)
+
+
 MIXED = [(256, 512), (512, 256), (384, 384), (100, 700), (700, 100), (130, 1000), (1, 50),
          (50, 1), (768, 3072), (3072, 768)]
 
