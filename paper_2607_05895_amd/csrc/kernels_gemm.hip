@@ -204,19 +204,25 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
     int first, int last, float ca, float cb, float cc) {
   using WG = WaveGrid<NW, TB>;
   constexpr int MI = WG::MI, NI = WG::NI, LOADS = WG::LOADS, STAGE_BYTES = WG::STAGE;
-  constexpr int PL = LOADS / 2;        // DMA instructions for P (and for Q) per thread per stage
+  // The first DW waves issue all of a stage's global->LDS loads (DLOADS each). With 8 waves that is
+  // the first four, one per SIMD: each SIMD then runs one wave that issues loads and one that
+  // never waits on their issue and keeps multiplying meanwhile.
+  constexpr int DW = NW == 8 ? 4 : NW;
+  constexpr int DLOADS = LOADS * NW / DW;
+  constexpr int PL = DLOADS / 2;       // DMA instructions for P (and for Q) per issuing thread
   __shared__ __attribute__((aligned(1024))) uint8_t smem[NSTAGE * STAGE_BYTES];
 
   const int xcd = blockIdx.x % kGemmXcds, slot = blockIdx.x / kGemmXcds;
   const int t = threadIdx.x;
   const int lane = t & 63, w = t >> 6;
   const int wm = w / WG::WN, wn = w % WG::WN;
-  // DMA mapping: instruction c of wave w covers staged rows j * 16 + lane / 4 with j = c * NW + w;
-  // j < TB / 16 are P rows, the others the rows j - TB / 16 of Q. Lane slot = lane % 4 holds global
-  // chunk slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
-  const int drow = w * 16 + (lane >> 2);
+  // DMA mapping: instruction c of issuing wave w covers staged rows j * 16 + lane / 4 with
+  // j = c * DW + w; j < TB / 16 are P rows, the others the rows j - TB / 16 of Q. Lane slot =
+  // lane % 4 holds global chunk slot ^ swz(row) (swz depends on row % 16 = lane / 4 only).
+  const bool issuer = w < DW;
+  const int drow = (w % DW) * 16 + (lane >> 2);
   const int dchunk = (lane & 3) ^ swz(lane >> 2);
-  const int dma_wave_off = w * 1024;  // + c * NW * 1024 within a stage
+  const int dma_wave_off = (w % DW) * 1024;  // + c * DW * 1024 within a stage
 
   // next non-idle tile of this workgroup at or after group g (g advances by kGemmXcds)
   auto next_tile = [&](int& g, TileCtx& c) -> bool {
@@ -237,8 +243,8 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
       const uint16_t* Q = static_cast<const uint16_t*>(dd.Q[parity]);
       c.psrc = P + blk_index(int64_t(c.bi) * TB + drow, dchunk * 8, dd.ldp) + k0;
       c.qsrc = Q + blk_index(int64_t(c.bj) * TB + drow, dchunk * 8, dd.ldq) + k0;
-      c.pstep = int64_t(NW * kBlkRows) * dd.ldp;  // NW row panels further down
-      c.qstep = int64_t(NW * kBlkRows) * dd.ldq;
+      c.pstep = int64_t(DW * kBlkRows) * dd.ldp;  // DW row panels further down
+      c.qstep = int64_t(DW * kBlkRows) * dd.ldq;
       return true;
     }
     return false;
@@ -248,10 +254,10 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
     lds_byte* sb = (lds_byte*)(smem + stage * STAGE_BYTES + dma_wave_off);
 #pragma unroll
     for (int i = 0; i < PL; ++i)
-      __builtin_amdgcn_global_load_lds(c.psrc + i * c.pstep + koff, sb + i * NW * 1024, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(c.psrc + i * c.pstep + koff, sb + i * DW * 1024, 16, 0, 0);
 #pragma unroll
     for (int i = 0; i < PL; ++i)
-      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + TB * ROWB + i * NW * 1024, 16, 0,
+      __builtin_amdgcn_global_load_lds(c.qsrc + i * c.qstep + koff, sb + TB * ROWB + i * DW * 1024, 16, 0,
                                        0);
   };
   // steps 0 .. NSTAGE-2 of a tile into stages 0 .. NSTAGE-2 (steps past the end are clamped to the
@@ -273,7 +279,7 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
   int g = xcd;
   TileCtx cur;
   if (!next_tile(g, cur)) return;
-  prologue(cur);
+  if (issuer) prologue(cur);
   while (true) {
     g += kGemmXcds;
     TileCtx nxt;
@@ -304,60 +310,80 @@ __global__ __launch_bounds__(NW * 64, TB == BT ? 1 : 2) void gemm_bf16_kernel(
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf[ni], pf[mi], acc[mi][ni], 0, 0, 0);
     };
 
-    // Main loop. Outstanding vector-memory operations of this wave at this point: this tile's
+    // Main loop. Outstanding vector-memory operations of an issuing wave at this point: this tile's
     // prologue loads, then the previous tile's epilogue stores. Loads complete in order among
-    // themselves, so "at most (NSTAGE - 2) * LOADS outstanding" implies step 0 has landed whether
+    // themselves, so "at most (NSTAGE - 2) * DLOADS outstanding" implies step 0 has landed whether
     // or not stores retire in order with loads (if they do, this waits a little longer than needed).
-    const int nk = cur.nk, last_kt = nk - 1;
-    MFSDP_WAIT_VMCNT((NSTAGE - 2) * LOADS);
-    __builtin_amdgcn_s_barrier();
-    read_frags(smem, slot0, pf0, qf0);
-    int cs = 0, ns = 1, fs = NSTAGE - 1;  // stages of steps kt, kt + 1 and of step kt + NSTAGE - 1
-    for (int kt = 0; kt < nk; ++kt) {
-      const uint8_t* sb = smem + cs * STAGE_BYTES;
-      read_frags(sb, slot1, pf1, qf1);
-      mfma_slice(pf0, qf0);
-      // scheduling: pairs of 1 MFMA + 1 fragment read, then the remaining MFMAs
-      static_assert(NMF >= NRD && NMF >= LOADS, "slice schedule assumes more MFMAs than reads");
-#pragma unroll
-      for (int i = 0; i < NRD; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
-      // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
-      MFSDP_WAIT_VMCNT((NSTAGE - 3) * LOADS);
+    // The other waves have no loads to wait for: the barrier after the issuers' wait covers them.
+    auto main_loop = [&](auto issue_c) {
+      constexpr bool ISS = decltype(issue_c)::value;
+      constexpr int L = ISS ? DLOADS : 0;  // DMA instructions of this wave per K step
+      const int nk = cur.nk, last_kt = nk - 1;
+      if constexpr (ISS) MFSDP_WAIT_VMCNT((NSTAGE - 2) * DLOADS);
       __builtin_amdgcn_s_barrier();
-      {
-        const int kload = kt + NSTAGE - 1;
-        issue(cur, kload < nk ? kload : last_kt, fs);
-      }
-      read_frags(smem + ns * STAGE_BYTES, slot0, pf0, qf0);
-      mfma_slice(pf1, qf1);
-      // scheduling: pairs of 1 MFMA + 1 DMA issue, then pairs of 1 MFMA + 1 fragment read while
-      // MFMAs last, then the remaining reads
-      constexpr int PAIRED = (NMF - LOADS < NRD) ? NMF - LOADS : NRD;
+      read_frags(smem, slot0, pf0, qf0);
+      int cs = 0, ns = 1, fs = NSTAGE - 1;  // stages of steps kt, kt + 1 and of step kt + NSTAGE - 1
+      for (int kt = 0; kt < nk; ++kt) {
+        const uint8_t* sb = smem + cs * STAGE_BYTES;
+        read_frags(sb, slot1, pf1, qf1);
+        mfma_slice(pf0, qf0);
+        // scheduling: pairs of 1 MFMA + 1 fragment read, then the remaining MFMAs
+        static_assert(NMF >= NRD && NMF >= DLOADS, "slice schedule assumes more MFMAs than reads");
 #pragma unroll
-      for (int i = 0; i < LOADS; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
-      }
+        for (int i = 0; i < NRD; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // 1 LDS read
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NMF - NRD, 0);
+        // step kt + 1 must have landed (steps kt + 2 .. kt + NSTAGE - 2 may still be in flight)
+        if constexpr (ISS) MFSDP_WAIT_VMCNT((NSTAGE - 3) * DLOADS);
+        __builtin_amdgcn_s_barrier();
+        if constexpr (ISS) {
+          const int kload = kt + NSTAGE - 1;
+          issue(cur, kload < nk ? kload : last_kt, fs);
+        }
+        read_frags(smem + ns * STAGE_BYTES, slot0, pf0, qf0);
+        mfma_slice(pf1, qf1);
+        if constexpr (DW == NW) {
+          // scheduling: pairs of 1 MFMA + 1 DMA issue, then pairs of 1 MFMA + 1 fragment read while
+          // MFMAs last, then the remaining reads
+          constexpr int PAIRED = (NMF - L < NRD) ? NMF - L : NRD;
 #pragma unroll
-      for (int i = 0; i < PAIRED; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          for (int i = 0; i < L; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // 1 VMEM (DMA) issue
+          }
+#pragma unroll
+          for (int i = 0; i < PAIRED; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          if constexpr (NRD > PAIRED) __builtin_amdgcn_sched_group_barrier(0x100, NRD - PAIRED, 0);
+          if constexpr (NMF - L > PAIRED) __builtin_amdgcn_sched_group_barrier(0x008, NMF - L - PAIRED, 0);
+        } else {
+          // scheduling: each MFMA followed by this wave's next DMA issue and next fragment read,
+          // while there are any
+#pragma unroll
+          for (int i = 0; i < NMF; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            if (i < L) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+            if (i < NRD) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+        }
+        cs = ns;
+        ns = (ns + 1 == NSTAGE) ? 0 : ns + 1;
+        fs = (fs + 1 == NSTAGE) ? 0 : fs + 1;
       }
-      if constexpr (NRD > PAIRED) __builtin_amdgcn_sched_group_barrier(0x100, NRD - PAIRED, 0);
-      if constexpr (NMF - LOADS > PAIRED) __builtin_amdgcn_sched_group_barrier(0x008, NMF - LOADS - PAIRED, 0);
-      cs = ns;
-      ns = (ns + 1 == NSTAGE) ? 0 : ns + 1;
-      fs = (fs + 1 == NSTAGE) ? 0 : fs + 1;
-    }
+    };
+    if (issuer)
+      main_loop(std::true_type{});
+    else
+      main_loop(std::false_type{});
     // The clamped tail loads of this tile must land before the next tile's prologue reuses the
     // stages, and every wave must be done reading LDS (its last fragments were consumed by MFMAs).
     MFSDP_WAIT_VMCNT(0);
     __builtin_amdgcn_s_barrier();
-    if (has_next) prologue(nxt);  // overlaps the epilogue below (it leaves stage NSTAGE-1 free)
+    if (has_next && issuer) prologue(nxt);  // overlaps the epilogue below (it leaves stage NSTAGE-1 free)
 
     // Epilogue (global-address-space accesses: flat ones would also hold lgkmcnt, which the next
     // tile's LDS reads wait on). acc[mi][ni] holds D[j][i] = C[i][j] with i = i0 + lane % 32 and
