@@ -139,11 +139,11 @@ __device__ __forceinline__ void apply4(const ApplyDesc& a, int64_t pr, int64_t p
 // tiles) followed by the Q rows of one K step. Stages are filled by direct global->LDS loads
 // (global_load_lds_dwordx4: each wave instruction writes 64 x 16 B = 1 KiB of LDS contiguously),
 // so no registers or ds_write instructions carry the tiles. One workgroup barrier per K step kt,
-// placed between its two 16-wide K slices: before it every wave waits (explicit vmcnt) for its own
-// loads of step kt + 1; after it the loads of step kt + NSTAGE - 1 are issued into the stage of step
-// kt - 1 (whose last fragments were consumed by MFMAs issued before the barrier), and the first
-// fragments of step kt + 1 are read while the second slice of step kt is multiplied. Steps
-// kt + 2 .. kt + NSTAGE - 1 are in flight meanwhile.
+// placed between its two 16-wide K slices: before it every wave that issues loads waits (explicit
+// vmcnt) for its loads of step kt + 1; after it the loads of step kt + NSTAGE - 1 are issued into
+// the stage of step kt - 1 (whose last fragments were consumed by MFMAs issued before the
+// barrier), and the first fragments of step kt + 1 are read while the second slice of step kt is
+// multiplied. Steps kt + 2 .. kt + NSTAGE - 1 are in flight meanwhile.
 //
 // LDS row layout: 64 B per row = four 16-B chunks; chunk c of row r is stored in slot c ^ g(r)
 // with g(r) = (r1 ^ r3) | r2 << 1 (bits of r). Groups of 8 (or 16) consecutive rows read by one
