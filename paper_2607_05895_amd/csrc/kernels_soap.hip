@@ -65,6 +65,19 @@ __device__ __forceinline__ float wave_sum(float x) {
   return ((r0 + r1) + r2) + r3;
 }
 
+// Sum of x over the four 16-lane rows of a wave, in every lane of the same column (all lanes
+// active): rows 0 + 1 and 2 + 3 by swapping odd and even rows, then the two halves by swapping them
+// (v_permlane16_swap, v_permlane32_swap: vector ALU exchanges, no LDS round trip). Each add has the
+// same two operands in every lane that forms it, so all lanes of a column agree bit for bit.
+__device__ __forceinline__ float sum_rows4(float x) {
+  const uint32_t xi = __float_as_uint(x);
+  const auto p = __builtin_amdgcn_permlane16_swap(xi, xi, false, false);
+  const float y = __uint_as_float(p[0]) + __uint_as_float(p[1]);  // (row 2k) + (row 2k + 1)
+  const uint32_t yi = __float_as_uint(y);
+  const auto q = __builtin_amdgcn_permlane32_swap(yi, yi, false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);  // (rows 0, 1) + (rows 2, 3)
+}
+
 // Reduce-scatter of 16 values over the 16 lanes of a DPP row (all lanes active): afterwards lane l
 // of each row holds that row's sum of value l (l = lane mod 16). Four exchange rounds with the lane
 // at distance 1, 2, 4 and 8 (quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_shl/row_shr 4,
@@ -250,9 +263,7 @@ __global__ __launch_bounds__(kQrPanelThreads) void qr_panel_kernel(const QrPanel
     }
     // lane l of every row: the row's sum of slot l; then over the four rows of the wave (the
     // adds are commutative pairs, so every lane of a column l agrees bit for bit)
-    float r = row_reduce_scatter16(part, lane & 15);
-    r += __shfl_xor(r, 16);
-    r += __shfl_xor(r, 32);
+    const float r = sum_rows4(row_reduce_scatter16(part, lane & 15));
     if (lane < kQrPanel) red[k & 1][w][lane] = r;
     if (t == k) {
 #pragma unroll
@@ -387,9 +398,7 @@ __global__ __launch_bounds__(kQrColThreads) void qr_col_kernel(const QrColDesc* 
       }
     }
   }
-  float rsum = row_reduce_scatter16(part, lane & 15);
-  rsum += __shfl_xor(rsum, 16);
-  rsum += __shfl_xor(rsum, 32);
+  const float rsum = sum_rows4(row_reduce_scatter16(part, lane & 15));
   if (lane < kQrPanel) red[w][lane] = rsum;
   __syncthreads();
   if (t < kQrPanel) ws[t] = ((red[0][t] + red[1][t]) + red[2][t]) + red[3][t];
